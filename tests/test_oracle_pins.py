@@ -1,0 +1,576 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Every check here compares the oracle with something other than itself: the
+published Philox known-answer vectors, the paper's worked negative count,
+Python big-integer and complex arithmetic, explicit per-pair loops on tiny
+inputs, closed-form losses and gradients, central finite differences, the
+bucketing and bucket-order invariants, and brute-force filtered ranks.
+"""
+
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import pbg_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+F64 = torch.float64
+
+
+# ---------------------------------------------------------------- Philox (O4)
+def _read_golden(name):
+    rows = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                rows.append(line.split())
+    return rows
+
+
+def test_philox_known_answers():
+    for row in _read_golden("philox4x32_10_kat.txt"):
+        vals = [int(x, 16) for x in row]
+        ctr, key, want = vals[0:4], vals[4:6], vals[6:10]
+        got = O.philox4x32_10(np.array(ctr, np.uint64), np.array(key, np.uint64))
+        assert [int(x) for x in got] == want
+
+
+def test_uniform_negative_map_is_exact_floor():
+    # u = floor(w * n / 2**32) in Python big integers, from the KAT-checked words
+    for n_rows in (1, 2, 3, 97, 5_206_529, 7_576_046, 2**31 - 1, 2**31):
+        for seed in (0, 1, 0xFFFFFFFF, 0x123456789ABCDEF0):
+            U = 9
+            got = O.uniform_negatives(seed, 5, 11, 1, U, n_rows)
+            for k in range(U):
+                words = O.philox4x32_10(np.array([k >> 2, 11, 5, 1], np.uint64),
+                                        np.array([seed & 0xFFFFFFFF, seed >> 32], np.uint64))
+                w = int(words[k & 3])
+                want = (w * n_rows) // (1 << 32)
+                assert int(got[k]) == want
+                assert 0 <= want < n_rows
+    # extreme words: w = 2**32 - 1 maps to n - 1 for every n
+    for n_rows in (1, 2, 2**31):
+        assert ((2**32 - 1) * n_rows) >> 32 == n_rows - 1
+
+
+def test_uniform_negatives_are_uniform():
+    n_rows, U = 97, 4096
+    counts = np.zeros(n_rows)
+    for chunk in range(25):
+        counts += np.bincount(O.uniform_negatives(20190001, 0, chunk, 0, U, n_rows),
+                              minlength=n_rows)
+    expected = counts.sum() / n_rows
+    chi2 = ((counts - expected) ** 2 / expected).sum()
+    # 96 degrees of freedom: the 1e-6 upper quantile is about 180
+    assert chi2 < 180
+
+
+def test_negative_streams_differ_by_side_chunk_bucket_and_seed():
+    base = O.uniform_negatives(7, 3, 4, 0, 64, 10**6)
+    for args in ((7, 3, 4, 1), (7, 3, 5, 0), (7, 2, 4, 0), (8, 3, 4, 0)):
+        other = O.uniform_negatives(args[0], args[1], args[2], args[3], 64, 10**6)
+        assert not np.array_equal(base, other)
+
+
+# -------------------------------------------------- partitions, buckets (O1, O2)
+def test_partition_sizes():
+    assert O.partition_size(121_216_723, 16) == 7_576_046
+    assert O.partition_size(41_652_230, 8) == 5_206_529
+    for n, P in ((10, 3), (121_216_723, 16), (41_652_230, 8), (7, 7), (1000, 1)):
+        rows = [O.partition_rows(n, P, p) for p in range(P)]
+        assert sum(rows) == n
+        assert all(r == O.partition_size(n, P) for r in rows[:-1])
+        assert 0 < rows[-1] <= O.partition_size(n, P)
+
+
+def test_bucketing_brute_force():
+    rng = np.random.default_rng(3)
+    n, P, E = 10, 3, 200
+    src = rng.integers(0, n, E)
+    dst = rng.integers(0, n, E)
+    rel = rng.integers(0, 4, E).astype(np.int32)
+    offsets, sl, rl, dl = O.bucket_edges(src, rel, dst, n, P)
+    # brute force: a dict of lists, filled in input order
+    ps = -(-n // P)
+    want = {}
+    for e in range(E):
+        want.setdefault((src[e] // ps, dst[e] // ps), []).append(
+            (src[e] % ps, rel[e], dst[e] % ps))
+    assert offsets[0] == 0 and offsets[-1] == E
+    assert np.all(np.diff(offsets) >= 0)
+    for i in range(P):
+        for j in range(P):
+            b = i * P + j
+            lo, hi = offsets[b], offsets[b + 1]
+            got = list(zip(sl[lo:hi].tolist(), rl[lo:hi].tolist(), dl[lo:hi].tolist()))
+            assert got == [tuple(int(v) for v in t) for t in want.get((i, j), [])]
+            assert np.all(sl[lo:hi] < O.partition_rows(n, P, i))
+            assert np.all(dl[lo:hi] < O.partition_rows(n, P, j))
+    # every edge lands in exactly one bucket, with part(src) = i and part(dst) = j
+    back_src = np.concatenate([sl[offsets[i * P + j]:offsets[i * P + j + 1]] + i * ps
+                               for i in range(P) for j in range(P)])
+    assert sorted(back_src.tolist()) == sorted(src.tolist())
+
+
+def test_bucketing_rejects_out_of_range():
+    with pytest.raises(ValueError):
+        O.bucket_edges([0, 10], [0, 0], [1, 2], 10, 2)
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 4, 5, 8, 16])
+def test_inside_out_order_invariant(P):
+    order = O.inside_out_order(P)
+    assert order[0] == (0, 0)
+    assert sorted(order) == [(i, j) for i in range(P) for j in range(P)]
+    seen = set()
+    for k, (i, j) in enumerate(order):
+        if k:
+            assert i in seen or j in seen      # shares a partition with an earlier bucket
+        seen.update((i, j))
+
+
+# -------------------------------------------------------- negatives count (O7)
+def test_paper_negative_count():
+    (C, U, want), = [tuple(int(v) for v in r) for r in _read_golden("batched_negatives_count.txt")]
+    mask = O.valid_mask(C, U)
+    assert int(mask.sum().item()) * 2 == want          # two corruption sides
+    assert 2 * C * (C + U) - 2 * C == want
+
+
+# ------------------------------------------------ operators, comparators (O5, O6)
+def test_complex_diagonal_matches_complex128():
+    rng = np.random.default_rng(1)
+    d = 10
+    h = d // 2
+    x, th, y = (rng.standard_normal(d) for _ in range(3))
+    g = O.apply_operator("complex_diagonal", torch.tensor(x), torch.tensor(th)).numpy()
+    xc = x[:h] + 1j * x[h:]
+    tc = th[:h] + 1j * th[h:]
+    yc = y[:h] + 1j * y[h:]
+    prod = xc * tc
+    assert np.allclose(g[:h], prod.real, rtol=0, atol=1e-14)
+    assert np.allclose(g[h:], prod.imag, rtol=0, atol=1e-14)
+    # the comparator's real dot on the split layout is Re <a, conj(b)>
+    score = O.compare_rows("dot", torch.tensor(g)[None], torch.tensor(y)[None]).item()
+    assert abs(score - np.real(np.sum(prod * np.conj(yc)))) < 1e-13
+
+
+def test_linear_operator_matches_matmul():
+    rng = np.random.default_rng(2)
+    d = 5
+    A = rng.standard_normal((d, d))
+    x = rng.standard_normal(d)
+    g = O.apply_operator("linear", torch.tensor(x), torch.tensor(A.reshape(-1))).numpy()
+    assert np.allclose(g, A @ x, atol=1e-14)
+    assert not np.allclose(g, A.T @ x)
+
+
+def test_translation_and_diagonal():
+    x = torch.tensor([1.0, -2.0, 3.0], dtype=F64)
+    t = torch.tensor([0.5, 4.0, -1.0], dtype=F64)
+    assert O.apply_operator("translation", x, t).tolist() == [1.5, 2.0, 2.0]
+    assert O.apply_operator("diagonal", x, t).tolist() == [0.5, -8.0, -3.0]
+    assert O.apply_operator("identity", x, None) is x
+
+
+@pytest.mark.parametrize("op", O.OPERATORS)
+def test_identity_parameters_reduce_to_identity(op):
+    from paper_1903_12287_amd import synth
+    d = 6
+    x = torch.tensor(np.random.default_rng(5).standard_normal((3, d)))
+    p = synth.identity_relation_params(op, 1, d)
+    th = None if p is None else torch.tensor(p[0].astype(np.float64))
+    assert torch.allclose(O.apply_operator(op, x, th), x, atol=0, rtol=0)
+
+
+def test_cos_comparator():
+    a = torch.tensor([[3.0, 4.0], [0.0, 0.0]], dtype=F64)
+    b = torch.tensor([[1.0, 0.0], [0.0, -2.0]], dtype=F64)
+    s = O.compare_all("cos", a, b)
+    assert abs(s[0, 0].item() - 0.6) < 1e-15
+    assert abs(s[0, 1].item() + 0.8) < 1e-15
+    assert s[1, 0].item() == 0.0 and s[1, 1].item() == 0.0      # zero norm is clamped
+    r = O.compare_rows("cos", a, b)
+    assert abs(r[0].item() - 0.6) < 1e-15
+
+
+# ---------------------------------------------------------- chunk scores (O7)
+def _py_operator(op, x, th):
+    """Explicit loops / Python complex numbers: an independent statement of g."""
+    d = len(x)
+    if op == "identity":
+        return list(x)
+    if op == "translation":
+        return [x[k] + th[k] for k in range(d)]
+    if op == "diagonal":
+        return [x[k] * th[k] for k in range(d)]
+    if op == "linear":
+        return [sum(th[k * d + l] * x[l] for l in range(d)) for k in range(d)]
+    h = d // 2
+    z = [complex(x[k], x[h + k]) * complex(th[k], th[h + k]) for k in range(h)]
+    return [v.real for v in z] + [v.imag for v in z]
+
+
+def _py_sim(cmp, a, b):
+    if cmp == "dot":
+        return sum(u * v for u, v in zip(a, b))
+    na = max(math.sqrt(sum(u * u for u in a)), 1e-12)
+    nb = max(math.sqrt(sum(v * v for v in b)), 1e-12)
+    return sum(u * v for u, v in zip(a, b)) / (na * nb)
+
+
+@pytest.mark.parametrize("op,cmp", [(o, c) for o in O.OPERATORS for c in O.COMPARATORS])
+def test_chunk_scores_brute_force(op, cmp):
+    rng = np.random.default_rng(11)
+    d, C, U, R = 4, 3, 2, 3
+    width = O.relation_param_width(op, d)
+    src_rows = rng.standard_normal((C + U, d))
+    dst_rows = rng.standard_normal((C + U, d))
+    rel_params = rng.standard_normal((R, max(width, 1)))
+    rel_e = np.array([2, 0, 2])
+    xs, xd = torch.tensor(src_rows[:C]), torch.tensor(dst_rows[:C])
+    cand_dst, cand_src = torch.tensor(dst_rows), torch.tensor(src_rows)
+    theta_e = None if width == 0 else torch.tensor(rel_params[rel_e])
+    theta_of = (lambda r: None) if width == 0 else (lambda r: torch.tensor(rel_params[r]))
+    p, S0, S1 = O.chunk_scores(op, cmp, xs, xd, theta_e, rel_e, cand_dst, cand_src, theta_of)
+    for e in range(C):
+        th = list(rel_params[rel_e[e]])
+        ge = _py_operator(op, list(src_rows[e]), th)
+        assert abs(p[e].item() - _py_sim(cmp, ge, list(dst_rows[e]))) < 1e-12
+        for t in range(C + U):
+            # destination corruption: f(s_e, r_e, candidate t)
+            assert abs(S0[e, t].item() - _py_sim(cmp, ge, list(dst_rows[t]))) < 1e-12
+            # source corruption: f(candidate t, r_e, d_e)
+            gt = _py_operator(op, list(src_rows[t]), th)
+            assert abs(S1[e, t].item() - _py_sim(cmp, gt, list(dst_rows[e]))) < 1e-12
+
+
+def test_identity_dot_scores_are_a_product():
+    rng = np.random.default_rng(4)
+    xs, xd = torch.tensor(rng.standard_normal((5, 3))), torch.tensor(rng.standard_normal((5, 3)))
+    p, S0, S1 = O.chunk_scores("identity", "dot", xs, xd, None, np.zeros(5, int), xd, xs,
+                               lambda r: None)
+    assert np.allclose(S0.numpy(), xs.numpy() @ xd.numpy().T, atol=1e-14)
+    assert np.allclose(S1.numpy(), xd.numpy() @ xs.numpy().T, atol=1e-14)
+    assert np.allclose(np.diag(S0.numpy()), p.numpy())
+
+
+# ----------------------------------------------------------------- losses (O8)
+def _single_edge_losses(loss, p, n0, n1, margin=0.1):
+    """C = 1, U = 1: the only valid negative on each side is the uniform one."""
+    pt = torch.tensor([p], dtype=F64)
+    valid = O.valid_mask(1, 1)
+    assert valid.tolist() == [[0.0, 1.0]]
+    S0 = torch.tensor([[123.0, n0]], dtype=F64)     # the masked diagonal must not matter
+    S1 = torch.tensor([[-77.0, n1]], dtype=F64)
+    return (O.side_loss(loss, margin, pt, S0, valid).item(),
+            O.side_loss(loss, margin, pt, S1, valid).item())
+
+
+def test_loss_closed_forms_single_edge():
+    p, n0, n1, lam = 0.3, 0.35, -0.9, 0.1
+    a, b = _single_edge_losses("ranking", p, n0, n1, lam)
+    assert abs(a - max(0.0, lam - p + n0)) < 1e-15 and abs(b - max(0.0, lam - p + n1)) < 1e-15
+    a, b = _single_edge_losses("softmax", p, n0, n1)
+    assert abs(a - math.log1p(math.exp(n0 - p))) < 1e-15
+    assert abs(b - math.log1p(math.exp(n1 - p))) < 1e-15
+    a, b = _single_edge_losses("logistic", p, n0, n1)
+    sp = lambda v: math.log1p(math.exp(v))
+    assert abs(a - (sp(-p) + sp(n0))) < 1e-15 and abs(b - (sp(-p) + sp(n1))) < 1e-15
+
+
+def test_ranking_sign_penalises_high_negatives():
+    # f is maximised on true edges: a negative scored above the positive costs more
+    lo, _ = _single_edge_losses("ranking", 1.0, -1.0, -1.0)
+    hi, _ = _single_edge_losses("ranking", 1.0, 2.0, -1.0)
+    assert lo == 0.0 and hi > 1.0
+
+
+def test_logistic_averages_negatives_over_k():
+    p = torch.tensor([0.2], dtype=F64)
+    S = torch.tensor([[9.0, 0.5, -0.25]], dtype=F64)      # C = 1, U = 2: K_e = 2
+    L = O.side_loss("logistic", 0.1, p, S, O.valid_mask(1, 2)).item()
+    sp = lambda v: math.log1p(math.exp(v))
+    assert abs(L - (sp(-0.2) + 0.5 * (sp(0.5) + sp(-0.25)))) < 1e-15
+
+
+@pytest.mark.parametrize("loss", O.LOSSES)
+def test_losses_invariant_to_negative_order(loss):
+    rng = np.random.default_rng(9)
+    C, U = 4, 5
+    p = torch.tensor(rng.standard_normal(C))
+    S = torch.tensor(rng.standard_normal((C, C + U)))
+    v = O.valid_mask(C, U)
+    base = O.side_loss(loss, 0.1, p, S, v)
+    perm = np.concatenate([np.arange(C), C + rng.permutation(U)])
+    assert torch.allclose(O.side_loss(loss, 0.1, p, S[:, perm], v), base, atol=1e-14, rtol=0)
+
+
+def test_softmax_gradient_closed_form():
+    p = torch.tensor([0.4, -0.2], dtype=F64, requires_grad=True)
+    S = torch.tensor([[0.0, 0.3, 1.1, -0.5], [2.0, 0.0, 0.1, 0.7]], dtype=F64, requires_grad=True)
+    v = O.valid_mask(2, 2)
+    O.side_loss("softmax", 0.1, p, S, v).sum().backward()
+    for e in range(2):
+        logits = [p[e].item()] + [S[e, t].item() for t in range(4) if t != e]
+        z = sum(math.exp(x) for x in logits)
+        sm = [math.exp(x) / z for x in logits]
+        assert abs(p.grad[e].item() - (sm[0] - 1.0)) < 1e-14
+        cols = [t for t in range(4) if t != e]
+        for k, t in enumerate(cols):
+            assert abs(S.grad[e, t].item() - sm[k + 1]) < 1e-14
+        assert S.grad[e, e].item() == 0.0
+
+
+# ----------------------------------------------- step gradient, Adagrad (O9, O10)
+def _tiny_model(op, cmp, loss, n=9, P=2, R=2, d=4, seed=0, scale=0.5, margin=0.1):
+    rng = np.random.default_rng(seed)
+    parts = [rng.standard_normal((O.partition_rows(n, P, p), d)) * scale for p in range(P)]
+    width = O.relation_param_width(op, d)
+    relp = None if width == 0 else rng.standard_normal((R, width)) * 0.5 + (
+        np.eye(d).reshape(-1) if op == "linear" else 0.0)
+    return O.Model.create(n, P, R, d, op, cmp, loss, margin, parts, relp)
+
+
+def _tiny_edges(model, i, j, m, seed):
+    rng = np.random.default_rng(seed + 100)
+    src = rng.integers(0, model.emb[i].shape[0], m)
+    dst = rng.integers(0, model.emb[j].shape[0], m)
+    rel = rng.integers(0, model.R, m)
+    return src, rel, dst
+
+
+def _near_kink(model, i, j, src, rel, dst, step, negs):
+    """Smallest |margin - p + n| over the step's valid ranking pairs."""
+    worst = np.inf
+    for (c, lo, hi), (u_dst, u_src) in zip(step, negs):
+        xs = torch.tensor(model.emb[i][src[lo:hi]])
+        xd = torch.tensor(model.emb[j][dst[lo:hi]])
+        cd = torch.cat([xd, torch.tensor(model.emb[j][u_dst])])
+        cs = torch.cat([xs, torch.tensor(model.emb[i][u_src])])
+        th = None if model.rel is None else torch.tensor(model.rel[rel[lo:hi]])
+        tof = (lambda r: None) if model.rel is None else (lambda r: torch.tensor(model.rel[r]))
+        p, S0, S1 = O.chunk_scores(model.op, model.cmp, xs, xd, th, rel[lo:hi], cd, cs, tof)
+        v = O.valid_mask(hi - lo, len(u_dst)).bool()
+        for S in (S0, S1):
+            z = (model.margin - p[:, None] + S)[v]
+            worst = min(worst, float(z.abs().min()))
+    return worst
+
+
+COMBOS = [(o, c, l) for o in O.OPERATORS for c in O.COMPARATORS for l in O.LOSSES]
+
+
+@pytest.mark.parametrize("op,cmp,loss", COMBOS)
+@pytest.mark.parametrize("bucket", [(0, 1), (1, 1)])
+def test_step_gradient_matches_finite_differences(op, cmp, loss, bucket):
+    i, j = bucket
+    R = 1 if (cmp == "cos" and op != "identity") else 2
+    for seed in range(20):
+        model = _tiny_model(op, cmp, loss, R=R, seed=seed)
+        src, rel, dst = _tiny_edges(model, i, j, 7, seed)
+        step = O.chunk_ranges(7, 3)[:2] + [(2, 6, 7)]     # chunks of 3, 3 and a short 1
+        negs = O.step_negatives(model, i, j, step, seed + 5, 2)
+        if loss != "ranking" or _near_kink(model, i, j, src, rel, dst, step, negs) > 1e-3:
+            break
+    loss0, grads, rel_grad = O.step_loss_and_grad(model, i, j, src, rel, dst, step, negs)
+    h = 1e-6
+
+    def f():
+        return O.step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=False)[0]
+
+    checked = 0
+    for p, (ids, g) in grads.items():
+        for a, row in enumerate(ids):
+            for k in range(model.d):
+                keep = model.emb[p][row, k]
+                model.emb[p][row, k] = keep + h
+                up = f()
+                model.emb[p][row, k] = keep - h
+                dn = f()
+                model.emb[p][row, k] = keep
+                fd = (up - dn) / (2 * h)
+                assert abs(fd - g[a, k]) <= 1e-6 * max(1.0, abs(g[a, k])), (p, row, k, fd, g[a, k])
+                checked += 1
+    if rel_grad is not None:
+        ids, g = rel_grad
+        for a, r in enumerate(ids):
+            for k in range(model.rel.shape[1]):
+                keep = model.rel[r, k]
+                model.rel[r, k] = keep + h
+                up = f()
+                model.rel[r, k] = keep - h
+                dn = f()
+                model.rel[r, k] = keep
+                fd = (up - dn) / (2 * h)
+                assert abs(fd - g[a, k]) <= 1e-6 * max(1.0, abs(g[a, k])), ("rel", r, k, fd, g[a, k])
+                checked += 1
+    assert checked > 0
+
+
+def test_ranking_gradient_one_active_pair():
+    """identity + dot, one edge (s, d), uniform negatives d' and s': with only the
+    destination-side hinge active, dL/ds = x_d' - x_d, dL/dd = -x_s, dL/dd' = x_s."""
+    n, d = 8, 3
+    for seed in range(1000):
+        u_dst = int(O.uniform_negatives(seed, 0, 0, 0, 1, n)[0])
+        u_src = int(O.uniform_negatives(seed, 0, 0, 1, 1, n)[0])
+        if len({0, 1, u_dst, u_src}) == 4:
+            break
+    E = np.zeros((n, d))
+    E[0] = [1.0, 0.5, 0.0]       # s
+    E[1] = [0.2, 0.1, 0.0]       # d
+    E[u_dst] = [0.3, -0.2, 0.4]  # d': lambda - <s,d> + <s,d'> = 0.1 - 0.25 + 0.2 > 0
+    E[u_src] = [-5.0, 0.0, 1.0]  # s': lambda - <s,d> + <s',d> = 0.1 - 0.25 - 1.0 < 0
+    model = O.Model.create(n, 1, 1, d, "identity", "dot", "ranking", 0.1, [E])
+    step = O.chunk_ranges(1, 1)
+    negs = O.step_negatives(model, 0, 0, step, seed, 1)
+    loss, grads, _ = O.step_loss_and_grad(model, 0, 0, np.array([0]), np.array([0]),
+                                          np.array([1]), step, negs)
+    assert abs(loss - (0.1 - 0.25 + 0.2)) < 1e-15
+    ids, g = grads[0]
+    gd = {int(r): g[k] for k, r in enumerate(ids)}
+    assert np.allclose(gd[0], E[u_dst] - E[1], atol=1e-15)
+    assert np.allclose(gd[1], -E[0], atol=1e-15)
+    assert np.allclose(gd[u_dst], E[0], atol=1e-15)
+    assert np.allclose(gd[u_src], 0.0, atol=0)
+
+
+def test_adagrad_closed_form():
+    n, d, lr = 8, 3, 0.1
+    rng = np.random.default_rng(0)
+    E = rng.standard_normal((n, d))
+    model = O.Model.create(n, 1, 1, d, "identity", "dot", "logistic", 0.1, [E.copy()])
+    step = O.chunk_ranges(2, 2)
+    src, dst, rel = np.array([0, 2]), np.array([1, 3]), np.array([0, 0])
+    negs = O.step_negatives(model, 0, 0, step, 4, 2)
+    _, g1, _ = O.step_loss_and_grad(model, 0, 0, src, rel, dst, step, negs)
+    O.adagrad_update(model, g1, None, lr)
+    ids, g = g1[0]
+    for k, r in enumerate(ids):
+        norm = np.linalg.norm(g[k])
+        moved = np.linalg.norm(model.emb[0][r] - E[r])
+        assert abs(moved - lr * norm / (norm + O.EPS_ADAGRAD)) < 1e-14
+        assert abs(model.G[0][r] - norm ** 2) < 1e-15 * max(1, norm ** 2)
+    # second step: the accumulator holds |g1|^2 + |g2|^2
+    before = model.emb[0].copy()
+    _, g2, _ = O.step_loss_and_grad(model, 0, 0, src, rel, dst, step, negs)
+    G_before = model.G[0].copy()
+    O.adagrad_update(model, g2, None, lr)
+    ids2, gg = g2[0]
+    for k, r in enumerate(ids2):
+        G = G_before[r] + np.sum(gg[k] ** 2)
+        assert abs(model.G[0][r] - G) < 1e-14
+        assert np.allclose(model.emb[0][r], before[r] - lr * gg[k] / (np.sqrt(G) + 1e-10), atol=1e-15)
+
+
+def test_relation_adagrad_is_elementwise():
+    model = _tiny_model("diagonal", "dot", "logistic", P=1, n=6, R=2, seed=3)
+    th0 = model.rel.copy()
+    src, rel, dst = np.array([0, 1, 2]), np.array([1, 1, 1]), np.array([3, 4, 5])
+    step = O.chunk_ranges(3, 3)
+    negs = O.step_negatives(model, 0, 0, step, 1, 2)
+    _, grads, (rids, rg) = O.step_loss_and_grad(model, 0, 0, src, rel, dst, step, negs)
+    O.adagrad_update(model, grads, (rids, rg), 0.05)
+    assert list(rids) == [1]
+    want = th0[1] - 0.05 * rg[0] / (np.abs(rg[0]) + 1e-10)
+    assert np.allclose(model.rel[1], want, atol=1e-15)
+    assert np.array_equal(model.rel[0], th0[0])           # untouched relation
+
+
+def test_step_gradient_is_taken_at_step_start():
+    """With S = 2 the two chunks' gradients are both evaluated before any update
+    (one Adagrad step with their sum); with S = 1 the second chunk sees the
+    first chunk's update."""
+    def run(S):
+        model = _tiny_model("translation", "dot", "softmax", P=1, n=6, R=1, seed=8)
+        src, dst = np.array([0, 1, 2, 0]), np.array([1, 2, 3, 4])
+        O.train_bucket(model, 0, 0, src, None, dst, 2, 2, S, 0.1, 9)
+        return model
+    m2 = run(2)
+    ref = _tiny_model("translation", "dot", "softmax", P=1, n=6, R=1, seed=8)
+    step = O.chunk_ranges(4, 2)
+    negs = O.step_negatives(ref, 0, 0, step, 9, 2)
+    src, dst, rel = np.array([0, 1, 2, 0]), np.array([1, 2, 3, 4]), np.zeros(4, int)
+    _, ga, ra = O.step_loss_and_grad(ref, 0, 0, src, rel, dst, step[:1], negs[:1])
+    _, gb, rb = O.step_loss_and_grad(ref, 0, 0, src, rel, dst, step[1:], negs[1:])
+    tot = {}
+    for gg in (ga, gb):
+        for p, (ids, g) in gg.items():
+            for k, r in enumerate(ids):
+                tot[int(r)] = tot.get(int(r), 0.0) + g[k]
+    ids = np.array(sorted(tot))
+    rel_tot = (ra[0], ra[1] + rb[1])
+    O.adagrad_update(ref, {0: (ids, np.stack([tot[r] for r in ids]))}, rel_tot, 0.1)
+    assert np.allclose(m2.emb[0], ref.emb[0], atol=1e-15)
+    assert np.allclose(m2.rel, ref.rel, atol=1e-15)
+    m1 = run(1)
+    assert not np.allclose(m1.emb[0], m2.emb[0], atol=1e-9)
+
+
+def test_short_last_chunk_and_chunk_offset():
+    """A call starting at chunk c0 draws the same negatives as the full pass."""
+    model_a = _tiny_model("diagonal", "dot", "ranking", P=1, n=9, R=2, seed=4)
+    model_b = _tiny_model("diagonal", "dot", "ranking", P=1, n=9, R=2, seed=4)
+    src, rel, dst = _tiny_edges(model_a, 0, 0, 10, 4)
+    la, steps_a = O.train_bucket(model_a, 0, 0, src, rel, dst, 3, 2, 2, 0.1, 17, return_steps=True)
+    assert len(steps_a) == 2                      # chunks 3,3,3,1 -> steps of 2 chunks
+    lb1 = O.train_bucket(model_b, 0, 0, src[:6], rel[:6], dst[:6], 3, 2, 2, 0.1, 17)
+    lb2 = O.train_bucket(model_b, 0, 0, src[6:], rel[6:], dst[6:], 3, 2, 2, 0.1, 17, first_chunk=2)
+    assert abs(la - (lb1 + lb2)) < 1e-12
+    assert np.array_equal(model_a.emb[0], model_b.emb[0])
+
+
+# ------------------------------------------------------------ ranking (O11)
+def test_rank_eval_brute_force():
+    rng = np.random.default_rng(12)
+    n, R, d = 7, 2, 4
+    E = rng.standard_normal((n, d))
+    model = O.Model.create(n, 1, R, d, "diagonal", "dot", "ranking", 0.1, [E],
+                           rng.standard_normal((R, d)))
+    src = np.array([0, 3, 5, 5])
+    rel = np.array([1, 0, 1, 1])
+    dst = np.array([2, 4, 6, 0])
+    ks = np.concatenate([src, [0, 0, 1]])
+    kr = np.concatenate([rel, [1, 0, 1]])
+    kd = np.concatenate([dst, [5, 2, 6]])
+    known = set(zip(ks.tolist(), kr.tolist(), kd.tolist()))
+    ranks, mrr, hits = O.rank_eval(model, src, rel, dst, ks, kr, kd)
+    for e in range(len(src)):
+        s, r, t = int(src[e]), int(rel[e]), int(dst[e])
+        pos = O.score_edges(model, 0, 0, [s], [r], [t])[0]
+        rd = 1 + sum(1 for c in range(n) if c != t and (s, r, c) not in known
+                     and O.score_edges(model, 0, 0, [s], [r], [c])[0] >= pos)
+        rs = 1 + sum(1 for c in range(n) if c != s and (c, r, t) not in known
+                     and O.score_edges(model, 0, 0, [c], [r], [t])[0] >= pos)
+        assert ranks[e] == rd and ranks[len(src) + e] == rs
+    assert abs(mrr - np.mean(1.0 / ranks)) < 1e-15
+    assert abs(hits - np.mean(ranks <= 10)) < 1e-15
+
+
+def test_rank_eval_monotone_construction():
+    """identity + dot with x_v = (v + 1) e_1: f(s, r, d) = (s + 1)(d + 1), so the
+    destination rank of d among unfiltered candidates is 1 + #{d' > d}."""
+    n = 12
+    E = np.zeros((n, 2))
+    E[:, 0] = np.arange(1, n + 1)
+    model = O.Model.create(n, 1, 1, 2, "identity", "dot", "ranking", 0.1, [E])
+    src, dst = np.array([2, 7, 0]), np.array([5, 1, 11])
+    ranks, _, _ = O.rank_eval(model, src, None, dst, src, None, dst)
+    for e in range(3):
+        assert ranks[e] == 1 + (n - 1 - dst[e])
+        assert ranks[3 + e] == 1 + (n - 1 - src[e])
+    # filtering a higher-scored candidate lowers the rank by one; ties count against
+    ranks2, _, _ = O.rank_eval(model, src[:1], None, dst[:1],
+                               np.array([2, 2]), None, np.array([5, 9]))
+    assert ranks2[0] == 1 + (n - 1 - 5) - 1
+    E2 = E.copy()
+    E2[4] = E2[5]                      # candidate 4 now ties with the true destination 5
+    model2 = O.Model.create(n, 1, 1, 2, "identity", "dot", "ranking", 0.1, [E2])
+    ranks3, _, _ = O.rank_eval(model2, src[:1], None, dst[:1], src[:1], None, dst[:1])
+    assert ranks3[0] == 1 + (n - 1 - 5) + 1
