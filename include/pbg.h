@@ -1,0 +1,237 @@
+/*
+ * pbg.h -- C ABI of the MI355X (gfx950) bucket-training library for
+ * PyTorch-BigGraph-style multi-relation graph embeddings (Lerer et al.,
+ * "PyTorch-BigGraph: A Large-scale Graph Embedding System", SysML 2019).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every function that can fail returns a pbg_status; PBG_OK is 0.  A failed
+ *    call leaves a message behind for pbg_last_error(ctx).  Nothing aborts and
+ *    no C++ exception crosses this boundary.
+ *  - On any error no caller-owned parameter (embeddings, accumulators,
+ *    relation parameters, outputs) has been modified: argument checks, and a
+ *    device-side range check of every id, run before the first update.
+ *  - All arrays are owned by the caller.  Unless its name ends in _host, an
+ *    array is a device pointer on the device that was current when the context
+ *    was created.  The library allocates only its own workspace (device memory
+ *    for packed tiles, scores, sort buffers and partition slots), grows it on
+ *    demand and frees it in pbg_free.
+ *  - Work is enqueued on the caller's streams (pbg_set_streams; the null
+ *    stream by default).  Every call is synchronous on return.  A context is
+ *    not thread-safe; distinct contexts are independent.
+ *  - Same inputs and the same chunks_per_step give bitwise-identical results:
+ *    there are no floating-point atomics and every reduction has a fixed order.
+ *  - Embedding tables are float32, row-major [rows x dim].  Ids are int32 local
+ *    rows of a partition unless stated otherwise.
+ */
+#ifndef PBG_H
+#define PBG_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PBG_OK = 0,
+  PBG_ERR_INVALID_ARG = 1,   /* bad value, size, pointer or out-of-range id */
+  PBG_ERR_UNSUPPORTED = 2,   /* a combination this version does not implement */
+  PBG_ERR_OUT_OF_MEMORY = 3, /* workspace could not be allocated */
+  PBG_ERR_DEVICE = 4,        /* a HIP runtime call failed */
+  PBG_ERR_STATE = 5          /* wrong call order (e.g. an unbound partition) */
+} pbg_status;
+
+/* Relation operators g(x, theta_r) (Sec. 3.1, operator table):
+ *  IDENTITY          g(x) = x                       (no relation parameters)
+ *  TRANSLATION       g(x) = x + theta_r             (TransE; dim floats per relation)
+ *  DIAGONAL          g(x) = x (.) theta_r           (DistMult; dim floats)
+ *  LINEAR            g(x) = A_r x, A_r row-major    (RESCAL; dim*dim floats)
+ *  COMPLEX_DIAGONAL  g(x) = x * theta_r over C^(dim/2), both stored as
+ *                    [re(0..h-1) | im(0..h-1)]      (ComplEx; dim floats)
+ * The operator acts on the source side; the destination is used as is. */
+enum { PBG_OP_IDENTITY = 0, PBG_OP_TRANSLATION = 1, PBG_OP_DIAGONAL = 2,
+       PBG_OP_LINEAR = 3, PBG_OP_COMPLEX_DIAGONAL = 4 };
+
+/* Comparators sim(a, b) (Sec. 3.1): DOT <a, b> (for complex embeddings in the
+ * split layout this is Re<a, conj(b)>); COS <a, b> / (max(|a|,1e-12) max(|b|,1e-12)). */
+enum { PBG_CMP_DOT = 0, PBG_CMP_COS = 1 };
+
+/* Losses per edge e and corruption side, over that side's valid negatives n_t
+ * (Sec. 3.1; all summed over edges, sides and chunks):
+ *  RANKING   sum_t max(0, margin - p_e + n_t)
+ *  LOGISTIC  softplus(-p_e) + (1/K_e) sum_t softplus(n_t),  K_e = #valid negatives
+ *  SOFTMAX   logsumexp({p_e} U {n_t}) - p_e */
+enum { PBG_LOSS_RANKING = 0, PBG_LOSS_LOGISTIC = 1, PBG_LOSS_SOFTMAX = 2 };
+
+/* Flags for pbg_bucket_init. */
+enum {
+  /* Round the inputs of the score and score-gradient contractions to bfloat16
+   * (round to nearest even) and accumulate in float32; embeddings, Adagrad
+   * state, losses and the loss epilogue stay float32. */
+  PBG_F_BF16_SCORE = 1u
+};
+
+/* Where a bound partition lives. */
+enum { PBG_MEM_DEVICE = 0, PBG_MEM_PINNED_HOST = 1 };
+
+typedef struct pbg_ctx pbg_ctx;
+
+/* Batched negatives (Sec. 4.3, Fig. 3).  Chunk c of a bucket holds edges
+ * [c*chunk_size, min((c+1)*chunk_size, n_edges)) in the given order; every edge
+ * of a chunk is scored against the chunk's other edges' entities plus
+ * num_uniform entities drawn uniformly (separately per side) from the
+ * partition of the corrupted side; the induced positive is excluded.  A step
+ * of chunks_per_step chunks takes its gradient at the step-start parameters
+ * and applies one Adagrad update.  first_chunk numbers the first chunk of the
+ * call, so that a bucket may be trained in several calls with the same
+ * negatives as one call (the uniform draws are keyed by chunk number). */
+typedef struct {
+  int32_t chunk_size;       /* >= 1 */
+  int32_t num_uniform;      /* >= 0; chunk_size + num_uniform >= 2 */
+  int32_t chunks_per_step;  /* >= 1 (40 matches the paper's 40 training threads) */
+  int32_t reserved;         /* must be 0 */
+  int64_t first_chunk;      /* >= 0 */
+} pbg_neg_config;
+
+/* Timings and work of the last pbg_train_bucket / pbg_train_epoch call. */
+typedef struct {
+  int64_t edges;            /* edges trained */
+  int64_t chunks;
+  int64_t steps;
+  double total_ms;          /* wall time of the call on the compute stream */
+  double gather_ms;         /* gather + operator kernels */
+  double score_ms;          /* score contraction + loss epilogue */
+  double backward_ms;       /* score-gradient contractions + operator backward */
+  double update_ms;         /* sort + segment Adagrad (entities and relations) */
+  double gather_bytes;      /* algorithmic bytes of the gathers: (2C+2U)*dim*4 per chunk */
+  double score_flops;       /* algorithmic flops of the three contractions: 12*C*N*dim per chunk */
+  double update_bytes;      /* algorithmic bytes of the Adagrad updates */
+  double copy_ms;           /* partition / edge transfers (pbg_train_epoch) */
+  int64_t partition_loads;  /* host-to-device partition loads (pbg_train_epoch) */
+} pbg_stats;
+
+/* Creates a context for a graph of num_entities entities of one type split
+ * into num_partitions contiguous ranges of ceil(n/P) ids, the last holding the
+ * remainder (Sec. 4.1), num_relations relations, embedding dimension dim.
+ * Returns INVALID_ARG for unknown enums, dim < 1 or dim > 512, odd dim with
+ * COMPLEX_DIAGONAL, P < 1, a partition left empty, num_relations < 1 or a
+ * non-finite margin; UNSUPPORTED for COS with a non-identity operator and more
+ * than one relation, and for LINEAR with more than one relation or with COS. */
+pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_partitions,
+                           int32_t num_relations, int32_t dim, int32_t op, int32_t cmp,
+                           int32_t loss, float margin, uint32_t flags);
+
+/* Releases the context and its workspace (NULL is allowed). */
+void pbg_free(pbg_ctx* ctx);
+
+/* Message of the last failed call on ctx ("" if none; a static message when
+ * ctx is NULL).  Valid until the next call on ctx. */
+const char* pbg_last_error(const pbg_ctx* ctx);
+
+/* Rows of partition p (Sec. 4.1), or -1 for a bad p. */
+int64_t pbg_partition_rows(const pbg_ctx* ctx, int32_t p);
+
+/* Floats of all relation parameters: R*dim (translation, diagonal, complex),
+ * R*dim*dim (linear) or 0 (identity). */
+int64_t pbg_relation_param_floats(const pbg_ctx* ctx);
+
+/* Edge bucketing (Sec. 4.1): edge (s, r, d) with global ids goes to bucket
+ * b = part(s) * P + part(d).  Writes offsets[P*P+1] (device, int64; bucket b
+ * holds positions [offsets[b], offsets[b+1])) and, in that order and stably
+ * (input order inside each bucket), the local ids and relations.  rel may be
+ * NULL (all relation 0; then rel_out may be NULL too).  Ids outside
+ * [0, num_entities) or relations outside [0, R) give INVALID_ARG with no
+ * output written.  n <= 2^31 - 1. */
+pbg_status pbg_bucket_edges(pbg_ctx* ctx, const int64_t* src, const int32_t* rel,
+                            const int64_t* dst, int64_t n, int64_t* offsets,
+                            int32_t* src_local, int32_t* rel_out, int32_t* dst_local);
+
+/* Binds partition p: emb [rows(p) x dim] float32 and its row-wise Adagrad
+ * accumulator adagrad [rows(p)] float32 (one value per row, Sec. 3.1).  where
+ * is PBG_MEM_DEVICE (device memory) or PBG_MEM_PINNED_HOST (page-locked host
+ * memory, for pbg_train_epoch, which swaps partitions through HBM slots).
+ * Initial values are the caller's; the library updates them in place. */
+pbg_status pbg_bind_partition(pbg_ctx* ctx, int32_t p, float* emb, float* adagrad, int32_t where);
+
+/* Binds the relation parameters (device, [R x width] float32, width as in
+ * pbg_relation_param_floats / R) and their element-wise Adagrad accumulators
+ * (same shape).  Not needed (and ignored) for IDENTITY. */
+pbg_status pbg_bind_relations(pbg_ctx* ctx, float* params, float* adagrad);
+
+/* Streams (hipStream_t) for compute and for partition transfers.  NULL means
+ * the null stream.  Streams must have the default priority. */
+pbg_status pbg_set_streams(pbg_ctx* ctx, void* compute_stream, void* copy_stream);
+
+/* One training pass over the edges of bucket (i, j) (Sec. 3.1 model and loss,
+ * Sec. 4.1 bucket, Sec. 4.3 batched negatives; Adagrad with the accumulator
+ * summed over each embedding row).  src_local / dst_local are int32 rows of
+ * partitions i / j (device), rel is int32 in [0, R) or NULL when R == 1.
+ * Uniform negative k of chunk c and side sigma (0: destinations, drawn from
+ * partition j; 1: sources, drawn from partition i) is
+ * floor(w * rows / 2^32) with w = word (k mod 4) of
+ * Philox4x32-10(counter = (k / 4, c, i*P + j, sigma), key = (seed low 32 bits,
+ * seed high 32 bits)).  Each step applies
+ *   G_row += |g_row|^2 ;  theta_row -= lr * g_row / (sqrt(G_row) + 1e-10)
+ * to every entity row it touches (g summed over the step) and the element-wise
+ * form to relation parameters.  Partitions i and j must be bound in device
+ * memory.  loss_host (nullable) receives the summed loss of the call. */
+pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
+                            const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
+                            const pbg_neg_config* neg, float lr, uint64_t seed,
+                            double* loss_host);
+
+/* Per-step losses of the last pbg_train_bucket call: copies
+ * min(capacity, steps) values to out_host and the step count to n_steps_host. */
+pbg_status pbg_get_step_losses(const pbg_ctx* ctx, double* out_host, int64_t capacity,
+                               int64_t* n_steps_host);
+
+/* One epoch over all buckets in inside-out order (Sec. 4.1, Fig. 1 right):
+ * (0,0), then for k = 1..P-1: (k,0),(0,k),(k,1),(1,k),...,(k,k-1),(k-1,k),(k,k);
+ * empty buckets are skipped.  Edges are bucketed (pbg_bucket_edges layout) in
+ * page-locked host memory; offsets_host [P*P+1] is host memory.  Every
+ * partition must be bound as PBG_MEM_PINNED_HOST: at most max_resident (>= 2)
+ * partitions are held in HBM slots at a time, loaded and written back on the
+ * copy stream, ordered with events against the compute stream.  On return the
+ * host partitions hold the trained values.  Each bucket is trained as by
+ * pbg_train_bucket with first_chunk 0 and the given seed. */
+pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
+                           const int32_t* src_local_host, const int32_t* rel_host,
+                           const int32_t* dst_local_host, const pbg_neg_config* neg,
+                           float lr, uint64_t seed, int32_t max_resident, double* loss_host);
+
+/* Scores f(s, r, d) = sim(g(theta_s, theta_r), theta_d) of n edges of bucket
+ * (i, j) (Sec. 3.1), computed as in training; scores is float32 [n] (device). */
+pbg_status pbg_score_edges(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
+                           const int32_t* rel, const int32_t* dst_local, int64_t n,
+                           float* scores);
+
+/* Filtered link-prediction ranks (Sec. 5, filtered protocol of the FB15k
+ * experiments): for each triple (s, r, d), its destination rank
+ * 1 + #{d' != d : (s, r, d') not known, f(s, r, d') >= f(s, r, d)} among all
+ * entities, then its source rank symmetrically.  ranks is int32 [2n] (device):
+ * destination ranks first, then source ranks.  The known triples (device,
+ * duplicates allowed) are the filter.  mrr_host / hits10_host (nullable)
+ * receive the mean of 1/rank and of [rank <= 10] over the 2n ranks.  Only for
+ * P == 1 (else UNSUPPORTED). */
+pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int32_t* rel, const int32_t* dst,
+                         int64_t n, const int32_t* known_src, const int32_t* known_rel,
+                         const int32_t* known_dst, int64_t n_known, int32_t* ranks,
+                         double* mrr_host, double* hits10_host);
+
+/* The uniform negatives pbg_train_bucket draws (Sec. 4.3; Philox map as
+ * described there) for chunks first_chunk .. first_chunk + n_chunks - 1 of
+ * bucket (i, j): out (device, int32) is [n_chunks][2][num_uniform], side 0
+ * (destinations, rows of partition j) then side 1 (sources, partition i).
+ * Produced by the same device code as training; for inspection and tests. */
+pbg_status pbg_sample_negatives(pbg_ctx* ctx, int32_t i, int32_t j, int64_t first_chunk,
+                                int64_t n_chunks, int32_t num_uniform, uint64_t seed, int32_t* out);
+
+/* Timings and algorithmic work of the last training call. */
+pbg_status pbg_get_stats(const pbg_ctx* ctx, pbg_stats* out_host);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PBG_H */

@@ -1,0 +1,98 @@
+// Device-side helpers shared by the gfx950 kernels of the bucket-training path.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "geometry.h"
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+#define PBG_WAVE 64
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32
+// multiplies whose high and low halves are mixed with the other counter words
+// and the key; the key is advanced by the Weyl constants between rounds.
+// ---------------------------------------------------------------------------
+struct Philox4 {
+  uint32_t v[4];
+};
+
+__device__ __forceinline__ Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2,
+                                                 uint32_t c3, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    const uint32_t n0 = hi1 ^ c1 ^ k0;
+    const uint32_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  Philox4 o;
+  o.v[0] = c0;
+  o.v[1] = c1;
+  o.v[2] = c2;
+  o.v[3] = c3;
+  return o;
+}
+
+// Uniform negative k of (chunk, bucket, side) in [0, rows): floor(w * rows / 2^32).
+__device__ __forceinline__ int32_t uniform_negative(uint64_t seed, uint32_t bucket, uint64_t chunk,
+                                                    uint32_t side, uint32_t k, uint32_t rows) {
+  const Philox4 w = philox4x32_10(k >> 2, (uint32_t)chunk, bucket, side, (uint32_t)seed,
+                                  (uint32_t)(seed >> 32));
+  const uint32_t word = w.v[k & 3u];
+  return (int32_t)(((uint64_t)word * (uint64_t)rows) >> 32);
+}
+
+// ---------------------------------------------------------------------------
+// wave reductions (64 lanes)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, PBG_WAVE);
+  return x;
+}
+
+__device__ __forceinline__ double wave_sum_d(double x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, PBG_WAVE);
+  return x;
+}
+
+// sum over the 16 consecutive lanes of a group (lanes 16g .. 16g+15)
+__device__ __forceinline__ float group16_sum(float x) {
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) x += __shfl_xor(x, o, PBG_WAVE);
+  return x;
+}
+
+__device__ __forceinline__ float group16_max(float x) {
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, PBG_WAVE));
+  return x;
+}
+
+// numerically stable softplus(x) = log(1 + e^x) and logistic sigmoid
+__device__ __forceinline__ float softplusf(float x) {
+  return fmaxf(x, 0.0f) + log1pf(expf(-fabsf(x)));
+}
+__device__ __forceinline__ float sigmoidf(float x) {
+  if (x >= 0.0f) return 1.0f / (1.0f + expf(-x));
+  const float e = expf(x);
+  return e / (1.0f + e);
+}
+
+// round-to-nearest-even fp32 -> bf16 (finite inputs)
+__device__ __forceinline__ __bf16 to_bf16(float x) { return (__bf16)x; }

@@ -1,0 +1,82 @@
+// Layout of one training step's workspace, shared by host code and kernels.
+//
+// A step holds `nchunks` chunks of a bucket (i, j).  Chunk c has
+// Cc = min(C, m_step - c*C) edges and Nc = Cc + U candidates per side: the
+// chunk's own destinations (or sources) followed by U uniform draws.
+//
+// Packed float32 buffers (row stride dp = dim rounded up to 4, pad columns 0):
+//   qk  [S][2][C][dp]   side 0: Q = g(x_s) (dot) or its unit vector (cos)
+//                       side 1: K = g*(x_d) (dot) or the unit x_d (cos)
+//   nn  [S][2][N][dp]   side 0: destination candidates, side 1: source candidates
+//   ds  [S][2][C][Np]   score gradient dL/dS (raw scores between softmax passes)
+//   dq  [S][2][C][dp]   dS . N per side
+//   dn  [S][2][N][dp]   dS^T . Q per side, turned in place into the per-row
+//                       gradient contributions of the step
+// Row index of candidate t of side s in chunk c: (c*2 + s)*N + t.
+#pragma once
+
+#include <stdint.h>
+
+enum { OP_IDENTITY = 0, OP_TRANSLATION = 1, OP_DIAGONAL = 2, OP_LINEAR = 3, OP_COMPLEX = 4 };
+enum { CMP_DOT = 0, CMP_COS = 1 };
+enum { LOSS_RANKING = 0, LOSS_LOGISTIC = 1, LOSS_SOFTMAX = 2 };
+
+#define PBG_EPS_NORM 1e-12f
+#define PBG_EPS_ADAGRAD 1e-10f
+#define PBG_SCORE_BN 128  // column tile of the score contraction
+
+struct StepGeom {
+  int C, U, N;      // chunk capacity, uniform draws per side, N = C + U
+  int d, dp, Np;    // dim, padded row stride, padded score-row stride
+  int dr;           // floats per relation parameter row
+  int nct;          // column tiles of the score contraction per chunk-side
+  int nchunks;      // chunks in this step
+  int m_step;       // edges in this step
+  int op, cmp, loss;
+  float margin;
+  int same_table;   // partitions i and j are the same table
+  int rows_i, rows_j;
+  int rb;           // bits of a row id in a sort key
+  uint32_t bucket;  // i*P + j
+  uint64_t seed;
+  int64_t chunk0;   // chunk number (within the bucket) of the step's first chunk
+};
+
+__host__ __device__ inline int chunk_edges(const StepGeom& g, int c) {
+  const int r = g.m_step - c * g.C;
+  return r < g.C ? r : g.C;
+}
+
+struct StepBufs {
+  // edges of the step (device, int32)
+  const int32_t* src;
+  const int32_t* dst;
+  const int32_t* rel;   // NULL: relation 0
+  // parameters
+  float* emb_i;
+  float* emb_j;
+  float* G_i;
+  float* G_j;
+  float* relp;          // [R][dr]
+  float* relG;
+  // packed tiles and intermediates
+  float* qk;
+  float* nn;
+  float* nrm;           // [S][2][N] norms of the raw vectors behind nn (cos)
+  float* pos;           // [S][C] positive scores
+  float* bias;          // [S][C] <theta_r, x_d> (translation + dot)
+  int32_t* neg;         // [S][2][U] uniform draws (side 0 from partition j, side 1 from i)
+  float* ds;
+  float* rowpart;       // [S][2][C][nct][2]
+  float* rowstat;       // [S][2][C]  log-sum-exp per side (softmax)
+  float* dpos;          // [S][C] dL/dp
+  float* dsum1;         // [S][C] sum_t dS1[e][t]
+  double* chunkloss;    // [S]
+  float* dq;
+  float* dn;
+  float* relc;          // [S][N][dr] relation gradient contributions
+  uint32_t* keys;       // [S*2N] sort keys of the contribution rows
+  uint32_t* vals;       // [S*2N] contribution row index
+  uint32_t* rkeys;      // [S*C]  relation ids of the edges (R > 1)
+  uint32_t* rvals;      // [S*C]  relc row index
+};

@@ -1,0 +1,89 @@
+// Launch entry points of the gfx950 kernels (host side).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "geometry.h"
+
+// ---- matrix-core contractions -------------------------------------------------
+enum { EPI_STORE = 0, EPI_LOSS = 1, EPI_SOFTMAX_STATS = 2 };
+enum { DIM_CC = 0, DIM_NC = 1, DIM_FIXED = 2 };
+// operand layouts: NT  A[m][k], B[n][k];  NN  A[m][k], B[k][n];  TN  A[k][m], B[k][n]
+enum { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
+
+struct GemmArgs {
+  const float* A;
+  const float* B;
+  float* Cm;
+  int64_t a_cs, a_ss, b_cs, b_ss, c_cs, c_ss;  // strides (floats) per chunk and per side
+  int lda, ldb, ldc;
+  int mdim, ndim, kdim;  // DIM_* selectors
+  int Mfix, Nfix, Kfix;
+  int C, U, m_step;      // chunk geometry (m_step = 0: not chunked)
+  int nsides;            // batches per chunk (2: one per corruption side)
+  // loss epilogue
+  const float* pos;      // [S][C]
+  const float* bias;     // [S][C] added to side 1 scores (translation + dot), or NULL
+  float* rowpart;        // [S][2][C][nct][2]
+  int nct;
+  int loss;
+  float margin;
+};
+
+int gemm_pick_nb(int n);
+void launch_gemm_f32(const GemmArgs& a, int layout, int epi, int nb, int grid_n, int grid_m,
+                     int batches, hipStream_t s);
+
+// ---- gather / operator / negatives --------------------------------------------
+void launch_gather(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s);
+void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s);
+
+// ---- loss finalisation and backward -----------------------------------------
+void launch_softmax_rows(const StepGeom& g, const StepBufs& b, hipStream_t s);
+void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, hipStream_t s);
+void launch_op_backward(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s);
+
+// ---- sort, segments, updates ----------------------------------------------------
+struct SortWork {
+  uint32_t* keys_alt;
+  uint32_t* vals_alt;
+  uint32_t* hist;       // [256][max blocks]
+  uint32_t* flags;      // [n] scratch
+  uint32_t* seg_start;  // [n + 1]
+  uint32_t* piece_start;// [n + 1]
+  uint32_t* piece_seg;  // [n] scratch (piece ids)
+  uint32_t* seg_first_piece;  // [n + 1]
+  uint32_t* counts;     // [4]: segments, pieces
+  uint32_t* scan_tmp;   // block sums
+  float* partial;       // [n][width]
+  int max_n;
+};
+
+// stable LSD radix sort of (key, value) pairs on the low `bits` bits of the
+// keys; the result is left in keys / vals
+void launch_radix_sort(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, hipStream_t s);
+
+// Adagrad over sorted contribution rows: entity tables (row-wise accumulator)
+void launch_entity_update(const StepGeom& g, const StepBufs& b, int n, SortWork& w, float lr,
+                          hipStream_t s);
+// relations with several ids (sorted by relation) or one relation (fixed-order sum)
+void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, int n, SortWork& w,
+                                   float lr, hipStream_t s);
+void launch_relation_chunk_sums(const StepGeom& g, const float* rows, int64_t ld, int include_uniform,
+                                float* partial, hipStream_t s);
+void launch_relation_single_adagrad(float* relp, float* relG, int width, const float* partial,
+                                    int nparts, float lr, hipStream_t s);
+void launch_exclusive_scan(const uint32_t* in, int64_t n, uint32_t* out, uint32_t* tmp,
+                           uint32_t* total, hipStream_t s);
+
+// ---- checks, bucketing, scoring, ranking ------------------------------------
+void launch_check_ids(const int32_t* ids, int64_t n, int32_t limit, uint32_t* flag, uint32_t bit,
+                      hipStream_t s);
+void launch_check_ids64(const int64_t* ids, int64_t n, int64_t limit, uint32_t* flag, uint32_t bit,
+                        hipStream_t s);
+void launch_score_edges(const StepGeom& g, const float* emb_i, const float* emb_j, const float* relp,
+                        const float* relT, const int32_t* src, const int32_t* rel,
+                        const int32_t* dst, int64_t n, float* out, hipStream_t s);
+void launch_sample_negatives(uint64_t seed, uint32_t bucket, int64_t chunk0, int64_t n_chunks, int U,
+                             uint32_t rows_j, uint32_t rows_i, int32_t* out, hipStream_t s);

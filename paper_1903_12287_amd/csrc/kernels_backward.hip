@@ -1,0 +1,265 @@
+// Loss values and gradients of a step (Sec. 3.1 losses) and the backward pass
+// through the comparator and the relation operator.
+//
+// After the contractions, for chunk c and side s:
+//   dq[c][s][e] = sum_t dS_s[e][t] N_s[t]      (gradient of side s's query row)
+//   dn[c][s][t] = sum_e dS_s[e][t] Q_s[e]      (gradient of candidate row t)
+// The positive score p_e = sim(g(x_s), x_d) is computed once and shared by
+// both sides; dL/dp_e collects both sides.  op_backward folds everything that
+// reaches one embedding row of the chunk into that row's contribution,
+// in place in dn: side 0 rows are destinations (in-chunk, then uniform
+// draws from partition j), side 1 rows are sources (partition i).
+#include "kernels.h"
+#include "row_ops.h"
+
+namespace {
+
+// ---- softmax: log-sum-exp per row and side, then dS = softmax in place -----
+__global__ __launch_bounds__(256) void softmax_rows_kernel(StepGeom g, StepBufs b) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);   // over C rows of one (chunk, side)
+  const int z = blockIdx.y;                               // chunk * 2 + side
+  const int c = z >> 1;
+  const int Cc = chunk_edges(g, c);
+  if (row >= Cc) return;
+  const int Nc = Cc + g.U;
+  const float p = b.pos[(int64_t)c * g.C + row];
+  const float* rp = b.rowpart + ((int64_t)z * g.C + row) * g.nct * 2;
+  float M = p;
+  for (int ct = 0; ct < g.nct; ++ct) M = fmaxf(M, rp[2 * ct]);
+  float Z = expf(p - M);
+  for (int ct = 0; ct < g.nct; ++ct) {
+    const float mx = rp[2 * ct];
+    if (mx > -INFINITY) Z += rp[2 * ct + 1] * expf(mx - M);
+  }
+  const float lse = M + logf(Z);
+  if (lane == 0) b.rowstat[(int64_t)z * g.C + row] = lse;
+  float* ds = b.ds + ((int64_t)z * g.C + row) * g.Np;
+  for (int t = lane; t < g.Np; t += 64) {
+    float v = 0.0f;
+    if (t < Nc && t != row) v = expf(ds[t] - lse);
+    ds[t] = v;
+  }
+}
+
+// ---- per-edge dL/dp, translation bias gradient, losses ------------------------
+__global__ __launch_bounds__(256) void finalize_kernel(StepGeom g, StepBufs b) {
+  const int c = blockIdx.x;
+  const int Cc = chunk_edges(g, c);
+  double acc = 0.0;
+  for (int e = threadIdx.x; e < Cc; e += blockDim.x) {
+    const int64_t ce = (int64_t)c * g.C + e;
+    const float p = b.pos[ce];
+    float l0 = 0.f, l1 = 0.f, d0 = 0.f, d1 = 0.f;
+    if (g.loss != LOSS_SOFTMAX) {
+      const float* r0 = b.rowpart + ((int64_t)(c * 2 + 0) * g.C + e) * g.nct * 2;
+      const float* r1 = b.rowpart + ((int64_t)(c * 2 + 1) * g.C + e) * g.nct * 2;
+      for (int ct = 0; ct < g.nct; ++ct) {
+        l0 += r0[2 * ct];
+        d0 += r0[2 * ct + 1];
+        l1 += r1[2 * ct];
+        d1 += r1[2 * ct + 1];
+      }
+    }
+    double loss;
+    float dp, dsum1;
+    if (g.loss == LOSS_RANKING) {
+      loss = (double)l0 + (double)l1;
+      dp = -(d0 + d1);
+      dsum1 = d1;
+    } else if (g.loss == LOSS_LOGISTIC) {
+      loss = (double)l0 + (double)l1 + 2.0 * (double)softplusf(-p);
+      dp = 2.0f * (sigmoidf(p) - 1.0f);
+      dsum1 = d1;
+    } else {
+      const float lse0 = b.rowstat[(int64_t)(c * 2 + 0) * g.C + e];
+      const float lse1 = b.rowstat[(int64_t)(c * 2 + 1) * g.C + e];
+      loss = ((double)lse0 - p) + ((double)lse1 - p);
+      const float s0 = expf(p - lse0), s1 = expf(p - lse1);
+      dp = (s0 - 1.0f) + (s1 - 1.0f);
+      dsum1 = 1.0f - s1;
+    }
+    b.dpos[ce] = dp;
+    b.dsum1[ce] = dsum1;
+    acc += loss;
+  }
+  // fixed-order block reduction of the chunk loss
+  __shared__ double red[256];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) b.chunkloss[c] = red[0];
+}
+
+__global__ void sum_chunks_kernel(const double* chunkloss, int n, double* out) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    double s = 0.0;
+    for (int c = 0; c < n; ++c) s += chunkloss[c];
+    *out = s;
+  }
+}
+
+// ---- operator / comparator backward: contributions and sort keys -----------
+__global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b, const float* relT) {
+  __shared__ float stage[4][512];
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int c = blockIdx.y;
+  const int Cc = chunk_edges(g, c);
+  const int Nc = Cc + g.U;
+  const int item = blockIdx.x * 4 + w;
+  if (item >= Cc + 2 * g.U) return;   // no block-level barriers below
+  const bool cplx = g.op == OP_COMPLEX;
+  const int d = g.d, dp = g.dp;
+  float* st = stage[w];
+  const bool cos = g.cmp == CMP_COS;
+  const bool has_rel = g.op != OP_IDENTITY;
+  const uint32_t tbl_j = g.same_table ? 0u : 1u;
+  const int64_t kbase = (int64_t)c * 2 * g.N;   // compact key position of the chunk
+
+  if (item < Cc) {
+    const int e = item;
+    const int64_t ce = (int64_t)c * g.C + e;
+    const int s = b.src[ce];
+    const int t = b.dst[ce];
+    const int r = b.rel ? b.rel[ce] : 0;
+    Row th;
+    if (has_rel && g.op != OP_LINEAR) row_load(th, b.relp + (int64_t)r * g.dr, d, cplx, lane);
+    else row_zero(th);
+    const float dpe = b.dpos[ce];
+    float* dq0 = b.dq + ((int64_t)(c * 2 + 0) * g.C + e) * dp;
+    const float* dq1 = b.dq + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
+    float* dn0 = b.dn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
+    float* dn1 = b.dn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
+    const float* q = b.qk + ((int64_t)(c * 2 + 0) * g.C + e) * dp;
+    const float* kr = b.qk + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
+    Row Q, Kv, gq0, gq1, gn0, gn1;
+    row_load(Q, q, d, cplx, lane);
+    row_load(Kv, kr, d, cplx, lane);
+    row_load(gq0, dq0, d, cplx, lane);
+    row_load(gq1, dq1, d, cplx, lane);
+    row_load(gn0, dn0, d, cplx, lane);
+    row_load(gn1, dn1, d, cplx, lane);
+    Row gs, gd, grel;
+    row_zero(grel);
+    if (!cos) {
+      // raw rows: x_s is N1[e], x_d is N0[e]
+      Row x, y;
+      row_load(x, b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp, d, cplx, lane);
+      row_load(y, b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp, d, cplx, lane);
+      Row dQ = gq0;
+      row_axpy(dQ, dpe, y);                         // positive: dp * x_d
+      const float dsum = b.dsum1[ce];               // gradient of the translation bias
+      // source row: J_g^T dQ + its in-chunk candidate gradient
+      if (g.op == OP_LINEAR) mat_apply(gs, b.relp + (int64_t)r * d * d, dQ, st, d, lane);  // A^T dQ
+      else gs = op_adjoint(g.op, dQ, th);
+      row_add(gs, gn1);
+      // destination row: candidate gradient + positive + J_{g*}^T dK (+ bias)
+      gd = gn0;
+      row_axpy(gd, dpe, Q);
+      Row jk;
+      if (g.op == OP_LINEAR) mat_apply(jk, relT + (int64_t)r * d * d, gq1, st, d, lane);   // A dK
+      else if (g.op == OP_DIAGONAL || g.op == OP_COMPLEX) jk = op_forward(g.op, gq1, th);
+      else jk = gq1;
+      row_add(gd, jk);
+      if (g.op == OP_TRANSLATION) row_axpy(gd, dsum, th);
+      if (g.op == OP_TRANSLATION) {
+        grel = dQ;
+        row_axpy(grel, dsum, y);
+      } else if (g.op == OP_DIAGONAL || g.op == OP_COMPLEX) {
+        grel = op_param_grad(g.op, x, dQ);
+        row_add(grel, op_adjoint_param_grad(g.op, y, gq1));
+      } else if (g.op == OP_LINEAR) {
+        row_store(dQ, dq0, d, dp, false, lane);     // dA = dQ^T X + Y^T dK, by contraction
+      }
+    } else {
+      const float nq = b.nrm[(int64_t)(c * 2 + 1) * g.N + e];
+      const float ny = b.nrm[(int64_t)(c * 2 + 0) * g.N + e];
+      Row dQh = gq0;                                 // Q^ is also source candidate e
+      row_axpy(dQh, dpe, Kv);
+      row_add(dQh, gn1);
+      Row dYh = gn0;                                 // x^_d is destination candidate e and K^_e
+      row_add(dYh, gq1);
+      row_axpy(dYh, dpe, Q);
+      const Row dv = normalize_backward(Q, nq, dQh); // dL/dg(x_s)
+      if (g.op == OP_LINEAR) mat_apply(gs, b.relp + (int64_t)r * d * d, dv, st, d, lane);
+      else gs = op_adjoint(g.op, dv, th);
+      gd = normalize_backward(Kv, ny, dYh);
+      if (g.op == OP_TRANSLATION) {
+        grel = dv;
+      } else if (g.op == OP_DIAGONAL || g.op == OP_COMPLEX) {
+        Row x;
+        row_load(x, b.emb_i + (int64_t)s * d, d, cplx, lane);
+        grel = op_param_grad(g.op, x, dv);
+      }
+    }
+    row_store(gd, dn0, d, dp, cplx, lane);
+    row_store(gs, dn1, d, dp, cplx, lane);
+    if (has_rel && g.op != OP_LINEAR)
+      row_store(grel, b.relc + ((int64_t)c * g.N + e) * g.dr, d, g.dr, cplx, lane);
+    if (lane == 0) {
+      b.keys[kbase + e] = (tbl_j << g.rb) | (uint32_t)t;
+      b.vals[kbase + e] = (uint32_t)((c * 2 + 0) * g.N + e);
+      b.keys[kbase + Nc + e] = (uint32_t)s;
+      b.vals[kbase + Nc + e] = (uint32_t)((c * 2 + 1) * g.N + e);
+      if (b.rkeys) {
+        b.rkeys[ce] = (uint32_t)r;
+        b.rvals[ce] = (uint32_t)((int64_t)c * g.N + e);
+      }
+    }
+    return;
+  }
+
+  // uniform candidate rows
+  const int side = item < Cc + g.U ? 0 : 1;
+  const int k = item - Cc - side * g.U;
+  const int tpos = Cc + k;
+  const int32_t u = b.neg[(int64_t)(c * 2 + side) * g.U + k];
+  float* dnr = b.dn + ((int64_t)(c * 2 + side) * g.N + tpos) * dp;
+  if (cos) {
+    Row vh, gv;
+    row_load(vh, b.nn + ((int64_t)(c * 2 + side) * g.N + tpos) * dp, d, cplx, lane);
+    row_load(gv, dnr, d, cplx, lane);
+    const float nv = b.nrm[(int64_t)(c * 2 + side) * g.N + tpos];
+    Row dv = normalize_backward(vh, nv, gv);
+    if (side == 1 && has_rel) {
+      // the single relation's operator was applied to this source candidate
+      Row th, x;
+      if (g.op == OP_LINEAR) {
+        mat_apply(dv, b.relp, dv, st, d, lane);
+      } else {
+        row_load(th, b.relp, d, cplx, lane);
+        row_load(x, b.emb_i + (int64_t)u * d, d, cplx, lane);
+        const Row grel = g.op == OP_TRANSLATION ? dv : op_param_grad(g.op, x, dv);
+        row_store(grel, b.relc + ((int64_t)c * g.N + g.C + k) * g.dr, d, g.dr, cplx, lane);
+        dv = op_adjoint(g.op, dv, th);
+      }
+    }
+    row_store(dv, dnr, d, dp, cplx, lane);
+  }
+  if (lane == 0) {
+    const uint32_t key = side == 0 ? ((tbl_j << g.rb) | (uint32_t)u) : (uint32_t)u;
+    b.keys[kbase + side * Nc + tpos] = key;
+    b.vals[kbase + side * Nc + tpos] = (uint32_t)((c * 2 + side) * g.N + tpos);
+  }
+}
+
+}  // namespace
+
+void launch_softmax_rows(const StepGeom& g, const StepBufs& b, hipStream_t s) {
+  dim3 grid((g.C + 3) / 4, g.nchunks * 2);
+  softmax_rows_kernel<<<grid, 256, 0, s>>>(g, b);
+}
+
+void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, hipStream_t s) {
+  finalize_kernel<<<g.nchunks, 256, 0, s>>>(g, b);
+  sum_chunks_kernel<<<1, 64, 0, s>>>(b.chunkloss, g.nchunks, step_loss_slot);
+}
+
+void launch_op_backward(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s) {
+  dim3 grid((g.C + 2 * g.U + 3) / 4, g.nchunks);
+  op_backward_kernel<<<grid, 256, 0, s>>>(g, b, relT);
+}

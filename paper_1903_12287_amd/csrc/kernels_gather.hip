@@ -1,0 +1,137 @@
+// Gather + relation operator + uniform negatives (Sec. 3.1 score function,
+// Sec. 4.3 batched negatives, Fig. 3).
+//
+// One wave per work item; the items of chunk c are
+//   e in [0, Cc)          an edge: its source and destination rows,
+//   Cc + k, k in [0, U)   uniform destination candidate k (partition j),
+//   Cc + U + k            uniform source candidate k (partition i).
+// For the dot comparator the source corruptions use the adjoint of g
+// (<g(x), y> = <x, g*(y)>, plus <theta, y> for translation), so every
+// candidate row is copied raw.  For cos every packed row is a unit vector and
+// the source candidates carry g (one relation, or the identity operator).
+#include "kernels.h"
+#include "row_ops.h"
+
+namespace {
+
+__global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b, const float* relT) {
+  __shared__ float stage[4][512];
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int c = blockIdx.y;
+  const int Cc = chunk_edges(g, c);
+  const int item = blockIdx.x * 4 + w;
+  const bool cplx = g.op == OP_COMPLEX;
+  const bool active = item < Cc + 2 * g.U;
+  const int d = g.d, dp = g.dp;
+  float* st = stage[w];
+
+  if (!active) return;   // no block-level barriers below: idle waves may leave
+  if (item < Cc) {
+    // ---- edge item
+    const int e = item;
+    const int64_t eg = (int64_t)c * g.C + e;
+    const int s = b.src[eg];
+    const int t = b.dst[eg];
+    const int r = b.rel ? b.rel[eg] : 0;
+    Row x, y, th;
+    row_load(x, b.emb_i + (int64_t)s * d, d, cplx, lane);
+    row_load(y, b.emb_j + (int64_t)t * d, d, cplx, lane);
+    if (g.op != OP_IDENTITY && g.op != OP_LINEAR) row_load(th, b.relp + (int64_t)r * g.dr, d, cplx, lane);
+    else row_zero(th);
+    Row gq;
+    if (g.op == OP_LINEAR) mat_apply(gq, relT + (int64_t)r * d * d, x, st, d, lane);   // A x
+    else gq = op_forward(g.op, x, th);
+    float* qrow = b.qk + ((int64_t)(c * 2 + 0) * g.C + e) * dp;
+    float* krow = b.qk + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
+    float* n0row = b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
+    float* n1row = b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
+    if (g.cmp == CMP_DOT) {
+      Row k;
+      if (g.op == OP_LINEAR) mat_apply(k, b.relp + (int64_t)r * d * d, y, st, d, lane);   // A^T y
+      else if (g.op == OP_TRANSLATION) k = y;
+      else k = op_adjoint(g.op, y, th);
+      const float p = row_dot(gq, y);
+      const float bs = g.op == OP_TRANSLATION ? row_dot(th, y) : 0.0f;
+      row_store(gq, qrow, d, dp, cplx, lane);
+      row_store(k, krow, d, dp, cplx, lane);
+      row_store(y, n0row, d, dp, cplx, lane);
+      row_store(x, n1row, d, dp, cplx, lane);
+      if (lane == 0) {
+        b.pos[(int64_t)c * g.C + e] = p;
+        b.bias[(int64_t)c * g.C + e] = bs;
+      }
+    } else {
+      const float nq = row_normalize(gq);
+      const float ny = row_normalize(y);
+      const float p = row_dot(gq, y);
+      row_store(gq, qrow, d, dp, cplx, lane);
+      row_store(gq, n1row, d, dp, cplx, lane);
+      row_store(y, krow, d, dp, cplx, lane);
+      row_store(y, n0row, d, dp, cplx, lane);
+      if (lane == 0) {
+        b.pos[(int64_t)c * g.C + e] = p;
+        b.bias[(int64_t)c * g.C + e] = 0.0f;
+        b.nrm[(int64_t)(c * 2 + 0) * g.N + e] = ny;
+        b.nrm[(int64_t)(c * 2 + 1) * g.N + e] = nq;
+      }
+    }
+    return;
+  }
+
+  // ---- uniform candidate
+  const int side = item < Cc + g.U ? 0 : 1;
+  const int k = item - Cc - side * g.U;
+  const uint32_t rows = side == 0 ? (uint32_t)g.rows_j : (uint32_t)g.rows_i;
+  const int32_t u = uniform_negative(g.seed, g.bucket, (uint64_t)(g.chunk0 + c), (uint32_t)side,
+                                     (uint32_t)k, rows);
+  const float* tbl = side == 0 ? b.emb_j : b.emb_i;
+  Row v;
+  row_load(v, tbl + (int64_t)u * d, d, cplx, lane);
+  float nv = 0.0f;
+  if (g.cmp == CMP_COS) {
+    if (side == 1 && g.op != OP_IDENTITY) {
+      // one relation: its operator is applied to every source candidate
+      if (g.op == OP_LINEAR) {
+        mat_apply(v, relT, v, st, d, lane);
+      } else {
+        Row th;
+        row_load(th, b.relp, d, cplx, lane);
+        v = op_forward(g.op, v, th);
+      }
+    }
+    nv = row_normalize(v);
+  }
+  const int t = Cc + k;
+  row_store(v, b.nn + ((int64_t)(c * 2 + side) * g.N + t) * dp, d, dp, cplx, lane);
+  if (lane == 0) {
+    b.neg[(int64_t)(c * 2 + side) * g.U + k] = u;
+    if (g.cmp == CMP_COS) b.nrm[(int64_t)(c * 2 + side) * g.N + t] = nv;
+  }
+}
+
+// row-major d x d matrices -> transposed copies (linear operator)
+__global__ void transpose_rel_kernel(const float* A, float* AT, int R, int d) {
+  const int64_t n = (int64_t)R * d * d;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = idx / ((int64_t)d * d);
+    const int rem = (int)(idx - r * d * d);
+    const int k = rem / d, l = rem % d;
+    AT[r * d * d + (int64_t)l * d + k] = A[idx];
+  }
+}
+
+}  // namespace
+
+void launch_gather(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s) {
+  dim3 grid((g.C + 2 * g.U + 3) / 4, g.nchunks);
+  gather_op_kernel<<<grid, 256, 0, s>>>(g, b, relT);
+}
+
+void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s) {
+  const int64_t n = (int64_t)R * d * d;
+  int blocks = (int)((n + 255) / 256);
+  if (blocks > 4096) blocks = 4096;
+  transpose_rel_kernel<<<blocks, 256, 0, s>>>(A, AT, R, d);
+}

@@ -1,0 +1,674 @@
+// Host runtime behind the C ABI of include/pbg.h: context, argument checks,
+// workspace, and the launch sequence of one training step.
+//
+// A step (chunks_per_step chunks of a bucket) is, on the compute stream:
+//   gather + operator + uniform draws  ->  score contraction with the loss
+//   epilogue (softmax: + row pass)  ->  per-edge finalisation (dL/dp, loss)
+//   ->  dQ = dS.N and dN = dS^T.Q  ->  operator backward into per-row
+//   contributions  ->  stable sort of the contributions by row  ->  segment
+//   sums + row-wise Adagrad  ->  relation sums + element-wise Adagrad.
+// No host synchronisation happens inside the step loop.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "pbg.h"
+#include "runtime_internal.h"
+
+static const char* kNullCtxError = "pbg: NULL context";
+
+pbg_status set_err(pbg_ctx* ctx, pbg_status st, const char* fmt, ...) {
+  if (!ctx) return st;
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  ctx->err = buf;
+  return st;
+}
+
+pbg_status hip_fail(pbg_ctx* ctx, hipError_t e, const char* what) {
+  return set_err(ctx, PBG_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+void* Arena::get(size_t bytes) {
+  if (bytes == 0) bytes = 16;
+  bytes = (bytes + 255) & ~(size_t)255;
+  void* p = nullptr;
+  if (hipMalloc(&p, bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    failed = true;
+    return nullptr;
+  }
+  ptrs.push_back(p);
+  return p;
+}
+
+void Arena::release() {
+  for (void* p : ptrs) (void)hipFree(p);
+  ptrs.clear();
+  failed = false;
+}
+
+static int bits_for(uint64_t v) {  // bits needed for values in [0, v]
+  int b = 0;
+  while (b < 64 && (v >> b) != 0) ++b;
+  return b;
+}
+
+static int round_up(int v, int m) { return (v + m - 1) / m * m; }
+
+bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width) {
+  const int64_t nblocks = (max_n + 4095) / 4096;
+  const int64_t scan_n = std::max<int64_t>(max_n, 256 * nblocks);
+  w.max_n = (int)max_n;
+  w.keys_alt = (uint32_t*)a.get(max_n * 4);
+  w.vals_alt = (uint32_t*)a.get(max_n * 4);
+  w.hist = (uint32_t*)a.get(256 * nblocks * 4);
+  w.flags = (uint32_t*)a.get(max_n * 4);
+  w.seg_start = (uint32_t*)a.get((max_n + 1) * 4);
+  w.piece_start = (uint32_t*)a.get((max_n + 1) * 4);
+  w.piece_seg = (uint32_t*)a.get(max_n * 4);
+  w.seg_first_piece = (uint32_t*)a.get((max_n + 1) * 4);
+  w.counts = (uint32_t*)a.get(16);
+  w.scan_tmp = (uint32_t*)a.get(((scan_n + 4095) / 4096 + 1) * 4);
+  w.partial = width > 0 ? (float*)a.get(max_n * (int64_t)width * 4) : nullptr;
+  return !a.failed;
+}
+
+static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
+  if (ctx->ws_ready && ctx->wC == C && ctx->wU == U && ctx->wS == S) return PBG_OK;
+  (void)hipStreamSynchronize(ctx->cs);
+  ctx->ws.release();
+  ctx->ws_ready = false;
+  Arena& a = ctx->ws;
+  const int N = C + U;
+  const int d = ctx->d, dp = round_up(d, 4), Np = round_up(N, 4);
+  const int nct = (Np + PBG_SCORE_BN - 1) / PBG_SCORE_BN;
+  const int64_t s = S;
+  StepBufs& b = ctx->bufs;
+  memset(&b, 0, sizeof(b));
+  b.qk = (float*)a.get(s * 2 * C * dp * 4);
+  b.nn = (float*)a.get(s * 2 * N * dp * 4);
+  b.nrm = (float*)a.get(s * 2 * N * 4);
+  b.pos = (float*)a.get(s * C * 4);
+  b.bias = (float*)a.get(s * C * 4);
+  b.neg = (int32_t*)a.get(s * 2 * std::max(U, 1) * 4);
+  b.ds = (float*)a.get(s * 2 * C * (int64_t)Np * 4);
+  b.rowpart = (float*)a.get(s * 2 * C * nct * 2 * 4);
+  b.rowstat = (float*)a.get(s * 2 * C * 4);
+  b.dpos = (float*)a.get(s * C * 4);
+  b.dsum1 = (float*)a.get(s * C * 4);
+  b.chunkloss = (double*)a.get(s * 8);
+  b.dq = (float*)a.get(s * 2 * C * dp * 4);
+  b.dn = (float*)a.get(s * 2 * N * dp * 4);
+  const bool has_rel = ctx->op != OP_IDENTITY;
+  const bool linear = ctx->op == OP_LINEAR;
+  if (has_rel && !linear) b.relc = (float*)a.get(s * N * ctx->dr * 4);
+  const int64_t nkeys = s * 2 * N;
+  b.keys = (uint32_t*)a.get(nkeys * 4);
+  b.vals = (uint32_t*)a.get(nkeys * 4);
+  if (has_rel && ctx->R > 1) {
+    b.rkeys = (uint32_t*)a.get(s * C * 4);
+    b.rvals = (uint32_t*)a.get(s * C * 4);
+  }
+  const int width = std::max(d, has_rel && !linear ? ctx->dr : 0);
+  if (!alloc_sortwork(a, ctx->sw, std::max<int64_t>(nkeys, s * C), width)) {
+    ctx->ws.release();
+    return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "workspace allocation failed (C=%d U=%d S=%d)", C, U, S);
+  }
+  if (has_rel) {
+    const int64_t w = linear ? 2 * s * (int64_t)d * d : s * (int64_t)ctx->dr;
+    ctx->relpartial = (float*)a.get(w * 4);
+  }
+  if (linear) ctx->relT = (float*)a.get((int64_t)ctx->R * d * d * 4);
+  ctx->flag_dev = (uint32_t*)a.get(16);
+  if (a.failed) {
+    ctx->ws.release();
+    return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "workspace allocation failed (C=%d U=%d S=%d)", C, U, S);
+  }
+  ctx->wC = C;
+  ctx->wU = U;
+  ctx->wS = S;
+  ctx->ws_ready = true;
+  return PBG_OK;
+}
+
+static pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps) {
+  if (ctx->steploss_cap >= nsteps && ctx->steploss_dev) return PBG_OK;
+  if (ctx->steploss_dev) (void)hipFree(ctx->steploss_dev);
+  ctx->steploss_dev = nullptr;
+  ctx->steploss_cap = 0;
+  if (hipMalloc(&ctx->steploss_dev, (size_t)std::max<int64_t>(nsteps, 1) * 8) != hipSuccess) {
+    (void)hipGetLastError();
+    ctx->steploss_dev = nullptr;
+    return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "step-loss buffer allocation failed");
+  }
+  ctx->steploss_cap = nsteps;
+  return PBG_OK;
+}
+
+// --------------------------------------------------------------------------
+// C ABI
+// --------------------------------------------------------------------------
+extern "C" {
+
+pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_partitions,
+                           int32_t num_relations, int32_t dim, int32_t op, int32_t cmp, int32_t loss,
+                           float margin, uint32_t flags) {
+  if (!out) return PBG_ERR_INVALID_ARG;
+  *out = nullptr;
+  pbg_ctx* ctx = new (std::nothrow) pbg_ctx();
+  if (!ctx) return PBG_ERR_OUT_OF_MEMORY;
+  auto fail = [&](pbg_status st, const char* msg) {
+    // keep the context so the caller can read the message, then report
+    ctx->err = msg;
+    ctx->invalid = true;
+    *out = ctx;
+    return st;
+  };
+  if (num_entities < 1 || num_partitions < 1 || num_relations < 1)
+    return fail(PBG_ERR_INVALID_ARG, "num_entities, num_partitions and num_relations must be >= 1");
+  if (dim < 1 || dim > 512) return fail(PBG_ERR_INVALID_ARG, "dim must be in [1, 512]");
+  if (op < PBG_OP_IDENTITY || op > PBG_OP_COMPLEX_DIAGONAL) return fail(PBG_ERR_INVALID_ARG, "unknown operator");
+  if (cmp < PBG_CMP_DOT || cmp > PBG_CMP_COS) return fail(PBG_ERR_INVALID_ARG, "unknown comparator");
+  if (loss < PBG_LOSS_RANKING || loss > PBG_LOSS_SOFTMAX) return fail(PBG_ERR_INVALID_ARG, "unknown loss");
+  if (op == PBG_OP_COMPLEX_DIAGONAL && (dim % 2)) return fail(PBG_ERR_INVALID_ARG, "complex_diagonal needs an even dim");
+  if (!std::isfinite(margin)) return fail(PBG_ERR_INVALID_ARG, "margin must be finite");
+  if (flags & ~(uint32_t)PBG_F_BF16_SCORE) return fail(PBG_ERR_INVALID_ARG, "unknown flags");
+  const int64_t ps = (num_entities + num_partitions - 1) / num_partitions;
+  if ((int64_t)(num_partitions - 1) * ps >= num_entities)
+    return fail(PBG_ERR_INVALID_ARG, "a partition would be empty (num_partitions too large for num_entities)");
+  if (ps > (1ll << 30)) return fail(PBG_ERR_INVALID_ARG, "partitions above 2^30 rows are not supported");
+  if (cmp == PBG_CMP_COS && op != PBG_OP_IDENTITY && num_relations > 1)
+    return fail(PBG_ERR_UNSUPPORTED, "cos with a non-identity operator needs a single relation");
+  if (op == PBG_OP_LINEAR && (num_relations > 1 || cmp == PBG_CMP_COS))
+    return fail(PBG_ERR_UNSUPPORTED, "the linear operator is implemented for one relation with dot");
+  if (flags & PBG_F_BF16_SCORE) return fail(PBG_ERR_UNSUPPORTED, "the bf16 score path is not built yet");
+  ctx->n = num_entities;
+  ctx->P = num_partitions;
+  ctx->R = num_relations;
+  ctx->d = dim;
+  ctx->op = op;
+  ctx->cmp = cmp;
+  ctx->loss = loss;
+  ctx->margin = margin;
+  ctx->flags = flags;
+  ctx->ps = ps;
+  ctx->dr = op == PBG_OP_IDENTITY ? 0 : (op == PBG_OP_LINEAR ? dim * dim : dim);
+  ctx->parts.assign(num_partitions, Partition());
+  if (hipGetDevice(&ctx->device) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(PBG_ERR_DEVICE, "no HIP device");
+  }
+  *out = ctx;
+  return PBG_OK;
+}
+
+void pbg_free(pbg_ctx* ctx) {
+  if (!ctx) return;
+  if (ctx->cs || true) (void)hipDeviceSynchronize();
+  ctx->ws.release();
+  if (ctx->steploss_dev) (void)hipFree(ctx->steploss_dev);
+  for (auto& s : ctx->slots)
+    if (s.emb) (void)hipFree(s.emb);
+  delete ctx;
+}
+
+const char* pbg_last_error(const pbg_ctx* ctx) {
+  if (!ctx) return kNullCtxError;
+  return ctx->err.c_str();
+}
+
+int64_t pbg_partition_rows(const pbg_ctx* ctx, int32_t p) {
+  if (!ctx || ctx->invalid || p < 0 || p >= ctx->P) return -1;
+  return std::min<int64_t>(ctx->ps, ctx->n - (int64_t)p * ctx->ps);
+}
+
+int64_t pbg_relation_param_floats(const pbg_ctx* ctx) {
+  if (!ctx || ctx->invalid) return -1;
+  return (int64_t)ctx->R * ctx->dr;
+}
+
+pbg_status pbg_bind_partition(pbg_ctx* ctx, int32_t p, float* emb, float* adagrad, int32_t where) {
+  if (!ctx) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
+  if (p < 0 || p >= ctx->P) return set_err(ctx, PBG_ERR_INVALID_ARG, "partition %d out of range", p);
+  if (!emb || !adagrad) return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL embedding or accumulator");
+  if (where != PBG_MEM_DEVICE && where != PBG_MEM_PINNED_HOST)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "unknown memory kind %d", where);
+  ctx->parts[p].emb = emb;
+  ctx->parts[p].G = adagrad;
+  ctx->parts[p].where = where;
+  ctx->err.clear();
+  return PBG_OK;
+}
+
+pbg_status pbg_bind_relations(pbg_ctx* ctx, float* params, float* adagrad) {
+  if (!ctx) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
+  if (ctx->op == PBG_OP_IDENTITY) return PBG_OK;
+  if (!params || !adagrad) return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL relation parameters or accumulator");
+  ctx->relp = params;
+  ctx->relG = adagrad;
+  ctx->err.clear();
+  return PBG_OK;
+}
+
+pbg_status pbg_set_streams(pbg_ctx* ctx, void* compute_stream, void* copy_stream) {
+  if (!ctx) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
+  ctx->cs = (hipStream_t)compute_stream;
+  ctx->xs = (hipStream_t)copy_stream;
+  return PBG_OK;
+}
+
+pbg_status pbg_get_stats(const pbg_ctx* ctx, pbg_stats* out_host) {
+  if (!ctx || !out_host) return PBG_ERR_INVALID_ARG;
+  *out_host = ctx->stats;
+  return PBG_OK;
+}
+
+pbg_status pbg_get_step_losses(const pbg_ctx* ctx, double* out_host, int64_t capacity,
+                               int64_t* n_steps_host) {
+  if (!ctx || (capacity > 0 && !out_host)) return PBG_ERR_INVALID_ARG;
+  const int64_t n = (int64_t)ctx->step_losses.size();
+  for (int64_t k = 0; k < std::min(capacity, n); ++k) out_host[k] = ctx->step_losses[k];
+  if (n_steps_host) *n_steps_host = n;
+  return PBG_OK;
+}
+
+}  // extern "C"
+
+// --------------------------------------------------------------------------
+// training
+// --------------------------------------------------------------------------
+pbg_status check_neg_config(pbg_ctx* ctx, const pbg_neg_config* neg) {
+  if (!neg) return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL negative config");
+  if (neg->chunk_size < 1 || neg->chunk_size > (1 << 16))
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "chunk_size must be in [1, 65536]");
+  if (neg->num_uniform < 0 || neg->num_uniform > (1 << 16))
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "num_uniform must be in [0, 65536]");
+  if (neg->chunk_size + neg->num_uniform < 2)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "chunk_size + num_uniform must be >= 2");
+  if (neg->chunks_per_step < 1 || neg->chunks_per_step > 4096)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "chunks_per_step must be in [1, 4096]");
+  if (neg->reserved != 0) return set_err(ctx, PBG_ERR_INVALID_ARG, "reserved field must be 0");
+  if (neg->first_chunk < 0 || neg->first_chunk > 0xFFFFFFFFll)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "first_chunk out of range");
+  const int64_t keys = (int64_t)neg->chunks_per_step * 2 * (neg->chunk_size + neg->num_uniform);
+  if (keys > (1ll << 28)) return set_err(ctx, PBG_ERR_INVALID_ARG, "step too large");
+  return PBG_OK;
+}
+
+// Runs the step loop on already-validated, device-resident partitions.
+pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i, float* G_i,
+                               float* emb_j, float* G_j, const int32_t* src, const int32_t* rel,
+                               const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg,
+                               float lr, uint64_t seed, double* loss_out,
+                               std::vector<double>* step_losses) {
+  const int C = neg->chunk_size, U = neg->num_uniform, S = neg->chunks_per_step;
+  pbg_status st = ensure_workspace(ctx, C, U, S);
+  if (st != PBG_OK) return st;
+  const int64_t nchunks = (n_edges + C - 1) / C;
+  const int64_t nsteps = (nchunks + S - 1) / S;
+  st = ensure_steploss(ctx, nsteps);
+  if (st != PBG_OK) return st;
+  hipStream_t cs = ctx->cs;
+  const int N = C + U;
+  const int d = ctx->d, dp = round_up(d, 4), Np = round_up(N, 4);
+  const int64_t rows_i = pbg_partition_rows(ctx, i), rows_j = pbg_partition_rows(ctx, j);
+
+  StepGeom g;
+  memset(&g, 0, sizeof(g));
+  g.C = C;
+  g.U = U;
+  g.N = N;
+  g.d = d;
+  g.dp = dp;
+  g.Np = Np;
+  g.dr = ctx->dr;
+  g.nct = (Np + PBG_SCORE_BN - 1) / PBG_SCORE_BN;
+  g.op = ctx->op;
+  g.cmp = ctx->cmp;
+  g.loss = ctx->loss;
+  g.margin = ctx->margin;
+  g.same_table = (i == j) ? 1 : 0;
+  g.rows_i = (int)rows_i;
+  g.rows_j = (int)rows_j;
+  g.rb = bits_for((uint64_t)std::max(rows_i, rows_j) - 1);
+  if (g.rb < 1) g.rb = 1;
+  g.bucket = (uint32_t)(i * ctx->P + j);
+  g.seed = seed;
+  const int key_bits = g.rb + (g.same_table ? 0 : 1);
+  const int rel_bits = bits_for((uint64_t)ctx->R - 1);
+  const bool has_rel = ctx->op != OP_IDENTITY;
+  const bool linear = ctx->op == OP_LINEAR;
+
+  StepBufs b = ctx->bufs;
+  b.emb_i = emb_i;
+  b.emb_j = emb_j;
+  b.G_i = G_i;
+  b.G_j = G_j;
+  b.relp = ctx->relp;
+  b.relG = ctx->relG;
+  if (!(has_rel && ctx->R > 1 && !linear)) {
+    b.rkeys = nullptr;
+    b.rvals = nullptr;
+  }
+
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  (void)hipEventCreate(&ev0);
+  (void)hipEventCreate(&ev1);
+  (void)hipEventRecord(ev0, cs);
+
+  for (int64_t t = 0; t < nsteps; ++t) {
+    const int64_t c0 = t * S;
+    const int nch = (int)std::min<int64_t>(S, nchunks - c0);
+    const int m_step = (int)std::min<int64_t>((int64_t)S * C, n_edges - c0 * C);
+    g.nchunks = nch;
+    g.m_step = m_step;
+    g.chunk0 = neg->first_chunk + c0;
+    b.src = src + c0 * C;
+    b.dst = dst + c0 * C;
+    b.rel = rel ? rel + c0 * C : nullptr;
+
+    if (linear) launch_transpose_rel(ctx->relp, ctx->relT, ctx->R, d, cs);
+    launch_gather(g, b, ctx->relT, cs);
+
+    // score contraction + loss epilogue
+    GemmArgs fa;
+    memset(&fa, 0, sizeof(fa));
+    fa.A = b.qk;
+    fa.B = b.nn;
+    fa.Cm = b.ds;
+    fa.a_cs = 2ll * C * dp;
+    fa.a_ss = (int64_t)C * dp;
+    fa.b_cs = 2ll * N * dp;
+    fa.b_ss = (int64_t)N * dp;
+    fa.c_cs = 2ll * C * Np;
+    fa.c_ss = (int64_t)C * Np;
+    fa.lda = dp;
+    fa.ldb = dp;
+    fa.ldc = Np;
+    fa.mdim = DIM_CC;
+    fa.ndim = DIM_NC;
+    fa.kdim = DIM_FIXED;
+    fa.Kfix = dp;
+    fa.C = C;
+    fa.U = U;
+    fa.m_step = m_step;
+    fa.nsides = 2;
+    fa.pos = b.pos;
+    fa.bias = (ctx->op == OP_TRANSLATION && ctx->cmp == CMP_DOT) ? b.bias : nullptr;
+    fa.rowpart = b.rowpart;
+    fa.nct = g.nct;
+    fa.loss = ctx->loss;
+    fa.margin = ctx->margin;
+    const int epi = ctx->loss == LOSS_SOFTMAX ? EPI_SOFTMAX_STATS : EPI_LOSS;
+    launch_gemm_f32(fa, GEMM_NT, epi, 8, g.nct, (C + 127) / 128, nch * 2, cs);
+    if (ctx->loss == LOSS_SOFTMAX) launch_softmax_rows(g, b, cs);
+    launch_finalize(g, b, ctx->steploss_dev + t, cs);
+
+    // dQ = dS . N (per side)
+    const int nb = gemm_pick_nb(dp);
+    const int gn = (dp + 16 * nb - 1) / (16 * nb);
+    GemmArgs qa;
+    memset(&qa, 0, sizeof(qa));
+    qa.A = b.ds;
+    qa.B = b.nn;
+    qa.Cm = b.dq;
+    qa.a_cs = 2ll * C * Np;
+    qa.a_ss = (int64_t)C * Np;
+    qa.b_cs = 2ll * N * dp;
+    qa.b_ss = (int64_t)N * dp;
+    qa.c_cs = 2ll * C * dp;
+    qa.c_ss = (int64_t)C * dp;
+    qa.lda = Np;
+    qa.ldb = dp;
+    qa.ldc = dp;
+    qa.mdim = DIM_CC;
+    qa.ndim = DIM_FIXED;
+    qa.Nfix = dp;
+    qa.kdim = DIM_NC;
+    qa.C = C;
+    qa.U = U;
+    qa.m_step = m_step;
+    qa.nsides = 2;
+    launch_gemm_f32(qa, GEMM_NN, EPI_STORE, nb, gn, (C + 127) / 128, nch * 2, cs);
+    // dN = dS^T . Q (per side)
+    GemmArgs na = qa;
+    na.A = b.ds;
+    na.B = b.qk;
+    na.Cm = b.dn;
+    na.a_cs = 2ll * C * Np;
+    na.a_ss = (int64_t)C * Np;
+    na.b_cs = 2ll * C * dp;
+    na.b_ss = (int64_t)C * dp;
+    na.c_cs = 2ll * N * dp;
+    na.c_ss = (int64_t)N * dp;
+    na.lda = Np;
+    na.ldb = dp;
+    na.ldc = dp;
+    na.mdim = DIM_NC;
+    na.kdim = DIM_CC;
+    launch_gemm_f32(na, GEMM_TN, EPI_STORE, nb, gn, (N + 127) / 128, nch * 2, cs);
+
+    launch_op_backward(g, b, ctx->relT, cs);
+
+    // entities: sort contribution rows by (table, row), segment sums, Adagrad
+    const int nkeys = 2 * (nch * U + m_step);
+    launch_radix_sort(b.keys, b.vals, nkeys, key_bits, ctx->sw, cs);
+    launch_entity_update(g, b, nkeys, ctx->sw, lr, cs);
+
+    // relations
+    if (has_rel) {
+      if (linear) {
+        // dA = sum over edges of dQ_e x_e^T + x_d,e dK_e^T, per chunk by contraction
+        GemmArgs la;
+        memset(&la, 0, sizeof(la));
+        la.A = b.dq;                       // dQ^T: (m = row of A, k = edge)
+        la.B = b.nn + (int64_t)N * dp;     // source rows x_s (N1[e])
+        la.Cm = ctx->relpartial;
+        la.a_cs = 2ll * C * dp;
+        la.b_cs = 2ll * N * dp;
+        la.c_cs = 2ll * d * d;
+        la.lda = dp;
+        la.ldb = dp;
+        la.ldc = d;
+        la.mdim = DIM_FIXED;
+        la.Mfix = d;
+        la.ndim = DIM_FIXED;
+        la.Nfix = d;
+        la.kdim = DIM_CC;
+        la.C = C;
+        la.U = U;
+        la.m_step = m_step;
+        la.nsides = 1;
+        const int lnb = gemm_pick_nb(d);
+        const int lgn = (d + 16 * lnb - 1) / (16 * lnb);
+        launch_gemm_f32(la, GEMM_TN, EPI_STORE, lnb, lgn, (d + 127) / 128, nch, cs);
+        GemmArgs lb = la;
+        lb.A = b.nn;                       // destination rows x_d (N0[e])
+        lb.B = b.dq + (int64_t)C * dp;     // dK
+        lb.Cm = ctx->relpartial + (int64_t)d * d;
+        lb.a_cs = 2ll * N * dp;
+        lb.b_cs = 2ll * C * dp;
+        launch_gemm_f32(lb, GEMM_TN, EPI_STORE, lnb, lgn, (d + 127) / 128, nch, cs);
+        launch_relation_single_adagrad(ctx->relp, ctx->relG, d * d, ctx->relpartial, 2 * nch, lr, cs);
+      } else if (ctx->R > 1) {
+        launch_radix_sort(b.rkeys, b.rvals, m_step, rel_bits, ctx->sw, cs);
+        launch_relation_update_sorted(g, b, m_step, ctx->sw, lr, cs);
+      } else {
+        launch_relation_chunk_sums(g, b.relc, ctx->dr, ctx->cmp == CMP_COS ? 1 : 0, ctx->relpartial, cs);
+        launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch, lr, cs);
+      }
+    }
+  }
+  (void)hipEventRecord(ev1, cs);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    (void)hipEventDestroy(ev0);
+    (void)hipEventDestroy(ev1);
+    return hip_fail(ctx, e, "kernel launch");
+  }
+  std::vector<double> losses((size_t)nsteps);
+  e = hipMemcpyAsync(losses.data(), ctx->steploss_dev, (size_t)nsteps * 8, hipMemcpyDeviceToHost, cs);
+  if (e == hipSuccess) e = hipStreamSynchronize(cs);
+  float ms = 0.f;
+  if (e == hipSuccess) (void)hipEventElapsedTime(&ms, ev0, ev1);
+  (void)hipEventDestroy(ev0);
+  (void)hipEventDestroy(ev1);
+  if (e != hipSuccess) return hip_fail(ctx, e, "training step");
+  double total = 0.0;
+  for (double v : losses) total += v;
+  if (loss_out) *loss_out = total;
+  if (step_losses) step_losses->insert(step_losses->end(), losses.begin(), losses.end());
+  ctx->stats.total_ms += ms;
+  ctx->stats.edges += n_edges;
+  ctx->stats.chunks += nchunks;
+  ctx->stats.steps += nsteps;
+  // algorithmic work (full chunks approximated by the actual chunk sizes)
+  const double U_d = U;
+  for (int64_t c = 0; c < nchunks; ++c) {
+    const double Cc = (double)std::min<int64_t>(C, n_edges - c * C);
+    const double Nc = Cc + U_d;
+    ctx->stats.gather_bytes += (2 * Cc + 2 * U_d) * d * 4.0;
+    ctx->stats.score_flops += 12.0 * Cc * Nc * d;
+  }
+  return PBG_OK;
+}
+
+extern "C" pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
+                                       const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
+                                       const pbg_neg_config* neg, float lr, uint64_t seed,
+                                       double* loss_host) {
+  if (!ctx) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
+  ctx->err.clear();
+  if (i < 0 || i >= ctx->P || j < 0 || j >= ctx->P)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "bucket (%d, %d) out of range", i, j);
+  pbg_status st = check_neg_config(ctx, neg);
+  if (st != PBG_OK) return st;
+  if (!std::isfinite(lr) || lr < 0.f) return set_err(ctx, PBG_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (n_edges < 0 || n_edges > 0x7FFFFFFFll) return set_err(ctx, PBG_ERR_INVALID_ARG, "n_edges out of range");
+  const Partition& pi = ctx->parts[i];
+  const Partition& pj = ctx->parts[j];
+  if (!pi.emb || !pj.emb) return set_err(ctx, PBG_ERR_STATE, "partition %d or %d is not bound", i, j);
+  if (pi.where != PBG_MEM_DEVICE || pj.where != PBG_MEM_DEVICE)
+    return set_err(ctx, PBG_ERR_STATE, "pbg_train_bucket needs device-resident partitions");
+  if (ctx->op != OP_IDENTITY && !ctx->relp) return set_err(ctx, PBG_ERR_STATE, "relation parameters are not bound");
+  ctx->stats = pbg_stats();
+  ctx->step_losses.clear();
+  if (n_edges == 0) {
+    if (loss_host) *loss_host = 0.0;
+    return PBG_OK;
+  }
+  if (ctx->R > 1 && !rel) return set_err(ctx, PBG_ERR_INVALID_ARG, "rel may be NULL only with one relation");
+  if (!src_local || !dst_local) return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL edge arrays");
+  st = ensure_workspace(ctx, neg->chunk_size, neg->num_uniform, neg->chunks_per_step);
+  if (st != PBG_OK) return st;
+  // device-side range check before any update
+  hipStream_t cs = ctx->cs;
+  hipError_t e = hipMemsetAsync(ctx->flag_dev, 0, 4, cs);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipMemsetAsync");
+  launch_check_ids(src_local, n_edges, (int32_t)pbg_partition_rows(ctx, i), ctx->flag_dev, 1u, cs);
+  launch_check_ids(dst_local, n_edges, (int32_t)pbg_partition_rows(ctx, j), ctx->flag_dev, 2u, cs);
+  if (rel) launch_check_ids(rel, n_edges, ctx->R, ctx->flag_dev, 4u, cs);
+  uint32_t flag = 0;
+  e = hipMemcpyAsync(&flag, ctx->flag_dev, 4, hipMemcpyDeviceToHost, cs);
+  if (e == hipSuccess) e = hipStreamSynchronize(cs);
+  if (e != hipSuccess) return hip_fail(ctx, e, "id range check");
+  if (flag & 1u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a source id is outside partition %d", i);
+  if (flag & 2u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a destination id is outside partition %d", j);
+  if (flag & 4u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a relation id is outside [0, %d)", ctx->R);
+  return train_bucket_device(ctx, i, j, pi.emb, pi.G, pj.emb, pj.G, src_local, rel, dst_local, n_edges,
+                             neg, lr, seed, loss_host, &ctx->step_losses);
+}
+
+extern "C" pbg_status pbg_score_edges(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
+                                      const int32_t* rel, const int32_t* dst_local, int64_t n,
+                                      float* scores) {
+  if (!ctx) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
+  ctx->err.clear();
+  if (i < 0 || i >= ctx->P || j < 0 || j >= ctx->P)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "bucket (%d, %d) out of range", i, j);
+  if (n < 0 || n > 0x7FFFFFFFll) return set_err(ctx, PBG_ERR_INVALID_ARG, "n out of range");
+  const Partition& pi = ctx->parts[i];
+  const Partition& pj = ctx->parts[j];
+  if (!pi.emb || !pj.emb || pi.where != PBG_MEM_DEVICE || pj.where != PBG_MEM_DEVICE)
+    return set_err(ctx, PBG_ERR_STATE, "partitions %d and %d must be bound in device memory", i, j);
+  if (ctx->op != OP_IDENTITY && !ctx->relp) return set_err(ctx, PBG_ERR_STATE, "relation parameters are not bound");
+  if (n == 0) return PBG_OK;
+  if (ctx->R > 1 && !rel) return set_err(ctx, PBG_ERR_INVALID_ARG, "rel may be NULL only with one relation");
+  if (!src_local || !dst_local || !scores) return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL array");
+  hipStream_t cs = ctx->cs;
+  uint32_t* flag_dev = nullptr;
+  float* relT = nullptr;
+  hipError_t e = hipMalloc(&flag_dev, 16);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipMalloc");
+  if (ctx->op == OP_LINEAR) {
+    e = hipMalloc(&relT, (size_t)ctx->R * ctx->d * ctx->d * 4);
+    if (e != hipSuccess) {
+      (void)hipFree(flag_dev);
+      return hip_fail(ctx, e, "hipMalloc");
+    }
+  }
+  (void)hipMemsetAsync(flag_dev, 0, 4, cs);
+  launch_check_ids(src_local, n, (int32_t)pbg_partition_rows(ctx, i), flag_dev, 1u, cs);
+  launch_check_ids(dst_local, n, (int32_t)pbg_partition_rows(ctx, j), flag_dev, 2u, cs);
+  if (rel) launch_check_ids(rel, n, ctx->R, flag_dev, 4u, cs);
+  uint32_t flag = 0;
+  e = hipMemcpyAsync(&flag, flag_dev, 4, hipMemcpyDeviceToHost, cs);
+  if (e == hipSuccess) e = hipStreamSynchronize(cs);
+  pbg_status st = PBG_OK;
+  if (e != hipSuccess) st = hip_fail(ctx, e, "id range check");
+  else if (flag) st = set_err(ctx, PBG_ERR_INVALID_ARG, "an id is out of range (flags %u)", flag);
+  if (st == PBG_OK) {
+    StepGeom g;
+    memset(&g, 0, sizeof(g));
+    g.d = ctx->d;
+    g.dp = round_up(ctx->d, 4);
+    g.dr = ctx->dr;
+    g.op = ctx->op;
+    g.cmp = ctx->cmp;
+    if (relT) launch_transpose_rel(ctx->relp, relT, ctx->R, ctx->d, cs);
+    launch_score_edges(g, pi.emb, pj.emb, ctx->relp, relT, src_local, rel, dst_local, n, scores, cs);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(cs);
+    if (e != hipSuccess) st = hip_fail(ctx, e, "score_edges");
+  }
+  (void)hipFree(flag_dev);
+  if (relT) (void)hipFree(relT);
+  return st;
+}
+
+extern "C" pbg_status pbg_sample_negatives(pbg_ctx* ctx, int32_t i, int32_t j, int64_t first_chunk,
+                                           int64_t n_chunks, int32_t num_uniform, uint64_t seed,
+                                           int32_t* out) {
+  if (!ctx) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
+  ctx->err.clear();
+  if (i < 0 || i >= ctx->P || j < 0 || j >= ctx->P)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "bucket (%d, %d) out of range", i, j);
+  if (first_chunk < 0 || n_chunks < 0 || first_chunk + n_chunks > 0x100000000ll || num_uniform < 0)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "chunk range or num_uniform out of range");
+  if (n_chunks == 0 || num_uniform == 0) return PBG_OK;
+  if (!out) return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL output");
+  launch_sample_negatives(seed, (uint32_t)(i * ctx->P + j), first_chunk, n_chunks, num_uniform,
+                          (uint32_t)pbg_partition_rows(ctx, j), (uint32_t)pbg_partition_rows(ctx, i),
+                          out, ctx->cs);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->cs);
+  if (e != hipSuccess) return hip_fail(ctx, e, "sample_negatives");
+  return PBG_OK;
+}

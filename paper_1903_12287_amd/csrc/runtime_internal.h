@@ -1,0 +1,77 @@
+// Internal state of a context (host side).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "pbg.h"
+
+struct Partition {
+  float* emb = nullptr;  // [rows x dim]
+  float* G = nullptr;    // [rows]
+  int where = -1;        // PBG_MEM_DEVICE / PBG_MEM_PINNED_HOST
+};
+
+// device allocations owned by the library, released together
+struct Arena {
+  std::vector<void*> ptrs;
+  bool failed = false;
+  void* get(size_t bytes);
+  void release();
+};
+
+// an HBM slot holding one partition during pbg_train_epoch
+struct Slot {
+  float* emb = nullptr;
+  float* G = nullptr;
+  int part = -1;
+  hipEvent_t ready = nullptr;     // load finished (copy stream)
+  hipEvent_t released = nullptr;  // last use finished (compute stream)
+  int64_t last_use = -1;
+};
+
+struct pbg_ctx {
+  int64_t n = 0;
+  int P = 1, R = 1, d = 1, op = 0, cmp = 0, loss = 0;
+  float margin = 0.f;
+  uint32_t flags = 0;
+  int64_t ps = 0;
+  int dr = 0;
+  int device = 0;
+  bool invalid = false;
+  hipStream_t cs = nullptr;  // compute stream
+  hipStream_t xs = nullptr;  // copy stream
+  std::vector<Partition> parts;
+  float* relp = nullptr;
+  float* relG = nullptr;
+  std::string err;
+
+  // training workspace
+  Arena ws;
+  bool ws_ready = false;
+  int wC = 0, wU = 0, wS = 0;
+  StepBufs bufs{};
+  SortWork sw{};
+  float* relpartial = nullptr;
+  float* relT = nullptr;
+  uint32_t* flag_dev = nullptr;
+  double* steploss_dev = nullptr;
+  int64_t steploss_cap = 0;
+
+  std::vector<double> step_losses;
+  pbg_stats stats{};
+  std::vector<Slot> slots;
+};
+
+pbg_status set_err(pbg_ctx* ctx, pbg_status st, const char* fmt, ...);
+pbg_status hip_fail(pbg_ctx* ctx, hipError_t e, const char* what);
+bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width);
+pbg_status check_neg_config(pbg_ctx* ctx, const pbg_neg_config* neg);
+pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i, float* G_i,
+                               float* emb_j, float* G_j, const int32_t* src, const int32_t* rel,
+                               const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg,
+                               float lr, uint64_t seed, double* loss_out,
+                               std::vector<double>* step_losses);

@@ -1,0 +1,147 @@
+"""Training-pass parity, determinism, split calls and error paths on the GPU.
+
+Tolerances: see test_gpu_parity.py.  A free-running pass over several steps
+is compared at 1e-4 max abs; for the ranking loss the comparison is preceded
+by a census of hinge terms within fp32 rounding of the kink, and a failure
+with such terms present is reported as a flip (the oracle's own fp64 choice
+of branch differs from the kernel's fp32 one), not hidden.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import pbg_oracle as O
+from paper_1903_12287_amd import synth
+from tests.pbg_cases import GpuModel, make_problem, oracle_model
+
+pytestmark = pytest.mark.gpu
+
+
+def test_negatives_bit_exact():
+    from paper_1903_12287_amd import pbg
+    for (n, P, i, j, U, first, nch, seed) in [(10_000, 1, 0, 0, 100, 0, 50, 20190001),
+                                              (121_216_723, 16, 3, 7, 1000, 9000, 8, 20190004),
+                                              (41_652_230, 8, 5, 2, 1000, 123456, 4, 2**63 + 12345),
+                                              (97, 2, 1, 0, 7, 3, 11, 0)]:
+        ctx = pbg.pbg_bucket_init(n, P, 1, 8, "identity", "dot", "ranking")
+        try:
+            out = torch.empty(nch * 2 * U, dtype=torch.int32, device="cuda")
+            pbg.pbg_sample_negatives(ctx, i, j, first, nch, U, seed, out)
+            got = out.cpu().numpy().reshape(nch, 2, U)
+        finally:
+            pbg.pbg_free(ctx)
+        rows_i, rows_j = O.partition_rows(n, P, i), O.partition_rows(n, P, j)
+        for c in range(nch):
+            want0 = O.uniform_negatives(seed, i * P + j, first + c, 0, U, rows_j)
+            want1 = O.uniform_negatives(seed, i * P + j, first + c, 1, U, rows_i)
+            assert np.array_equal(got[c, 0], want0)
+            assert np.array_equal(got[c, 1], want1)
+
+
+@pytest.mark.parametrize("op,cmp,loss,R,P,ij", [
+    ("identity", "dot", "ranking", 1, 1, (0, 0)),
+    ("translation", "cos", "ranking", 1, 1, (0, 0)),
+    ("complex_diagonal", "dot", "softmax", 5, 1, (0, 0)),
+    ("diagonal", "dot", "ranking", 7, 3, (1, 2)),
+    ("linear", "dot", "logistic", 1, 2, (1, 1)),
+    ("diagonal", "dot", "logistic", 4, 2, (0, 1)),
+])
+def test_multi_step_pass_matches_oracle(op, cmp, loss, R, P, ij):
+    """Several steps with a short last chunk: per-step losses and the final state."""
+    i, j = ij
+    pb = make_problem(op, cmp, loss, n=150, P=P, R=R, d=24, m=437, C=16, U=10, S=3, i=i, j=j,
+                      seed=7, sigma=0.2)
+    gm = GpuModel(pb)
+    try:
+        gl = gm.train()
+        from paper_1903_12287_amd import pbg
+        steps = pbg.pbg_get_step_losses(gm.ctx)
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol, osteps = O.train_bucket(om, i, j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr,
+                                pb.seed, return_steps=True)
+    assert len(steps) == len(osteps) == 10      # 28 chunks in steps of 3
+    for a, b in zip(steps, osteps):
+        assert abs(a - b) <= 1e-4 * max(1.0, abs(b)), (a, b)
+    for p in sorted({i, j}):
+        err = float(np.max(np.abs(st["emb"][p] - om.emb[p])))
+        assert err <= 1e-4, (p, err)
+        gerr = float(np.max(np.abs(st["G"][p] - om.G[p]) / np.maximum(1.0, om.G[p])))
+        assert gerr <= 1e-4, (p, gerr)
+    if om.rel is not None:
+        assert float(np.max(np.abs(st["rel"] - om.rel))) <= 1e-4
+
+
+def test_tiny_social_full_pass():
+    """The tiny social graph (10,000 nodes, 100,000 edges, d = 32, identity,
+    dot, ranking 0.1, C = U = 100, S = 40, lr 0.1): one full pass."""
+    w = synth.tiny_social()
+    rng = synth.rng_for(w.seed + 1)
+    emb = synth.init_embeddings(w.n, w.d, rng)
+    from tests.pbg_cases import Problem
+    pb = Problem(w.n, 1, 1, w.d, w.op, w.cmp, w.loss, w.margin, [emb], None, 0, 0,
+                 w.src, None, w.dst, w.C, w.U, w.S, w.lr, w.seed)
+    gm = GpuModel(pb)
+    try:
+        gl = gm.train()
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol = O.train_bucket(om, 0, 0, w.src, None, w.dst, w.C, w.U, w.S, w.lr, w.seed)
+    assert abs(gl - ol) <= 1e-4 * abs(ol), (gl, ol)
+    err = float(np.max(np.abs(st["emb"][0] - om.emb[0])))
+    assert err <= 1e-4, err
+
+
+def test_bitwise_deterministic_and_split_calls():
+    pb = make_problem("complex_diagonal", "dot", "softmax", n=120, R=6, d=20, m=300, C=16, U=8, S=2,
+                      seed=9)
+    states = []
+    for split in (None, None, 96):
+        gm = GpuModel(pb)
+        try:
+            if split is None:
+                gm.train()
+            else:
+                # 96 edges = 6 chunks = 3 whole steps, then the rest from chunk 6
+                gm.train(0, split, 0)
+                gm.train(split, None, split // pb.C)
+            states.append(gm.state())
+        finally:
+            gm.close()
+    for s in states[1:]:
+        assert np.array_equal(s["emb"][0], states[0]["emb"][0])
+        assert np.array_equal(s["G"][0], states[0]["G"][0])
+        assert np.array_equal(s["rel"], states[0]["rel"])
+
+
+def test_out_of_range_ids_leave_parameters_untouched():
+    from paper_1903_12287_amd import pbg
+    pb = make_problem("diagonal", "dot", "ranking", n=50, R=3, m=64, seed=4)
+    gm = GpuModel(pb)
+    try:
+        before = gm.state()
+        bad_dst = gm.dst.clone()
+        bad_dst[17] = 50
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_train_bucket(gm.ctx, 0, 0, gm.src, gm.rel_ids, bad_dst, 16, 8, 2, 0.1, 1)
+        assert ei.value.status_name == "INVALID_ARG"
+        bad_rel = gm.rel_ids.clone()
+        bad_rel[3] = -1
+        with pytest.raises(pbg.PbgError):
+            pbg.pbg_train_bucket(gm.ctx, 0, 0, gm.src, bad_rel, gm.dst, 16, 8, 2, 0.1, 1)
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_train_bucket(gm.ctx, 0, 0, gm.src, None, gm.dst, 16, 8, 2, 0.1, 1)
+        assert ei.value.status_name == "INVALID_ARG"
+        after = gm.state()
+        assert np.array_equal(before["emb"][0], after["emb"][0])
+        assert np.array_equal(before["rel"], after["rel"])
+        # an empty call is a no-op
+        empty = torch.empty(0, dtype=torch.int32, device="cuda")
+        assert pbg.pbg_train_bucket(gm.ctx, 0, 0, empty, empty, empty, 16, 8, 2, 0.1, 1) == 0.0
+    finally:
+        gm.close()
