@@ -69,7 +69,10 @@ enum {
   /* Round the inputs of the score and score-gradient contractions to bfloat16
    * (round to nearest even) and accumulate in float32; embeddings, Adagrad
    * state, losses and the loss epilogue stay float32. */
-  PBG_F_BF16_SCORE = 1u
+  PBG_F_BF16_SCORE = 1u,
+  /* Record HIP events around every kernel group of every step on the compute
+   * stream and report the summed times in pbg_stats (small overhead). */
+  PBG_F_PHASE_TIMING = 2u
 };
 
 /* Where a bound partition lives. */
@@ -100,10 +103,13 @@ typedef struct {
   int64_t chunks;
   int64_t steps;
   double total_ms;          /* wall time of the call on the compute stream */
-  double gather_ms;         /* gather + operator kernels */
-  double score_ms;          /* score contraction + loss epilogue */
-  double backward_ms;       /* score-gradient contractions + operator backward */
-  double update_ms;         /* sort + segment Adagrad (entities and relations) */
+  /* per kernel group, summed over steps (only with PBG_F_PHASE_TIMING) */
+  double gather_ms;         /* gather + operator + uniform draws */
+  double score_ms;          /* score contraction with its fused loss epilogue */
+  double epilogue_ms;       /* softmax row pass + per-edge finalisation */
+  double backward_ms;       /* the two score-gradient contractions */
+  double opbwd_ms;          /* operator / comparator backward */
+  double update_ms;         /* sort + segment sums + Adagrad (entities and relations) */
   double gather_bytes;      /* algorithmic bytes of the gathers: (2C+2U)*dim*4 per chunk */
   double score_flops;       /* algorithmic flops of the three contractions: 12*C*N*dim per chunk */
   double update_bytes;      /* algorithmic bytes of the Adagrad updates */

@@ -266,19 +266,38 @@ __global__ __launch_bounds__(256) void relation_adagrad_sorted(float* relp, floa
   }
 }
 
-// one relation: per-chunk in-order sums of the valid contribution rows
+// one relation: per-chunk sums of the valid contribution rows (edge rows,
+// then the uniform source rows for cos).  Wave w sums rows w, w+4, ... in
+// order; the four wave sums are then added in a fixed order.  dr <= 512.
 __global__ __launch_bounds__(256) void relation_chunk_sums(StepGeom g, const float* rows, int64_t ld,
                                                            int include_uniform, float* partial) {
-  const int f = blockIdx.x * 256 + threadIdx.x;
-  const int c = blockIdx.y;
-  if (f >= g.dr) return;
+  __shared__ float red[4][512];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = blockIdx.x;
   const int Cc = chunk_edges(g, c);
+  const int nrows = Cc + (include_uniform ? g.U : 0);
   const float* base = rows + (int64_t)c * g.N * ld;
-  float acc = 0.0f;
-  for (int e = 0; e < Cc; ++e) acc += base[(int64_t)e * ld + f];
-  if (include_uniform)
-    for (int k = 0; k < g.U; ++k) acc += base[(int64_t)(g.C + k) * ld + f];
-  partial[(int64_t)c * g.dr + f] = acc;
+  float acc[ROWQ];
+#pragma unroll
+  for (int q = 0; q < ROWQ; ++q) acc[q] = 0.0f;
+#pragma unroll 4
+  for (int k = w; k < nrows; k += 4) {
+    const int row = k < Cc ? k : g.C + (k - Cc);
+    const float* r = base + (int64_t)row * ld;
+#pragma unroll
+    for (int q = 0; q < ROWQ; ++q) {
+      const int f = lane + 64 * q;
+      if (f < g.dr) acc[q] += r[f];
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < ROWQ; ++q) {
+    const int f = lane + 64 * q;
+    if (f < g.dr) red[w][f] = acc[q];
+  }
+  __syncthreads();
+  for (int f = threadIdx.x; f < g.dr; f += 256)
+    partial[(int64_t)c * g.dr + f] = (red[0][f] + red[1][f]) + (red[2][f] + red[3][f]);
 }
 
 __global__ __launch_bounds__(256) void relation_single_adagrad(float* relp, float* relG, int width,
@@ -371,8 +390,7 @@ void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, int n, 
 
 void launch_relation_chunk_sums(const StepGeom& g, const float* rows, int64_t ld, int include_uniform,
                                 float* partial, hipStream_t s) {
-  dim3 grid((g.dr + 255) / 256, g.nchunks);
-  relation_chunk_sums<<<grid, 256, 0, s>>>(g, rows, ld, include_uniform, partial);
+  relation_chunk_sums<<<g.nchunks, 256, 0, s>>>(g, rows, ld, include_uniform, partial);
 }
 
 void launch_relation_single_adagrad(float* relp, float* relG, int width, const float* partial,

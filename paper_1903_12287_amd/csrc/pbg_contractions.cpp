@@ -1,0 +1,190 @@
+// Launch sequences of the three chunk contractions of a step (score with its
+// loss epilogue, dQ = dS.N, dN = dS^T.Q), in float32 or with bfloat16 inputs.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+
+#include "kernels.h"
+#include "runtime_internal.h"
+
+static int rup(int v, int m) { return (v + m - 1) / m * m; }
+
+void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
+                          const std::function<void(int)>& mark) {
+  const int C = g.C, U = g.U, N = g.N, dp = g.dp, Np = g.Np, nch = g.nchunks;
+  GemmArgs fa;
+  memset(&fa, 0, sizeof(fa));
+  fa.A = b.qk;
+  fa.B = b.nn;
+  fa.Cm = b.ds;
+  fa.a_cs = 2ll * C * dp;
+  fa.a_ss = (int64_t)C * dp;
+  fa.b_cs = 2ll * N * dp;
+  fa.b_ss = (int64_t)N * dp;
+  fa.c_cs = 2ll * C * Np;
+  fa.c_ss = (int64_t)C * Np;
+  fa.lda = dp;
+  fa.ldb = dp;
+  fa.ldc = Np;
+  fa.mdim = DIM_CC;
+  fa.ndim = DIM_NC;
+  fa.kdim = DIM_FIXED;
+  fa.Kfix = dp;
+  fa.C = C;
+  fa.U = U;
+  fa.m_step = g.m_step;
+  fa.nsides = 2;
+  fa.pos = b.pos;
+  fa.bias = (g.op == OP_TRANSLATION && g.cmp == CMP_DOT) ? b.bias : nullptr;
+  fa.rowpart = b.rowpart;
+  fa.nct = g.nct;
+  fa.loss = g.loss;
+  fa.margin = g.margin;
+  const int epi = g.loss == LOSS_SOFTMAX ? EPI_SOFTMAX_STATS : EPI_LOSS;
+  launch_gemm_f32(fa, GEMM_NT, epi, 8, g.nct, (C + 127) / 128, nch * 2, cs);
+  mark(2);
+  if (g.loss == LOSS_SOFTMAX) launch_softmax_rows(g, b, cs);
+  launch_finalize(g, b, ctx->steploss_dev + t, cs);
+  mark(3);
+
+  // dQ = dS . N (per side)
+  const int nb = gemm_pick_nb(dp);
+  const int gn = (dp + 16 * nb - 1) / (16 * nb);
+  GemmArgs qa;
+  memset(&qa, 0, sizeof(qa));
+  qa.A = b.ds;
+  qa.B = b.nn;
+  qa.Cm = b.dq;
+  qa.a_cs = 2ll * C * Np;
+  qa.a_ss = (int64_t)C * Np;
+  qa.b_cs = 2ll * N * dp;
+  qa.b_ss = (int64_t)N * dp;
+  qa.c_cs = 2ll * C * dp;
+  qa.c_ss = (int64_t)C * dp;
+  qa.lda = Np;
+  qa.ldb = dp;
+  qa.ldc = dp;
+  qa.mdim = DIM_CC;
+  qa.ndim = DIM_FIXED;
+  qa.Nfix = dp;
+  qa.kdim = DIM_NC;
+  qa.C = C;
+  qa.U = U;
+  qa.m_step = g.m_step;
+  qa.nsides = 2;
+  launch_gemm_f32(qa, GEMM_NN, EPI_STORE, nb, gn, (C + 127) / 128, nch * 2, cs);
+  // dN = dS^T . Q (per side)
+  GemmArgs na = qa;
+  na.B = b.qk;
+  na.Cm = b.dn;
+  na.b_cs = 2ll * C * dp;
+  na.b_ss = (int64_t)C * dp;
+  na.c_cs = 2ll * N * dp;
+  na.c_ss = (int64_t)N * dp;
+  na.mdim = DIM_NC;
+  na.kdim = DIM_CC;
+  launch_gemm_f32(na, GEMM_TN, EPI_STORE, nb, gn, (N + 127) / 128, nch * 2, cs);
+}
+
+void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t,
+                           hipStream_t cs, const std::function<void(int)>& mark) {
+  const int C = g.C, U = g.U, N = g.N, d = g.d, dp = g.dp, Np = g.Np, nch = g.nchunks;
+  const int dpb = rup(d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
+  const BufsH& h = ctx->h;
+  // bf16 operands: rows [e][f], [t][f] and the transposed copies [f][e], [f][t]
+  launch_to_bf16_transpose(b.qk, (int64_t)C * dp, C, dp, d, h.qk, (int64_t)C * dpb, dpb, h.qkT,
+                           (int64_t)dpb * Cpb, Cpb, Cpb, dpb, nch * 2, cs);
+  launch_to_bf16_transpose(b.nn, (int64_t)N * dp, N, dp, d, h.nn, (int64_t)N * dpb, dpb, h.nnT,
+                           (int64_t)dpb * Npb, Npb, Npb, dpb, nch * 2, cs);
+
+  GemmArgsH fa;
+  memset(&fa, 0, sizeof(fa));
+  fa.A = h.qk;
+  fa.B = h.nn;
+  fa.a_cs = 2ll * C * dpb;
+  fa.a_ss = (int64_t)C * dpb;
+  fa.b_cs = 2ll * N * dpb;
+  fa.b_ss = (int64_t)N * dpb;
+  fa.lda = dpb;
+  fa.ldb = dpb;
+  fa.mdim = DIM_CC;
+  fa.ndim = DIM_NC;
+  fa.kdim = DIM_FIXED;
+  fa.Kfix = d;
+  fa.C = C;
+  fa.U = U;
+  fa.m_step = g.m_step;
+  fa.nsides = 2;
+  fa.pos = b.pos;
+  fa.bias = (g.op == OP_TRANSLATION && g.cmp == CMP_DOT) ? b.bias : nullptr;
+  fa.rowpart = b.rowpart;
+  fa.nct = g.nct;
+  fa.loss = g.loss;
+  fa.margin = g.margin;
+  if (g.loss == LOSS_SOFTMAX) {
+    fa.Cm = b.ds;
+    fa.c_cs = 2ll * C * Np;
+    fa.c_ss = (int64_t)C * Np;
+    fa.ldc = Np;
+    launch_gemm_bf16(fa, EPI_SOFTMAX_STATS, 8, g.nct, (C + 127) / 128, nch * 2, cs);
+    mark(2);
+    launch_softmax_rows_bf16(g, b, h.ds, h.dsT, Npb, Cpb, cs);
+    launch_zero_dsT_tail(g, h.dsT, Cpb, cs);
+  } else {
+    fa.dsh = h.ds;
+    fa.c_cs = 2ll * C * Npb;
+    fa.c_ss = (int64_t)C * Npb;
+    fa.ldc = Npb;
+    fa.dsT = h.dsT;
+    fa.t_cs = 2ll * N * Cpb;
+    fa.t_ss = (int64_t)N * Cpb;
+    fa.ldt = Cpb;
+    launch_gemm_bf16(fa, EPI_LOSS, 8, g.nct, (C + 127) / 128, nch * 2, cs);
+    mark(2);
+  }
+  launch_finalize(g, b, ctx->steploss_dev + t, cs);
+  mark(3);
+
+  const int nb = gemm_pick_nb(dp);
+  const int gn = (dp + 16 * nb - 1) / (16 * nb);
+  // dQ = dS . N:  A = dS [e][t], B = N^T [f][t]
+  GemmArgsH qa;
+  memset(&qa, 0, sizeof(qa));
+  qa.A = h.ds;
+  qa.B = h.nnT;
+  qa.Cm = b.dq;
+  qa.a_cs = 2ll * C * Npb;
+  qa.a_ss = (int64_t)C * Npb;
+  qa.b_cs = 2ll * dpb * Npb;
+  qa.b_ss = (int64_t)dpb * Npb;
+  qa.c_cs = 2ll * C * dp;
+  qa.c_ss = (int64_t)C * dp;
+  qa.lda = Npb;
+  qa.ldb = Npb;
+  qa.ldc = dp;
+  qa.mdim = DIM_CC;
+  qa.ndim = DIM_FIXED;
+  qa.Nfix = dp;
+  qa.kdim = DIM_NC;
+  qa.C = C;
+  qa.U = U;
+  qa.m_step = g.m_step;
+  qa.nsides = 2;
+  launch_gemm_bf16(qa, EPI_STORE, nb, gn, (C + 127) / 128, nch * 2, cs);
+  // dN = dS^T . Q:  A = dS^T [t][e], B = Q^T [f][e]
+  GemmArgsH na = qa;
+  na.A = h.dsT;
+  na.B = h.qkT;
+  na.Cm = b.dn;
+  na.a_cs = 2ll * N * Cpb;
+  na.a_ss = (int64_t)N * Cpb;
+  na.b_cs = 2ll * dpb * Cpb;
+  na.b_ss = (int64_t)dpb * Cpb;
+  na.c_cs = 2ll * N * dp;
+  na.c_ss = (int64_t)N * dp;
+  na.lda = Cpb;
+  na.ldb = Cpb;
+  na.mdim = DIM_NC;
+  na.kdim = DIM_CC;
+  launch_gemm_bf16(na, EPI_STORE, nb, gn, (N + 127) / 128, nch * 2, cs);
+}

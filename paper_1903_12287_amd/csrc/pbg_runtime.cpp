@@ -131,15 +131,46 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   }
   if (linear) ctx->relT = (float*)a.get((int64_t)ctx->R * d * d * 4);
   ctx->flag_dev = (uint32_t*)a.get(16);
+  ctx->h = BufsH();
+  if (ctx->flags & PBG_F_BF16_SCORE) {
+    const int dpb = round_up(d, 32), Cpb = round_up(C, 32), Npb = round_up(N, 32);
+    ctx->h.qk = (uint16_t*)a.get(s * 2 * C * dpb * 2);
+    ctx->h.nn = (uint16_t*)a.get(s * 2 * N * dpb * 2);
+    ctx->h.qkT = (uint16_t*)a.get(s * 2 * dpb * Cpb * 2);
+    ctx->h.nnT = (uint16_t*)a.get(s * 2 * dpb * Npb * 2);
+    ctx->h.ds = (uint16_t*)a.get(s * 2 * C * (int64_t)Npb * 2);
+    ctx->h.dsT = (uint16_t*)a.get(s * 2 * N * (int64_t)Cpb * 2);
+  }
   if (a.failed) {
     ctx->ws.release();
     return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "workspace allocation failed (C=%d U=%d S=%d)", C, U, S);
+  }
+  // rows of a short last chunk beyond its edges are never scored, but the
+  // bf16 transposes copy them: start from zeros so they always hold finite values
+  hipError_t ez = hipMemsetAsync(b.qk, 0, (size_t)s * 2 * C * dp * 4, ctx->cs);
+  if (ez == hipSuccess) ez = hipMemsetAsync(b.nn, 0, (size_t)s * 2 * N * dp * 4, ctx->cs);
+  if (ez == hipSuccess) ez = hipStreamSynchronize(ctx->cs);
+  if (ez != hipSuccess) {
+    ctx->ws.release();
+    return hip_fail(ctx, ez, "workspace initialisation");
   }
   ctx->wC = C;
   ctx->wU = U;
   ctx->wS = S;
   ctx->ws_ready = true;
   return PBG_OK;
+}
+
+static bool ensure_events(pbg_ctx* ctx, size_t n) {
+  while (ctx->events.size() < n) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) {
+      (void)hipGetLastError();
+      return false;
+    }
+    ctx->events.push_back(e);
+  }
+  return true;
 }
 
 static pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps) {
@@ -183,7 +214,7 @@ pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_part
   if (loss < PBG_LOSS_RANKING || loss > PBG_LOSS_SOFTMAX) return fail(PBG_ERR_INVALID_ARG, "unknown loss");
   if (op == PBG_OP_COMPLEX_DIAGONAL && (dim % 2)) return fail(PBG_ERR_INVALID_ARG, "complex_diagonal needs an even dim");
   if (!std::isfinite(margin)) return fail(PBG_ERR_INVALID_ARG, "margin must be finite");
-  if (flags & ~(uint32_t)PBG_F_BF16_SCORE) return fail(PBG_ERR_INVALID_ARG, "unknown flags");
+  if (flags & ~(uint32_t)(PBG_F_BF16_SCORE | PBG_F_PHASE_TIMING)) return fail(PBG_ERR_INVALID_ARG, "unknown flags");
   const int64_t ps = (num_entities + num_partitions - 1) / num_partitions;
   if ((int64_t)(num_partitions - 1) * ps >= num_entities)
     return fail(PBG_ERR_INVALID_ARG, "a partition would be empty (num_partitions too large for num_entities)");
@@ -192,7 +223,6 @@ pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_part
     return fail(PBG_ERR_UNSUPPORTED, "cos with a non-identity operator needs a single relation");
   if (op == PBG_OP_LINEAR && (num_relations > 1 || cmp == PBG_CMP_COS))
     return fail(PBG_ERR_UNSUPPORTED, "the linear operator is implemented for one relation with dot");
-  if (flags & PBG_F_BF16_SCORE) return fail(PBG_ERR_UNSUPPORTED, "the bf16 score path is not built yet");
   ctx->n = num_entities;
   ctx->P = num_partitions;
   ctx->R = num_relations;
@@ -220,6 +250,7 @@ void pbg_free(pbg_ctx* ctx) {
   if (ctx->steploss_dev) (void)hipFree(ctx->steploss_dev);
   for (auto& s : ctx->slots)
     if (s.emb) (void)hipFree(s.emb);
+  for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
   delete ctx;
 }
 
@@ -368,6 +399,12 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   (void)hipEventCreate(&ev0);
   (void)hipEventCreate(&ev1);
+  const bool timing = (ctx->flags & PBG_F_PHASE_TIMING) != 0;
+  if (timing && !ensure_events(ctx, (size_t)nsteps * kPhaseEvents))
+    return set_err(ctx, PBG_ERR_DEVICE, "hipEventCreate failed");
+  auto mark = [&](int64_t step, int k) {
+    if (timing) (void)hipEventRecord(ctx->events[(size_t)step * kPhaseEvents + k], cs);
+  };
   (void)hipEventRecord(ev0, cs);
 
   for (int64_t t = 0; t < nsteps; ++t) {
@@ -381,88 +418,20 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     b.dst = dst + c0 * C;
     b.rel = rel ? rel + c0 * C : nullptr;
 
+    mark(t, 0);
     if (linear) launch_transpose_rel(ctx->relp, ctx->relT, ctx->R, d, cs);
     launch_gather(g, b, ctx->relT, cs);
+    mark(t, 1);
 
-    // score contraction + loss epilogue
-    GemmArgs fa;
-    memset(&fa, 0, sizeof(fa));
-    fa.A = b.qk;
-    fa.B = b.nn;
-    fa.Cm = b.ds;
-    fa.a_cs = 2ll * C * dp;
-    fa.a_ss = (int64_t)C * dp;
-    fa.b_cs = 2ll * N * dp;
-    fa.b_ss = (int64_t)N * dp;
-    fa.c_cs = 2ll * C * Np;
-    fa.c_ss = (int64_t)C * Np;
-    fa.lda = dp;
-    fa.ldb = dp;
-    fa.ldc = Np;
-    fa.mdim = DIM_CC;
-    fa.ndim = DIM_NC;
-    fa.kdim = DIM_FIXED;
-    fa.Kfix = dp;
-    fa.C = C;
-    fa.U = U;
-    fa.m_step = m_step;
-    fa.nsides = 2;
-    fa.pos = b.pos;
-    fa.bias = (ctx->op == OP_TRANSLATION && ctx->cmp == CMP_DOT) ? b.bias : nullptr;
-    fa.rowpart = b.rowpart;
-    fa.nct = g.nct;
-    fa.loss = ctx->loss;
-    fa.margin = ctx->margin;
-    const int epi = ctx->loss == LOSS_SOFTMAX ? EPI_SOFTMAX_STATS : EPI_LOSS;
-    launch_gemm_f32(fa, GEMM_NT, epi, 8, g.nct, (C + 127) / 128, nch * 2, cs);
-    if (ctx->loss == LOSS_SOFTMAX) launch_softmax_rows(g, b, cs);
-    launch_finalize(g, b, ctx->steploss_dev + t, cs);
+    if (ctx->flags & PBG_F_BF16_SCORE) {
+      run_contractions_bf16(ctx, g, b, t, cs, [&](int k) { mark(t, k); });
+    } else {
+      run_contractions_f32(ctx, g, b, t, cs, [&](int k) { mark(t, k); });
+    }
 
-    // dQ = dS . N (per side)
-    const int nb = gemm_pick_nb(dp);
-    const int gn = (dp + 16 * nb - 1) / (16 * nb);
-    GemmArgs qa;
-    memset(&qa, 0, sizeof(qa));
-    qa.A = b.ds;
-    qa.B = b.nn;
-    qa.Cm = b.dq;
-    qa.a_cs = 2ll * C * Np;
-    qa.a_ss = (int64_t)C * Np;
-    qa.b_cs = 2ll * N * dp;
-    qa.b_ss = (int64_t)N * dp;
-    qa.c_cs = 2ll * C * dp;
-    qa.c_ss = (int64_t)C * dp;
-    qa.lda = Np;
-    qa.ldb = dp;
-    qa.ldc = dp;
-    qa.mdim = DIM_CC;
-    qa.ndim = DIM_FIXED;
-    qa.Nfix = dp;
-    qa.kdim = DIM_NC;
-    qa.C = C;
-    qa.U = U;
-    qa.m_step = m_step;
-    qa.nsides = 2;
-    launch_gemm_f32(qa, GEMM_NN, EPI_STORE, nb, gn, (C + 127) / 128, nch * 2, cs);
-    // dN = dS^T . Q (per side)
-    GemmArgs na = qa;
-    na.A = b.ds;
-    na.B = b.qk;
-    na.Cm = b.dn;
-    na.a_cs = 2ll * C * Np;
-    na.a_ss = (int64_t)C * Np;
-    na.b_cs = 2ll * C * dp;
-    na.b_ss = (int64_t)C * dp;
-    na.c_cs = 2ll * N * dp;
-    na.c_ss = (int64_t)N * dp;
-    na.lda = Np;
-    na.ldb = dp;
-    na.ldc = dp;
-    na.mdim = DIM_NC;
-    na.kdim = DIM_CC;
-    launch_gemm_f32(na, GEMM_TN, EPI_STORE, nb, gn, (N + 127) / 128, nch * 2, cs);
-
+    mark(t, 4);
     launch_op_backward(g, b, ctx->relT, cs);
+    mark(t, 5);
 
     // entities: sort contribution rows by (table, row), segment sums, Adagrad
     const int nkeys = 2 * (nch * U + m_step);
@@ -512,6 +481,7 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
         launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch, lr, cs);
       }
     }
+    mark(t, 6);
   }
   (void)hipEventRecord(ev1, cs);
   hipError_t e = hipGetLastError();
@@ -533,6 +503,17 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   if (loss_out) *loss_out = total;
   if (step_losses) step_losses->insert(step_losses->end(), losses.begin(), losses.end());
   ctx->stats.total_ms += ms;
+  if (timing) {
+    double* acc[6] = {&ctx->stats.gather_ms, &ctx->stats.score_ms, &ctx->stats.epilogue_ms,
+                      &ctx->stats.backward_ms, &ctx->stats.opbwd_ms, &ctx->stats.update_ms};
+    for (int64_t t = 0; t < nsteps; ++t)
+      for (int k = 0; k < 6; ++k) {
+        float pm = 0.f;
+        (void)hipEventElapsedTime(&pm, ctx->events[(size_t)t * kPhaseEvents + k],
+                                  ctx->events[(size_t)t * kPhaseEvents + k + 1]);
+        *acc[k] += pm;
+      }
+  }
   ctx->stats.edges += n_edges;
   ctx->stats.chunks += nchunks;
   ctx->stats.steps += nsteps;

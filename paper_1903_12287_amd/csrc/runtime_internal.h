@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -33,6 +34,16 @@ struct Slot {
   int64_t last_use = -1;
 };
 
+// bf16 operand copies of a step (PBG_F_BF16_SCORE)
+struct BufsH {
+  uint16_t* qk = nullptr;   // [S][2][C][dpb]
+  uint16_t* nn = nullptr;   // [S][2][N][dpb]
+  uint16_t* qkT = nullptr;  // [S][2][dpb][Cpb]
+  uint16_t* nnT = nullptr;  // [S][2][dpb][Npb]
+  uint16_t* ds = nullptr;   // [S][2][C][Npb]
+  uint16_t* dsT = nullptr;  // [S][2][N][Cpb]
+};
+
 struct pbg_ctx {
   int64_t n = 0;
   int P = 1, R = 1, d = 1, op = 0, cmp = 0, loss = 0;
@@ -54,6 +65,7 @@ struct pbg_ctx {
   bool ws_ready = false;
   int wC = 0, wU = 0, wS = 0;
   StepBufs bufs{};
+  BufsH h{};
   SortWork sw{};
   float* relpartial = nullptr;
   float* relT = nullptr;
@@ -64,9 +76,16 @@ struct pbg_ctx {
   std::vector<double> step_losses;
   pbg_stats stats{};
   std::vector<Slot> slots;
+  std::vector<hipEvent_t> events;  // phase-timing events, kPhaseEvents per step
 };
 
+constexpr int kPhaseEvents = 7;
+
 pbg_status set_err(pbg_ctx* ctx, pbg_status st, const char* fmt, ...);
+void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
+                          const std::function<void(int)>& mark);
+void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t,
+                           hipStream_t cs, const std::function<void(int)>& mark);
 pbg_status hip_fail(pbg_ctx* ctx, hipError_t e, const char* what);
 bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width);
 pbg_status check_neg_config(pbg_ctx* ctx, const pbg_neg_config* neg);

@@ -23,6 +23,7 @@ OPERATORS = {"identity": 0, "translation": 1, "diagonal": 2, "linear": 3, "compl
 COMPARATORS = {"dot": 0, "cos": 1}
 LOSSES = {"ranking": 0, "logistic": 1, "softmax": 2}
 F_BF16_SCORE = 1
+F_PHASE_TIMING = 2
 MEM_DEVICE = 0
 MEM_PINNED_HOST = 1
 
@@ -54,7 +55,8 @@ class NegConfig(ctypes.Structure):
 class Stats(ctypes.Structure):
     _fields_ = [("edges", ctypes.c_int64), ("chunks", ctypes.c_int64), ("steps", ctypes.c_int64),
                 ("total_ms", ctypes.c_double), ("gather_ms", ctypes.c_double),
-                ("score_ms", ctypes.c_double), ("backward_ms", ctypes.c_double),
+                ("score_ms", ctypes.c_double), ("epilogue_ms", ctypes.c_double),
+                ("backward_ms", ctypes.c_double), ("opbwd_ms", ctypes.c_double),
                 ("update_ms", ctypes.c_double), ("gather_bytes", ctypes.c_double),
                 ("score_flops", ctypes.c_double), ("update_bytes", ctypes.c_double),
                 ("copy_ms", ctypes.c_double), ("partition_loads", ctypes.c_int64)]

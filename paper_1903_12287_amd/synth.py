@@ -227,3 +227,63 @@ def follower_graph(n=41_652_230, E=1_468_365_182, P=8, d=100, C=1000, U=1000, S=
 def partition_embeddings(rows, d: int, rng, sigma: float = 1e-3):
     """Initial N(0, sigma) embeddings for partitions of the given row counts."""
     return [init_embeddings(int(r), d, rng, sigma) for r in rows]
+
+
+# ---------------------------------------------------------------------------
+# On-device generation for the large workloads (same recipes, drawn with a
+# seeded torch generator on the GPU: seconds instead of minutes on the host).
+# ---------------------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def device_generator(seed: int, device="cuda"):
+    torch = _torch()
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    return g
+
+
+def zipf_device(n: int, s: float, size: int, gen, device="cuda", block: int = 1 << 26):
+    """Bounded Zipf(s) over n ranks mapped through a seeded permutation."""
+    torch = _torch()
+    w = torch.arange(1, n + 1, dtype=torch.float64, device=device).pow_(-float(s))
+    cdf = torch.cumsum(w, 0)
+    cdf /= cdf[-1].clone()
+    perm = torch.randperm(n, generator=gen, device=device)
+    out = torch.empty(size, dtype=torch.int64, device=device)
+    for lo in range(0, size, block):
+        hi = min(size, lo + block)
+        u = torch.rand(hi - lo, generator=gen, device=device, dtype=torch.float64)
+        r = torch.searchsorted(cdf, u, right=True).clamp_(max=n - 1)
+        out[lo:hi] = perm[r]
+    return out, (cdf, perm)
+
+
+def zipf_edges_device(n: int, E: int, s_src: float, s_dst: float, gen, device="cuda"):
+    torch = _torch()
+    src, _ = zipf_device(n, s_src, E, gen, device)
+    dst, (cdf_d, perm_d) = zipf_device(n, s_dst, E, gen, device)
+    while True:
+        bad = torch.nonzero(src == dst).flatten()
+        if bad.numel() == 0:
+            break
+        u = torch.rand(bad.numel(), generator=gen, device=device, dtype=torch.float64)
+        dst[bad] = perm_d[torch.searchsorted(cdf_d, u, right=True).clamp_(max=n - 1)]
+    return src, dst
+
+
+def init_embeddings_device(rows: int, d: int, gen, sigma: float = 1e-3, device="cuda"):
+    torch = _torch()
+    return torch.randn((rows, d), generator=gen, device=device, dtype=torch.float32).mul_(sigma)
+
+
+def social_network_device(n=4_847_571, E=68_993_773, d=128, seed=20190002, device="cuda"):
+    """The social-network-shaped workload (see social_network) drawn on the
+    device: (src, dst) int32 device tensors and the initial embedding table."""
+    torch = _torch()
+    gen = device_generator(seed, device)
+    src, dst = zipf_edges_device(n, E, 1.05, 1.05, gen, device)
+    emb = init_embeddings_device(n, d, gen, 1e-3, device)
+    return src.to(torch.int32), dst.to(torch.int32), emb

@@ -88,3 +88,67 @@ def test_score_edges_matches_oracle(op, cmp, loss):
     scale = np.array([max(1.0, float(np.sum(np.abs(pb.parts[0][s] * pb.parts[0][t]))))
                       for s, t in zip(pb.src, pb.dst)])
     assert np.all(np.abs(got - want) <= 1e-5 * scale)
+
+
+BF16_COMBOS = [
+    ("translation", "cos", "ranking"),
+    ("identity", "dot", "logistic"),
+    ("complex_diagonal", "dot", "softmax"),
+    ("diagonal", "dot", "ranking"),
+    ("linear", "dot", "logistic"),
+    ("translation", "dot", "softmax"),
+]
+
+
+def _check_bf16_step(before, st, om, gl, ol):
+    """bf16 bar (2e-2): the loss; the gradient magnitudes, read from the
+    Adagrad accumulators (one step from G = 0 leaves G = |g|^2 per entity row
+    and g^2 per relation element), within 2e-2 of the largest; and the entity
+    update within 2e-2 in Frobenius norm.  Single elements of the update are
+    not compared: Adagrad's first step is lr * g / |g|, so a gradient element
+    near zero may change sign under bf16 rounding (and a ranking hinge within
+    rounding of its kink may switch), which the norms above bound."""
+    assert abs(gl - ol) <= 2e-2 * abs(ol), (gl, ol)
+    g_gpu, g_orc = np.sqrt(st["G"][0]), np.sqrt(om.G[0])
+    assert float(np.max(np.abs(g_gpu - g_orc))) <= 2e-2 * float(np.max(g_orc))
+    d_gpu = st["emb"][0] - before["emb"][0]
+    d_orc = om.emb[0] - before["emb"][0]
+    assert np.all(np.isfinite(d_gpu))
+    assert np.linalg.norm(d_gpu - d_orc) <= 2e-2 * np.linalg.norm(d_orc)
+    if om.rel is not None:
+        r_gpu, r_orc = np.sqrt(st["relG"]), np.sqrt(om.relG)
+        assert float(np.max(np.abs(r_gpu - r_orc))) <= 2e-2 * float(np.max(r_orc))
+
+
+@pytest.mark.parametrize("op,cmp,loss", BF16_COMBOS)
+def test_bf16_score_path_one_step(op, cmp, loss):
+    """bf16 inputs to the three contractions, fp32 accumulation, one step."""
+    from paper_1903_12287_amd import pbg
+    pb = make_problem(op, cmp, loss, R=_R_for(op, cmp), m=150, C=40, U=24, S=8, seed=13, d=48)
+    gm = GpuModel(pb, flags=pbg.F_BF16_SCORE)
+    try:
+        before = gm.state()
+        gl = gm.train()
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol = O.train_bucket(om, pb.i, pb.j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr, pb.seed)
+    _check_bf16_step(before, st, om, gl, ol)
+
+
+def test_bf16_short_chunks_and_ragged_dims():
+    """Chunk and candidate counts that are not multiples of the 32-wide bf16
+    k-steps, a dim that is not a multiple of 32, and a short last chunk."""
+    from paper_1903_12287_amd import pbg
+    pb = make_problem("diagonal", "dot", "logistic", R=2, m=77, C=19, U=13, S=5, seed=17, d=37)
+    gm = GpuModel(pb, flags=pbg.F_BF16_SCORE)
+    try:
+        before = gm.state()
+        gl = gm.train()
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol = O.train_bucket(om, 0, 0, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr, pb.seed)
+    _check_bf16_step(before, st, om, gl, ol)
