@@ -101,6 +101,8 @@ void launch_entity_update(const StepGeom& g, const StepBufs& b, int n, SortWork&
 // relations with several ids (sorted by relation) or one relation (fixed-order sum)
 void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, int n, SortWork& w,
                                    float lr, hipStream_t s);
+// pieces per chunk of the single-relation gradient sum (partial rows per chunk)
+#define RELSUM_PIECES 32
 void launch_relation_chunk_sums(const StepGeom& g, const float* rows, int64_t ld, int include_uniform,
                                 float* partial, hipStream_t s);
 void launch_relation_single_adagrad(float* relp, float* relG, int width, const float* partial,

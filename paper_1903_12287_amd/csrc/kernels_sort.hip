@@ -269,19 +269,28 @@ __global__ __launch_bounds__(256) void relation_adagrad_sorted(float* relp, floa
 // one relation: per-chunk sums of the valid contribution rows (edge rows,
 // then the uniform source rows for cos).  Wave w sums rows w, w+4, ... in
 // order; the four wave sums are then added in a fixed order.  dr <= 512.
+// First level of the single-relation gradient sum: block (c, piece) adds, in
+// a fixed order, the contribution rows of chunk c that fall in its piece of
+// the chunk's row list (the Cc edge rows, then the U uniform rows when they
+// carry relation gradient).  Spreading a chunk over RELSUM_PIECES blocks keeps
+// enough waves in flight to stream the rows at HBM speed.
 __global__ __launch_bounds__(256) void relation_chunk_sums(StepGeom g, const float* rows, int64_t ld,
                                                            int include_uniform, float* partial) {
   __shared__ float red[4][512];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int c = blockIdx.x;
+  const int piece = blockIdx.y;
   const int Cc = chunk_edges(g, c);
   const int nrows = Cc + (include_uniform ? g.U : 0);
+  const int per = (nrows + RELSUM_PIECES - 1) / RELSUM_PIECES;
+  const int k0 = piece * per;
+  const int k1 = min(nrows, k0 + per);
   const float* base = rows + (int64_t)c * g.N * ld;
   float acc[ROWQ];
 #pragma unroll
   for (int q = 0; q < ROWQ; ++q) acc[q] = 0.0f;
 #pragma unroll 4
-  for (int k = w; k < nrows; k += 4) {
+  for (int k = k0 + w; k < k1; k += 4) {
     const int row = k < Cc ? k : g.C + (k - Cc);
     const float* r = base + (int64_t)row * ld;
 #pragma unroll
@@ -296,20 +305,33 @@ __global__ __launch_bounds__(256) void relation_chunk_sums(StepGeom g, const flo
     if (f < g.dr) red[w][f] = acc[q];
   }
   __syncthreads();
-  for (int f = threadIdx.x; f < g.dr; f += 256)
-    partial[(int64_t)c * g.dr + f] = (red[0][f] + red[1][f]) + (red[2][f] + red[3][f]);
+  float* out = partial + ((int64_t)c * RELSUM_PIECES + piece) * g.dr;
+  for (int f = threadIdx.x; f < g.dr; f += 256) out[f] = (red[0][f] + red[1][f]) + (red[2][f] + red[3][f]);
 }
 
+// Second level and element-wise Adagrad: 64 elements per block; wave w adds a
+// contiguous quarter of the partial rows in order, then the four quarter sums
+// are combined in a fixed order.
 __global__ __launch_bounds__(256) void relation_single_adagrad(float* relp, float* relG, int width,
                                                                const float* partial, int nparts,
                                                                float lr) {
-  const int f = blockIdx.x * 256 + threadIdx.x;
-  if (f >= width) return;
+  __shared__ float red[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int f = blockIdx.x * 64 + lane;
+  const int per = (nparts + 3) / 4;
+  const int p0 = w * per, p1 = min(nparts, p0 + per);
   float gsum = 0.0f;
-  for (int c = 0; c < nparts; ++c) gsum += partial[(int64_t)c * width + f];
-  const float Gn = relG[f] + gsum * gsum;
+  if (f < width) {
+#pragma unroll 8
+    for (int c = p0; c < p1; ++c) gsum += partial[(int64_t)c * width + f];
+  }
+  red[w][lane] = gsum;
+  __syncthreads();
+  if (w != 0 || f >= width) return;
+  const float gt = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+  const float Gn = relG[f] + gt * gt;
   relG[f] = Gn;
-  relp[f] -= lr * gsum / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
+  relp[f] -= lr * gt / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
 }
 
 int grid_for(int64_t n, int per_block, int cap) {
@@ -390,10 +412,10 @@ void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, int n, 
 
 void launch_relation_chunk_sums(const StepGeom& g, const float* rows, int64_t ld, int include_uniform,
                                 float* partial, hipStream_t s) {
-  relation_chunk_sums<<<g.nchunks, 256, 0, s>>>(g, rows, ld, include_uniform, partial);
+  relation_chunk_sums<<<dim3(g.nchunks, RELSUM_PIECES), 256, 0, s>>>(g, rows, ld, include_uniform, partial);
 }
 
 void launch_relation_single_adagrad(float* relp, float* relG, int width, const float* partial,
                                     int nparts, float lr, hipStream_t s) {
-  relation_single_adagrad<<<(width + 255) / 256, 256, 0, s>>>(relp, relG, width, partial, nparts, lr);
+  relation_single_adagrad<<<(width + 63) / 64, 256, 0, s>>>(relp, relG, width, partial, nparts, lr);
 }

@@ -126,7 +126,7 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
     return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "workspace allocation failed (C=%d U=%d S=%d)", C, U, S);
   }
   if (has_rel) {
-    const int64_t w = linear ? 2 * s * (int64_t)d * d : s * (int64_t)ctx->dr;
+    const int64_t w = linear ? 2 * s * (int64_t)d * d : s * RELSUM_PIECES * (int64_t)ctx->dr;
     ctx->relpartial = (float*)a.get(w * 4);
   }
   if (linear) ctx->relT = (float*)a.get((int64_t)ctx->R * d * d * 4);
@@ -478,7 +478,8 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
         launch_relation_update_sorted(g, b, m_step, ctx->sw, lr, cs);
       } else {
         launch_relation_chunk_sums(g, b.relc, ctx->dr, ctx->cmp == CMP_COS ? 1 : 0, ctx->relpartial, cs);
-        launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch, lr, cs);
+        launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch * RELSUM_PIECES,
+                                       lr, cs);
       }
     }
     mark(t, 6);

@@ -12,6 +12,7 @@ HEADER = os.path.join(ROOT, "include", "pbg.h")
 
 def _declared():
     text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)   # declarations only, not comments
     return sorted(set(re.findall(r"\b(pbg_[a-z0-9_]+)\s*\(", text)))
 
 
