@@ -266,9 +266,6 @@ __global__ __launch_bounds__(256) void relation_adagrad_sorted(float* relp, floa
   }
 }
 
-// one relation: per-chunk sums of the valid contribution rows (edge rows,
-// then the uniform source rows for cos).  Wave w sums rows w, w+4, ... in
-// order; the four wave sums are then added in a fixed order.  dr <= 512.
 // First level of the single-relation gradient sum: block (c, piece) adds, in
 // a fixed order, the contribution rows of chunk c that fall in its piece of
 // the chunk's row list (the Cc edge rows, then the U uniform rows when they
