@@ -110,7 +110,15 @@ void launch_relation_single_adagrad(float* relp, float* relG, int width, const f
 void launch_exclusive_scan(const uint32_t* in, int64_t n, uint32_t* out, uint32_t* tmp,
                            uint32_t* total, hipStream_t s);
 
-// ---- checks, bucketing, scoring, ranking ------------------------------------
+// ---- bucketing (Sec. 4.1) ----------------------------------------------------
+void launch_bucket_keys(const int64_t* src, const int64_t* dst, int64_t n, int64_t ps, int P,
+                        uint32_t* keys, uint32_t* vals, hipStream_t s);
+void launch_bucket_offsets(const uint32_t* keys, int64_t n, int nb, int64_t* offsets, hipStream_t s);
+void launch_bucket_gather(const uint32_t* vals, const int64_t* src, const int32_t* rel,
+                          const int64_t* dst, int64_t n, int64_t ps, int32_t* src_local,
+                          int32_t* rel_out, int32_t* dst_local, hipStream_t s);
+
+// ---- checks, scoring, ranking --------------------------------------------------
 void launch_check_ids(const int32_t* ids, int64_t n, int32_t limit, uint32_t* flag, uint32_t bit,
                       hipStream_t s);
 void launch_check_ids64(const int64_t* ids, int64_t n, int64_t limit, uint32_t* flag, uint32_t bit,

@@ -1,0 +1,114 @@
+"""Edge bucketing on the device (pbg_bucket_edges) against the oracle.
+
+Bucketing is integer work, so the bar is bit-exact: offsets, the order of the
+edges inside each bucket (stable) and the local ids.  At the follower-graph
+size (41,652,230 nodes, 1,468,365,182 edges, 8 partitions) the oracle cannot
+hold the whole input, so the test checks properties that fix the result at
+any size: the offsets equal the running bucket counts, and sampled whole
+buckets equal the input's edges of that bucket in input order (selected with
+torch on the device, independently of the library)."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import pbg_oracle as O
+from paper_1903_12287_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(n, P, R, src, rel, dst):
+    from paper_1903_12287_amd import pbg
+    ctx = pbg.pbg_bucket_init(n, P, R, 8, "identity", "dot", "ranking")
+    try:
+        dev = torch.device("cuda")
+        m = src.numel()
+        offsets = torch.full((P * P + 1,), -7, dtype=torch.int64, device=dev)
+        sl = torch.full((m,), -7, dtype=torch.int32, device=dev)
+        rl = torch.full((m,), -7, dtype=torch.int32, device=dev)
+        dl = torch.full((m,), -7, dtype=torch.int32, device=dev)
+        pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
+        pbg.pbg_bucket_edges(ctx, src, rel, dst, offsets, sl, rl, dl)
+        torch.cuda.synchronize()
+        return offsets, sl, rl, dl
+    finally:
+        pbg.pbg_free(ctx)
+
+
+@pytest.mark.parametrize("n,P,R,m,seed", [
+    (1000, 3, 5, 20_000, 1),        # 1000 = 334 + 334 + 332: short last partition
+    (97, 1, 1, 5_000, 2),           # one bucket: the identity map
+    (50_000, 8, 3, 300_000, 3),     # the follower graph's 8 partitions at a small size
+    (10, 10, 2, 777, 4),            # one entity per partition, 100 buckets
+    (70_001, 16, 1, 9_000, 5),      # more buckets than edges in some of them (empty buckets)
+])
+def test_bucket_edges_matches_oracle(n, P, R, m, seed):
+    rng = synth.rng_for(seed)
+    src, dst = synth.zipf_edges(n, m, 1.1, 0.9, rng)
+    rel = rng.integers(0, R, m).astype(np.int32) if R > 1 else None
+    dev = torch.device("cuda")
+    out = _run(n, P, R, torch.from_numpy(src).to(dev), None if rel is None else torch.from_numpy(rel).to(dev),
+               torch.from_numpy(dst).to(dev))
+    offsets, sl, rl, dl = (t.cpu().numpy() for t in out)
+    w_off, w_src, w_rel, w_dst = O.bucket_edges(src, np.zeros(m, np.int32) if rel is None else rel, dst, n, P)
+    assert np.array_equal(offsets, w_off)
+    assert np.array_equal(sl, w_src)
+    assert np.array_equal(dl, w_dst)
+    assert np.array_equal(rl, w_rel)
+
+
+def test_bucket_edges_empty_and_out_of_range():
+    from paper_1903_12287_amd import pbg
+    dev = torch.device("cuda")
+    e64 = torch.empty(0, dtype=torch.int64, device=dev)
+    offsets, _, _, _ = _run(100, 4, 1, e64, None, e64)
+    assert np.array_equal(offsets.cpu().numpy(), np.zeros(17, np.int64))
+    src = torch.arange(0, 50, dtype=torch.int64, device=dev)
+    dst = torch.arange(50, 100, dtype=torch.int64, device=dev)
+    for bad_src, bad_dst, bad_rel in ((100, None, None), (None, -1, None), (None, None, 3)):
+        s, d = src.clone(), dst.clone()
+        r = torch.zeros(50, dtype=torch.int32, device=dev)
+        if bad_src is not None:
+            s[13] = bad_src
+        if bad_dst is not None:
+            d[40] = bad_dst
+        if bad_rel is not None:
+            r[7] = bad_rel
+        ctx = pbg.pbg_bucket_init(100, 4, 3, 8, "identity", "dot", "ranking")
+        try:
+            offsets = torch.full((17,), -7, dtype=torch.int64, device=dev)
+            sl = torch.full((50,), -7, dtype=torch.int32, device=dev)
+            with pytest.raises(pbg.PbgError) as ei:
+                pbg.pbg_bucket_edges(ctx, s, r, d, offsets, sl, None, sl.clone())
+            assert ei.value.status_name == "INVALID_ARG"
+            assert bool((offsets == -7).all()) and bool((sl == -7).all())
+        finally:
+            pbg.pbg_free(ctx)
+
+
+def test_bucket_edges_follower_graph_full_size():
+    """41,652,230 nodes, 1,468,365,182 edges (src Zipf 1.2, dst Zipf 0.9), 8 partitions."""
+    n, E, P = 41_652_230, 1_468_365_182, 8
+    dev = torch.device("cuda")
+    gen = synth.device_generator(20190005)
+    src, dst = synth.zipf_edges_device(n, E, 1.2, 0.9, gen)
+    print(f"follower graph drawn: {E} edges", flush=True)
+    offsets, sl, _, dl = _run(n, P, 1, src, None, dst)
+    ps = O.partition_size(n, P)
+    # running bucket counts, computed with torch from the global ids
+    b = (src // ps) * P + (dst // ps)
+    counts = torch.bincount(b, minlength=P * P).cpu().numpy()
+    want = np.zeros(P * P + 1, np.int64)
+    want[1:] = np.cumsum(counts)
+    assert np.array_equal(offsets.cpu().numpy(), want)
+    off = offsets.cpu().numpy()
+    for (i, j) in [(0, 0), (7, 7), (3, 5), (6, 1)]:
+        bb = i * P + j
+        idx = torch.nonzero(b == bb).flatten()       # input order
+        lo, hi = int(off[bb]), int(off[bb + 1])
+        assert hi - lo == idx.numel()
+        assert torch.equal(sl[lo:hi].to(torch.int64), src[idx] - i * ps)
+        assert torch.equal(dl[lo:hi].to(torch.int64), dst[idx] - j * ps)
+    assert int(sl.min()) >= 0 and int(dl.min()) >= 0
+    assert int(sl.max()) < ps and int(dl.max()) < ps
