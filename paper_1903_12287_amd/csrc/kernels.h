@@ -118,6 +118,22 @@ void launch_bucket_gather(const uint32_t* vals, const int64_t* src, const int32_
                           const int64_t* dst, int64_t n, int64_t ps, int32_t* src_local,
                           int32_t* rel_out, int32_t* dst_local, hipStream_t s);
 
+// ---- filtered ranks (Sec. 5.4) -------------------------------------------------
+void launch_rank_tables(const StepGeom& g, const float* emb, const float* relp, int64_t n_ent, float* T0,
+                        float* T1, hipStream_t s);
+void launch_rank_queries(const StepGeom& g, const float* emb, const float* relp, const float* relT,
+                         const int32_t* src, const int32_t* rel, const int32_t* dst, int64_t e0, int rows,
+                         int side, float* Q, float* pos, float* bias, hipStream_t s);
+void launch_rank_count(const float* S, int64_t ldS, int64_t n_ent, int64_t e0, int rows, int side,
+                       int64_t n_eval, const int32_t* src, const int32_t* rel, const int32_t* dst,
+                       const float* pos, const float* bias, const int32_t* ka, const int32_t* kb,
+                       const int32_t* kc, int64_t n_known, int32_t* ranks, hipStream_t s);
+void launch_rank_metrics(const int32_t* ranks, int64_t n, double* out, hipStream_t s);
+void launch_perm_keys(const int32_t* field, const uint32_t* perm, int64_t n, uint32_t* keys,
+                      uint32_t* vals_init, hipStream_t s);
+void launch_gather3(const uint32_t* perm, const int32_t* a, const int32_t* b, const int32_t* c, int64_t n,
+                    int32_t* oa, int32_t* ob, int32_t* oc, hipStream_t s);
+
 // ---- checks, scoring, ranking --------------------------------------------------
 void launch_check_ids(const int32_t* ids, int64_t n, int32_t limit, uint32_t* flag, uint32_t bit,
                       hipStream_t s);

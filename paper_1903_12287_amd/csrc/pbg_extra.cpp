@@ -7,10 +7,3 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t*, const int32_
   if (!ctx) return PBG_ERR_INVALID_ARG;
   return set_err(ctx, PBG_ERR_UNSUPPORTED, "pbg_train_epoch is not built yet");
 }
-
-extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t*, const int32_t*, const int32_t*,
-                                    int64_t, const int32_t*, const int32_t*, const int32_t*, int64_t,
-                                    int32_t*, double*, double*) {
-  if (!ctx) return PBG_ERR_INVALID_ARG;
-  return set_err(ctx, PBG_ERR_UNSUPPORTED, "pbg_rank_eval is not built yet");
-}

@@ -1,0 +1,152 @@
+"""Filtered ranks (pbg_rank_eval) against the oracle (needs an MI355X).
+
+Ranks are integers decided by float comparisons (f(candidate) >= f(positive)).
+The GPU scores in fp32 and the oracle in fp64, so a candidate whose score is
+within the fp32 error of the positive's may fall on either side.  The oracle
+therefore reports, with each rank, the ranks obtained when only candidates
+above f_pos + tol, or all above f_pos - tol, are counted; the GPU rank must
+lie in that range, with tol = 1e-5 x (largest L1 norm of a query) x (largest
+|table entry|), a bound on the fp32 rounding of a d-term dot product at these
+sizes.  Almost every rank has no candidate that close, so most ranks must be
+equal outright.  MRR and Hits@10 are checked against the GPU's own ranks and
+the oracle's."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import pbg_oracle as O
+from paper_1903_12287_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_ranks(n, R, d, op, cmp, emb, relp, src, rel, dst, ksrc, krel, kdst):
+    from paper_1903_12287_amd import pbg
+    dev = torch.device("cuda")
+    ctx = pbg.pbg_bucket_init(n, 1, R, d, op, cmp, "softmax")
+    try:
+        E = torch.from_numpy(emb).to(dev)
+        G = torch.zeros(n, dtype=torch.float32, device=dev)
+        pbg.pbg_bind_partition(ctx, 0, E, G)
+        if relp is not None:
+            rp = torch.from_numpy(relp).to(dev)
+            pbg.pbg_bind_relations(ctx, rp, torch.zeros_like(rp))
+        pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
+        t = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
+        ranks = torch.zeros(2 * len(src), dtype=torch.int32, device=dev)
+        mrr, hits = pbg.pbg_rank_eval(ctx, t(src), t(rel), t(dst), t(ksrc), t(krel), t(kdst), ranks)
+        return ranks.cpu().numpy().astype(np.int64), mrr, hits
+    finally:
+        pbg.pbg_free(ctx)
+
+
+def _tol(op, cmp, emb, relp):
+    if cmp == "cos":
+        return 1e-5 * emb.shape[1]
+    m = O.Model.create(emb.shape[0], 1, 1 if relp is None else relp.shape[0], emb.shape[1], op, cmp,
+                       "softmax", 0.1, [emb.astype(np.float64)], None if relp is None else relp.astype(np.float64))
+    th = None if m.rel is None else torch.tensor(m.rel)
+    x = torch.tensor(m.emb[0])
+    l1 = 0.0
+    for r in range(1 if th is None else th.shape[0]):
+        q = O.apply_operator(op, x, None if th is None else th[r])
+        l1 = max(l1, float(q.abs().sum(1).max()))
+    l1 = max(l1, float(np.abs(emb).sum(1).max()))
+    return 1e-5 * l1 * float(np.abs(emb).max()) * (1.0 if relp is None else max(1.0, float(np.abs(relp).max())))
+
+
+def _check(n, R, d, op, cmp, emb, relp, src, rel, dst, ksrc, krel, kdst, sample=None, min_exact=0.97):
+    got, mrr, hits = _gpu_ranks(n, R, d, op, cmp, emb, relp, src, rel, dst, ksrc, krel, kdst)
+    assert abs(mrr - float(np.mean(1.0 / got))) <= 1e-12
+    assert abs(hits - float(np.mean(got <= 10))) <= 1e-12
+    model = O.Model.create(n, 1, R, d, op, cmp, "softmax", 0.1, [emb.astype(np.float64)],
+                           None if relp is None else relp.astype(np.float64))
+    tol = _tol(op, cmp, emb, relp)
+    m = len(src)
+    idx = np.arange(m) if sample is None else sample
+    want, _, _, lo, hi = O.rank_eval(model, src[idx], None if rel is None else rel[idx], dst[idx],
+                                     ksrc, krel, kdst, tol=tol)
+    g = np.concatenate([got[idx], got[m + idx]])
+    assert np.all(g >= lo) and np.all(g <= hi), (np.nonzero((g < lo) | (g > hi))[0][:10], tol)
+    assert np.mean(g == want) >= min_exact
+    return got
+
+
+CASES = [
+    ("complex_diagonal", "dot", 7),
+    ("translation", "dot", 5),
+    ("diagonal", "dot", 4),
+    ("linear", "dot", 1),
+    ("identity", "dot", 1),
+    ("identity", "cos", 3),
+    ("translation", "cos", 1),
+    ("complex_diagonal", "cos", 1),
+]
+
+
+@pytest.mark.parametrize("op,cmp,R", CASES)
+def test_rank_eval_matches_oracle(op, cmp, R):
+    n, d, m_train, m_eval = 300, 24, 3000, 200
+    rng = synth.rng_for(31 + R)
+    emb = (rng.standard_normal((n, d)) * 0.3).astype(np.float32)
+    relp = synth.perturbed_relation_params(op, R, d, rng, 0.3)
+    src, dst = synth.zipf_edges(n, m_train + m_eval, 1.0, 1.0, rng)
+    rel = rng.integers(0, R, m_train + m_eval).astype(np.int32) if R > 1 else None
+    es, ed = src[m_train:], dst[m_train:]
+    er = None if rel is None else rel[m_train:]
+    # known = train + eval, with duplicates
+    ksrc = np.concatenate([src, src[:50]])
+    kdst = np.concatenate([dst, dst[:50]])
+    krel = None if rel is None else np.concatenate([rel, rel[:50]])
+    _check(n, R, d, op, cmp, emb, relp, es, er, ed, ksrc, krel, kdst)
+
+
+def test_rank_eval_without_filter_and_errors():
+    from paper_1903_12287_amd import pbg
+    n, d = 120, 16
+    rng = synth.rng_for(5)
+    emb = (rng.standard_normal((n, d)) * 0.3).astype(np.float32)
+    src, dst = synth.zipf_edges(n, 60, 1.0, 1.0, rng)
+    e = np.zeros(0, np.int64)
+    _check(n, 1, d, "identity", "dot", emb, None, src, None, dst, e, None, e)
+    dev = torch.device("cuda")
+    ctx = pbg.pbg_bucket_init(n, 2, 1, d, "identity", "dot", "softmax")
+    try:
+        z = torch.zeros(4, dtype=torch.int32, device=dev)
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_rank_eval(ctx, z, None, z, z, None, z, torch.zeros(8, dtype=torch.int32, device=dev))
+        assert ei.value.status_name in ("UNSUPPORTED", "STATE")
+    finally:
+        pbg.pbg_free(ctx)
+    ctx = pbg.pbg_bucket_init(n, 1, 1, d, "identity", "dot", "softmax")
+    try:
+        E = torch.from_numpy(emb).to(dev)
+        pbg.pbg_bind_partition(ctx, 0, E, torch.zeros(n, dtype=torch.float32, device=dev))
+        z = torch.zeros(4, dtype=torch.int32, device=dev)
+        bad = z.clone()
+        bad[2] = n
+        ranks = torch.full((8,), -3, dtype=torch.int32, device=dev)
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_rank_eval(ctx, z, None, z, bad, None, z, ranks)
+        assert ei.value.status_name == "INVALID_ARG"
+        assert bool((ranks == -3).all())
+    finally:
+        pbg.pbg_free(ctx)
+
+
+def test_rank_eval_knowledge_graph_full_size():
+    """15,000 entities, 1,345 relations, d = 400 complex_diagonal with dot:
+    all 50,000 held-out triples ranked on both sides, filtered by the 533,000
+    known triples; 120 sampled triples checked against the oracle one by one."""
+    w = synth.knowledge_graph()
+    rng = synth.rng_for(w.seed + 1)
+    emb = (rng.standard_normal((w.n, w.d)) * 0.05).astype(np.float32)
+    relp = synth.perturbed_relation_params("complex_diagonal", w.R, w.d, rng, 0.3)
+    ksrc = np.concatenate([w.src, w.held_src])
+    krel = np.concatenate([w.rel, w.held_rel])
+    kdst = np.concatenate([w.dst, w.held_dst])
+    sample = synth.rng_for(7).choice(len(w.held_src), 120, replace=False)
+    got = _check(w.n, w.R, w.d, "complex_diagonal", "dot", emb, relp, w.held_src, w.held_rel, w.held_dst,
+                 ksrc, krel, kdst, sample=sample, min_exact=0.95)
+    assert got.shape == (100_000,) and int(got.min()) >= 1 and int(got.max()) <= w.n
