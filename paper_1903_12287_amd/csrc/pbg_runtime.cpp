@@ -245,11 +245,15 @@ pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_part
 
 void pbg_free(pbg_ctx* ctx) {
   if (!ctx) return;
-  if (ctx->cs || true) (void)hipDeviceSynchronize();
+  (void)hipDeviceSynchronize();
   ctx->ws.release();
   if (ctx->steploss_dev) (void)hipFree(ctx->steploss_dev);
-  for (auto& s : ctx->slots)
+  for (auto& s : ctx->slots) {
     if (s.emb) (void)hipFree(s.emb);
+    if (s.ready) (void)hipEventDestroy(s.ready);
+    if (s.released) (void)hipEventDestroy(s.released);
+  }
+  if (ctx->own_xs) (void)hipStreamDestroy(ctx->own_xs);
   for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
   delete ctx;
 }

@@ -24,14 +24,16 @@ struct Arena {
   void release();
 };
 
-// an HBM slot holding one partition during pbg_train_epoch
+// an HBM slot holding one partition during pbg_train_epoch: the embedding rows
+// followed by the row-wise Adagrad accumulator, in one allocation
 struct Slot {
   float* emb = nullptr;
   float* G = nullptr;
+  int64_t rows_cap = 0;
   int part = -1;
   hipEvent_t ready = nullptr;     // load finished (copy stream)
   hipEvent_t released = nullptr;  // last use finished (compute stream)
-  int64_t last_use = -1;
+  bool used = false;              // `released` has been recorded
 };
 
 // bf16 operand copies of a step (PBG_F_BF16_SCORE)
@@ -76,6 +78,7 @@ struct pbg_ctx {
   std::vector<double> step_losses;
   pbg_stats stats{};
   std::vector<Slot> slots;
+  hipStream_t own_xs = nullptr;    // copy stream created for pbg_train_epoch when none was given
   std::vector<hipEvent_t> events;  // phase-timing events, kPhaseEvents per step
 };
 

@@ -164,6 +164,7 @@ def pbg_free(ctx):
     if ctx is not None and ctx.value:
         library().pbg_free(ctx)
         ctx.value = None
+        ctx._bound = None
 
 
 def pbg_last_error(ctx) -> str:
@@ -178,17 +179,29 @@ def pbg_relation_param_floats(ctx) -> int:
     return int(library().pbg_relation_param_floats(ctx))
 
 
+def _keep(ctx, key, *tensors):
+    """The library keeps raw pointers to bound buffers: hold the tensors for as
+    long as the context lives, so that they cannot be freed under it."""
+    bound = getattr(ctx, "_bound", None)
+    if bound is None:
+        bound = {}
+        ctx._bound = bound
+    bound[key] = tensors
+
+
 def pbg_bind_partition(ctx, p, emb, adagrad, where=MEM_DEVICE):
     on_dev = where == MEM_DEVICE
     if not on_dev and not (emb.is_pinned() and adagrad.is_pinned()):
         raise ValueError("host partitions must be in page-locked (pinned) memory")
     _check(ctx, library().pbg_bind_partition(ctx, int(p), _ptr(emb, torch.float32, "emb", on_dev),
                                              _ptr(adagrad, torch.float32, "adagrad", on_dev), int(where)))
+    _keep(ctx, ("partition", int(p)), emb, adagrad)
 
 
 def pbg_bind_relations(ctx, params, adagrad):
     _check(ctx, library().pbg_bind_relations(ctx, _ptr(params, torch.float32, "params", allow_none=True),
                                              _ptr(adagrad, torch.float32, "adagrad", allow_none=True)))
+    _keep(ctx, "relations", params, adagrad)
 
 
 def pbg_set_streams(ctx, compute_stream=None, copy_stream=None):

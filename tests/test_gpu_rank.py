@@ -31,7 +31,8 @@ def _gpu_ranks(n, R, d, op, cmp, emb, relp, src, rel, dst, ksrc, krel, kdst):
         pbg.pbg_bind_partition(ctx, 0, E, G)
         if relp is not None:
             rp = torch.from_numpy(relp).to(dev)
-            pbg.pbg_bind_relations(ctx, rp, torch.zeros_like(rp))
+            rG = torch.zeros_like(rp)
+            pbg.pbg_bind_relations(ctx, rp, rG)
         pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
         t = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
         ranks = torch.zeros(2 * len(src), dtype=torch.int32, device=dev)
