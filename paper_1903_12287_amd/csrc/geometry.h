@@ -8,7 +8,10 @@
 //   qk  [S][2][C][dp]   side 0: Q = g(x_s) (dot) or its unit vector (cos)
 //                       side 1: K = g*(x_d) (dot) or the unit x_d (cos)
 //   nn  [S][2][N][dp]   side 0: destination candidates, side 1: source candidates
-//   ds  [S][2][C][Np]   score gradient dL/dS (raw scores between softmax passes)
+//   ds  [S][2][C][Np]   score gradient dL/dS (raw scores between softmax passes);
+//                       for the ranking loss dL/dS is 0 or 1 and is kept as bits,
+//                       dsb [S][2][ceil(Np/16)][C] 16-bit words (16 columns of a
+//                       row per word, stored word-column major)
 //   dq  [S][2][C][dp]   dS . N per side
 //   dn  [S][2][N][dp]   dS^T . Q per side, turned in place into the per-row
 //                       gradient contributions of the step
@@ -66,7 +69,8 @@ struct StepBufs {
   float* pos;           // [S][C] positive scores
   float* bias;          // [S][C] <theta_r, x_d> (translation + dot)
   int32_t* neg;         // [S][2][U] uniform draws (side 0 from partition j, side 1 from i)
-  float* ds;
+  float* ds;            // [S][2][C][Np] dL/dS (logistic, softmax)
+  uint16_t* dsb;        // [S][2][ceil(Np/16)][C] dL/dS bits (ranking, float32 path)
   float* rowpart;       // [S][2][C][nct][2]
   float* rowstat;       // [S][2][C]  log-sum-exp per side (softmax)
   float* dpos;          // [S][C] dL/dp

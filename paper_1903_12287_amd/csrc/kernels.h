@@ -7,7 +7,10 @@
 #include "geometry.h"
 
 // ---- matrix-core contractions -------------------------------------------------
-enum { EPI_STORE = 0, EPI_LOSS = 1, EPI_SOFTMAX_STATS = 2 };
+// EPI_LOSS_BITS: ranking loss with dS (0 or 1) written as bits, 16 columns per
+// uint16 word, word (w, row) at dsb[w * ldcb + row] (nwcb words per row; batch
+// strides cb_cs / cb_ss in words)
+enum { EPI_STORE = 0, EPI_LOSS = 1, EPI_SOFTMAX_STATS = 2, EPI_LOSS_BITS = 3 };
 enum { DIM_CC = 0, DIM_NC = 1, DIM_FIXED = 2 };
 // operand layouts: NT  A[m][k], B[n][k];  NN  A[m][k], B[k][n];  TN  A[k][m], B[k][n]
 enum { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
@@ -16,6 +19,10 @@ struct GemmArgs {
   const float* A;
   const float* B;
   float* Cm;
+  const uint16_t* Ab;    // A as a bit matrix in the dsb layout (a_cs, a_ss, lda = row pitch, in words), or NULL
+  uint16_t* dsb;         // EPI_LOSS_BITS output
+  int64_t cb_cs, cb_ss;
+  int ldcb, nwcb;
   int64_t a_cs, a_ss, b_cs, b_ss, c_cs, c_ss;  // strides (floats) per chunk and per side
   int lda, ldb, ldc;
   int mdim, ndim, kdim;  // DIM_* selectors
@@ -32,8 +39,9 @@ struct GemmArgs {
 };
 
 int gemm_pick_nb(int n);
-void launch_gemm_f32(const GemmArgs& a, int layout, int epi, int nb, int grid_n, int grid_m,
-                     int batches, hipStream_t s);
+// float32 contraction of `batches` (chunk, side) pairs; the tiling and grid
+// follow from the largest M and N of the batches
+void launch_gemm_f32(const GemmArgs& a, int layout, int epi, int batches, hipStream_t s);
 
 // bf16 operands (both contiguous along k, rows zero-padded to 32), fp32 accumulation
 struct GemmArgsH {

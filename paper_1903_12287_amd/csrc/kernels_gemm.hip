@@ -1,49 +1,173 @@
-// Chunk x candidates contractions on the gfx950 matrix cores (Sec. 4.3: the
-// scores of a chunk against its negatives form one matrix product, Fig. 3).
+// Chunk x candidates contractions on the gfx950 matrix cores, float32 (Sec.
+// 4.3: the scores of a chunk against its negatives form one matrix product,
+// Fig. 3).
 //
 //   forward   S  = Q . N^T   (C x N, K = dim)  + fused loss epilogue
 //   backward  dQ = dS . N    (C x dim, K = N)
 //             dN = dS^T . Q  (N x dim, K = C)
 //
-// One kernel template covers all three: a 256-thread workgroup (4 waves)
-// computes a 128 x (16*NB) tile; wave w owns rows [32w, 32w+32) and all
-// columns, i.e. 2 x NB blocks of v_mfma_f32_16x16x4_f32.  Operands are staged
-// through LDS in [k][m] layout (pitch = 16 mod 64 floats: conflict-free
-// fragment reads) with a register-prefetched double buffer, so the global
-// read of tile k+1 overlaps the matrix work on tile k.  Either operand may be
-// contiguous along k (rows of Q, N, dS) or along m/n (dS^T, N and Q in the
-// backward products); the loader transposes on the way into LDS.
+// One kernel template covers all three.  A 256-thread workgroup (4 waves in
+// a 2 x 2 arrangement) computes a 128 x BN tile (BN = 128, or 64 for narrow
+// outputs) with v_mfma_f32_16x16x4_f32; each wave owns 64 x BN/2 outputs,
+// i.e. 4 x BN/32 blocks of 16 x 16.
 //
-// Fragment layout of v_mfma_f32_16x16x4_f32 (checked on the device):
-//   A: lane L holds A[L % 16][L / 16]; B: lane L holds B[L / 16][L % 16];
-//   D: lane L, register r holds D[4 (L / 16) + r][L % 16].
+// Operands reach LDS through buffer loads (a load whose offset is out of the
+// buffer's range returns zeros, which pads ragged tiles without branches) and
+// a register-held prefetch of the next 16-deep k-slice, double-buffered in
+// LDS.  An operand that is contiguous along k in memory (rows of Q, N, dS) is
+// kept as [row][k] (pitch 20 floats) and read back as one 128-bit fragment per
+// 16 x 16 block and k-slice; an operand contiguous along its row/column index
+// (N and Q in dQ, dS^T and Q in dN) is kept as [k][row] (pitch BM + 4) and
+// read one float per step.  Both layouts are free of LDS bank conflicts for
+// the fragment reads.
+//
+// The 16x16x4 instruction sums A[m][k] B[k][n] over the four k held by the
+// four 16-lane groups (lane L: A row L % 16, B column L % 16, k index L / 16).
+// Lane group g supplies k = 4g + kk at step kk of a slice, so a 128-bit read
+// of four consecutive k feeds four steps; every k of the slice is used once.
+// Accumulator: lane L, register r holds D[4 (L / 16) + r][L % 16].
+//
+// Workgroups are numbered so that the tiles of one batch (one chunk and side)
+// run on the same XCD, whose L2 then holds that batch's operands.
+#include <type_traits>
+
 #include "kernels.h"
 #include "device_common.h"
 
 namespace {
 
 constexpr int BM = 128;
-constexpr int BKT = 16;
-constexpr int PA = 144;
+constexpr int BK = 16;
+constexpr int KP = BK + 4;     // pitch of a [row][k] tile
+constexpr uint32_t OOB = 0x80000000u;
 
-__host__ __device__ constexpr int lds_pitch(int bn) { return ((bn - 16 + 63) / 64) * 64 + 16; }
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const float* p) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, 0x7FFFFFF0, 0x00020000);
+}
+
+__device__ __forceinline__ v4f bload(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
 
 __device__ __forceinline__ int pick_dim(int sel, int fixed, int Cc, int Nc) {
   return sel == DIM_CC ? Cc : (sel == DIM_NC ? Nc : fixed);
 }
 
-template <int NB, bool AK, bool BKC, int EPI>
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
-  constexpr int BN = 16 * NB;
-  constexpr int PB = lds_pitch(BN);
-  constexpr int NBV = (64 * NB + 255) / 256;  // float4 loads of B per thread
-  __shared__ __align__(16) float As[2][BKT * PA];
-  __shared__ __align__(16) float Bs[2][BKT * PB];
+// One operand tile of TX rows (M or N) x BK k.  KC: global [x][k] with leading
+// dimension ld (k contiguous); otherwise global [k][x] (x contiguous).
+template <int TX, bool KC>
+struct Tile {
+  static constexpr int LOADS = TX * BK / 4 / 256;   // float4 per thread
+  static constexpr int PITCH = KC ? KP : TX + 4;
+  static constexpr int SIZE = KC ? TX * KP : BK * (TX + 4);
+
+  __device__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      uint32_t off = OOB;
+      if (KC) {
+        const int x = f >> 2, kq = f & 3;
+        const int gx = x0 + x, gk = k0 + 4 * kq;
+        if (gx < xdim && gk < ((kdim + 3) & ~3)) off = (uint32_t)(((int64_t)gx * ld + gk) * 4);
+      } else {
+        const int k = f / (TX / 4), xq = f % (TX / 4);
+        const int gk = k0 + k, gx = x0 + 4 * xq;
+        if (gk < kdim && gx < ((xdim + 3) & ~3)) off = (uint32_t)(((int64_t)gk * ld + gx) * 4);
+      }
+      r[q] = bload(rs, off);
+    }
+  }
+
+  __device__ static void store(float* s, const v4f* r, int tid) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      if (KC) {
+        const int x = f >> 2, kq = f & 3;
+        *(v4f*)(s + x * KP + 4 * kq) = r[q];
+      } else {
+        const int k = f / (TX / 4), xq = f % (TX / 4);
+        *(v4f*)(s + k * (TX + 4) + 4 * xq) = r[q];
+      }
+    }
+  }
+};
+
+// The same tile read from a 0/1 matrix stored as bits (ranking-loss dS):
+// bit b of word (w, row) is column 16 w + b of that row, and the words are
+// stored word-column major, word (w, row) at w * ld + row (ld = row pitch), so
+// that a 16-deep k-slice of consecutive rows is one contiguous run of words.
+// Each float4 of the tile is four bits of one word, expanded to 0.0 / 1.0.
+template <int TX, bool KC>
+struct BitTile {
+  static constexpr int LOADS = TX * BK / 4 / 256;
+  static constexpr int SIZE = Tile<TX, KC>::SIZE;
+
+  __device__ static v4f expand(uint32_t w, int shift) {
+    const uint32_t b = w >> shift;
+    return (v4f){(float)(b & 1u), (float)((b >> 1) & 1u), (float)((b >> 2) & 1u), (float)((b >> 3) & 1u)};
+  }
+
+  __device__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      uint32_t off = OOB;
+      int shift;
+      if (KC) {
+        const int x = f >> 2, kq = f & 3;
+        const int gx = x0 + x, gk = k0 + 4 * kq;
+        if (gx < xdim && gk < ((kdim + 3) & ~3)) off = (uint32_t)(((int64_t)(gk >> 4) * ld + gx) * 2);
+        shift = gk & 15;
+      } else {
+        const int k = f / (TX / 4), xq = f % (TX / 4);
+        const int gk = k0 + k, gx = x0 + 4 * xq;
+        if (gk < kdim && gx < ((xdim + 3) & ~3)) off = (uint32_t)(((int64_t)(gx >> 4) * ld + gk) * 2);
+        shift = gx & 15;
+      }
+      // the raw word and its shift stay in registers until the store, so that
+      // nothing waits for the load before the matrix work of the slice
+      const uint32_t word = __builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0);
+      r[q] = (v4f){__uint_as_float(word), __uint_as_float((uint32_t)shift), 0.0f, 0.0f};
+    }
+  }
+
+  __device__ static void store(float* s, const v4f* r, int tid) {
+    v4f e[LOADS];
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) e[q] = expand(__float_as_uint(r[q].x), (int)__float_as_uint(r[q].y));
+    Tile<TX, KC>::store(s, e, tid);
+  }
+};
+
+template <int BN, bool AK, bool BKC, int EPI, bool ABITS>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int tiles_n, int tiles_m) {
+  constexpr int WN = BN / 2;       // columns per wave
+  constexpr int JN = WN / 16;      // 16-wide column blocks per wave
+  using TA = typename std::conditional<ABITS, BitTile<BM, AK>, Tile<BM, AK>>::type;
+  using TB = Tile<BN, BKC>;
+  __shared__ __align__(16) float As[2][TA::SIZE];
+  __shared__ __align__(16) float Bs[2][TB::SIZE];
+  __shared__ float red[2][BM][2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
-  const int z = blockIdx.z;
+  const int wm = w >> 1, wn = w & 1;
+  const int l16 = lane & 15, g = lane >> 4;
+
+  // XCD-aware numbering: consecutive hardware ids go round-robin over 8 XCDs
+  const int nwg = gridDim.x, id = blockIdx.x;
+  const int q8 = nwg >> 3, r8 = nwg & 7, xcd = id & 7;
+  const int lid = xcd * q8 + min(xcd, r8) + (id >> 3);
+  const int tn = lid % tiles_n;
+  const int rest = lid / tiles_n;
+  const int tm = rest % tiles_m;
+  const int z = rest / tiles_m;
+
   const int c = z / a.nsides;
   const int side = z - c * a.nsides;
   int Cc = a.C, Nc = a.C + a.U;
@@ -54,143 +178,102 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   const int M = pick_dim(a.mdim, a.Mfix, Cc, Nc);
   const int N = pick_dim(a.ndim, a.Nfix, Cc, Nc);
   const int K = pick_dim(a.kdim, a.Kfix, Cc, Nc);
-  const int m0 = blockIdx.y * BM;
-  const int n0 = blockIdx.x * BN;
+  const int m0 = tm * BM;
+  const int n0 = tn * BN;
   if (m0 >= M) return;
 
   float* rowpart = nullptr;
   if (EPI != EPI_STORE) rowpart = a.rowpart + ((int64_t)(c * 2 + side) * a.C) * a.nct * 2;
   if (n0 >= N) {
     if (EPI != EPI_STORE && tid < BM && m0 + tid < M) {
-      float* rp = rowpart + ((int64_t)(m0 + tid) * a.nct + blockIdx.x) * 2;
+      float* rp = rowpart + ((int64_t)(m0 + tid) * a.nct + tn) * 2;
       rp[0] = (EPI == EPI_SOFTMAX_STATS) ? -INFINITY : 0.0f;
       rp[1] = 0.0f;
     }
     return;
   }
 
-  const float* A = a.A + c * a.a_cs + side * a.a_ss;
-  const float* B = a.B + c * a.b_cs + side * a.b_ss;
-  const int Kp4 = (K + 3) & ~3;
-  const int Mp4 = (M + 3) & ~3;
-  const int Np4 = (N + 3) & ~3;
+  const rsrc_t ra_s = ABITS ? make_rsrc((const float*)(a.Ab + c * a.a_cs + side * a.a_ss))
+                            : make_rsrc(a.A + c * a.a_cs + side * a.a_ss);
+  const rsrc_t rb_s = make_rsrc(a.B + c * a.b_cs + side * a.b_ss);
 
-  v4f acc[2][NB];
+  v4f acc[4][JN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < NB; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < JN; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
 
-  float4 ra[2], rb[NBV];
-  const float4 zero4 = make_float4(0.f, 0.f, 0.f, 0.f);
-
-  auto load_tiles = [&](int k0) {
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int idx = tid + 256 * q;
-      if (AK) {
-        const int m = idx >> 2, kq = idx & 3;
-        const int gm = m0 + m, gk = k0 + 4 * kq;
-        ra[q] = (gm < M && gk < Kp4) ? *(const float4*)(A + (int64_t)gm * a.lda + gk) : zero4;
-      } else {
-        const int k = idx >> 5, mq = idx & 31;
-        const int gk = k0 + k, gm = m0 + 4 * mq;
-        ra[q] = (gk < K && gm < Mp4) ? *(const float4*)(A + (int64_t)gk * a.lda + gm) : zero4;
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < NBV; ++q) {
-      const int idx = tid + 256 * q;
-      rb[q] = zero4;
-      if (idx < 64 * NB) {
-        if (BKC) {
-          const int n = idx >> 2, kq = idx & 3;
-          const int gn = n0 + n, gk = k0 + 4 * kq;
-          if (gn < N && gk < Kp4) rb[q] = *(const float4*)(B + (int64_t)gn * a.ldb + gk);
-        } else {
-          const int k = idx / (4 * NB), nq = idx % (4 * NB);
-          const int gk = k0 + k, gn = n0 + 4 * nq;
-          if (gk < K && gn < Np4) rb[q] = *(const float4*)(B + (int64_t)gk * a.ldb + gn);
-        }
-      }
-    }
-  };
-  auto store_tiles = [&](int buf) {
-    float* as = As[buf];
-    float* bs = Bs[buf];
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int idx = tid + 256 * q;
-      if (AK) {
-        const int m = idx >> 2, kq = idx & 3;
-        as[(4 * kq + 0) * PA + m] = ra[q].x;
-        as[(4 * kq + 1) * PA + m] = ra[q].y;
-        as[(4 * kq + 2) * PA + m] = ra[q].z;
-        as[(4 * kq + 3) * PA + m] = ra[q].w;
-      } else {
-        const int k = idx >> 5, mq = idx & 31;
-        *(float4*)(as + k * PA + 4 * mq) = ra[q];
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < NBV; ++q) {
-      const int idx = tid + 256 * q;
-      if (idx < 64 * NB) {
-        if (BKC) {
-          const int n = idx >> 2, kq = idx & 3;
-          bs[(4 * kq + 0) * PB + n] = rb[q].x;
-          bs[(4 * kq + 1) * PB + n] = rb[q].y;
-          bs[(4 * kq + 2) * PB + n] = rb[q].z;
-          bs[(4 * kq + 3) * PB + n] = rb[q].w;
-        } else {
-          const int k = idx / (4 * NB), nq = idx % (4 * NB);
-          *(float4*)(bs + k * PB + 4 * nq) = rb[q];
-        }
-      }
-    }
-  };
-
-  const int nk = (K + BKT - 1) / BKT;
-  load_tiles(0);
-  store_tiles(0);
+  v4f pa[TA::LOADS], pb[TB::LOADS];
+  const int nk = (K + BK - 1) / BK;
+  TA::load(pa, ra_s, a.lda, m0, M, 0, K, tid);
+  TB::load(pb, rb_s, a.ldb, n0, N, 0, K, tid);
+  TA::store(As[0], pa, tid);
+  TB::store(Bs[0], pb, tid);
   __syncthreads();
+
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) load_tiles((kt + 1) * BKT);
+    if (kt + 1 < nk) {
+      TA::load(pa, ra_s, a.lda, m0, M, (kt + 1) * BK, K, tid);
+      TB::load(pb, rb_s, a.ldb, n0, N, (kt + 1) * BK, K, tid);
+    }
     const float* as = As[buf];
     const float* bs = Bs[buf];
+    if (AK && BKC) {
+      v4f af[4], bf[JN];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int kr = 4 * kk + (lane >> 4);
-      float af[2], bf[NB];
+      for (int i = 0; i < 4; ++i) af[i] = *(const v4f*)(as + (64 * wm + 16 * i + l16) * KP + 4 * g);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) af[i] = as[kr * PA + 32 * w + 16 * i + (lane & 15)];
+      for (int j = 0; j < JN; ++j) bf[j] = *(const v4f*)(bs + (WN * wn + 16 * j + l16) * KP + 4 * g);
 #pragma unroll
-      for (int j = 0; j < NB; ++j) bf[j] = bs[kr * PB + 16 * j + (lane & 15)];
+      for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < NB; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i], bf[j], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < JN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i][kk], bf[j][kk], acc[i][j], 0, 0, 0);
+    } else {
+      v4f af4[4];
+      if (AK) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) af4[i] = *(const v4f*)(as + (64 * wm + 16 * i + l16) * KP + 4 * g);
+      }
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        float af[4], bf[JN];
+        const int kr = 4 * g + kk;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          af[i] = AK ? af4[i][kk] : as[kr * (BM + 4) + 64 * wm + 16 * i + l16];
+#pragma unroll
+        for (int j = 0; j < JN; ++j) bf[j] = bs[kr * (BN + 4) + WN * wn + 16 * j + l16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < JN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i], bf[j], acc[i][j], 0, 0, 0);
+      }
     }
-    if (kt + 1 < nk) store_tiles(buf ^ 1);
+    if (kt + 1 < nk) {
+      TA::store(As[buf ^ 1], pa, tid);
+      TB::store(Bs[buf ^ 1], pb, tid);
+    }
     __syncthreads();
   }
 
   float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
-  const int col = lane & 15;
-  const int rq = 4 * (lane >> 4);
+  const int colb = n0 + WN * wn + l16;
 
   if (EPI == EPI_STORE) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = m0 + 32 * w + 16 * i + rq + r;
+        const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
         if (m < M) {
 #pragma unroll
-          for (int j = 0; j < NB; ++j) {
-            const int n = n0 + 16 * j + col;
+          for (int j = 0; j < JN; ++j) {
+            const int n = colb + 16 * j;
             if (n < N) Cm[(int64_t)m * a.ldc + n] = acc[i][j][r];
           }
         }
@@ -199,54 +282,58 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   }
 
   // loss epilogues: M = Cc rows, valid columns [0, Nc) minus the diagonal,
-  // stored columns [0, ldc)
+  // stored columns [0, ldc).  Each wave leaves its row partials over its half
+  // of the tile's columns in LDS; they are combined left half first.
   const float* pos = a.pos + (int64_t)c * a.C;
   // translation + dot: source corruptions score <x_t, x_d> + <theta_r, x_d>
   const float* bias = (a.bias && side == 1) ? a.bias + (int64_t)c * a.C : nullptr;
   const float kinv = (Nc - 1 > 0) ? 1.0f / (float)(Nc - 1) : 0.0f;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int m = m0 + 32 * w + 16 * i + rq + r;
+      const int ml = 64 * wm + 16 * i + 4 * g + r;
+      const int m = m0 + ml;
       const bool mrow = m < M;
       const float p = mrow ? pos[m] : 0.0f;
       const float bm = (bias && mrow) ? bias[m] : 0.0f;
-      if (EPI == EPI_LOSS) {
+      float v0, v1;
+      if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
         float lsum = 0.0f, dsum = 0.0f;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int n = n0 + 16 * j + col;
+        for (int j = 0; j < JN; ++j) {
+          const int n = colb + 16 * j;
           const float s = acc[i][j][r] + bm;
           const bool valid = mrow && n < N && n != m;
           float dsv = 0.0f;
-          if (a.loss == LOSS_RANKING) {
+          if (EPI == EPI_LOSS_BITS || a.loss == LOSS_RANKING) {
             const float zz = a.margin - p + s;
             if (valid && zz > 0.0f) {
               dsv = 1.0f;
               lsum += zz;
             }
-          } else {
-            if (valid) {
-              dsv = sigmoidf(s) * kinv;
-              lsum += softplusf(s) * kinv;
-            }
+          } else if (valid) {
+            dsv = sigmoidf(s) * kinv;
+            lsum += softplusf(s) * kinv;
           }
           dsum += dsv;
-          if (mrow && n < a.ldc) Cm[(int64_t)m * a.ldc + n] = dsv;
+          if (EPI == EPI_LOSS_BITS) {
+            // 16 lanes of a lane group hold 16 consecutive columns of one row
+            const uint64_t mask = __ballot(dsv != 0.0f);
+            const int wcol = (n0 + WN * wn + 16 * j) >> 4;
+            if (l16 == 0 && mrow && wcol < a.nwcb)
+              a.dsb[c * a.cb_cs + side * a.cb_ss + (int64_t)wcol * a.ldcb + m] = (uint16_t)(mask >> (16 * g));
+          } else if (mrow && n < a.ldc) {
+            Cm[(int64_t)m * a.ldc + n] = dsv;
+          }
         }
-        lsum = group16_sum(lsum);
-        dsum = group16_sum(dsum);
-        if (col == 0 && mrow) {
-          float* rp = rowpart + ((int64_t)m * a.nct + blockIdx.x) * 2;
-          rp[0] = lsum;
-          rp[1] = dsum;
-        }
+        v0 = group16_sum(lsum);
+        v1 = group16_sum(dsum);
       } else {  // EPI_SOFTMAX_STATS: raw scores + per-tile (max, sum exp)
         float mx = -INFINITY;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int n = n0 + 16 * j + col;
+        for (int j = 0; j < JN; ++j) {
+          const int n = colb + 16 * j;
           const float s = acc[i][j][r] + bm;
           if (mrow && n < N && n != m) mx = fmaxf(mx, s);
           if (mrow && n < a.ldc) Cm[(int64_t)m * a.ldc + n] = s;
@@ -254,61 +341,86 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
         mx = group16_max(mx);
         float se = 0.0f;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int n = n0 + 16 * j + col;
+        for (int j = 0; j < JN; ++j) {
+          const int n = colb + 16 * j;
           if (mrow && n < N && n != m) se += expf(acc[i][j][r] + bm - mx);
         }
-        se = group16_sum(se);
-        if (col == 0 && mrow) {
-          float* rp = rowpart + ((int64_t)m * a.nct + blockIdx.x) * 2;
-          rp[0] = mx;
-          rp[1] = se;
-        }
+        v0 = mx;
+        v1 = group16_sum(se);
+      }
+      if (l16 == 0) {
+        red[wn][ml][0] = v0;
+        red[wn][ml][1] = v1;
       }
     }
-}
-
-template <int NB, bool AK, bool BKC, int EPI>
-void launch_nb(const GemmArgs& a, dim3 grid, hipStream_t s) {
-  gemm_f32_kernel<NB, AK, BKC, EPI><<<grid, 256, 0, s>>>(a);
-}
-
-template <bool AK, bool BKC, int EPI>
-void launch_any_nb(int nb, const GemmArgs& a, dim3 grid, hipStream_t s) {
-  switch (nb) {
-    case 1: launch_nb<1, AK, BKC, EPI>(a, grid, s); break;
-    case 2: launch_nb<2, AK, BKC, EPI>(a, grid, s); break;
-    case 3: launch_nb<3, AK, BKC, EPI>(a, grid, s); break;
-    case 4: launch_nb<4, AK, BKC, EPI>(a, grid, s); break;
-    case 5: launch_nb<5, AK, BKC, EPI>(a, grid, s); break;
-    case 6: launch_nb<6, AK, BKC, EPI>(a, grid, s); break;
-    case 7: launch_nb<7, AK, BKC, EPI>(a, grid, s); break;
-    default: launch_nb<8, AK, BKC, EPI>(a, grid, s); break;
+  __syncthreads();
+  if (tid < BM && m0 + tid < M) {
+    const int ml = tid;
+    float v0, v1;
+    if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
+      v0 = red[0][ml][0] + red[1][ml][0];
+      v1 = red[0][ml][1] + red[1][ml][1];
+    } else {
+      const float ma = red[0][ml][0], mb = red[1][ml][0];
+      const float mx = fmaxf(ma, mb);
+      v0 = mx;
+      v1 = (mx == -INFINITY) ? 0.0f
+                             : (ma == -INFINITY ? 0.0f : red[0][ml][1] * expf(ma - mx)) +
+                                   (mb == -INFINITY ? 0.0f : red[1][ml][1] * expf(mb - mx));
+    }
+    float* rp = rowpart + ((int64_t)(m0 + ml) * a.nct + tn) * 2;
+    rp[0] = v0;
+    rp[1] = v1;
   }
 }
 
+template <int BN, bool AK, bool BKC, int EPI, bool ABITS>
+void launch_t(const GemmArgs& a, int tiles_n, int tiles_m, int batches, hipStream_t s) {
+  const int64_t nwg = (int64_t)tiles_n * tiles_m * batches;
+  gemm_f32_kernel<BN, AK, BKC, EPI, ABITS><<<(unsigned)nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+}
+
+template <bool ABITS>
+void launch_store(const GemmArgs& a, int layout, bool narrow, int tiles_n, int tiles_m, int batches,
+                  hipStream_t s) {
+  if (layout == GEMM_NT) {
+    if (narrow) launch_t<64, true, true, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
+    else launch_t<128, true, true, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
+  } else if (layout == GEMM_NN) {
+    if (narrow) launch_t<64, true, false, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
+    else launch_t<128, true, false, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
+  } else {
+    if (narrow) launch_t<64, false, false, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
+    else launch_t<128, false, false, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
+  }
+}
+
+int dim_max(int sel, int fixed, int C, int U) { return sel == DIM_CC ? C : (sel == DIM_NC ? C + U : fixed); }
+
 }  // namespace
 
+void launch_gemm_f32(const GemmArgs& a, int layout, int epi, int batches, hipStream_t s) {
+  const int maxM = dim_max(a.mdim, a.Mfix, a.C, a.U);
+  const int maxN = dim_max(a.ndim, a.Nfix, a.C, a.U);
+  if (maxM <= 0 || maxN <= 0 || batches <= 0) return;
+  const int tiles_m = (maxM + BM - 1) / BM;
+  if (epi != EPI_STORE) {
+    const int tiles_n = (maxN + 127) / 128;   // = nct (PBG_SCORE_BN columns per tile)
+    if (epi == EPI_LOSS) launch_t<128, true, true, EPI_LOSS, false>(a, tiles_n, tiles_m, batches, s);
+    else if (epi == EPI_LOSS_BITS) launch_t<128, true, true, EPI_LOSS_BITS, false>(a, tiles_n, tiles_m, batches, s);
+    else launch_t<128, true, true, EPI_SOFTMAX_STATS, false>(a, tiles_n, tiles_m, batches, s);
+    return;
+  }
+  const bool narrow = maxN <= 64;
+  const int tiles_n = (maxN + (narrow ? 63 : 127)) / (narrow ? 64 : 128);
+  if (a.Ab) launch_store<true>(a, layout, narrow, tiles_n, tiles_m, batches, s);
+  else launch_store<false>(a, layout, narrow, tiles_n, tiles_m, batches, s);
+}
+
 // column blocks of 16 per tile for an output of width n: as few tiles as
-// possible, each at most 128 wide
+// possible, each at most 128 wide (tile choice of the bfloat16 contractions)
 int gemm_pick_nb(int n) {
   const int blocks = (n + 15) / 16;
   const int tiles = (blocks + 7) / 8;
   return (blocks + tiles - 1) / tiles;
-}
-
-void launch_gemm_f32(const GemmArgs& a, int layout, int epi, int nb, int grid_n, int grid_m,
-                     int batches, hipStream_t s) {
-  dim3 grid(grid_n, grid_m, batches);
-  if (epi == EPI_LOSS) {
-    launch_nb<8, true, true, EPI_LOSS>(a, grid, s);
-  } else if (epi == EPI_SOFTMAX_STATS) {
-    launch_nb<8, true, true, EPI_SOFTMAX_STATS>(a, grid, s);
-  } else if (layout == GEMM_NT) {
-    launch_any_nb<true, true, EPI_STORE>(nb, a, grid, s);
-  } else if (layout == GEMM_NN) {
-    launch_any_nb<true, false, EPI_STORE>(nb, a, grid, s);
-  } else {
-    launch_any_nb<false, false, EPI_STORE>(nb, a, grid, s);
-  }
 }

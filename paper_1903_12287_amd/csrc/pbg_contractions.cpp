@@ -40,16 +40,25 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   fa.nct = g.nct;
   fa.loss = g.loss;
   fa.margin = g.margin;
-  const int epi = g.loss == LOSS_SOFTMAX ? EPI_SOFTMAX_STATS : EPI_LOSS;
-  launch_gemm_f32(fa, GEMM_NT, epi, 8, g.nct, (C + 127) / 128, nch * 2, cs);
+  // ranking: dS is 0 or 1 and travels as bits, 16 columns per word
+  const bool bits = g.loss == LOSS_RANKING;
+  const int nw = (Np + 15) / 16;
+  int epi = g.loss == LOSS_SOFTMAX ? EPI_SOFTMAX_STATS : EPI_LOSS;
+  if (bits) {
+    epi = EPI_LOSS_BITS;
+    fa.dsb = b.dsb;
+    fa.cb_cs = 2ll * C * nw;
+    fa.cb_ss = (int64_t)C * nw;
+    fa.ldcb = C;
+    fa.nwcb = nw;
+  }
+  launch_gemm_f32(fa, GEMM_NT, epi, nch * 2, cs);
   mark(2);
   if (g.loss == LOSS_SOFTMAX) launch_softmax_rows(g, b, cs);
   launch_finalize(g, b, ctx->steploss_dev + t, cs);
   mark(3);
 
   // dQ = dS . N (per side)
-  const int nb = gemm_pick_nb(dp);
-  const int gn = (dp + 16 * nb - 1) / (16 * nb);
   GemmArgs qa;
   memset(&qa, 0, sizeof(qa));
   qa.A = b.ds;
@@ -72,7 +81,14 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   qa.U = U;
   qa.m_step = g.m_step;
   qa.nsides = 2;
-  launch_gemm_f32(qa, GEMM_NN, EPI_STORE, nb, gn, (C + 127) / 128, nch * 2, cs);
+  if (bits) {
+    qa.A = nullptr;
+    qa.Ab = b.dsb;
+    qa.a_cs = 2ll * C * nw;
+    qa.a_ss = (int64_t)C * nw;
+    qa.lda = C;
+  }
+  launch_gemm_f32(qa, GEMM_NN, EPI_STORE, nch * 2, cs);
   // dN = dS^T . Q (per side)
   GemmArgs na = qa;
   na.B = b.qk;
@@ -83,7 +99,7 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   na.c_ss = (int64_t)N * dp;
   na.mdim = DIM_NC;
   na.kdim = DIM_CC;
-  launch_gemm_f32(na, GEMM_TN, EPI_STORE, nb, gn, (N + 127) / 128, nch * 2, cs);
+  launch_gemm_f32(na, GEMM_TN, EPI_STORE, nch * 2, cs);
 }
 
 void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t,

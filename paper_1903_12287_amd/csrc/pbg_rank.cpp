@@ -155,7 +155,6 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
                kx[5], s);
   }
 
-  const int nb = gemm_pick_nb((int)std::min<int64_t>(n_ent, 1 << 30));
   for (int side = 0; side < 2; ++side) {
     const float* T = side == 1 && T1 ? T1 : T0;
     for (int64_t e0 = 0; e0 < n; e0 += qb) {
@@ -177,8 +176,7 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
       a.Kfix = dp;
       a.C = 1;
       a.nsides = 1;
-      const int grid_n = (int)((n_ent + 16 * nb - 1) / (16 * nb));
-      launch_gemm_f32(a, GEMM_NT, EPI_STORE, nb, grid_n, (rows + 127) / 128, 1, s);
+      launch_gemm_f32(a, GEMM_NT, EPI_STORE, 1, s);
       launch_rank_count(S, n_ent, n_ent, e0, rows, side, n, src, rel, dst, pos, bias,
                         side == 0 ? kx[0] : kx[3], side == 0 ? kx[1] : kx[4], side == 0 ? kx[2] : kx[5],
                         n_known, ranks, s);

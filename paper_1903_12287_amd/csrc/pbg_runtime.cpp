@@ -102,7 +102,11 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   b.pos = (float*)a.get(s * C * 4);
   b.bias = (float*)a.get(s * C * 4);
   b.neg = (int32_t*)a.get(s * 2 * std::max(U, 1) * 4);
-  b.ds = (float*)a.get(s * 2 * C * (int64_t)Np * 4);
+  // float32 ranking keeps dS as bits; dS as floats serves the other losses and
+  // the softmax passes of the bf16 path
+  const bool f32_ranking = ctx->loss == PBG_LOSS_RANKING && !(ctx->flags & PBG_F_BF16_SCORE);
+  b.ds = f32_ranking ? nullptr : (float*)a.get(s * 2 * C * (int64_t)Np * 4);
+  b.dsb = f32_ranking ? (uint16_t*)a.get(s * 2 * C * (int64_t)((Np + 15) / 16) * 2) : nullptr;
   b.rowpart = (float*)a.get(s * 2 * C * nct * 2 * 4);
   b.rowstat = (float*)a.get(s * 2 * C * 4);
   b.dpos = (float*)a.get(s * C * 4);
@@ -466,16 +470,14 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
         la.U = U;
         la.m_step = m_step;
         la.nsides = 1;
-        const int lnb = gemm_pick_nb(d);
-        const int lgn = (d + 16 * lnb - 1) / (16 * lnb);
-        launch_gemm_f32(la, GEMM_TN, EPI_STORE, lnb, lgn, (d + 127) / 128, nch, cs);
+        launch_gemm_f32(la, GEMM_TN, EPI_STORE, nch, cs);
         GemmArgs lb = la;
         lb.A = b.nn;                       // destination rows x_d (N0[e])
         lb.B = b.dq + (int64_t)C * dp;     // dK
         lb.Cm = ctx->relpartial + (int64_t)d * d;
         lb.a_cs = 2ll * N * dp;
         lb.b_cs = 2ll * C * dp;
-        launch_gemm_f32(lb, GEMM_TN, EPI_STORE, lnb, lgn, (d + 127) / 128, nch, cs);
+        launch_gemm_f32(lb, GEMM_TN, EPI_STORE, nch, cs);
         launch_relation_single_adagrad(ctx->relp, ctx->relG, d * d, ctx->relpartial, 2 * nch, lr, cs);
       } else if (ctx->R > 1) {
         launch_radix_sort(b.rkeys, b.rvals, m_step, rel_bits, ctx->sw, cs);
