@@ -46,7 +46,23 @@ def parse():
                     help="chunks of the same bucket the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true", help="skip the bf16-input leg")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy five times (reference kernel of known "
+                         "size for scaling hardware byte counters) and exit")
     return ap.parse_args()
+
+
+def calibrate_copy():
+    """A plain copy of known size: 2^28 float32 read and written per launch."""
+    import torch
+    torch.cuda.set_device(0)
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": src.numel() * 4, "copy_bytes_written": dst.numel() * 4,
+                      "launches": 5}))
 
 
 def train_range(pbg, ctx, src, dst, step0, nsteps, total_steps):
@@ -109,7 +125,22 @@ def run_leg(pbg, torch, flags, emb0, relp0, src, dst, args, total_steps):
     return dt, st
 
 
-def roofline(st, peak, kernel):
+def measured_traffic(kernel_source_rel):
+    """HBM bytes per launch of the score kernel from the committed rocprofv3
+    counter runs, or None when the kernel source has changed since they were
+    taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "score_kernel_hbm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = open(os.path.join(ROOT, kernel_source_rel), "rb").read()
+    if rec.get("source_sha256") != hashlib.sha256(src).hexdigest():
+        return None
+    return rec["hbm_read_bytes_per_launch"] + rec["hbm_write_bytes_per_launch"]
+
+
+def roofline(st, peak, kernel, traffic=None):
     """Dominant kernel: the score contraction with its fused loss epilogue.
     Algorithmic flops per launch: 2 sides x 2 C N d per chunk (a third of the
     12 C N d of the three contractions), one launch per step."""
@@ -117,7 +148,7 @@ def roofline(st, peak, kernel):
     flops = st["score_flops"] / 3.0
     achieved = flops / (st["score_ms"] / 1e3) / 1e12 if st["score_ms"] > 0 else None
     return {"kernel": kernel, "bound": "mfma", "achieved": achieved, "peak": peak,
-            "unit": "TFLOP/s", "frac": achieved / peak if achieved else None, "traffic": None,
+            "unit": "TFLOP/s", "frac": achieved / peak if achieved else None, "traffic": traffic,
             "avg_launch_ms": st["score_ms"] / launches, "flops_per_launch": flops / launches}
 
 
@@ -128,6 +159,9 @@ def phases(st):
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path is not "
               "built", file=sys.stderr)
@@ -165,7 +199,9 @@ def main():
                    "operator": "translation", "comparator": "cos", "loss": "ranking",
                    "chunk": C, "uniform_negatives": U, "chunks_per_step": S,
                    "edges_per_step": S * C, "partitions": 1},
-        "roofline": roofline(st, PEAK_FP32_MFMA, "gemm_f32_kernel<8,NT,LOSS> (score + ranking epilogue)"),
+        "roofline": roofline(st, PEAK_FP32_MFMA,
+                             "gemm_f32_kernel<128,true,true,EPI_LOSS_BITS> (score + ranking epilogue)",
+                             measured_traffic("paper_1903_12287_amd/csrc/kernels_gemm.hip")),
         "phases_ms_per_step": phases(st),
         "backward_contractions_tflops": (2 * st["score_flops"] / 3.0) / (st["backward_ms"] / 1e3) / 1e12
         if st["backward_ms"] > 0 else None,

@@ -85,30 +85,29 @@ void launch_op_backward(const StepGeom& g, const StepBufs& b, const float* relT,
 
 // ---- sort, segments, updates ----------------------------------------------------
 struct SortWork {
-  uint32_t* keys_alt;
+  uint32_t* keys_alt;   // [max_n] ping-pong buffers of the sort
   uint32_t* vals_alt;
   uint32_t* hist;       // [256][max blocks]
-  uint32_t* flags;      // [n] scratch
-  uint32_t* seg_start;  // [n + 1]
-  uint32_t* piece_start;// [n + 1]
-  uint32_t* piece_seg;  // [n] scratch (piece ids)
-  uint32_t* seg_first_piece;  // [n + 1]
-  uint32_t* counts;     // [4]: segments, pieces
-  uint32_t* scan_tmp;   // block sums
-  float* partial;       // [n][width]
+  uint32_t* scan_tmp;   // block sums of the multi-launch scan
+  float* partial;       // [max_n][width] per-block partial sums of segments
   int max_n;
 };
 
 // stable LSD radix sort of (key, value) pairs on the low `bits` bits of the
 // keys; the result is left in keys / vals
 void launch_radix_sort(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, hipStream_t s);
+// the same sort without the final copy: *out_keys / *out_vals receive the
+// buffers that hold the result (keys / vals or the work buffers)
+void launch_radix_sort_to(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, uint32_t** out_keys,
+                          uint32_t** out_vals, hipStream_t s);
 
-// Adagrad over sorted contribution rows: entity tables (row-wise accumulator)
-void launch_entity_update(const StepGeom& g, const StepBufs& b, int n, SortWork& w, float lr,
-                          hipStream_t s);
-// relations with several ids (sorted by relation) or one relation (fixed-order sum)
-void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, int n, SortWork& w,
-                                   float lr, hipStream_t s);
+// Adagrad over sorted contribution rows (keys / vals as left by the sort):
+// entity tables (row-wise accumulator) and relations with several ids
+// (element-wise accumulators)
+void launch_entity_update(const StepGeom& g, const StepBufs& b, const uint32_t* keys, const uint32_t* vals,
+                          int n, SortWork& w, float lr, hipStream_t s);
+void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, const uint32_t* keys,
+                                   const uint32_t* vals, int n, SortWork& w, float lr, hipStream_t s);
 // pieces per chunk of the single-relation gradient sum (partial rows per chunk)
 #define RELSUM_PIECES 32
 void launch_relation_chunk_sums(const StepGeom& g, const float* rows, int64_t ld, int include_uniform,

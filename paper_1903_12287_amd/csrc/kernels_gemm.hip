@@ -185,6 +185,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int tiles_n, 
   float* rowpart = nullptr;
   if (EPI != EPI_STORE) rowpart = a.rowpart + ((int64_t)(c * 2 + side) * a.C) * a.nct * 2;
   if (n0 >= N) {
+    // neutral row partials: no valid column in this tile
     if (EPI != EPI_STORE && tid < BM && m0 + tid < M) {
       float* rp = rowpart + ((int64_t)(m0 + tid) * a.nct + tn) * 2;
       rp[0] = (EPI == EPI_SOFTMAX_STATS) ? -INFINITY : 0.0f;

@@ -1,15 +1,22 @@
 // Deterministic sparse update (replaces the paper's lock-free HOGWILD
 // updates, Sec. 4): the contribution rows of a step are sorted by
-// (table, row) with a stable radix sort, each run of equal keys is summed in
-// position order, and row-wise Adagrad (Sec. 3.1: one accumulator per
-// embedding row, summed over the row) is applied once per touched row.
-// Long runs (hub rows of heavy-tailed graphs) are cut into pieces of PIECE
-// positions that are summed in parallel, then combined in order: the result
-// does not depend on scheduling.
+// (table, row) with a stable radix sort, each run of equal keys (a segment)
+// is summed in position order, and row-wise Adagrad (Sec. 3.1: one
+// accumulator per embedding row, summed over the row) is applied once per
+// touched row.
+//
+// The sorted positions are cut into fixed blocks of 32.  A wave per block sums
+// every piece of the block (a piece = the positions of one segment inside the
+// block) in position order; a segment that lies inside one block is updated
+// there and then.  A segment that crosses block boundaries (a hub row of a
+// heavy-tailed graph) leaves one partial sum per block it touches, and the
+// wave of the block where it starts adds them in block order and updates it.
+// No scan or compaction is needed, and the summation order is fixed, so the
+// result does not depend on scheduling.
 #include "kernels.h"
 #include "row_ops.h"
 
-#define PIECE 32
+#define SEG_BLOCK 32
 #define SORT_IPT 16
 #define SORT_TILE (256 * SORT_IPT)
 
@@ -143,127 +150,252 @@ __global__ __launch_bounds__(256) void radix_scatter(const uint32_t* keys, const
   }
 }
 
+// ------------------------------------------------------- single-launch scan
+// exclusive prefix sum of up to 1024 * 64 values by one workgroup
+__global__ __launch_bounds__(1024) void scan_single(const uint32_t* in, int n, uint32_t* out) {
+  __shared__ uint32_t wsum[16];
+  const int per = (n + 1023) / 1024;
+  const int lo = min(n, (int)threadIdx.x * per), hi = min(n, lo + per);
+  uint32_t s = 0;
+  for (int i = lo; i < hi; ++i) s += in[i];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint32_t x = s;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  uint32_t base = 0;
+  for (int i = 0; i < w; ++i) base += wsum[i];
+  uint32_t run = base + x - s;
+  for (int i = lo; i < hi; ++i) {
+    const uint32_t v = in[i];
+    out[i] = run;
+    run += v;
+  }
+}
+
 // ---------------------------------------------------------------- segments
-__global__ void seg_flags(const uint32_t* keys, int n, uint32_t* flags) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
-    flags[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1u : 0u;
-}
+enum { SEG_ENTITY = 0, SEG_RELATION = 1 };
 
-// segment starts; piece flags (a piece starts at a segment start and every
-// PIECE positions inside a segment)
-__global__ void seg_starts(const uint32_t* flags, const uint32_t* segex, int n, uint32_t* seg_start) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
-    if (flags[i]) seg_start[segex[i]] = (uint32_t)i;
-}
-
-__global__ void piece_flags(const uint32_t* flags, const uint32_t* segex, const uint32_t* seg_start,
-                            int n, uint32_t* pflags) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
-    const uint32_t sid = segex[i] + flags[i] - 1u;
-    pflags[i] = ((uint32_t)i - seg_start[sid]) % PIECE == 0 ? 1u : 0u;
-  }
-}
-
-__global__ void piece_starts(const uint32_t* pflags, const uint32_t* pex, const uint32_t* flags,
-                             const uint32_t* segex, int n, uint32_t* piece_start,
-                             uint32_t* seg_first_piece, const uint32_t* counts) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
-    if (pflags[i]) piece_start[pex[i]] = (uint32_t)i;
-    if (flags[i]) seg_first_piece[segex[i]] = pex[i];
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    piece_start[counts[1]] = (uint32_t)n;
-    seg_first_piece[counts[0]] = counts[1];
-  }
-}
-
-// one wave per piece: in-order sum of its contribution rows
-__global__ __launch_bounds__(256) void piece_sum(const uint32_t* vals, const float* rows, int64_t ld,
-                                                 int width, const uint32_t* piece_start,
-                                                 const uint32_t* counts, float* partial) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t npieces = counts[1];
-  for (uint32_t p = blockIdx.x * 4 + (threadIdx.x >> 6); p < npieces; p += gridDim.x * 4) {
-    const uint32_t lo = piece_start[p], hi = piece_start[p + 1];
-    for (int f0 = 0; f0 < width; f0 += 64 * ROWQ) {
-      float acc[ROWQ];
-#pragma unroll
-      for (int q = 0; q < ROWQ; ++q) acc[q] = 0.0f;
-      for (uint32_t i = lo; i < hi; ++i) {
-        const float* row = rows + (int64_t)vals[i] * ld;
-#pragma unroll
-        for (int q = 0; q < ROWQ; ++q) {
-          const int f = f0 + lane + 64 * q;
-          if (f < width) acc[q] += row[f];
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < ROWQ; ++q) {
-        const int f = f0 + lane + 64 * q;
-        if (f < width) partial[(int64_t)p * width + f] = acc[q];
-      }
-    }
-  }
-}
-
-// one wave per touched entity row: g = sum of its pieces, then
-//   G += |g|^2,  theta -= lr g / (sqrt(G) + eps)
-__global__ __launch_bounds__(256) void entity_adagrad(StepGeom g, StepBufs b, const uint32_t* keys,
-                                                      const uint32_t* seg_start,
-                                                      const uint32_t* seg_first_piece,
-                                                      const uint32_t* counts, const float* partial,
-                                                      float lr) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t nseg = counts[0];
-  const int d = g.d;
-  const uint32_t mask = (1u << g.rb) - 1u;
-  for (uint32_t sgi = blockIdx.x * 4 + (threadIdx.x >> 6); sgi < nseg; sgi += gridDim.x * 4) {
-    const uint32_t key = keys[seg_start[sgi]];
+// applies the summed gradient g of the segment with key `key`
+template <int MODE>
+__device__ __forceinline__ void seg_apply(const StepGeom& g, const StepBufs& b, uint32_t key, const Row& acc,
+                                          int width, float lr, int lane) {
+  if (MODE == SEG_ENTITY) {
     const uint32_t tbl = key >> g.rb;
-    const uint32_t row = key & mask;
-    float* emb = (tbl ? b.emb_j : b.emb_i) + (int64_t)row * d;
+    const uint32_t row = key & ((1u << g.rb) - 1u);
+    float* emb = (tbl ? b.emb_j : b.emb_i) + (int64_t)row * g.d;
     float* G = (tbl ? b.G_j : b.G_i) + row;
-    Row acc;
-    row_zero(acc);
-    for (uint32_t p = seg_first_piece[sgi]; p < seg_first_piece[sgi + 1]; ++p) {
-      Row part;
-      row_load(part, partial + (int64_t)p * d, d, false, lane);
-      row_add(acc, part);
-    }
     const float gg = row_dot(acc, acc);
     const float Gn = *G + gg;
     const float scale = lr / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
-    Row th;
-    row_load(th, emb, d, false, lane);
-    row_axpy(th, -scale, acc);
 #pragma unroll
-    for (int q = 0; q < ROWQ; ++q)
-      if (lane + 64 * q < d) emb[lane + 64 * q] = th.v[q];
+    for (int q = 0; q < ROWQ; ++q) {
+      const int f = lane + 64 * q;
+      if (f < g.d) emb[f] -= scale * acc.v[q];
+    }
     if (lane == 0) *G = Gn;
+  } else {
+    float* p = b.relp + (int64_t)key * width;
+    float* G = b.relG + (int64_t)key * width;
+#pragma unroll
+    for (int q = 0; q < ROWQ; ++q) {
+      const int f = lane + 64 * q;
+      if (f < width) {
+        const float gf = acc.v[q];
+        const float Gn = G[f] + gf * gf;
+        G[f] = Gn;
+        p[f] -= lr * gf / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
+      }
+    }
   }
 }
 
-// relations with several ids: element-wise Adagrad per relation segment
-__global__ __launch_bounds__(256) void relation_adagrad_sorted(float* relp, float* relG, int dr,
-                                                               const uint32_t* keys,
-                                                               const uint32_t* seg_start,
-                                                               const uint32_t* seg_first_piece,
-                                                               const uint32_t* counts,
-                                                               const float* partial, float lr) {
+// Block of SEG_BLOCK sorted positions, one wave.  RQ floats of a row per lane
+// (lane L holds elements L + 64 q, q < RQ; width <= 64 RQ).  The rows are
+// loaded SB positions at a time with all loads in flight together, and a
+// running sum restarted at every piece start leaves each piece's in-order
+// total at its last position.  Pieces that are whole segments are updated in
+// one more round of loads; the (at most two) pieces that continue into a
+// neighbouring block are written to `partial` at their first position.
+template <int MODE, int RQ>
+__global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, const uint32_t* keys,
+                                                        const uint32_t* vals, int n, const float* rows,
+                                                        int64_t ld, int width, float* partial, float lr) {
+  constexpr int SB = 64 / RQ;                      // positions per batch of loads
   const int lane = threadIdx.x & 63;
-  const uint32_t nseg = counts[0];
-  for (uint32_t sgi = blockIdx.x * 4 + (threadIdx.x >> 6); sgi < nseg; sgi += gridDim.x * 4) {
-    const uint32_t r = keys[seg_start[sgi]];
-    for (int f = lane; f < dr; f += 64) {
-      float gsum = 0.0f;
-      for (uint32_t p = seg_first_piece[sgi]; p < seg_first_piece[sgi + 1]; ++p)
-        gsum += partial[(int64_t)p * dr + f];
-      const int64_t o = (int64_t)r * dr + f;
-      const float Gn = relG[o] + gsum * gsum;
-      relG[o] = Gn;
-      relp[o] -= lr * gsum / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
+  const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int p0 = blk * SEG_BLOCK;
+  if (p0 >= n) return;
+  const int np = min(SEG_BLOCK, n - p0);
+  const int pos = p0 + (lane & (SEG_BLOCK - 1));
+  const bool valid = lane < SEG_BLOCK && pos < p0 + np;
+  const uint32_t k = valid ? keys[pos] : 0u;
+  const uint32_t vidx = valid ? vals[pos] : 0u;
+  const bool diff_prev = valid && (pos == 0 || keys[pos - 1] != k);
+  const bool diff_next = valid && (pos == n - 1 || keys[pos + 1] != k);
+  const uint32_t pstart = (uint32_t)__ballot(valid && (pos == p0 || diff_prev));
+  const uint32_t segs = (uint32_t)__ballot(diff_prev);
+  const uint32_t sege = (uint32_t)__ballot(diff_next);
+  const uint32_t live = np == 32 ? 0xFFFFFFFFu : ((1u << np) - 1u);
+  const uint32_t pend = ((pstart >> 1) | (1u << (np - 1))) & live;   // last position of each piece
+  const bool cont_prev = !(segs & 1u);                  // first piece continues an earlier block
+  const bool cont_next = !((sege >> (np - 1)) & 1u);    // last piece continues into the next block
+  const int last_start = 31 - __builtin_clz(pstart);
+
+  float run[RQ];
+#pragma unroll
+  for (int q = 0; q < RQ; ++q) run[q] = 0.0f;
+#pragma unroll 1
+  for (int b0 = 0; b0 < np; b0 += SB) {
+    float t[SB][RQ];
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const int uu = b0 + u;
+      const bool ok = uu < np;
+      const uint32_t vu = (uint32_t)__shfl((int)vidx, uu & 31, 64);
+      const float* r = rows + (int64_t)vu * ld;
+#pragma unroll
+      for (int q = 0; q < RQ; ++q) {
+        const int f = lane + 64 * q;
+        t[u][q] = (ok && f < width) ? r[f] : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const int uu = b0 + u;
+      const bool restart = (pstart >> (uu & 31)) & 1u;
+#pragma unroll
+      for (int q = 0; q < RQ; ++q) {
+        run[q] = restart ? t[u][q] : run[q] + t[u][q];
+        t[u][q] = run[q];
+      }
+    }
+    // pieces ending in this batch: whole segments are updated, the rest saved
+    float th[SB][RQ];
+    float gsum[SB];
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const int uu = b0 + u;
+      gsum[u] = 0.0f;
+      if (uu >= np || !((pend >> uu) & 1u)) continue;
+      const bool first = !(pstart & ((2u << uu) - 2u));   // no piece start in (0, uu]
+      const bool last = uu == np - 1;
+      const bool whole = !(first && cont_prev) && !(last && cont_next);
+      const uint32_t key = (uint32_t)__shfl((int)k, uu, 64);
+      if (whole && MODE == SEG_ENTITY) {
+        const uint32_t tbl = key >> g.rb;
+        const uint32_t row = key & ((1u << g.rb) - 1u);
+        const float* emb = (tbl ? b.emb_j : b.emb_i) + (int64_t)row * g.d;
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) {
+          const int f = lane + 64 * q;
+          th[u][q] = f < width ? emb[f] : 0.0f;
+          gsum[u] += t[u][q] * t[u][q];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const int uu = b0 + u;
+      if (uu >= np || !((pend >> uu) & 1u)) continue;
+      const bool first = !(pstart & ((2u << uu) - 2u));
+      const bool last = uu == np - 1;
+      const bool whole = !(first && cont_prev) && !(last && cont_next);
+      const uint32_t key = (uint32_t)__shfl((int)k, uu, 64);
+      if (!whole) {
+        const int s0 = first ? 0 : last_start;
+        float* out = partial + (int64_t)(p0 + s0) * width;
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) {
+          const int f = lane + 64 * q;
+          if (f < width) out[f] = t[u][q];
+        }
+      } else if (MODE == SEG_ENTITY) {
+        const uint32_t tbl = key >> g.rb;
+        const uint32_t row = key & ((1u << g.rb) - 1u);
+        float* emb = (tbl ? b.emb_j : b.emb_i) + (int64_t)row * g.d;
+        float* G = (tbl ? b.G_j : b.G_i) + row;
+        const float Gn = *G + wave_sum(gsum[u]);
+        const float scale = lr / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) {
+          const int f = lane + 64 * q;
+          if (f < width) emb[f] = th[u][q] - scale * t[u][q];
+        }
+        if (lane == 0) *G = Gn;
+      } else {
+        float* p = b.relp + (int64_t)key * width;
+        float* G = b.relG + (int64_t)key * width;
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) {
+          const int f = lane + 64 * q;
+          if (f < width) {
+            const float gf = t[u][q];
+            const float Gn = G[f] + gf * gf;
+            G[f] = Gn;
+            p[f] -= lr * gf / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
+          }
+        }
+      }
     }
   }
+}
+
+// segments that cross block boundaries, updated by the wave of the block
+// where they start: its last piece plus the leading piece of every following
+// block the segment covers, added in block order, 16 loads in flight
+template <int MODE>
+__global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, const uint32_t* keys, int n,
+                                                       int width, const float* partial, float lr) {
+  const int lane = threadIdx.x & 63;
+  const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int p0 = blk * SEG_BLOCK;
+  const int p1 = p0 + SEG_BLOCK;
+  if (p1 >= n) return;
+  const uint32_t key = keys[p1 - 1];
+  if (keys[p1] != key) return;                       // nothing crosses the end of this block
+  // start of the crossing segment; not this block's if it starts before p0
+  int lo = p0, hi = p1 - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (keys[mid] < key) lo = mid + 1;
+    else hi = mid;
+  }
+  const int s = lo;
+  if (s == p0 && p0 > 0 && keys[p0 - 1] == key) return;
+  // end of the segment: first position after it
+  int a = p1, z = n;
+  while (a < z) {
+    const int mid = a + ((z - a) >> 1);
+    if (keys[mid] <= key) a = mid + 1;
+    else z = mid;
+  }
+  const int nparts = 1 + (a - 1 - p1) / SEG_BLOCK + 1;   // block of s, then blocks p1, p1 + 32, ...
+  Row acc;
+  row_zero(acc);
+  for (int i0 = 0; i0 < nparts; i0 += 16) {
+    float t[16][ROWQ];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int i = i0 + u;
+      const int at = i == 0 ? s : p1 + (i - 1) * SEG_BLOCK;
+      const float* part = partial + (int64_t)at * width;
+#pragma unroll
+      for (int q = 0; q < ROWQ; ++q) {
+        const int f = lane + 64 * q;
+        t[u][q] = (i < nparts && f < width) ? part[f] : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+#pragma unroll
+      for (int q = 0; q < ROWQ; ++q) acc.v[q] += t[u][q];
+  }
+  seg_apply<MODE>(g, b, key, acc, width, lr, lane);
 }
 
 // First level of the single-relation gradient sum: block (c, piece) adds, in
@@ -348,63 +480,61 @@ void launch_exclusive_scan(const uint32_t* in, int64_t n, uint32_t* out, uint32_
   scan_tiles<<<nb, 256, 0, s>>>(in, n, tmp, out, total);
 }
 
-void launch_radix_sort(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, hipStream_t s) {
-  if (n <= 1 || bits <= 0) return;
-  const int nblocks = (n + SORT_TILE - 1) / SORT_TILE;
+void launch_radix_sort_to(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, uint32_t** out_keys,
+                          uint32_t** out_vals, hipStream_t s) {
   uint32_t* k_in = keys;
   uint32_t* v_in = vals;
-  uint32_t* k_out = w.keys_alt;
-  uint32_t* v_out = w.vals_alt;
-  const int passes = (bits + 7) / 8;
-  for (int p = 0; p < passes; ++p) {
-    const int shift = 8 * p;
-    radix_hist<<<nblocks, 256, 0, s>>>(k_in, n, shift, nblocks, w.hist);
-    launch_exclusive_scan(w.hist, (int64_t)256 * nblocks, w.hist, w.scan_tmp, nullptr, s);
-    radix_scatter<<<nblocks, 256, 0, s>>>(k_in, v_in, n, shift, nblocks, w.hist, k_out, v_out);
-    uint32_t* t = k_in; k_in = k_out; k_out = t;
-    t = v_in; v_in = v_out; v_out = t;
+  if (n > 1 && bits > 0) {
+    const int nblocks = (n + SORT_TILE - 1) / SORT_TILE;
+    const int64_t nh = (int64_t)256 * nblocks;
+    uint32_t* k_out = w.keys_alt;
+    uint32_t* v_out = w.vals_alt;
+    const int passes = (bits + 7) / 8;
+    for (int p = 0; p < passes; ++p) {
+      const int shift = 8 * p;
+      radix_hist<<<nblocks, 256, 0, s>>>(k_in, n, shift, nblocks, w.hist);
+      if (nh <= 1024 * 64) scan_single<<<1, 1024, 0, s>>>(w.hist, (int)nh, w.hist);
+      else launch_exclusive_scan(w.hist, nh, w.hist, w.scan_tmp, nullptr, s);
+      radix_scatter<<<nblocks, 256, 0, s>>>(k_in, v_in, n, shift, nblocks, w.hist, k_out, v_out);
+      uint32_t* t = k_in; k_in = k_out; k_out = t;
+      t = v_in; v_in = v_out; v_out = t;
+    }
   }
-  if (k_in != keys) {
-    (void)hipMemcpyAsync(keys, k_in, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
-    (void)hipMemcpyAsync(vals, v_in, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
+  *out_keys = k_in;
+  *out_vals = v_in;
+}
+
+void launch_radix_sort(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, hipStream_t s) {
+  uint32_t *k = nullptr, *v = nullptr;
+  launch_radix_sort_to(keys, vals, n, bits, w, &k, &v, s);
+  if (k != keys) {
+    (void)hipMemcpyAsync(keys, k, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
+    (void)hipMemcpyAsync(vals, v, (size_t)n * 4, hipMemcpyDeviceToDevice, s);
   }
 }
 
-// builds segments (runs of equal sorted keys) and PIECE-long pieces, then
-// sums every piece; leaves counts[0] = segments, counts[1] = pieces
-static void build_and_sum_pieces(const uint32_t* keys, const uint32_t* vals, int n, const float* rows,
-                                 int64_t ld, int width, SortWork& w, hipStream_t s) {
-  const int gb = grid_for(n, 256, 4096);
-  uint32_t* flags = w.flags;
-  uint32_t* segex = w.keys_alt;     // the sort's ping-pong buffers are free here
-  uint32_t* pflags = w.vals_alt;
-  uint32_t* pex = w.piece_seg;
-  seg_flags<<<gb, 256, 0, s>>>(keys, n, flags);
-  launch_exclusive_scan(flags, n, segex, w.scan_tmp, w.counts + 0, s);
-  seg_starts<<<gb, 256, 0, s>>>(flags, segex, n, w.seg_start);
-  piece_flags<<<gb, 256, 0, s>>>(flags, segex, w.seg_start, n, pflags);
-  launch_exclusive_scan(pflags, n, pex, w.scan_tmp, w.counts + 1, s);
-  piece_starts<<<gb, 256, 0, s>>>(pflags, pex, flags, segex, n, w.piece_start, w.seg_first_piece,
-                                  w.counts);
-  piece_sum<<<grid_for(n, 4, 8192), 256, 0, s>>>(vals, rows, ld, width, w.piece_start, w.counts,
-                                                  w.partial);
+template <int MODE>
+static void seg_update(const StepGeom& g, const StepBufs& b, const uint32_t* keys, const uint32_t* vals, int n,
+                       const float* rows, int64_t ld, int width, SortWork& w, float lr, hipStream_t s) {
+  if (n <= 0) return;
+  const int blocks = (n + 4 * SEG_BLOCK - 1) / (4 * SEG_BLOCK);
+  if (width <= 128)
+    seg_update_local<MODE, 2><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial, lr);
+  else if (width <= 256)
+    seg_update_local<MODE, 4><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial, lr);
+  else
+    seg_update_local<MODE, 8><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial, lr);
+  seg_update_span<MODE><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, lr);
 }
 
-void launch_entity_update(const StepGeom& g, const StepBufs& b, int n, SortWork& w, float lr,
-                          hipStream_t s) {
-  if (n <= 0) return;
-  build_and_sum_pieces(b.keys, b.vals, n, b.dn, g.dp, g.d, w, s);
-  entity_adagrad<<<grid_for(n, 4, 8192), 256, 0, s>>>(g, b, b.keys, w.seg_start, w.seg_first_piece,
-                                                       w.counts, w.partial, lr);
+void launch_entity_update(const StepGeom& g, const StepBufs& b, const uint32_t* keys, const uint32_t* vals,
+                          int n, SortWork& w, float lr, hipStream_t s) {
+  seg_update<SEG_ENTITY>(g, b, keys, vals, n, b.dn, g.dp, g.d, w, lr, s);
 }
 
-void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, int n, SortWork& w, float lr,
-                                   hipStream_t s) {
-  if (n <= 0) return;
-  build_and_sum_pieces(b.rkeys, b.rvals, n, b.relc, g.dr, g.dr, w, s);
-  relation_adagrad_sorted<<<grid_for(n, 4, 8192), 256, 0, s>>>(b.relp, b.relG, g.dr, b.rkeys,
-                                                               w.seg_start, w.seg_first_piece,
-                                                               w.counts, w.partial, lr);
+void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, const uint32_t* keys,
+                                   const uint32_t* vals, int n, SortWork& w, float lr, hipStream_t s) {
+  seg_update<SEG_RELATION>(g, b, keys, vals, n, b.relc, g.dr, g.dr, w, lr, s);
 }
 
 void launch_relation_chunk_sums(const StepGeom& g, const float* rows, int64_t ld, int include_uniform,

@@ -68,18 +68,11 @@ static int round_up(int v, int m) { return (v + m - 1) / m * m; }
 
 bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width) {
   const int64_t nblocks = (max_n + 4095) / 4096;
-  const int64_t scan_n = std::max<int64_t>(max_n, 256 * nblocks);
   w.max_n = (int)max_n;
   w.keys_alt = (uint32_t*)a.get(max_n * 4);
   w.vals_alt = (uint32_t*)a.get(max_n * 4);
   w.hist = (uint32_t*)a.get(256 * nblocks * 4);
-  w.flags = (uint32_t*)a.get(max_n * 4);
-  w.seg_start = (uint32_t*)a.get((max_n + 1) * 4);
-  w.piece_start = (uint32_t*)a.get((max_n + 1) * 4);
-  w.piece_seg = (uint32_t*)a.get(max_n * 4);
-  w.seg_first_piece = (uint32_t*)a.get((max_n + 1) * 4);
-  w.counts = (uint32_t*)a.get(16);
-  w.scan_tmp = (uint32_t*)a.get(((scan_n + 4095) / 4096 + 1) * 4);
+  w.scan_tmp = (uint32_t*)a.get(((256 * nblocks + 4095) / 4096 + 1) * 4);
   w.partial = width > 0 ? (float*)a.get(max_n * (int64_t)width * 4) : nullptr;
   return !a.failed;
 }
@@ -443,8 +436,9 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
 
     // entities: sort contribution rows by (table, row), segment sums, Adagrad
     const int nkeys = 2 * (nch * U + m_step);
-    launch_radix_sort(b.keys, b.vals, nkeys, key_bits, ctx->sw, cs);
-    launch_entity_update(g, b, nkeys, ctx->sw, lr, cs);
+    uint32_t *skeys = nullptr, *svals = nullptr;
+    launch_radix_sort_to(b.keys, b.vals, nkeys, key_bits, ctx->sw, &skeys, &svals, cs);
+    launch_entity_update(g, b, skeys, svals, nkeys, ctx->sw, lr, cs);
 
     // relations
     if (has_rel) {
@@ -480,8 +474,9 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
         launch_gemm_f32(lb, GEMM_TN, EPI_STORE, nch, cs);
         launch_relation_single_adagrad(ctx->relp, ctx->relG, d * d, ctx->relpartial, 2 * nch, lr, cs);
       } else if (ctx->R > 1) {
-        launch_radix_sort(b.rkeys, b.rvals, m_step, rel_bits, ctx->sw, cs);
-        launch_relation_update_sorted(g, b, m_step, ctx->sw, lr, cs);
+        uint32_t *rk = nullptr, *rv = nullptr;
+        launch_radix_sort_to(b.rkeys, b.rvals, m_step, rel_bits, ctx->sw, &rk, &rv, cs);
+        launch_relation_update_sorted(g, b, rk, rv, m_step, ctx->sw, lr, cs);
       } else {
         launch_relation_chunk_sums(g, b.relc, ctx->dr, ctx->cmp == CMP_COS ? 1 : 0, ctx->relpartial, cs);
         launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch * RELSUM_PIECES,
