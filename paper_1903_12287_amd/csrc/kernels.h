@@ -43,15 +43,25 @@ int gemm_pick_nb(int n);
 // follow from the largest M and N of the batches
 void launch_gemm_f32(const GemmArgs& a, int layout, int epi, int batches, hipStream_t s);
 
-// bf16 operands (both contiguous along k, rows zero-padded to 32), fp32 accumulation
+// bf16 contractions, fp32 accumulation.  B is bf16 [n][k] (k contiguous,
+// zero-padded to 8); A is one of
+enum {
+  GA_KC = 0,        // bf16 [m][k], k contiguous
+  GA_MC = 1,        // bf16 [k][m], m contiguous
+  GA_BITS_ROW = 2,  // the ranking dS bit matrix (dsb layout), A[m][k] = bit (row m, column k)
+  GA_BITS_COL = 3   // the same matrix transposed: A[m][k] = bit (row k, column m)
+};
 struct GemmArgsH {
   const uint16_t* A;
   const uint16_t* B;
   float* Cm;             // fp32 output (STORE, SOFTMAX_STATS)
-  uint16_t* dsh;         // loss epilogue: dS rows in bf16 (strides c_*, ldc)
-  uint16_t* dsT;         // loss epilogue: dS^T rows in bf16 (strides t_*, ldt)
-  int64_t a_cs, a_ss, b_cs, b_ss, c_cs, c_ss, t_cs, t_ss;
-  int lda, ldb, ldc, ldt;
+  uint16_t* dsh;         // EPI_LOSS: dS rows in bf16 (strides c_*, ldc)
+  uint16_t* dsb;         // EPI_LOSS_BITS output (as in GemmArgs)
+  int64_t cb_cs, cb_ss;
+  int ldcb, nwcb;
+  int64_t a_cs, a_ss, b_cs, b_ss, c_cs, c_ss;
+  int lda, ldb, ldc;     // in elements (bf16 or float), or words for a bit matrix
+  int amode;             // GA_*
   int mdim, ndim, kdim;
   int Mfix, Nfix, Kfix;
   int C, U, m_step;
@@ -64,8 +74,7 @@ struct GemmArgsH {
   float margin;
 };
 
-void launch_gemm_bf16(const GemmArgsH& a, int epi, int nb, int grid_n, int grid_m, int batches,
-                      hipStream_t s);
+void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s);
 void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d,
                               uint16_t* dst, int64_t dst_bs, int ld_dst, uint16_t* dstT,
                               int64_t dstT_bs, int ld_T, int rows_p, int kp, int batches,
@@ -77,9 +86,7 @@ void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s
 
 // ---- loss finalisation and backward -----------------------------------------
 void launch_softmax_rows(const StepGeom& g, const StepBufs& b, hipStream_t s);
-void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, uint16_t* dsT,
-                              int ldh, int ldt, hipStream_t s);
-void launch_zero_dsT_tail(const StepGeom& g, uint16_t* dsT, int ldt, hipStream_t s);
+void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s);
 void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, hipStream_t s);
 void launch_op_backward(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s);
 

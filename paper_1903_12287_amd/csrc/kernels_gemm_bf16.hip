@@ -1,33 +1,42 @@
 // bfloat16 inputs / float32 accumulation for the three chunk contractions
 // (Sec. 4.3 batched negatives; the score block of a chunk is one product).
 //
-// Every product is written as C[m][n] = sum_k A[m][k] B[n][k] with both
-// operands contiguous along k, in bf16 with rows zero-padded to a multiple
-// of 32 elements:
-//   forward  S  = Q  . N^T  :  A = Q   [e][f],   B = N   [t][f]
-//   dQ       dQ = dS . N    :  A = dS  [e][t],   B = N^T [f][t]
-//   dN       dN = dS^T . Q  :  A = dS^T[t][e],   B = Q^T [f][e]
-// so the transposed operands are produced once (an LDS-tiled transpose for
-// Q^T and N^T; the forward epilogue writes dS^T next to dS).
+//   forward  S  = Q  . N^T  :  A = Q    [e][f],  B = N   [t][f]
+//   dQ       dQ = dS . N    :  A = dS   [e][t],  B = N^T [f][t]
+//   dN       dN = dS^T . Q  :  A = dS^T [t][e],  B = Q^T [f][e]
+// The B operands are contiguous along k: the bf16 copies of Q and N and their
+// transposes are produced once per step (LDS-tiled transpose).  The A operand
+// of the backward products is dS itself, read in place: for the ranking loss
+// from its bit matrix (rows for dQ, columns for dN), otherwise from bf16 dS
+// rows (transposed on the way into LDS for dN), so no copy of dS^T exists.
 //
-// A workgroup of 4 waves computes a 128 x (16*NB) tile; wave w owns rows
-// [32w, 32w+32).  Tiles of 64 k are staged in LDS as [row][k] with a pitch of
-// 72 elements (144 bytes: rows fall on distinct bank groups) and read as one
-// 16-byte fragment per lane per v_mfma_f32_16x16x32_bf16.  Fragment layout
-// (checked on the device): A lane L holds A[L % 16][8 (L / 16) + i],
-// B lane L holds B[8 (L / 16) + i][L % 16] (i = 0..7), D as in the fp32 case.
+// Layout and schedule follow the float32 kernel: 256-thread workgroups of
+// 2 x 2 waves on 128 x BN tiles, buffer loads with hardware zero-fill,
+// register prefetch one k-slice ahead, double-buffered LDS tiles [row][k]
+// (pitch 40 elements = 80 bytes: conflict-free 16-byte fragment reads), and
+// all tiles of one batch on one XCD.  A slice is 32 deep, one
+// v_mfma_f32_16x16x32_bf16 step: lane L feeds A[L % 16][8 (L / 16) + i] and
+// B[8 (L / 16) + i][L % 16], i = 0..7, one 16-byte LDS read each; the
+// accumulator holds D[4 (L / 16) + r][L % 16] in register r.
 #include "kernels.h"
 #include "device_common.h"
 
 namespace {
 
 constexpr int BM = 128;
-constexpr int BK = 64;
-constexpr int PK = 72;  // LDS pitch in bf16 elements
+constexpr int BK = 32;
+constexpr int PK = BK + 8;     // LDS pitch in bf16 elements
+constexpr uint32_t OOB = 0x80000000u;
 
-struct alignas(16) bf8 {
-  uint4 v;
-};
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, 0x7FFFFFF0, 0x00020000);
+}
+__device__ __forceinline__ u32x4 bload16(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
 
 __device__ __forceinline__ float bf16_to_f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
@@ -41,17 +50,117 @@ __device__ __forceinline__ int pick_dim(int sel, int fixed, int Cc, int Nc) {
   return sel == DIM_CC ? Cc : (sel == DIM_NC ? Nc : fixed);
 }
 
-template <int NB, int EPI>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a) {
-  constexpr int BN = 16 * NB;
-  constexpr int A_LOADS = BM * BK / 8 / 256;           // 16-byte loads of A per thread (4)
-  constexpr int B_VEC = BN * BK / 8;                    // 16-byte vectors in a B tile
-  constexpr int B_LOADS = (B_VEC + 255) / 256;
-  __shared__ __align__(16) uint16_t As[2][BM * PK];
-  __shared__ __align__(16) uint16_t Bs[2][BN * PK];
+// 0.0 / 1.0 in bf16 for bits b and b+1 of v, packed low / high
+__device__ __forceinline__ uint32_t bits2(uint32_t v, int b) {
+  return (((v >> b) & 1u) * 0x3F80u) | ((((v >> (b + 1)) & 1u) * 0x3F80u) << 16);
+}
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int z = blockIdx.z;
+// One operand tile of TX rows x BK k as LDS [row][k] bf16 (pitch PK); each
+// thread moves TX * BK / 8 / 256 groups of eight elements per slice.  Loaded
+// words stay raw in registers until the store, after the slice's matrix work.
+//   GA_KC        global [x][k] bf16, ld elements, k contiguous (zero-padded to 8)
+//   GA_MC        global [k][x] bf16, x contiguous: eight x of one k go to eight
+//                tile rows
+//   GA_BITS_ROW  bit matrix (dsb layout), tile row x = matrix row, k = column
+//   GA_BITS_COL  bit matrix, tile row x = matrix column, k = matrix row; the
+//                words of eight consecutive rows of one word column are 16
+//                contiguous bytes (row pitch a multiple of 8)
+template <int TX, int MODE>
+struct TileH {
+  static constexpr int LOADS = TX * BK / 8 / 256;
+  static constexpr int SIZE = TX * PK;
+
+  __device__ static void load(u32x4* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      uint32_t off = OOB;
+      if (MODE == GA_MC) {
+        const int k = f / (TX / 8), xq = f % (TX / 8);
+        const int gk = k0 + k, gx = x0 + 8 * xq;
+        if (gk < kdim && gx < ((xdim + 7) & ~7)) off = (uint32_t)(((int64_t)gk * ld + gx) * 2);
+        r[q] = bload16(rs, off);
+      } else {
+        const int x = f >> 2, kq = f & 3;
+        const int gx = x0 + x, gk = k0 + 8 * kq;
+        if (MODE == GA_KC) {
+          if (gx < xdim && gk < ((kdim + 7) & ~7)) off = (uint32_t)(((int64_t)gx * ld + gk) * 2);
+          r[q] = bload16(rs, off);
+        } else if (MODE == GA_BITS_ROW) {
+          if (gx < xdim && gk < ((kdim + 7) & ~7)) off = (uint32_t)(((int64_t)(gk >> 4) * ld + gx) * 2);
+          const uint32_t w = __builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0);
+          r[q] = (u32x4){w, 0u, 0u, 0u};
+        } else {
+          if (gx < ((xdim + 7) & ~7) && gk < kdim) off = (uint32_t)(((int64_t)(gx >> 4) * ld + gk) * 2);
+          r[q] = bload16(rs, off);
+        }
+      }
+    }
+  }
+
+  __device__ static void store(uint16_t* s, const u32x4* r, int tid, int x0, int k0, int kdim) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      if (MODE == GA_MC) {
+        const int k = f / (TX / 8), xq = f % (TX / 8);
+        const u32x4 v = r[q];
+        uint16_t* col = s + (8 * xq) * PK + k;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          col[(2 * i) * PK] = (uint16_t)(v[i] & 0xFFFFu);
+          col[(2 * i + 1) * PK] = (uint16_t)(v[i] >> 16);
+        }
+      } else {
+        const int x = f >> 2, kq = f & 3;
+        u32x4 v = r[q];
+        if (MODE == GA_BITS_ROW) {
+          const int b = (8 * kq) & 15;        // bit of column k0 + 8 kq in its word
+          const uint32_t w = v.x;
+          v = (u32x4){bits2(w, b), bits2(w, b + 2), bits2(w, b + 4), bits2(w, b + 6)};
+        } else if (MODE == GA_BITS_COL) {
+          const int b = (x0 + x) & 15;        // bit of this column in each row's word
+          const int gk = k0 + 8 * kq;         // rows gk + i >= kdim lie outside the chunk
+          uint32_t h[8];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            h[2 * i] = v[i] & 0xFFFFu;
+            h[2 * i + 1] = v[i] >> 16;
+          }
+#pragma unroll
+          for (int i = 0; i < 8; ++i) h[i] = (gk + i < kdim) ? ((h[i] >> b) & 1u) * 0x3F80u : 0u;
+          v = (u32x4){h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+        }
+        *(u32x4*)(s + x * PK + 8 * kq) = v;
+      }
+    }
+  }
+};
+
+template <int BN, int AMODE, int EPI>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a, int tiles_n, int tiles_m) {
+  constexpr int WN = BN / 2;
+  constexpr int JN = WN / 16;
+  using TA = TileH<BM, AMODE>;
+  using TB = TileH<BN, GA_KC>;
+  __shared__ __align__(16) uint16_t As[2][TA::SIZE];
+  __shared__ __align__(16) uint16_t Bs[2][TB::SIZE];
+  __shared__ float red[2][BM][2];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int l16 = lane & 15, g = lane >> 4;
+
+  const int nwg = gridDim.x, id = blockIdx.x;
+  const int q8 = nwg >> 3, r8 = nwg & 7, xcd = id & 7;
+  const int lid = xcd * q8 + min(xcd, r8) + (id >> 3);
+  const int tn = lid % tiles_n;
+  const int rest = lid / tiles_n;
+  const int tm = rest % tiles_m;
+  const int z = rest / tiles_m;
+
   const int c = z / a.nsides;
   const int side = z - c * a.nsides;
   int Cc = a.C, Nc = a.C + a.U;
@@ -62,98 +171,76 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a) {
   const int M = pick_dim(a.mdim, a.Mfix, Cc, Nc);
   const int N = pick_dim(a.ndim, a.Nfix, Cc, Nc);
   const int K = pick_dim(a.kdim, a.Kfix, Cc, Nc);
-  const int Kp = (K + 31) & ~31;   // operands are zero beyond K up to a multiple of 32
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int m0 = tm * BM;
+  const int n0 = tn * BN;
   if (m0 >= M) return;
+
   float* rowpart = nullptr;
   if (EPI != EPI_STORE) rowpart = a.rowpart + ((int64_t)(c * 2 + side) * a.C) * a.nct * 2;
   if (n0 >= N) {
+    // neutral row partials: no valid column in this tile
     if (EPI != EPI_STORE && tid < BM && m0 + tid < M) {
-      float* rp = rowpart + ((int64_t)(m0 + tid) * a.nct + blockIdx.x) * 2;
+      float* rp = rowpart + ((int64_t)(m0 + tid) * a.nct + tn) * 2;
       rp[0] = (EPI == EPI_SOFTMAX_STATS) ? -INFINITY : 0.0f;
       rp[1] = 0.0f;
     }
     return;
   }
-  const uint16_t* A = a.A + c * a.a_cs + side * a.a_ss;
-  const uint16_t* B = a.B + c * a.b_cs + side * a.b_ss;
 
-  v4f acc[2][NB];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < NB; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
+  const rsrc_t ra_s = make_rsrc(a.A + c * a.a_cs + side * a.a_ss);
+  const rsrc_t rb_s = make_rsrc(a.B + c * a.b_cs + side * a.b_ss);
 
-  uint4 ra[A_LOADS], rb[B_LOADS];
-  const uint4 z4 = make_uint4(0, 0, 0, 0);
-  auto load_tiles = [&](int k0) {
+  v4f acc[4][JN];
 #pragma unroll
-    for (int q = 0; q < A_LOADS; ++q) {
-      const int idx = tid + 256 * q;
-      const int m = idx >> 3, kv = idx & 7;
-      const int gm = m0 + m, gk = k0 + 8 * kv;
-      ra[q] = (gm < M && gk < Kp) ? *(const uint4*)(A + (int64_t)gm * a.lda + gk) : z4;
-    }
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int q = 0; q < B_LOADS; ++q) {
-      const int idx = tid + 256 * q;
-      const int n = idx >> 3, kv = idx & 7;
-      const int gn = n0 + n, gk = k0 + 8 * kv;
-      rb[q] = (idx < B_VEC && gn < N && gk < Kp) ? *(const uint4*)(B + (int64_t)gn * a.ldb + gk) : z4;
-    }
-  };
-  auto store_tiles = [&](int buf) {
-#pragma unroll
-    for (int q = 0; q < A_LOADS; ++q) {
-      const int idx = tid + 256 * q;
-      *(uint4*)(&As[buf][(idx >> 3) * PK + 8 * (idx & 7)]) = ra[q];
-    }
-#pragma unroll
-    for (int q = 0; q < B_LOADS; ++q) {
-      const int idx = tid + 256 * q;
-      if (idx < B_VEC) *(uint4*)(&Bs[buf][(idx >> 3) * PK + 8 * (idx & 7)]) = rb[q];
-    }
-  };
+    for (int j = 0; j < JN; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
 
-  const int nk = (Kp + BK - 1) / BK;
-  load_tiles(0);
-  store_tiles(0);
+  u32x4 pa[TA::LOADS], pb[TB::LOADS];
+  const int nk = (K + BK - 1) / BK;
+  TA::load(pa, ra_s, a.lda, m0, M, 0, K, tid);
+  TB::load(pb, rb_s, a.ldb, n0, N, 0, K, tid);
+  TA::store(As[0], pa, tid, m0, 0, K);
+  TB::store(Bs[0], pb, tid, n0, 0, K);
   __syncthreads();
+
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) load_tiles((kt + 1) * BK);
-#pragma unroll
-    for (int kk = 0; kk < BK / 32; ++kk) {
-      const int ko = 32 * kk + 8 * (lane >> 4);
-      v8bf af[2], bfr[NB];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *(const v8bf*)(&As[buf][(32 * w + 16 * i + (lane & 15)) * PK + ko]);
-#pragma unroll
-      for (int j = 0; j < NB; ++j) bfr[j] = *(const v8bf*)(&Bs[buf][(16 * j + (lane & 15)) * PK + ko]);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    if (kt + 1 < nk) {
+      TA::load(pa, ra_s, a.lda, m0, M, (kt + 1) * BK, K, tid);
+      TB::load(pb, rb_s, a.ldb, n0, N, (kt + 1) * BK, K, tid);
     }
-    if (kt + 1 < nk) store_tiles(buf ^ 1);
+    const uint16_t* as = As[buf];
+    const uint16_t* bs = Bs[buf];
+    v8bf af[4], bf[JN];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) af[i] = *(const v8bf*)(as + (64 * wm + 16 * i + l16) * PK + 8 * g);
+#pragma unroll
+    for (int j = 0; j < JN; ++j) bf[j] = *(const v8bf*)(bs + (WN * wn + 16 * j + l16) * PK + 8 * g);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < JN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    if (kt + 1 < nk) {
+      TA::store(As[buf ^ 1], pa, tid, m0, (kt + 1) * BK, K);
+      TB::store(Bs[buf ^ 1], pb, tid, n0, (kt + 1) * BK, K);
+    }
     __syncthreads();
   }
 
-  const int col = lane & 15;
-  const int rq = 4 * (lane >> 4);
+  const int colb = n0 + WN * wn + l16;
   if (EPI == EPI_STORE) {
     float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = m0 + 32 * w + 16 * i + rq + r;
+        const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
         if (m < M) {
 #pragma unroll
-          for (int j = 0; j < NB; ++j) {
-            const int n = n0 + 16 * j + col;
+          for (int j = 0; j < JN; ++j) {
+            const int n = colb + 16 * j;
             if (n < N) Cm[(int64_t)m * a.ldc + n] = acc[i][j][r];
           }
         }
@@ -161,21 +248,57 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a) {
     return;
   }
 
-  if (EPI == EPI_SOFTMAX_STATS) {
-    // raw fp32 scores + per-tile (max, sum exp) of the valid negatives
-    float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
-    const float* sbias = (a.bias && side == 1) ? a.bias + (int64_t)c * a.C : nullptr;
+  // loss epilogues, as in the float32 kernel; dS leaves as bits (ranking),
+  // bf16 (logistic) or raw fp32 scores for the softmax row pass
+  const float* pos = a.pos + (int64_t)c * a.C;
+  const float* bias = (a.bias && side == 1) ? a.bias + (int64_t)c * a.C : nullptr;
+  const float kinv = (Nc - 1 > 0) ? 1.0f / (float)(Nc - 1) : 0.0f;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + 32 * w + 16 * i + rq + r;
-        const bool mrow = m < M;
-        const float bm = (sbias && mrow) ? sbias[m] : 0.0f;
+    for (int r = 0; r < 4; ++r) {
+      const int ml = 64 * wm + 16 * i + 4 * g + r;
+      const int m = m0 + ml;
+      const bool mrow = m < M;
+      const float p = mrow ? pos[m] : 0.0f;
+      const float bm = (bias && mrow) ? bias[m] : 0.0f;
+      float v0, v1;
+      if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
+        float lsum = 0.0f, dsum = 0.0f;
+#pragma unroll
+        for (int j = 0; j < JN; ++j) {
+          const int n = colb + 16 * j;
+          const float s = acc[i][j][r] + bm;
+          const bool valid = mrow && n < N && n != m;
+          float dsv = 0.0f;
+          if (EPI == EPI_LOSS_BITS) {
+            const float zz = a.margin - p + s;
+            if (valid && zz > 0.0f) {
+              dsv = 1.0f;
+              lsum += zz;
+            }
+          } else if (valid) {
+            dsv = sigmoidf(s) * kinv;
+            lsum += softplusf(s) * kinv;
+          }
+          dsum += dsv;
+          if (EPI == EPI_LOSS_BITS) {
+            const uint64_t mask = __ballot(dsv != 0.0f);
+            const int wcol = (n0 + WN * wn + 16 * j) >> 4;
+            if (l16 == 0 && mrow && wcol < a.nwcb)
+              a.dsb[c * a.cb_cs + side * a.cb_ss + (int64_t)wcol * a.ldcb + m] = (uint16_t)(mask >> (16 * g));
+          } else if (mrow && n < a.ldc) {
+            a.dsh[c * a.c_cs + side * a.c_ss + (int64_t)m * a.ldc + n] = f_to_bf16(dsv);
+          }
+        }
+        v0 = group16_sum(lsum);
+        v1 = group16_sum(dsum);
+      } else {  // EPI_SOFTMAX_STATS
+        float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
         float mx = -INFINITY;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int n = n0 + 16 * j + col;
+        for (int j = 0; j < JN; ++j) {
+          const int n = colb + 16 * j;
           const float s = acc[i][j][r] + bm;
           if (mrow && n < N && n != m) mx = fmaxf(mx, s);
           if (mrow && n < a.ldc) Cm[(int64_t)m * a.ldc + n] = s;
@@ -183,78 +306,36 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a) {
         mx = group16_max(mx);
         float se = 0.0f;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int n = n0 + 16 * j + col;
+        for (int j = 0; j < JN; ++j) {
+          const int n = colb + 16 * j;
           if (mrow && n < N && n != m) se += expf(acc[i][j][r] + bm - mx);
         }
-        se = group16_sum(se);
-        if (col == 0 && mrow) {
-          float* rp = rowpart + ((int64_t)m * a.nct + blockIdx.x) * 2;
-          rp[0] = mx;
-          rp[1] = se;
-        }
+        v0 = mx;
+        v1 = group16_sum(se);
       }
-    return;
-  }
-
-  // loss epilogue (ranking / logistic): dS in bf16, row-major and transposed
-  uint16_t* dsh = a.dsh + c * a.c_cs + side * a.c_ss;      // [C][ldc]
-  uint16_t* dsT = a.dsT + c * a.t_cs + side * a.t_ss;      // [N][ldt]
-  const float* pos = a.pos + (int64_t)c * a.C;
-  const float* bias = (a.bias && side == 1) ? a.bias + (int64_t)c * a.C : nullptr;
-  const float kinv = (Nc - 1 > 0) ? 1.0f / (float)(Nc - 1) : 0.0f;
-  const int Mp = (M + 31) & ~31;   // dS^T columns that the backward product reads
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    float dsv[NB][4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + 32 * w + 16 * i + rq + r;
-      const bool mrow = m < M;
-      const float p = mrow ? pos[m] : 0.0f;
-      const float bm = (bias && mrow) ? bias[m] : 0.0f;
-      float lsum = 0.0f, dsum = 0.0f;
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const int n = n0 + 16 * j + col;
-        const float s = acc[i][j][r] + bm;
-        const bool valid = mrow && n < N && n != m;
-        float v = 0.0f;
-        if (a.loss == LOSS_RANKING) {
-          const float zz = a.margin - p + s;
-          if (valid && zz > 0.0f) {
-            v = 1.0f;
-            lsum += zz;
-          }
-        } else if (valid) {
-          v = sigmoidf(s) * kinv;
-          lsum += softplusf(s) * kinv;
-        }
-        const uint16_t hv = f_to_bf16(v);
-        dsv[j][r] = bf16_to_f(hv);
-        dsum += v;
-        if (mrow && n < a.ldc) dsh[(int64_t)m * a.ldc + n] = hv;
-      }
-      lsum = group16_sum(lsum);
-      dsum = group16_sum(dsum);
-      if (col == 0 && mrow) {
-        float* rp = rowpart + ((int64_t)m * a.nct + blockIdx.x) * 2;
-        rp[0] = lsum;
-        rp[1] = dsum;
+      if (l16 == 0) {
+        red[wn][ml][0] = v0;
+        red[wn][ml][1] = v1;
       }
     }
-    // transposed copy: lane writes rows n, 4 consecutive columns m
-    const int mb = m0 + 32 * w + 16 * i + rq;
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int n = n0 + 16 * j + col;
-      if (n < N && mb < Mp) {
-        uint16_t* dst = dsT + (int64_t)n * a.ldt + mb;
-        const uint32_t lo = (uint32_t)f_to_bf16(dsv[j][0]) | ((uint32_t)f_to_bf16(dsv[j][1]) << 16);
-        const uint32_t hi = (uint32_t)f_to_bf16(dsv[j][2]) | ((uint32_t)f_to_bf16(dsv[j][3]) << 16);
-        *(uint2*)dst = make_uint2(lo, hi);
-      }
+  __syncthreads();
+  if (tid < BM && m0 + tid < M) {
+    const int ml = tid;
+    float v0, v1;
+    if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
+      v0 = red[0][ml][0] + red[1][ml][0];
+      v1 = red[0][ml][1] + red[1][ml][1];
+    } else {
+      const float ma = red[0][ml][0], mb = red[1][ml][0];
+      const float mx = fmaxf(ma, mb);
+      v0 = mx;
+      v1 = (mx == -INFINITY) ? 0.0f
+                             : (ma == -INFINITY ? 0.0f : red[0][ml][1] * expf(ma - mx)) +
+                                   (mb == -INFINITY ? 0.0f : red[1][ml][1] * expf(mb - mx));
     }
+    float* rp = rowpart + ((int64_t)(m0 + ml) * a.nct + tn) * 2;
+    rp[0] = v0;
+    rp[1] = v1;
   }
 }
 
@@ -314,54 +395,52 @@ __global__ __launch_bounds__(256) void softmax_rows_bf16_kernel(StepGeom g, cons
   if (lane == 0) rowstat[(int64_t)z * g.C + row] = lse;
   const float* srow = S + ((int64_t)z * g.C + row) * g.Np;
   uint16_t* hrow = dsh + ((int64_t)z * g.C) * ldh + (int64_t)row * ldh;
-  uint16_t* tcol = dsT + ((int64_t)z * g.N) * ldt + row;
+  uint16_t* tcol = dsT ? dsT + ((int64_t)z * g.N) * ldt + row : nullptr;
   const int Nh = (Nc + 31) & ~31;
   for (int t = lane; t < Nh; t += 64) {
     float v = 0.0f;
     if (t < Nc && t != row) v = expf(srow[t] - lse);
     const uint16_t h = f_to_bf16(v);
     hrow[t] = h;
-    tcol[(int64_t)t * ldt] = h;
+    if (dsT) tcol[(int64_t)t * ldt] = h;
   }
 }
 
-// zero the dS^T columns [Cc, Cc rounded up to 32) of a short chunk
-__global__ void zero_dsT_tail_kernel(StepGeom g, uint16_t* dsT, int ldt) {
-  const int z = blockIdx.y;
-  const int c = z >> 1;
-  const int Cc = chunk_edges(g, c);
-  const int Cp = (Cc + 31) & ~31;
-  const int Nc = Cc + g.U;
-  const int width = Cp - Cc;
-  if (width == 0) return;
-  for (int idx = blockIdx.x * blockDim.x + threadIdx.x; idx < Nc * width; idx += gridDim.x * blockDim.x) {
-    const int t = idx / width, e = Cc + idx % width;
-    dsT[((int64_t)z * g.N + t) * ldt + e] = 0;
+
+template <int BN, int AMODE, int EPI>
+void launch_t(const GemmArgsH& a, int tiles_n, int tiles_m, int batches, hipStream_t s) {
+  const int64_t nwg = (int64_t)tiles_n * tiles_m * batches;
+  gemm_bf16_kernel<BN, AMODE, EPI><<<(unsigned)nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+}
+
+template <int BN>
+void launch_store(const GemmArgsH& a, int tiles_n, int tiles_m, int batches, hipStream_t s) {
+  switch (a.amode) {
+    case GA_KC: launch_t<BN, GA_KC, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
+    case GA_MC: launch_t<BN, GA_MC, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
+    case GA_BITS_ROW: launch_t<BN, GA_BITS_ROW, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
+    default: launch_t<BN, GA_BITS_COL, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
   }
 }
 
-template <int EPI>
-void launch_nb(int nb, const GemmArgsH& a, dim3 grid, hipStream_t s) {
-  switch (nb) {
-    case 1: gemm_bf16_kernel<1, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 2: gemm_bf16_kernel<2, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 3: gemm_bf16_kernel<3, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 4: gemm_bf16_kernel<4, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 5: gemm_bf16_kernel<5, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 6: gemm_bf16_kernel<6, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 7: gemm_bf16_kernel<7, EPI><<<grid, 256, 0, s>>>(a); break;
-    default: gemm_bf16_kernel<8, EPI><<<grid, 256, 0, s>>>(a); break;
-  }
-}
+int dim_max(int sel, int fixed, int C, int U) { return sel == DIM_CC ? C : (sel == DIM_NC ? C + U : fixed); }
 
 }  // namespace
 
-void launch_gemm_bf16(const GemmArgsH& a, int epi, int nb, int grid_n, int grid_m, int batches,
-                      hipStream_t s) {
-  dim3 grid(grid_n, grid_m, batches);
-  if (epi == EPI_LOSS) gemm_bf16_kernel<8, EPI_LOSS><<<grid, 256, 0, s>>>(a);
-  else if (epi == EPI_SOFTMAX_STATS) gemm_bf16_kernel<8, EPI_SOFTMAX_STATS><<<grid, 256, 0, s>>>(a);
-  else launch_nb<EPI_STORE>(nb, a, grid, s);
+void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s) {
+  const int maxM = dim_max(a.mdim, a.Mfix, a.C, a.U);
+  const int maxN = dim_max(a.ndim, a.Nfix, a.C, a.U);
+  if (maxM <= 0 || maxN <= 0 || batches <= 0) return;
+  const int tiles_m = (maxM + BM - 1) / BM;
+  if (epi != EPI_STORE) {
+    const int tiles_n = (maxN + 127) / 128;   // = nct (PBG_SCORE_BN columns per tile)
+    if (epi == EPI_LOSS) launch_t<128, GA_KC, EPI_LOSS>(a, tiles_n, tiles_m, batches, s);
+    else if (epi == EPI_LOSS_BITS) launch_t<128, GA_KC, EPI_LOSS_BITS>(a, tiles_n, tiles_m, batches, s);
+    else launch_t<128, GA_KC, EPI_SOFTMAX_STATS>(a, tiles_n, tiles_m, batches, s);
+    return;
+  }
+  if (maxN <= 64) launch_store<64>(a, (maxN + 63) / 64, tiles_m, batches, s);
+  else launch_store<128>(a, (maxN + 127) / 128, tiles_m, batches, s);
 }
 
 void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d,
@@ -369,17 +448,11 @@ void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld
                               int64_t dstT_bs, int ld_T, int rows_p, int kp, int batches,
                               hipStream_t s) {
   dim3 grid((kp + 63) / 64, (rows_p + 63) / 64, batches);
-  to_bf16_transpose_kernel<<<grid, 256, 0, s>>>(src, src_bs, rows, ld_src, d, dst, dst_bs, ld_dst,
-                                                dstT, dstT_bs, ld_T, rows_p, kp);
+  to_bf16_transpose_kernel<<<grid, 256, 0, s>>>(src, src_bs, rows, ld_src, d, dst, dst_bs, ld_dst, dstT,
+                                                dstT_bs, ld_T, rows_p, kp);
 }
 
-void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, uint16_t* dsT,
-                              int ldh, int ldt, hipStream_t s) {
+void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s) {
   dim3 grid((g.C + 3) / 4, g.nchunks * 2);
-  softmax_rows_bf16_kernel<<<grid, 256, 0, s>>>(g, b.ds, b.rowpart, b.pos, b.rowstat, dsh, dsT, ldh, ldt);
-}
-
-void launch_zero_dsT_tail(const StepGeom& g, uint16_t* dsT, int ldt, hipStream_t s) {
-  dim3 grid(4, g.nchunks * 2);
-  zero_dsT_tail_kernel<<<grid, 256, 0, s>>>(g, dsT, ldt);
+  softmax_rows_bf16_kernel<<<grid, 256, 0, s>>>(g, b.ds, b.rowpart, b.pos, b.rowstat, dsh, nullptr, ldh, 0);
 }

@@ -42,14 +42,14 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   fa.margin = g.margin;
   // ranking: dS is 0 or 1 and travels as bits, 16 columns per word
   const bool bits = g.loss == LOSS_RANKING;
-  const int nw = (Np + 15) / 16;
+  const int nw = (Np + 15) / 16, ldw = rup(C, 8);   // bit-matrix words per row, row pitch
   int epi = g.loss == LOSS_SOFTMAX ? EPI_SOFTMAX_STATS : EPI_LOSS;
   if (bits) {
     epi = EPI_LOSS_BITS;
     fa.dsb = b.dsb;
-    fa.cb_cs = 2ll * C * nw;
-    fa.cb_ss = (int64_t)C * nw;
-    fa.ldcb = C;
+    fa.cb_cs = 2ll * nw * ldw;
+    fa.cb_ss = (int64_t)nw * ldw;
+    fa.ldcb = ldw;
     fa.nwcb = nw;
   }
   launch_gemm_f32(fa, GEMM_NT, epi, nch * 2, cs);
@@ -84,9 +84,9 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   if (bits) {
     qa.A = nullptr;
     qa.Ab = b.dsb;
-    qa.a_cs = 2ll * C * nw;
-    qa.a_ss = (int64_t)C * nw;
-    qa.lda = C;
+    qa.a_cs = 2ll * nw * ldw;
+    qa.a_ss = (int64_t)nw * ldw;
+    qa.lda = ldw;
   }
   launch_gemm_f32(qa, GEMM_NN, EPI_STORE, nch * 2, cs);
   // dN = dS^T . Q (per side)
@@ -113,10 +113,13 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   launch_to_bf16_transpose(b.nn, (int64_t)N * dp, N, dp, d, h.nn, (int64_t)N * dpb, dpb, h.nnT,
                            (int64_t)dpb * Npb, Npb, Npb, dpb, nch * 2, cs);
 
+  const bool bits = g.loss == LOSS_RANKING;
+  const int nw = (Np + 15) / 16, ldw = rup(C, 8);
   GemmArgsH fa;
   memset(&fa, 0, sizeof(fa));
   fa.A = h.qk;
   fa.B = h.nn;
+  fa.amode = GA_KC;
   fa.a_cs = 2ll * C * dpb;
   fa.a_ss = (int64_t)C * dpb;
   fa.b_cs = 2ll * N * dpb;
@@ -137,45 +140,55 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   fa.nct = g.nct;
   fa.loss = g.loss;
   fa.margin = g.margin;
-  if (g.loss == LOSS_SOFTMAX) {
+  if (bits) {
+    fa.dsb = b.dsb;
+    fa.cb_cs = 2ll * nw * ldw;
+    fa.cb_ss = (int64_t)nw * ldw;
+    fa.ldcb = ldw;
+    fa.nwcb = nw;
+    launch_gemm_bf16(fa, EPI_LOSS_BITS, nch * 2, cs);
+    mark(2);
+  } else if (g.loss == LOSS_SOFTMAX) {
     fa.Cm = b.ds;
     fa.c_cs = 2ll * C * Np;
     fa.c_ss = (int64_t)C * Np;
     fa.ldc = Np;
-    launch_gemm_bf16(fa, EPI_SOFTMAX_STATS, 8, g.nct, (C + 127) / 128, nch * 2, cs);
+    launch_gemm_bf16(fa, EPI_SOFTMAX_STATS, nch * 2, cs);
     mark(2);
-    launch_softmax_rows_bf16(g, b, h.ds, h.dsT, Npb, Cpb, cs);
-    launch_zero_dsT_tail(g, h.dsT, Cpb, cs);
+    launch_softmax_rows_bf16(g, b, h.ds, Npb, cs);
   } else {
     fa.dsh = h.ds;
     fa.c_cs = 2ll * C * Npb;
     fa.c_ss = (int64_t)C * Npb;
     fa.ldc = Npb;
-    fa.dsT = h.dsT;
-    fa.t_cs = 2ll * N * Cpb;
-    fa.t_ss = (int64_t)N * Cpb;
-    fa.ldt = Cpb;
-    launch_gemm_bf16(fa, EPI_LOSS, 8, g.nct, (C + 127) / 128, nch * 2, cs);
+    launch_gemm_bf16(fa, EPI_LOSS, nch * 2, cs);
     mark(2);
   }
   launch_finalize(g, b, ctx->steploss_dev + t, cs);
   mark(3);
 
-  const int nb = gemm_pick_nb(dp);
-  const int gn = (dp + 16 * nb - 1) / (16 * nb);
-  // dQ = dS . N:  A = dS [e][t], B = N^T [f][t]
+  // dQ = dS . N:  A = dS (rows), B = N^T [f][t]
   GemmArgsH qa;
   memset(&qa, 0, sizeof(qa));
-  qa.A = h.ds;
+  if (bits) {
+    qa.A = b.dsb;
+    qa.amode = GA_BITS_ROW;
+    qa.a_cs = 2ll * nw * ldw;
+    qa.a_ss = (int64_t)nw * ldw;
+    qa.lda = ldw;
+  } else {
+    qa.A = h.ds;
+    qa.amode = GA_KC;
+    qa.a_cs = 2ll * C * Npb;
+    qa.a_ss = (int64_t)C * Npb;
+    qa.lda = Npb;
+  }
   qa.B = h.nnT;
   qa.Cm = b.dq;
-  qa.a_cs = 2ll * C * Npb;
-  qa.a_ss = (int64_t)C * Npb;
   qa.b_cs = 2ll * dpb * Npb;
   qa.b_ss = (int64_t)dpb * Npb;
   qa.c_cs = 2ll * C * dp;
   qa.c_ss = (int64_t)C * dp;
-  qa.lda = Npb;
   qa.ldb = Npb;
   qa.ldc = dp;
   qa.mdim = DIM_CC;
@@ -186,21 +199,18 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   qa.U = U;
   qa.m_step = g.m_step;
   qa.nsides = 2;
-  launch_gemm_bf16(qa, EPI_STORE, nb, gn, (C + 127) / 128, nch * 2, cs);
-  // dN = dS^T . Q:  A = dS^T [t][e], B = Q^T [f][e]
+  launch_gemm_bf16(qa, EPI_STORE, nch * 2, cs);
+  // dN = dS^T . Q:  A = dS read by columns, B = Q^T [f][e]
   GemmArgsH na = qa;
-  na.A = h.dsT;
+  na.amode = bits ? GA_BITS_COL : GA_MC;
   na.B = h.qkT;
   na.Cm = b.dn;
-  na.a_cs = 2ll * N * Cpb;
-  na.a_ss = (int64_t)N * Cpb;
   na.b_cs = 2ll * dpb * Cpb;
   na.b_ss = (int64_t)dpb * Cpb;
   na.c_cs = 2ll * N * dp;
   na.c_ss = (int64_t)N * dp;
-  na.lda = Cpb;
   na.ldb = Cpb;
   na.mdim = DIM_NC;
   na.kdim = DIM_CC;
-  launch_gemm_bf16(na, EPI_STORE, nb, gn, (N + 127) / 128, nch * 2, cs);
+  launch_gemm_bf16(na, EPI_STORE, nch * 2, cs);
 }

@@ -95,11 +95,11 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   b.pos = (float*)a.get(s * C * 4);
   b.bias = (float*)a.get(s * C * 4);
   b.neg = (int32_t*)a.get(s * 2 * std::max(U, 1) * 4);
-  // float32 ranking keeps dS as bits; dS as floats serves the other losses and
-  // the softmax passes of the bf16 path
-  const bool f32_ranking = ctx->loss == PBG_LOSS_RANKING && !(ctx->flags & PBG_F_BF16_SCORE);
-  b.ds = f32_ranking ? nullptr : (float*)a.get(s * 2 * C * (int64_t)Np * 4);
-  b.dsb = f32_ranking ? (uint16_t*)a.get(s * 2 * C * (int64_t)((Np + 15) / 16) * 2) : nullptr;
+  // the ranking loss keeps dS as bits (word-column major, row pitch C rounded
+  // up to 8); dS as floats serves the other losses (raw scores for softmax)
+  const bool ranking = ctx->loss == PBG_LOSS_RANKING;
+  b.ds = ranking ? nullptr : (float*)a.get(s * 2 * C * (int64_t)Np * 4);
+  b.dsb = ranking ? (uint16_t*)a.get(s * 2 * (int64_t)round_up(C, 8) * ((Np + 15) / 16) * 2) : nullptr;
   b.rowpart = (float*)a.get(s * 2 * C * nct * 2 * 4);
   b.rowstat = (float*)a.get(s * 2 * C * 4);
   b.dpos = (float*)a.get(s * C * 4);
@@ -135,8 +135,7 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
     ctx->h.nn = (uint16_t*)a.get(s * 2 * N * dpb * 2);
     ctx->h.qkT = (uint16_t*)a.get(s * 2 * dpb * Cpb * 2);
     ctx->h.nnT = (uint16_t*)a.get(s * 2 * dpb * Npb * 2);
-    ctx->h.ds = (uint16_t*)a.get(s * 2 * C * (int64_t)Npb * 2);
-    ctx->h.dsT = (uint16_t*)a.get(s * 2 * N * (int64_t)Cpb * 2);
+    if (!ranking) ctx->h.ds = (uint16_t*)a.get(s * 2 * C * (int64_t)Npb * 2);
   }
   if (a.failed) {
     ctx->ws.release();

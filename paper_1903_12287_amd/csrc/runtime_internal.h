@@ -42,8 +42,7 @@ struct BufsH {
   uint16_t* nn = nullptr;   // [S][2][N][dpb]
   uint16_t* qkT = nullptr;  // [S][2][dpb][Cpb]
   uint16_t* nnT = nullptr;  // [S][2][dpb][Npb]
-  uint16_t* ds = nullptr;   // [S][2][C][Npb]
-  uint16_t* dsT = nullptr;  // [S][2][N][Cpb]
+  uint16_t* ds = nullptr;   // [S][2][C][Npb] dS rows (logistic, softmax)
 };
 
 struct pbg_ctx {
