@@ -100,6 +100,10 @@ struct SortWork {
   int max_n;
 };
 
+// work-buffer sizes (entries) of a radix sort of n keys: digit histograms and
+// the multi-launch scan's block sums
+int64_t radix_hist_entries(int64_t n);
+int64_t radix_scan_tmp_entries(int64_t n);
 // stable LSD radix sort of (key, value) pairs on the low `bits` bits of the
 // keys; the result is left in keys / vals
 void launch_radix_sort(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, hipStream_t s);

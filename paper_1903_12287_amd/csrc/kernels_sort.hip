@@ -17,6 +17,7 @@
 #include "row_ops.h"
 
 #define SEG_BLOCK 32
+// scan tiles and radix-sort tiles: SORT_IPT * 256 values per workgroup
 #define SORT_IPT 16
 #define SORT_TILE (256 * SORT_IPT)
 
@@ -93,20 +94,33 @@ __global__ __launch_bounds__(256) void scan_tiles(const uint32_t* in, int64_t n,
 }
 
 // ---------------------------------------------------------------- radix sort
+// Per-block digit counts; each thread loads its IPT keys up front.
+template <int IPT>
 __global__ __launch_bounds__(256) void radix_hist(const uint32_t* keys, int n, int shift, int nblocks,
                                                   uint32_t* hist) {
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
-  __syncthreads();
-  const int base = blockIdx.x * SORT_TILE;
-  for (int r = 0; r < SORT_IPT; ++r) {
+  const int base = blockIdx.x * (256 * IPT);
+  uint32_t k[IPT];
+#pragma unroll
+  for (int r = 0; r < IPT; ++r) {
     const int idx = base + r * 256 + threadIdx.x;
-    if (idx < n) atomicAdd(&h[(keys[idx] >> shift) & 255u], 1u);   // integer: order-free
+    k[r] = idx < n ? keys[idx] : 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < IPT; ++r) {
+    const int idx = base + r * 256 + threadIdx.x;
+    if (idx < n) atomicAdd(&h[(k[r] >> shift) & 255u], 1u);   // integer: order-free
   }
   __syncthreads();
   hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
 }
 
+// Stable scatter: rows of 256 keys are ranked in order (wave ballots over the
+// digit bits give each key's rank among equal digits of its wave; earlier waves
+// and rows add their counts).  Keys and values are loaded up front.
+template <int IPT>
 __global__ __launch_bounds__(256) void radix_scatter(const uint32_t* keys, const uint32_t* vals, int n,
                                                      int shift, int nblocks, const uint32_t* offs,
                                                      uint32_t* okeys, uint32_t* ovals) {
@@ -114,17 +128,24 @@ __global__ __launch_bounds__(256) void radix_scatter(const uint32_t* keys, const
   __shared__ uint32_t wc[4][256];
   __shared__ uint32_t gofs[256];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int base = blockIdx.x * (256 * IPT);
+  uint32_t kr[IPT], vr[IPT];
+#pragma unroll
+  for (int r = 0; r < IPT; ++r) {
+    const int idx = base + r * 256 + tid;
+    kr[r] = idx < n ? keys[idx] : 0u;
+    vr[r] = idx < n ? vals[idx] : 0u;
+  }
   run[tid] = 0;
   for (int q = 0; q < 4; ++q) wc[q][tid] = 0;
   gofs[tid] = offs[(int64_t)tid * nblocks + blockIdx.x];
   __syncthreads();
   const unsigned long long lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-  const int base = blockIdx.x * SORT_TILE;
-  for (int r = 0; r < SORT_IPT; ++r) {
+#pragma unroll
+  for (int r = 0; r < IPT; ++r) {
     const int idx = base + r * 256 + tid;
     const bool valid = idx < n;
-    const uint32_t key = valid ? keys[idx] : 0u;
-    const uint32_t val = valid ? vals[idx] : 0u;
+    const uint32_t key = kr[r];
     const uint32_t dig = (key >> shift) & 255u;
     unsigned long long peers = __ballot(valid);
 #pragma unroll
@@ -141,7 +162,7 @@ __global__ __launch_bounds__(256) void radix_scatter(const uint32_t* keys, const
       for (int q = 0; q < w; ++q) off += wc[q][dig];
       const uint32_t pos = gofs[dig] + off;
       okeys[pos] = key;
-      ovals[pos] = val;
+      ovals[pos] = vr[r];
     }
     __syncthreads();
     run[tid] += wc[0][tid] + wc[1][tid] + wc[2][tid] + wc[3][tid];
@@ -151,13 +172,18 @@ __global__ __launch_bounds__(256) void radix_scatter(const uint32_t* keys, const
 }
 
 // ------------------------------------------------------- single-launch scan
-// exclusive prefix sum of up to 1024 * 64 values by one workgroup
+// exclusive prefix sum of up to 1024 * 64 values by one workgroup: thread t
+// owns a run of at most 64 consecutive values, loaded all at once
 __global__ __launch_bounds__(1024) void scan_single(const uint32_t* in, int n, uint32_t* out) {
   __shared__ uint32_t wsum[16];
   const int per = (n + 1023) / 1024;
-  const int lo = min(n, (int)threadIdx.x * per), hi = min(n, lo + per);
+  const int lo = min(n, (int)threadIdx.x * per), cnt = min(n, lo + per) - lo;
+  uint32_t v[64];
+#pragma unroll
+  for (int i = 0; i < 64; ++i) v[i] = i < cnt ? in[lo + i] : 0u;
   uint32_t s = 0;
-  for (int i = lo; i < hi; ++i) s += in[i];
+#pragma unroll
+  for (int i = 0; i < 64; ++i) s += v[i];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   uint32_t x = s;
 #pragma unroll
@@ -167,13 +193,12 @@ __global__ __launch_bounds__(1024) void scan_single(const uint32_t* in, int n, u
   }
   if (lane == 63) wsum[w] = x;
   __syncthreads();
-  uint32_t base = 0;
-  for (int i = 0; i < w; ++i) base += wsum[i];
-  uint32_t run = base + x - s;
-  for (int i = lo; i < hi; ++i) {
-    const uint32_t v = in[i];
-    out[i] = run;
-    run += v;
+  uint32_t run = x - s;
+  for (int i = 0; i < w; ++i) run += wsum[i];
+#pragma unroll
+  for (int i = 0; i < 64; ++i) {
+    if (i < cnt) out[lo + i] = run;
+    run += v[i];
   }
 }
 
@@ -480,22 +505,29 @@ void launch_exclusive_scan(const uint32_t* in, int64_t n, uint32_t* out, uint32_
   scan_tiles<<<nb, 256, 0, s>>>(in, n, tmp, out, total);
 }
 
+int radix_tile(int64_t) { return SORT_TILE; }
+
+int64_t radix_hist_entries(int64_t n) { return 256 * ((n + radix_tile(n) - 1) / radix_tile(n)); }
+
+int64_t radix_scan_tmp_entries(int64_t n) { return (radix_hist_entries(n) + SORT_TILE - 1) / SORT_TILE + 1; }
+
 void launch_radix_sort_to(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, uint32_t** out_keys,
                           uint32_t** out_vals, hipStream_t s) {
   uint32_t* k_in = keys;
   uint32_t* v_in = vals;
   if (n > 1 && bits > 0) {
-    const int nblocks = (n + SORT_TILE - 1) / SORT_TILE;
+    const int tile = radix_tile(n);
+    const int nblocks = (n + tile - 1) / tile;
     const int64_t nh = (int64_t)256 * nblocks;
     uint32_t* k_out = w.keys_alt;
     uint32_t* v_out = w.vals_alt;
     const int passes = (bits + 7) / 8;
     for (int p = 0; p < passes; ++p) {
       const int shift = 8 * p;
-      radix_hist<<<nblocks, 256, 0, s>>>(k_in, n, shift, nblocks, w.hist);
+      radix_hist<SORT_IPT><<<nblocks, 256, 0, s>>>(k_in, n, shift, nblocks, w.hist);
       if (nh <= 1024 * 64) scan_single<<<1, 1024, 0, s>>>(w.hist, (int)nh, w.hist);
       else launch_exclusive_scan(w.hist, nh, w.hist, w.scan_tmp, nullptr, s);
-      radix_scatter<<<nblocks, 256, 0, s>>>(k_in, v_in, n, shift, nblocks, w.hist, k_out, v_out);
+      radix_scatter<SORT_IPT><<<nblocks, 256, 0, s>>>(k_in, v_in, n, shift, nblocks, w.hist, k_out, v_out);
       uint32_t* t = k_in; k_in = k_out; k_out = t;
       t = v_in; v_in = v_out; v_out = t;
     }

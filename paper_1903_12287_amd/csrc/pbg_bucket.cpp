@@ -55,7 +55,6 @@ extern "C" pbg_status pbg_bucket_edges(pbg_ctx* ctx, const int64_t* src, const i
   const int nb = P * P;
   if (nb > (1 << 24)) return set_err(ctx, PBG_ERR_UNSUPPORTED, "too many buckets");
   hipStream_t s = ctx->cs;
-  const int64_t nblocks = (n + 4095) / 4096;
   DevBuf buf;
   uint32_t* flag = (uint32_t*)buf.get(16);
   uint32_t* keys = (uint32_t*)buf.get((size_t)n * 4);
@@ -64,8 +63,8 @@ extern "C" pbg_status pbg_bucket_edges(pbg_ctx* ctx, const int64_t* src, const i
   memset(&w, 0, sizeof(w));
   w.keys_alt = (uint32_t*)buf.get((size_t)n * 4);
   w.vals_alt = (uint32_t*)buf.get((size_t)n * 4);
-  w.hist = (uint32_t*)buf.get((size_t)256 * nblocks * 4);
-  w.scan_tmp = (uint32_t*)buf.get((size_t)((256 * nblocks + 4095) / 4096 + 1) * 4);
+  w.hist = (uint32_t*)buf.get((size_t)radix_hist_entries(n) * 4);
+  w.scan_tmp = (uint32_t*)buf.get((size_t)radix_scan_tmp_entries(n) * 4);
   w.max_n = (int)n;
   if (buf.failed)
     return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "bucketing workspace (%lld edges) could not be allocated",

@@ -112,11 +112,10 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
     for (auto& p : kx) p = (int32_t*)buf.get((size_t)n_known * 4);
     keys = (uint32_t*)buf.get((size_t)n_known * 4);
     vals = (uint32_t*)buf.get((size_t)n_known * 4);
-    const int64_t nblocks = (n_known + 4095) / 4096;
     w.keys_alt = (uint32_t*)buf.get((size_t)n_known * 4);
     w.vals_alt = (uint32_t*)buf.get((size_t)n_known * 4);
-    w.hist = (uint32_t*)buf.get((size_t)256 * nblocks * 4);
-    w.scan_tmp = (uint32_t*)buf.get((size_t)((256 * nblocks + 4095) / 4096 + 1) * 4);
+    w.hist = (uint32_t*)buf.get((size_t)radix_hist_entries(n_known) * 4);
+    w.scan_tmp = (uint32_t*)buf.get((size_t)radix_scan_tmp_entries(n_known) * 4);
     w.max_n = (int)n_known;
   }
   if (buf.failed) return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "rank-eval workspace could not be allocated");

@@ -67,12 +67,11 @@ static int bits_for(uint64_t v) {  // bits needed for values in [0, v]
 static int round_up(int v, int m) { return (v + m - 1) / m * m; }
 
 bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width) {
-  const int64_t nblocks = (max_n + 4095) / 4096;
   w.max_n = (int)max_n;
   w.keys_alt = (uint32_t*)a.get(max_n * 4);
   w.vals_alt = (uint32_t*)a.get(max_n * 4);
-  w.hist = (uint32_t*)a.get(256 * nblocks * 4);
-  w.scan_tmp = (uint32_t*)a.get(((256 * nblocks + 4095) / 4096 + 1) * 4);
+  w.hist = (uint32_t*)a.get(radix_hist_entries(max_n) * 4);
+  w.scan_tmp = (uint32_t*)a.get(radix_scan_tmp_entries(max_n) * 4);
   w.partial = width > 0 ? (float*)a.get(max_n * (int64_t)width * 4) : nullptr;
   return !a.failed;
 }
