@@ -46,6 +46,11 @@ def parse():
                     help="chunks of the same bucket the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true", help="skip the bf16-input leg")
+    ap.add_argument("--row", choices=["bucketing", "knowledge_graph", "big_bucket", "epoch", "tiny"],
+                    help="measure another row of the hot path instead of the default training step: "
+                         "edge bucketing of the follower graph, the knowledge-graph pass and filtered "
+                         "rank evaluation, one bucket of the large partitioned graph, the follower-graph "
+                         "epoch with partition swapping, or the tiny social graph")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy five times (reference kernel of known "
                          "size for scaling hardware byte counters) and exit")
@@ -162,6 +167,12 @@ def main():
     if args.calibrate_copy:
         calibrate_copy()
         return
+    if args.row:
+        if args.gpus != 1:
+            print("bench.py runs on one GPU only", file=sys.stderr)
+            sys.exit(2)
+        print(json.dumps(ROWS[args.row]()))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path is not "
               "built", file=sys.stderr)
@@ -220,6 +231,345 @@ def main():
         out["cpu_baseline"] = cpu_baseline(src.cpu().numpy(), dst.cpu().numpy(), emb0.cpu().numpy(),
                                            args.cpu_sample_chunks)
     print(json.dumps(out))
+
+
+# ---------------------------------------------------------------------------
+# Other rows of the hot path (bench.py --row ...).  Each prints one JSON line
+# with its throughput, the roofline of its dominant kernel and the oracle
+# timed on a bounded sample on the host.
+# ---------------------------------------------------------------------------
+def _median_time(fn, reps=3):
+    import torch
+    times = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        fn()
+        torch.cuda.synchronize()
+        times.append(time.perf_counter() - t0)
+    times.sort()
+    return times[len(times) // 2]
+
+
+def _cores():
+    import torch
+    return torch.get_num_threads()
+
+
+def row_bucketing():
+    """Edge bucketing of the follower-graph-shaped graph (41,652,230 nodes,
+    1,468,365,182 edges, Zipf 1.2 sources / 0.9 destinations, 8 partitions)."""
+    import numpy as np
+    import torch
+    from oracle import pbg_oracle as O
+    from paper_1903_12287_amd import pbg, synth
+    n, E, P = 41_652_230, 1_468_365_182, 8
+    torch.cuda.set_device(0)
+    src, dst = synth.zipf_edges_device(n, E, 1.2, 0.9, synth.device_generator(20190005))
+    dev = torch.device("cuda")
+    offsets = torch.empty(P * P + 1, dtype=torch.int64, device=dev)
+    sl = torch.empty(E, dtype=torch.int32, device=dev)
+    dl = torch.empty(E, dtype=torch.int32, device=dev)
+    ctx = pbg.pbg_bucket_init(n, P, 1, 100, "linear", "dot", "logistic")
+    try:
+        pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
+        pbg.pbg_bucket_edges(ctx, src, None, dst, offsets, sl, None, dl)
+        dt = _median_time(lambda: pbg.pbg_bucket_edges(ctx, src, None, dst, offsets, sl, None, dl))
+    finally:
+        pbg.pbg_free(ctx)
+    alg_bytes = E * (8 + 8 + 4 + 4)          # read two int64 ids, write two int32 local ids
+    m = 30_000_000
+    hs, hd = src[:m].cpu().numpy(), dst[:m].cpu().numpy()
+    t0 = time.perf_counter()
+    O.bucket_edges(hs, np.zeros(m, np.int32), hd, n, P)
+    ct = time.perf_counter() - t0
+    return {"metric": "edges bucketed/sec on 1 MI355X", "value": E / dt, "unit": "edges/s",
+            "ms": dt * 1e3, "dtype": "int64 -> int32",
+            "config": {"workload": "follower_graph", "nodes": n, "edges": E, "partitions": P},
+            "roofline": {"bound": "hbm", "achieved": alg_bytes / dt / 1e9, "peak": PEAK_HBM, "unit": "GB/s",
+                         "frac": alg_bytes / dt / 1e9 / PEAK_HBM, "traffic": None,
+                         "note": "algorithmic bytes = 24 per edge (two int64 ids in, two int32 local ids out); "
+                                 "the call also makes one stable radix pass over 8-byte key/position pairs"},
+            "cpu_baseline": {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+                             "sample": f"first {m} edges, numpy stable argsort, {ct:.1f} s"}}
+
+
+def row_knowledge_graph():
+    """Knowledge-graph-shaped graph (15,000 entities, 1,345 relations, 483,000
+    training + 50,000 held-out triples, d = 400, complex_diagonal, dot,
+    softmax): one training pass and the filtered rank evaluation of the
+    held-out triples against all entities on both sides."""
+    import numpy as np
+    import torch
+    from oracle import pbg_oracle as O
+    from paper_1903_12287_amd import pbg, synth
+    torch.cuda.set_device(0)
+    w = synth.knowledge_graph()
+    rng = synth.rng_for(w.seed + 1)
+    emb0 = synth.init_embeddings(w.n, w.d, rng)
+    rel0 = synth.identity_relation_params(w.op, w.R, w.d)
+    dev = torch.device("cuda")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
+    src, rel, dst = t(w.src), t(w.rel), t(w.dst)
+    out = {"metric": "trained edges/sec on 1 MI355X", "unit": "edges/s", "dtype": "f32",
+           "config": {"workload": "knowledge_graph", "entities": w.n, "relations": w.R, "train": w.E,
+                      "held_out": len(w.held_src), "dim": w.d, "operator": w.op, "comparator": w.cmp,
+                      "loss": w.loss, "chunk": w.C, "uniform_negatives": w.U, "chunks_per_step": w.S}}
+    emb = torch.from_numpy(emb0.copy()).to(dev)
+    G = torch.zeros(w.n, dtype=torch.float32, device=dev)
+    relp = torch.from_numpy(rel0.copy()).to(dev)
+    relG = torch.zeros_like(relp)
+    ctx = pbg.pbg_bucket_init(w.n, 1, w.R, w.d, w.op, w.cmp, w.loss, w.margin, pbg.F_PHASE_TIMING)
+    try:
+        pbg.pbg_bind_partition(ctx, 0, emb, G)
+        pbg.pbg_bind_relations(ctx, relp, relG)
+        pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
+        pbg.pbg_train_bucket(ctx, 0, 0, src, rel, dst, w.C, w.U, w.S, w.lr, w.seed)   # warm-up pass
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pbg.pbg_train_bucket(ctx, 0, 0, src, rel, dst, w.C, w.U, w.S, w.lr, w.seed + 1)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        st = pbg.pbg_get_stats(ctx)
+        out["value"] = w.E / dt
+        out["ms_per_pass"] = dt * 1e3
+        out["roofline"] = roofline(st, PEAK_FP32_MFMA, "gemm_f32_kernel<128,true,true,EPI_SOFTMAX_STATS> (score)")
+        out["phases_ms_per_step"] = phases(st)
+        # filtered ranks of the held-out triples, known = train + held-out
+        hs, hr, hd = t(w.held_src), t(w.held_rel), t(w.held_dst)
+        ks, kr, kd = (t(np.concatenate([w.src, w.held_src])), t(np.concatenate([w.rel, w.held_rel])),
+                      t(np.concatenate([w.dst, w.held_dst])))
+        ranks = torch.empty(2 * len(w.held_src), dtype=torch.int32, device=dev)
+        pbg.pbg_rank_eval(ctx, hs, hr, hd, ks, kr, kd, ranks)
+        et = _median_time(lambda: pbg.pbg_rank_eval(ctx, hs, hr, hd, ks, kr, kd, ranks))
+        mrr, hits = pbg.pbg_rank_eval(ctx, hs, hr, hd, ks, kr, kd, ranks)
+        flops = 2.0 * 2.0 * len(w.held_src) * w.n * w.d
+        out["rank_eval"] = {"value": len(w.held_src) / et, "unit": "held-out triples/s (both sides)",
+                            "ms": et * 1e3, "mrr": mrr, "hits10": hits,
+                            "roofline": {"bound": "mfma", "achieved": flops / et / 1e12, "peak": PEAK_FP32_MFMA,
+                                         "unit": "TFLOP/s", "frac": flops / et / 1e12 / PEAK_FP32_MFMA,
+                                         "traffic": None,
+                                         "note": "2 sides x 2 x held-out x entities x dim flops of candidate "
+                                                 "scores, whole call time"}}
+        emb_h = emb.cpu().numpy()
+        relp_h = relp.cpu().numpy()
+    finally:
+        pbg.pbg_free(ctx)
+    model = O.Model.create(w.n, 1, w.R, w.d, w.op, w.cmp, w.loss, w.margin, [emb0.astype(np.float64)],
+                           rel0.astype(np.float64))
+    m = 10 * w.C
+    c0 = time.perf_counter()
+    O.train_bucket(model, 0, 0, w.src[:m], w.rel[:m], w.dst[:m], w.C, w.U, w.S, w.lr, w.seed)
+    ct = time.perf_counter() - c0
+    out["cpu_baseline"] = {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+                           "sample": f"first 10 chunks ({m} edges), one step, fp64, {ct:.1f} s"}
+    emodel = O.Model.create(w.n, 1, w.R, w.d, w.op, w.cmp, w.loss, w.margin, [emb_h.astype(np.float64)],
+                            relp_h.astype(np.float64))
+    k = 100
+    c0 = time.perf_counter()
+    O.rank_eval(emodel, w.held_src[:k], w.held_rel[:k], w.held_dst[:k], np.concatenate([w.src, w.held_src]),
+                np.concatenate([w.rel, w.held_rel]), np.concatenate([w.dst, w.held_dst]))
+    ct = time.perf_counter() - c0
+    out["rank_eval"]["cpu_baseline"] = {"value": k / ct, "unit": "held-out triples/s", "cores": _cores(),
+                                        "kind": "oracle", "sample": f"first {k} held-out triples, {ct:.1f} s"}
+    return out
+
+
+def _big_bucket_tensors(torch, synth):
+    n, P, i, j, R, E, d = 121_216_723, 16, 3, 7, 5_000, 9_375_000, 100
+    ps = -(-n // P)
+    gen = synth.device_generator(20190004)
+    src, _ = synth.zipf_device(ps, 1.0, E, gen)
+    dst, _ = synth.zipf_device(ps, 1.0, E, gen)
+    rel, _ = synth.zipf_device(R, 1.3, E, gen)
+    emb_i = synth.init_embeddings_device(ps, d, gen)
+    emb_j = synth.init_embeddings_device(ps, d, gen)
+    return (n, P, i, j, R, E, d, ps, src.to(torch.int32), rel.to(torch.int32), dst.to(torch.int32),
+            emb_i, emb_j)
+
+
+def row_big_bucket():
+    """Bucket (3, 7) of a large partitioned knowledge-graph-shaped run
+    (121,216,723 entities in 16 partitions of 7,576,046 rows, 9,375,000 edges,
+    5,000 relations Zipf 1.3, d = 100, diagonal, dot, ranking 0.1): one pass
+    in fp32 and one with bf16 score inputs, both partitions resident."""
+    import numpy as np
+    import torch
+    from oracle import pbg_oracle as O
+    from paper_1903_12287_amd import pbg, synth
+    torch.cuda.set_device(0)
+    n, P, i, j, R, E, d, ps, src, rel, dst, emb_i0, emb_j0 = _big_bucket_tensors(torch, synth)
+    relp0 = torch.ones(R, d, dtype=torch.float32, device="cuda")
+    Cb, Ub, Sb = 1000, 1000, 40
+    out = {"metric": "trained edges/sec on 1 MI355X", "unit": "edges/s", "dtype": "f32",
+           "config": {"workload": "big_bucket", "entities": n, "partitions": P, "bucket": [i, j],
+                      "rows_per_partition": ps, "edges": E, "relations": R, "dim": d, "operator": "diagonal",
+                      "comparator": "dot", "loss": "ranking", "chunk": Cb, "uniform_negatives": Ub,
+                      "chunks_per_step": Sb}}
+    for flags, key in ((0, None), (pbg.F_BF16_SCORE, "bf16")):
+        emb_i, emb_j, relp = emb_i0.clone(), emb_j0.clone(), relp0.clone()
+        Gi = torch.zeros(ps, device="cuda")
+        Gj = torch.zeros(ps, device="cuda")
+        relG = torch.zeros_like(relp)
+        ctx = pbg.pbg_bucket_init(n, P, R, d, "diagonal", "dot", "ranking", 0.1, flags | pbg.F_PHASE_TIMING)
+        try:
+            pbg.pbg_bind_partition(ctx, i, emb_i, Gi)
+            pbg.pbg_bind_partition(ctx, j, emb_j, Gj)
+            pbg.pbg_bind_relations(ctx, relp, relG)
+            pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
+            w = 10 * Sb * Cb
+            pbg.pbg_train_bucket(ctx, i, j, src[:w], rel[:w], dst[:w], Cb, Ub, Sb, 0.1, 1)   # warm-up
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            pbg.pbg_train_bucket(ctx, i, j, src, rel, dst, Cb, Ub, Sb, 0.1, 20190004)
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            st = pbg.pbg_get_stats(ctx)
+        finally:
+            pbg.pbg_free(ctx)
+        peak = PEAK_BF16_MFMA if flags else PEAK_FP32_MFMA
+        leg = {"value": E / dt, "ms_per_pass": dt * 1e3,
+               "roofline": roofline(st, peak, "score contraction with the ranking epilogue"),
+               "phases_ms_per_step": phases(st)}
+        if key:
+            out[key] = leg
+        else:
+            out.update(leg)
+    # oracle: the first 10 chunks from the same initial state, partitions i and j only
+    m = 10 * Cb
+    model = O.Model(n, P, R, d, "diagonal", "dot", "ranking", 0.1)
+    model.emb = {i: emb_i0.cpu().numpy().astype(np.float64), j: emb_j0.cpu().numpy().astype(np.float64)}
+    model.G = {i: np.zeros(ps), j: np.zeros(ps)}
+    model.rel = np.ones((R, d))
+    model.relG = np.zeros((R, d))
+    hs, hr, hd = src[:m].cpu().numpy(), rel[:m].cpu().numpy(), dst[:m].cpu().numpy()
+    c0 = time.perf_counter()
+    O.train_bucket(model, i, j, hs, hr, hd, Cb, Ub, Sb, 0.1, 20190004)
+    ct = time.perf_counter() - c0
+    out["cpu_baseline"] = {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+                           "sample": f"first 10 chunks ({m} edges) of the bucket, fp64, {ct:.1f} s"}
+    return out
+
+
+def row_epoch():
+    """Follower-graph-shaped partitioned epoch (41,652,230 nodes,
+    1,468,365,182 edges, 8 partitions, d = 100, linear, dot, logistic): every
+    non-empty bucket in inside-out order, partitions in page-locked host memory
+    swapped through 3 HBM slots on a copy stream.  Edges are bucketed on the
+    device first (not timed)."""
+    import numpy as np
+    import torch
+    from oracle import pbg_oracle as O
+    from paper_1903_12287_amd import pbg, synth
+    torch.cuda.set_device(0)
+    n, E, P, d = 41_652_230, 1_468_365_182, 8, 100
+    Ce, Ue, Se = 1000, 1000, 40
+    gen = synth.device_generator(20190005)
+    src, dst = synth.zipf_edges_device(n, E, 1.2, 0.9, gen)
+    dev = torch.device("cuda")
+    offsets = torch.empty(P * P + 1, dtype=torch.int64, device=dev)
+    sl = torch.empty(E, dtype=torch.int32, device=dev)
+    dl = torch.empty(E, dtype=torch.int32, device=dev)
+    ctx = pbg.pbg_bucket_init(n, P, 1, d, "linear", "dot", "logistic", 0.1, pbg.F_PHASE_TIMING)
+    try:
+        pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
+        pbg.pbg_bucket_edges(ctx, src, None, dst, offsets, sl, None, dl)
+        del src, dst
+        off_h = offsets.cpu()
+        sl_h = torch.empty(E, dtype=torch.int32, pin_memory=True)
+        dl_h = torch.empty(E, dtype=torch.int32, pin_memory=True)
+        sl_h.copy_(sl)
+        dl_h.copy_(dl)
+        del sl, dl
+        rows = [pbg.pbg_partition_rows(ctx, p) for p in range(P)]
+        embs, Gs = [], []
+        for p in range(P):
+            e = torch.empty(rows[p], d, dtype=torch.float32, pin_memory=True)
+            e.copy_(synth.init_embeddings_device(rows[p], d, gen))
+            embs.append(e)
+            Gs.append(torch.zeros(rows[p], dtype=torch.float32, pin_memory=True))
+            pbg.pbg_bind_partition(ctx, p, embs[p], Gs[p], pbg.MEM_PINNED_HOST)
+        relp = torch.eye(d, dtype=torch.float32, device=dev).reshape(1, d * d).contiguous()
+        relG = torch.zeros_like(relp)
+        pbg.pbg_bind_relations(ctx, relp, relG)
+        copy = torch.cuda.Stream()
+        pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), copy)
+        torch.cuda.synchronize()
+        emb0_h = embs[0].numpy().copy()
+        print(f"# epoch inputs ready: {E} edges in {P * P} buckets, {P} pinned partitions", file=sys.stderr)
+        t0 = time.perf_counter()
+        loss = pbg.pbg_train_epoch(ctx, off_h, sl_h, None, dl_h, Ce, Ue, Se, 0.1, 20190005, 3)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        st = pbg.pbg_get_stats(ctx)
+    finally:
+        pbg.pbg_free(ctx)
+    m = Se * Ce
+    b00 = int(off_h[1])
+    model = O.Model(n, P, 1, d, "linear", "dot", "logistic", 0.1)
+    model.emb = {0: emb0_h.astype(np.float64)}
+    model.G = {0: np.zeros(rows[0])}
+    model.rel = np.eye(d).reshape(1, d * d)
+    model.relG = np.zeros((1, d * d))
+    c0 = time.perf_counter()
+    O.train_bucket(model, 0, 0, sl_h[:min(m, b00)].numpy(), None, dl_h[:min(m, b00)].numpy(), Ce, Ue, Se, 0.1,
+                   20190005)
+    ct = time.perf_counter() - c0
+    return {"metric": "trained edges/sec on 1 MI355X, whole epoch incl. partition swaps and edge transfers",
+            "value": E / dt, "unit": "edges/s", "seconds": dt, "dtype": "f32", "loss": loss,
+            "config": {"workload": "follower_graph_epoch", "nodes": n, "edges": E, "partitions": P,
+                       "buckets": P * P, "dim": d, "operator": "linear", "comparator": "dot",
+                       "loss": "logistic", "chunk": Ce, "uniform_negatives": Ue, "chunks_per_step": Se,
+                       "max_resident": 3},
+            "partition_loads": st["partition_loads"], "copy_ms": st["copy_ms"],
+            "compute_ms": sum(st[k] for k in ("gather_ms", "score_ms", "epilogue_ms", "backward_ms",
+                                               "opbwd_ms", "update_ms")),
+            "roofline": roofline(st, PEAK_FP32_MFMA, "score contraction with the logistic epilogue"),
+            "phases_ms_per_step": phases(st),
+            "cpu_baseline": {"value": min(m, b00) / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+                             "sample": f"first {min(m, b00)} edges of bucket (0, 0), fp64, {ct:.1f} s"}}
+
+
+def row_tiny():
+    """Tiny social graph (10,000 nodes, 100,000 edges, d = 32, identity, dot,
+    ranking 0.1, C = U = 100): one full pass, and the oracle's full pass."""
+    import numpy as np
+    import torch
+    from oracle import pbg_oracle as O
+    from paper_1903_12287_amd import pbg, synth
+    torch.cuda.set_device(0)
+    w = synth.tiny_social()
+    emb0 = synth.init_embeddings(w.n, w.d, synth.rng_for(w.seed + 1))
+    dev = torch.device("cuda")
+    src = torch.from_numpy(w.src.astype(np.int32)).to(dev)
+    dst = torch.from_numpy(w.dst.astype(np.int32)).to(dev)
+    emb = torch.from_numpy(emb0.copy()).to(dev)
+    G = torch.zeros(w.n, device=dev)
+    ctx = pbg.pbg_bucket_init(w.n, 1, 1, w.d, w.op, w.cmp, w.loss, w.margin)
+    try:
+        pbg.pbg_bind_partition(ctx, 0, emb, G)
+        pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
+        pbg.pbg_train_bucket(ctx, 0, 0, src, None, dst, w.C, w.U, w.S, w.lr, w.seed)
+        dt = _median_time(lambda: pbg.pbg_train_bucket(ctx, 0, 0, src, None, dst, w.C, w.U, w.S, w.lr, w.seed))
+    finally:
+        pbg.pbg_free(ctx)
+    model = O.Model.create(w.n, 1, 1, w.d, w.op, w.cmp, w.loss, w.margin, [emb0.astype(np.float64)])
+    c0 = time.perf_counter()
+    O.train_bucket(model, 0, 0, w.src, None, w.dst, w.C, w.U, w.S, w.lr, w.seed)
+    ct = time.perf_counter() - c0
+    return {"metric": "trained edges/sec on 1 MI355X", "value": w.E / dt, "unit": "edges/s",
+            "ms_per_pass": dt * 1e3, "dtype": "f32",
+            "config": {"workload": "tiny_social", "nodes": w.n, "edges": w.E, "dim": w.d, "operator": w.op,
+                       "comparator": w.cmp, "loss": w.loss, "chunk": w.C, "uniform_negatives": w.U,
+                       "chunks_per_step": w.S},
+            "note": "the 1.3 MB table stays in cache and a pass is 25 steps of ~30 small launches: "
+                    "launch latency bound, no roofline figure",
+            "cpu_baseline": {"value": w.E / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+                             "sample": f"full pass ({w.E} edges), fp64, {ct:.1f} s"}}
+
+
+ROWS = {"bucketing": row_bucketing, "knowledge_graph": row_knowledge_graph, "big_bucket": row_big_bucket,
+        "epoch": row_epoch, "tiny": row_tiny}
 
 
 if __name__ == "__main__":
