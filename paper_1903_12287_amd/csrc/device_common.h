@@ -94,5 +94,19 @@ __device__ __forceinline__ float sigmoidf(float x) {
   return e / (1.0f + e);
 }
 
+// sigmoid(s) and softplus(s) = log(1 + e^s) from one exponential
+// e = exp(-|s|) in (0, 1]: sigmoid = 1/(1+e) or e/(1+e), softplus =
+// max(s, 0) + log1p(e), with log1p(e) = log(u) * e / (u - 1), u = 1 + e,
+// which stays accurate when e is tiny (u - 1 is then exact)
+__device__ __forceinline__ void logistic_pair(float s, float& sig, float& sp) {
+  const float e = __expf(-fabsf(s));
+  const float u = 1.0f + e;
+  const float r = 1.0f / u;
+  sig = s >= 0.0f ? r : e * r;
+  const float um1 = u - 1.0f;
+  const float l1p = um1 == 0.0f ? e : __logf(u) * (e / um1);
+  sp = fmaxf(s, 0.0f) + l1p;
+}
+
 // round-to-nearest-even fp32 -> bf16 (finite inputs)
 __device__ __forceinline__ __bf16 to_bf16(float x) { return (__bf16)x; }

@@ -29,6 +29,7 @@ struct GemmArgs {
   int Mfix, Nfix, Kfix;
   int C, U, m_step;      // chunk geometry (m_step = 0: not chunked)
   int nsides;            // batches per chunk (2: one per corruption side)
+  int accumulate;        // EPI_STORE: add to C instead of overwriting it
   // loss epilogue
   const float* pos;      // [S][C]
   const float* bias;     // [S][C] added to side 1 scores (translation + dot), or NULL
@@ -83,6 +84,10 @@ void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld
 // ---- gather / operator / negatives --------------------------------------------
 void launch_gather(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s);
 void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s);
+// linear operator (one relation): padded copies of A and A^T, and the positive
+// scores once Q has been formed by contraction
+void launch_pad_linear(const float* A, int d, int dp, float* Ap, float* ATp, hipStream_t s);
+void launch_positive_scores(const StepGeom& g, const StepBufs& b, hipStream_t s);
 
 // ---- loss finalisation and backward -----------------------------------------
 void launch_softmax_rows(const StepGeom& g, const StepBufs& b, hipStream_t s);

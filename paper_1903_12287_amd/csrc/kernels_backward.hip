@@ -154,14 +154,16 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
       row_axpy(dQ, dpe, y);                         // positive: dp * x_d
       const float dsum = b.dsum1[ce];               // gradient of the translation bias
       // source row: J_g^T dQ + its in-chunk candidate gradient
-      if (g.op == OP_LINEAR) mat_apply(gs, b.relp + (int64_t)r * d * d, dQ, st, d, lane);  // A^T dQ
+      // (linear: A^T dQ and A dK are added afterwards by contractions over the
+      // whole step, see the launch sequence)
+      if (g.op == OP_LINEAR) row_zero(gs);
       else gs = op_adjoint(g.op, dQ, th);
       row_add(gs, gn1);
       // destination row: candidate gradient + positive + J_{g*}^T dK (+ bias)
       gd = gn0;
       row_axpy(gd, dpe, Q);
       Row jk;
-      if (g.op == OP_LINEAR) mat_apply(jk, relT + (int64_t)r * d * d, gq1, st, d, lane);   // A dK
+      if (g.op == OP_LINEAR) row_zero(jk);
       else if (g.op == OP_DIAGONAL || g.op == OP_COMPLEX) jk = op_forward(g.op, gq1, th);
       else jk = gq1;
       row_add(gd, jk);

@@ -39,17 +39,22 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b, 
     row_load(y, b.emb_j + (int64_t)t * d, d, cplx, lane);
     if (g.op != OP_IDENTITY && g.op != OP_LINEAR) row_load(th, b.relp + (int64_t)r * g.dr, d, cplx, lane);
     else row_zero(th);
-    Row gq;
-    if (g.op == OP_LINEAR) mat_apply(gq, relT + (int64_t)r * d * d, x, st, d, lane);   // A x
-    else gq = op_forward(g.op, x, th);
     float* qrow = b.qk + ((int64_t)(c * 2 + 0) * g.C + e) * dp;
     float* krow = b.qk + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
     float* n0row = b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
     float* n1row = b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
+    if (g.op == OP_LINEAR) {
+      // one relation: Q = X A^T and K = Y A are formed afterwards as
+      // contractions over the whole step, from these raw rows
+      row_store(y, n0row, d, dp, cplx, lane);
+      row_store(x, n1row, d, dp, cplx, lane);
+      if (lane == 0) b.bias[(int64_t)c * g.C + e] = 0.0f;
+      return;
+    }
+    Row gq = op_forward(g.op, x, th);
     if (g.cmp == CMP_DOT) {
       Row k;
-      if (g.op == OP_LINEAR) mat_apply(k, b.relp + (int64_t)r * d * d, y, st, d, lane);   // A^T y
-      else if (g.op == OP_TRANSLATION) k = y;
+      if (g.op == OP_TRANSLATION) k = y;
       else k = op_adjoint(g.op, y, th);
       const float p = row_dot(gq, y);
       const float bs = g.op == OP_TRANSLATION ? row_dot(th, y) : 0.0f;
@@ -110,6 +115,30 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b, 
   }
 }
 
+// the single relation's matrix A as row-padded copies A [d][dp] and A^T [d][dp]
+// (pad columns zero), the B operands of the linear operator's contractions
+__global__ void pad_linear_kernel(const float* A, int d, int dp, float* Ap, float* ATp) {
+  const int n = d * dp;
+  for (int idx = blockIdx.x * blockDim.x + threadIdx.x; idx < n; idx += gridDim.x * blockDim.x) {
+    const int r = idx / dp, k = idx - r * dp;
+    Ap[idx] = k < d ? A[r * d + k] : 0.0f;
+    ATp[idx] = k < d ? A[k * d + r] : 0.0f;
+  }
+}
+
+// p_e = <Q_e, x_d,e> once Q has been formed by contraction (linear operator)
+__global__ __launch_bounds__(256) void positive_scores_kernel(StepGeom g, StepBufs b) {
+  const int lane = threadIdx.x & 63;
+  const int c = blockIdx.y;
+  const int e = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (e >= chunk_edges(g, c)) return;
+  Row q, y;
+  row_load(q, b.qk + ((int64_t)(c * 2 + 0) * g.C + e) * g.dp, g.d, false, lane);
+  row_load(y, b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * g.dp, g.d, false, lane);
+  const float p = row_dot(q, y);
+  if (lane == 0) b.pos[(int64_t)c * g.C + e] = p;
+}
+
 // row-major d x d matrices -> transposed copies (linear operator)
 __global__ void transpose_rel_kernel(const float* A, float* AT, int R, int d) {
   const int64_t n = (int64_t)R * d * d;
@@ -134,4 +163,16 @@ void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s
   int blocks = (int)((n + 255) / 256);
   if (blocks > 4096) blocks = 4096;
   transpose_rel_kernel<<<blocks, 256, 0, s>>>(A, AT, R, d);
+}
+
+void launch_pad_linear(const float* A, int d, int dp, float* Ap, float* ATp, hipStream_t s) {
+  const int n = d * dp;
+  int blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  pad_linear_kernel<<<blocks, 256, 0, s>>>(A, d, dp, Ap, ATp);
+}
+
+void launch_positive_scores(const StepGeom& g, const StepBufs& b, hipStream_t s) {
+  dim3 grid((g.C + 3) / 4, g.nchunks);
+  positive_scores_kernel<<<grid, 256, 0, s>>>(g, b);
 }

@@ -275,7 +275,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int tiles_n, 
 #pragma unroll
           for (int j = 0; j < JN; ++j) {
             const int n = colb + 16 * j;
-            if (n < N) Cm[(int64_t)m * a.ldc + n] = acc[i][j][r];
+            if (n < N) {
+              float* o = Cm + (int64_t)m * a.ldc + n;
+              *o = a.accumulate ? *o + acc[i][j][r] : acc[i][j][r];
+            }
           }
         }
       }
@@ -314,8 +317,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int tiles_n, 
               lsum += zz;
             }
           } else if (valid) {
-            dsv = sigmoidf(s) * kinv;
-            lsum += softplusf(s) * kinv;
+            float sg, sp;
+            logistic_pair(s, sg, sp);
+            dsv = sg * kinv;
+            lsum += sp * kinv;
           }
           dsum += dsv;
           if (EPI == EPI_LOSS_BITS) {

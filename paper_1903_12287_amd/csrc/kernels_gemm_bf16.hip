@@ -278,8 +278,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a, int tiles_n
               lsum += zz;
             }
           } else if (valid) {
-            dsv = sigmoidf(s) * kinv;
-            lsum += softplusf(s) * kinv;
+            float sg, sp;
+            logistic_pair(s, sg, sp);
+            dsv = sg * kinv;
+            lsum += sp * kinv;
           }
           dsum += dsv;
           if (EPI == EPI_LOSS_BITS) {

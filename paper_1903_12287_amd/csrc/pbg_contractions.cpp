@@ -214,3 +214,55 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   na.kdim = DIM_CC;
   launch_gemm_bf16(na, EPI_STORE, nch * 2, cs);
 }
+
+// Linear operator with one relation (Sec. 4.3: with a single relation the
+// operator of a batch is one matrix product): Q = X A^T and K = Y A over all
+// chunks of the step, from the raw rows the gather left in the candidate
+// buffers (x_s is source candidate e, x_d destination candidate e), then the
+// positive scores.  Ap / ATp are A and A^T with rows padded to dp.
+static GemmArgs linear_args(const StepGeom& g, const float* A, int64_t a_cs, const float* B, float* Cm,
+                            int64_t c_cs) {
+  GemmArgs la;
+  memset(&la, 0, sizeof(la));
+  la.A = A;
+  la.B = B;
+  la.Cm = Cm;
+  la.a_cs = a_cs;
+  la.c_cs = c_cs;
+  la.lda = g.dp;
+  la.ldb = g.dp;
+  la.ldc = g.dp;
+  la.mdim = DIM_CC;
+  la.ndim = DIM_FIXED;
+  la.Nfix = g.d;
+  la.kdim = DIM_FIXED;
+  la.Kfix = g.d;
+  la.C = g.C;
+  la.U = g.U;
+  la.m_step = g.m_step;
+  la.nsides = 1;
+  return la;
+}
+
+void run_linear_forward(const StepGeom& g, const StepBufs& b, const float* Ap, const float* ATp, hipStream_t cs) {
+  const int64_t n_cs = 2ll * g.N * g.dp, q_cs = 2ll * g.C * g.dp;
+  GemmArgs q = linear_args(g, b.nn + (int64_t)g.N * g.dp, n_cs, Ap, b.qk, q_cs);     // Q = X A^T
+  launch_gemm_f32(q, GEMM_NT, EPI_STORE, g.nchunks, cs);
+  GemmArgs k = linear_args(g, b.nn, n_cs, ATp, b.qk + (int64_t)g.C * g.dp, q_cs);    // K = Y A
+  launch_gemm_f32(k, GEMM_NT, EPI_STORE, g.nchunks, cs);
+  launch_positive_scores(g, b, cs);
+}
+
+// the operator's part of the row gradients: source rows += dQ A (i.e. A^T dQ),
+// destination rows += dK A^T (i.e. A dK), added to the contributions that the
+// operator backward left in the candidate-gradient buffer
+void run_linear_backward(const StepGeom& g, const StepBufs& b, const float* Ap, const float* ATp,
+                         hipStream_t cs) {
+  const int64_t n_cs = 2ll * g.N * g.dp, q_cs = 2ll * g.C * g.dp;
+  GemmArgs s = linear_args(g, b.dq, q_cs, ATp, b.dn + (int64_t)g.N * g.dp, n_cs);
+  s.accumulate = 1;
+  launch_gemm_f32(s, GEMM_NT, EPI_STORE, g.nchunks, cs);
+  GemmArgs d = linear_args(g, b.dq + (int64_t)g.C * g.dp, q_cs, Ap, b.dn, n_cs);
+  d.accumulate = 1;
+  launch_gemm_f32(d, GEMM_NT, EPI_STORE, g.nchunks, cs);
+}

@@ -125,7 +125,10 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
     const int64_t w = linear ? 2 * s * (int64_t)d * d : s * RELSUM_PIECES * (int64_t)ctx->dr;
     ctx->relpartial = (float*)a.get(w * 4);
   }
-  if (linear) ctx->relT = (float*)a.get((int64_t)ctx->R * d * d * 4);
+  if (linear) {
+    ctx->relA = (float*)a.get((int64_t)d * dp * 4);
+    ctx->relAT = (float*)a.get((int64_t)d * dp * 4);
+  }
   ctx->flag_dev = (uint32_t*)a.get(16);
   ctx->h = BufsH();
   if (ctx->flags & PBG_F_BF16_SCORE) {
@@ -418,8 +421,9 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     b.rel = rel ? rel + c0 * C : nullptr;
 
     mark(t, 0);
-    if (linear) launch_transpose_rel(ctx->relp, ctx->relT, ctx->R, d, cs);
-    launch_gather(g, b, ctx->relT, cs);
+    if (linear) launch_pad_linear(ctx->relp, d, dp, ctx->relA, ctx->relAT, cs);
+    launch_gather(g, b, nullptr, cs);
+    if (linear) run_linear_forward(g, b, ctx->relA, ctx->relAT, cs);
     mark(t, 1);
 
     if (ctx->flags & PBG_F_BF16_SCORE) {
@@ -429,7 +433,8 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     }
 
     mark(t, 4);
-    launch_op_backward(g, b, ctx->relT, cs);
+    launch_op_backward(g, b, nullptr, cs);
+    if (linear) run_linear_backward(g, b, ctx->relA, ctx->relAT, cs);
     mark(t, 5);
 
     // entities: sort contribution rows by (table, row), segment sums, Adagrad

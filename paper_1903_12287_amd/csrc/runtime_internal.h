@@ -69,7 +69,8 @@ struct pbg_ctx {
   BufsH h{};
   SortWork sw{};
   float* relpartial = nullptr;
-  float* relT = nullptr;
+  float* relA = nullptr;    // linear operator: A and A^T, rows padded to dp
+  float* relAT = nullptr;
   uint32_t* flag_dev = nullptr;
   double* steploss_dev = nullptr;
   int64_t steploss_cap = 0;
@@ -88,6 +89,9 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
                           const std::function<void(int)>& mark);
 void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t,
                            hipStream_t cs, const std::function<void(int)>& mark);
+void run_linear_forward(const StepGeom& g, const StepBufs& b, const float* Ap, const float* ATp, hipStream_t cs);
+void run_linear_backward(const StepGeom& g, const StepBufs& b, const float* Ap, const float* ATp,
+                         hipStream_t cs);
 pbg_status hip_fail(pbg_ctx* ctx, hipError_t e, const char* what);
 bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width);
 pbg_status check_neg_config(pbg_ctx* ctx, const pbg_neg_config* neg);
