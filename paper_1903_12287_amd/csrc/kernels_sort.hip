@@ -250,7 +250,7 @@ template <int MODE, int RQ>
 __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, const uint32_t* keys,
                                                         const uint32_t* vals, int n, const float* rows,
                                                         int64_t ld, int width, float* partial, float lr) {
-  constexpr int SB = 64 / RQ;                      // positions per batch of loads
+  constexpr int SB = 32 / RQ;                      // positions per batch of loads
   const int lane = threadIdx.x & 63;
   const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int p0 = blk * SEG_BLOCK;
