@@ -82,7 +82,7 @@ void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld
                               hipStream_t s);
 
 // ---- gather / operator / negatives --------------------------------------------
-void launch_gather(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s);
+void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s);
 void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s);
 // linear operator (one relation): padded copies of A and A^T, and the positive
 // scores once Q has been formed by contraction
@@ -93,7 +93,7 @@ void launch_positive_scores(const StepGeom& g, const StepBufs& b, hipStream_t s)
 void launch_softmax_rows(const StepGeom& g, const StepBufs& b, hipStream_t s);
 void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s);
 void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, hipStream_t s);
-void launch_op_backward(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s);
+void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s);
 
 // ---- sort, segments, updates ----------------------------------------------------
 struct SortWork {

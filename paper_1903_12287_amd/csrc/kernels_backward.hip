@@ -103,8 +103,9 @@ __global__ void sum_chunks_kernel(const double* chunkloss, int n, double* out) {
 }
 
 // ---- operator / comparator backward: contributions and sort keys -----------
-__global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b, const float* relT) {
-  __shared__ float stage[4][512];
+template <int RQ>
+__global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b) {
+  using Row = RowT<RQ>;
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int c = blockIdx.y;
@@ -114,7 +115,6 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
   if (item >= Cc + 2 * g.U) return;   // no block-level barriers below
   const bool cplx = g.op == OP_COMPLEX;
   const int d = g.d, dp = g.dp;
-  float* st = stage[w];
   const bool cos = g.cmp == CMP_COS;
   const bool has_rel = g.op != OP_IDENTITY;
   const uint32_t tbl_j = g.same_table ? 0u : 1u;
@@ -186,9 +186,8 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
       Row dYh = gn0;                                 // x^_d is destination candidate e and K^_e
       row_add(dYh, gq1);
       row_axpy(dYh, dpe, Q);
-      const Row dv = normalize_backward(Q, nq, dQh); // dL/dg(x_s)
-      if (g.op == OP_LINEAR) mat_apply(gs, b.relp + (int64_t)r * d * d, dv, st, d, lane);
-      else gs = op_adjoint(g.op, dv, th);
+      const Row dv = normalize_backward(Q, nq, dQh); // dL/dg(x_s)   (cos: never linear)
+      gs = op_adjoint(g.op, dv, th);
       gd = normalize_backward(Kv, ny, dYh);
       if (g.op == OP_TRANSLATION) {
         grel = dv;
@@ -228,17 +227,13 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     const float nv = b.nrm[(int64_t)(c * 2 + side) * g.N + tpos];
     Row dv = normalize_backward(vh, nv, gv);
     if (side == 1 && has_rel) {
-      // the single relation's operator was applied to this source candidate
+      // the single relation's operator (not linear) was applied to this source candidate
       Row th, x;
-      if (g.op == OP_LINEAR) {
-        mat_apply(dv, b.relp, dv, st, d, lane);
-      } else {
-        row_load(th, b.relp, d, cplx, lane);
-        row_load(x, b.emb_i + (int64_t)u * d, d, cplx, lane);
-        const Row grel = g.op == OP_TRANSLATION ? dv : op_param_grad(g.op, x, dv);
-        row_store(grel, b.relc + ((int64_t)c * g.N + g.C + k) * g.dr, d, g.dr, cplx, lane);
-        dv = op_adjoint(g.op, dv, th);
-      }
+      row_load(th, b.relp, d, cplx, lane);
+      row_load(x, b.emb_i + (int64_t)u * d, d, cplx, lane);
+      const Row grel = g.op == OP_TRANSLATION ? dv : op_param_grad(g.op, x, dv);
+      row_store(grel, b.relc + ((int64_t)c * g.N + g.C + k) * g.dr, d, g.dr, cplx, lane);
+      dv = op_adjoint(g.op, dv, th);
     }
     row_store(dv, dnr, d, dp, cplx, lane);
   }
@@ -261,7 +256,11 @@ void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slo
   sum_chunks_kernel<<<1, 64, 0, s>>>(b.chunkloss, g.nchunks, step_loss_slot);
 }
 
-void launch_op_backward(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s) {
+void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s) {
   dim3 grid((g.C + 2 * g.U + 3) / 4, g.nchunks);
-  op_backward_kernel<<<grid, 256, 0, s>>>(g, b, relT);
+  switch (row_width_for(g.d)) {
+    case 2: op_backward_kernel<2><<<grid, 256, 0, s>>>(g, b); break;
+    case 4: op_backward_kernel<4><<<grid, 256, 0, s>>>(g, b); break;
+    default: op_backward_kernel<8><<<grid, 256, 0, s>>>(g, b); break;
+  }
 }

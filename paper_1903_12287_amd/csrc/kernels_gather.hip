@@ -14,17 +14,16 @@
 
 namespace {
 
-__global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b, const float* relT) {
-  __shared__ float stage[4][512];
+template <int RQ>
+__global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) {
+  using Row = RowT<RQ>;
   const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
   const int c = blockIdx.y;
   const int Cc = chunk_edges(g, c);
-  const int item = blockIdx.x * 4 + w;
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
   const bool cplx = g.op == OP_COMPLEX;
   const bool active = item < Cc + 2 * g.U;
   const int d = g.d, dp = g.dp;
-  float* st = stage[w];
 
   if (!active) return;   // no block-level barriers below: idle waves may leave
   if (item < Cc) {
@@ -96,14 +95,10 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b, 
   float nv = 0.0f;
   if (g.cmp == CMP_COS) {
     if (side == 1 && g.op != OP_IDENTITY) {
-      // one relation: its operator is applied to every source candidate
-      if (g.op == OP_LINEAR) {
-        mat_apply(v, relT, v, st, d, lane);
-      } else {
-        Row th;
-        row_load(th, b.relp, d, cplx, lane);
-        v = op_forward(g.op, v, th);
-      }
+      // one relation (not linear): its operator is applied to every source candidate
+      Row th;
+      row_load(th, b.relp, d, cplx, lane);
+      v = op_forward(g.op, v, th);
     }
     nv = row_normalize(v);
   }
@@ -153,9 +148,13 @@ __global__ void transpose_rel_kernel(const float* A, float* AT, int R, int d) {
 
 }  // namespace
 
-void launch_gather(const StepGeom& g, const StepBufs& b, const float* relT, hipStream_t s) {
+void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s) {
   dim3 grid((g.C + 2 * g.U + 3) / 4, g.nchunks);
-  gather_op_kernel<<<grid, 256, 0, s>>>(g, b, relT);
+  switch (row_width_for(g.d)) {
+    case 2: gather_op_kernel<2><<<grid, 256, 0, s>>>(g, b); break;
+    case 4: gather_op_kernel<4><<<grid, 256, 0, s>>>(g, b); break;
+    default: gather_op_kernel<8><<<grid, 256, 0, s>>>(g, b); break;
+  }
 }
 
 void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s) {

@@ -422,7 +422,7 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
 
     mark(t, 0);
     if (linear) launch_pad_linear(ctx->relp, d, dp, ctx->relA, ctx->relAT, cs);
-    launch_gather(g, b, nullptr, cs);
+    launch_gather(g, b, cs);
     if (linear) run_linear_forward(g, b, ctx->relA, ctx->relAT, cs);
     mark(t, 1);
 
@@ -433,7 +433,7 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     }
 
     mark(t, 4);
-    launch_op_backward(g, b, nullptr, cs);
+    launch_op_backward(g, b, cs);
     if (linear) run_linear_backward(g, b, ctx->relA, ctx->relAT, cs);
     mark(t, 5);
 
