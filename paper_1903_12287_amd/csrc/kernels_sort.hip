@@ -206,9 +206,9 @@ __global__ __launch_bounds__(1024) void scan_single(const uint32_t* in, int n, u
 enum { SEG_ENTITY = 0, SEG_RELATION = 1 };
 
 // applies the summed gradient g of the segment with key `key`
-template <int MODE>
-__device__ __forceinline__ void seg_apply(const StepGeom& g, const StepBufs& b, uint32_t key, const Row& acc,
-                                          int width, float lr, int lane) {
+template <int MODE, int RQ>
+__device__ __forceinline__ void seg_apply(const StepGeom& g, const StepBufs& b, uint32_t key,
+                                          const RowT<RQ>& acc, int width, float lr, int lane) {
   if (MODE == SEG_ENTITY) {
     const uint32_t tbl = key >> g.rb;
     const uint32_t row = key & ((1u << g.rb) - 1u);
@@ -218,7 +218,7 @@ __device__ __forceinline__ void seg_apply(const StepGeom& g, const StepBufs& b, 
     const float Gn = *G + gg;
     const float scale = lr / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
 #pragma unroll
-    for (int q = 0; q < ROWQ; ++q) {
+    for (int q = 0; q < RQ; ++q) {
       const int f = lane + 64 * q;
       if (f < g.d) emb[f] -= scale * acc.v[q];
     }
@@ -227,7 +227,7 @@ __device__ __forceinline__ void seg_apply(const StepGeom& g, const StepBufs& b, 
     float* p = b.relp + (int64_t)key * width;
     float* G = b.relG + (int64_t)key * width;
 #pragma unroll
-    for (int q = 0; q < ROWQ; ++q) {
+    for (int q = 0; q < RQ; ++q) {
       const int f = lane + 64 * q;
       if (f < width) {
         const float gf = acc.v[q];
@@ -373,7 +373,7 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
 // segments that cross block boundaries, updated by the wave of the block
 // where they start: its last piece plus the leading piece of every following
 // block the segment covers, added in block order, 16 loads in flight
-template <int MODE>
+template <int MODE, int RQ>
 __global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, const uint32_t* keys, int n,
                                                        int width, const float* partial, float lr) {
   const int lane = threadIdx.x & 63;
@@ -400,17 +400,17 @@ __global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, c
     else z = mid;
   }
   const int nparts = 1 + (a - 1 - p1) / SEG_BLOCK + 1;   // block of s, then blocks p1, p1 + 32, ...
-  Row acc;
+  RowT<RQ> acc;
   row_zero(acc);
   for (int i0 = 0; i0 < nparts; i0 += 16) {
-    float t[16][ROWQ];
+    float t[16][RQ];
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const int i = i0 + u;
       const int at = i == 0 ? s : p1 + (i - 1) * SEG_BLOCK;
       const float* part = partial + (int64_t)at * width;
 #pragma unroll
-      for (int q = 0; q < ROWQ; ++q) {
+      for (int q = 0; q < RQ; ++q) {
         const int f = lane + 64 * q;
         t[u][q] = (i < nparts && f < width) ? part[f] : 0.0f;
       }
@@ -418,9 +418,9 @@ __global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, c
 #pragma unroll
     for (int u = 0; u < 16; ++u)
 #pragma unroll
-      for (int q = 0; q < ROWQ; ++q) acc.v[q] += t[u][q];
+      for (int q = 0; q < RQ; ++q) acc.v[q] += t[u][q];
   }
-  seg_apply<MODE>(g, b, key, acc, width, lr, lane);
+  seg_apply<MODE, RQ>(g, b, key, acc, width, lr, lane);
 }
 
 // First level of the single-relation gradient sum: block (c, piece) adds, in
@@ -550,13 +550,16 @@ static void seg_update(const StepGeom& g, const StepBufs& b, const uint32_t* key
                        const float* rows, int64_t ld, int width, SortWork& w, float lr, hipStream_t s) {
   if (n <= 0) return;
   const int blocks = (n + 4 * SEG_BLOCK - 1) / (4 * SEG_BLOCK);
-  if (width <= 128)
+  if (width <= 128) {
     seg_update_local<MODE, 2><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial, lr);
-  else if (width <= 256)
+    seg_update_span<MODE, 2><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, lr);
+  } else if (width <= 256) {
     seg_update_local<MODE, 4><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial, lr);
-  else
+    seg_update_span<MODE, 4><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, lr);
+  } else {
     seg_update_local<MODE, 8><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial, lr);
-  seg_update_span<MODE><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, lr);
+    seg_update_span<MODE, 8><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, lr);
+  }
 }
 
 void launch_entity_update(const StepGeom& g, const StepBufs& b, const uint32_t* keys, const uint32_t* vals,
