@@ -54,7 +54,9 @@ enum {
 };
 struct GemmArgsH {
   const uint16_t* A;
-  const uint16_t* B;
+  const uint16_t* B;     // planes pieces of B, b_ps elements apart
+  int planes;            // 1, or 3: the exact bf16 pieces of a float32 operand (A = bit matrix only)
+  int64_t b_ps;
   float* Cm;             // fp32 output (STORE, SOFTMAX_STATS)
   uint16_t* dsh;         // EPI_LOSS: dS rows in bf16 (strides c_*, ldc)
   uint16_t* dsb;         // EPI_LOSS_BITS output (as in GemmArgs)
@@ -80,6 +82,12 @@ void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld
                               uint16_t* dst, int64_t dst_bs, int ld_dst, uint16_t* dstT,
                               int64_t dstT_bs, int ld_T, int rows_p, int kp, int batches,
                               hipStream_t s);
+// fp32 rows [rows][ld_src] -> three planes (ps elements apart) of the exact
+// bf16 pieces x = h + m + l, each transposed to [kp][ld_T] with zero padding
+// up to rows_p rows (rows_p, ld_T multiples of 4)
+void launch_split3_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d, uint16_t* dstT,
+                             int64_t dstT_bs, int64_t ps, int ld_T, int rows_p, int kp, int batches,
+                             hipStream_t s);
 
 // ---- gather / operator / negatives --------------------------------------------
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s);

@@ -10,22 +10,32 @@
 // from its bit matrix (rows for dQ, columns for dN), otherwise from bf16 dS
 // rows (transposed on the way into LDS for dN), so no copy of dS^T exists.
 //
+// Float32 backward of the ranking loss on the same instruction: there dS is
+// 0 or 1, and a float32 operand x splits exactly into three bf16 pieces,
+// x = h + m + l (h = bf16(x), m = bf16(x - h), l = x - h - m, which needs at
+// most 8 significant bits).  Every product dS * piece is then exact and the
+// sums run in float32, so dS . N equals a float32 contraction up to the order
+// of the float32 additions.  The kernel takes B as PL = 3 planes (pieces) and
+// adds the three products into one accumulator.
+//
 // Layout and schedule follow the float32 kernel: 256-thread workgroups of
 // 2 x 2 waves on 128 x BN tiles, buffer loads with hardware zero-fill,
-// register prefetch one k-slice ahead, double-buffered LDS tiles [row][k]
-// (pitch 40 elements = 80 bytes: conflict-free 16-byte fragment reads), and
-// all tiles of one batch on one XCD.  A slice is 32 deep, one
+// register prefetch one k-slice ahead, double-buffered LDS tiles and all
+// tiles of one batch on one XCD.  A slice is 32 deep, one
 // v_mfma_f32_16x16x32_bf16 step: lane L feeds A[L % 16][8 (L / 16) + i] and
 // B[8 (L / 16) + i][L % 16], i = 0..7, one 16-byte LDS read each; the
 // accumulator holds D[4 (L / 16) + r][L % 16] in register r.
+// LDS tiles are [row][k], 32 bf16 (64 bytes) per row with no padding: the
+// 16-byte group q of row x is kept at group q ^ ((x >> 2) & 3), so that the
+// fragment reads of 16 consecutive rows and the tile stores of 16 rows x 4
+// groups each touch all 64 banks once.
 #include "kernels.h"
 #include "device_common.h"
 
 namespace {
 
 constexpr int BM = 128;
-constexpr int BK = 32;
-constexpr int PK = BK + 8;     // LDS pitch in bf16 elements
+constexpr int BK = 32;          // k per slice = bf16 elements per LDS tile row
 constexpr uint32_t OOB = 0x80000000u;
 
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
@@ -46,16 +56,31 @@ __device__ __forceinline__ uint16_t f_to_bf16(float x) {
   return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
+// x = h + m + l exactly, each piece a bf16 (returned in the low 16 bits):
+// h = bf16(x) leaves a remainder of at most 16 significant bits, m = bf16 of
+// that remainder leaves at most 8, which l holds exactly
+__device__ __forceinline__ void split3(float x, uint32_t* pc) {
+  const uint16_t h = f_to_bf16(x);
+  const float r1 = x - bf16_to_f(h);
+  const uint16_t m = f_to_bf16(r1);
+  pc[0] = h;
+  pc[1] = m;
+  pc[2] = f_to_bf16(r1 - bf16_to_f(m));
+}
+
 __device__ __forceinline__ int pick_dim(int sel, int fixed, int Cc, int Nc) {
   return sel == DIM_CC ? Cc : (sel == DIM_NC ? Nc : fixed);
 }
+
+// element offset of the 16-byte group q of row x in a swizzled LDS tile
+__device__ __forceinline__ int swz(int x, int q) { return x * BK + ((q ^ ((x >> 2) & 3)) << 3); }
 
 // 0.0 / 1.0 in bf16 for bits b and b+1 of v, packed low / high
 __device__ __forceinline__ uint32_t bits2(uint32_t v, int b) {
   return (((v >> b) & 1u) * 0x3F80u) | ((((v >> (b + 1)) & 1u) * 0x3F80u) << 16);
 }
 
-// One operand tile of TX rows x BK k as LDS [row][k] bf16 (pitch PK); each
+// One operand tile of TX rows x BK k as LDS [row][k] bf16 (swizzled); each
 // thread moves TX * BK / 8 / 256 groups of eight elements per slice.  Loaded
 // words stay raw in registers until the store, after the slice's matrix work.
 //   GA_KC        global [x][k] bf16, ld elements, k contiguous (zero-padded to 8)
@@ -68,7 +93,7 @@ __device__ __forceinline__ uint32_t bits2(uint32_t v, int b) {
 template <int TX, int MODE>
 struct TileH {
   static constexpr int LOADS = TX * BK / 8 / 256;
-  static constexpr int SIZE = TX * PK;
+  static constexpr int SIZE = TX * BK;
 
   __device__ static void load(u32x4* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
 #pragma unroll
@@ -105,11 +130,10 @@ struct TileH {
       if (MODE == GA_MC) {
         const int k = f / (TX / 8), xq = f % (TX / 8);
         const u32x4 v = r[q];
-        uint16_t* col = s + (8 * xq) * PK + k;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          col[(2 * i) * PK] = (uint16_t)(v[i] & 0xFFFFu);
-          col[(2 * i + 1) * PK] = (uint16_t)(v[i] >> 16);
+        for (int i = 0; i < 8; ++i) {
+          const int x = 8 * xq + i;
+          s[swz(x, k >> 3) + (k & 7)] = (uint16_t)((i & 1) ? (v[i >> 1] >> 16) : (v[i >> 1] & 0xFFFFu));
         }
       } else {
         const int x = f >> 2, kq = f & 3;
@@ -131,20 +155,20 @@ struct TileH {
           for (int i = 0; i < 8; ++i) h[i] = (gk + i < kdim) ? ((h[i] >> b) & 1u) * 0x3F80u : 0u;
           v = (u32x4){h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
         }
-        *(u32x4*)(s + x * PK + 8 * kq) = v;
+        *(u32x4*)(s + swz(x, kq)) = v;
       }
     }
   }
 };
 
-template <int BN, int AMODE, int EPI>
+template <int BN, int AMODE, int EPI, int PL>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a, int tiles_n, int tiles_m) {
   constexpr int WN = BN / 2;
   constexpr int JN = WN / 16;
   using TA = TileH<BM, AMODE>;
   using TB = TileH<BN, GA_KC>;
   __shared__ __align__(16) uint16_t As[2][TA::SIZE];
-  __shared__ __align__(16) uint16_t Bs[2][TB::SIZE];
+  __shared__ __align__(16) uint16_t Bs[2][PL][TB::SIZE];
   __shared__ float red[2][BM][2];
 
   const int tid = threadIdx.x;
@@ -196,35 +220,51 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a, int tiles_n
 #pragma unroll
     for (int j = 0; j < JN; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
 
-  u32x4 pa[TA::LOADS], pb[TB::LOADS];
+  // one plane resource per B piece (planes b_ps elements apart)
+  rsrc_t rb[PL];
+  rb[0] = rb_s;
+#pragma unroll
+  for (int p = 1; p < PL; ++p) rb[p] = make_rsrc(a.B + p * a.b_ps + c * a.b_cs + side * a.b_ss);
+
+  u32x4 pa[TA::LOADS], pb[PL][TB::LOADS];
   const int nk = (K + BK - 1) / BK;
   TA::load(pa, ra_s, a.lda, m0, M, 0, K, tid);
-  TB::load(pb, rb_s, a.ldb, n0, N, 0, K, tid);
+#pragma unroll
+  for (int p = 0; p < PL; ++p) TB::load(pb[p], rb[p], a.ldb, n0, N, 0, K, tid);
   TA::store(As[0], pa, tid, m0, 0, K);
-  TB::store(Bs[0], pb, tid, n0, 0, K);
+#pragma unroll
+  for (int p = 0; p < PL; ++p) TB::store(Bs[0][p], pb[p], tid, n0, 0, K);
   __syncthreads();
 
+  // fragment offsets: row 16 i + l16 of the wave's block, group g (swizzled)
+  const int fa0 = swz(64 * wm + l16, g), fb0 = swz(WN * wn + l16, g);
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
     if (kt + 1 < nk) {
       TA::load(pa, ra_s, a.lda, m0, M, (kt + 1) * BK, K, tid);
-      TB::load(pb, rb_s, a.ldb, n0, N, (kt + 1) * BK, K, tid);
+#pragma unroll
+      for (int p = 0; p < PL; ++p) TB::load(pb[p], rb[p], a.ldb, n0, N, (kt + 1) * BK, K, tid);
     }
     const uint16_t* as = As[buf];
-    const uint16_t* bs = Bs[buf];
-    v8bf af[4], bf[JN];
+    v8bf af[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = *(const v8bf*)(as + (64 * wm + 16 * i + l16) * PK + 8 * g);
+    for (int i = 0; i < 4; ++i) af[i] = *(const v8bf*)(as + fa0 + 16 * i * BK);
 #pragma unroll
-    for (int j = 0; j < JN; ++j) bf[j] = *(const v8bf*)(bs + (WN * wn + 16 * j + l16) * PK + 8 * g);
+    for (int p = 0; p < PL; ++p) {
+      const uint16_t* bs = Bs[buf][p];
+      v8bf bf[JN];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < JN; ++j) bf[j] = *(const v8bf*)(bs + fb0 + 16 * j * BK);
 #pragma unroll
-      for (int j = 0; j < JN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < JN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
     if (kt + 1 < nk) {
       TA::store(As[buf ^ 1], pa, tid, m0, (kt + 1) * BK, K);
-      TB::store(Bs[buf ^ 1], pb, tid, n0, (kt + 1) * BK, K);
+#pragma unroll
+      for (int p = 0; p < PL; ++p) TB::store(Bs[buf ^ 1][p], pb[p], tid, n0, (kt + 1) * BK, K);
     }
     __syncthreads();
   }
@@ -371,6 +411,44 @@ __global__ __launch_bounds__(256) void to_bf16_transpose_kernel(const float* src
   }
 }
 
+// fp32 rows -> the three exact bf16 pieces (h, m, l) of every element, each
+// transposed: plane p is [kp][ld_T] (source column, then source row), planes
+// ps elements apart; rows [rows, rows_p) and columns [d, kp) are zeros.
+// rows_p and ld_T are multiples of 4 (each thread writes four rows).
+__global__ __launch_bounds__(256) void split3_transpose_kernel(const float* src, int64_t src_bs, int rows,
+                                                               int ld_src, int d, uint16_t* dstT,
+                                                               int64_t dstT_bs, int64_t ps, int ld_T,
+                                                               int rows_p, int kp) {
+  __shared__ float tile[64][65];
+  const int b = blockIdx.z;
+  const int r0 = blockIdx.y * 64, k0 = blockIdx.x * 64;
+  const float* s = src + (int64_t)b * src_bs;
+  for (int q = threadIdx.x; q < 64 * 64; q += 256) {
+    const int rr = q >> 6, kk = q & 63;
+    const int r = r0 + rr, k = k0 + kk;
+    tile[rr][kk] = (r < rows && k < d) ? s[(int64_t)r * ld_src + k] : 0.0f;
+  }
+  __syncthreads();
+  uint16_t* o = dstT + (int64_t)b * dstT_bs;
+  for (int q = threadIdx.x; q < 64 * 16; q += 256) {
+    const int kk = q >> 4, r4 = 4 * (q & 15);
+    const int k = k0 + kk, r = r0 + r4;
+    if (k >= kp || r >= rows_p) continue;
+    uint32_t pc[3][2];
+#pragma unroll
+    for (int i = 0; i < 4; i += 2) {
+      uint32_t lo[3], hi[3];
+      split3(tile[r4 + i][kk], lo);
+      split3(tile[r4 + i + 1][kk], hi);
+#pragma unroll
+      for (int p = 0; p < 3; ++p) pc[p][i >> 1] = lo[p] | (hi[p] << 16);
+    }
+#pragma unroll
+    for (int p = 0; p < 3; ++p)
+      *(uint2*)(o + p * ps + (int64_t)k * ld_T + r) = make_uint2(pc[p][0], pc[p][1]);
+  }
+}
+
 // softmax row pass in bf16 mode: raw fp32 scores -> dS = softmax (masked),
 // written as bf16 rows and into the transposed copy
 __global__ __launch_bounds__(256) void softmax_rows_bf16_kernel(StepGeom g, const float* S, const float* rowpart,
@@ -409,14 +487,20 @@ __global__ __launch_bounds__(256) void softmax_rows_bf16_kernel(StepGeom g, cons
 }
 
 
-template <int BN, int AMODE, int EPI>
+template <int BN, int AMODE, int EPI, int PL = 1>
 void launch_t(const GemmArgsH& a, int tiles_n, int tiles_m, int batches, hipStream_t s) {
   const int64_t nwg = (int64_t)tiles_n * tiles_m * batches;
-  gemm_bf16_kernel<BN, AMODE, EPI><<<(unsigned)nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+  gemm_bf16_kernel<BN, AMODE, EPI, PL><<<(unsigned)nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
 }
 
 template <int BN>
 void launch_store(const GemmArgsH& a, int tiles_n, int tiles_m, int batches, hipStream_t s) {
+  if (a.planes == 3) {
+    // float32 operand as three exact pieces: only the 0/1 ranking dS as A
+    if (a.amode == GA_BITS_ROW) launch_t<BN, GA_BITS_ROW, EPI_STORE, 3>(a, tiles_n, tiles_m, batches, s);
+    else launch_t<BN, GA_BITS_COL, EPI_STORE, 3>(a, tiles_n, tiles_m, batches, s);
+    return;
+  }
   switch (a.amode) {
     case GA_KC: launch_t<BN, GA_KC, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
     case GA_MC: launch_t<BN, GA_MC, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
@@ -452,6 +536,14 @@ void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld
   dim3 grid((kp + 63) / 64, (rows_p + 63) / 64, batches);
   to_bf16_transpose_kernel<<<grid, 256, 0, s>>>(src, src_bs, rows, ld_src, d, dst, dst_bs, ld_dst, dstT,
                                                 dstT_bs, ld_T, rows_p, kp);
+}
+
+void launch_split3_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d, uint16_t* dstT,
+                             int64_t dstT_bs, int64_t ps, int ld_T, int rows_p, int kp, int batches,
+                             hipStream_t s) {
+  dim3 grid((kp + 63) / 64, (rows_p + 63) / 64, batches);
+  split3_transpose_kernel<<<grid, 256, 0, s>>>(src, src_bs, rows, ld_src, d, dstT, dstT_bs, ps, ld_T, rows_p,
+                                               kp);
 }
 
 void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s) {

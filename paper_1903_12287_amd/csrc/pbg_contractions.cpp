@@ -9,6 +9,68 @@
 
 static int rup(int v, int m) { return (v + m - 1) / m * m; }
 
+// dQ = dS . N and dN = dS^T . Q on the bf16 matrix instructions.  A is dS:
+// the ranking bit matrix (rows for dQ, columns for dN), else bf16 rows dsh.
+// B is N^T [f][t] / Q^T [f][e] in bf16, as `planes` pieces (1: bf16 operands;
+// 3: the exact pieces of the float32 operands, ranking only) n_ps / q_ps
+// elements apart.
+static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t* dsh, const uint16_t* nT,
+                           int64_t n_ps, const uint16_t* qT, int64_t q_ps, int planes, hipStream_t cs) {
+  const int C = g.C, N = g.N, dp = g.dp, Np = g.Np, nch = g.nchunks;
+  const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
+  const bool bits = g.loss == LOSS_RANKING;
+  const int nw = (Np + 15) / 16, ldw = rup(C, 8);
+  // dQ = dS . N:  A = dS (rows), B = N^T [f][t]
+  GemmArgsH qa;
+  memset(&qa, 0, sizeof(qa));
+  if (bits) {
+    qa.A = b.dsb;
+    qa.amode = GA_BITS_ROW;
+    qa.a_cs = 2ll * nw * ldw;
+    qa.a_ss = (int64_t)nw * ldw;
+    qa.lda = ldw;
+  } else {
+    qa.A = dsh;
+    qa.amode = GA_KC;
+    qa.a_cs = 2ll * C * Npb;
+    qa.a_ss = (int64_t)C * Npb;
+    qa.lda = Npb;
+  }
+  qa.B = nT;
+  qa.planes = planes;
+  qa.b_ps = n_ps;
+  qa.Cm = b.dq;
+  qa.b_cs = 2ll * dpb * Npb;
+  qa.b_ss = (int64_t)dpb * Npb;
+  qa.c_cs = 2ll * C * dp;
+  qa.c_ss = (int64_t)C * dp;
+  qa.ldb = Npb;
+  qa.ldc = dp;
+  qa.mdim = DIM_CC;
+  qa.ndim = DIM_FIXED;
+  qa.Nfix = dp;
+  qa.kdim = DIM_NC;
+  qa.C = C;
+  qa.U = g.U;
+  qa.m_step = g.m_step;
+  qa.nsides = 2;
+  launch_gemm_bf16(qa, EPI_STORE, nch * 2, cs);
+  // dN = dS^T . Q:  A = dS read by columns, B = Q^T [f][e]
+  GemmArgsH na = qa;
+  na.amode = bits ? GA_BITS_COL : GA_MC;
+  na.B = qT;
+  na.b_ps = q_ps;
+  na.Cm = b.dn;
+  na.b_cs = 2ll * dpb * Cpb;
+  na.b_ss = (int64_t)dpb * Cpb;
+  na.c_cs = 2ll * N * dp;
+  na.c_ss = (int64_t)N * dp;
+  na.ldb = Cpb;
+  na.mdim = DIM_NC;
+  na.kdim = DIM_CC;
+  launch_gemm_bf16(na, EPI_STORE, nch * 2, cs);
+}
+
 void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
                           const std::function<void(int)>& mark) {
   const int C = g.C, U = g.U, N = g.N, dp = g.dp, Np = g.Np, nch = g.nchunks;
@@ -58,6 +120,18 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   launch_finalize(g, b, ctx->steploss_dev + t, cs);
   mark(3);
 
+  if (bits) {
+    // dS is 0 or 1: exact products on the bf16 instructions with Q and N in
+    // three exact bf16 pieces each (float32 sums)
+    const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
+    const BufsH& h = ctx->h;
+    launch_split3_transpose(b.qk, (int64_t)C * dp, C, dp, g.d, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, Cpb,
+                            dpb, nch * 2, cs);
+    launch_split3_transpose(b.nn, (int64_t)N * dp, N, dp, g.d, h.nnT3, (int64_t)dpb * Npb, h.n3_ps, Npb, Npb,
+                            dpb, nch * 2, cs);
+    run_backward_h(g, b, nullptr, h.nnT3, h.n3_ps, h.qkT3, h.q3_ps, 3, cs);
+    return;
+  }
   // dQ = dS . N (per side)
   GemmArgs qa;
   memset(&qa, 0, sizeof(qa));
@@ -167,52 +241,7 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   launch_finalize(g, b, ctx->steploss_dev + t, cs);
   mark(3);
 
-  // dQ = dS . N:  A = dS (rows), B = N^T [f][t]
-  GemmArgsH qa;
-  memset(&qa, 0, sizeof(qa));
-  if (bits) {
-    qa.A = b.dsb;
-    qa.amode = GA_BITS_ROW;
-    qa.a_cs = 2ll * nw * ldw;
-    qa.a_ss = (int64_t)nw * ldw;
-    qa.lda = ldw;
-  } else {
-    qa.A = h.ds;
-    qa.amode = GA_KC;
-    qa.a_cs = 2ll * C * Npb;
-    qa.a_ss = (int64_t)C * Npb;
-    qa.lda = Npb;
-  }
-  qa.B = h.nnT;
-  qa.Cm = b.dq;
-  qa.b_cs = 2ll * dpb * Npb;
-  qa.b_ss = (int64_t)dpb * Npb;
-  qa.c_cs = 2ll * C * dp;
-  qa.c_ss = (int64_t)C * dp;
-  qa.ldb = Npb;
-  qa.ldc = dp;
-  qa.mdim = DIM_CC;
-  qa.ndim = DIM_FIXED;
-  qa.Nfix = dp;
-  qa.kdim = DIM_NC;
-  qa.C = C;
-  qa.U = U;
-  qa.m_step = g.m_step;
-  qa.nsides = 2;
-  launch_gemm_bf16(qa, EPI_STORE, nch * 2, cs);
-  // dN = dS^T . Q:  A = dS read by columns, B = Q^T [f][e]
-  GemmArgsH na = qa;
-  na.amode = bits ? GA_BITS_COL : GA_MC;
-  na.B = h.qkT;
-  na.Cm = b.dn;
-  na.b_cs = 2ll * dpb * Cpb;
-  na.b_ss = (int64_t)dpb * Cpb;
-  na.c_cs = 2ll * N * dp;
-  na.c_ss = (int64_t)N * dp;
-  na.ldb = Cpb;
-  na.mdim = DIM_NC;
-  na.kdim = DIM_CC;
-  launch_gemm_bf16(na, EPI_STORE, nch * 2, cs);
+  run_backward_h(g, b, h.ds, h.nnT, 0, h.qkT, 0, 1, cs);
 }
 
 // Linear operator with one relation (Sec. 4.3: with a single relation the

@@ -43,6 +43,11 @@ struct BufsH {
   uint16_t* qkT = nullptr;  // [S][2][dpb][Cpb]
   uint16_t* nnT = nullptr;  // [S][2][dpb][Npb]
   uint16_t* ds = nullptr;   // [S][2][C][Npb] dS rows (logistic, softmax)
+  // float32 ranking backward: the exact three-piece split of Q^T and N^T,
+  // [3][S][2][dpb][Cpb] and [3][S][2][dpb][Npb], planes q3_ps / n3_ps apart
+  uint16_t* qkT3 = nullptr;
+  uint16_t* nnT3 = nullptr;
+  int64_t q3_ps = 0, n3_ps = 0;
 };
 
 struct pbg_ctx {
