@@ -78,6 +78,9 @@ struct GemmArgsH {
 };
 
 void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s);
+// two EPI_STORE products in one launch: a0 with A as dS rows (GA_BITS_ROW or
+// GA_KC), a1 with A as dS columns (GA_BITS_COL or GA_MC), same planes
+void launch_gemm_bf16_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s);
 void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d,
                               uint16_t* dst, int64_t dst_bs, int ld_dst, uint16_t* dstT,
                               int64_t dstT_bs, int ld_T, int rows_p, int kp, int batches,

@@ -29,6 +29,8 @@
 // 16-byte group q of row x is kept at group q ^ ((x >> 2) & 3), so that the
 // fragment reads of 16 consecutive rows and the tile stores of 16 rows x 4
 // groups each touch all 64 banks once.
+#include <algorithm>
+
 #include "kernels.h"
 #include "device_common.h"
 
@@ -161,15 +163,26 @@ struct TileH {
   }
 };
 
+// LDS of one workgroup: double-buffered A tile and PL B tiles, row partials
+template <int BN, int PL>
+struct SmemH {
+  uint16_t As[2][BM * BK];
+  uint16_t Bs[2][PL][BN * BK];
+  float red[2][BM][2];
+};
+
+// One 128 x BN output tile; `id` numbers the workgroup among the nwg of this
+// product (hardware order), remapped so that each batch stays on one XCD.
 template <int BN, int AMODE, int EPI, int PL>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a, int tiles_n, int tiles_m) {
+__device__ __forceinline__ void gemm_bf16_tile(const GemmArgsH& a, int tiles_n, int tiles_m, int nwg, int id,
+                                               SmemH<BN, PL>& sm) {
   constexpr int WN = BN / 2;
   constexpr int JN = WN / 16;
   using TA = TileH<BM, AMODE>;
   using TB = TileH<BN, GA_KC>;
-  __shared__ __align__(16) uint16_t As[2][TA::SIZE];
-  __shared__ __align__(16) uint16_t Bs[2][PL][TB::SIZE];
-  __shared__ float red[2][BM][2];
+  auto& As = sm.As;
+  auto& Bs = sm.Bs;
+  auto& red = sm.red;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -177,7 +190,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a, int tiles_n
   const int wm = w >> 1, wn = w & 1;
   const int l16 = lane & 15, g = lane >> 4;
 
-  const int nwg = gridDim.x, id = blockIdx.x;
   const int q8 = nwg >> 3, r8 = nwg & 7, xcd = id & 7;
   const int lid = xcd * q8 + min(xcd, r8) + (id >> 3);
   const int tn = lid % tiles_n;
@@ -381,6 +393,24 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a, int tiles_n
   }
 }
 
+template <int BN, int AMODE, int EPI, int PL>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a, int tiles_n, int tiles_m) {
+  __shared__ __align__(16) SmemH<BN, PL> sm;
+  gemm_bf16_tile<BN, AMODE, EPI, PL>(a, tiles_n, tiles_m, gridDim.x, blockIdx.x, sm);
+}
+
+// two independent products in one launch (dQ and dN of a step): workgroups
+// [0, nwg0) take the first, the rest the second, so that the long-k tiles of
+// the first start first and the short ones of the second fill in behind them
+template <int BN, int AM0, int AM1, int PL>
+__global__ __launch_bounds__(256) void gemm_bf16_pair_kernel(GemmArgsH a0, int tn0, int tm0, int nwg0,
+                                                             GemmArgsH a1, int tn1, int tm1) {
+  __shared__ __align__(16) SmemH<BN, PL> sm;
+  const int id = blockIdx.x;
+  if (id < nwg0) gemm_bf16_tile<BN, AM0, EPI_STORE, PL>(a0, tn0, tm0, nwg0, id, sm);
+  else gemm_bf16_tile<BN, AM1, EPI_STORE, PL>(a1, tn1, tm1, (int)gridDim.x - nwg0, id - nwg0, sm);
+}
+
 // fp32 packed rows -> bf16 rows (zero-padded to kp) and the transposed copy
 // [kp][rows_p]: 64 x 64 tiles through LDS, coalesced on both sides.
 __global__ __launch_bounds__(256) void to_bf16_transpose_kernel(const float* src, int64_t src_bs,
@@ -527,6 +557,33 @@ void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s) {
   }
   if (maxN <= 64) launch_store<64>(a, (maxN + 63) / 64, tiles_m, batches, s);
   else launch_store<128>(a, (maxN + 127) / 128, tiles_m, batches, s);
+}
+
+namespace {
+template <int BN, int AM0, int AM1, int PL>
+void launch_pair_t(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s) {
+  const int tn0 = (dim_max(a0.ndim, a0.Nfix, a0.C, a0.U) + BN - 1) / BN;
+  const int tm0 = (dim_max(a0.mdim, a0.Mfix, a0.C, a0.U) + BM - 1) / BM;
+  const int tn1 = (dim_max(a1.ndim, a1.Nfix, a1.C, a1.U) + BN - 1) / BN;
+  const int tm1 = (dim_max(a1.mdim, a1.Mfix, a1.C, a1.U) + BM - 1) / BM;
+  const int64_t nwg0 = (int64_t)tn0 * tm0 * batches, nwg1 = (int64_t)tn1 * tm1 * batches;
+  gemm_bf16_pair_kernel<BN, AM0, AM1, PL><<<(unsigned)(nwg0 + nwg1), 256, 0, s>>>(a0, tn0, tm0, (int)nwg0, a1,
+                                                                                 tn1, tm1);
+}
+
+template <int BN>
+void launch_pair_bn(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s) {
+  if (a0.planes == 3) launch_pair_t<BN, GA_BITS_ROW, GA_BITS_COL, 3>(a0, a1, batches, s);
+  else if (a0.amode == GA_BITS_ROW) launch_pair_t<BN, GA_BITS_ROW, GA_BITS_COL, 1>(a0, a1, batches, s);
+  else launch_pair_t<BN, GA_KC, GA_MC, 1>(a0, a1, batches, s);
+}
+}  // namespace
+
+void launch_gemm_bf16_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s) {
+  const int maxN = std::max(dim_max(a0.ndim, a0.Nfix, a0.C, a0.U), dim_max(a1.ndim, a1.Nfix, a1.C, a1.U));
+  if (maxN <= 0 || batches <= 0) return;
+  if (maxN <= 64) launch_pair_bn<64>(a0, a1, batches, s);
+  else launch_pair_bn<128>(a0, a1, batches, s);
 }
 
 void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d,

@@ -54,7 +54,6 @@ static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t*
   qa.U = g.U;
   qa.m_step = g.m_step;
   qa.nsides = 2;
-  launch_gemm_bf16(qa, EPI_STORE, nch * 2, cs);
   // dN = dS^T . Q:  A = dS read by columns, B = Q^T [f][e]
   GemmArgsH na = qa;
   na.amode = bits ? GA_BITS_COL : GA_MC;
@@ -68,7 +67,7 @@ static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t*
   na.ldb = Cpb;
   na.mdim = DIM_NC;
   na.kdim = DIM_CC;
-  launch_gemm_bf16(na, EPI_STORE, nch * 2, cs);
+  launch_gemm_bf16_pair(qa, na, nch * 2, cs);
 }
 
 void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
