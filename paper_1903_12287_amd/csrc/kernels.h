@@ -57,6 +57,8 @@ struct GemmArgsH {
   const uint16_t* B;     // planes pieces of B, b_ps elements apart
   int planes;            // 1, or 3: the exact bf16 pieces of a float32 operand (A = bit matrix only)
   int64_t b_ps;
+  const float* Af;       // launch_score_split: float32 operands [m][k] and [n][k]
+  const float* Bf;
   float* Cm;             // fp32 output (STORE, SOFTMAX_STATS)
   uint16_t* dsh;         // EPI_LOSS: dS rows in bf16 (strides c_*, ldc)
   uint16_t* dsb;         // EPI_LOSS_BITS output (as in GemmArgs)
@@ -78,6 +80,10 @@ struct GemmArgsH {
 };
 
 void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s);
+// float32 score contraction with its loss epilogue (EPI_LOSS: float32 dS in
+// Cm; EPI_LOSS_BITS; EPI_SOFTMAX_STATS) on the bf16 instructions, operands
+// Af / Bf split into exact bf16 pieces on the way into LDS
+void launch_score_split(const GemmArgsH& a, int epi, int batches, hipStream_t s);
 // two EPI_STORE products in one launch: a0 with A as dS rows (GA_BITS_ROW or
 // GA_KC), a1 with A as dS columns (GA_BITS_COL or GA_MC), same planes
 void launch_gemm_bf16_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s);
@@ -85,12 +91,13 @@ void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld
                               uint16_t* dst, int64_t dst_bs, int ld_dst, uint16_t* dstT,
                               int64_t dstT_bs, int ld_T, int rows_p, int kp, int batches,
                               hipStream_t s);
-// fp32 rows [rows][ld_src] -> three planes (ps elements apart) of the exact
-// bf16 pieces x = h + m + l, each transposed to [kp][ld_T] with zero padding
-// up to rows_p rows (rows_p, ld_T multiples of 4)
-void launch_split3_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d, uint16_t* dstT,
-                             int64_t dstT_bs, int64_t ps, int ld_T, int rows_p, int kp, int batches,
-                             hipStream_t s);
+// fp32 rows [rows][ld_src] -> the exact bf16 pieces x = h + m + l as three
+// row-major planes [rows][ld_R] (psR elements apart) and / or three
+// transposed planes [kp][ld_T] with zero rows up to rows_p (psT apart); a
+// null output is skipped.  kp, ld_R, rows_p, ld_T are multiples of 4.
+void launch_split3_planes(const float* src, int64_t src_bs, int rows, int ld_src, int d, uint16_t* dstR,
+                          int64_t dstR_bs, int64_t psR, int ld_R, uint16_t* dstT, int64_t dstT_bs, int64_t psT,
+                          int ld_T, int rows_p, int kp, int batches, hipStream_t s);
 
 // ---- gather / operator / negatives --------------------------------------------
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s);

@@ -52,22 +52,26 @@ __device__ __forceinline__ u32x4 bload16(rsrc_t r, uint32_t off) {
 
 __device__ __forceinline__ float bf16_to_f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-__device__ __forceinline__ uint16_t f_to_bf16(float x) {
-  // round to nearest even (finite inputs)
-  const uint32_t u = __float_as_uint(x);
-  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// round to nearest even (v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint16_t f_to_bf16(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
+
+// two floats -> one packed bf16 pair (a in the low half), round to nearest even
+__device__ __forceinline__ uint32_t f2_to_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, (bf16x2_t){(__bf16)a, (__bf16)b});
 }
 
-// x = h + m + l exactly, each piece a bf16 (returned in the low 16 bits):
-// h = bf16(x) leaves a remainder of at most 16 significant bits, m = bf16 of
-// that remainder leaves at most 8, which l holds exactly
-__device__ __forceinline__ void split3(float x, uint32_t* pc) {
-  const uint16_t h = f_to_bf16(x);
-  const float r1 = x - bf16_to_f(h);
-  const uint16_t m = f_to_bf16(r1);
+// x = h + m + l exactly, each piece a bf16: h = bf16(x) leaves a remainder of
+// at most 16 significant bits, m = bf16 of that remainder leaves at most 8,
+// which l holds exactly.  Two floats at a time: pc[0..2] = packed h, m, l.
+__device__ __forceinline__ void split3_pair(float a, float b, uint32_t* pc) {
+  const uint32_t h = f2_to_bf16x2(a, b);
+  const float ra = a - __uint_as_float(h << 16), rb = b - __uint_as_float(h & 0xFFFF0000u);
+  const uint32_t m = f2_to_bf16x2(ra, rb);
   pc[0] = h;
   pc[1] = m;
-  pc[2] = f_to_bf16(r1 - bf16_to_f(m));
+  pc[2] = f2_to_bf16x2(ra - __uint_as_float(m << 16), rb - __uint_as_float(m & 0xFFFF0000u));
 }
 
 __device__ __forceinline__ int pick_dim(int sel, int fixed, int Cc, int Nc) {
@@ -169,10 +173,240 @@ struct SmemH {
   uint16_t As[2][BM * BK];
   uint16_t Bs[2][PL][BN * BK];
   float red[2][BM][2];
+  float rowv[BM][2];
 };
 
-// One 128 x BN output tile; `id` numbers the workgroup among the nwg of this
-// product (hardware order), remapped so that each batch stays on one XCD.
+// Position of a workgroup's 128 x BN tile: `id` numbers the workgroup among
+// the nwg of its product (hardware order) and is remapped so that all tiles of
+// one batch (chunk, side) run on one XCD.
+struct TileGeo {
+  int c, side, Nc, M, N, K, m0, n0, tn;
+};
+
+// false: nothing to compute (the tile lies beyond this batch's rows, or beyond
+// its columns, where a loss epilogue still leaves neutral row partials)
+template <int BN, int EPI>
+__device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int tiles_m, int nwg, int id,
+                                         TileGeo& t) {
+  const int q8 = nwg >> 3, r8 = nwg & 7, xcd = id & 7;
+  const int lid = xcd * q8 + min(xcd, r8) + (id >> 3);
+  t.tn = lid % tiles_n;
+  const int rest = lid / tiles_n;
+  const int tm = rest % tiles_m;
+  const int z = rest / tiles_m;
+  t.c = z / a.nsides;
+  t.side = z - t.c * a.nsides;
+  int Cc = a.C;
+  t.Nc = a.C + a.U;
+  if (a.m_step > 0) {
+    Cc = min(a.C, a.m_step - t.c * a.C);
+    t.Nc = Cc + a.U;
+  }
+  t.M = pick_dim(a.mdim, a.Mfix, Cc, t.Nc);
+  t.N = pick_dim(a.ndim, a.Nfix, Cc, t.Nc);
+  t.K = pick_dim(a.kdim, a.Kfix, Cc, t.Nc);
+  t.m0 = tm * BM;
+  t.n0 = t.tn * BN;
+  if (t.m0 >= t.M) return false;
+  if (t.n0 >= t.N) {
+    const int tid = threadIdx.x;
+    if (EPI != EPI_STORE && tid < BM && t.m0 + tid < t.M) {
+      float* rp = a.rowpart + (((int64_t)(t.c * 2 + t.side) * a.C + t.m0 + tid) * a.nct + t.tn) * 2;
+      rp[0] = (EPI == EPI_SOFTMAX_STATS) ? -INFINITY : 0.0f;
+      rp[1] = 0.0f;
+    }
+    return false;
+  }
+  return true;
+}
+
+// positive score and bias of the tile's rows, for the loss epilogues (read
+// once at the start of the tile, while its first operands load)
+__device__ __forceinline__ void load_rowv(const GemmArgsH& a, const TileGeo& t, float (&rowv)[BM][2]) {
+  const int tid = threadIdx.x;
+  if (tid < BM) {
+    const int m = t.m0 + tid;
+    const bool mrow = m < t.M;
+    const int64_t o = (int64_t)t.c * a.C + m;
+    rowv[tid][0] = mrow ? a.pos[o] : 0.0f;
+    rowv[tid][1] = (mrow && a.bias && t.side == 1) ? a.bias[o] : 0.0f;
+  }
+}
+
+// Stores the tile (EPI_STORE) or runs the loss epilogue on it: dS leaves as
+// bits (ranking), as bf16 rows (logistic, when dsh is set) or float32 rows in
+// Cm, or the raw float32 scores go to Cm for the softmax row pass; row
+// partials (loss, dS sum / max, sum exp) are combined over the tile's two
+// column halves and written per column tile.
+template <int BN, int EPI>
+__device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[4][BN / 32],
+                                              float (&red)[2][BM][2], const float (&rowv)[BM][2]) {
+  constexpr int WN = BN / 2;
+  constexpr int JN = WN / 16;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int c = t.c, side = t.side, M = t.M, N = t.N, Nc = t.Nc, m0 = t.m0, n0 = t.n0;
+  const int colb = n0 + WN * wn + l16;
+  if (EPI == EPI_STORE) {
+    float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
+        if (m < M) {
+#pragma unroll
+          for (int j = 0; j < JN; ++j) {
+            const int n = colb + 16 * j;
+            if (n < N) Cm[(int64_t)m * a.ldc + n] = acc[i][j][r];
+          }
+        }
+      }
+    return;
+  }
+
+  const float kinv = (Nc - 1 > 0) ? 1.0f / (float)(Nc - 1) : 0.0f;
+  // column tiles past the batch's last column and the tile that holds the
+  // masked diagonal (m0 == n0 as BM == BN) need per-element checks
+  const bool ragged = n0 + BN > N;
+  const bool diag = m0 == n0;
+  if (EPI == EPI_LOSS_BITS) {
+    // hinge z = s + margin - p (> 0: dS = 1); each lane group's ballot word
+    // is the bit-matrix word of its row for these 16 columns, and its
+    // population count that row's share of the dS row sum
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int mb = 64 * wm + 16 * i + 4 * g;   // first of this lane group's four rows
+      float thr[4], ls[4];
+      uint32_t cnt[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        thr[r] = (m0 + mb + r < M) ? a.margin - rowv[mb + r][0] + rowv[mb + r][1] : -INFINITY;
+        ls[r] = 0.0f;
+        cnt[r] = 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < JN; ++j) {
+        const int n = colb + 16 * j;
+        uint32_t wd[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float z = acc[i][j][r] + thr[r];
+          if ((ragged && n >= N) || (diag && n == m0 + mb + r)) z = -INFINITY;
+          const uint64_t mk = __ballot(z > 0.0f);
+          ls[r] += fmaxf(z, 0.0f);
+          wd[r] = (uint32_t)(mk >> (16 * g)) & 0xFFFFu;
+          cnt[r] += __builtin_popcount(wd[r]);
+        }
+        // the words of four consecutive rows are adjacent (word-column major)
+        const int wcol = (n0 + WN * wn + 16 * j) >> 4;
+        if (l16 == 0 && m0 + mb < M && wcol < a.nwcb)
+          *(uint2*)(a.dsb + c * a.cb_cs + side * a.cb_ss + (int64_t)wcol * a.ldcb + m0 + mb) =
+              make_uint2(wd[0] | (wd[1] << 16), wd[2] | (wd[3] << 16));
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float v0 = group16_sum(ls[r]);
+        if (l16 == 0) {
+          red[wn][mb + r][0] = v0;
+          red[wn][mb + r][1] = (float)cnt[r];
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int ml = 64 * wm + 16 * i + 4 * g + r;
+        const int m = m0 + ml;
+        const bool mrow = m < M;
+        const float p = rowv[ml][0];
+        const float bm = rowv[ml][1];
+        float v0, v1;
+        if (EPI == EPI_LOSS) {
+          float lsum = 0.0f, dsum = 0.0f;
+#pragma unroll
+          for (int j = 0; j < JN; ++j) {
+            const int n = colb + 16 * j;
+            const float s = acc[i][j][r] + bm;
+            const bool valid = mrow && !(ragged && n >= N) && !(diag && n == m);
+            float dsv = 0.0f;
+            if (valid) {
+              if (a.loss == LOSS_RANKING) {
+                const float zz = a.margin - p + s;
+                if (zz > 0.0f) {
+                  dsv = 1.0f;
+                  lsum += zz;
+                }
+              } else {
+                float sg, sp;
+                logistic_pair(s, sg, sp);
+                dsv = sg * kinv;
+                lsum += sp * kinv;
+              }
+            }
+            dsum += dsv;
+            if (mrow && n < a.ldc) {
+              const int64_t o = c * a.c_cs + side * a.c_ss + (int64_t)m * a.ldc + n;
+              if (a.dsh) a.dsh[o] = f_to_bf16(dsv);
+              else a.Cm[o] = dsv;
+            }
+          }
+          v0 = group16_sum(lsum);
+          v1 = group16_sum(dsum);
+        } else {  // EPI_SOFTMAX_STATS
+          float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
+          float mx = -INFINITY;
+#pragma unroll
+          for (int j = 0; j < JN; ++j) {
+            const int n = colb + 16 * j;
+            const float s = acc[i][j][r] + bm;
+            if (mrow && !(ragged && n >= N) && !(diag && n == m)) mx = fmaxf(mx, s);
+            if (mrow && n < a.ldc) Cm[(int64_t)m * a.ldc + n] = s;
+          }
+          mx = group16_max(mx);
+          float se = 0.0f;
+#pragma unroll
+          for (int j = 0; j < JN; ++j) {
+            const int n = colb + 16 * j;
+            if (mrow && !(ragged && n >= N) && !(diag && n == m)) se += expf(acc[i][j][r] + bm - mx);
+          }
+          v0 = mx;
+          v1 = group16_sum(se);
+        }
+        if (l16 == 0) {
+          red[wn][ml][0] = v0;
+          red[wn][ml][1] = v1;
+        }
+      }
+  }
+  __syncthreads();
+  if (tid < BM && m0 + tid < M) {
+    const int ml = tid;
+    float v0, v1;
+    if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
+      v0 = red[0][ml][0] + red[1][ml][0];
+      v1 = red[0][ml][1] + red[1][ml][1];
+    } else {
+      const float ma = red[0][ml][0], mb = red[1][ml][0];
+      const float mx = fmaxf(ma, mb);
+      v0 = mx;
+      v1 = (mx == -INFINITY) ? 0.0f
+                             : (ma == -INFINITY ? 0.0f : red[0][ml][1] * expf(ma - mx)) +
+                                   (mb == -INFINITY ? 0.0f : red[1][ml][1] * expf(mb - mx));
+    }
+    float* rp = a.rowpart + (((int64_t)(c * 2 + side) * a.C + m0 + ml) * a.nct + t.tn) * 2;
+    rp[0] = v0;
+    rp[1] = v1;
+  }
+}
+
+
+// One 128 x BN output tile of A . B with bf16 operands (B in PL planes).
 template <int BN, int AMODE, int EPI, int PL>
 __device__ __forceinline__ void gemm_bf16_tile(const GemmArgsH& a, int tiles_n, int tiles_m, int nwg, int id,
                                                SmemH<BN, PL>& sm) {
@@ -182,46 +416,15 @@ __device__ __forceinline__ void gemm_bf16_tile(const GemmArgsH& a, int tiles_n, 
   using TB = TileH<BN, GA_KC>;
   auto& As = sm.As;
   auto& Bs = sm.Bs;
-  auto& red = sm.red;
-
+  TileGeo t;
+  if (!tile_geo<BN, EPI>(a, tiles_n, tiles_m, nwg, id, t)) return;
+  if (EPI != EPI_STORE) load_rowv(a, t, sm.rowv);
+  const int c = t.c, side = t.side, M = t.M, N = t.N, K = t.K, m0 = t.m0, n0 = t.n0;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
   const int wm = w >> 1, wn = w & 1;
   const int l16 = lane & 15, g = lane >> 4;
-
-  const int q8 = nwg >> 3, r8 = nwg & 7, xcd = id & 7;
-  const int lid = xcd * q8 + min(xcd, r8) + (id >> 3);
-  const int tn = lid % tiles_n;
-  const int rest = lid / tiles_n;
-  const int tm = rest % tiles_m;
-  const int z = rest / tiles_m;
-
-  const int c = z / a.nsides;
-  const int side = z - c * a.nsides;
-  int Cc = a.C, Nc = a.C + a.U;
-  if (a.m_step > 0) {
-    Cc = min(a.C, a.m_step - c * a.C);
-    Nc = Cc + a.U;
-  }
-  const int M = pick_dim(a.mdim, a.Mfix, Cc, Nc);
-  const int N = pick_dim(a.ndim, a.Nfix, Cc, Nc);
-  const int K = pick_dim(a.kdim, a.Kfix, Cc, Nc);
-  const int m0 = tm * BM;
-  const int n0 = tn * BN;
-  if (m0 >= M) return;
-
-  float* rowpart = nullptr;
-  if (EPI != EPI_STORE) rowpart = a.rowpart + ((int64_t)(c * 2 + side) * a.C) * a.nct * 2;
-  if (n0 >= N) {
-    // neutral row partials: no valid column in this tile
-    if (EPI != EPI_STORE && tid < BM && m0 + tid < M) {
-      float* rp = rowpart + ((int64_t)(m0 + tid) * a.nct + tn) * 2;
-      rp[0] = (EPI == EPI_SOFTMAX_STATS) ? -INFINITY : 0.0f;
-      rp[1] = 0.0f;
-    }
-    return;
-  }
 
   const rsrc_t ra_s = make_rsrc(a.A + c * a.a_cs + side * a.a_ss);
   const rsrc_t rb_s = make_rsrc(a.B + c * a.b_cs + side * a.b_ss);
@@ -281,116 +484,137 @@ __device__ __forceinline__ void gemm_bf16_tile(const GemmArgsH& a, int tiles_n, 
     __syncthreads();
   }
 
-  const int colb = n0 + WN * wn + l16;
-  if (EPI == EPI_STORE) {
-    float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
+  tile_epilogue<BN, EPI>(a, t, acc, sm.red, sm.rowv);
+}
+
+// ---- float32 score contraction on the bf16 instructions --------------------
+// S = Q . N^T with both operands float32: each element is split exactly into
+// three bf16 pieces (x = h + m + l, as in split3_pair) when its tile is stored to
+// LDS, and the tile is the sum of the piece products.  NPROD = 9 takes all
+// nine, so every product is exact and only the float32 sums round; NPROD = 6
+// leaves out m.l, l.m and l.l, whose sum is at most about 2^-23 |a| |b| per
+// term (|m| <= 2^-8 |x|, |l| <= 2^-16 |x|), below the rounding bound of a
+// float32 dot product of the same length.
+
+// TX rows x 32 k of a float32 [x][k] matrix (k contiguous, ld floats): each
+// thread moves groups of eight floats (two 16-byte loads) and stores their
+// three pieces to three LDS planes (swizzled [row][k] bf16 tiles).
+template <int TX>
+struct TileS {
+  static constexpr int LOADS = TX * BK / 8 / 256;   // groups of eight per thread
+
+  __device__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
+    const int k4 = (kdim + 3) & ~3;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
-        if (m < M) {
-#pragma unroll
-          for (int j = 0; j < JN; ++j) {
-            const int n = colb + 16 * j;
-            if (n < N) Cm[(int64_t)m * a.ldc + n] = acc[i][j][r];
-          }
-        }
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      const int x = f >> 2, kq = f & 3;
+      const int gx = x0 + x, gk = k0 + 8 * kq;
+      uint32_t o0 = OOB, o1 = OOB;
+      if (gx < xdim) {
+        const uint32_t base = (uint32_t)(((int64_t)gx * ld + gk) * 4);
+        if (gk < k4) o0 = base;
+        if (gk + 4 < k4) o1 = base + 16;
       }
-    return;
+      r[2 * q] = __builtin_amdgcn_raw_buffer_load_b128(rs, o0, 0, 0);
+      r[2 * q + 1] = __builtin_amdgcn_raw_buffer_load_b128(rs, o1, 0, 0);
+    }
   }
 
-  // loss epilogues, as in the float32 kernel; dS leaves as bits (ranking),
-  // bf16 (logistic) or raw fp32 scores for the softmax row pass
-  const float* pos = a.pos + (int64_t)c * a.C;
-  const float* bias = (a.bias && side == 1) ? a.bias + (int64_t)c * a.C : nullptr;
-  const float kinv = (Nc - 1 > 0) ? 1.0f / (float)(Nc - 1) : 0.0f;
+  __device__ static void store(uint16_t (*s)[TX * BK], const v4f* r, int tid) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      const int x = f >> 2, kq = f & 3;
+      const float v[8] = {r[2 * q].x, r[2 * q].y, r[2 * q].z, r[2 * q].w,
+                          r[2 * q + 1].x, r[2 * q + 1].y, r[2 * q + 1].z, r[2 * q + 1].w};
+      uint32_t pc[3][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t pp[3];
+        split3_pair(v[2 * i], v[2 * i + 1], pp);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) pc[p][i] = pp[p];
+      }
+      const int o = swz(x, kq);
+#pragma unroll
+      for (int p = 0; p < 3; ++p) *(u32x4*)(s[p] + o) = (u32x4){pc[p][0], pc[p][1], pc[p][2], pc[p][3]};
+    }
+  }
+};
+
+// one LDS buffer of three A and three B planes (single-buffered, so that
+// three workgroups fit a CU), and the row partials
+struct SmemS {
+  uint16_t As[3][BM * BK];
+  uint16_t Bs[3][128 * BK];
+  float red[2][BM][2];
+  float rowv[BM][2];
+};
+
+template <int EPI, int NPROD>
+__global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles_n, int tiles_m) {
+  constexpr int BN = 128, WN = 64, JN = 4;
+  __shared__ __align__(16) SmemS sm;
+  TileGeo t;
+  if (!tile_geo<BN, EPI>(a, tiles_n, tiles_m, gridDim.x, blockIdx.x, t)) return;
+  load_rowv(a, t, sm.rowv);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int l16 = lane & 15, g = lane >> 4;
+
+  const rsrc_t ra = make_rsrc(a.Af + t.c * a.a_cs + t.side * a.a_ss);
+  const rsrc_t rb = make_rsrc(a.Bf + t.c * a.b_cs + t.side * a.b_ss);
+  v4f acc[4][JN];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int ml = 64 * wm + 16 * i + 4 * g + r;
-      const int m = m0 + ml;
-      const bool mrow = m < M;
-      const float p = mrow ? pos[m] : 0.0f;
-      const float bm = (bias && mrow) ? bias[m] : 0.0f;
-      float v0, v1;
-      if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
-        float lsum = 0.0f, dsum = 0.0f;
-#pragma unroll
-        for (int j = 0; j < JN; ++j) {
-          const int n = colb + 16 * j;
-          const float s = acc[i][j][r] + bm;
-          const bool valid = mrow && n < N && n != m;
-          float dsv = 0.0f;
-          if (EPI == EPI_LOSS_BITS) {
-            const float zz = a.margin - p + s;
-            if (valid && zz > 0.0f) {
-              dsv = 1.0f;
-              lsum += zz;
-            }
-          } else if (valid) {
-            float sg, sp;
-            logistic_pair(s, sg, sp);
-            dsv = sg * kinv;
-            lsum += sp * kinv;
-          }
-          dsum += dsv;
-          if (EPI == EPI_LOSS_BITS) {
-            const uint64_t mask = __ballot(dsv != 0.0f);
-            const int wcol = (n0 + WN * wn + 16 * j) >> 4;
-            if (l16 == 0 && mrow && wcol < a.nwcb)
-              a.dsb[c * a.cb_cs + side * a.cb_ss + (int64_t)wcol * a.ldcb + m] = (uint16_t)(mask >> (16 * g));
-          } else if (mrow && n < a.ldc) {
-            a.dsh[c * a.c_cs + side * a.c_ss + (int64_t)m * a.ldc + n] = f_to_bf16(dsv);
-          }
-        }
-        v0 = group16_sum(lsum);
-        v1 = group16_sum(dsum);
-      } else {  // EPI_SOFTMAX_STATS
-        float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
-        float mx = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < JN; ++j) {
-          const int n = colb + 16 * j;
-          const float s = acc[i][j][r] + bm;
-          if (mrow && n < N && n != m) mx = fmaxf(mx, s);
-          if (mrow && n < a.ldc) Cm[(int64_t)m * a.ldc + n] = s;
-        }
-        mx = group16_max(mx);
-        float se = 0.0f;
-#pragma unroll
-        for (int j = 0; j < JN; ++j) {
-          const int n = colb + 16 * j;
-          if (mrow && n < N && n != m) se += expf(acc[i][j][r] + bm - mx);
-        }
-        v0 = mx;
-        v1 = group16_sum(se);
-      }
-      if (l16 == 0) {
-        red[wn][ml][0] = v0;
-        red[wn][ml][1] = v1;
-      }
-    }
+    for (int j = 0; j < JN; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
+
+  v4f pa[2 * TileS<BM>::LOADS], pb[2 * TileS<BN>::LOADS];
+  const int nk = (t.K + BK - 1) / BK;
+  TileS<BM>::load(pa, ra, a.lda, t.m0, t.M, 0, t.K, tid);
+  TileS<BN>::load(pb, rb, a.ldb, t.n0, t.N, 0, t.K, tid);
+  TileS<BM>::store(sm.As, pa, tid);
+  TileS<BN>::store(sm.Bs, pb, tid);
   __syncthreads();
-  if (tid < BM && m0 + tid < M) {
-    const int ml = tid;
-    float v0, v1;
-    if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
-      v0 = red[0][ml][0] + red[1][ml][0];
-      v1 = red[0][ml][1] + red[1][ml][1];
-    } else {
-      const float ma = red[0][ml][0], mb = red[1][ml][0];
-      const float mx = fmaxf(ma, mb);
-      v0 = mx;
-      v1 = (mx == -INFINITY) ? 0.0f
-                             : (ma == -INFINITY ? 0.0f : red[0][ml][1] * expf(ma - mx)) +
-                                   (mb == -INFINITY ? 0.0f : red[1][ml][1] * expf(mb - mx));
+
+  const int fa0 = swz(64 * wm + l16, g), fb0 = swz(WN * wn + l16, g);
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) {
+      TileS<BM>::load(pa, ra, a.lda, t.m0, t.M, (kt + 1) * BK, t.K, tid);
+      TileS<BN>::load(pb, rb, a.ldb, t.n0, t.N, (kt + 1) * BK, t.K, tid);
     }
-    float* rp = rowpart + ((int64_t)(m0 + ml) * a.nct + tn) * 2;
-    rp[0] = v0;
-    rp[1] = v1;
+    v8bf bq[3][JN];
+#pragma unroll
+    for (int p = 0; p < 3; ++p)
+#pragma unroll
+      for (int j = 0; j < JN; ++j) bq[p][j] = *(const v8bf*)(sm.Bs[p] + fb0 + 16 * j * BK);
+#pragma unroll
+    for (int pa_ = 0; pa_ < 3; ++pa_) {
+      v8bf af[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = *(const v8bf*)(sm.As[pa_] + fa0 + 16 * i * BK);
+#pragma unroll
+      for (int pb_ = 0; pb_ < 3; ++pb_) {
+        if (NPROD == 6 && pa_ + pb_ > 2) continue;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < JN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bq[pb_][j], acc[i][j], 0, 0, 0);
+      }
+    }
+    if (kt + 1 < nk) {
+      __syncthreads();
+      TileS<BM>::store(sm.As, pa, tid);
+      TileS<BN>::store(sm.Bs, pb, tid);
+      __syncthreads();
+    }
   }
+  tile_epilogue<BN, EPI>(a, t, acc, sm.red, sm.rowv);
 }
 
 template <int BN, int AMODE, int EPI, int PL>
@@ -441,14 +665,17 @@ __global__ __launch_bounds__(256) void to_bf16_transpose_kernel(const float* src
   }
 }
 
-// fp32 rows -> the three exact bf16 pieces (h, m, l) of every element, each
-// transposed: plane p is [kp][ld_T] (source column, then source row), planes
-// ps elements apart; rows [rows, rows_p) and columns [d, kp) are zeros.
-// rows_p and ld_T are multiples of 4 (each thread writes four rows).
-__global__ __launch_bounds__(256) void split3_transpose_kernel(const float* src, int64_t src_bs, int rows,
-                                                               int ld_src, int d, uint16_t* dstT,
-                                                               int64_t dstT_bs, int64_t ps, int ld_T,
-                                                               int rows_p, int kp) {
+// fp32 rows -> the three exact bf16 pieces (split3_pair) of every element, as
+// row-major planes [rows][ld_R] (dstR, planes psR apart, columns [d, kp)
+// zero) and / or transposed planes [kp][ld_T] (dstT, planes psT apart, rows
+// [rows, rows_p) zero); either output may be null.  64 x 64 tiles through
+// LDS; each thread writes four consecutive elements (8 bytes) per plane, so
+// kp, ld_R, rows_p and ld_T are multiples of 4.
+__global__ __launch_bounds__(256) void split3_planes_kernel(const float* src, int64_t src_bs, int rows,
+                                                            int ld_src, int d, uint16_t* dstR, int64_t dstR_bs,
+                                                            int64_t psR, int ld_R, uint16_t* dstT,
+                                                            int64_t dstT_bs, int64_t psT, int ld_T, int rows_p,
+                                                            int kp) {
   __shared__ float tile[64][65];
   const int b = blockIdx.z;
   const int r0 = blockIdx.y * 64, k0 = blockIdx.x * 64;
@@ -459,23 +686,31 @@ __global__ __launch_bounds__(256) void split3_transpose_kernel(const float* src,
     tile[rr][kk] = (r < rows && k < d) ? s[(int64_t)r * ld_src + k] : 0.0f;
   }
   __syncthreads();
-  uint16_t* o = dstT + (int64_t)b * dstT_bs;
-  for (int q = threadIdx.x; q < 64 * 16; q += 256) {
-    const int kk = q >> 4, r4 = 4 * (q & 15);
-    const int k = k0 + kk, r = r0 + r4;
-    if (k >= kp || r >= rows_p) continue;
-    uint32_t pc[3][2];
-#pragma unroll
-    for (int i = 0; i < 4; i += 2) {
+  if (dstR) {
+    uint16_t* o = dstR + (int64_t)b * dstR_bs;
+    for (int q = threadIdx.x; q < 64 * 16; q += 256) {
+      const int rr = q >> 4, k4 = 4 * (q & 15);
+      const int r = r0 + rr, k = k0 + k4;
+      if (r >= rows || k >= kp) continue;
       uint32_t lo[3], hi[3];
-      split3(tile[r4 + i][kk], lo);
-      split3(tile[r4 + i + 1][kk], hi);
+      split3_pair(tile[rr][k4], tile[rr][k4 + 1], lo);
+      split3_pair(tile[rr][k4 + 2], tile[rr][k4 + 3], hi);
 #pragma unroll
-      for (int p = 0; p < 3; ++p) pc[p][i >> 1] = lo[p] | (hi[p] << 16);
+      for (int p = 0; p < 3; ++p) *(uint2*)(o + p * psR + (int64_t)r * ld_R + k) = make_uint2(lo[p], hi[p]);
     }
+  }
+  if (dstT) {
+    uint16_t* o = dstT + (int64_t)b * dstT_bs;
+    for (int q = threadIdx.x; q < 64 * 16; q += 256) {
+      const int kk = q >> 4, r4 = 4 * (q & 15);
+      const int k = k0 + kk, r = r0 + r4;
+      if (k >= kp || r >= rows_p) continue;
+      uint32_t lo[3], hi[3];
+      split3_pair(tile[r4][kk], tile[r4 + 1][kk], lo);
+      split3_pair(tile[r4 + 2][kk], tile[r4 + 3][kk], hi);
 #pragma unroll
-    for (int p = 0; p < 3; ++p)
-      *(uint2*)(o + p * ps + (int64_t)k * ld_T + r) = make_uint2(pc[p][0], pc[p][1]);
+      for (int p = 0; p < 3; ++p) *(uint2*)(o + p * psT + (int64_t)k * ld_T + r) = make_uint2(lo[p], hi[p]);
+    }
   }
 }
 
@@ -586,6 +821,19 @@ void launch_gemm_bf16_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches
   else launch_pair_bn<128>(a0, a1, batches, s);
 }
 
+void launch_score_split(const GemmArgsH& a, int epi, int batches, hipStream_t s) {
+  constexpr int NPROD = 6;
+  const int maxM = dim_max(a.mdim, a.Mfix, a.C, a.U);
+  const int maxN = dim_max(a.ndim, a.Nfix, a.C, a.U);
+  if (maxM <= 0 || maxN <= 0 || batches <= 0) return;
+  const int tiles_m = (maxM + BM - 1) / BM;
+  const int tiles_n = (maxN + 127) / 128;   // = nct (PBG_SCORE_BN columns per tile)
+  const unsigned nwg = (unsigned)((int64_t)tiles_n * tiles_m * batches);
+  if (epi == EPI_LOSS) score_split_kernel<EPI_LOSS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+  else if (epi == EPI_LOSS_BITS) score_split_kernel<EPI_LOSS_BITS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+  else score_split_kernel<EPI_SOFTMAX_STATS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+}
+
 void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d,
                               uint16_t* dst, int64_t dst_bs, int ld_dst, uint16_t* dstT,
                               int64_t dstT_bs, int ld_T, int rows_p, int kp, int batches,
@@ -595,12 +843,12 @@ void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld
                                                 dstT_bs, ld_T, rows_p, kp);
 }
 
-void launch_split3_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d, uint16_t* dstT,
-                             int64_t dstT_bs, int64_t ps, int ld_T, int rows_p, int kp, int batches,
-                             hipStream_t s) {
-  dim3 grid((kp + 63) / 64, (rows_p + 63) / 64, batches);
-  split3_transpose_kernel<<<grid, 256, 0, s>>>(src, src_bs, rows, ld_src, d, dstT, dstT_bs, ps, ld_T, rows_p,
-                                               kp);
+void launch_split3_planes(const float* src, int64_t src_bs, int rows, int ld_src, int d, uint16_t* dstR,
+                          int64_t dstR_bs, int64_t psR, int ld_R, uint16_t* dstT, int64_t dstT_bs, int64_t psT,
+                          int ld_T, int rows_p, int kp, int batches, hipStream_t s) {
+  dim3 grid((kp + 63) / 64, (std::max(rows, rows_p) + 63) / 64, batches);
+  split3_planes_kernel<<<grid, 256, 0, s>>>(src, src_bs, rows, ld_src, d, dstR, dstR_bs, psR, ld_R, dstT, dstT_bs,
+                                            psT, ld_T, rows_p, kp);
 }
 
 void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s) {

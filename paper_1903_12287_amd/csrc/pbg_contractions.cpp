@@ -73,10 +73,12 @@ static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t*
 void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
                           const std::function<void(int)>& mark) {
   const int C = g.C, U = g.U, N = g.N, dp = g.dp, Np = g.Np, nch = g.nchunks;
-  GemmArgs fa;
+  // ranking: dS is 0 or 1 and travels as bits, 16 columns per word
+  const bool bits = g.loss == LOSS_RANKING;
+  GemmArgsH fa;
   memset(&fa, 0, sizeof(fa));
-  fa.A = b.qk;
-  fa.B = b.nn;
+  fa.Af = b.qk;
+  fa.Bf = b.nn;
   fa.Cm = b.ds;
   fa.a_cs = 2ll * C * dp;
   fa.a_ss = (int64_t)C * dp;
@@ -90,7 +92,7 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   fa.mdim = DIM_CC;
   fa.ndim = DIM_NC;
   fa.kdim = DIM_FIXED;
-  fa.Kfix = dp;
+  fa.Kfix = g.d;
   fa.C = C;
   fa.U = U;
   fa.m_step = g.m_step;
@@ -101,8 +103,6 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   fa.nct = g.nct;
   fa.loss = g.loss;
   fa.margin = g.margin;
-  // ranking: dS is 0 or 1 and travels as bits, 16 columns per word
-  const bool bits = g.loss == LOSS_RANKING;
   const int nw = (Np + 15) / 16, ldw = rup(C, 8);   // bit-matrix words per row, row pitch
   int epi = g.loss == LOSS_SOFTMAX ? EPI_SOFTMAX_STATS : EPI_LOSS;
   if (bits) {
@@ -113,7 +113,7 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
     fa.ldcb = ldw;
     fa.nwcb = nw;
   }
-  launch_gemm_f32(fa, GEMM_NT, epi, nch * 2, cs);
+  launch_score_split(fa, epi, nch * 2, cs);
   mark(2);
   if (g.loss == LOSS_SOFTMAX) launch_softmax_rows(g, b, cs);
   launch_finalize(g, b, ctx->steploss_dev + t, cs);
@@ -121,13 +121,13 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
 
   if (bits) {
     // dS is 0 or 1: exact products on the bf16 instructions with Q and N in
-    // three exact bf16 pieces each (float32 sums)
+    // three exact bf16 pieces each (transposed planes), float32 sums
     const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
     const BufsH& h = ctx->h;
-    launch_split3_transpose(b.qk, (int64_t)C * dp, C, dp, g.d, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, Cpb,
-                            dpb, nch * 2, cs);
-    launch_split3_transpose(b.nn, (int64_t)N * dp, N, dp, g.d, h.nnT3, (int64_t)dpb * Npb, h.n3_ps, Npb, Npb,
-                            dpb, nch * 2, cs);
+    launch_split3_planes(b.qk, (int64_t)C * dp, C, dp, g.d, nullptr, 0, 0, 0, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps,
+                         Cpb, Cpb, dpb, nch * 2, cs);
+    launch_split3_planes(b.nn, (int64_t)N * dp, N, dp, g.d, nullptr, 0, 0, 0, h.nnT3, (int64_t)dpb * Npb, h.n3_ps,
+                         Npb, Npb, dpb, nch * 2, cs);
     run_backward_h(g, b, nullptr, h.nnT3, h.n3_ps, h.qkT3, h.q3_ps, 3, cs);
     return;
   }
