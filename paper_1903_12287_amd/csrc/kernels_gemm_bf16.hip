@@ -173,7 +173,7 @@ struct SmemH {
   uint16_t As[2][BM * BK];
   uint16_t Bs[2][PL][BN * BK];
   float red[2][BM][2];
-  float rowv[BM][2];
+  float rowv[2][BM];
 };
 
 // Position of a workgroup's 128 x BN tile: `id` numbers the workgroup among
@@ -220,17 +220,159 @@ __device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int ti
   return true;
 }
 
-// positive score and bias of the tile's rows, for the loss epilogues (read
-// once at the start of the tile, while its first operands load)
-__device__ __forceinline__ void load_rowv(const GemmArgsH& a, const TileGeo& t, float (&rowv)[BM][2]) {
+// per-row values of the tile for the loss epilogues, read once at the start
+// of the tile while its first operands load: the hinge threshold
+// margin - p + bias (-inf for rows past the batch) for the ranking bits, else
+// the positive score p and the bias
+template <int EPI>
+__device__ __forceinline__ void load_rowv(const GemmArgsH& a, const TileGeo& t, float (&rowv)[2][BM]) {
   const int tid = threadIdx.x;
   if (tid < BM) {
     const int m = t.m0 + tid;
     const bool mrow = m < t.M;
     const int64_t o = (int64_t)t.c * a.C + m;
-    rowv[tid][0] = mrow ? a.pos[o] : 0.0f;
-    rowv[tid][1] = (mrow && a.bias && t.side == 1) ? a.bias[o] : 0.0f;
+    const float p = mrow ? a.pos[o] : 0.0f;
+    const float bm = (mrow && a.bias && t.side == 1) ? a.bias[o] : 0.0f;
+    if (EPI == EPI_LOSS_BITS) {
+      rowv[0][tid] = mrow ? a.margin - p + bm : -INFINITY;
+    } else {
+      rowv[0][tid] = p;
+      rowv[1][tid] = bm;
+    }
   }
+}
+
+// Ranking loss rows of a tile (MASKED: the tile holds columns past the batch
+// or the masked diagonal).  Hinge z = s + margin - p, dS = [z > 0]; each lane
+// group's ballot word is the bit-matrix word of its row for these 16 columns
+// and its population count that row's share of the dS row sum.
+template <int BN, bool MASKED>
+__device__ __forceinline__ void bits_rows(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[4][BN / 32],
+                                          float (&red)[2][BM][2], const float (&rowv)[2][BM]) {
+  constexpr int WN = BN / 2;
+  constexpr int JN = WN / 16;
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int colb = t.n0 + WN * wn + l16;
+  const int wcol0 = (t.n0 + WN * wn) >> 4;
+  // the words of four consecutive rows are adjacent (word-column major)
+  uint16_t* dbase = a.dsb + t.c * a.cb_cs + t.side * a.cb_ss + (int64_t)wcol0 * a.ldcb + t.m0 + 64 * wm + 4 * g;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int mb = 64 * wm + 16 * i + 4 * g;   // first of this lane group's four rows
+    const v4f thr = *(const v4f*)&rowv[0][mb];
+    float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    uint32_t cnt[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < JN; ++j) {
+      uint32_t wd[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float z = acc[i][j][r] + thr[r];
+        if (MASKED) {
+          const int n = colb + 16 * j;
+          if (n >= t.N || n == t.m0 + mb + r) z = -INFINITY;
+        }
+        const uint64_t mk = __ballot(z > 0.0f);
+        ls[r] += fmaxf(z, 0.0f);
+        wd[r] = (uint32_t)(mk >> (16 * g)) & 0xFFFFu;
+        cnt[r] += __builtin_popcount(wd[r]);
+      }
+      if (l16 == 0 && t.m0 + mb < t.M && wcol0 + j < a.nwcb)
+        *(uint2*)(dbase + (int64_t)j * a.ldcb + 16 * i) = make_uint2(wd[0] | (wd[1] << 16), wd[2] | (wd[3] << 16));
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float v0 = group16_sum(ls[r]);
+      if (l16 == 0) {
+        red[wn][mb + r][0] = v0;
+        red[wn][mb + r][1] = (float)cnt[r];
+      }
+    }
+  }
+}
+
+// logistic loss (dS rows in bf16 or float32) and softmax statistics (raw
+// scores + per-tile max and sum of exp) rows of a tile
+template <int BN, int EPI, bool MASKED>
+__device__ __forceinline__ void value_rows(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[4][BN / 32],
+                                           float (&red)[2][BM][2], const float (&rowv)[2][BM]) {
+  constexpr int WN = BN / 2;
+  constexpr int JN = WN / 16;
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int c = t.c, side = t.side, M = t.M, N = t.N, m0 = t.m0;
+  const int colb = t.n0 + WN * wn + l16;
+  const float kinv = (t.Nc - 1 > 0) ? 1.0f / (float)(t.Nc - 1) : 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int ml = 64 * wm + 16 * i + 4 * g + r;
+      const int m = m0 + ml;
+      const bool mrow = m < M;
+      const float p = rowv[0][ml];
+      const float bm = rowv[1][ml];
+      const int64_t orow = c * a.c_cs + side * a.c_ss + (int64_t)m * a.ldc;
+      float v0, v1;
+      if (EPI == EPI_LOSS) {
+        float lsum = 0.0f, dsum = 0.0f;
+#pragma unroll
+        for (int j = 0; j < JN; ++j) {
+          const int n = colb + 16 * j;
+          const float s = acc[i][j][r] + bm;
+          const bool valid = mrow && !(MASKED && (n >= N || n == m));
+          float dsv = 0.0f;
+          if (valid) {
+            if (a.loss == LOSS_RANKING) {
+              const float zz = a.margin - p + s;
+              if (zz > 0.0f) {
+                dsv = 1.0f;
+                lsum += zz;
+              }
+            } else {
+              float sg, sp;
+              logistic_pair(s, sg, sp);
+              dsv = sg * kinv;
+              lsum += sp * kinv;
+            }
+          }
+          dsum += dsv;
+          if (mrow && n < a.ldc) {
+            if (a.dsh) a.dsh[orow + n] = f_to_bf16(dsv);
+            else a.Cm[orow + n] = dsv;
+          }
+        }
+        v0 = group16_sum(lsum);
+        v1 = group16_sum(dsum);
+      } else {  // EPI_SOFTMAX_STATS
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < JN; ++j) {
+          const int n = colb + 16 * j;
+          const float s = acc[i][j][r] + bm;
+          if (mrow && !(MASKED && (n >= N || n == m))) mx = fmaxf(mx, s);
+          if (mrow && n < a.ldc) a.Cm[orow + n] = s;
+        }
+        mx = group16_max(mx);
+        float se = 0.0f;
+#pragma unroll
+        for (int j = 0; j < JN; ++j) {
+          const int n = colb + 16 * j;
+          if (mrow && !(MASKED && (n >= N || n == m))) se += expf(acc[i][j][r] + bm - mx);
+        }
+        v0 = mx;
+        v1 = group16_sum(se);
+      }
+      if (l16 == 0) {
+        red[wn][ml][0] = v0;
+        red[wn][ml][1] = v1;
+      }
+    }
 }
 
 // Stores the tile (EPI_STORE) or runs the loss epilogue on it: dS leaves as
@@ -240,7 +382,7 @@ __device__ __forceinline__ void load_rowv(const GemmArgsH& a, const TileGeo& t, 
 // column halves and written per column tile.
 template <int BN, int EPI>
 __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[4][BN / 32],
-                                              float (&red)[2][BM][2], const float (&rowv)[BM][2]) {
+                                              float (&red)[2][BM][2], const float (&rowv)[2][BM]) {
   constexpr int WN = BN / 2;
   constexpr int JN = WN / 16;
   const int tid = threadIdx.x;
@@ -268,121 +410,15 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
     return;
   }
 
-  const float kinv = (Nc - 1 > 0) ? 1.0f / (float)(Nc - 1) : 0.0f;
   // column tiles past the batch's last column and the tile that holds the
   // masked diagonal (m0 == n0 as BM == BN) need per-element checks
-  const bool ragged = n0 + BN > N;
-  const bool diag = m0 == n0;
+  const bool masked = (n0 + BN > N) || (m0 == n0);
   if (EPI == EPI_LOSS_BITS) {
-    // hinge z = s + margin - p (> 0: dS = 1); each lane group's ballot word
-    // is the bit-matrix word of its row for these 16 columns, and its
-    // population count that row's share of the dS row sum
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int mb = 64 * wm + 16 * i + 4 * g;   // first of this lane group's four rows
-      float thr[4], ls[4];
-      uint32_t cnt[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        thr[r] = (m0 + mb + r < M) ? a.margin - rowv[mb + r][0] + rowv[mb + r][1] : -INFINITY;
-        ls[r] = 0.0f;
-        cnt[r] = 0u;
-      }
-#pragma unroll
-      for (int j = 0; j < JN; ++j) {
-        const int n = colb + 16 * j;
-        uint32_t wd[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float z = acc[i][j][r] + thr[r];
-          if ((ragged && n >= N) || (diag && n == m0 + mb + r)) z = -INFINITY;
-          const uint64_t mk = __ballot(z > 0.0f);
-          ls[r] += fmaxf(z, 0.0f);
-          wd[r] = (uint32_t)(mk >> (16 * g)) & 0xFFFFu;
-          cnt[r] += __builtin_popcount(wd[r]);
-        }
-        // the words of four consecutive rows are adjacent (word-column major)
-        const int wcol = (n0 + WN * wn + 16 * j) >> 4;
-        if (l16 == 0 && m0 + mb < M && wcol < a.nwcb)
-          *(uint2*)(a.dsb + c * a.cb_cs + side * a.cb_ss + (int64_t)wcol * a.ldcb + m0 + mb) =
-              make_uint2(wd[0] | (wd[1] << 16), wd[2] | (wd[3] << 16));
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float v0 = group16_sum(ls[r]);
-        if (l16 == 0) {
-          red[wn][mb + r][0] = v0;
-          red[wn][mb + r][1] = (float)cnt[r];
-        }
-      }
-    }
+    if (masked) bits_rows<BN, true>(a, t, acc, red, rowv);
+    else bits_rows<BN, false>(a, t, acc, red, rowv);
   } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int ml = 64 * wm + 16 * i + 4 * g + r;
-        const int m = m0 + ml;
-        const bool mrow = m < M;
-        const float p = rowv[ml][0];
-        const float bm = rowv[ml][1];
-        float v0, v1;
-        if (EPI == EPI_LOSS) {
-          float lsum = 0.0f, dsum = 0.0f;
-#pragma unroll
-          for (int j = 0; j < JN; ++j) {
-            const int n = colb + 16 * j;
-            const float s = acc[i][j][r] + bm;
-            const bool valid = mrow && !(ragged && n >= N) && !(diag && n == m);
-            float dsv = 0.0f;
-            if (valid) {
-              if (a.loss == LOSS_RANKING) {
-                const float zz = a.margin - p + s;
-                if (zz > 0.0f) {
-                  dsv = 1.0f;
-                  lsum += zz;
-                }
-              } else {
-                float sg, sp;
-                logistic_pair(s, sg, sp);
-                dsv = sg * kinv;
-                lsum += sp * kinv;
-              }
-            }
-            dsum += dsv;
-            if (mrow && n < a.ldc) {
-              const int64_t o = c * a.c_cs + side * a.c_ss + (int64_t)m * a.ldc + n;
-              if (a.dsh) a.dsh[o] = f_to_bf16(dsv);
-              else a.Cm[o] = dsv;
-            }
-          }
-          v0 = group16_sum(lsum);
-          v1 = group16_sum(dsum);
-        } else {  // EPI_SOFTMAX_STATS
-          float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
-          float mx = -INFINITY;
-#pragma unroll
-          for (int j = 0; j < JN; ++j) {
-            const int n = colb + 16 * j;
-            const float s = acc[i][j][r] + bm;
-            if (mrow && !(ragged && n >= N) && !(diag && n == m)) mx = fmaxf(mx, s);
-            if (mrow && n < a.ldc) Cm[(int64_t)m * a.ldc + n] = s;
-          }
-          mx = group16_max(mx);
-          float se = 0.0f;
-#pragma unroll
-          for (int j = 0; j < JN; ++j) {
-            const int n = colb + 16 * j;
-            if (mrow && !(ragged && n >= N) && !(diag && n == m)) se += expf(acc[i][j][r] + bm - mx);
-          }
-          v0 = mx;
-          v1 = group16_sum(se);
-        }
-        if (l16 == 0) {
-          red[wn][ml][0] = v0;
-          red[wn][ml][1] = v1;
-        }
-      }
+    if (masked) value_rows<BN, EPI, true>(a, t, acc, red, rowv);
+    else value_rows<BN, EPI, false>(a, t, acc, red, rowv);
   }
   __syncthreads();
   if (tid < BM && m0 + tid < M) {
@@ -418,7 +454,7 @@ __device__ __forceinline__ void gemm_bf16_tile(const GemmArgsH& a, int tiles_n, 
   auto& Bs = sm.Bs;
   TileGeo t;
   if (!tile_geo<BN, EPI>(a, tiles_n, tiles_m, nwg, id, t)) return;
-  if (EPI != EPI_STORE) load_rowv(a, t, sm.rowv);
+  if (EPI != EPI_STORE) load_rowv<EPI>(a, t, sm.rowv);
   const int c = t.c, side = t.side, M = t.M, N = t.N, K = t.K, m0 = t.m0, n0 = t.n0;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -549,7 +585,7 @@ struct SmemS {
   uint16_t As[3][BM * BK];
   uint16_t Bs[3][128 * BK];
   float red[2][BM][2];
-  float rowv[BM][2];
+  float rowv[2][BM];
 };
 
 template <int EPI, int NPROD>
@@ -558,7 +594,7 @@ __global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles
   __shared__ __align__(16) SmemS sm;
   TileGeo t;
   if (!tile_geo<BN, EPI>(a, tiles_n, tiles_m, gridDim.x, blockIdx.x, t)) return;
-  load_rowv(a, t, sm.rowv);
+  load_rowv<EPI>(a, t, sm.rowv);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
