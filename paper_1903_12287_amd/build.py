@@ -28,6 +28,9 @@ COMMON = [
     "-I", INCLUDE, "-I", CSRC,
     # keep the compiler from forming packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-instruction accumulators in ordinary VGPRs: the loss epilogues
+    # then read them in place instead of copying 64 AGPRs out first
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wno-unused-result",
 ]
 

@@ -63,7 +63,7 @@ struct Tile {
   static constexpr int PITCH = KC ? KP : TX + 4;
   static constexpr int SIZE = KC ? TX * KP : BK * (TX + 4);
 
-  __device__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
+  __device__ __forceinline__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
       const int f = tid + 256 * q;
@@ -81,7 +81,7 @@ struct Tile {
     }
   }
 
-  __device__ static void store(float* s, const v4f* r, int tid) {
+  __device__ __forceinline__ static void store(float* s, const v4f* r, int tid) {
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
       const int f = tid + 256 * q;
@@ -106,12 +106,12 @@ struct BitTile {
   static constexpr int LOADS = TX * BK / 4 / 256;
   static constexpr int SIZE = Tile<TX, KC>::SIZE;
 
-  __device__ static v4f expand(uint32_t w, int shift) {
+  __device__ __forceinline__ static v4f expand(uint32_t w, int shift) {
     const uint32_t b = w >> shift;
     return (v4f){(float)(b & 1u), (float)((b >> 1) & 1u), (float)((b >> 2) & 1u), (float)((b >> 3) & 1u)};
   }
 
-  __device__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
+  __device__ __forceinline__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
       const int f = tid + 256 * q;
@@ -135,7 +135,7 @@ struct BitTile {
     }
   }
 
-  __device__ static void store(float* s, const v4f* r, int tid) {
+  __device__ __forceinline__ static void store(float* s, const v4f* r, int tid) {
     v4f e[LOADS];
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) e[q] = expand(__float_as_uint(r[q].x), (int)__float_as_uint(r[q].y));

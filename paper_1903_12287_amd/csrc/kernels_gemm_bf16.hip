@@ -81,10 +81,9 @@ __device__ __forceinline__ int pick_dim(int sel, int fixed, int Cc, int Nc) {
 // element offset of the 16-byte group q of row x in a swizzled LDS tile
 __device__ __forceinline__ int swz(int x, int q) { return x * BK + ((q ^ ((x >> 2) & 3)) << 3); }
 
-// 0.0 / 1.0 in bf16 for bits b and b+1 of v, packed low / high
-__device__ __forceinline__ uint32_t bits2(uint32_t v, int b) {
-  return (((v >> b) & 1u) * 0x3F80u) | ((((v >> (b + 1)) & 1u) * 0x3F80u) << 16);
-}
+// two bits t (0..3) -> the packed bf16 pair (bit 0 low, bit 1 high) of 0.0 / 1.0:
+// t * 0x8001 puts bit 0 at bit 0 and bit 1 at bit 16, and 0x3F80 is 1.0
+__device__ __forceinline__ uint32_t bit_pair(uint32_t t) { return ((t * 0x8001u) & 0x10001u) * 0x3F80u; }
 
 // One operand tile of TX rows x BK k as LDS [row][k] bf16 (swizzled); each
 // thread moves TX * BK / 8 / 256 groups of eight elements per slice.  Loaded
@@ -101,7 +100,7 @@ struct TileH {
   static constexpr int LOADS = TX * BK / 8 / 256;
   static constexpr int SIZE = TX * BK;
 
-  __device__ static void load(u32x4* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
+  __device__ __forceinline__ static void load(u32x4* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
       const int f = tid + 256 * q;
@@ -129,7 +128,7 @@ struct TileH {
     }
   }
 
-  __device__ static void store(uint16_t* s, const u32x4* r, int tid, int x0, int k0, int kdim) {
+  __device__ __forceinline__ static void store(uint16_t* s, const u32x4* r, int tid, int x0, int k0, int kdim) {
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
       const int f = tid + 256 * q;
@@ -145,21 +144,20 @@ struct TileH {
         const int x = f >> 2, kq = f & 3;
         u32x4 v = r[q];
         if (MODE == GA_BITS_ROW) {
-          const int b = (8 * kq) & 15;        // bit of column k0 + 8 kq in its word
-          const uint32_t w = v.x;
-          v = (u32x4){bits2(w, b), bits2(w, b + 2), bits2(w, b + 4), bits2(w, b + 6)};
+          // bits of columns k0 + 8 kq + 0..7 -> four packed bf16 pairs
+          const uint32_t bits = v.x >> ((8 * kq) & 15);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = bit_pair(__builtin_amdgcn_ubfe(bits, 2 * i, 2));
         } else if (MODE == GA_BITS_COL) {
-          const int b = (x0 + x) & 15;        // bit of this column in each row's word
-          const int gk = k0 + 8 * kq;         // rows gk + i >= kdim lie outside the chunk
-          uint32_t h[8];
+          // bit b of the words of rows gk .. gk + 7 (two rows per dword)
+          const int b = (x0 + x) & 15;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            h[2 * i] = v[i] & 0xFFFFu;
-            h[2 * i + 1] = v[i] >> 16;
+          for (int i = 0; i < 4; ++i) v[i] = ((v[i] >> b) & 0x00010001u) * 0x3F80u;
+          const int nv = kdim - (k0 + 8 * kq);   // rows from nv on lie outside the chunk
+          if (nv < 8) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] &= (2 * i + 1 < nv) ? 0xFFFFFFFFu : (2 * i < nv ? 0xFFFFu : 0u);
           }
-#pragma unroll
-          for (int i = 0; i < 8; ++i) h[i] = (gk + i < kdim) ? ((h[i] >> b) & 1u) * 0x3F80u : 0u;
-          v = (u32x4){h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
         }
         *(u32x4*)(s + swz(x, kq)) = v;
       }
@@ -539,7 +537,7 @@ template <int TX>
 struct TileS {
   static constexpr int LOADS = TX * BK / 8 / 256;   // groups of eight per thread
 
-  __device__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
+  __device__ __forceinline__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
     const int k4 = (kdim + 3) & ~3;
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
@@ -557,7 +555,7 @@ struct TileS {
     }
   }
 
-  __device__ static void store(uint16_t (*s)[TX * BK], const v4f* r, int tid) {
+  __device__ __forceinline__ static void store(uint16_t (*s)[TX * BK], const v4f* r, int tid) {
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
       const int f = tid + 256 * q;
@@ -623,11 +621,8 @@ __global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles
       TileS<BM>::load(pa, ra, a.lda, t.m0, t.M, (kt + 1) * BK, t.K, tid);
       TileS<BN>::load(pb, rb, a.ldb, t.n0, t.N, (kt + 1) * BK, t.K, tid);
     }
-    v8bf bq[3][JN];
-#pragma unroll
-    for (int p = 0; p < 3; ++p)
-#pragma unroll
-      for (int j = 0; j < JN; ++j) bq[p][j] = *(const v8bf*)(sm.Bs[p] + fb0 + 16 * j * BK);
+    // one A plane and one B plane in registers at a time (B planes are read
+    // again for each A plane): fewer live registers, three waves per SIMD
 #pragma unroll
     for (int pa_ = 0; pa_ < 3; ++pa_) {
       v8bf af[4];
@@ -636,11 +631,14 @@ __global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles
 #pragma unroll
       for (int pb_ = 0; pb_ < 3; ++pb_) {
         if (NPROD == 6 && pa_ + pb_ > 2) continue;
+        v8bf bf[JN];
+#pragma unroll
+        for (int j = 0; j < JN; ++j) bf[j] = *(const v8bf*)(sm.Bs[pb_] + fb0 + 16 * j * BK);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int j = 0; j < JN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bq[pb_][j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
       }
     }
     if (kt + 1 < nk) {
