@@ -43,7 +43,7 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(StepGeom g, StepBufs 
 }
 
 // ---- per-edge dL/dp, translation bias gradient, losses ------------------------
-__global__ __launch_bounds__(256) void finalize_kernel(StepGeom g, StepBufs b) {
+__global__ __launch_bounds__(1024) void finalize_kernel(StepGeom g, StepBufs b) {
   const int c = blockIdx.x;
   const int Cc = chunk_edges(g, c);
   double acc = 0.0;
@@ -54,11 +54,13 @@ __global__ __launch_bounds__(256) void finalize_kernel(StepGeom g, StepBufs b) {
     if (g.loss != LOSS_SOFTMAX) {
       const float* r0 = b.rowpart + ((int64_t)(c * 2 + 0) * g.C + e) * g.nct * 2;
       const float* r1 = b.rowpart + ((int64_t)(c * 2 + 1) * g.C + e) * g.nct * 2;
+#pragma unroll 8
       for (int ct = 0; ct < g.nct; ++ct) {
-        l0 += r0[2 * ct];
-        d0 += r0[2 * ct + 1];
-        l1 += r1[2 * ct];
-        d1 += r1[2 * ct + 1];
+        const float2 a0 = *(const float2*)(r0 + 2 * ct), a1 = *(const float2*)(r1 + 2 * ct);
+        l0 += a0.x;
+        d0 += a0.y;
+        l1 += a1.x;
+        d1 += a1.y;
       }
     }
     double loss;
@@ -84,10 +86,10 @@ __global__ __launch_bounds__(256) void finalize_kernel(StepGeom g, StepBufs b) {
     acc += loss;
   }
   // fixed-order block reduction of the chunk loss
-  __shared__ double red[256];
+  __shared__ double red[1024];
   red[threadIdx.x] = acc;
   __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
+  for (int o = 512; o > 0; o >>= 1) {
     if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
     __syncthreads();
   }
@@ -252,7 +254,7 @@ void launch_softmax_rows(const StepGeom& g, const StepBufs& b, hipStream_t s) {
 }
 
 void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, hipStream_t s) {
-  finalize_kernel<<<g.nchunks, 256, 0, s>>>(g, b);
+  finalize_kernel<<<g.nchunks, 1024, 0, s>>>(g, b);
   sum_chunks_kernel<<<1, 64, 0, s>>>(b.chunkloss, g.nchunks, step_loss_slot);
 }
 

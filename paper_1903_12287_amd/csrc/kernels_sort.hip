@@ -250,7 +250,7 @@ template <int MODE, int RQ>
 __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, const uint32_t* keys,
                                                         const uint32_t* vals, int n, const float* rows,
                                                         int64_t ld, int width, float* partial, float lr) {
-  constexpr int SB = 32 / RQ;                      // positions per batch of loads
+  constexpr int SB = 16 / RQ;                      // positions per batch of loads
   const int lane = threadIdx.x & 63;
   const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int p0 = blk * SEG_BLOCK;
@@ -443,7 +443,7 @@ __global__ __launch_bounds__(256) void relation_chunk_sums(StepGeom g, const flo
   float acc[ROWQ];
 #pragma unroll
   for (int q = 0; q < ROWQ; ++q) acc[q] = 0.0f;
-#pragma unroll 4
+#pragma unroll 16
   for (int k = k0 + w; k < k1; k += 4) {
     const int row = k < Cc ? k : g.C + (k - Cc);
     const float* r = base + (int64_t)row * ld;
@@ -463,26 +463,28 @@ __global__ __launch_bounds__(256) void relation_chunk_sums(StepGeom g, const flo
   for (int f = threadIdx.x; f < g.dr; f += 256) out[f] = (red[0][f] + red[1][f]) + (red[2][f] + red[3][f]);
 }
 
-// Second level and element-wise Adagrad: 64 elements per block; wave w adds a
-// contiguous quarter of the partial rows in order, then the four quarter sums
-// are combined in a fixed order.
-__global__ __launch_bounds__(256) void relation_single_adagrad(float* relp, float* relG, int width,
-                                                               const float* partial, int nparts,
-                                                               float lr) {
-  __shared__ float red[4][64];
+// Second level and element-wise Adagrad: 64 elements per block; wave w of 16
+// adds a contiguous sixteenth of the partial rows in order (all its loads in
+// flight at once), then the sixteen sums are combined in a fixed order.
+__global__ __launch_bounds__(1024) void relation_single_adagrad(float* relp, float* relG, int width,
+                                                                const float* partial, int nparts,
+                                                                float lr) {
+  __shared__ float red[16][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int f = blockIdx.x * 64 + lane;
-  const int per = (nparts + 3) / 4;
+  const int per = (nparts + 15) / 16;
   const int p0 = w * per, p1 = min(nparts, p0 + per);
   float gsum = 0.0f;
   if (f < width) {
-#pragma unroll 8
+#pragma unroll 16
     for (int c = p0; c < p1; ++c) gsum += partial[(int64_t)c * width + f];
   }
   red[w][lane] = gsum;
   __syncthreads();
   if (w != 0 || f >= width) return;
-  const float gt = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+  float gt = 0.0f;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) gt += red[q][lane];
   const float Gn = relG[f] + gt * gt;
   relG[f] = Gn;
   relp[f] -= lr * gt / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
@@ -579,5 +581,5 @@ void launch_relation_chunk_sums(const StepGeom& g, const float* rows, int64_t ld
 
 void launch_relation_single_adagrad(float* relp, float* relG, int width, const float* partial,
                                     int nparts, float lr, hipStream_t s) {
-  relation_single_adagrad<<<(width + 63) / 64, 256, 0, s>>>(relp, relG, width, partial, nparts, lr);
+  relation_single_adagrad<<<(width + 63) / 64, 1024, 0, s>>>(relp, relG, width, partial, nparts, lr);
 }
