@@ -26,9 +26,12 @@
 // B[8 (L / 16) + i][L % 16], i = 0..7, one 16-byte LDS read each; the
 // accumulator holds D[4 (L / 16) + r][L % 16] in register r.
 // LDS tiles are [row][k], 32 bf16 (64 bytes) per row with no padding: the
-// 16-byte group q of row x is kept at group q ^ ((x >> 2) & 3), so that the
-// fragment reads of 16 consecutive rows and the tile stores of 16 rows x 4
-// groups each touch all 64 banks once.
+// 16-byte group q of row x is kept at group q ^ (((x >> 1) ^ ((x >> 3) & 1)) & 3),
+// which repeats every 16 rows.
+// A fragment read (16 consecutive rows, one group each) then touches every
+// 16-byte bank group once, whether the LDS serves 16 lanes over 64 banks or
+// 8 lanes over 32 banks per cycle, and so do the tile stores (four groups of
+// consecutive rows).
 #include <algorithm>
 
 #include "kernels.h"
@@ -79,7 +82,9 @@ __device__ __forceinline__ int pick_dim(int sel, int fixed, int Cc, int Nc) {
 }
 
 // element offset of the 16-byte group q of row x in a swizzled LDS tile
-__device__ __forceinline__ int swz(int x, int q) { return x * BK + ((q ^ ((x >> 2) & 3)) << 3); }
+__device__ __forceinline__ int swz(int x, int q) {
+  return x * BK + ((q ^ (((x >> 1) ^ ((x >> 3) & 1)) & 3)) << 3);
+}
 
 // two bits t (0..3) -> the packed bf16 pair (bit 0 low, bit 1 high) of 0.0 / 1.0:
 // t * 0x8001 puts bit 0 at bit 0 and bit 1 at bit 16, and 0x3F80 is 1.0
@@ -165,11 +170,13 @@ struct TileH {
   }
 };
 
-// LDS of one workgroup: double-buffered A tile and PL B tiles, row partials
+// LDS of one workgroup: the A tile and PL B tiles (NB buffers), row partials
 template <int BN, int PL>
 struct SmemH {
-  uint16_t As[2][BM * BK];
-  uint16_t Bs[2][PL][BN * BK];
+  // three B planes: one buffer (three workgroups per CU); otherwise two
+  static constexpr int NB = PL == 3 ? 1 : 2;
+  uint16_t As[NB][BM * BK];
+  uint16_t Bs[NB][PL][BN * BK];
   float red[2][BM][2];
   float rowv[2][BM];
 };
@@ -485,10 +492,12 @@ __device__ __forceinline__ void gemm_bf16_tile(const GemmArgsH& a, int tiles_n, 
   for (int p = 0; p < PL; ++p) TB::store(Bs[0][p], pb[p], tid, n0, 0, K);
   __syncthreads();
 
-  // fragment offsets: row 16 i + l16 of the wave's block, group g (swizzled)
+  // fragment offsets: row 16 i + l16 of the wave's block, group g (the
+  // swizzle repeats every 16 rows)
   const int fa0 = swz(64 * wm + l16, g), fb0 = swz(WN * wn + l16, g);
+  constexpr int NB = SmemH<BN, PL>::NB;
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
+    const int buf = NB == 2 ? (kt & 1) : 0;
     if (kt + 1 < nk) {
       TA::load(pa, ra_s, a.lda, m0, M, (kt + 1) * BK, K, tid);
 #pragma unroll
@@ -511,9 +520,12 @@ __device__ __forceinline__ void gemm_bf16_tile(const GemmArgsH& a, int tiles_n, 
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) {
-      TA::store(As[buf ^ 1], pa, tid, m0, (kt + 1) * BK, K);
+      // one buffer: every wave is done reading it before it is overwritten
+      if (NB == 1) __syncthreads();
+      const int nbuf = NB == 2 ? (buf ^ 1) : 0;
+      TA::store(As[nbuf], pa, tid, m0, (kt + 1) * BK, K);
 #pragma unroll
-      for (int p = 0; p < PL; ++p) TB::store(Bs[buf ^ 1][p], pb[p], tid, n0, (kt + 1) * BK, K);
+      for (int p = 0; p < PL; ++p) TB::store(Bs[nbuf][p], pb[p], tid, n0, (kt + 1) * BK, K);
     }
     __syncthreads();
   }
