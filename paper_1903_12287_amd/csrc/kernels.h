@@ -150,8 +150,22 @@ void launch_relation_single_adagrad(float* relp, float* relG, int width, const f
                                     int nparts, float lr, hipStream_t s);
 void launch_exclusive_scan(const uint32_t* in, int64_t n, uint32_t* out, uint32_t* tmp,
                            uint32_t* total, hipStream_t s);
+// entries of `tmp` that launch_exclusive_scan needs for n values (n > 0)
+int64_t exclusive_scan_tmp_entries(int64_t n);
 
 // ---- bucketing (Sec. 4.1) ----------------------------------------------------
+// direct counting sort for up to BUCKET_DIRECT_MAX buckets: pass 1 counts each
+// tile's edges per bucket into hist[bucket][tile] and ORs id-range failures
+// into *flag (1 src, 2 dst, 4 rel); after an exclusive scan of hist, pass 2
+// writes the offsets and every edge's local ids at its stable position
+#define BUCKET_DIRECT_MAX 256
+#define BUCKET_TILE 4096
+int64_t bucket_direct_units(int64_t n);
+void launch_bucket_count(const int64_t* src, const int64_t* dst, const int32_t* rel, int64_t n, int64_t n_ent,
+                         int32_t n_rel, int64_t ps, int P, uint32_t* hist, uint32_t* flag, hipStream_t s);
+void launch_bucket_scatter(const int64_t* src, const int64_t* dst, const int32_t* rel, int64_t n, int64_t ps,
+                           int P, const uint32_t* start, int64_t* offsets, int32_t* src_local,
+                           int32_t* rel_out, int32_t* dst_local, hipStream_t s);
 void launch_bucket_keys(const int64_t* src, const int64_t* dst, int64_t n, int64_t ps, int P,
                         uint32_t* keys, uint32_t* vals, hipStream_t s);
 void launch_bucket_offsets(const uint32_t* keys, int64_t n, int nb, int64_t* offsets, hipStream_t s);

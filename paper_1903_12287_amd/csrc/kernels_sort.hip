@@ -507,6 +507,8 @@ void launch_exclusive_scan(const uint32_t* in, int64_t n, uint32_t* out, uint32_
   scan_tiles<<<nb, 256, 0, s>>>(in, n, tmp, out, total);
 }
 
+int64_t exclusive_scan_tmp_entries(int64_t n) { return (n + SORT_TILE - 1) / SORT_TILE + 1; }
+
 int radix_tile(int64_t) { return SORT_TILE; }
 
 int64_t radix_hist_entries(int64_t n) { return 256 * ((n + radix_tile(n) - 1) / radix_tile(n)); }

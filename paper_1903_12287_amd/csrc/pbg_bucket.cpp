@@ -1,10 +1,14 @@
 // pbg_bucket_edges: edge bucketing on the device (Sec. 4.1).
 //
-// Range check of every id first (nothing is written on an error), then bucket
-// keys b = part(src) * P + part(dst), a stable radix sort of (b, position),
-// bucket offsets by lower bound, and the local ids gathered in sorted order.
-// The sort buffers (16 bytes per edge plus the digit histograms) are
-// allocated for the call and released before it returns.
+// Up to BUCKET_DIRECT_MAX buckets: a counting sort in two passes over the ids
+// (count per bucket and unit of consecutive edges, with the range checks;
+// after a scan, write each edge's local ids at its stable position), with
+// 8 bytes per bucket and unit of work memory.  More buckets: range check of
+// every id first, then bucket keys b = part(src) * P + part(dst), a stable
+// radix sort of (b, position), bucket offsets by lower bound, and the local
+// ids gathered in sorted order (16 bytes per edge of sort buffers).  Either
+// way nothing is written on an error, and the work memory is allocated for
+// the call and released before it returns.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -56,6 +60,35 @@ extern "C" pbg_status pbg_bucket_edges(pbg_ctx* ctx, const int64_t* src, const i
   if (nb > (1 << 24)) return set_err(ctx, PBG_ERR_UNSUPPORTED, "too many buckets");
   hipStream_t s = ctx->cs;
   DevBuf buf;
+  if (nb <= BUCKET_DIRECT_MAX) {
+    // counting sort: count per (bucket, unit) with the id checks, scan, and
+    // write the local ids at their positions (no key or position arrays)
+    const int64_t units = bucket_direct_units(n);
+    const int64_t nh = (int64_t)nb * units;
+    uint32_t* flag = (uint32_t*)buf.get(16);
+    uint32_t* hist = (uint32_t*)buf.get((size_t)nh * 4);
+    uint32_t* start = (uint32_t*)buf.get((size_t)nh * 4);
+    uint32_t* tmp = (uint32_t*)buf.get((size_t)exclusive_scan_tmp_entries(nh) * 4);
+    if (buf.failed)
+      return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "bucketing workspace (%lld edges) could not be allocated",
+                     (long long)n);
+    hipError_t e = hipMemsetAsync(flag, 0, 4, s);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipMemsetAsync");
+    launch_bucket_count(src, dst, rel, n, ctx->n, ctx->R, ctx->ps, P, hist, flag, s);
+    if (nh > 0) launch_exclusive_scan(hist, nh, start, tmp, nullptr, s);
+    uint32_t hflag = 0;
+    e = hipMemcpyAsync(&hflag, flag, 4, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(ctx, e, "bucket counts");
+    if (hflag & 3u)
+      return set_err(ctx, PBG_ERR_INVALID_ARG, "an entity id is outside [0, %lld)", (long long)ctx->n);
+    if (hflag & 4u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a relation id is outside [0, %d)", ctx->R);
+    launch_bucket_scatter(src, dst, rel, n, ctx->ps, P, start, offsets, src_local, rel_out, dst_local, s);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(ctx, e, "bucketing");
+    return PBG_OK;
+  }
   uint32_t* flag = (uint32_t*)buf.get(16);
   uint32_t* keys = (uint32_t*)buf.get((size_t)n * 4);
   uint32_t* vals = (uint32_t*)buf.get((size_t)n * 4);
