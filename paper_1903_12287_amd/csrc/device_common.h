@@ -59,28 +59,48 @@ __device__ __forceinline__ int32_t uniform_negative(uint64_t seed, uint32_t buck
 // ---------------------------------------------------------------------------
 // wave reductions (64 lanes)
 // ---------------------------------------------------------------------------
+// Lane exchanges inside a 16-lane row through DPP (no LDS round trip):
+// quad_perm [1,0,3,2] and [2,3,0,1] swap lanes 1 and 2 apart, half-mirror
+// swaps the two quads of each half-row, mirror the two halves of the row.
+// Each step pairs lanes symmetrically, so all lanes of a row end with the
+// same value (a + b and b + a are equal).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+#define PBG_DPP_QUAD_XOR1 0xB1
+#define PBG_DPP_QUAD_XOR2 0x4E
+#define PBG_DPP_ROW_HALF_MIRROR 0x141
+#define PBG_DPP_ROW_MIRROR 0x140
+
+// sum over the 16 consecutive lanes of a group (lanes 16g .. 16g+15)
+__device__ __forceinline__ float group16_sum(float x) {
+  x += dpp_f<PBG_DPP_QUAD_XOR1>(x);
+  x += dpp_f<PBG_DPP_QUAD_XOR2>(x);
+  x += dpp_f<PBG_DPP_ROW_HALF_MIRROR>(x);
+  x += dpp_f<PBG_DPP_ROW_MIRROR>(x);
+  return x;
+}
+
+__device__ __forceinline__ float group16_max(float x) {
+  x = fmaxf(x, dpp_f<PBG_DPP_QUAD_XOR1>(x));
+  x = fmaxf(x, dpp_f<PBG_DPP_QUAD_XOR2>(x));
+  x = fmaxf(x, dpp_f<PBG_DPP_ROW_HALF_MIRROR>(x));
+  x = fmaxf(x, dpp_f<PBG_DPP_ROW_MIRROR>(x));
+  return x;
+}
+
+// sum over the wave: the four rows by DPP, then the rows pairwise
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, PBG_WAVE);
+  x = group16_sum(x);
+  x += __shfl_xor(x, 16, PBG_WAVE);
+  x += __shfl_xor(x, 32, PBG_WAVE);
   return x;
 }
 
 __device__ __forceinline__ double wave_sum_d(double x) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, PBG_WAVE);
-  return x;
-}
-
-// sum over the 16 consecutive lanes of a group (lanes 16g .. 16g+15)
-__device__ __forceinline__ float group16_sum(float x) {
-#pragma unroll
-  for (int o = 8; o > 0; o >>= 1) x += __shfl_xor(x, o, PBG_WAVE);
-  return x;
-}
-
-__device__ __forceinline__ float group16_max(float x) {
-#pragma unroll
-  for (int o = 8; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, PBG_WAVE));
   return x;
 }
 
