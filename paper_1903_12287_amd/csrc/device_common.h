@@ -56,6 +56,14 @@ __device__ __forceinline__ int32_t uniform_negative(uint64_t seed, uint32_t buck
   return (int32_t)(((uint64_t)word * (uint64_t)rows) >> 32);
 }
 
+// the four candidates k4 .. k4 + 3 (k4 a multiple of 4) of one Philox block
+__device__ __forceinline__ void uniform_negatives4(uint64_t seed, uint32_t bucket, uint64_t chunk, uint32_t side,
+                                                   uint32_t k4, uint32_t rows, int32_t* out) {
+  const Philox4 w = philox4x32_10(k4 >> 2, (uint32_t)chunk, bucket, side, (uint32_t)seed, (uint32_t)(seed >> 32));
+#pragma unroll
+  for (int q = 0; q < 4; ++q) out[q] = (int32_t)(((uint64_t)w.v[q] * (uint64_t)rows) >> 32);
+}
+
 // ---------------------------------------------------------------------------
 // wave reductions (64 lanes)
 // ---------------------------------------------------------------------------

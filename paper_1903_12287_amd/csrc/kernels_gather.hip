@@ -2,9 +2,10 @@
 // Sec. 4.3 batched negatives, Fig. 3).
 //
 // One wave per work item; the items of chunk c are
-//   e in [0, Cc)          an edge: its source and destination rows,
-//   Cc + k, k in [0, U)   uniform destination candidate k (partition j),
-//   Cc + U + k            uniform source candidate k (partition i).
+//   e in [0, Cc)              an edge: its source and destination rows,
+//   Cc + q, q in [0, U4)      uniform destination candidates 4q .. 4q+3 (partition j),
+//   Cc + U4 + q               uniform source candidates 4q .. 4q+3 (partition i),
+// with U4 = ceil(U / 4): the four draws of one Philox block go to one wave.
 // For the dot comparator the source corruptions use the adjoint of g
 // (<g(x), y> = <x, g*(y)>, plus <theta, y> for translation), so every
 // candidate row is copied raw.  For cos every packed row is a unit vector and
@@ -22,7 +23,7 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   const int Cc = chunk_edges(g, c);
   const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
   const bool cplx = g.op == OP_COMPLEX;
-  const bool active = item < Cc + 2 * g.U;
+  const bool active = item < Cc + 2 * ((g.U + 3) >> 2);
   const int d = g.d, dp = g.dp;
 
   if (!active) return;   // no block-level barriers below: idle waves may leave
@@ -83,30 +84,45 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     return;
   }
 
-  // ---- uniform candidate
-  const int side = item < Cc + g.U ? 0 : 1;
-  const int k = item - Cc - side * g.U;
+  // ---- uniform candidates: four consecutive draws k0 .. k0 + 3 of one side
+  // per wave (one Philox block gives all four words, the four rows load
+  // together)
+  const int ng = (g.U + 3) >> 2;
+  const int grp = item - Cc;
+  const int side = grp < ng ? 0 : 1;
+  const int k0 = 4 * (grp - side * ng);
   const uint32_t rows = side == 0 ? (uint32_t)g.rows_j : (uint32_t)g.rows_i;
-  const int32_t u = uniform_negative(g.seed, g.bucket, (uint64_t)(g.chunk0 + c), (uint32_t)side,
-                                     (uint32_t)k, rows);
+  int32_t u[4];
+  uniform_negatives4(g.seed, g.bucket, (uint64_t)(g.chunk0 + c), (uint32_t)side, (uint32_t)k0, rows, u);
   const float* tbl = side == 0 ? b.emb_j : b.emb_i;
-  Row v;
-  row_load(v, tbl + (int64_t)u * d, d, cplx, lane);
-  float nv = 0.0f;
+  Row v[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (k0 + q < g.U) row_load(v[q], tbl + (int64_t)u[q] * d, d, cplx, lane);
+    else row_zero(v[q]);
+  }
+  float nv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (g.cmp == CMP_COS) {
     if (side == 1 && g.op != OP_IDENTITY) {
       // one relation (not linear): its operator is applied to every source candidate
       Row th;
       row_load(th, b.relp, d, cplx, lane);
-      v = op_forward(g.op, v, th);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = op_forward(g.op, v[q], th);
     }
-    nv = row_normalize(v);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) nv[q] = row_normalize(v[q]);
   }
-  const int t = Cc + k;
-  row_store(v, b.nn + ((int64_t)(c * 2 + side) * g.N + t) * dp, d, dp, cplx, lane);
-  if (lane == 0) {
-    b.neg[(int64_t)(c * 2 + side) * g.U + k] = u;
-    if (g.cmp == CMP_COS) b.nrm[(int64_t)(c * 2 + side) * g.N + t] = nv;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int k = k0 + q;
+    if (k >= g.U) break;
+    const int t = Cc + k;
+    row_store(v[q], b.nn + ((int64_t)(c * 2 + side) * g.N + t) * dp, d, dp, cplx, lane);
+    if (lane == 0) {
+      b.neg[(int64_t)(c * 2 + side) * g.U + k] = u[q];
+      if (g.cmp == CMP_COS) b.nrm[(int64_t)(c * 2 + side) * g.N + t] = nv[q];
+    }
   }
 }
 
@@ -149,7 +165,7 @@ __global__ void transpose_rel_kernel(const float* A, float* AT, int R, int d) {
 }  // namespace
 
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s) {
-  dim3 grid((g.C + 2 * g.U + 3) / 4, g.nchunks);
+  dim3 grid((g.C + 2 * ((g.U + 3) / 4) + 3) / 4, g.nchunks);
   switch (row_width_for(g.d)) {
     case 2: gather_op_kernel<2><<<grid, 256, 0, s>>>(g, b); break;
     case 4: gather_op_kernel<4><<<grid, 256, 0, s>>>(g, b); break;
