@@ -114,7 +114,7 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
   const int Cc = chunk_edges(g, c);
   const int Nc = Cc + g.U;
   const int item = blockIdx.x * 4 + w;
-  if (item >= Cc + 2 * g.U) return;   // no block-level barriers below
+  if (item >= Cc + 2 * ((g.U + 3) >> 2)) return;   // no block-level barriers below
   const bool cplx = g.op == OP_COMPLEX;
   const int d = g.d, dp = g.dp;
   const bool cos = g.cmp == CMP_COS;
@@ -216,31 +216,60 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     return;
   }
 
-  // uniform candidate rows
-  const int side = item < Cc + g.U ? 0 : 1;
-  const int k = item - Cc - side * g.U;
-  const int tpos = Cc + k;
-  const int32_t u = b.neg[(int64_t)(c * 2 + side) * g.U + k];
-  float* dnr = b.dn + ((int64_t)(c * 2 + side) * g.N + tpos) * dp;
+  // uniform candidate rows, four consecutive candidates of one side per wave
+  // (all their rows load together)
+  const int ng = (g.U + 3) >> 2;
+  const int grp = item - Cc;
+  const int side = grp < ng ? 0 : 1;
+  const int k0 = 4 * (grp - side * ng);
+  const int nq = min(4, g.U - k0);
+  const int64_t rbase = (int64_t)(c * 2 + side) * g.N + Cc + k0;   // row of candidate k0
+  int32_t u[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) u[q] = q < nq ? b.neg[(int64_t)(c * 2 + side) * g.U + k0 + q] : 0;
   if (cos) {
-    Row vh, gv;
-    row_load(vh, b.nn + ((int64_t)(c * 2 + side) * g.N + tpos) * dp, d, cplx, lane);
-    row_load(gv, dnr, d, cplx, lane);
-    const float nv = b.nrm[(int64_t)(c * 2 + side) * g.N + tpos];
-    Row dv = normalize_backward(vh, nv, gv);
-    if (side == 1 && has_rel) {
-      // the single relation's operator (not linear) was applied to this source candidate
-      Row th, x;
-      row_load(th, b.relp, d, cplx, lane);
-      row_load(x, b.emb_i + (int64_t)u * d, d, cplx, lane);
-      const Row grel = g.op == OP_TRANSLATION ? dv : op_param_grad(g.op, x, dv);
-      row_store(grel, b.relc + ((int64_t)c * g.N + g.C + k) * g.dr, d, g.dr, cplx, lane);
-      dv = op_adjoint(g.op, dv, th);
+    Row vh[4], gv[4];
+    float nv[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (q < nq) {
+        row_load(vh[q], b.nn + (rbase + q) * dp, d, cplx, lane);
+        row_load(gv[q], b.dn + (rbase + q) * dp, d, cplx, lane);
+        nv[q] = b.nrm[rbase + q];
+      } else {
+        row_zero(vh[q]);
+        row_zero(gv[q]);
+        nv[q] = 1.0f;
+      }
     }
-    row_store(dv, dnr, d, dp, cplx, lane);
+    Row th;
+    const bool op_side = side == 1 && has_rel;   // the single relation's operator was applied here
+    if (op_side) row_load(th, b.relp, d, cplx, lane);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (q >= nq) break;
+      Row dv = normalize_backward(vh[q], nv[q], gv[q]);
+      if (op_side) {
+        Row grel = dv;   // translation: the parameter gradient is dv itself
+        if (g.op != OP_TRANSLATION) {
+          Row x;
+          row_load(x, b.emb_i + (int64_t)u[q] * d, d, cplx, lane);
+          grel = op_param_grad(g.op, x, dv);
+        }
+        row_store(grel, b.relc + ((int64_t)c * g.N + g.C + k0 + q) * g.dr, d, g.dr, cplx, lane);
+        dv = op_adjoint(g.op, dv, th);
+      }
+      row_store(dv, b.dn + (rbase + q) * dp, d, dp, cplx, lane);
+    }
   }
-  if (lane == 0) {
-    const uint32_t key = side == 0 ? ((tbl_j << g.rb) | (uint32_t)u) : (uint32_t)u;
+  if (lane < nq) {
+    const int q = lane;
+    const int tpos = Cc + k0 + q;
+    int32_t uq = u[0];
+#pragma unroll
+    for (int i = 1; i < 4; ++i)
+      if (q == i) uq = u[i];
+    const uint32_t key = side == 0 ? ((tbl_j << g.rb) | (uint32_t)uq) : (uint32_t)uq;
     b.keys[kbase + side * Nc + tpos] = key;
     b.vals[kbase + side * Nc + tpos] = (uint32_t)((c * 2 + side) * g.N + tpos);
   }
@@ -259,7 +288,7 @@ void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slo
 }
 
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s) {
-  dim3 grid((g.C + 2 * g.U + 3) / 4, g.nchunks);
+  dim3 grid((g.C + 2 * ((g.U + 3) / 4) + 3) / 4, g.nchunks);
   switch (row_width_for(g.d)) {
     case 2: op_backward_kernel<2><<<grid, 256, 0, s>>>(g, b); break;
     case 4: op_backward_kernel<4><<<grid, 256, 0, s>>>(g, b); break;
