@@ -117,36 +117,56 @@ __global__ __launch_bounds__(256) void radix_hist(const uint32_t* keys, int n, i
   hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
 }
 
-// Stable scatter: rows of 256 keys are ranked in order (wave ballots over the
-// digit bits give each key's rank among equal digits of its wave; earlier waves
-// and rows add their counts).  Keys and values are loaded up front.
-template <int IPT>
+// Stable scatter.  Wave w of a block owns the 64 * IPT consecutive keys
+// base + w * 64 IPT ..., walked 64 at a time in order: wave ballots over
+// the digit bits rank each key among the equal digits of its round, a per-wave
+// count per digit carries the rank across rounds, and after one barrier the
+// waves' counts give each wave its base per digit (earlier waves first).
+// Keys and values are loaded up front.  RAW: `offs` holds the raw digit
+// counts [256][nblocks] (nblocks <= 64) and every block derives its own first
+// position per digit from them (its digit's earlier blocks, plus a block scan
+// of the digit totals), so no separate scan launch is needed.
+template <int IPT, bool RAW>
 __global__ __launch_bounds__(256) void radix_scatter(const uint32_t* keys, const uint32_t* vals, int n,
                                                      int shift, int nblocks, const uint32_t* offs,
                                                      uint32_t* okeys, uint32_t* ovals) {
-  __shared__ uint32_t run[256];
-  __shared__ uint32_t wc[4][256];
-  __shared__ uint32_t gofs[256];
+  __shared__ uint32_t smem[4];
+  constexpr int R = IPT;                     // rounds of 64 keys per wave (a quarter of the tile)
+  __shared__ uint32_t cnt[4][256];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int base = blockIdx.x * (256 * IPT);
-  uint32_t kr[IPT], vr[IPT];
+  const int base = blockIdx.x * (256 * IPT) + w * (64 * R);
+  uint32_t kr[R], vr[R], rk[R];
 #pragma unroll
-  for (int r = 0; r < IPT; ++r) {
-    const int idx = base + r * 256 + tid;
+  for (int r = 0; r < R; ++r) {
+    const int idx = base + r * 64 + lane;
     kr[r] = idx < n ? keys[idx] : 0u;
     vr[r] = idx < n ? vals[idx] : 0u;
   }
-  run[tid] = 0;
-  for (int q = 0; q < 4; ++q) wc[q][tid] = 0;
-  gofs[tid] = offs[(int64_t)tid * nblocks + blockIdx.x];
+  uint32_t first;   // first output position of digit tid in this block
+  if (RAW) {
+    const uint32_t* hrow = offs + (int64_t)tid * nblocks;
+    uint32_t v[64];
+#pragma unroll
+    for (int i = 0; i < 64; ++i) v[i] = i < nblocks ? hrow[i] : 0u;
+    uint32_t tot = 0u, pre = 0u;
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+      tot += v[i];
+      if (i < (int)blockIdx.x) pre += v[i];
+    }
+    uint32_t all;
+    first = block_exclusive_scan(tot, &all, smem) + pre;
+  } else {
+    first = offs[(int64_t)tid * nblocks + blockIdx.x];
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) cnt[q][tid] = 0u;
   __syncthreads();
   const unsigned long long lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
 #pragma unroll
-  for (int r = 0; r < IPT; ++r) {
-    const int idx = base + r * 256 + tid;
-    const bool valid = idx < n;
-    const uint32_t key = kr[r];
-    const uint32_t dig = (key >> shift) & 255u;
+  for (int r = 0; r < R; ++r) {
+    const bool valid = base + r * 64 + lane < n;
+    const uint32_t dig = (kr[r] >> shift) & 255u;
     unsigned long long peers = __ballot(valid);
 #pragma unroll
     for (int bit = 0; bit < 8; ++bit) {
@@ -154,53 +174,37 @@ __global__ __launch_bounds__(256) void radix_scatter(const uint32_t* keys, const
       const unsigned long long bal = __ballot(on);
       peers &= on ? bal : ~bal;
     }
-    const uint32_t rank = (uint32_t)__popcll(peers & lt);
-    if (valid && rank == 0) wc[w][dig] = (uint32_t)__popcll(peers);
-    __syncthreads();
-    if (valid) {
-      uint32_t off = run[dig] + rank;
-      for (int q = 0; q < w; ++q) off += wc[q][dig];
-      const uint32_t pos = gofs[dig] + off;
-      okeys[pos] = key;
-      ovals[pos] = vr[r];
+    const uint32_t below = (uint32_t)__popcll(peers & lt);
+    rk[r] = valid ? cnt[w][dig] + below : 0u;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    if (valid && below == 0u) cnt[w][dig] += (uint32_t)__popcll(peers);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  }
+  __syncthreads();
+  {
+    // digit tid: each wave's first output position
+    uint32_t run = first;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t c = cnt[q][tid];
+      cnt[q][tid] = run;
+      run += c;
     }
-    __syncthreads();
-    run[tid] += wc[0][tid] + wc[1][tid] + wc[2][tid] + wc[3][tid];
-    for (int q = 0; q < 4; ++q) wc[q][tid] = 0;
-    __syncthreads();
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (base + r * 64 + lane >= n) continue;
+    const uint32_t pos = cnt[w][(kr[r] >> shift) & 255u] + rk[r];
+    okeys[pos] = kr[r];
+    ovals[pos] = vr[r];
   }
 }
 
-// ------------------------------------------------------- single-launch scan
-// exclusive prefix sum of up to 1024 * 64 values by one workgroup: thread t
-// owns a run of at most 64 consecutive values, loaded all at once
-__global__ __launch_bounds__(1024) void scan_single(const uint32_t* in, int n, uint32_t* out) {
-  __shared__ uint32_t wsum[16];
-  const int per = (n + 1023) / 1024;
-  const int lo = min(n, (int)threadIdx.x * per), cnt = min(n, lo + per) - lo;
-  uint32_t v[64];
-#pragma unroll
-  for (int i = 0; i < 64; ++i) v[i] = i < cnt ? in[lo + i] : 0u;
-  uint32_t s = 0;
-#pragma unroll
-  for (int i = 0; i < 64; ++i) s += v[i];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  uint32_t x = s;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wsum[w] = x;
-  __syncthreads();
-  uint32_t run = x - s;
-  for (int i = 0; i < w; ++i) run += wsum[i];
-#pragma unroll
-  for (int i = 0; i < 64; ++i) {
-    if (i < cnt) out[lo + i] = run;
-    run += v[i];
-  }
-}
 
 // ---------------------------------------------------------------- segments
 enum { SEG_ENTITY = 0, SEG_RELATION = 1 };
@@ -529,9 +533,13 @@ void launch_radix_sort_to(uint32_t* keys, uint32_t* vals, int n, int bits, SortW
     for (int p = 0; p < passes; ++p) {
       const int shift = 8 * p;
       radix_hist<SORT_IPT><<<nblocks, 256, 0, s>>>(k_in, n, shift, nblocks, w.hist);
-      if (nh <= 1024 * 64) scan_single<<<1, 1024, 0, s>>>(w.hist, (int)nh, w.hist);
-      else launch_exclusive_scan(w.hist, nh, w.hist, w.scan_tmp, nullptr, s);
-      radix_scatter<SORT_IPT><<<nblocks, 256, 0, s>>>(k_in, v_in, n, shift, nblocks, w.hist, k_out, v_out);
+      if (nblocks <= 64) {
+        radix_scatter<SORT_IPT, true><<<nblocks, 256, 0, s>>>(k_in, v_in, n, shift, nblocks, w.hist, k_out, v_out);
+      } else {
+        launch_exclusive_scan(w.hist, nh, w.hist, w.scan_tmp, nullptr, s);
+        radix_scatter<SORT_IPT, false><<<nblocks, 256, 0, s>>>(k_in, v_in, n, shift, nblocks, w.hist, k_out,
+                                                               v_out);
+      }
       uint32_t* t = k_in; k_in = k_out; k_out = t;
       t = v_in; v_in = v_out; v_out = t;
     }

@@ -42,6 +42,8 @@ def _run(n, P, R, src, rel, dst):
     (50_000, 8, 3, 300_000, 3),     # the follower graph's 8 partitions at a small size
     (10, 10, 2, 777, 4),            # one entity per partition, 100 buckets
     (70_001, 16, 1, 9_000, 5),      # more buckets than edges in some of them (empty buckets)
+    (5_000, 20, 2, 30_000, 6),      # 400 buckets: the radix-sort path (one 8-bit pass + one more bit)
+    (100_000, 40, 1, 50_000, 7),    # 1600 buckets: two radix passes
 ])
 def test_bucket_edges_matches_oracle(n, P, R, m, seed):
     rng = synth.rng_for(seed)
