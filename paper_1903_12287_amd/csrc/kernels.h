@@ -120,6 +120,7 @@ struct SortWork {
   uint32_t* hist;       // [256][max blocks]
   uint32_t* scan_tmp;   // block sums of the multi-launch scan
   float* partial;       // [max_n][width] per-block partial sums of segments
+  uint32_t* segflag;    // [max_n / 32 + 2] piece flags per block of 32 sorted positions
   int max_n;
 };
 

@@ -253,7 +253,8 @@ __device__ __forceinline__ void seg_apply(const StepGeom& g, const StepBufs& b, 
 template <int MODE, int RQ>
 __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, const uint32_t* keys,
                                                         const uint32_t* vals, int n, const float* rows,
-                                                        int64_t ld, int width, float* partial, float lr) {
+                                                        int64_t ld, int width, float* partial, uint32_t* segflag,
+                                                        float lr) {
   constexpr int SB = 16 / RQ;                      // positions per batch of loads
   const int lane = threadIdx.x & 63;
   const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -274,6 +275,13 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
   const bool cont_prev = !(segs & 1u);                  // first piece continues an earlier block
   const bool cont_next = !((sege >> (np - 1)) & 1u);    // last piece continues into the next block
   const int last_start = 31 - __builtin_clz(pstart);
+  // piece flags of this block for the spanning-segment pass: bit 1 the first
+  // piece continues an earlier block, bit 2 the last piece continues into the
+  // next, bit 4 the block is one piece continuing an earlier block; bits 8..
+  // the position of the last piece's start
+  if (lane == 0)
+    segflag[blk] = (cont_prev ? 1u : 0u) | (cont_next ? 2u : 0u) | ((pstart == 1u && cont_prev) ? 4u : 0u) |
+                   ((uint32_t)last_start << 8);
 
   float run[RQ];
 #pragma unroll
@@ -376,34 +384,36 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
 
 // segments that cross block boundaries, updated by the wave of the block
 // where they start: its last piece plus the leading piece of every following
-// block the segment covers, added in block order, 16 loads in flight
+// block the segment covers, added in block order, 16 loads in flight; the
+// extent comes from the piece flags the local pass left per block
 template <int MODE, int RQ>
 __global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, const uint32_t* keys, int n,
-                                                       int width, const float* partial, float lr) {
+                                                       int width, const float* partial, const uint32_t* segflag,
+                                                       float lr) {
   const int lane = threadIdx.x & 63;
   const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int p0 = blk * SEG_BLOCK;
   const int p1 = p0 + SEG_BLOCK;
   if (p1 >= n) return;
-  const uint32_t key = keys[p1 - 1];
-  if (keys[p1] != key) return;                       // nothing crosses the end of this block
-  // start of the crossing segment; not this block's if it starts before p0
-  int lo = p0, hi = p1 - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (keys[mid] < key) lo = mid + 1;
-    else hi = mid;
+  const uint32_t f = segflag[blk];
+  if (!(f & 2u) || (f & 4u)) return;     // nothing crosses the end, or the segment started earlier
+  const int s = p0 + (int)(f >> 8);      // start of the crossing segment
+  const uint32_t key = keys[s];
+  // blocks the segment covers entirely (flags 2 | 4), 64 flags per probe; it
+  // ends inside the first following block that is not one of them
+  const int nblk = (n + SEG_BLOCK - 1) / SEG_BLOCK;
+  int nfull = 0;
+  for (int j0 = blk + 1;; j0 += 64) {
+    const int j = j0 + lane;
+    const uint32_t fj = j < nblk ? segflag[j] : 0u;
+    const uint64_t stop = __ballot((fj & 6u) != 6u);
+    if (stop) {
+      nfull += __ffsll((unsigned long long)stop) - 1;
+      break;
+    }
+    nfull += 64;
   }
-  const int s = lo;
-  if (s == p0 && p0 > 0 && keys[p0 - 1] == key) return;
-  // end of the segment: first position after it
-  int a = p1, z = n;
-  while (a < z) {
-    const int mid = a + ((z - a) >> 1);
-    if (keys[mid] <= key) a = mid + 1;
-    else z = mid;
-  }
-  const int nparts = 1 + (a - 1 - p1) / SEG_BLOCK + 1;   // block of s, then blocks p1, p1 + 32, ...
+  const int nparts = 1 + nfull + 1;   // block of s, the covered blocks, the block where it ends
   RowT<RQ> acc;
   row_zero(acc);
   for (int i0 = 0; i0 < nparts; i0 += 16) {
@@ -563,14 +573,17 @@ static void seg_update(const StepGeom& g, const StepBufs& b, const uint32_t* key
   if (n <= 0) return;
   const int blocks = (n + 4 * SEG_BLOCK - 1) / (4 * SEG_BLOCK);
   if (width <= 128) {
-    seg_update_local<MODE, 2><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial, lr);
-    seg_update_span<MODE, 2><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, lr);
+    seg_update_local<MODE, 2><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial,
+                                                      w.segflag, lr);
+    seg_update_span<MODE, 2><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, w.segflag, lr);
   } else if (width <= 256) {
-    seg_update_local<MODE, 4><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial, lr);
-    seg_update_span<MODE, 4><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, lr);
+    seg_update_local<MODE, 4><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial,
+                                                      w.segflag, lr);
+    seg_update_span<MODE, 4><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, w.segflag, lr);
   } else {
-    seg_update_local<MODE, 8><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial, lr);
-    seg_update_span<MODE, 8><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, lr);
+    seg_update_local<MODE, 8><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial,
+                                                      w.segflag, lr);
+    seg_update_span<MODE, 8><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, w.segflag, lr);
   }
 }
 

@@ -73,6 +73,7 @@ bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width) {
   w.hist = (uint32_t*)a.get(radix_hist_entries(max_n) * 4);
   w.scan_tmp = (uint32_t*)a.get(radix_scan_tmp_entries(max_n) * 4);
   w.partial = width > 0 ? (float*)a.get(max_n * (int64_t)width * 4) : nullptr;
+  w.segflag = (uint32_t*)a.get((max_n / 32 + 2) * 4);
   return !a.failed;
 }
 
