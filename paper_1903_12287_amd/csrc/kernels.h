@@ -84,6 +84,11 @@ void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s);
 // Cm; EPI_LOSS_BITS; EPI_SOFTMAX_STATS) on the bf16 instructions, operands
 // Af / Bf split into exact bf16 pieces on the way into LDS
 void launch_score_split(const GemmArgsH& a, int epi, int batches, hipStream_t s);
+// dQ = dS . N (a0: Af = dS rows [e][t]) and dN = dS^T . Q (a1: Af = the same
+// dS rows, read by columns) in one launch, dS a general float32 matrix split
+// into exact bf16 pieces on the way into LDS, B the three transposed planes
+// of N / Q (planes = 3, b_ps apart); six piece products
+void launch_gemm_split_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s);
 // two EPI_STORE products in one launch: a0 with A as dS rows (GA_BITS_ROW or
 // GA_KC), a1 with A as dS columns (GA_BITS_COL or GA_MC), same planes
 void launch_gemm_bf16_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s);

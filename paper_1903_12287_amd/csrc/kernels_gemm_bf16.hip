@@ -663,6 +663,143 @@ __global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles
   tile_epilogue<BN, EPI>(a, t, acc, sm.red, sm.rowv);
 }
 
+// ---- float32 backward products of a general dS on the bf16 instructions ----
+// dQ = dS . N and dN = dS^T . Q for the logistic and softmax losses: dS is
+// float32, so it is split into its three pieces on the way into LDS like the
+// score operands, B comes as the three transposed planes of N or Q, and the
+// six products hh, hm, mh, hl, mm, lh are summed (as in the score).
+
+// TX rows (m) x 32 k of a float32 [k][m] matrix (m contiguous, ld floats):
+// each thread loads two consecutive k rows of four consecutive m, splits the
+// pairs (k, k + 1) of each m and stores them as one 32-bit word per plane
+// into the [m][k] tile.
+template <int TX>
+struct TileSM {
+  static constexpr int LOADS = TX * BK / 8 / 256;   // (k pair, m quad) per thread
+
+  __device__ __forceinline__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim,
+                                              int tid) {
+    const int x4 = (xdim + 3) & ~3;
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      const int kp = f / (TX / 4), xq = f % (TX / 4);
+      const int gk = k0 + 2 * kp, gx = x0 + 4 * xq;
+      uint32_t o0 = OOB, o1 = OOB;
+      if (gx < x4) {
+        if (gk < kdim) o0 = (uint32_t)(((int64_t)gk * ld + gx) * 4);
+        if (gk + 1 < kdim) o1 = (uint32_t)(((int64_t)(gk + 1) * ld + gx) * 4);
+      }
+      r[2 * q] = __builtin_amdgcn_raw_buffer_load_b128(rs, o0, 0, 0);
+      r[2 * q + 1] = __builtin_amdgcn_raw_buffer_load_b128(rs, o1, 0, 0);
+    }
+  }
+
+  __device__ __forceinline__ static void store(uint16_t (*s)[TX * BK], const v4f* r, int tid) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      const int kp = f / (TX / 4), xq = f % (TX / 4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t pc[3];
+        split3_pair(r[2 * q][i], r[2 * q + 1][i], pc);
+        const int o = swz(4 * xq + i, kp >> 2) + ((2 * kp) & 7);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) *(uint32_t*)(s[p] + o) = pc[p];
+      }
+    }
+  }
+};
+
+// One 128 x 128 output tile of dS . B (AF = 0: dS rows, A = dS [m][k]) or
+// dS^T . B (AF = 1: A[m][k] = dS[k][m]); one LDS buffer.
+template <int AF>
+__device__ __forceinline__ void gemm_split_tile(const GemmArgsH& a, int tiles_n, int tiles_m, int nwg, int id,
+                                                SmemS& sm) {
+  constexpr int BN = 128, WN = 64, JN = 4;
+  using TB = TileH<BN, GA_KC>;
+  TileGeo t;
+  if (!tile_geo<BN, EPI_STORE>(a, tiles_n, tiles_m, nwg, id, t)) return;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int l16 = lane & 15, g = lane >> 4;
+  const rsrc_t ra = make_rsrc(a.Af + t.c * a.a_cs + t.side * a.a_ss);
+  rsrc_t rb[3];
+#pragma unroll
+  for (int p = 0; p < 3; ++p) rb[p] = make_rsrc(a.B + p * a.b_ps + t.c * a.b_cs + t.side * a.b_ss);
+  v4f acc[4][JN];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < JN; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
+
+  constexpr int ALOADS = AF == 0 ? 2 * TileS<BM>::LOADS : 2 * TileSM<BM>::LOADS;
+  v4f pa[ALOADS];
+  u32x4 pb[3][TB::LOADS];
+  const int nk = (t.K + BK - 1) / BK;
+  auto load_a = [&](int k0) {
+    if (AF == 0) TileS<BM>::load(pa, ra, a.lda, t.m0, t.M, k0, t.K, tid);
+    else TileSM<BM>::load(pa, ra, a.lda, t.m0, t.M, k0, t.K, tid);
+  };
+  auto store_a = [&]() {
+    if (AF == 0) TileS<BM>::store(sm.As, pa, tid);
+    else TileSM<BM>::store(sm.As, pa, tid);
+  };
+  load_a(0);
+#pragma unroll
+  for (int p = 0; p < 3; ++p) TB::load(pb[p], rb[p], a.ldb, t.n0, t.N, 0, t.K, tid);
+  store_a();
+#pragma unroll
+  for (int p = 0; p < 3; ++p) TB::store(sm.Bs[p], pb[p], tid, 0, 0, 0);
+  __syncthreads();
+
+  const int fa0 = swz(64 * wm + l16, g), fb0 = swz(WN * wn + l16, g);
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) {
+      load_a((kt + 1) * BK);
+#pragma unroll
+      for (int p = 0; p < 3; ++p) TB::load(pb[p], rb[p], a.ldb, t.n0, t.N, (kt + 1) * BK, t.K, tid);
+    }
+#pragma unroll
+    for (int pa_ = 0; pa_ < 3; ++pa_) {
+      v8bf af[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = *(const v8bf*)(sm.As[pa_] + fa0 + 16 * i * BK);
+#pragma unroll
+      for (int pb_ = 0; pb_ < 3 - pa_; ++pb_) {
+        v8bf bf[JN];
+#pragma unroll
+        for (int j = 0; j < JN; ++j) bf[j] = *(const v8bf*)(sm.Bs[pb_] + fb0 + 16 * j * BK);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < JN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+      }
+    }
+    if (kt + 1 < nk) {
+      __syncthreads();
+      store_a();
+#pragma unroll
+      for (int p = 0; p < 3; ++p) TB::store(sm.Bs[p], pb[p], tid, 0, 0, 0);
+      __syncthreads();
+    }
+  }
+  tile_epilogue<BN, EPI_STORE>(a, t, acc, sm.red, sm.rowv);
+}
+
+// dQ (workgroups [0, nwg0)) and dN (the rest) of a step in one launch
+__global__ __launch_bounds__(256) void gemm_split_pair_kernel(GemmArgsH a0, int tn0, int tm0, int nwg0,
+                                                              GemmArgsH a1, int tn1, int tm1) {
+  __shared__ __align__(16) SmemS sm;
+  const int id = blockIdx.x;
+  if (id < nwg0) gemm_split_tile<0>(a0, tn0, tm0, nwg0, id, sm);
+  else gemm_split_tile<1>(a1, tn1, tm1, (int)gridDim.x - nwg0, id - nwg0, sm);
+}
+
 template <int BN, int AMODE, int EPI, int PL>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgsH a, int tiles_n, int tiles_m) {
   __shared__ __align__(16) SmemH<BN, PL> sm;
@@ -859,6 +996,17 @@ void launch_pair_bn(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipSt
   else launch_pair_t<BN, GA_KC, GA_MC, 1>(a0, a1, batches, s);
 }
 }  // namespace
+
+void launch_gemm_split_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s) {
+  if (batches <= 0) return;
+  const int tn0 = (dim_max(a0.ndim, a0.Nfix, a0.C, a0.U) + 127) / 128;
+  const int tm0 = (dim_max(a0.mdim, a0.Mfix, a0.C, a0.U) + BM - 1) / BM;
+  const int tn1 = (dim_max(a1.ndim, a1.Nfix, a1.C, a1.U) + 127) / 128;
+  const int tm1 = (dim_max(a1.mdim, a1.Mfix, a1.C, a1.U) + BM - 1) / BM;
+  const int64_t nwg0 = (int64_t)tn0 * tm0 * batches, nwg1 = (int64_t)tn1 * tm1 * batches;
+  if (nwg0 + nwg1 <= 0) return;
+  gemm_split_pair_kernel<<<(unsigned)(nwg0 + nwg1), 256, 0, s>>>(a0, tn0, tm0, (int)nwg0, a1, tn1, tm1);
+}
 
 void launch_gemm_bf16_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s) {
   const int maxN = std::max(dim_max(a0.ndim, a0.Nfix, a0.C, a0.U), dim_max(a1.ndim, a1.Nfix, a1.C, a1.U));

@@ -119,32 +119,36 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   launch_finalize(g, b, ctx->steploss_dev + t, cs);
   mark(3);
 
+  // Q and N in three exact bf16 pieces each, transposed (the B operands of
+  // both backward products)
+  const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
+  const BufsH& h = ctx->h;
+  launch_split3_planes(b.qk, (int64_t)C * dp, C, dp, g.d, nullptr, 0, 0, 0, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps,
+                       Cpb, Cpb, dpb, nch * 2, cs);
+  launch_split3_planes(b.nn, (int64_t)N * dp, N, dp, g.d, nullptr, 0, 0, 0, h.nnT3, (int64_t)dpb * Npb, h.n3_ps,
+                       Npb, Npb, dpb, nch * 2, cs);
   if (bits) {
-    // dS is 0 or 1: exact products on the bf16 instructions with Q and N in
-    // three exact bf16 pieces each (transposed planes), float32 sums
-    const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
-    const BufsH& h = ctx->h;
-    launch_split3_planes(b.qk, (int64_t)C * dp, C, dp, g.d, nullptr, 0, 0, 0, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps,
-                         Cpb, Cpb, dpb, nch * 2, cs);
-    launch_split3_planes(b.nn, (int64_t)N * dp, N, dp, g.d, nullptr, 0, 0, 0, h.nnT3, (int64_t)dpb * Npb, h.n3_ps,
-                         Npb, Npb, dpb, nch * 2, cs);
+    // dS is 0 or 1: its products with the pieces are exact (float32 sums)
     run_backward_h(g, b, nullptr, h.nnT3, h.n3_ps, h.qkT3, h.q3_ps, 3, cs);
     return;
   }
-  // dQ = dS . N (per side)
-  GemmArgs qa;
+  // general float32 dS (logistic, softmax): split into pieces as it is staged,
+  // six piece products
+  GemmArgsH qa;
   memset(&qa, 0, sizeof(qa));
-  qa.A = b.ds;
-  qa.B = b.nn;
-  qa.Cm = b.dq;
+  qa.Af = b.ds;
   qa.a_cs = 2ll * C * Np;
   qa.a_ss = (int64_t)C * Np;
-  qa.b_cs = 2ll * N * dp;
-  qa.b_ss = (int64_t)N * dp;
+  qa.lda = Np;
+  qa.B = h.nnT3;
+  qa.planes = 3;
+  qa.b_ps = h.n3_ps;
+  qa.b_cs = 2ll * dpb * Npb;
+  qa.b_ss = (int64_t)dpb * Npb;
+  qa.ldb = Npb;
+  qa.Cm = b.dq;
   qa.c_cs = 2ll * C * dp;
   qa.c_ss = (int64_t)C * dp;
-  qa.lda = Np;
-  qa.ldb = dp;
   qa.ldc = dp;
   qa.mdim = DIM_CC;
   qa.ndim = DIM_FIXED;
@@ -154,25 +158,18 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   qa.U = U;
   qa.m_step = g.m_step;
   qa.nsides = 2;
-  if (bits) {
-    qa.A = nullptr;
-    qa.Ab = b.dsb;
-    qa.a_cs = 2ll * nw * ldw;
-    qa.a_ss = (int64_t)nw * ldw;
-    qa.lda = ldw;
-  }
-  launch_gemm_f32(qa, GEMM_NN, EPI_STORE, nch * 2, cs);
-  // dN = dS^T . Q (per side)
-  GemmArgs na = qa;
-  na.B = b.qk;
+  GemmArgsH na = qa;
+  na.B = h.qkT3;
+  na.b_ps = h.q3_ps;
+  na.b_cs = 2ll * dpb * Cpb;
+  na.b_ss = (int64_t)dpb * Cpb;
+  na.ldb = Cpb;
   na.Cm = b.dn;
-  na.b_cs = 2ll * C * dp;
-  na.b_ss = (int64_t)C * dp;
   na.c_cs = 2ll * N * dp;
   na.c_ss = (int64_t)N * dp;
   na.mdim = DIM_NC;
   na.kdim = DIM_CC;
-  launch_gemm_f32(na, GEMM_TN, EPI_STORE, nch * 2, cs);
+  launch_gemm_split_pair(qa, na, nch * 2, cs);
 }
 
 void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t,

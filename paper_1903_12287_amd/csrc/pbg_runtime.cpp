@@ -139,7 +139,8 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
     ctx->h.qkT = (uint16_t*)a.get(s * 2 * dpb * Cpb * 2);
     ctx->h.nnT = (uint16_t*)a.get(s * 2 * dpb * Npb * 2);
     if (!ranking) ctx->h.ds = (uint16_t*)a.get(s * 2 * C * (int64_t)Npb * 2);
-  } else if (ranking) {
+  } else {
+    // float32 backward on the bf16 instructions: transposed pieces of Q and N
     const int dpb = round_up(d, 32), Cpb = round_up(C, 32), Npb = round_up(N, 32);
     ctx->h.q3_ps = s * 2 * dpb * (int64_t)Cpb;
     ctx->h.n3_ps = s * 2 * dpb * (int64_t)Npb;
