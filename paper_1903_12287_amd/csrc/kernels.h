@@ -12,37 +12,25 @@
 // strides cb_cs / cb_ss in words)
 enum { EPI_STORE = 0, EPI_LOSS = 1, EPI_SOFTMAX_STATS = 2, EPI_LOSS_BITS = 3 };
 enum { DIM_CC = 0, DIM_NC = 1, DIM_FIXED = 2 };
-// operand layouts: NT  A[m][k], B[n][k];  NN  A[m][k], B[k][n];  TN  A[k][m], B[k][n]
-enum { GEMM_NT = 0, GEMM_NN = 1, GEMM_TN = 2 };
+// float32 operand layouts: NT  A[m][k], B[n][k];  TN  A[k][m], B[k][n]
+enum { GEMM_NT = 0, GEMM_TN = 2 };
 
 struct GemmArgs {
   const float* A;
   const float* B;
   float* Cm;
-  const uint16_t* Ab;    // A as a bit matrix in the dsb layout (a_cs, a_ss, lda = row pitch, in words), or NULL
-  uint16_t* dsb;         // EPI_LOSS_BITS output
-  int64_t cb_cs, cb_ss;
-  int ldcb, nwcb;
   int64_t a_cs, a_ss, b_cs, b_ss, c_cs, c_ss;  // strides (floats) per chunk and per side
   int lda, ldb, ldc;
   int mdim, ndim, kdim;  // DIM_* selectors
   int Mfix, Nfix, Kfix;
   int C, U, m_step;      // chunk geometry (m_step = 0: not chunked)
-  int nsides;            // batches per chunk (2: one per corruption side)
-  int accumulate;        // EPI_STORE: add to C instead of overwriting it
-  // loss epilogue
-  const float* pos;      // [S][C]
-  const float* bias;     // [S][C] added to side 1 scores (translation + dot), or NULL
-  float* rowpart;        // [S][2][C][nct][2]
-  int nct;
-  int loss;
-  float margin;
+  int nsides;            // batches per chunk
+  int accumulate;        // add to C instead of overwriting it
 };
 
-int gemm_pick_nb(int n);
-// float32 contraction of `batches` (chunk, side) pairs; the tiling and grid
-// follow from the largest M and N of the batches
-void launch_gemm_f32(const GemmArgs& a, int layout, int epi, int batches, hipStream_t s);
+// float32 contraction C = A . B (or C += A . B) of `batches` (chunk, side)
+// pairs; the tiling and grid follow from the largest M and N of the batches
+void launch_gemm_f32(const GemmArgs& a, int layout, int batches, hipStream_t s);
 
 // bf16 contractions, fp32 accumulation.  B is bf16 [n][k] (k contiguous,
 // zero-padded to 8); A is one of

@@ -1,25 +1,22 @@
-// Chunk x candidates contractions on the gfx950 matrix cores, float32 (Sec.
-// 4.3: the scores of a chunk against its negatives form one matrix product,
-// Fig. 3).
+// Float32 contractions on the gfx950 matrix cores (v_mfma_f32_16x16x4_f32),
+// for the small products of the linear operator (Sec. 3.1: g(x) = A x with one
+// relation, formed for a whole step: Q = X A^T, K = Y A, and in the backward
+// X and Y gradients and dA).  The chunk x candidates contractions of the score
+// and its backward run on the bf16 instructions (kernels_gemm_bf16.hip).
 //
-//   forward   S  = Q . N^T   (C x N, K = dim)  + fused loss epilogue
-//   backward  dQ = dS . N    (C x dim, K = N)
-//             dN = dS^T . Q  (N x dim, K = C)
-//
-// One kernel template covers all three.  A 256-thread workgroup (4 waves in
-// a 2 x 2 arrangement) computes a 128 x BN tile (BN = 128, or 64 for narrow
-// outputs) with v_mfma_f32_16x16x4_f32; each wave owns 64 x BN/2 outputs,
-// i.e. 4 x BN/32 blocks of 16 x 16.
+// A 256-thread workgroup (4 waves in a 2 x 2 arrangement) computes a 128 x BN
+// tile (BN = 128, or 64 for narrow outputs); each wave owns 64 x BN/2 outputs,
+// i.e. 4 x BN/32 blocks of 16 x 16.  Layouts: NT  A[m][k], B[n][k];
+// TN  A[k][m], B[k][n].
 //
 // Operands reach LDS through buffer loads (a load whose offset is out of the
 // buffer's range returns zeros, which pads ragged tiles without branches) and
 // a register-held prefetch of the next 16-deep k-slice, double-buffered in
-// LDS.  An operand that is contiguous along k in memory (rows of Q, N, dS) is
-// kept as [row][k] (pitch 20 floats) and read back as one 128-bit fragment per
-// 16 x 16 block and k-slice; an operand contiguous along its row/column index
-// (N and Q in dQ, dS^T and Q in dN) is kept as [k][row] (pitch BM + 4) and
-// read one float per step.  Both layouts are free of LDS bank conflicts for
-// the fragment reads.
+// LDS.  An operand that is contiguous along k is kept as [row][k] (pitch 20
+// floats) and read back as one 128-bit fragment per 16 x 16 block and
+// k-slice; an operand contiguous along its row index is kept as [k][row]
+// (pitch BM + 4) and read one float per step.  Both layouts are free of LDS
+// bank conflicts for the fragment reads.
 //
 // The 16x16x4 instruction sums A[m][k] B[k][n] over the four k held by the
 // four 16-lane groups (lane L: A row L % 16, B column L % 16, k index L / 16).
@@ -27,10 +24,8 @@
 // of four consecutive k feeds four steps; every k of the slice is used once.
 // Accumulator: lane L, register r holds D[4 (L / 16) + r][L % 16].
 //
-// Workgroups are numbered so that the tiles of one batch (one chunk and side)
-// run on the same XCD, whose L2 then holds that batch's operands.
-#include <type_traits>
-
+// Workgroups are numbered so that the tiles of one batch run on the same XCD,
+// whose L2 then holds that batch's operands.
 #include "kernels.h"
 #include "device_common.h"
 
@@ -96,62 +91,14 @@ struct Tile {
   }
 };
 
-// The same tile read from a 0/1 matrix stored as bits (ranking-loss dS):
-// bit b of word (w, row) is column 16 w + b of that row, and the words are
-// stored word-column major, word (w, row) at w * ld + row (ld = row pitch), so
-// that a 16-deep k-slice of consecutive rows is one contiguous run of words.
-// Each float4 of the tile is four bits of one word, expanded to 0.0 / 1.0.
-template <int TX, bool KC>
-struct BitTile {
-  static constexpr int LOADS = TX * BK / 4 / 256;
-  static constexpr int SIZE = Tile<TX, KC>::SIZE;
-
-  __device__ __forceinline__ static v4f expand(uint32_t w, int shift) {
-    const uint32_t b = w >> shift;
-    return (v4f){(float)(b & 1u), (float)((b >> 1) & 1u), (float)((b >> 2) & 1u), (float)((b >> 3) & 1u)};
-  }
-
-  __device__ __forceinline__ static void load(v4f* r, rsrc_t rs, int ld, int x0, int xdim, int k0, int kdim, int tid) {
-#pragma unroll
-    for (int q = 0; q < LOADS; ++q) {
-      const int f = tid + 256 * q;
-      uint32_t off = OOB;
-      int shift;
-      if (KC) {
-        const int x = f >> 2, kq = f & 3;
-        const int gx = x0 + x, gk = k0 + 4 * kq;
-        if (gx < xdim && gk < ((kdim + 3) & ~3)) off = (uint32_t)(((int64_t)(gk >> 4) * ld + gx) * 2);
-        shift = gk & 15;
-      } else {
-        const int k = f / (TX / 4), xq = f % (TX / 4);
-        const int gk = k0 + k, gx = x0 + 4 * xq;
-        if (gk < kdim && gx < ((xdim + 3) & ~3)) off = (uint32_t)(((int64_t)(gx >> 4) * ld + gk) * 2);
-        shift = gx & 15;
-      }
-      // the raw word and its shift stay in registers until the store, so that
-      // nothing waits for the load before the matrix work of the slice
-      const uint32_t word = __builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0);
-      r[q] = (v4f){__uint_as_float(word), __uint_as_float((uint32_t)shift), 0.0f, 0.0f};
-    }
-  }
-
-  __device__ __forceinline__ static void store(float* s, const v4f* r, int tid) {
-    v4f e[LOADS];
-#pragma unroll
-    for (int q = 0; q < LOADS; ++q) e[q] = expand(__float_as_uint(r[q].x), (int)__float_as_uint(r[q].y));
-    Tile<TX, KC>::store(s, e, tid);
-  }
-};
-
-template <int BN, bool AK, bool BKC, int EPI, bool ABITS>
+template <int BN, bool AK, bool BKC>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int tiles_n, int tiles_m) {
   constexpr int WN = BN / 2;       // columns per wave
   constexpr int JN = WN / 16;      // 16-wide column blocks per wave
-  using TA = typename std::conditional<ABITS, BitTile<BM, AK>, Tile<BM, AK>>::type;
+  using TA = Tile<BM, AK>;
   using TB = Tile<BN, BKC>;
   __shared__ __align__(16) float As[2][TA::SIZE];
   __shared__ __align__(16) float Bs[2][TB::SIZE];
-  __shared__ float red[2][BM][2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -182,20 +129,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int tiles_n, 
   const int n0 = tn * BN;
   if (m0 >= M) return;
 
-  float* rowpart = nullptr;
-  if (EPI != EPI_STORE) rowpart = a.rowpart + ((int64_t)(c * 2 + side) * a.C) * a.nct * 2;
-  if (n0 >= N) {
-    // neutral row partials: no valid column in this tile
-    if (EPI != EPI_STORE && tid < BM && m0 + tid < M) {
-      float* rp = rowpart + ((int64_t)(m0 + tid) * a.nct + tn) * 2;
-      rp[0] = (EPI == EPI_SOFTMAX_STATS) ? -INFINITY : 0.0f;
-      rp[1] = 0.0f;
-    }
-    return;
-  }
+  if (n0 >= N) return;
 
-  const rsrc_t ra_s = ABITS ? make_rsrc((const float*)(a.Ab + c * a.a_cs + side * a.a_ss))
-                            : make_rsrc(a.A + c * a.a_cs + side * a.a_ss);
+  const rsrc_t ra_s = make_rsrc(a.A + c * a.a_cs + side * a.a_ss);
   const rsrc_t rb_s = make_rsrc(a.B + c * a.b_cs + side * a.b_ss);
 
   v4f acc[4][JN];
@@ -264,169 +200,46 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int tiles_n, 
 
   float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
   const int colb = n0 + WN * wn + l16;
-
-  if (EPI == EPI_STORE) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
-        if (m < M) {
-#pragma unroll
-          for (int j = 0; j < JN; ++j) {
-            const int n = colb + 16 * j;
-            if (n < N) {
-              float* o = Cm + (int64_t)m * a.ldc + n;
-              *o = a.accumulate ? *o + acc[i][j][r] : acc[i][j][r];
-            }
-          }
-        }
-      }
-    return;
-  }
-
-  // loss epilogues: M = Cc rows, valid columns [0, Nc) minus the diagonal,
-  // stored columns [0, ldc).  Each wave leaves its row partials over its half
-  // of the tile's columns in LDS; they are combined left half first.
-  const float* pos = a.pos + (int64_t)c * a.C;
-  // translation + dot: source corruptions score <x_t, x_d> + <theta_r, x_d>
-  const float* bias = (a.bias && side == 1) ? a.bias + (int64_t)c * a.C : nullptr;
-  const float kinv = (Nc - 1 > 0) ? 1.0f / (float)(Nc - 1) : 0.0f;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int ml = 64 * wm + 16 * i + 4 * g + r;
-      const int m = m0 + ml;
-      const bool mrow = m < M;
-      const float p = mrow ? pos[m] : 0.0f;
-      const float bm = (bias && mrow) ? bias[m] : 0.0f;
-      float v0, v1;
-      if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
-        float lsum = 0.0f, dsum = 0.0f;
+      const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
+      if (m < M) {
 #pragma unroll
         for (int j = 0; j < JN; ++j) {
           const int n = colb + 16 * j;
-          const float s = acc[i][j][r] + bm;
-          const bool valid = mrow && n < N && n != m;
-          float dsv = 0.0f;
-          if (EPI == EPI_LOSS_BITS || a.loss == LOSS_RANKING) {
-            const float zz = a.margin - p + s;
-            if (valid && zz > 0.0f) {
-              dsv = 1.0f;
-              lsum += zz;
-            }
-          } else if (valid) {
-            float sg, sp;
-            logistic_pair(s, sg, sp);
-            dsv = sg * kinv;
-            lsum += sp * kinv;
-          }
-          dsum += dsv;
-          if (EPI == EPI_LOSS_BITS) {
-            // 16 lanes of a lane group hold 16 consecutive columns of one row
-            const uint64_t mask = __ballot(dsv != 0.0f);
-            const int wcol = (n0 + WN * wn + 16 * j) >> 4;
-            if (l16 == 0 && mrow && wcol < a.nwcb)
-              a.dsb[c * a.cb_cs + side * a.cb_ss + (int64_t)wcol * a.ldcb + m] = (uint16_t)(mask >> (16 * g));
-          } else if (mrow && n < a.ldc) {
-            Cm[(int64_t)m * a.ldc + n] = dsv;
+          if (n < N) {
+            float* o = Cm + (int64_t)m * a.ldc + n;
+            *o = a.accumulate ? *o + acc[i][j][r] : acc[i][j][r];
           }
         }
-        v0 = group16_sum(lsum);
-        v1 = group16_sum(dsum);
-      } else {  // EPI_SOFTMAX_STATS: raw scores + per-tile (max, sum exp)
-        float mx = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < JN; ++j) {
-          const int n = colb + 16 * j;
-          const float s = acc[i][j][r] + bm;
-          if (mrow && n < N && n != m) mx = fmaxf(mx, s);
-          if (mrow && n < a.ldc) Cm[(int64_t)m * a.ldc + n] = s;
-        }
-        mx = group16_max(mx);
-        float se = 0.0f;
-#pragma unroll
-        for (int j = 0; j < JN; ++j) {
-          const int n = colb + 16 * j;
-          if (mrow && n < N && n != m) se += expf(acc[i][j][r] + bm - mx);
-        }
-        v0 = mx;
-        v1 = group16_sum(se);
-      }
-      if (l16 == 0) {
-        red[wn][ml][0] = v0;
-        red[wn][ml][1] = v1;
       }
     }
-  __syncthreads();
-  if (tid < BM && m0 + tid < M) {
-    const int ml = tid;
-    float v0, v1;
-    if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
-      v0 = red[0][ml][0] + red[1][ml][0];
-      v1 = red[0][ml][1] + red[1][ml][1];
-    } else {
-      const float ma = red[0][ml][0], mb = red[1][ml][0];
-      const float mx = fmaxf(ma, mb);
-      v0 = mx;
-      v1 = (mx == -INFINITY) ? 0.0f
-                             : (ma == -INFINITY ? 0.0f : red[0][ml][1] * expf(ma - mx)) +
-                                   (mb == -INFINITY ? 0.0f : red[1][ml][1] * expf(mb - mx));
-    }
-    float* rp = rowpart + ((int64_t)(m0 + ml) * a.nct + tn) * 2;
-    rp[0] = v0;
-    rp[1] = v1;
-  }
 }
 
-template <int BN, bool AK, bool BKC, int EPI, bool ABITS>
+template <int BN, bool AK, bool BKC>
 void launch_t(const GemmArgs& a, int tiles_n, int tiles_m, int batches, hipStream_t s) {
   const int64_t nwg = (int64_t)tiles_n * tiles_m * batches;
-  gemm_f32_kernel<BN, AK, BKC, EPI, ABITS><<<(unsigned)nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
-}
-
-template <bool ABITS>
-void launch_store(const GemmArgs& a, int layout, bool narrow, int tiles_n, int tiles_m, int batches,
-                  hipStream_t s) {
-  if (layout == GEMM_NT) {
-    if (narrow) launch_t<64, true, true, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
-    else launch_t<128, true, true, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
-  } else if (layout == GEMM_NN) {
-    if (narrow) launch_t<64, true, false, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
-    else launch_t<128, true, false, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
-  } else {
-    if (narrow) launch_t<64, false, false, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
-    else launch_t<128, false, false, EPI_STORE, ABITS>(a, tiles_n, tiles_m, batches, s);
-  }
+  gemm_f32_kernel<BN, AK, BKC><<<(unsigned)nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
 }
 
 int dim_max(int sel, int fixed, int C, int U) { return sel == DIM_CC ? C : (sel == DIM_NC ? C + U : fixed); }
 
 }  // namespace
 
-void launch_gemm_f32(const GemmArgs& a, int layout, int epi, int batches, hipStream_t s) {
+void launch_gemm_f32(const GemmArgs& a, int layout, int batches, hipStream_t s) {
   const int maxM = dim_max(a.mdim, a.Mfix, a.C, a.U);
   const int maxN = dim_max(a.ndim, a.Nfix, a.C, a.U);
   if (maxM <= 0 || maxN <= 0 || batches <= 0) return;
   const int tiles_m = (maxM + BM - 1) / BM;
-  if (epi != EPI_STORE) {
-    const int tiles_n = (maxN + 127) / 128;   // = nct (PBG_SCORE_BN columns per tile)
-    if (epi == EPI_LOSS) launch_t<128, true, true, EPI_LOSS, false>(a, tiles_n, tiles_m, batches, s);
-    else if (epi == EPI_LOSS_BITS) launch_t<128, true, true, EPI_LOSS_BITS, false>(a, tiles_n, tiles_m, batches, s);
-    else launch_t<128, true, true, EPI_SOFTMAX_STATS, false>(a, tiles_n, tiles_m, batches, s);
-    return;
-  }
   const bool narrow = maxN <= 64;
   const int tiles_n = (maxN + (narrow ? 63 : 127)) / (narrow ? 64 : 128);
-  if (a.Ab) launch_store<true>(a, layout, narrow, tiles_n, tiles_m, batches, s);
-  else launch_store<false>(a, layout, narrow, tiles_n, tiles_m, batches, s);
-}
-
-// column blocks of 16 per tile for an output of width n: as few tiles as
-// possible, each at most 128 wide (tile choice of the bfloat16 contractions)
-int gemm_pick_nb(int n) {
-  const int blocks = (n + 15) / 16;
-  const int tiles = (blocks + 7) / 8;
-  return (blocks + tiles - 1) / tiles;
+  if (layout == GEMM_NT) {
+    if (narrow) launch_t<64, true, true>(a, tiles_n, tiles_m, batches, s);
+    else launch_t<128, true, true>(a, tiles_n, tiles_m, batches, s);
+  } else {
+    if (narrow) launch_t<64, false, false>(a, tiles_n, tiles_m, batches, s);
+    else launch_t<128, false, false>(a, tiles_n, tiles_m, batches, s);
+  }
 }

@@ -604,7 +604,7 @@ __global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles
   __shared__ __align__(16) SmemS sm;
   TileGeo t;
   if (!tile_geo<BN, EPI>(a, tiles_n, tiles_m, gridDim.x, blockIdx.x, t)) return;
-  load_rowv<EPI>(a, t, sm.rowv);
+  if (EPI != EPI_STORE) load_rowv<EPI>(a, t, sm.rowv);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
@@ -1025,7 +1025,8 @@ void launch_score_split(const GemmArgsH& a, int epi, int batches, hipStream_t s)
   const unsigned nwg = (unsigned)((int64_t)tiles_n * tiles_m * batches);
   if (epi == EPI_LOSS) score_split_kernel<EPI_LOSS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
   else if (epi == EPI_LOSS_BITS) score_split_kernel<EPI_LOSS_BITS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
-  else score_split_kernel<EPI_SOFTMAX_STATS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+  else if (epi == EPI_SOFTMAX_STATS) score_split_kernel<EPI_SOFTMAX_STATS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+  else score_split_kernel<EPI_STORE, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
 }
 
 void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d,

@@ -272,9 +272,9 @@ static GemmArgs linear_args(const StepGeom& g, const float* A, int64_t a_cs, con
 void run_linear_forward(const StepGeom& g, const StepBufs& b, const float* Ap, const float* ATp, hipStream_t cs) {
   const int64_t n_cs = 2ll * g.N * g.dp, q_cs = 2ll * g.C * g.dp;
   GemmArgs q = linear_args(g, b.nn + (int64_t)g.N * g.dp, n_cs, Ap, b.qk, q_cs);     // Q = X A^T
-  launch_gemm_f32(q, GEMM_NT, EPI_STORE, g.nchunks, cs);
+  launch_gemm_f32(q, GEMM_NT, g.nchunks, cs);
   GemmArgs k = linear_args(g, b.nn, n_cs, ATp, b.qk + (int64_t)g.C * g.dp, q_cs);    // K = Y A
-  launch_gemm_f32(k, GEMM_NT, EPI_STORE, g.nchunks, cs);
+  launch_gemm_f32(k, GEMM_NT, g.nchunks, cs);
   launch_positive_scores(g, b, cs);
 }
 
@@ -286,8 +286,8 @@ void run_linear_backward(const StepGeom& g, const StepBufs& b, const float* Ap, 
   const int64_t n_cs = 2ll * g.N * g.dp, q_cs = 2ll * g.C * g.dp;
   GemmArgs s = linear_args(g, b.dq, q_cs, ATp, b.dn + (int64_t)g.N * g.dp, n_cs);
   s.accumulate = 1;
-  launch_gemm_f32(s, GEMM_NT, EPI_STORE, g.nchunks, cs);
+  launch_gemm_f32(s, GEMM_NT, g.nchunks, cs);
   GemmArgs d = linear_args(g, b.dq + (int64_t)g.C * g.dp, q_cs, Ap, b.dn, n_cs);
   d.accumulate = 1;
-  launch_gemm_f32(d, GEMM_NT, EPI_STORE, g.nchunks, cs);
+  launch_gemm_f32(d, GEMM_NT, g.nchunks, cs);
 }

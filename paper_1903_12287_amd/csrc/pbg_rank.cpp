@@ -159,10 +159,11 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
     for (int64_t e0 = 0; e0 < n; e0 += qb) {
       const int rows = (int)std::min<int64_t>(qb, n - e0);
       launch_rank_queries(g, pt.emb, ctx->relp, relT, src, rel, dst, e0, rows, side, Q, pos, bias, s);
-      GemmArgs a;
+      // candidate scores S = Q . T^T, float32 operands as exact bf16 pieces
+      GemmArgsH a;
       memset(&a, 0, sizeof(a));
-      a.A = Q;
-      a.B = T;
+      a.Af = Q;
+      a.Bf = T;
       a.Cm = S;
       a.lda = dp;
       a.ldb = dp;
@@ -175,7 +176,7 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
       a.Kfix = dp;
       a.C = 1;
       a.nsides = 1;
-      launch_gemm_f32(a, GEMM_NT, EPI_STORE, 1, s);
+      launch_score_split(a, EPI_STORE, 1, s);
       launch_rank_count(S, n_ent, n_ent, e0, rows, side, n, src, rel, dst, pos, bias,
                         side == 0 ? kx[0] : kx[3], side == 0 ? kx[1] : kx[4], side == 0 ? kx[2] : kx[5],
                         n_known, ranks, s);

@@ -475,14 +475,14 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
         la.U = U;
         la.m_step = m_step;
         la.nsides = 1;
-        launch_gemm_f32(la, GEMM_TN, EPI_STORE, nch, cs);
+        launch_gemm_f32(la, GEMM_TN, nch, cs);
         GemmArgs lb = la;
         lb.A = b.nn;                       // destination rows x_d (N0[e])
         lb.B = b.dq + (int64_t)C * dp;     // dK
         lb.Cm = ctx->relpartial + (int64_t)d * d;
         lb.a_cs = 2ll * N * dp;
         lb.b_cs = 2ll * C * dp;
-        launch_gemm_f32(lb, GEMM_TN, EPI_STORE, nch, cs);
+        launch_gemm_f32(lb, GEMM_TN, nch, cs);
         launch_relation_single_adagrad(ctx->relp, ctx->relG, d * d, ctx->relpartial, 2 * nch, lr, cs);
       } else if (ctx->R > 1) {
         uint32_t *rk = nullptr, *rv = nullptr;
