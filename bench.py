@@ -340,7 +340,7 @@ def row_knowledge_graph():
         st = pbg.pbg_get_stats(ctx)
         out["value"] = w.E / dt
         out["ms_per_pass"] = dt * 1e3
-        out["roofline"] = roofline(st, PEAK_FP32_MFMA, "score_split_kernel<EPI_SOFTMAX_STATS, 6> (score)",
+        out["roofline"] = roofline(st, PEAK_FP32_MFMA, "score_split_kernel<EPI_SOFTMAX_EXP, 6> (score)",
                                    pieces=6)
         out["phases_ms_per_step"] = phases(st)
         # filtered ranks of the held-out triples, known = train + held-out

@@ -71,11 +71,12 @@ struct StepBufs {
   int32_t* neg;         // [S][2][U] uniform draws (side 0 from partition j, side 1 from i)
   float* ds;            // [S][2][C][Np] dL/dS (logistic, softmax)
   uint16_t* dsb;        // [S][2][ceil(Np/16)][C] dL/dS bits (ranking, float32 path)
-  float* rowpart;       // [S][2][C][nct][2]
-  float* rowstat;       // [S][2][C]  log-sum-exp per side (softmax)
+  float* rowpart;       // [S][2][C][nct][2]  per score tile: (loss, dS sum) or, for
+                        // softmax, (tile max, sum exp(s - tile max))
+  float* rowscale;      // [S][2][nct][C]  softmax on split pieces: exp(tile max - lse)
   float* dpos;          // [S][C] dL/dp
   float* dsum1;         // [S][C] sum_t dS1[e][t]
-  double* chunkloss;    // [S]
+  double* chunkloss;    // [S][FIN_BLOCKS(C)]  loss partials of the finalisation
   float* dq;
   float* dn;
   float* relc;          // [S][N][dr] relation gradient contributions

@@ -10,7 +10,7 @@
 // EPI_LOSS_BITS: ranking loss with dS (0 or 1) written as bits, 16 columns per
 // uint16 word, word (w, row) at dsb[w * ldcb + row] (nwcb words per row; batch
 // strides cb_cs / cb_ss in words)
-enum { EPI_STORE = 0, EPI_LOSS = 1, EPI_SOFTMAX_STATS = 2, EPI_LOSS_BITS = 3 };
+enum { EPI_STORE = 0, EPI_LOSS = 1, EPI_SOFTMAX_STATS = 2, EPI_LOSS_BITS = 3, EPI_SOFTMAX_EXP = 4 };
 enum { DIM_CC = 0, DIM_NC = 1, DIM_FIXED = 2 };
 // float32 operand layouts: NT  A[m][k], B[n][k];  TN  A[k][m], B[k][n]
 enum { GEMM_NT = 0, GEMM_TN = 2 };
@@ -47,6 +47,8 @@ struct GemmArgsH {
   int64_t b_ps;
   const float* Af;       // launch_score_split: float32 operands [m][k] and [n][k]
   const float* Bf;
+  const float* smscale;  // launch_gemm_split_pair: Af holds exp(s - tile max) of the softmax loss and
+                         // smscale[(z * nct + tile) * C + row] = exp(tile max - lse) (z = chunk*2 + side)
   float* Cm;             // fp32 output (STORE, SOFTMAX_STATS)
   uint16_t* dsh;         // EPI_LOSS: dS rows in bf16 (strides c_*, ldc)
   uint16_t* dsb;         // EPI_LOSS_BITS output (as in GemmArgs)
@@ -75,7 +77,9 @@ void launch_score_split(const GemmArgsH& a, int epi, int batches, hipStream_t s)
 // dQ = dS . N (a0: Af = dS rows [e][t]) and dN = dS^T . Q (a1: Af = the same
 // dS rows, read by columns) in one launch, dS a general float32 matrix split
 // into exact bf16 pieces on the way into LDS, B the three transposed planes
-// of N / Q (planes = 3, b_ps apart); six piece products
+// of N / Q (planes = 3, b_ps apart); six piece products.  With smscale set,
+// Af holds the per-tile exponentials of the softmax loss and dS is formed on
+// the way
 void launch_gemm_split_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s);
 // two EPI_STORE products in one launch: a0 with A as dS rows (GA_BITS_ROW or
 // GA_KC), a1 with A as dS columns (GA_BITS_COL or GA_MC), same planes
@@ -101,9 +105,14 @@ void launch_pad_linear(const float* A, int d, int dp, float* Ap, float* ATp, hip
 void launch_positive_scores(const StepGeom& g, const StepBufs& b, hipStream_t s);
 
 // ---- loss finalisation and backward -----------------------------------------
-void launch_softmax_rows(const StepGeom& g, const StepBufs& b, hipStream_t s);
 void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s);
-void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, hipStream_t s);
+// The finalisation runs fin_blocks(C) workgroups of FIN_THREADS rows per
+// chunk; softmax_scales: it also writes rowscale = exp(tile max - lse) for the
+// backward on split pieces (score epilogue EPI_SOFTMAX_EXP)
+#define FIN_THREADS 256
+inline int fin_blocks(int C) { return (C + FIN_THREADS - 1) / FIN_THREADS; }
+void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, bool softmax_scales,
+                     hipStream_t s);
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s);
 
 // ---- sort, segments, updates ----------------------------------------------------

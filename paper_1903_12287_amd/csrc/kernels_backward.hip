@@ -14,40 +14,13 @@
 
 namespace {
 
-// ---- softmax: log-sum-exp per row and side, then dS = softmax in place -----
-__global__ __launch_bounds__(256) void softmax_rows_kernel(StepGeom g, StepBufs b) {
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);   // over C rows of one (chunk, side)
-  const int z = blockIdx.y;                               // chunk * 2 + side
-  const int c = z >> 1;
-  const int Cc = chunk_edges(g, c);
-  if (row >= Cc) return;
-  const int Nc = Cc + g.U;
-  const float p = b.pos[(int64_t)c * g.C + row];
-  const float* rp = b.rowpart + ((int64_t)z * g.C + row) * g.nct * 2;
-  float M = p;
-  for (int ct = 0; ct < g.nct; ++ct) M = fmaxf(M, rp[2 * ct]);
-  float Z = expf(p - M);
-  for (int ct = 0; ct < g.nct; ++ct) {
-    const float mx = rp[2 * ct];
-    if (mx > -INFINITY) Z += rp[2 * ct + 1] * expf(mx - M);
-  }
-  const float lse = M + logf(Z);
-  if (lane == 0) b.rowstat[(int64_t)z * g.C + row] = lse;
-  float* ds = b.ds + ((int64_t)z * g.C + row) * g.Np;
-  for (int t = lane; t < g.Np; t += 64) {
-    float v = 0.0f;
-    if (t < Nc && t != row) v = expf(ds[t] - lse);
-    ds[t] = v;
-  }
-}
-
 // ---- per-edge dL/dp, translation bias gradient, losses ------------------------
-__global__ __launch_bounds__(1024) void finalize_kernel(StepGeom g, StepBufs b) {
-  const int c = blockIdx.x;
+__global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepBufs b, int softmax_scales) {
+  const int c = blockIdx.y;
   const int Cc = chunk_edges(g, c);
   double acc = 0.0;
-  for (int e = threadIdx.x; e < Cc; e += blockDim.x) {
+  const int e = blockIdx.x * FIN_THREADS + threadIdx.x;
+  if (e < Cc) {
     const int64_t ce = (int64_t)c * g.C + e;
     const float p = b.pos[ce];
     float l0 = 0.f, l1 = 0.f, d0 = 0.f, d1 = 0.f;
@@ -74,8 +47,30 @@ __global__ __launch_bounds__(1024) void finalize_kernel(StepGeom g, StepBufs b) 
       dp = 2.0f * (sigmoidf(p) - 1.0f);
       dsum1 = d1;
     } else {
-      const float lse0 = b.rowstat[(int64_t)(c * 2 + 0) * g.C + e];
-      const float lse1 = b.rowstat[(int64_t)(c * 2 + 1) * g.C + e];
+      // log-sum-exp of each side's row over {p} and its valid candidates, from
+      // the per-tile (max M, sum exp(s - M)) partials; each tile's sum is then
+      // replaced by exp(M - lse), which turns the stored exp(s - M) into dS
+      float lse[2];
+#pragma unroll
+      for (int side = 0; side < 2; ++side) {
+        const float* rp = b.rowpart + ((int64_t)(c * 2 + side) * g.C + e) * g.nct * 2;
+        float M = p;
+        for (int ct = 0; ct < g.nct; ++ct) M = fmaxf(M, rp[2 * ct]);
+        float Z = expf(p - M);
+        for (int ct = 0; ct < g.nct; ++ct) {
+          const float mx = rp[2 * ct];
+          if (mx > -INFINITY) Z += rp[2 * ct + 1] * expf(mx - M);
+        }
+        lse[side] = M + logf(Z);
+        if (softmax_scales) {
+          float* rs = b.rowscale + (int64_t)(c * 2 + side) * g.nct * g.C + e;
+          for (int ct = 0; ct < g.nct; ++ct) {
+            const float mx = rp[2 * ct];
+            rs[(int64_t)ct * g.C] = mx > -INFINITY ? expf(mx - lse[side]) : 0.0f;
+          }
+        }
+      }
+      const float lse0 = lse[0], lse1 = lse[1];
       loss = ((double)lse0 - p) + ((double)lse1 - p);
       const float s0 = expf(p - lse0), s1 = expf(p - lse1);
       dp = (s0 - 1.0f) + (s1 - 1.0f);
@@ -85,15 +80,15 @@ __global__ __launch_bounds__(1024) void finalize_kernel(StepGeom g, StepBufs b) 
     b.dsum1[ce] = dsum1;
     acc += loss;
   }
-  // fixed-order block reduction of the chunk loss
-  __shared__ double red[1024];
+  // fixed-order block reduction of this workgroup's share of the chunk loss
+  __shared__ double red[FIN_THREADS];
   red[threadIdx.x] = acc;
   __syncthreads();
-  for (int o = 512; o > 0; o >>= 1) {
+  for (int o = FIN_THREADS / 2; o > 0; o >>= 1) {
     if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
     __syncthreads();
   }
-  if (threadIdx.x == 0) b.chunkloss[c] = red[0];
+  if (threadIdx.x == 0) b.chunkloss[(int64_t)c * gridDim.x + blockIdx.x] = red[0];
 }
 
 __global__ void sum_chunks_kernel(const double* chunkloss, int n, double* out) {
@@ -277,14 +272,12 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
 
 }  // namespace
 
-void launch_softmax_rows(const StepGeom& g, const StepBufs& b, hipStream_t s) {
-  dim3 grid((g.C + 3) / 4, g.nchunks * 2);
-  softmax_rows_kernel<<<grid, 256, 0, s>>>(g, b);
-}
 
-void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, hipStream_t s) {
-  finalize_kernel<<<g.nchunks, 1024, 0, s>>>(g, b);
-  sum_chunks_kernel<<<1, 64, 0, s>>>(b.chunkloss, g.nchunks, step_loss_slot);
+void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, bool softmax_scales,
+                     hipStream_t s) {
+  const int fb = fin_blocks(g.C);
+  finalize_kernel<<<dim3(fb, g.nchunks), FIN_THREADS, 0, s>>>(g, b, softmax_scales ? 1 : 0);
+  sum_chunks_kernel<<<1, 64, 0, s>>>(b.chunkloss, g.nchunks * fb, step_loss_slot);
 }
 
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s) {

@@ -217,7 +217,7 @@ __device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int ti
     const int tid = threadIdx.x;
     if (EPI != EPI_STORE && tid < BM && t.m0 + tid < t.M) {
       float* rp = a.rowpart + (((int64_t)(t.c * 2 + t.side) * a.C + t.m0 + tid) * a.nct + t.tn) * 2;
-      rp[0] = (EPI == EPI_SOFTMAX_STATS) ? -INFINITY : 0.0f;
+      rp[0] = (EPI == EPI_SOFTMAX_STATS || EPI == EPI_SOFTMAX_EXP) ? -INFINITY : 0.0f;
       rp[1] = 0.0f;
     }
     return false;
@@ -380,6 +380,62 @@ __device__ __forceinline__ void value_rows(const GemmArgsH& a, const TileGeo& t,
     }
 }
 
+// Softmax rows of a tile for the backward on split pieces: the tile's row
+// maximum M over the valid columns (both column halves), then exp(s - M) on
+// the valid columns and 0 elsewhere (columns past the batch, the diagonal)
+// goes to Cm and its row sum to the partials.  dS = exp(s - M) exp(M - lse)
+// is completed in the backward once lse is known.
+template <int BN, bool MASKED>
+__device__ __forceinline__ void softmax_exp_rows(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[4][BN / 32],
+                                                 float (&red)[2][BM][2], const float (&rowv)[2][BM]) {
+  constexpr int WN = BN / 2;
+  constexpr int JN = WN / 16;
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int M = t.M, N = t.N, m0 = t.m0;
+  const int colb = t.n0 + WN * wn + l16;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int ml = 64 * wm + 16 * i + 4 * g + r;
+      const int m = m0 + ml;
+      const float bm = rowv[1][ml];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < JN; ++j) {
+        const int n = colb + 16 * j;
+        acc[i][j][r] += bm;
+        if (m < M && !(MASKED && (n >= N || n == m))) mx = fmaxf(mx, acc[i][j][r]);
+      }
+      mx = group16_max(mx);
+      if (l16 == 0) red[wn][ml][0] = mx;
+    }
+  __syncthreads();
+  float* Cm = a.Cm + t.c * a.c_cs + t.side * a.c_ss;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int ml = 64 * wm + 16 * i + 4 * g + r;
+      const int m = m0 + ml;
+      const float mt = fmaxf(red[0][ml][0], red[1][ml][0]);
+      float se = 0.0f;
+#pragma unroll
+      for (int j = 0; j < JN; ++j) {
+        const int n = colb + 16 * j;
+        const bool valid = m < M && !(MASKED && (n >= N || n == m));
+        const float ev = valid ? expf(acc[i][j][r] - mt) : 0.0f;
+        se += ev;
+        if (m < M && n < a.ldc) Cm[(int64_t)m * a.ldc + n] = ev;
+      }
+      se = group16_sum(se);
+      if (l16 == 0) red[wn][ml][1] = se;
+    }
+}
+
 // Stores the tile (EPI_STORE) or runs the loss epilogue on it: dS leaves as
 // bits (ranking), as bf16 rows (logistic, when dsh is set) or float32 rows in
 // Cm, or the raw float32 scores go to Cm for the softmax row pass; row
@@ -421,6 +477,9 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
   if (EPI == EPI_LOSS_BITS) {
     if (masked) bits_rows<BN, true>(a, t, acc, red, rowv);
     else bits_rows<BN, false>(a, t, acc, red, rowv);
+  } else if (EPI == EPI_SOFTMAX_EXP) {
+    if (masked) softmax_exp_rows<BN, true>(a, t, acc, red, rowv);
+    else softmax_exp_rows<BN, false>(a, t, acc, red, rowv);
   } else {
     if (masked) value_rows<BN, EPI, true>(a, t, acc, red, rowv);
     else value_rows<BN, EPI, false>(a, t, acc, red, rowv);
@@ -431,6 +490,9 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
     float v0, v1;
     if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
       v0 = red[0][ml][0] + red[1][ml][0];
+      v1 = red[0][ml][1] + red[1][ml][1];
+    } else if (EPI == EPI_SOFTMAX_EXP) {
+      v0 = fmaxf(red[0][ml][0], red[1][ml][0]);
       v1 = red[0][ml][1] + red[1][ml][1];
     } else {
       const float ma = red[0][ml][0], mb = red[1][ml][0];
@@ -713,8 +775,12 @@ struct TileSM {
 };
 
 // One 128 x 128 output tile of dS . B (AF = 0: dS rows, A = dS [m][k]) or
-// dS^T . B (AF = 1: A[m][k] = dS[k][m]); one LDS buffer.
-template <int AF>
+// dS^T . B (AF = 1: A[m][k] = dS[k][m]); one LDS buffer.  SM: softmax, dS is
+// formed as A is staged, dS[e][t] = exp(s[e][t] - lse[e]) on the valid
+// candidates t (t < Nc, t != e) of the valid rows e (e < Cc), else 0: the A
+// source holds exp(s - M) per score tile (0 off the valid set) and each row
+// is scaled by exp(M - lse) of its tile.
+template <int AF, bool SM>
 __device__ __forceinline__ void gemm_split_tile(const GemmArgsH& a, int tiles_n, int tiles_m, int nwg, int id,
                                                 SmemS& sm) {
   constexpr int BN = 128, WN = 64, JN = 4;
@@ -736,15 +802,56 @@ __device__ __forceinline__ void gemm_split_tile(const GemmArgsH& a, int tiles_n,
 #pragma unroll
     for (int j = 0; j < JN; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
 
-  constexpr int ALOADS = AF == 0 ? 2 * TileS<BM>::LOADS : 2 * TileSM<BM>::LOADS;
-  v4f pa[ALOADS];
+  constexpr int AQ = AF == 0 ? TileS<BM>::LOADS : TileSM<BM>::LOADS;   // A groups per thread
+  v4f pa[2 * AQ];
   u32x4 pb[3][TB::LOADS];
+  // softmax: the scale exp(M - lse) of this thread's rows in the score tile
+  // of the staged slice (AF = 0: one row per group, the tile of the slice's
+  // columns, reloaded when the slice enters a new tile; AF = 1: two rows per
+  // group, the tile of this output tile's rows)
+  static_assert(BM == PBG_SCORE_BN && BK <= PBG_SCORE_BN, "slices and tiles within one score tile");
+  const int Cc = AF == 0 ? t.M : t.K;
+  const float* rsc = SM ? a.smscale + (int64_t)(t.c * 2 + t.side) * a.nct * a.C : nullptr;
+  float lr[2 * AQ];
   const int nk = (t.K + BK - 1) / BK;
   auto load_a = [&](int k0) {
-    if (AF == 0) TileS<BM>::load(pa, ra, a.lda, t.m0, t.M, k0, t.K, tid);
-    else TileSM<BM>::load(pa, ra, a.lda, t.m0, t.M, k0, t.K, tid);
+    if (AF == 0) {
+      TileS<BM>::load(pa, ra, a.lda, t.m0, t.M, k0, t.K, tid);
+      if (SM && (k0 & 127) == 0) {
+        const float* rc = rsc + (int64_t)(k0 >> 7) * a.C;
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) {
+          const int e = t.m0 + ((tid + 256 * q) >> 2);
+          lr[q] = e < Cc ? rc[e] : 0.0f;
+        }
+      }
+    } else {
+      TileSM<BM>::load(pa, ra, a.lda, t.m0, t.M, k0, t.K, tid);
+      if (SM) {
+        const float* rc = rsc + (int64_t)(t.m0 >> 7) * a.C;
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) {
+          const int e = k0 + 2 * ((tid + 256 * q) / (BM / 4));
+          lr[2 * q] = e < Cc ? rc[e] : 0.0f;
+          lr[2 * q + 1] = e + 1 < Cc ? rc[e + 1] : 0.0f;
+        }
+      }
+    }
+  };
+  auto softmax_a = [&]() {
+#pragma unroll
+    for (int q = 0; q < AQ; ++q) {
+      if (AF == 0) {
+        pa[2 * q] *= lr[q];
+        pa[2 * q + 1] *= lr[q];
+      } else {
+        pa[2 * q] *= lr[2 * q];
+        pa[2 * q + 1] *= lr[2 * q + 1];
+      }
+    }
   };
   auto store_a = [&]() {
+    if (SM) softmax_a();
     if (AF == 0) TileS<BM>::store(sm.As, pa, tid);
     else TileSM<BM>::store(sm.As, pa, tid);
   };
@@ -792,12 +899,13 @@ __device__ __forceinline__ void gemm_split_tile(const GemmArgsH& a, int tiles_n,
 }
 
 // dQ (workgroups [0, nwg0)) and dN (the rest) of a step in one launch
+template <bool SM>
 __global__ __launch_bounds__(256) void gemm_split_pair_kernel(GemmArgsH a0, int tn0, int tm0, int nwg0,
                                                               GemmArgsH a1, int tn1, int tm1) {
   __shared__ __align__(16) SmemS sm;
   const int id = blockIdx.x;
-  if (id < nwg0) gemm_split_tile<0>(a0, tn0, tm0, nwg0, id, sm);
-  else gemm_split_tile<1>(a1, tn1, tm1, (int)gridDim.x - nwg0, id - nwg0, sm);
+  if (id < nwg0) gemm_split_tile<0, SM>(a0, tn0, tm0, nwg0, id, sm);
+  else gemm_split_tile<1, SM>(a1, tn1, tm1, (int)gridDim.x - nwg0, id - nwg0, sm);
 }
 
 template <int BN, int AMODE, int EPI, int PL>
@@ -898,11 +1006,9 @@ __global__ __launch_bounds__(256) void split3_planes_kernel(const float* src, in
 }
 
 // softmax row pass in bf16 mode: raw fp32 scores -> dS = softmax (masked),
-// written as bf16 rows and into the transposed copy
+// written as bf16 rows
 __global__ __launch_bounds__(256) void softmax_rows_bf16_kernel(StepGeom g, const float* S, const float* rowpart,
-                                                                const float* pos, float* rowstat,
-                                                                uint16_t* dsh, uint16_t* dsT, int ldh,
-                                                                int ldt) {
+                                                                const float* pos, uint16_t* dsh, int ldh) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int z = blockIdx.y;
@@ -920,17 +1026,13 @@ __global__ __launch_bounds__(256) void softmax_rows_bf16_kernel(StepGeom g, cons
     if (mx > -INFINITY) Z += rp[2 * ct + 1] * expf(mx - Mx);
   }
   const float lse = Mx + logf(Z);
-  if (lane == 0) rowstat[(int64_t)z * g.C + row] = lse;
   const float* srow = S + ((int64_t)z * g.C + row) * g.Np;
   uint16_t* hrow = dsh + ((int64_t)z * g.C) * ldh + (int64_t)row * ldh;
-  uint16_t* tcol = dsT ? dsT + ((int64_t)z * g.N) * ldt + row : nullptr;
   const int Nh = (Nc + 31) & ~31;
   for (int t = lane; t < Nh; t += 64) {
     float v = 0.0f;
     if (t < Nc && t != row) v = expf(srow[t] - lse);
-    const uint16_t h = f_to_bf16(v);
-    hrow[t] = h;
-    if (dsT) tcol[(int64_t)t * ldt] = h;
+    hrow[t] = f_to_bf16(v);
   }
 }
 
@@ -1005,7 +1107,8 @@ void launch_gemm_split_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batche
   const int tm1 = (dim_max(a1.mdim, a1.Mfix, a1.C, a1.U) + BM - 1) / BM;
   const int64_t nwg0 = (int64_t)tn0 * tm0 * batches, nwg1 = (int64_t)tn1 * tm1 * batches;
   if (nwg0 + nwg1 <= 0) return;
-  gemm_split_pair_kernel<<<(unsigned)(nwg0 + nwg1), 256, 0, s>>>(a0, tn0, tm0, (int)nwg0, a1, tn1, tm1);
+  if (a0.smscale) gemm_split_pair_kernel<true><<<(unsigned)(nwg0 + nwg1), 256, 0, s>>>(a0, tn0, tm0, (int)nwg0, a1, tn1, tm1);
+  else gemm_split_pair_kernel<false><<<(unsigned)(nwg0 + nwg1), 256, 0, s>>>(a0, tn0, tm0, (int)nwg0, a1, tn1, tm1);
 }
 
 void launch_gemm_bf16_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s) {
@@ -1025,7 +1128,7 @@ void launch_score_split(const GemmArgsH& a, int epi, int batches, hipStream_t s)
   const unsigned nwg = (unsigned)((int64_t)tiles_n * tiles_m * batches);
   if (epi == EPI_LOSS) score_split_kernel<EPI_LOSS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
   else if (epi == EPI_LOSS_BITS) score_split_kernel<EPI_LOSS_BITS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
-  else if (epi == EPI_SOFTMAX_STATS) score_split_kernel<EPI_SOFTMAX_STATS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+  else if (epi == EPI_SOFTMAX_EXP) score_split_kernel<EPI_SOFTMAX_EXP, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
   else score_split_kernel<EPI_STORE, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
 }
 
@@ -1048,5 +1151,5 @@ void launch_split3_planes(const float* src, int64_t src_bs, int rows, int ld_src
 
 void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s) {
   dim3 grid((g.C + 3) / 4, g.nchunks * 2);
-  softmax_rows_bf16_kernel<<<grid, 256, 0, s>>>(g, b.ds, b.rowpart, b.pos, b.rowstat, dsh, nullptr, ldh, 0);
+  softmax_rows_bf16_kernel<<<grid, 256, 0, s>>>(g, b.ds, b.rowpart, b.pos, dsh, ldh);
 }

@@ -104,7 +104,7 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   fa.loss = g.loss;
   fa.margin = g.margin;
   const int nw = (Np + 15) / 16, ldw = rup(C, 8);   // bit-matrix words per row, row pitch
-  int epi = g.loss == LOSS_SOFTMAX ? EPI_SOFTMAX_STATS : EPI_LOSS;
+  int epi = g.loss == LOSS_SOFTMAX ? EPI_SOFTMAX_EXP : EPI_LOSS;
   if (bits) {
     epi = EPI_LOSS_BITS;
     fa.dsb = b.dsb;
@@ -115,8 +115,10 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   }
   launch_score_split(fa, epi, nch * 2, cs);
   mark(2);
-  if (g.loss == LOSS_SOFTMAX) launch_softmax_rows(g, b, cs);
-  launch_finalize(g, b, ctx->steploss_dev + t, cs);
+  // softmax: the score pass leaves exp(s - tile max), the finalisation each
+  // row's log-sum-exp and per-tile scales, and the backward forms dS as it
+  // stages the exponentials
+  launch_finalize(g, b, ctx->steploss_dev + t, g.loss == LOSS_SOFTMAX, cs);
   mark(3);
 
   // Q and N in three exact bf16 pieces each, transposed (the B operands of
@@ -137,6 +139,8 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   GemmArgsH qa;
   memset(&qa, 0, sizeof(qa));
   qa.Af = b.ds;
+  qa.smscale = g.loss == LOSS_SOFTMAX ? b.rowscale : nullptr;
+  qa.nct = g.nct;
   qa.a_cs = 2ll * C * Np;
   qa.a_ss = (int64_t)C * Np;
   qa.lda = Np;
@@ -234,7 +238,7 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
     launch_gemm_bf16(fa, EPI_LOSS, nch * 2, cs);
     mark(2);
   }
-  launch_finalize(g, b, ctx->steploss_dev + t, cs);
+  launch_finalize(g, b, ctx->steploss_dev + t, false, cs);
   mark(3);
 
   run_backward_h(g, b, h.ds, h.nnT, 0, h.qkT, 0, 1, cs);

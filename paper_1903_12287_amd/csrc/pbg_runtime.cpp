@@ -101,10 +101,10 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   b.ds = ranking ? nullptr : (float*)a.get(s * 2 * C * (int64_t)Np * 4);
   b.dsb = ranking ? (uint16_t*)a.get(s * 2 * (int64_t)round_up(C, 8) * ((Np + 15) / 16) * 2) : nullptr;
   b.rowpart = (float*)a.get(s * 2 * C * nct * 2 * 4);
-  b.rowstat = (float*)a.get(s * 2 * C * 4);
+  if (ctx->loss == PBG_LOSS_SOFTMAX) b.rowscale = (float*)a.get(s * 2 * nct * (int64_t)C * 4);
   b.dpos = (float*)a.get(s * C * 4);
   b.dsum1 = (float*)a.get(s * C * 4);
-  b.chunkloss = (double*)a.get(s * 8);
+  b.chunkloss = (double*)a.get(s * fin_blocks(C) * 8);
   b.dq = (float*)a.get(s * 2 * C * dp * 4);
   b.dn = (float*)a.get(s * 2 * N * dp * 4);
   const bool has_rel = ctx->op != OP_IDENTITY;
