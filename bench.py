@@ -218,7 +218,7 @@ def main():
                    "chunk": C, "uniform_negatives": U, "chunks_per_step": S,
                    "edges_per_step": S * C, "partitions": 1},
         "roofline": roofline(st, PEAK_FP32_MFMA,
-                             "score_split_kernel<EPI_LOSS_BITS, 6> (float32 score + ranking epilogue)",
+                             "score_split_kernel3<EPI_LOSS_BITS, 6> (float32 score + ranking epilogue)",
                              measured_traffic("paper_1903_12287_amd/csrc/kernels_gemm_bf16.hip"), pieces=6),
         "phases_ms_per_step": phases(st),
         "backward_contractions_tflops": (2 * st["score_flops"] / 3.0) / (st["backward_ms"] / 1e3) / 1e12

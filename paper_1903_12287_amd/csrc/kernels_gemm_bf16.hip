@@ -67,7 +67,8 @@ __device__ __forceinline__ uint32_t f2_to_bf16x2(float a, float b) {
 
 // x = h + m + l exactly, each piece a bf16: h = bf16(x) leaves a remainder of
 // at most 16 significant bits, m = bf16 of that remainder leaves at most 8,
-// which l holds exactly.  Two floats at a time: pc[0..2] = packed h, m, l.
+// which l holds exactly (for |x| >= 2^-110, where every piece is a normal
+// number).  Two floats at a time: pc[0..2] = packed h, m, l.
 __device__ __forceinline__ void split3_pair(float a, float b, uint32_t* pc) {
   const uint32_t h = f2_to_bf16x2(a, b);
   const float ra = a - __uint_as_float(h << 16), rb = b - __uint_as_float(h & 0xFFFF0000u);
@@ -181,7 +182,7 @@ struct SmemH {
   float rowv[2][BM];
 };
 
-// Position of a workgroup's 128 x BN tile: `id` numbers the workgroup among
+// Position of a workgroup's TM x BN tile (TM = 128 rows unless stated): `id` numbers the workgroup among
 // the nwg of its product (hardware order) and is remapped so that all tiles of
 // one batch (chunk, side) run on one XCD.
 struct TileGeo {
@@ -190,7 +191,7 @@ struct TileGeo {
 
 // false: nothing to compute (the tile lies beyond this batch's rows, or beyond
 // its columns, where a loss epilogue still leaves neutral row partials)
-template <int BN, int EPI>
+template <int BN, int EPI, int TM = BM>
 __device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int tiles_m, int nwg, int id,
                                          TileGeo& t) {
   const int q8 = nwg >> 3, r8 = nwg & 7, xcd = id & 7;
@@ -210,12 +211,12 @@ __device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int ti
   t.M = pick_dim(a.mdim, a.Mfix, Cc, t.Nc);
   t.N = pick_dim(a.ndim, a.Nfix, Cc, t.Nc);
   t.K = pick_dim(a.kdim, a.Kfix, Cc, t.Nc);
-  t.m0 = tm * BM;
+  t.m0 = tm * TM;
   t.n0 = t.tn * BN;
   if (t.m0 >= t.M) return false;
   if (t.n0 >= t.N) {
     const int tid = threadIdx.x;
-    if (EPI != EPI_STORE && tid < BM && t.m0 + tid < t.M) {
+    if (EPI != EPI_STORE && tid < TM && t.m0 + tid < t.M) {
       float* rp = a.rowpart + (((int64_t)(t.c * 2 + t.side) * a.C + t.m0 + tid) * a.nct + t.tn) * 2;
       rp[0] = (EPI == EPI_SOFTMAX_STATS || EPI == EPI_SOFTMAX_EXP) ? -INFINITY : 0.0f;
       rp[1] = 0.0f;
@@ -229,10 +230,10 @@ __device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int ti
 // of the tile while its first operands load: the hinge threshold
 // margin - p + bias (-inf for rows past the batch) for the ranking bits, else
 // the positive score p and the bias
-template <int EPI>
-__device__ __forceinline__ void load_rowv(const GemmArgsH& a, const TileGeo& t, float (&rowv)[2][BM]) {
+template <int EPI, int TM = BM>
+__device__ __forceinline__ void load_rowv(const GemmArgsH& a, const TileGeo& t, float (&rowv)[2][TM]) {
   const int tid = threadIdx.x;
-  if (tid < BM) {
+  if (tid < TM) {
     const int m = t.m0 + tid;
     const bool mrow = m < t.M;
     const int64_t o = (int64_t)t.c * a.C + m;
@@ -251,11 +252,11 @@ __device__ __forceinline__ void load_rowv(const GemmArgsH& a, const TileGeo& t, 
 // or the masked diagonal).  Hinge z = s + margin - p, dS = [z > 0]; each lane
 // group's ballot word is the bit-matrix word of its row for these 16 columns
 // and its population count that row's share of the dS row sum.
-template <int BN, bool MASKED>
-__device__ __forceinline__ void bits_rows(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[4][BN / 32],
-                                          float (&red)[2][BM][2], const float (&rowv)[2][BM]) {
-  constexpr int WN = BN / 2;
-  constexpr int JN = WN / 16;
+template <int BN, bool MASKED, int TM = BM>
+__device__ __forceinline__ void bits_rows(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[TM / 32][BN / 32],
+                                          float (&red)[2][TM][2], const float (&rowv)[2][TM]) {
+  constexpr int WN = BN / 2, WMR = TM / 2;
+  constexpr int JN = WN / 16, IM = TM / 32;
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wm = w >> 1, wn = w & 1;
@@ -263,10 +264,10 @@ __device__ __forceinline__ void bits_rows(const GemmArgsH& a, const TileGeo& t, 
   const int colb = t.n0 + WN * wn + l16;
   const int wcol0 = (t.n0 + WN * wn) >> 4;
   // the words of four consecutive rows are adjacent (word-column major)
-  uint16_t* dbase = a.dsb + t.c * a.cb_cs + t.side * a.cb_ss + (int64_t)wcol0 * a.ldcb + t.m0 + 64 * wm + 4 * g;
+  uint16_t* dbase = a.dsb + t.c * a.cb_cs + t.side * a.cb_ss + (int64_t)wcol0 * a.ldcb + t.m0 + WMR * wm + 4 * g;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int mb = 64 * wm + 16 * i + 4 * g;   // first of this lane group's four rows
+  for (int i = 0; i < IM; ++i) {
+    const int mb = WMR * wm + 16 * i + 4 * g;   // first of this lane group's four rows
     const v4f thr = *(const v4f*)&rowv[0][mb];
     float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     uint32_t cnt[4] = {0u, 0u, 0u, 0u};
@@ -301,11 +302,11 @@ __device__ __forceinline__ void bits_rows(const GemmArgsH& a, const TileGeo& t, 
 
 // logistic loss (dS rows in bf16 or float32) and softmax statistics (raw
 // scores + per-tile max and sum of exp) rows of a tile
-template <int BN, int EPI, bool MASKED>
-__device__ __forceinline__ void value_rows(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[4][BN / 32],
-                                           float (&red)[2][BM][2], const float (&rowv)[2][BM]) {
-  constexpr int WN = BN / 2;
-  constexpr int JN = WN / 16;
+template <int BN, int EPI, bool MASKED, int TM = BM>
+__device__ __forceinline__ void value_rows(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[TM / 32][BN / 32],
+                                           float (&red)[2][TM][2], const float (&rowv)[2][TM]) {
+  constexpr int WN = BN / 2, WMR = TM / 2;
+  constexpr int JN = WN / 16, IM = TM / 32;
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wm = w >> 1, wn = w & 1;
@@ -314,10 +315,10 @@ __device__ __forceinline__ void value_rows(const GemmArgsH& a, const TileGeo& t,
   const int colb = t.n0 + WN * wn + l16;
   const float kinv = (t.Nc - 1 > 0) ? 1.0f / (float)(t.Nc - 1) : 0.0f;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < IM; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int ml = 64 * wm + 16 * i + 4 * g + r;
+      const int ml = WMR * wm + 16 * i + 4 * g + r;
       const int m = m0 + ml;
       const bool mrow = m < M;
       const float p = rowv[0][ml];
@@ -385,11 +386,12 @@ __device__ __forceinline__ void value_rows(const GemmArgsH& a, const TileGeo& t,
 // the valid columns and 0 elsewhere (columns past the batch, the diagonal)
 // goes to Cm and its row sum to the partials.  dS = exp(s - M) exp(M - lse)
 // is completed in the backward once lse is known.
-template <int BN, bool MASKED>
-__device__ __forceinline__ void softmax_exp_rows(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[4][BN / 32],
-                                                 float (&red)[2][BM][2], const float (&rowv)[2][BM]) {
-  constexpr int WN = BN / 2;
-  constexpr int JN = WN / 16;
+template <int BN, bool MASKED, int TM = BM>
+__device__ __forceinline__ void softmax_exp_rows(const GemmArgsH& a, const TileGeo& t,
+                                                 v4f (&acc)[TM / 32][BN / 32], float (&red)[2][TM][2],
+                                                 const float (&rowv)[2][TM]) {
+  constexpr int WN = BN / 2, WMR = TM / 2;
+  constexpr int JN = WN / 16, IM = TM / 32;
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wm = w >> 1, wn = w & 1;
@@ -397,10 +399,10 @@ __device__ __forceinline__ void softmax_exp_rows(const GemmArgsH& a, const TileG
   const int M = t.M, N = t.N, m0 = t.m0;
   const int colb = t.n0 + WN * wn + l16;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < IM; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int ml = 64 * wm + 16 * i + 4 * g + r;
+      const int ml = WMR * wm + 16 * i + 4 * g + r;
       const int m = m0 + ml;
       const float bm = rowv[1][ml];
       float mx = -INFINITY;
@@ -416,10 +418,10 @@ __device__ __forceinline__ void softmax_exp_rows(const GemmArgsH& a, const TileG
   __syncthreads();
   float* Cm = a.Cm + t.c * a.c_cs + t.side * a.c_ss;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < IM; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int ml = 64 * wm + 16 * i + 4 * g + r;
+      const int ml = WMR * wm + 16 * i + 4 * g + r;
       const int m = m0 + ml;
       const float mt = fmaxf(red[0][ml][0], red[1][ml][0]);
       float se = 0.0f;
@@ -441,11 +443,11 @@ __device__ __forceinline__ void softmax_exp_rows(const GemmArgsH& a, const TileG
 // Cm, or the raw float32 scores go to Cm for the softmax row pass; row
 // partials (loss, dS sum / max, sum exp) are combined over the tile's two
 // column halves and written per column tile.
-template <int BN, int EPI>
-__device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[4][BN / 32],
-                                              float (&red)[2][BM][2], const float (&rowv)[2][BM]) {
-  constexpr int WN = BN / 2;
-  constexpr int JN = WN / 16;
+template <int BN, int EPI, int TM = BM>
+__device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo& t, v4f (&acc)[TM / 32][BN / 32],
+                                              float (&red)[2][TM][2], const float (&rowv)[2][TM]) {
+  constexpr int WN = BN / 2, WMR = TM / 2;
+  constexpr int JN = WN / 16, IM = TM / 32;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
@@ -456,10 +458,10 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
   if (EPI == EPI_STORE) {
     float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < IM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = m0 + 64 * wm + 16 * i + 4 * g + r;
+        const int m = m0 + WMR * wm + 16 * i + 4 * g + r;
         if (m < M) {
 #pragma unroll
           for (int j = 0; j < JN; ++j) {
@@ -471,21 +473,21 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
     return;
   }
 
-  // column tiles past the batch's last column and the tile that holds the
-  // masked diagonal (m0 == n0 as BM == BN) need per-element checks
-  const bool masked = (n0 + BN > N) || (m0 == n0);
+  // column tiles past the batch's last column and tiles that meet the masked
+  // diagonal need per-element checks
+  const bool masked = (n0 + BN > N) || (m0 < n0 + BN && n0 < m0 + TM);
   if (EPI == EPI_LOSS_BITS) {
-    if (masked) bits_rows<BN, true>(a, t, acc, red, rowv);
-    else bits_rows<BN, false>(a, t, acc, red, rowv);
+    if (masked) bits_rows<BN, true, TM>(a, t, acc, red, rowv);
+    else bits_rows<BN, false, TM>(a, t, acc, red, rowv);
   } else if (EPI == EPI_SOFTMAX_EXP) {
-    if (masked) softmax_exp_rows<BN, true>(a, t, acc, red, rowv);
-    else softmax_exp_rows<BN, false>(a, t, acc, red, rowv);
+    if (masked) softmax_exp_rows<BN, true, TM>(a, t, acc, red, rowv);
+    else softmax_exp_rows<BN, false, TM>(a, t, acc, red, rowv);
   } else {
-    if (masked) value_rows<BN, EPI, true>(a, t, acc, red, rowv);
-    else value_rows<BN, EPI, false>(a, t, acc, red, rowv);
+    if (masked) value_rows<BN, EPI, true, TM>(a, t, acc, red, rowv);
+    else value_rows<BN, EPI, false, TM>(a, t, acc, red, rowv);
   }
   __syncthreads();
-  if (tid < BM && m0 + tid < M) {
+  if (tid < TM && m0 + tid < M) {
     const int ml = tid;
     float v0, v1;
     if (EPI == EPI_LOSS || EPI == EPI_LOSS_BITS) {
@@ -653,16 +655,20 @@ struct TileS {
 
 // one LDS buffer of three A and three B planes (single-buffered, so that
 // three workgroups fit a CU), and the row partials
-struct SmemS {
-  uint16_t As[3][BM * BK];
+template <int TM>
+struct SmemST {
+  uint16_t As[3][TM * BK];
   uint16_t Bs[3][128 * BK];
-  float red[2][BM][2];
-  float rowv[2][BM];
+  float red[2][TM][2];
+  float rowv[2][TM];
 };
+using SmemS = SmemST<BM>;
 
+// Score tile body: four waves of 64 x 64.  One A plane and one B plane in
+// registers at a time (B planes are read again for each A plane).
 template <int EPI, int NPROD>
-__global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles_n, int tiles_m) {
-  constexpr int BN = 128, WN = 64, JN = 4;
+__device__ __forceinline__ void score_split_body(const GemmArgsH& a, int tiles_n, int tiles_m) {
+  constexpr int BN = 128, WN = 64, JN = 4, WMR = BM / 2, IM = BM / 32;
   __shared__ __align__(16) SmemS sm;
   TileGeo t;
   if (!tile_geo<BN, EPI>(a, tiles_n, tiles_m, gridDim.x, blockIdx.x, t)) return;
@@ -675,9 +681,9 @@ __global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles
 
   const rsrc_t ra = make_rsrc(a.Af + t.c * a.a_cs + t.side * a.a_ss);
   const rsrc_t rb = make_rsrc(a.Bf + t.c * a.b_cs + t.side * a.b_ss);
-  v4f acc[4][JN];
+  v4f acc[IM][JN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < IM; ++i)
 #pragma unroll
     for (int j = 0; j < JN; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
 
@@ -689,19 +695,17 @@ __global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles
   TileS<BN>::store(sm.Bs, pb, tid);
   __syncthreads();
 
-  const int fa0 = swz(64 * wm + l16, g), fb0 = swz(WN * wn + l16, g);
+  const int fa0 = swz(WMR * wm + l16, g), fb0 = swz(WN * wn + l16, g);
   for (int kt = 0; kt < nk; ++kt) {
     if (kt + 1 < nk) {
       TileS<BM>::load(pa, ra, a.lda, t.m0, t.M, (kt + 1) * BK, t.K, tid);
       TileS<BN>::load(pb, rb, a.ldb, t.n0, t.N, (kt + 1) * BK, t.K, tid);
     }
-    // one A plane and one B plane in registers at a time (B planes are read
-    // again for each A plane): fewer live registers, three waves per SIMD
 #pragma unroll
     for (int pa_ = 0; pa_ < 3; ++pa_) {
-      v8bf af[4];
+      v8bf af[IM];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = *(const v8bf*)(sm.As[pa_] + fa0 + 16 * i * BK);
+      for (int i = 0; i < IM; ++i) af[i] = *(const v8bf*)(sm.As[pa_] + fa0 + 16 * i * BK);
 #pragma unroll
       for (int pb_ = 0; pb_ < 3; ++pb_) {
         if (NPROD == 6 && pa_ + pb_ > 2) continue;
@@ -709,7 +713,7 @@ __global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles
 #pragma unroll
         for (int j = 0; j < JN; ++j) bf[j] = *(const v8bf*)(sm.Bs[pb_] + fb0 + 16 * j * BK);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < IM; ++i)
 #pragma unroll
           for (int j = 0; j < JN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
@@ -723,6 +727,20 @@ __global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles
     }
   }
   tile_epilogue<BN, EPI>(a, t, acc, sm.red, sm.rowv);
+}
+
+// The ranking-bits epilogue keeps register use low enough for three waves per
+// SIMD (a few spill slots, one 16-byte slot in the k loop), which pays for the
+// short k loop of d = 128; the value epilogues spill more and run at two.
+template <int EPI, int NPROD>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) void score_split_kernel3(
+    GemmArgsH a, int tiles_n, int tiles_m) {
+  score_split_body<EPI, NPROD>(a, tiles_n, tiles_m);
+}
+
+template <int EPI, int NPROD>
+__global__ __launch_bounds__(256) void score_split_kernel(GemmArgsH a, int tiles_n, int tiles_m) {
+  score_split_body<EPI, NPROD>(a, tiles_n, tiles_m);
 }
 
 // ---- float32 backward products of a general dS on the bf16 instructions ----
@@ -1127,7 +1145,7 @@ void launch_score_split(const GemmArgsH& a, int epi, int batches, hipStream_t s)
   const int tiles_n = (maxN + 127) / 128;   // = nct (PBG_SCORE_BN columns per tile)
   const unsigned nwg = (unsigned)((int64_t)tiles_n * tiles_m * batches);
   if (epi == EPI_LOSS) score_split_kernel<EPI_LOSS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
-  else if (epi == EPI_LOSS_BITS) score_split_kernel<EPI_LOSS_BITS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
+  else if (epi == EPI_LOSS_BITS) score_split_kernel3<EPI_LOSS_BITS, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
   else if (epi == EPI_SOFTMAX_EXP) score_split_kernel<EPI_SOFTMAX_EXP, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
   else score_split_kernel<EPI_STORE, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
 }
