@@ -91,12 +91,13 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
   if (threadIdx.x == 0) b.chunkloss[(int64_t)c * gridDim.x + blockIdx.x] = red[0];
 }
 
-__global__ void sum_chunks_kernel(const double* chunkloss, int n, double* out) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) {
-    double s = 0.0;
-    for (int c = 0; c < n; ++c) s += chunkloss[c];
-    *out = s;
-  }
+// step loss = sum of the partials in a fixed order: lane l sums partials
+// l, l + 64, ... in turn, then a fixed butterfly over the wave
+__global__ __launch_bounds__(64) void sum_chunks_kernel(const double* chunkloss, int n, double* out) {
+  double s = 0.0;
+  for (int c = threadIdx.x; c < n; c += 64) s += chunkloss[c];
+  s = wave_sum_d(s);
+  if (threadIdx.x == 0) *out = s;
 }
 
 // ---- operator / comparator backward: contributions and sort keys -----------
