@@ -88,13 +88,13 @@ void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld
                               uint16_t* dst, int64_t dst_bs, int ld_dst, uint16_t* dstT,
                               int64_t dstT_bs, int ld_T, int rows_p, int kp, int batches,
                               hipStream_t s);
-// fp32 rows [rows][ld_src] -> the exact bf16 pieces x = h + m + l as three
-// row-major planes [rows][ld_R] (psR elements apart) and / or three
-// transposed planes [kp][ld_T] with zero rows up to rows_p (psT apart); a
-// null output is skipped.  kp, ld_R, rows_p, ld_T are multiples of 4.
-void launch_split3_planes(const float* src, int64_t src_bs, int rows, int ld_src, int d, uint16_t* dstR,
-                          int64_t dstR_bs, int64_t psR, int ld_R, uint16_t* dstT, int64_t dstT_bs, int64_t psT,
-                          int ld_T, int rows_p, int kp, int batches, hipStream_t s);
+// fp32 rows [rows][ld_src] of Q and of N -> the exact bf16 pieces
+// x = h + m + l as three transposed planes [kp][ld_T] each (ps elements
+// apart, rows past `rows` up to ld_T zero), both operands in one launch.
+// ld_src is a multiple of 4, ld_T of 8.
+void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,
+                     int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nT, int64_t nT_bs,
+                     int64_t n_ps, int n_ldT, int ld_src, int kp, int batches, hipStream_t s);
 
 // ---- gather / operator / negatives --------------------------------------------
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s);

@@ -974,52 +974,57 @@ __global__ __launch_bounds__(256) void to_bf16_transpose_kernel(const float* src
   }
 }
 
-// fp32 rows -> the three exact bf16 pieces (split3_pair) of every element, as
-// row-major planes [rows][ld_R] (dstR, planes psR apart, columns [d, kp)
-// zero) and / or transposed planes [kp][ld_T] (dstT, planes psT apart, rows
-// [rows, rows_p) zero); either output may be null.  64 x 64 tiles through
-// LDS; each thread writes four consecutive elements (8 bytes) per plane, so
-// kp, ld_R, rows_p and ld_T are multiples of 4.
-__global__ __launch_bounds__(256) void split3_planes_kernel(const float* src, int64_t src_bs, int rows,
-                                                            int ld_src, int d, uint16_t* dstR, int64_t dstR_bs,
-                                                            int64_t psR, int ld_R, uint16_t* dstT,
-                                                            int64_t dstT_bs, int64_t psT, int ld_T, int rows_p,
-                                                            int kp) {
+// fp32 rows [rows][ld_src] (columns [d, ld_src) zero) -> the three exact
+// bf16 pieces (split3_pair) of every element, transposed: planes [kp][ld_T],
+// ps elements apart, rows [rows, rows_p) and columns past ld_src zero.  Two
+// operands in one launch (blockIdx.z < nz0: the first).  64 x 64 tiles: each
+// thread loads 16-byte groups into an LDS tile, then gathers eight
+// consecutive rows of one column and writes 16 bytes per plane (eight lanes
+// cover 64 rows of a plane row).  ld_src is a multiple of 4, rows_p and ld_T
+// of 8.
+struct Split3T {
+  const float* src;
+  int64_t src_bs;
+  int rows, ld_src;
+  uint16_t* dst;
+  int64_t dst_bs, ps;
+  int ld_T, rows_p;
+};
+
+__global__ __launch_bounds__(256) void split3_t_kernel(Split3T o0, Split3T o1, int nz0, int kp) {
   __shared__ float tile[64][65];
-  const int b = blockIdx.z;
+  const bool first = (int)blockIdx.z < nz0;
+  const Split3T& o = first ? o0 : o1;
+  const int b = first ? blockIdx.z : blockIdx.z - nz0;
   const int r0 = blockIdx.y * 64, k0 = blockIdx.x * 64;
-  const float* s = src + (int64_t)b * src_bs;
-  for (int q = threadIdx.x; q < 64 * 64; q += 256) {
-    const int rr = q >> 6, kk = q & 63;
-    const int r = r0 + rr, k = k0 + kk;
-    tile[rr][kk] = (r < rows && k < d) ? s[(int64_t)r * ld_src + k] : 0.0f;
+  if (r0 >= o.rows_p) return;
+  const float* s = o.src + (int64_t)b * o.src_bs;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int it = threadIdx.x + 256 * j;
+    const int rr = it >> 4, k4 = 4 * (it & 15);
+    const int r = r0 + rr, k = k0 + k4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < o.rows && k < o.ld_src) v = *(const float4*)(s + (int64_t)r * o.ld_src + k);
+    tile[rr][k4] = v.x;
+    tile[rr][k4 + 1] = v.y;
+    tile[rr][k4 + 2] = v.z;
+    tile[rr][k4 + 3] = v.w;
   }
   __syncthreads();
-  if (dstR) {
-    uint16_t* o = dstR + (int64_t)b * dstR_bs;
-    for (int q = threadIdx.x; q < 64 * 16; q += 256) {
-      const int rr = q >> 4, k4 = 4 * (q & 15);
-      const int r = r0 + rr, k = k0 + k4;
-      if (r >= rows || k >= kp) continue;
-      uint32_t lo[3], hi[3];
-      split3_pair(tile[rr][k4], tile[rr][k4 + 1], lo);
-      split3_pair(tile[rr][k4 + 2], tile[rr][k4 + 3], hi);
+  uint16_t* dst = o.dst + (int64_t)b * o.dst_bs;
 #pragma unroll
-      for (int p = 0; p < 3; ++p) *(uint2*)(o + p * psR + (int64_t)r * ld_R + k) = make_uint2(lo[p], hi[p]);
-    }
-  }
-  if (dstT) {
-    uint16_t* o = dstT + (int64_t)b * dstT_bs;
-    for (int q = threadIdx.x; q < 64 * 16; q += 256) {
-      const int kk = q >> 4, r4 = 4 * (q & 15);
-      const int k = k0 + kk, r = r0 + r4;
-      if (k >= kp || r >= rows_p) continue;
-      uint32_t lo[3], hi[3];
-      split3_pair(tile[r4][kk], tile[r4 + 1][kk], lo);
-      split3_pair(tile[r4 + 2][kk], tile[r4 + 3][kk], hi);
+  for (int j = 0; j < 2; ++j) {
+    const int it = threadIdx.x + 256 * j;
+    const int kk = it >> 3, r8 = 8 * (it & 7);
+    const int k = k0 + kk, r = r0 + r8;
+    if (k >= kp || r >= o.rows_p) continue;
+    uint32_t pc[4][3];
 #pragma unroll
-      for (int p = 0; p < 3; ++p) *(uint2*)(o + p * psT + (int64_t)k * ld_T + r) = make_uint2(lo[p], hi[p]);
-    }
+    for (int i = 0; i < 4; ++i) split3_pair(tile[r8 + 2 * i][kk], tile[r8 + 2 * i + 1][kk], pc[i]);
+#pragma unroll
+    for (int p = 0; p < 3; ++p)
+      *(u32x4*)(dst + p * o.ps + (int64_t)k * o.ld_T + r) = (u32x4){pc[0][p], pc[1][p], pc[2][p], pc[3][p]};
   }
 }
 
@@ -1159,12 +1164,14 @@ void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld
                                                 dstT_bs, ld_T, rows_p, kp);
 }
 
-void launch_split3_planes(const float* src, int64_t src_bs, int rows, int ld_src, int d, uint16_t* dstR,
-                          int64_t dstR_bs, int64_t psR, int ld_R, uint16_t* dstT, int64_t dstT_bs, int64_t psT,
-                          int ld_T, int rows_p, int kp, int batches, hipStream_t s) {
-  dim3 grid((kp + 63) / 64, (std::max(rows, rows_p) + 63) / 64, batches);
-  split3_planes_kernel<<<grid, 256, 0, s>>>(src, src_bs, rows, ld_src, d, dstR, dstR_bs, psR, ld_R, dstT, dstT_bs,
-                                            psT, ld_T, rows_p, kp);
+void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,
+                     int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nT, int64_t nT_bs,
+                     int64_t n_ps, int n_ldT, int ld_src, int kp, int batches, hipStream_t s) {
+  if (batches <= 0 || kp <= 0) return;
+  const Split3T o0{q, q_bs, q_rows, ld_src, qT, qT_bs, q_ps, q_ldT, q_ldT};
+  const Split3T o1{n, n_bs, n_rows, ld_src, nT, nT_bs, n_ps, n_ldT, n_ldT};
+  dim3 grid((kp + 63) / 64, (std::max(q_ldT, n_ldT) + 63) / 64, 2 * batches);
+  split3_t_kernel<<<grid, 256, 0, s>>>(o0, o1, batches, kp);
 }
 
 void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s) {

@@ -125,10 +125,8 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   // both backward products)
   const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const BufsH& h = ctx->h;
-  launch_split3_planes(b.qk, (int64_t)C * dp, C, dp, g.d, nullptr, 0, 0, 0, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps,
-                       Cpb, Cpb, dpb, nch * 2, cs);
-  launch_split3_planes(b.nn, (int64_t)N * dp, N, dp, g.d, nullptr, 0, 0, 0, h.nnT3, (int64_t)dpb * Npb, h.n3_ps,
-                       Npb, Npb, dpb, nch * 2, cs);
+  launch_split3_t(b.qk, (int64_t)C * dp, C, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, b.nn, (int64_t)N * dp, N,
+                  h.nnT3, (int64_t)dpb * Npb, h.n3_ps, Npb, dp, dpb, nch * 2, cs);
   if (bits) {
     // dS is 0 or 1: its products with the pieces are exact (float32 sums)
     run_backward_h(g, b, nullptr, h.nnT3, h.n3_ps, h.qkT3, h.q3_ps, 3, cs);
