@@ -245,17 +245,18 @@ __device__ __forceinline__ void seg_apply(const StepGeom& g, const StepBufs& b, 
 
 // Block of SEG_BLOCK sorted positions, one wave.  RQ floats of a row per lane
 // (lane L holds elements L + 64 q, q < RQ; width <= 64 RQ).  The rows are
-// loaded SB positions at a time with all loads in flight together, and a
+// loaded SB positions at a time, together with the embedding rows of the
+// whole segments ending among them, all loads in flight together, and a
 // running sum restarted at every piece start leaves each piece's in-order
-// total at its last position.  Pieces that are whole segments are updated in
-// one more round of loads; the (at most two) pieces that continue into a
-// neighbouring block are written to `partial` at their first position.
+// total at its last position.  Whole segments are updated in place; the (at
+// most two) pieces that continue into a neighbouring block are written to
+// `partial` at their first position.
 template <int MODE, int RQ>
 __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, const uint32_t* keys,
                                                         const uint32_t* vals, int n, const float* rows,
                                                         int64_t ld, int width, float* partial, uint32_t* segflag,
                                                         float lr) {
-  constexpr int SB = 16 / RQ;                      // positions per batch of loads
+  constexpr int SB = 32 / RQ;                      // positions per batch of loads
   const int lane = threadIdx.x & 63;
   const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int p0 = blk * SEG_BLOCK;
@@ -282,13 +283,27 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
   if (lane == 0)
     segflag[blk] = (cont_prev ? 1u : 0u) | (cont_next ? 2u : 0u) | ((pstart == 1u && cont_prev) ? 4u : 0u) |
                    ((uint32_t)last_start << 8);
+  // pieces that are whole segments (updated here), as a position mask: the
+  // first piece unless it continues an earlier block, the last unless it
+  // continues into the next
+  const uint32_t first_end = pend & (~pend + 1u);
+  const uint32_t last_end = 1u << (np - 1);
+  const uint32_t whole = pend & ~(cont_prev ? first_end : 0u) & ~(cont_next ? last_end : 0u);
+  // this lane's position: the row's table, row id and Adagrad state, read
+  // with the contributions so that one round of loads serves both
+  const uint32_t tbl = k >> g.rb;
+  const uint32_t rowid = k & ((1u << g.rb) - 1u);
+  float gold = 0.0f;
+  if (MODE == SEG_ENTITY && valid && ((whole >> (pos - p0)) & 1u)) gold = (tbl ? b.G_j : b.G_i)[rowid];
 
   float run[RQ];
 #pragma unroll
   for (int q = 0; q < RQ; ++q) run[q] = 0.0f;
 #pragma unroll 1
   for (int b0 = 0; b0 < np; b0 += SB) {
-    float t[SB][RQ];
+    // the batch's contribution rows and, for whole segments ending in it, the
+    // embedding rows they update: all loads in flight together
+    float t[SB][RQ], th[SB][RQ];
 #pragma unroll
     for (int u = 0; u < SB; ++u) {
       const int uu = b0 + u;
@@ -299,6 +314,14 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
       for (int q = 0; q < RQ; ++q) {
         const int f = lane + 64 * q;
         t[u][q] = (ok && f < width) ? r[f] : 0.0f;
+      }
+      const bool upd = MODE == SEG_ENTITY && ok && ((whole >> uu) & 1u);
+      const uint32_t key = (uint32_t)__shfl((int)k, uu & 31, 64);
+      const float* emb = ((key >> g.rb) ? b.emb_j : b.emb_i) + (int64_t)(key & ((1u << g.rb) - 1u)) * g.d;
+#pragma unroll
+      for (int q = 0; q < RQ; ++q) {
+        const int f = lane + 64 * q;
+        th[u][q] = (upd && f < width) ? emb[f] : 0.0f;
       }
     }
 #pragma unroll
@@ -312,38 +335,13 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
       }
     }
     // pieces ending in this batch: whole segments are updated, the rest saved
-    float th[SB][RQ];
-    float gsum[SB];
-#pragma unroll
-    for (int u = 0; u < SB; ++u) {
-      const int uu = b0 + u;
-      gsum[u] = 0.0f;
-      if (uu >= np || !((pend >> uu) & 1u)) continue;
-      const bool first = !(pstart & ((2u << uu) - 2u));   // no piece start in (0, uu]
-      const bool last = uu == np - 1;
-      const bool whole = !(first && cont_prev) && !(last && cont_next);
-      const uint32_t key = (uint32_t)__shfl((int)k, uu, 64);
-      if (whole && MODE == SEG_ENTITY) {
-        const uint32_t tbl = key >> g.rb;
-        const uint32_t row = key & ((1u << g.rb) - 1u);
-        const float* emb = (tbl ? b.emb_j : b.emb_i) + (int64_t)row * g.d;
-#pragma unroll
-        for (int q = 0; q < RQ; ++q) {
-          const int f = lane + 64 * q;
-          th[u][q] = f < width ? emb[f] : 0.0f;
-          gsum[u] += t[u][q] * t[u][q];
-        }
-      }
-    }
 #pragma unroll
     for (int u = 0; u < SB; ++u) {
       const int uu = b0 + u;
       if (uu >= np || !((pend >> uu) & 1u)) continue;
-      const bool first = !(pstart & ((2u << uu) - 2u));
-      const bool last = uu == np - 1;
-      const bool whole = !(first && cont_prev) && !(last && cont_next);
       const uint32_t key = (uint32_t)__shfl((int)k, uu, 64);
-      if (!whole) {
+      if (!((whole >> uu) & 1u)) {
+        const bool first = !(pstart & ((2u << uu) - 2u));   // no piece start in (0, uu]
         const int s0 = first ? 0 : last_start;
         float* out = partial + (int64_t)(p0 + s0) * width;
 #pragma unroll
@@ -352,18 +350,20 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
           if (f < width) out[f] = t[u][q];
         }
       } else if (MODE == SEG_ENTITY) {
-        const uint32_t tbl = key >> g.rb;
+        const uint32_t tb = key >> g.rb;
         const uint32_t row = key & ((1u << g.rb) - 1u);
-        float* emb = (tbl ? b.emb_j : b.emb_i) + (int64_t)row * g.d;
-        float* G = (tbl ? b.G_j : b.G_i) + row;
-        const float Gn = *G + wave_sum(gsum[u]);
+        float* emb = (tb ? b.emb_j : b.emb_i) + (int64_t)row * g.d;
+        float gs = 0.0f;
+#pragma unroll
+        for (int q = 0; q < RQ; ++q) gs += t[u][q] * t[u][q];
+        const float Gn = __shfl(gold, uu, 64) + wave_sum(gs);
         const float scale = lr / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
 #pragma unroll
         for (int q = 0; q < RQ; ++q) {
           const int f = lane + 64 * q;
           if (f < width) emb[f] = th[u][q] - scale * t[u][q];
         }
-        if (lane == 0) *G = Gn;
+        if (lane == 0) (tb ? b.G_j : b.G_i)[row] = Gn;
       } else {
         float* p = b.relp + (int64_t)key * width;
         float* G = b.relG + (int64_t)key * width;
