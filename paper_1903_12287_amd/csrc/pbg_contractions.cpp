@@ -73,6 +73,7 @@ static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t*
 void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
                           const std::function<void(int)>& mark) {
   const int C = g.C, U = g.U, N = g.N, dp = g.dp, Np = g.Np, nch = g.nchunks;
+
   // ranking: dS is 0 or 1 and travels as bits, 16 columns per word
   const bool bits = g.loss == LOSS_RANKING;
   GemmArgsH fa;
@@ -122,7 +123,8 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   mark(3);
 
   // Q and N in three exact bf16 pieces each, transposed (the B operands of
-  // both backward products)
+  // both backward products).  On a second stream beside the score
+  // contraction it only delays the score kernel by as much.
   const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const BufsH& h = ctx->h;
   launch_split3_t(b.qk, (int64_t)C * dp, C, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, b.nn, (int64_t)N * dp, N,

@@ -167,6 +167,34 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   return PBG_OK;
 }
 
+// the side stream and its events, created once per context
+static bool ensure_side(pbg_ctx* ctx) {
+  if (ctx->side) return true;
+  hipStream_t st = nullptr;
+  if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if ((!ctx->fork_ev && hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming) != hipSuccess) ||
+      (!ctx->join_ev && hipEventCreateWithFlags(&ctx->join_ev, hipEventDisableTiming) != hipSuccess)) {
+    (void)hipGetLastError();
+    (void)hipStreamDestroy(st);
+    return false;
+  }
+  ctx->side = st;
+  return true;
+}
+
+void side_fork(pbg_ctx* ctx) {
+  (void)hipEventRecord(ctx->fork_ev, ctx->cs);
+  (void)hipStreamWaitEvent(ctx->side, ctx->fork_ev, 0);
+}
+
+void side_join(pbg_ctx* ctx) {
+  (void)hipEventRecord(ctx->join_ev, ctx->side);
+  (void)hipStreamWaitEvent(ctx->cs, ctx->join_ev, 0);
+}
+
 static bool ensure_events(pbg_ctx* ctx, size_t n) {
   while (ctx->events.size() < n) {
     hipEvent_t e = nullptr;
@@ -260,6 +288,9 @@ void pbg_free(pbg_ctx* ctx) {
     if (s.released) (void)hipEventDestroy(s.released);
   }
   if (ctx->own_xs) (void)hipStreamDestroy(ctx->own_xs);
+  if (ctx->side) (void)hipStreamDestroy(ctx->side);
+  if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
+  if (ctx->join_ev) (void)hipEventDestroy(ctx->join_ev);
   for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
   delete ctx;
 }
@@ -406,6 +437,7 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     b.rvals = nullptr;
   }
 
+  if (!ensure_side(ctx)) return set_err(ctx, PBG_ERR_DEVICE, "could not create the side stream");
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   (void)hipEventCreate(&ev0);
   (void)hipEventCreate(&ev1);
@@ -444,6 +476,8 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     launch_op_backward(g, b, cs);
     if (linear) run_linear_backward(g, b, ctx->relA, ctx->relAT, cs);
     mark(t, 5);
+    const bool rel_side = has_rel && !linear && ctx->R == 1;
+    if (rel_side) side_fork(ctx);
 
     // entities: sort contribution rows by (table, row), segment sums, Adagrad
     const int nkeys = 2 * (nch * U + m_step);
@@ -489,9 +523,13 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
         launch_radix_sort_to(b.rkeys, b.rvals, m_step, rel_bits, ctx->sw, &rk, &rv, cs);
         launch_relation_update_sorted(g, b, rk, rv, m_step, ctx->sw, lr, cs);
       } else {
-        launch_relation_chunk_sums(g, b.relc, ctx->dr, ctx->cmp == CMP_COS ? 1 : 0, ctx->relpartial, cs);
+        // the single relation's gradient sums and update read only what the
+        // operator backward wrote: on the side stream, beside the entity sort
+        // and update, joined before the step ends
+        launch_relation_chunk_sums(g, b.relc, ctx->dr, ctx->cmp == CMP_COS ? 1 : 0, ctx->relpartial, ctx->side);
         launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch * RELSUM_PIECES,
-                                       lr, cs);
+                                       lr, ctx->side);
+        side_join(ctx);
       }
     }
     mark(t, 6);

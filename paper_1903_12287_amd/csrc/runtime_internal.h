@@ -84,12 +84,24 @@ struct pbg_ctx {
   pbg_stats stats{};
   std::vector<Slot> slots;
   hipStream_t own_xs = nullptr;    // copy stream created for pbg_train_epoch when none was given
+  // second compute stream for work of a step that does not depend on its
+  // neighbours on the compute stream (default priority), with the events that
+  // fork work onto it and join it back
+  hipStream_t side = nullptr;
+  hipEvent_t fork_ev = nullptr;
+  hipEvent_t join_ev = nullptr;
   std::vector<hipEvent_t> events;  // phase-timing events, kPhaseEvents per step
 };
 
 constexpr int kPhaseEvents = 7;
 
 pbg_status set_err(pbg_ctx* ctx, pbg_status st, const char* fmt, ...);
+// work of a step on the side stream: side_fork makes the side stream wait for
+// what the compute stream has queued so far, side_join makes the compute
+// stream wait for what the side stream has queued
+void side_fork(pbg_ctx* ctx);
+void side_join(pbg_ctx* ctx);
+
 void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
                           const std::function<void(int)>& mark);
 void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t,
