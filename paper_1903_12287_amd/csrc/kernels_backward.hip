@@ -108,15 +108,12 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
   const int w = threadIdx.x >> 6;
   const int c = blockIdx.y;
   const int Cc = chunk_edges(g, c);
-  const int Nc = Cc + g.U;
   const int item = blockIdx.x * 4 + w;
   if (item >= Cc + 2 * ((g.U + 3) >> 2)) return;   // no block-level barriers below
   const bool cplx = g.op == OP_COMPLEX;
   const int d = g.d, dp = g.dp;
   const bool cos = g.cmp == CMP_COS;
   const bool has_rel = g.op != OP_IDENTITY;
-  const uint32_t tbl_j = g.same_table ? 0u : 1u;
-  const int64_t kbase = (int64_t)c * 2 * g.N;   // compact key position of the chunk
 
   if (item < Cc) {
     const int e = item;
@@ -199,21 +196,13 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     row_store(gs, dn1, d, dp, cplx, lane);
     if (has_rel && g.op != OP_LINEAR)
       row_store(grel, b.relc + ((int64_t)c * g.N + e) * g.dr, d, g.dr, cplx, lane);
-    if (lane == 0) {
-      b.keys[kbase + e] = (tbl_j << g.rb) | (uint32_t)t;
-      b.vals[kbase + e] = (uint32_t)((c * 2 + 0) * g.N + e);
-      b.keys[kbase + Nc + e] = (uint32_t)s;
-      b.vals[kbase + Nc + e] = (uint32_t)((c * 2 + 1) * g.N + e);
-      if (b.rkeys) {
-        b.rkeys[ce] = (uint32_t)r;
-        b.rvals[ce] = (uint32_t)((int64_t)c * g.N + e);
-      }
-    }
     return;
   }
 
   // uniform candidate rows, four consecutive candidates of one side per wave
-  // (all their rows load together)
+  // (all their rows load together); with the dot comparator their gradients
+  // are dS^T Q as the contraction left them
+  if (!cos) return;
   const int ng = (g.U + 3) >> 2;
   const int grp = item - Cc;
   const int side = grp < ng ? 0 : 1;
@@ -223,7 +212,7 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
   int32_t u[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) u[q] = q < nq ? b.neg[(int64_t)(c * 2 + side) * g.U + k0 + q] : 0;
-  if (cos) {
+  {
     Row vh[4], gv[4];
     float nv[4];
 #pragma unroll
@@ -258,17 +247,6 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
       row_store(dv, b.dn + (rbase + q) * dp, d, dp, cplx, lane);
     }
   }
-  if (lane < nq) {
-    const int q = lane;
-    const int tpos = Cc + k0 + q;
-    int32_t uq = u[0];
-#pragma unroll
-    for (int i = 1; i < 4; ++i)
-      if (q == i) uq = u[i];
-    const uint32_t key = side == 0 ? ((tbl_j << g.rb) | (uint32_t)uq) : (uint32_t)uq;
-    b.keys[kbase + side * Nc + tpos] = key;
-    b.vals[kbase + side * Nc + tpos] = (uint32_t)((c * 2 + side) * g.N + tpos);
-  }
 }
 
 }  // namespace
@@ -282,7 +260,10 @@ void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slo
 }
 
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s) {
-  dim3 grid((g.C + 2 * ((g.U + 3) / 4) + 3) / 4, g.nchunks);
+  // waves for the uniform candidates only where the cos normalisation has a
+  // backward to run
+  const int items = g.C + (g.cmp == CMP_COS ? 2 * ((g.U + 3) / 4) : 0);
+  dim3 grid((items + 3) / 4, g.nchunks);
   switch (row_width_for(g.d)) {
     case 2: op_backward_kernel<2><<<grid, 256, 0, s>>>(g, b); break;
     case 4: op_backward_kernel<4><<<grid, 256, 0, s>>>(g, b); break;

@@ -27,6 +27,9 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   const int d = g.d, dp = g.dp;
 
   if (!active) return;   // no block-level barriers below: idle waves may leave
+  const uint32_t tbl_j = g.same_table ? 0u : 1u;
+  const int Nc = Cc + g.U;
+  const int64_t kbase = (int64_t)c * 2 * g.N;   // compact sort-key position of the chunk
   if (item < Cc) {
     // ---- edge item
     const int e = item;
@@ -34,6 +37,19 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     const int s = b.src[eg];
     const int t = b.dst[eg];
     const int r = b.rel ? b.rel[eg] : 0;
+    // sort keys (table, row) of the rows this edge's gradients reach, with the
+    // position of their contribution rows; known now, so the sort can run
+    // beside the contractions
+    if (lane == 0) {
+      b.keys[kbase + e] = (tbl_j << g.rb) | (uint32_t)t;
+      b.vals[kbase + e] = (uint32_t)((c * 2 + 0) * g.N + e);
+      b.keys[kbase + Nc + e] = (uint32_t)s;
+      b.vals[kbase + Nc + e] = (uint32_t)((c * 2 + 1) * g.N + e);
+      if (b.rkeys) {
+        b.rkeys[eg] = (uint32_t)r;
+        b.rvals[eg] = (uint32_t)((int64_t)c * g.N + e);
+      }
+    }
     Row x, y, th;
     row_load(x, b.emb_i + (int64_t)s * d, d, cplx, lane);
     row_load(y, b.emb_j + (int64_t)t * d, d, cplx, lane);
@@ -122,6 +138,8 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     if (lane == 0) {
       b.neg[(int64_t)(c * 2 + side) * g.U + k] = u[q];
       if (g.cmp == CMP_COS) b.nrm[(int64_t)(c * 2 + side) * g.N + t] = nv[q];
+      b.keys[kbase + side * Nc + t] = side == 0 ? ((tbl_j << g.rb) | (uint32_t)u[q]) : (uint32_t)u[q];
+      b.vals[kbase + side * Nc + t] = (uint32_t)((c * 2 + side) * g.N + t);
     }
   }
 }

@@ -176,7 +176,8 @@ static bool ensure_side(pbg_ctx* ctx) {
     return false;
   }
   if ((!ctx->fork_ev && hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming) != hipSuccess) ||
-      (!ctx->join_ev && hipEventCreateWithFlags(&ctx->join_ev, hipEventDisableTiming) != hipSuccess)) {
+      (!ctx->join_ev[0] && hipEventCreateWithFlags(&ctx->join_ev[0], hipEventDisableTiming) != hipSuccess) ||
+      (!ctx->join_ev[1] && hipEventCreateWithFlags(&ctx->join_ev[1], hipEventDisableTiming) != hipSuccess)) {
     (void)hipGetLastError();
     (void)hipStreamDestroy(st);
     return false;
@@ -190,10 +191,9 @@ void side_fork(pbg_ctx* ctx) {
   (void)hipStreamWaitEvent(ctx->side, ctx->fork_ev, 0);
 }
 
-void side_join(pbg_ctx* ctx) {
-  (void)hipEventRecord(ctx->join_ev, ctx->side);
-  (void)hipStreamWaitEvent(ctx->cs, ctx->join_ev, 0);
-}
+void side_mark(pbg_ctx* ctx, int k) { (void)hipEventRecord(ctx->join_ev[k], ctx->side); }
+
+void side_wait(pbg_ctx* ctx, int k) { (void)hipStreamWaitEvent(ctx->cs, ctx->join_ev[k], 0); }
 
 static bool ensure_events(pbg_ctx* ctx, size_t n) {
   while (ctx->events.size() < n) {
@@ -290,7 +290,8 @@ void pbg_free(pbg_ctx* ctx) {
   if (ctx->own_xs) (void)hipStreamDestroy(ctx->own_xs);
   if (ctx->side) (void)hipStreamDestroy(ctx->side);
   if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
-  if (ctx->join_ev) (void)hipEventDestroy(ctx->join_ev);
+  for (hipEvent_t e : ctx->join_ev)
+    if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
   delete ctx;
 }
@@ -466,6 +467,14 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     if (linear) run_linear_forward(g, b, ctx->relA, ctx->relAT, cs);
     mark(t, 1);
 
+    // the gather wrote the sort keys (table, row) of every contribution row:
+    // the entity sort runs on the side stream beside the contractions
+    const int nkeys = 2 * (nch * U + m_step);
+    uint32_t *skeys = nullptr, *svals = nullptr;
+    side_fork(ctx);
+    launch_radix_sort_to(b.keys, b.vals, nkeys, key_bits, ctx->sw, &skeys, &svals, ctx->side);
+    side_mark(ctx, 0);
+
     if (ctx->flags & PBG_F_BF16_SCORE) {
       run_contractions_bf16(ctx, g, b, t, cs, [&](int k) { mark(t, k); });
     } else {
@@ -479,10 +488,8 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     const bool rel_side = has_rel && !linear && ctx->R == 1;
     if (rel_side) side_fork(ctx);
 
-    // entities: sort contribution rows by (table, row), segment sums, Adagrad
-    const int nkeys = 2 * (nch * U + m_step);
-    uint32_t *skeys = nullptr, *svals = nullptr;
-    launch_radix_sort_to(b.keys, b.vals, nkeys, key_bits, ctx->sw, &skeys, &svals, cs);
+    // entities: contribution rows in (table, row) order, segment sums, Adagrad
+    side_wait(ctx, 0);
     launch_entity_update(g, b, skeys, svals, nkeys, ctx->sw, lr, cs);
 
     // relations
@@ -529,7 +536,8 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
         launch_relation_chunk_sums(g, b.relc, ctx->dr, ctx->cmp == CMP_COS ? 1 : 0, ctx->relpartial, ctx->side);
         launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch * RELSUM_PIECES,
                                        lr, ctx->side);
-        side_join(ctx);
+        side_mark(ctx, 1);
+        side_wait(ctx, 1);
       }
     }
     mark(t, 6);

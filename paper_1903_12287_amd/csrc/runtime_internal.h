@@ -89,7 +89,7 @@ struct pbg_ctx {
   // fork work onto it and join it back
   hipStream_t side = nullptr;
   hipEvent_t fork_ev = nullptr;
-  hipEvent_t join_ev = nullptr;
+  hipEvent_t join_ev[2] = {nullptr, nullptr};
   std::vector<hipEvent_t> events;  // phase-timing events, kPhaseEvents per step
 };
 
@@ -97,10 +97,12 @@ constexpr int kPhaseEvents = 7;
 
 pbg_status set_err(pbg_ctx* ctx, pbg_status st, const char* fmt, ...);
 // work of a step on the side stream: side_fork makes the side stream wait for
-// what the compute stream has queued so far, side_join makes the compute
-// stream wait for what the side stream has queued
+// what the compute stream has queued so far; side_mark(k) marks what the side
+// stream has queued so far and side_wait(k) makes the compute stream wait for
+// that mark (two marks, k = 0, 1)
 void side_fork(pbg_ctx* ctx);
-void side_join(pbg_ctx* ctx);
+void side_mark(pbg_ctx* ctx, int k);
+void side_wait(pbg_ctx* ctx, int k);
 
 void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
                           const std::function<void(int)>& mark);
