@@ -123,8 +123,8 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   mark(3);
 
   // Q and N in three exact bf16 pieces each, transposed (the B operands of
-  // both backward products).  On a second stream beside the score
-  // contraction it only delays the score kernel by as much.
+  // both backward products).  On the second stream beside the score
+  // contraction it delays the score kernel by as much as it saves here.
   const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const BufsH& h = ctx->h;
   launch_split3_t(b.qk, (int64_t)C * dp, C, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, b.nn, (int64_t)N * dp, N,
