@@ -98,6 +98,8 @@ void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int
 
 // ---- gather / operator / negatives --------------------------------------------
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s);
+// sort keys and values of a step's contribution rows (and relation keys)
+void launch_sort_keys(const StepGeom& g, const StepBufs& b, hipStream_t s);
 void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s);
 // linear operator (one relation): padded copies of A and A^T, and the positive
 // scores once Q has been formed by contraction

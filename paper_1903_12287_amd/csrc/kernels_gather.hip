@@ -27,9 +27,6 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   const int d = g.d, dp = g.dp;
 
   if (!active) return;   // no block-level barriers below: idle waves may leave
-  const uint32_t tbl_j = g.same_table ? 0u : 1u;
-  const int Nc = Cc + g.U;
-  const int64_t kbase = (int64_t)c * 2 * g.N;   // compact sort-key position of the chunk
   if (item < Cc) {
     // ---- edge item
     const int e = item;
@@ -37,19 +34,6 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     const int s = b.src[eg];
     const int t = b.dst[eg];
     const int r = b.rel ? b.rel[eg] : 0;
-    // sort keys (table, row) of the rows this edge's gradients reach, with the
-    // position of their contribution rows; known now, so the sort can run
-    // beside the contractions
-    if (lane == 0) {
-      b.keys[kbase + e] = (tbl_j << g.rb) | (uint32_t)t;
-      b.vals[kbase + e] = (uint32_t)((c * 2 + 0) * g.N + e);
-      b.keys[kbase + Nc + e] = (uint32_t)s;
-      b.vals[kbase + Nc + e] = (uint32_t)((c * 2 + 1) * g.N + e);
-      if (b.rkeys) {
-        b.rkeys[eg] = (uint32_t)r;
-        b.rvals[eg] = (uint32_t)((int64_t)c * g.N + e);
-      }
-    }
     Row x, y, th;
     row_load(x, b.emb_i + (int64_t)s * d, d, cplx, lane);
     row_load(y, b.emb_j + (int64_t)t * d, d, cplx, lane);
@@ -138,9 +122,52 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     if (lane == 0) {
       b.neg[(int64_t)(c * 2 + side) * g.U + k] = u[q];
       if (g.cmp == CMP_COS) b.nrm[(int64_t)(c * 2 + side) * g.N + t] = nv[q];
-      b.keys[kbase + side * Nc + t] = side == 0 ? ((tbl_j << g.rb) | (uint32_t)u[q]) : (uint32_t)u[q];
-      b.vals[kbase + side * Nc + t] = (uint32_t)((c * 2 + side) * g.N + t);
     }
+  }
+}
+
+// Sort keys of a step, from the edges and the negative draws alone (so that
+// the sort can run beside the gather and the contractions): for chunk c the
+// compact key block [side 0: Nc][side 1: Nc] at c * 2N holds (table, row) of
+// the row each contribution row reaches and, as value, that contribution
+// row's position; edge e: destination t (side 0) and source s (side 1), then
+// the uniform draws of each side.  With several relations the relation of
+// every edge is keyed too.  One thread per edge or per four draws.
+__global__ __launch_bounds__(256) void sort_keys_kernel(StepGeom g, StepBufs b) {
+  const int c = blockIdx.y;
+  const int Cc = chunk_edges(g, c);
+  const int Nc = Cc + g.U;
+  const int ng = (g.U + 3) >> 2;
+  const int item = blockIdx.x * 256 + threadIdx.x;
+  const uint32_t tbl_j = g.same_table ? 0u : 1u;
+  const int64_t kbase = (int64_t)c * 2 * g.N;
+  if (item < Cc) {
+    const int e = item;
+    const int64_t eg = (int64_t)c * g.C + e;
+    b.keys[kbase + e] = (tbl_j << g.rb) | (uint32_t)b.dst[eg];
+    b.vals[kbase + e] = (uint32_t)((c * 2 + 0) * g.N + e);
+    b.keys[kbase + Nc + e] = (uint32_t)b.src[eg];
+    b.vals[kbase + Nc + e] = (uint32_t)((c * 2 + 1) * g.N + e);
+    if (b.rkeys) {
+      b.rkeys[eg] = (uint32_t)(b.rel ? b.rel[eg] : 0);
+      b.rvals[eg] = (uint32_t)((int64_t)c * g.N + e);
+    }
+    return;
+  }
+  const int grp = item - Cc;
+  if (grp >= 2 * ng) return;
+  const int side = grp < ng ? 0 : 1;
+  const int k0 = 4 * (grp - side * ng);
+  const uint32_t rows = side == 0 ? (uint32_t)g.rows_j : (uint32_t)g.rows_i;
+  int32_t u[4];
+  uniform_negatives4(g.seed, g.bucket, (uint64_t)(g.chunk0 + c), (uint32_t)side, (uint32_t)k0, rows, u);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int k = k0 + q;
+    if (k >= g.U) break;
+    const int t = Cc + k;
+    b.keys[kbase + side * Nc + t] = side == 0 ? ((tbl_j << g.rb) | (uint32_t)u[q]) : (uint32_t)u[q];
+    b.vals[kbase + side * Nc + t] = (uint32_t)((c * 2 + side) * g.N + t);
   }
 }
 
@@ -181,6 +208,11 @@ __global__ void transpose_rel_kernel(const float* A, float* AT, int R, int d) {
 }
 
 }  // namespace
+
+void launch_sort_keys(const StepGeom& g, const StepBufs& b, hipStream_t s) {
+  dim3 grid((g.C + 2 * ((g.U + 3) / 4) + 255) / 256, g.nchunks);
+  sort_keys_kernel<<<grid, 256, 0, s>>>(g, b);
+}
 
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s) {
   dim3 grid((g.C + 2 * ((g.U + 3) / 4) + 3) / 4, g.nchunks);

@@ -462,18 +462,20 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     b.rel = rel ? rel + c0 * C : nullptr;
 
     mark(t, 0);
+    // the sort keys (table, row) of every contribution row follow from the
+    // edges and the negative draws alone: keys and entity sort run on the
+    // side stream beside the gather and the contractions
+    const int nkeys = 2 * (nch * U + m_step);
+    uint32_t *skeys = nullptr, *svals = nullptr;
+    side_fork(ctx);
+    launch_sort_keys(g, b, ctx->side);
+    launch_radix_sort_to(b.keys, b.vals, nkeys, key_bits, ctx->sw, &skeys, &svals, ctx->side);
+    side_mark(ctx, 0);
+
     if (linear) launch_pad_linear(ctx->relp, d, dp, ctx->relA, ctx->relAT, cs);
     launch_gather(g, b, cs);
     if (linear) run_linear_forward(g, b, ctx->relA, ctx->relAT, cs);
     mark(t, 1);
-
-    // the gather wrote the sort keys (table, row) of every contribution row:
-    // the entity sort runs on the side stream beside the contractions
-    const int nkeys = 2 * (nch * U + m_step);
-    uint32_t *skeys = nullptr, *svals = nullptr;
-    side_fork(ctx);
-    launch_radix_sort_to(b.keys, b.vals, nkeys, key_bits, ctx->sw, &skeys, &svals, ctx->side);
-    side_mark(ctx, 0);
 
     if (ctx->flags & PBG_F_BF16_SCORE) {
       run_contractions_bf16(ctx, g, b, t, cs, [&](int k) { mark(t, k); });
