@@ -282,7 +282,7 @@ __device__ __forceinline__ void bits_rows(const GemmArgsH& a, const TileGeo& t, 
           if (n >= t.N || n == t.m0 + mb + r) z = -INFINITY;
         }
         const uint64_t mk = __ballot(z > 0.0f);
-        ls[r] += fmaxf(z, 0.0f);
+        ls[r] += z > 0.0f ? z : 0.0f;   // one select on the compare already made
         wd[r] = (uint32_t)(mk >> (16 * g)) & 0xFFFFu;
         cnt[r] += __builtin_popcount(wd[r]);
       }
