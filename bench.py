@@ -130,19 +130,39 @@ def run_leg(pbg, torch, flags, emb0, relp0, src, dst, args, total_steps):
     return dt, st
 
 
-def measured_traffic(kernel_source_rel):
-    """HBM bytes per launch of the score kernel from the committed rocprofv3
-    counter runs, or None when the kernel source has changed since they were
-    taken."""
+def measured_traffic(name):
+    """HBM bytes per step of a kernel group ("score", "gather", "adagrad") from
+    the committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs, or None when a source
+    of the group has changed since they were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "score_kernel_hbm_traffic.json")
+    path = os.path.join(ROOT, "profiles", "kernel_hbm_traffic.json")
     if not os.path.exists(path):
         return None
-    rec = json.load(open(path))
-    src = open(os.path.join(ROOT, kernel_source_rel), "rb").read()
-    if rec.get("source_sha256") != hashlib.sha256(src).hexdigest():
+    rec = json.load(open(path)).get(name)
+    if rec is None:
         return None
-    return rec["hbm_read_bytes_per_launch"] + rec["hbm_write_bytes_per_launch"]
+    for rel, sha in rec["sources"].items():
+        if hashlib.sha256(open(os.path.join(ROOT, rel), "rb").read()).hexdigest() != sha:
+            return None
+    return rec["hbm_read_bytes_per_step"] + rec["hbm_write_bytes_per_step"]
+
+
+def hbm_rate(st, bytes_key, ms_key, traffic):
+    """Achieved HBM rate of a memory-bound phase: algorithmic bytes and, when
+    the counters match the sources, measured bytes, over the phase time."""
+    sec = st[ms_key] / 1e3
+    if sec <= 0:
+        return None
+    steps = max(1, st["steps"])
+    out = {"bound": "hbm", "peak": PEAK_HBM, "unit": "GB/s",
+           "achieved_effective": st[bytes_key] / sec / 1e9,
+           "frac_effective": st[bytes_key] / sec / 1e9 / PEAK_HBM,
+           "algorithmic_bytes_per_step": st[bytes_key] / steps}
+    if traffic is not None:
+        out["traffic_per_step"] = traffic
+        out["achieved_measured"] = traffic * steps / sec / 1e9
+        out["frac_measured"] = out["achieved_measured"] / PEAK_HBM
+    return out
 
 
 def roofline(st, peak, kernel, traffic=None, pieces=None):
@@ -219,12 +239,14 @@ def main():
                    "edges_per_step": S * C, "partitions": 1},
         "roofline": roofline(st, PEAK_FP32_MFMA,
                              "score_split_kernel3<EPI_LOSS_BITS, 6> (float32 score + ranking epilogue)",
-                             measured_traffic("paper_1903_12287_amd/csrc/kernels_gemm_bf16.hip"), pieces=6),
+                             measured_traffic("score"), pieces=6),
         "phases_ms_per_step": phases(st),
         "backward_contractions_tflops": (2 * st["score_flops"] / 3.0) / (st["backward_ms"] / 1e3) / 1e12
         if st["backward_ms"] > 0 else None,
-        "gather_gbps_effective": st["gather_bytes"] / (st["gather_ms"] / 1e3) / 1e9
-        if st["gather_ms"] > 0 else None,
+        # the gather (gather_op_kernel) and the entity Adagrad update
+        # (seg_update_local + seg_update_span) against HBM peak
+        "gather_hbm": hbm_rate(st, "gather_bytes", "gather_ms", measured_traffic("gather")),
+        "adagrad_hbm": hbm_rate(st, "update_bytes", "update_ms", measured_traffic("adagrad")),
     }
     if not args.no_bf16:
         dt16, st16 = run_leg(pbg, torch, pbg.F_BF16_SCORE, emb0, relp0, src, dst, args, total_steps)

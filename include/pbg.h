@@ -112,7 +112,9 @@ typedef struct {
   double update_ms;         /* sort + segment sums + Adagrad (entities and relations) */
   double gather_bytes;      /* algorithmic bytes of the gathers: (2C+2U)*dim*4 per chunk */
   double score_flops;       /* algorithmic flops of the three contractions: 12*C*N*dim per chunk */
-  double update_bytes;      /* algorithmic bytes of the Adagrad updates */
+  double update_bytes;      /* algorithmic bytes of the entity Adagrad updates: contribution rows
+                               read ((2C+2U)*dim*4 per chunk), then per touched row its embedding
+                               read and written and its Adagrad scalar read and written */
   double copy_ms;           /* partition / edge transfers (pbg_train_epoch) */
   int64_t partition_loads;  /* host-to-device partition loads (pbg_train_epoch) */
 } pbg_stats;

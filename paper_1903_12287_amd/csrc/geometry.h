@@ -77,6 +77,7 @@ struct StepBufs {
   float* dpos;          // [S][C] dL/dp
   float* dsum1;         // [S][C] sum_t dS1[e][t]
   double* chunkloss;    // [S][FIN_BLOCKS(C)]  loss partials of the finalisation
+  unsigned long long* nuniq;   // rows touched by the entity updates of the call (segment count)
   float* dq;
   float* dn;
   float* relc;          // [S][N][dr] relation gradient contributions

@@ -118,13 +118,16 @@ void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slo
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s);
 
 // ---- sort, segments, updates ----------------------------------------------------
+// sorted positions per wave of the segment update (a power of two <= 32)
+#define SEG_BLOCK 32
+
 struct SortWork {
   uint32_t* keys_alt;   // [max_n] ping-pong buffers of the sort
   uint32_t* vals_alt;
   uint32_t* hist;       // [256][max blocks]
   uint32_t* scan_tmp;   // block sums of the multi-launch scan
   float* partial;       // [max_n][width] per-block partial sums of segments
-  uint32_t* segflag;    // [max_n / 32 + 2] piece flags per block of 32 sorted positions
+  uint32_t* segflag;    // [max_n / SEG_BLOCK + 2] piece flags per block of sorted positions
   int max_n;
 };
 

@@ -5,7 +5,7 @@
 // accumulator per embedding row, summed over the row) is applied once per
 // touched row.
 //
-// The sorted positions are cut into fixed blocks of 32.  A wave per block sums
+// The sorted positions are cut into fixed blocks of SEG_BLOCK.  A wave per block sums
 // every piece of the block (a piece = the positions of one segment inside the
 // block) in position order; a segment that lies inside one block is updated
 // there and then.  A segment that crosses block boundaries (a hub row of a
@@ -16,7 +16,6 @@
 #include "kernels.h"
 #include "row_ops.h"
 
-#define SEG_BLOCK 32
 // scan tiles and radix-sort tiles: SORT_IPT * 256 values per workgroup
 #define SORT_IPT 16
 #define SORT_TILE (256 * SORT_IPT)
@@ -278,11 +277,12 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
   const int last_start = 31 - __builtin_clz(pstart);
   // piece flags of this block for the spanning-segment pass: bit 1 the first
   // piece continues an earlier block, bit 2 the last piece continues into the
-  // next, bit 4 the block is one piece continuing an earlier block; bits 8..
-  // the position of the last piece's start
+  // next, bit 4 the block is one piece continuing an earlier block; bits
+  // 8..12 the position of the last piece's start; bits 16..21 the number of
+  // segments starting in the block (the touched rows, summed by that pass)
   if (lane == 0)
     segflag[blk] = (cont_prev ? 1u : 0u) | (cont_next ? 2u : 0u) | ((pstart == 1u && cont_prev) ? 4u : 0u) |
-                   ((uint32_t)last_start << 8);
+                   ((uint32_t)last_start << 8) | ((uint32_t)__builtin_popcount(segs) << 16);
   // pieces that are whole segments (updated here), as a position mask: the
   // first piece unless it continues an earlier block, the last unless it
   // continues into the next
@@ -394,14 +394,22 @@ __global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, c
   const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int p0 = blk * SEG_BLOCK;
   const int p1 = p0 + SEG_BLOCK;
+  const int nblk = (n + SEG_BLOCK - 1) / SEG_BLOCK;
+  if (MODE == SEG_ENTITY && blk == 0 && b.nuniq) {
+    // the step's touched rows: the blocks' segment counts (integer sum)
+    uint32_t cnt = 0;
+    for (int j = lane; j < nblk; j += 64) cnt += (segflag[j] >> 16) & 63u;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) cnt += (uint32_t)__shfl_xor((int)cnt, o, 64);
+    if (lane == 0) atomicAdd(b.nuniq, (unsigned long long)cnt);
+  }
   if (p1 >= n) return;
   const uint32_t f = segflag[blk];
   if (!(f & 2u) || (f & 4u)) return;     // nothing crosses the end, or the segment started earlier
-  const int s = p0 + (int)(f >> 8);      // start of the crossing segment
+  const int s = p0 + (int)((f >> 8) & 31u);   // start of the crossing segment
   const uint32_t key = keys[s];
   // blocks the segment covers entirely (flags 2 | 4), 64 flags per probe; it
   // ends inside the first following block that is not one of them
-  const int nblk = (n + SEG_BLOCK - 1) / SEG_BLOCK;
   int nfull = 0;
   for (int j0 = blk + 1;; j0 += 64) {
     const int j = j0 + lane;

@@ -73,7 +73,7 @@ bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width) {
   w.hist = (uint32_t*)a.get(radix_hist_entries(max_n) * 4);
   w.scan_tmp = (uint32_t*)a.get(radix_scan_tmp_entries(max_n) * 4);
   w.partial = width > 0 ? (float*)a.get(max_n * (int64_t)width * 4) : nullptr;
-  w.segflag = (uint32_t*)a.get((max_n / 32 + 2) * 4);
+  w.segflag = (uint32_t*)a.get((max_n / SEG_BLOCK + 2) * 4);
   return !a.failed;
 }
 
@@ -212,7 +212,8 @@ static pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps) {
   if (ctx->steploss_dev) (void)hipFree(ctx->steploss_dev);
   ctx->steploss_dev = nullptr;
   ctx->steploss_cap = 0;
-  if (hipMalloc(&ctx->steploss_dev, (size_t)std::max<int64_t>(nsteps, 1) * 8) != hipSuccess) {
+  // one double per step, then the 64-bit count of touched rows
+  if (hipMalloc(&ctx->steploss_dev, (size_t)(std::max<int64_t>(nsteps, 1) + 1) * 8) != hipSuccess) {
     (void)hipGetLastError();
     ctx->steploss_dev = nullptr;
     return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "step-loss buffer allocation failed");
@@ -427,6 +428,8 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   const bool linear = ctx->op == OP_LINEAR;
 
   StepBufs b = ctx->bufs;
+  b.nuniq = (unsigned long long*)(ctx->steploss_dev + std::max<int64_t>(ctx->steploss_cap, 1));
+  if (hipMemsetAsync(b.nuniq, 0, 8, cs) != hipSuccess) return hip_fail(ctx, hipGetLastError(), "counter reset");
   b.emb_i = emb_i;
   b.emb_j = emb_j;
   b.G_i = G_i;
@@ -552,7 +555,9 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     return hip_fail(ctx, e, "kernel launch");
   }
   std::vector<double> losses((size_t)nsteps);
+  unsigned long long nuniq = 0;
   e = hipMemcpyAsync(losses.data(), ctx->steploss_dev, (size_t)nsteps * 8, hipMemcpyDeviceToHost, cs);
+  if (e == hipSuccess) e = hipMemcpyAsync(&nuniq, b.nuniq, 8, hipMemcpyDeviceToHost, cs);
   if (e == hipSuccess) e = hipStreamSynchronize(cs);
   float ms = 0.f;
   if (e == hipSuccess) (void)hipEventElapsedTime(&ms, ev0, ev1);
@@ -585,7 +590,11 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     const double Nc = Cc + U_d;
     ctx->stats.gather_bytes += (2 * Cc + 2 * U_d) * d * 4.0;
     ctx->stats.score_flops += 12.0 * Cc * Nc * d;
+    ctx->stats.update_bytes += (2 * Cc + 2 * U_d) * d * 4.0;   // contribution rows read
   }
+  // each touched row: its embedding read and written, its Adagrad scalar read
+  // and written
+  ctx->stats.update_bytes += (double)nuniq * (2.0 * d * 4 + 8);
   return PBG_OK;
 }
 
