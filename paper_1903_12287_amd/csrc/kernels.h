@@ -84,10 +84,12 @@ void launch_gemm_split_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batche
 // two EPI_STORE products in one launch: a0 with A as dS rows (GA_BITS_ROW or
 // GA_KC), a1 with A as dS columns (GA_BITS_COL or GA_MC), same planes
 void launch_gemm_bf16_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s);
-void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d,
-                              uint16_t* dst, int64_t dst_bs, int ld_dst, uint16_t* dstT,
-                              int64_t dstT_bs, int ld_T, int rows_p, int kp, int batches,
-                              hipStream_t s);
+// bf16 path: Q and N rows (fp32, [rows][ld_src]) rounded once to bf16 rows
+// [rows][kp] and transposed copies [kp][ldT], both operands in one launch
+void launch_to_bf16_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qh, int64_t qh_bs, uint16_t* qT,
+                      int64_t qT_bs, int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nh,
+                      int64_t nh_bs, uint16_t* nT, int64_t nT_bs, int n_ldT, int ld_src, int kp, int batches,
+                      hipStream_t s);
 // fp32 rows [rows][ld_src] of Q and of N -> the exact bf16 pieces
 // x = h + m + l as three transposed planes [kp][ld_T] each (ps elements
 // apart, rows past `rows` up to ld_T zero), both operands in one launch.

@@ -1100,33 +1100,57 @@ __global__ __launch_bounds__(256) void gemm_bits_pair_kernel(GemmArgsH a0, int t
   else gemm_bits_tile<BN, 1, PL>(a1, tn1, tm1, (int)gridDim.x - nwg0, id - nwg0, sm);
 }
 
-// fp32 packed rows -> bf16 rows (zero-padded to kp) and the transposed copy
-// [kp][rows_p]: 64 x 64 tiles through LDS, coalesced on both sides.
-__global__ __launch_bounds__(256) void to_bf16_transpose_kernel(const float* src, int64_t src_bs,
-                                                                int rows, int ld_src, int d,
-                                                                uint16_t* dst, int64_t dst_bs, int ld_dst,
-                                                                uint16_t* dstT, int64_t dstT_bs,
-                                                                int ld_T, int rows_p, int kp) {
-  __shared__ uint16_t tile[64][66];
-  const int b = blockIdx.z;
+// fp32 rows [rows][ld_src] (columns [d, ld_src) zero) of Q and of N -> bf16
+// rows [rows][ld_dst] (columns up to kp) and the transposed copy [kp][ld_T]
+// (rows [rows, ld_T) zero), both operands in one launch (blockIdx.z < nz0:
+// the first).  64 x 64 tiles: 16-byte loads, rounded once, eight bytes per
+// thread to the row-major copy and into an LDS tile, then eight consecutive
+// rows of one column per 16-byte store of the transposed copy.  ld_src is a
+// multiple of 4, ld_dst of 4, ld_T of 8.
+struct Bf16T {
+  const float* src;
+  int64_t src_bs;
+  int rows, ld_src;
+  uint16_t* dst;
+  int64_t dst_bs;
+  int ld_dst;
+  uint16_t* dstT;
+  int64_t dstT_bs;
+  int ld_T;
+};
+
+__global__ __launch_bounds__(256) void to_bf16_t_kernel(Bf16T o0, Bf16T o1, int nz0, int kp) {
+  __shared__ uint16_t tile[64][72];
+  const bool first = (int)blockIdx.z < nz0;
+  const Bf16T& o = first ? o0 : o1;
+  const int b = first ? blockIdx.z : blockIdx.z - nz0;
   const int r0 = blockIdx.y * 64, k0 = blockIdx.x * 64;
-  const float* s = src + (int64_t)b * src_bs;
-  uint16_t* o = dst + (int64_t)b * dst_bs;
-  uint16_t* oT = dstT + (int64_t)b * dstT_bs;
-  for (int q = threadIdx.x; q < 64 * 64; q += 256) {
-    const int rr = q >> 6, kk = q & 63;
-    const int r = r0 + rr, k = k0 + kk;
-    float v = 0.0f;
-    if (r < rows && k < d) v = s[(int64_t)r * ld_src + k];
-    const uint16_t h = f_to_bf16(v);
-    tile[rr][kk] = h;
-    if (r < rows && k < kp) o[(int64_t)r * ld_dst + k] = h;
+  if (r0 >= o.ld_T) return;
+  const float* s = o.src + (int64_t)b * o.src_bs;
+  uint16_t* dr = o.dst + (int64_t)b * o.dst_bs;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int it = threadIdx.x + 256 * j;
+    const int rr = it >> 4, k4 = 4 * (it & 15);
+    const int r = r0 + rr, k = k0 + k4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < o.rows && k < o.ld_src) v = *(const float4*)(s + (int64_t)r * o.ld_src + k);
+    const uint32_t lo = f2_to_bf16x2(v.x, v.y), hi = f2_to_bf16x2(v.z, v.w);
+    *(uint2*)&tile[rr][k4] = make_uint2(lo, hi);
+    if (r < o.rows && k < kp) *(uint2*)(dr + (int64_t)r * o.ld_dst + k) = make_uint2(lo, hi);
   }
   __syncthreads();
-  for (int q = threadIdx.x; q < 64 * 64; q += 256) {
-    const int kk = q >> 6, rr = q & 63;
-    const int r = r0 + rr, k = k0 + kk;
-    if (k < kp && r < rows_p) oT[(int64_t)k * ld_T + r] = (r < rows) ? tile[rr][kk] : (uint16_t)0;
+  uint16_t* dT = o.dstT + (int64_t)b * o.dstT_bs;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int it = threadIdx.x + 256 * j;
+    const int kk = it >> 3, r8 = 8 * (it & 7);
+    const int k = k0 + kk, r = r0 + r8;
+    if (k >= kp || r >= o.ld_T) continue;
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)tile[r8 + 2 * i][kk] | ((uint32_t)tile[r8 + 2 * i + 1][kk] << 16);
+    *(u32x4*)(dT + (int64_t)k * o.ld_T + r) = (u32x4){w[0], w[1], w[2], w[3]};
   }
 }
 
@@ -1324,13 +1348,15 @@ void launch_score_split(const GemmArgsH& a, int epi, int batches, hipStream_t s)
   else score_split_kernel<EPI_STORE, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
 }
 
-void launch_to_bf16_transpose(const float* src, int64_t src_bs, int rows, int ld_src, int d,
-                              uint16_t* dst, int64_t dst_bs, int ld_dst, uint16_t* dstT,
-                              int64_t dstT_bs, int ld_T, int rows_p, int kp, int batches,
-                              hipStream_t s) {
-  dim3 grid((kp + 63) / 64, (rows_p + 63) / 64, batches);
-  to_bf16_transpose_kernel<<<grid, 256, 0, s>>>(src, src_bs, rows, ld_src, d, dst, dst_bs, ld_dst, dstT,
-                                                dstT_bs, ld_T, rows_p, kp);
+void launch_to_bf16_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qh, int64_t qh_bs, uint16_t* qT,
+                      int64_t qT_bs, int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nh,
+                      int64_t nh_bs, uint16_t* nT, int64_t nT_bs, int n_ldT, int ld_src, int kp, int batches,
+                      hipStream_t s) {
+  if (batches <= 0 || kp <= 0) return;
+  const Bf16T o0{q, q_bs, q_rows, ld_src, qh, qh_bs, kp, qT, qT_bs, q_ldT};
+  const Bf16T o1{n, n_bs, n_rows, ld_src, nh, nh_bs, kp, nT, nT_bs, n_ldT};
+  dim3 grid((kp + 63) / 64, (std::max(q_ldT, n_ldT) + 63) / 64, 2 * batches);
+  to_bf16_t_kernel<<<grid, 256, 0, s>>>(o0, o1, batches, kp);
 }
 
 void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,

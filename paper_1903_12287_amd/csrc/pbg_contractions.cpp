@@ -182,10 +182,8 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   const int dpb = rup(d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const BufsH& h = ctx->h;
   // bf16 operands: rows [e][f], [t][f] and the transposed copies [f][e], [f][t]
-  launch_to_bf16_transpose(b.qk, (int64_t)C * dp, C, dp, d, h.qk, (int64_t)C * dpb, dpb, h.qkT,
-                           (int64_t)dpb * Cpb, Cpb, Cpb, dpb, nch * 2, cs);
-  launch_to_bf16_transpose(b.nn, (int64_t)N * dp, N, dp, d, h.nn, (int64_t)N * dpb, dpb, h.nnT,
-                           (int64_t)dpb * Npb, Npb, Npb, dpb, nch * 2, cs);
+  launch_to_bf16_t(b.qk, (int64_t)C * dp, C, h.qk, (int64_t)C * dpb, h.qkT, (int64_t)dpb * Cpb, Cpb, b.nn,
+                   (int64_t)N * dp, N, h.nn, (int64_t)N * dpb, h.nnT, (int64_t)dpb * Npb, Npb, dp, dpb, nch * 2, cs);
 
   const bool bits = g.loss == LOSS_RANKING;
   const int nw = (Np + 15) / 16, ldw = rup(C, 8);
