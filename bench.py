@@ -103,16 +103,21 @@ def cpu_baseline(src_h, dst_h, emb_h, chunks):
                       f"state, fp64 numpy/torch-CPU oracle, {dt:.1f} s"}
 
 
-def run_leg(pbg, torch, flags, emb0, relp0, src, dst, args, total_steps):
+def run_leg(pbg, torch, flags, emb0, relp0, src, dst, args, total_steps, timing=None, steps=None):
     """Warm-up + timed steps from a copy of the initial state; returns the
-    wall time of the timed steps and the library's stats for them."""
+    wall time of the timed steps and the library's stats for them.  `timing`:
+    the library's event flag (score-only events by default, which add two
+    events per step; all phases add seven)."""
+    if timing is None:
+        timing = pbg.F_SCORE_TIMING
+    if steps is None:
+        steps = args.steps
     dev = emb0.device
     emb = emb0.clone()
     relp = relp0.clone()
     G = torch.zeros(N_NODES, dtype=torch.float32, device=dev)
     relG = torch.zeros_like(relp)
-    ctx = pbg.pbg_bucket_init(N_NODES, 1, 1, DIM, "translation", "cos", "ranking", MARGIN,
-                              flags | pbg.F_PHASE_TIMING)
+    ctx = pbg.pbg_bucket_init(N_NODES, 1, 1, DIM, "translation", "cos", "ranking", MARGIN, flags | timing)
     try:
         pbg.pbg_bind_partition(ctx, 0, emb, G)
         pbg.pbg_bind_relations(ctx, relp, relG)
@@ -120,7 +125,7 @@ def run_leg(pbg, torch, flags, emb0, relp0, src, dst, args, total_steps):
         train_range(pbg, ctx, src, dst, 0, args.warmup, total_steps)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        train_range(pbg, ctx, src, dst, args.warmup, args.steps, total_steps)
+        train_range(pbg, ctx, src, dst, args.warmup, steps, total_steps)
         torch.cuda.synchronize()
         dt = time.perf_counter() - t0
         st = pbg.pbg_get_stats(ctx)
@@ -219,6 +224,11 @@ def main():
     total_steps = -(-N_EDGES // (S * C))
 
     dt, st = run_leg(pbg, torch, 0, emb0, relp0, src, dst, args, total_steps)
+    # the phase breakdown from a separate, shorter run with events around every
+    # kernel group (they add to each step, so the timed run records only the
+    # two around the score contraction)
+    phase_steps = min(args.steps, 100)
+    _, stp = run_leg(pbg, torch, 0, emb0, relp0, src, dst, args, total_steps, pbg.F_PHASE_TIMING, phase_steps)
     print(f"# fp32: {st['edges'] / dt:.4g} edges/s", file=sys.stderr)
     out = {
         "metric": "trained edges/sec on 1 MI355X",
@@ -240,22 +250,26 @@ def main():
         "roofline": roofline(st, PEAK_FP32_MFMA,
                              "score_split_kernel3<EPI_LOSS_BITS, 6> (float32 score + ranking epilogue)",
                              measured_traffic("score"), pieces=6),
-        "phases_ms_per_step": phases(st),
-        "backward_contractions_tflops": (2 * st["score_flops"] / 3.0) / (st["backward_ms"] / 1e3) / 1e12
-        if st["backward_ms"] > 0 else None,
+        # from the phase-timing run of phase_steps steps
+        "phases_ms_per_step": phases(stp),
+        "phase_steps": phase_steps,
+        "backward_contractions_tflops": (2 * stp["score_flops"] / 3.0) / (stp["backward_ms"] / 1e3) / 1e12
+        if stp["backward_ms"] > 0 else None,
         # the gather (gather_op_kernel) and the entity Adagrad update
         # (seg_update_local + seg_update_span) against HBM peak
-        "gather_hbm": hbm_rate(st, "gather_bytes", "gather_ms", measured_traffic("gather")),
-        "adagrad_hbm": hbm_rate(st, "update_bytes", "update_ms", measured_traffic("adagrad")),
+        "gather_hbm": hbm_rate(stp, "gather_bytes", "gather_ms", measured_traffic("gather")),
+        "adagrad_hbm": hbm_rate(stp, "update_bytes", "update_ms", measured_traffic("adagrad")),
     }
     if not args.no_bf16:
         dt16, st16 = run_leg(pbg, torch, pbg.F_BF16_SCORE, emb0, relp0, src, dst, args, total_steps)
+        _, st16p = run_leg(pbg, torch, pbg.F_BF16_SCORE, emb0, relp0, src, dst, args, total_steps,
+                           pbg.F_PHASE_TIMING, phase_steps)
         print(f"# bf16: {st16['edges'] / dt16:.4g} edges/s", file=sys.stderr)
         out["bf16"] = {"value": st16["edges"] / dt16, "unit": "edges/s",
                        "ms_per_step": dt16 * 1e3 / args.steps, "dtype": "bf16 inputs, f32 accumulate",
                        "roofline": roofline(st16, PEAK_BF16_MFMA,
                                             "gemm_bf16_kernel<128,GA_KC,EPI_LOSS_BITS,1> (score + ranking epilogue)"),
-                       "phases_ms_per_step": phases(st16)}
+                       "phases_ms_per_step": phases(st16p)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(src.cpu().numpy(), dst.cpu().numpy(), emb0.cpu().numpy(),
                                            args.cpu_sample_chunks)

@@ -71,8 +71,12 @@ enum {
    * state, losses and the loss epilogue stay float32. */
   PBG_F_BF16_SCORE = 1u,
   /* Record HIP events around every kernel group of every step on the compute
-   * stream and report the summed times in pbg_stats (small overhead). */
-  PBG_F_PHASE_TIMING = 2u
+   * stream and report the summed times in pbg_stats (each event adds a few
+   * microseconds to a step). */
+  PBG_F_PHASE_TIMING = 2u,
+  /* Record HIP events around the score contraction only (score_ms in
+   * pbg_stats) at two events per step; PBG_F_PHASE_TIMING includes it. */
+  PBG_F_SCORE_TIMING = 4u
 };
 
 /* Where a bound partition lives. */

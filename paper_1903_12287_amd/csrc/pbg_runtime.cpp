@@ -249,7 +249,8 @@ pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_part
   if (loss < PBG_LOSS_RANKING || loss > PBG_LOSS_SOFTMAX) return fail(PBG_ERR_INVALID_ARG, "unknown loss");
   if (op == PBG_OP_COMPLEX_DIAGONAL && (dim % 2)) return fail(PBG_ERR_INVALID_ARG, "complex_diagonal needs an even dim");
   if (!std::isfinite(margin)) return fail(PBG_ERR_INVALID_ARG, "margin must be finite");
-  if (flags & ~(uint32_t)(PBG_F_BF16_SCORE | PBG_F_PHASE_TIMING)) return fail(PBG_ERR_INVALID_ARG, "unknown flags");
+  if (flags & ~(uint32_t)(PBG_F_BF16_SCORE | PBG_F_PHASE_TIMING | PBG_F_SCORE_TIMING))
+    return fail(PBG_ERR_INVALID_ARG, "unknown flags");
   const int64_t ps = (num_entities + num_partitions - 1) / num_partitions;
   if ((int64_t)(num_partitions - 1) * ps >= num_entities)
     return fail(PBG_ERR_INVALID_ARG, "a partition would be empty (num_partitions too large for num_entities)");
@@ -446,10 +447,13 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   (void)hipEventCreate(&ev0);
   (void)hipEventCreate(&ev1);
   const bool timing = (ctx->flags & PBG_F_PHASE_TIMING) != 0;
-  if (timing && !ensure_events(ctx, (size_t)nsteps * kPhaseEvents))
+  const bool score_timing = timing || (ctx->flags & PBG_F_SCORE_TIMING) != 0;
+  if (score_timing && !ensure_events(ctx, (size_t)nsteps * kPhaseEvents))
     return set_err(ctx, PBG_ERR_DEVICE, "hipEventCreate failed");
+  // events 1 and 2 of a step bracket the score contraction
   auto mark = [&](int64_t step, int k) {
-    if (timing) (void)hipEventRecord(ctx->events[(size_t)step * kPhaseEvents + k], cs);
+    if (timing || (score_timing && (k == 1 || k == 2)))
+      (void)hipEventRecord(ctx->events[(size_t)step * kPhaseEvents + k], cs);
   };
   (void)hipEventRecord(ev0, cs);
 
@@ -569,11 +573,11 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   if (loss_out) *loss_out = total;
   if (step_losses) step_losses->insert(step_losses->end(), losses.begin(), losses.end());
   ctx->stats.total_ms += ms;
-  if (timing) {
+  if (score_timing) {
     double* acc[6] = {&ctx->stats.gather_ms, &ctx->stats.score_ms, &ctx->stats.epilogue_ms,
                       &ctx->stats.backward_ms, &ctx->stats.opbwd_ms, &ctx->stats.update_ms};
     for (int64_t t = 0; t < nsteps; ++t)
-      for (int k = 0; k < 6; ++k) {
+      for (int k = timing ? 0 : 1; k < (timing ? 6 : 2); ++k) {
         float pm = 0.f;
         (void)hipEventElapsedTime(&pm, ctx->events[(size_t)t * kPhaseEvents + k],
                                   ctx->events[(size_t)t * kPhaseEvents + k + 1]);

@@ -24,6 +24,7 @@ COMPARATORS = {"dot": 0, "cos": 1}
 LOSSES = {"ranking": 0, "logistic": 1, "softmax": 2}
 F_BF16_SCORE = 1
 F_PHASE_TIMING = 2
+F_SCORE_TIMING = 4
 MEM_DEVICE = 0
 MEM_PINNED_HOST = 1
 
