@@ -100,8 +100,12 @@ void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int
 
 // ---- gather / operator / negatives --------------------------------------------
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s);
-// sort keys and values of a step's contribution rows (and relation keys)
-void launch_sort_keys(const StepGeom& g, const StepBufs& b, hipStream_t s);
+// sort keys and values of the contribution rows of a window of nsteps steps
+// of S chunks ([step][stride], compact per step), and relation keys
+// ([step][S * C]) when rkeys is set
+void launch_window_keys(const StepGeom& g, const int32_t* src, const int32_t* dst, const int32_t* rel,
+                        int64_t n_edges, int64_t chunk0, int S, int nsteps, int64_t stride, uint32_t* keys,
+                        uint32_t* vals, uint32_t* rkeys, uint32_t* rvals, hipStream_t s);
 void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s);
 // linear operator (one relation): padded copies of A and A^T, and the positive
 // scores once Q has been formed by contraction
@@ -142,6 +146,15 @@ int64_t radix_scan_tmp_entries(int64_t n);
 void launch_radix_sort(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, hipStream_t s);
 // the same sort without the final copy: *out_keys / *out_vals receive the
 // buffers that hold the result (keys / vals or the work buffers)
+// nseg independent sorts in one set of launches: segment y holds n_full
+// pairs at keys / vals + y * stride (the last segment n_last), sorted stably
+// on the low `bits` bits, results at *out_keys / *out_vals + y * stride (the
+// inputs or the alternate buffers, of the same layout).  hist holds
+// radix_segments_hist_entries(max n, nseg) entries.
+void launch_radix_sort_segments(uint32_t* keys, uint32_t* vals, uint32_t* keys_alt, uint32_t* vals_alt,
+                                int64_t stride, int n_full, int n_last, int nseg, int bits, uint32_t* hist,
+                                uint32_t** out_keys, uint32_t** out_vals, hipStream_t s);
+int64_t radix_segments_hist_entries(int64_t n, int nseg);
 void launch_radix_sort_to(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, uint32_t** out_keys,
                           uint32_t** out_vals, hipStream_t s);
 

@@ -10,6 +10,7 @@
 // (<g(x), y> = <x, g*(y)>, plus <theta, y> for translation), so every
 // candidate row is copied raw.  For cos every packed row is a unit vector and
 // the source candidates carry g (one relation, or the identity operator).
+#include <algorithm>
 #include "kernels.h"
 #include "row_ops.h"
 
@@ -126,31 +127,41 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   }
 }
 
-// Sort keys of a step, from the edges and the negative draws alone (so that
-// the sort can run beside the gather and the contractions): for chunk c the
-// compact key block [side 0: Nc][side 1: Nc] at c * 2N holds (table, row) of
-// the row each contribution row reaches and, as value, that contribution
-// row's position; edge e: destination t (side 0) and source s (side 1), then
-// the uniform draws of each side.  With several relations the relation of
-// every edge is keyed too.  One thread per edge or per four draws.
-__global__ __launch_bounds__(256) void sort_keys_kernel(StepGeom g, StepBufs b) {
-  const int c = blockIdx.y;
-  const int Cc = chunk_edges(g, c);
+// Sort keys of a window of steps, from the edges and the negative draws
+// alone (so that the sorts of a whole window run as one batch before its
+// steps): for chunk c of step w the compact key block [side 0: Nc][side 1:
+// Nc] at w * stride + c * 2N holds (table, row) of the row each contribution
+// row reaches and, as value, that contribution row's position in the step;
+// edge e: destination t (side 0) and source s (side 1), then the uniform
+// draws of each side.  With several relations the relation of every edge is
+// keyed too ([w][S][C]).  One thread per edge or per four draws; src / dst /
+// rel start at the window's first edge, n_edges edges, chunk0 is the
+// window's first chunk (for the draws).
+__global__ __launch_bounds__(256) void window_keys_kernel(StepGeom g, const int32_t* src, const int32_t* dst,
+                                                          const int32_t* rel, int64_t n_edges, int64_t chunk0,
+                                                          int S, int64_t stride, uint32_t* keys, uint32_t* vals,
+                                                          uint32_t* rkeys, uint32_t* rvals) {
+  const int c = blockIdx.y, w = blockIdx.z;
+  const int64_t cw = (int64_t)w * S + c;   // chunk within the window
+  const int64_t left = n_edges - cw * g.C;
+  if (left <= 0) return;
+  const int Cc = (int)std::min<int64_t>(g.C, left);
   const int Nc = Cc + g.U;
   const int ng = (g.U + 3) >> 2;
   const int item = blockIdx.x * 256 + threadIdx.x;
   const uint32_t tbl_j = g.same_table ? 0u : 1u;
-  const int64_t kbase = (int64_t)c * 2 * g.N;
+  const int64_t kbase = w * stride + (int64_t)c * 2 * g.N;
   if (item < Cc) {
     const int e = item;
-    const int64_t eg = (int64_t)c * g.C + e;
-    b.keys[kbase + e] = (tbl_j << g.rb) | (uint32_t)b.dst[eg];
-    b.vals[kbase + e] = (uint32_t)((c * 2 + 0) * g.N + e);
-    b.keys[kbase + Nc + e] = (uint32_t)b.src[eg];
-    b.vals[kbase + Nc + e] = (uint32_t)((c * 2 + 1) * g.N + e);
-    if (b.rkeys) {
-      b.rkeys[eg] = (uint32_t)(b.rel ? b.rel[eg] : 0);
-      b.rvals[eg] = (uint32_t)((int64_t)c * g.N + e);
+    const int64_t eg = cw * g.C + e;
+    keys[kbase + e] = (tbl_j << g.rb) | (uint32_t)dst[eg];
+    vals[kbase + e] = (uint32_t)((c * 2 + 0) * g.N + e);
+    keys[kbase + Nc + e] = (uint32_t)src[eg];
+    vals[kbase + Nc + e] = (uint32_t)((c * 2 + 1) * g.N + e);
+    if (rkeys) {
+      const int64_t rw = (int64_t)w * S * g.C + (int64_t)c * g.C + e;
+      rkeys[rw] = (uint32_t)(rel ? rel[eg] : 0);
+      rvals[rw] = (uint32_t)((int64_t)c * g.N + e);
     }
     return;
   }
@@ -160,14 +171,14 @@ __global__ __launch_bounds__(256) void sort_keys_kernel(StepGeom g, StepBufs b) 
   const int k0 = 4 * (grp - side * ng);
   const uint32_t rows = side == 0 ? (uint32_t)g.rows_j : (uint32_t)g.rows_i;
   int32_t u[4];
-  uniform_negatives4(g.seed, g.bucket, (uint64_t)(g.chunk0 + c), (uint32_t)side, (uint32_t)k0, rows, u);
+  uniform_negatives4(g.seed, g.bucket, (uint64_t)(chunk0 + cw), (uint32_t)side, (uint32_t)k0, rows, u);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int k = k0 + q;
     if (k >= g.U) break;
     const int t = Cc + k;
-    b.keys[kbase + side * Nc + t] = side == 0 ? ((tbl_j << g.rb) | (uint32_t)u[q]) : (uint32_t)u[q];
-    b.vals[kbase + side * Nc + t] = (uint32_t)((c * 2 + side) * g.N + t);
+    keys[kbase + side * Nc + t] = side == 0 ? ((tbl_j << g.rb) | (uint32_t)u[q]) : (uint32_t)u[q];
+    vals[kbase + side * Nc + t] = (uint32_t)((c * 2 + side) * g.N + t);
   }
 }
 
@@ -209,9 +220,12 @@ __global__ void transpose_rel_kernel(const float* A, float* AT, int R, int d) {
 
 }  // namespace
 
-void launch_sort_keys(const StepGeom& g, const StepBufs& b, hipStream_t s) {
-  dim3 grid((g.C + 2 * ((g.U + 3) / 4) + 255) / 256, g.nchunks);
-  sort_keys_kernel<<<grid, 256, 0, s>>>(g, b);
+void launch_window_keys(const StepGeom& g, const int32_t* src, const int32_t* dst, const int32_t* rel,
+                        int64_t n_edges, int64_t chunk0, int S, int nsteps, int64_t stride, uint32_t* keys,
+                        uint32_t* vals, uint32_t* rkeys, uint32_t* rvals, hipStream_t s) {
+  if (nsteps <= 0 || n_edges <= 0) return;
+  dim3 grid((g.C + 2 * ((g.U + 3) / 4) + 255) / 256, S, nsteps);
+  window_keys_kernel<<<grid, 256, 0, s>>>(g, src, dst, rel, n_edges, chunk0, S, stride, keys, vals, rkeys, rvals);
 }
 
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s) {

@@ -93,11 +93,23 @@ __global__ __launch_bounds__(256) void scan_tiles(const uint32_t* in, int64_t n,
 }
 
 // ---------------------------------------------------------------- radix sort
+// Sorts of several independent segments run as one launch: segment
+// blockIdx.y holds n_full keys at keys + y * stride (the last n_last), with
+// its own digit counts at hist + y * 256 * nblocks.
+struct SortSeg {
+  int64_t stride;
+  int n_full, n_last, nseg;
+  __device__ __forceinline__ int n(int y) const { return y == nseg - 1 ? n_last : n_full; }
+};
+
 // Per-block digit counts; each thread loads its IPT keys up front.
 template <int IPT>
-__global__ __launch_bounds__(256) void radix_hist(const uint32_t* keys, int n, int shift, int nblocks,
+__global__ __launch_bounds__(256) void radix_hist(const uint32_t* keys, SortSeg sg, int shift, int nblocks,
                                                   uint32_t* hist) {
   __shared__ uint32_t h[256];
+  const int n = sg.n(blockIdx.y);
+  keys += blockIdx.y * sg.stride;
+  hist += (int64_t)blockIdx.y * 256 * nblocks;
   h[threadIdx.x] = 0;
   const int base = blockIdx.x * (256 * IPT);
   uint32_t k[IPT];
@@ -126,10 +138,19 @@ __global__ __launch_bounds__(256) void radix_hist(const uint32_t* keys, int n, i
 // position per digit from them (its digit's earlier blocks, plus a block scan
 // of the digit totals), so no separate scan launch is needed.
 template <int IPT, bool RAW>
-__global__ __launch_bounds__(256) void radix_scatter(const uint32_t* keys, const uint32_t* vals, int n,
+__global__ __launch_bounds__(256) void radix_scatter(const uint32_t* keys, const uint32_t* vals, SortSeg sg,
                                                      int shift, int nblocks, const uint32_t* offs,
                                                      uint32_t* okeys, uint32_t* ovals) {
   __shared__ uint32_t smem[4];
+  const int n = sg.n(blockIdx.y);
+  {
+    const int64_t o = blockIdx.y * sg.stride;
+    keys += o;
+    vals += o;
+    okeys += o;
+    ovals += o;
+    offs += (int64_t)blockIdx.y * 256 * nblocks;
+  }
   constexpr int R = IPT;                     // rounds of 64 keys per wave (a quarter of the tile)
   __shared__ uint32_t cnt[4][256];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -537,26 +558,36 @@ int64_t radix_hist_entries(int64_t n) { return 256 * ((n + radix_tile(n) - 1) / 
 
 int64_t radix_scan_tmp_entries(int64_t n) { return (radix_hist_entries(n) + SORT_TILE - 1) / SORT_TILE + 1; }
 
-void launch_radix_sort_to(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, uint32_t** out_keys,
-                          uint32_t** out_vals, hipStream_t s) {
+int64_t radix_segments_hist_entries(int64_t n, int nseg) {
+  return std::max<int64_t>(nseg, 1) * radix_hist_entries(n) + radix_scan_tmp_entries(n);
+}
+
+// LSD passes of 8 bits over nseg segments at once (each segment on its own;
+// nblocks <= 64 per segment for the single-launch digit offsets, else one
+// segment through the multi-launch scan).  Ping-pong with the alternate
+// buffers; the result ends in either.
+static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_alt, uint32_t* vals_alt, SortSeg sg,
+                         int bits, uint32_t* hist, uint32_t* scan_tmp, uint32_t** out_keys, uint32_t** out_vals,
+                         hipStream_t s) {
   uint32_t* k_in = keys;
   uint32_t* v_in = vals;
-  if (n > 1 && bits > 0) {
-    const int tile = radix_tile(n);
-    const int nblocks = (n + tile - 1) / tile;
+  const int nmax = std::max(sg.n_full, sg.n_last);
+  if (nmax > 1 && bits > 0) {
+    const int tile = radix_tile(nmax);
+    const int nblocks = (nmax + tile - 1) / tile;
     const int64_t nh = (int64_t)256 * nblocks;
-    uint32_t* k_out = w.keys_alt;
-    uint32_t* v_out = w.vals_alt;
+    uint32_t* k_out = keys_alt;
+    uint32_t* v_out = vals_alt;
     const int passes = (bits + 7) / 8;
+    const dim3 grid(nblocks, sg.nseg);
     for (int p = 0; p < passes; ++p) {
       const int shift = 8 * p;
-      radix_hist<SORT_IPT><<<nblocks, 256, 0, s>>>(k_in, n, shift, nblocks, w.hist);
+      radix_hist<SORT_IPT><<<grid, 256, 0, s>>>(k_in, sg, shift, nblocks, hist);
       if (nblocks <= 64) {
-        radix_scatter<SORT_IPT, true><<<nblocks, 256, 0, s>>>(k_in, v_in, n, shift, nblocks, w.hist, k_out, v_out);
+        radix_scatter<SORT_IPT, true><<<grid, 256, 0, s>>>(k_in, v_in, sg, shift, nblocks, hist, k_out, v_out);
       } else {
-        launch_exclusive_scan(w.hist, nh, w.hist, w.scan_tmp, nullptr, s);
-        radix_scatter<SORT_IPT, false><<<nblocks, 256, 0, s>>>(k_in, v_in, n, shift, nblocks, w.hist, k_out,
-                                                               v_out);
+        launch_exclusive_scan(hist, nh, hist, scan_tmp, nullptr, s);
+        radix_scatter<SORT_IPT, false><<<grid, 256, 0, s>>>(k_in, v_in, sg, shift, nblocks, hist, k_out, v_out);
       }
       uint32_t* t = k_in; k_in = k_out; k_out = t;
       t = v_in; v_in = v_out; v_out = t;
@@ -564,6 +595,42 @@ void launch_radix_sort_to(uint32_t* keys, uint32_t* vals, int n, int bits, SortW
   }
   *out_keys = k_in;
   *out_vals = v_in;
+}
+
+void launch_radix_sort_to(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, uint32_t** out_keys,
+                          uint32_t** out_vals, hipStream_t s) {
+  const SortSeg sg{0, n, n, 1};
+  radix_passes(keys, vals, w.keys_alt, w.vals_alt, sg, bits, w.hist, w.scan_tmp, out_keys, out_vals, s);
+}
+
+void launch_radix_sort_segments(uint32_t* keys, uint32_t* vals, uint32_t* keys_alt, uint32_t* vals_alt,
+                                int64_t stride, int n_full, int n_last, int nseg, int bits, uint32_t* hist,
+                                uint32_t** out_keys, uint32_t** out_vals, hipStream_t s) {
+  if (nseg <= 0) {
+    *out_keys = keys;
+    *out_vals = vals;
+    return;
+  }
+  const int nmax = std::max(n_full, n_last);
+  if ((nmax + radix_tile(nmax) - 1) / radix_tile(nmax) <= 64) {
+    const SortSeg sg{stride, n_full, n_last, nseg};
+    radix_passes(keys, vals, keys_alt, vals_alt, sg, bits, hist, nullptr, out_keys, out_vals, s);
+    return;
+  }
+  // segments too long for single-launch offsets: one at a time (the same
+  // number of passes, so every result lands in the same buffer)
+  for (int y = 0; y < nseg; ++y) {
+    const int64_t o = y * stride;
+    const int n = y == nseg - 1 ? n_last : n_full;
+    const SortSeg sg{0, n, n, 1};
+    uint32_t *ok = nullptr, *ov = nullptr;
+    radix_passes(keys + o, vals + o, keys_alt + o, vals_alt + o, sg, bits, hist, hist + radix_hist_entries(nmax),
+                 &ok, &ov, s);
+    if (y == 0) {
+      *out_keys = ok - o;
+      *out_vals = ov - o;
+    }
+  }
 }
 
 void launch_radix_sort(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork& w, hipStream_t s) {

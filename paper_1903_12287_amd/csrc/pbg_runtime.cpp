@@ -111,11 +111,15 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   const bool linear = ctx->op == OP_LINEAR;
   if (has_rel && !linear) b.relc = (float*)a.get(s * N * ctx->dr * 4);
   const int64_t nkeys = s * 2 * N;
-  b.keys = (uint32_t*)a.get(nkeys * 4);
-  b.vals = (uint32_t*)a.get(nkeys * 4);
+  // a window of steps: keys, values, the sort's alternate buffers and counts
+  b.keys = (uint32_t*)a.get(kSortWindow * nkeys * 4);
+  b.vals = (uint32_t*)a.get(kSortWindow * nkeys * 4);
+  ctx->wkeys_alt = (uint32_t*)a.get(kSortWindow * nkeys * 4);
+  ctx->wvals_alt = (uint32_t*)a.get(kSortWindow * nkeys * 4);
+  ctx->whist = (uint32_t*)a.get(radix_segments_hist_entries(nkeys, kSortWindow) * 4);
   if (has_rel && ctx->R > 1) {
-    b.rkeys = (uint32_t*)a.get(s * C * 4);
-    b.rvals = (uint32_t*)a.get(s * C * 4);
+    b.rkeys = (uint32_t*)a.get(kSortWindow * s * C * 4);
+    b.rvals = (uint32_t*)a.get(kSortWindow * s * C * 4);
   }
   const int width = std::max(d, has_rel && !linear ? ctx->dr : 0);
   if (!alloc_sortwork(a, ctx->sw, std::max<int64_t>(nkeys, s * C), width)) {
@@ -457,6 +461,12 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   };
   (void)hipEventRecord(ev0, cs);
 
+  const int64_t kstride = (int64_t)S * 2 * N;   // sort keys per step (a full step)
+  uint32_t* const win_keys = ctx->bufs.keys;
+  uint32_t* const win_vals = ctx->bufs.vals;
+  uint32_t* const win_rkeys = b.rkeys;
+  uint32_t* const win_rvals = b.rvals;
+  uint32_t *wsk = nullptr, *wsv = nullptr;   // the window's sorted keys and values
   for (int64_t t = 0; t < nsteps; ++t) {
     const int64_t c0 = t * S;
     const int nch = (int)std::min<int64_t>(S, nchunks - c0);
@@ -468,16 +478,30 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     b.dst = dst + c0 * C;
     b.rel = rel ? rel + c0 * C : nullptr;
 
-    mark(t, 0);
     // the sort keys (table, row) of every contribution row follow from the
-    // edges and the negative draws alone: keys and entity sort run on the
-    // side stream beside the gather and the contractions
+    // edges and the negative draws alone: at the start of each window of
+    // steps, its keys are built and its sorts run as one batch
+    const int64_t wi = t % kSortWindow;
+    if (wi == 0) {
+      const int wn = (int)std::min<int64_t>(kSortWindow, nsteps - t);
+      const int64_t e1 = std::min<int64_t>(n_edges, (t + wn) * (int64_t)S * C);
+      launch_window_keys(g, src + c0 * C, dst + c0 * C, rel ? rel + c0 * C : nullptr, e1 - c0 * C,
+                         neg->first_chunk + c0, S, wn, kstride, win_keys, win_vals, win_rkeys, win_rvals, cs);
+      const int64_t tl = t + wn - 1;   // the window's last step
+      const int nch_l = (int)std::min<int64_t>(S, nchunks - tl * S);
+      const int m_l = (int)std::min<int64_t>((int64_t)S * C, n_edges - tl * S * C);
+      launch_radix_sort_segments(win_keys, win_vals, ctx->wkeys_alt, ctx->wvals_alt, kstride, (int)kstride,
+                                 2 * (nch_l * U + m_l), wn, key_bits, ctx->whist, &wsk, &wsv, cs);
+    }
     const int nkeys = 2 * (nch * U + m_step);
-    uint32_t *skeys = nullptr, *svals = nullptr;
-    side_fork(ctx);
-    launch_sort_keys(g, b, ctx->side);
-    launch_radix_sort_to(b.keys, b.vals, nkeys, key_bits, ctx->sw, &skeys, &svals, ctx->side);
-    side_mark(ctx, 0);
+    uint32_t* skeys = wsk + wi * kstride;
+    uint32_t* svals = wsv + wi * kstride;
+    if (win_rkeys) {
+      b.rkeys = win_rkeys + wi * (int64_t)S * C;
+      b.rvals = win_rvals + wi * (int64_t)S * C;
+    }
+
+    mark(t, 0);
 
     if (linear) launch_pad_linear(ctx->relp, d, dp, ctx->relA, ctx->relAT, cs);
     launch_gather(g, b, cs);
@@ -498,7 +522,6 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     if (rel_side) side_fork(ctx);
 
     // entities: contribution rows in (table, row) order, segment sums, Adagrad
-    side_wait(ctx, 0);
     launch_entity_update(g, b, skeys, svals, nkeys, ctx->sw, lr, cs);
 
     // relations

@@ -73,6 +73,11 @@ struct pbg_ctx {
   StepBufs bufs{};
   BufsH h{};
   SortWork sw{};
+  // sort keys / values of a window of steps ([kSortWindow][2 S N]) and the
+  // alternate buffers and digit counts of their batched sort
+  uint32_t* wkeys_alt = nullptr;
+  uint32_t* wvals_alt = nullptr;
+  uint32_t* whist = nullptr;
   float* relpartial = nullptr;
   float* relA = nullptr;    // linear operator: A and A^T, rows padded to dp
   float* relAT = nullptr;
@@ -94,6 +99,8 @@ struct pbg_ctx {
 };
 
 constexpr int kPhaseEvents = 7;
+// steps whose entity sort keys are built and sorted together, as one batch
+constexpr int kSortWindow = 32;
 
 pbg_status set_err(pbg_ctx* ctx, pbg_status st, const char* fmt, ...);
 // work of a step on the side stream: side_fork makes the side stream wait for
