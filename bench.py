@@ -177,11 +177,13 @@ def roofline(st, peak, kernel, traffic=None, pieces=None):
     float32 contraction runs as that many exact-piece bf16 products, reported
     beside it as the executed matrix-instruction rate."""
     launches = max(1, st["steps"])
-    flops = st["score_flops"] / 3.0
-    achieved = flops / (st["score_ms"] / 1e3) / 1e12 if st["score_ms"] > 0 else None
+    timed = max(1, st.get("score_timed_steps") or launches)   # launches the events bracketed
+    flops = st["score_flops"] / 3.0 / launches                   # per launch
+    avg_ms = st["score_ms"] / timed
+    achieved = flops / (avg_ms / 1e3) / 1e12 if avg_ms > 0 else None
     out = {"kernel": kernel, "bound": "mfma", "achieved": achieved, "peak": peak,
            "unit": "TFLOP/s", "frac": achieved / peak if achieved else None, "traffic": traffic,
-           "avg_launch_ms": st["score_ms"] / launches, "flops_per_launch": flops / launches}
+           "avg_launch_ms": avg_ms, "flops_per_launch": flops, "timed_launches": timed}
     if pieces and achieved:
         out["executed"] = {"instruction": "v_mfma_f32_16x16x32_bf16", "piece_products": pieces,
                            "achieved": pieces * achieved, "peak": PEAK_BF16_MFMA, "unit": "TFLOP/s",

@@ -74,8 +74,9 @@ enum {
    * stream and report the summed times in pbg_stats (each event adds a few
    * microseconds to a step). */
   PBG_F_PHASE_TIMING = 2u,
-  /* Record HIP events around the score contraction only (score_ms in
-   * pbg_stats) at two events per step; PBG_F_PHASE_TIMING includes it. */
+  /* Record HIP events around the score contraction of every eighth step only
+   * (score_ms and score_timed_steps in pbg_stats); PBG_F_PHASE_TIMING times
+   * it on every step. */
   PBG_F_SCORE_TIMING = 4u
 };
 
@@ -121,6 +122,7 @@ typedef struct {
                                read and written and its Adagrad scalar read and written */
   double copy_ms;           /* partition / edge transfers (pbg_train_epoch) */
   int64_t partition_loads;  /* host-to-device partition loads (pbg_train_epoch) */
+  int64_t score_timed_steps; /* steps whose score contraction score_ms sums */
 } pbg_stats;
 
 /* Creates a context for a graph of num_entities entities of one type split

@@ -455,8 +455,9 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   if (score_timing && !ensure_events(ctx, (size_t)nsteps * kPhaseEvents))
     return set_err(ctx, PBG_ERR_DEVICE, "hipEventCreate failed");
   // events 1 and 2 of a step bracket the score contraction
+  auto sampled = [&](int64_t step) { return timing || step % kScoreSample == 0; };
   auto mark = [&](int64_t step, int k) {
-    if (timing || (score_timing && (k == 1 || k == 2)))
+    if (timing || (score_timing && (k == 1 || k == 2) && sampled(step)))
       (void)hipEventRecord(ctx->events[(size_t)step * kPhaseEvents + k], cs);
   };
   (void)hipEventRecord(ev0, cs);
@@ -599,13 +600,16 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   if (score_timing) {
     double* acc[6] = {&ctx->stats.gather_ms, &ctx->stats.score_ms, &ctx->stats.epilogue_ms,
                       &ctx->stats.backward_ms, &ctx->stats.opbwd_ms, &ctx->stats.update_ms};
-    for (int64_t t = 0; t < nsteps; ++t)
+    for (int64_t t = 0; t < nsteps; ++t) {
+      if (!sampled(t)) continue;
+      ++ctx->stats.score_timed_steps;
       for (int k = timing ? 0 : 1; k < (timing ? 6 : 2); ++k) {
         float pm = 0.f;
         (void)hipEventElapsedTime(&pm, ctx->events[(size_t)t * kPhaseEvents + k],
                                   ctx->events[(size_t)t * kPhaseEvents + k + 1]);
         *acc[k] += pm;
       }
+    }
   }
   ctx->stats.edges += n_edges;
   ctx->stats.chunks += nchunks;

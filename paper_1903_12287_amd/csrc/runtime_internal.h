@@ -99,6 +99,9 @@ struct pbg_ctx {
 };
 
 constexpr int kPhaseEvents = 7;
+// score-only timing brackets every kScoreSample-th step (each event record
+// costs the compute stream a few microseconds)
+constexpr int kScoreSample = 8;
 // steps whose entity sort keys are built and sorted together, as one batch
 constexpr int kSortWindow = 32;
 

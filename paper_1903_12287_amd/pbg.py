@@ -60,7 +60,8 @@ class Stats(ctypes.Structure):
                 ("backward_ms", ctypes.c_double), ("opbwd_ms", ctypes.c_double),
                 ("update_ms", ctypes.c_double), ("gather_bytes", ctypes.c_double),
                 ("score_flops", ctypes.c_double), ("update_bytes", ctypes.c_double),
-                ("copy_ms", ctypes.c_double), ("partition_loads", ctypes.c_int64)]
+                ("copy_ms", ctypes.c_double), ("partition_loads", ctypes.c_int64),
+                ("score_timed_steps", ctypes.c_int64)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
