@@ -78,6 +78,7 @@ struct StepBufs {
   float* dsum1;         // [S][C] sum_t dS1[e][t]
   double* chunkloss;    // [S][FIN_BLOCKS(C)]  loss partials of the finalisation
   unsigned long long* nuniq;   // rows touched by the entity updates of the call (segment count)
+  unsigned int* fin_ticket;    // finished workgroups of the finalisation (zero between steps)
   float* dq;
   float* dn;
   float* relc;          // [S][N][dr] relation gradient contributions

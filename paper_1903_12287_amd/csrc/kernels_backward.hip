@@ -15,7 +15,8 @@
 namespace {
 
 // ---- per-edge dL/dp, translation bias gradient, losses ------------------------
-__global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepBufs b, int softmax_scales) {
+__global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepBufs b, int softmax_scales,
+                                                                double* step_loss) {
   const int c = blockIdx.y;
   const int Cc = chunk_edges(g, c);
   double acc = 0.0;
@@ -88,16 +89,29 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
     if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
     __syncthreads();
   }
-  if (threadIdx.x == 0) b.chunkloss[(int64_t)c * gridDim.x + blockIdx.x] = red[0];
-}
-
-// step loss = sum of the partials in a fixed order: lane l sums partials
-// l, l + 64, ... in turn, then a fixed butterfly over the wave
-__global__ __launch_bounds__(64) void sum_chunks_kernel(const double* chunkloss, int n, double* out) {
-  double s = 0.0;
-  for (int c = threadIdx.x; c < n; c += 64) s += chunkloss[c];
-  s = wave_sum_d(s);
-  if (threadIdx.x == 0) *out = s;
+  // the last workgroup to finish adds all partials into the step loss, in a
+  // fixed order (lane l sums partials l, l + 64, ..., then a fixed butterfly
+  // over the wave), and re-arms the ticket for the next step
+  __shared__ bool last;
+  if (threadIdx.x == 0) {
+    b.chunkloss[(int64_t)c * gridDim.x + blockIdx.x] = red[0];
+    __threadfence();
+    const unsigned total = gridDim.x * gridDim.y;
+    last = atomicAdd(b.fin_ticket, 1u) == total - 1;
+  }
+  __syncthreads();
+  if (last && threadIdx.x < 64) {
+    __threadfence();
+    const int n = (int)(gridDim.x * gridDim.y);
+    const volatile double* part = b.chunkloss;
+    double sum = 0.0;
+    for (int i = threadIdx.x; i < n; i += 64) sum += part[i];
+    sum = wave_sum_d(sum);
+    if (threadIdx.x == 0) {
+      *step_loss = sum;
+      *b.fin_ticket = 0u;
+    }
+  }
 }
 
 // ---- operator / comparator backward: contributions and sort keys -----------
@@ -255,8 +269,7 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
 void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, bool softmax_scales,
                      hipStream_t s) {
   const int fb = fin_blocks(g.C);
-  finalize_kernel<<<dim3(fb, g.nchunks), FIN_THREADS, 0, s>>>(g, b, softmax_scales ? 1 : 0);
-  sum_chunks_kernel<<<1, 64, 0, s>>>(b.chunkloss, g.nchunks * fb, step_loss_slot);
+  finalize_kernel<<<dim3(fb, g.nchunks), FIN_THREADS, 0, s>>>(g, b, softmax_scales ? 1 : 0, step_loss_slot);
 }
 
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s) {

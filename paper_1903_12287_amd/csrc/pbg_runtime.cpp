@@ -105,6 +105,7 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   b.dpos = (float*)a.get(s * C * 4);
   b.dsum1 = (float*)a.get(s * C * 4);
   b.chunkloss = (double*)a.get(s * fin_blocks(C) * 8);
+  b.fin_ticket = (unsigned int*)a.get(4);
   b.dq = (float*)a.get(s * 2 * C * dp * 4);
   b.dn = (float*)a.get(s * 2 * N * dp * 4);
   const bool has_rel = ctx->op != OP_IDENTITY;
@@ -159,6 +160,7 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   // bf16 transposes copy them: start from zeros so they always hold finite values
   hipError_t ez = hipMemsetAsync(b.qk, 0, (size_t)s * 2 * C * dp * 4, ctx->cs);
   if (ez == hipSuccess) ez = hipMemsetAsync(b.nn, 0, (size_t)s * 2 * N * dp * 4, ctx->cs);
+  if (ez == hipSuccess) ez = hipMemsetAsync(b.fin_ticket, 0, 4, ctx->cs);
   if (ez == hipSuccess) ez = hipStreamSynchronize(ctx->cs);
   if (ez != hipSuccess) {
     ctx->ws.release();
