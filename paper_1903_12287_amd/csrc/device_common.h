@@ -99,6 +99,14 @@ __device__ __forceinline__ float group16_max(float x) {
 }
 
 // sum over the wave: the four rows by DPP, then the rows pairwise
+// Row-wise Adagrad step size 1 / (sqrt(G) + eps) (Sec. 3.1: the accumulated
+// squared gradient of a row scales its update), from the hardware square
+// root and reciprocal, each within one unit in the last place: every update
+// of the library takes it from here, so all paths round alike.
+__device__ __forceinline__ float adagrad_rcp(float G) {
+  return __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(G) + PBG_EPS_ADAGRAD);
+}
+
 __device__ __forceinline__ float wave_sum(float x) {
   x = group16_sum(x);
   x += __shfl_xor(x, 16, PBG_WAVE);

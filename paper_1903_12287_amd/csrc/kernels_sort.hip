@@ -240,7 +240,7 @@ __device__ __forceinline__ void seg_apply(const StepGeom& g, const StepBufs& b, 
     float* G = (tbl ? b.G_j : b.G_i) + row;
     const float gg = row_dot(acc, acc);
     const float Gn = *G + gg;
-    const float scale = lr / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
+    const float scale = lr * adagrad_rcp(Gn);
 #pragma unroll
     for (int q = 0; q < RQ; ++q) {
       const int f = lane + 64 * q;
@@ -257,14 +257,61 @@ __device__ __forceinline__ void seg_apply(const StepGeom& g, const StepBufs& b, 
         const float gf = acc.v[q];
         const float Gn = G[f] + gf * gf;
         G[f] = Gn;
-        p[f] -= lr * gf / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
+        p[f] -= lr * gf * adagrad_rcp(Gn);
       }
     }
   }
 }
 
+// Rows as RQ contiguous floats per lane (lane L holds elements RQ L .. RQ L +
+// RQ - 1): one 8- or 16-byte access per lane instead of RQ strided ones.  vec:
+// the row pitch and the width are multiples of RQ (the row starts are then
+// aligned for the vector access); the lane holding the width's end, and every
+// lane when vec is false, moves element by element.
+template <int RQ>
+__device__ __forceinline__ void crow_load(float (&v)[RQ], const float* r, int lane, int width, bool vec) {
+  const int f0 = RQ * lane;
+  if (vec && f0 + RQ <= width) {
+    if (RQ == 2) {
+      const float2 x = *(const float2*)(r + f0);
+      v[0] = x.x;
+      v[1] = x.y;
+    } else {
+#pragma unroll
+      for (int c = 0; c < RQ / 4; ++c) {
+        const float4 x = *(const float4*)(r + f0 + 4 * c);
+        v[4 * c] = x.x;
+        v[4 * c + 1] = x.y;
+        v[4 * c + 2] = x.z;
+        v[4 * c + 3] = x.w;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < RQ; ++q) v[q] = f0 + q < width ? r[f0 + q] : 0.0f;
+  }
+}
+
+template <int RQ>
+__device__ __forceinline__ void crow_store(float* r, const float (&v)[RQ], int lane, int width, bool vec) {
+  const int f0 = RQ * lane;
+  if (vec && f0 + RQ <= width) {
+    if (RQ == 2) {
+      *(float2*)(r + f0) = make_float2(v[0], v[1]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < RQ / 4; ++c)
+        *(float4*)(r + f0 + 4 * c) = make_float4(v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < RQ; ++q)
+      if (f0 + q < width) r[f0 + q] = v[q];
+  }
+}
+
 // Block of SEG_BLOCK sorted positions, one wave.  RQ floats of a row per lane
-// (lane L holds elements L + 64 q, q < RQ; width <= 64 RQ).  The rows are
+// (lane L holds elements RQ L .. RQ L + RQ - 1; width <= 64 RQ).  The rows are
 // loaded SB positions at a time, together with the embedding rows of the
 // whole segments ending among them, all loads in flight together, and a
 // running sum restarted at every piece start leaves each piece's in-order
@@ -278,7 +325,7 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
                                                         float lr) {
   constexpr int SB = 32 / RQ;                      // positions per batch of loads
   const int lane = threadIdx.x & 63;
-  const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int blk = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int p0 = blk * SEG_BLOCK;
   if (p0 >= n) return;
   const int np = min(SEG_BLOCK, n - p0);
@@ -317,6 +364,15 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
   float gold = 0.0f;
   if (MODE == SEG_ENTITY && valid && ((whole >> (pos - p0)) & 1u)) gold = (tbl ? b.G_j : b.G_i)[rowid];
 
+  // row pointers are wave-uniform (the position's value and key are read
+  // from their lane into scalar registers), so the addresses cost no vector
+  // instructions
+  // the keys, values and Adagrad state of the block have landed before the
+  // loop: their lanes are read into scalar registers inside it, and without
+  // this wait every such read would wait for all loads in flight
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  const bool vec_c = (ld % RQ) == 0 && (width % RQ) == 0;
+  const bool vec_e = (g.d % RQ) == 0 && (width % RQ) == 0;
   float run[RQ];
 #pragma unroll
   for (int q = 0; q < RQ; ++q) run[q] = 0.0f;
@@ -328,21 +384,16 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
 #pragma unroll
     for (int u = 0; u < SB; ++u) {
       const int uu = b0 + u;
-      const bool ok = uu < np;
-      const uint32_t vu = (uint32_t)__shfl((int)vidx, uu & 31, 64);
-      const float* r = rows + (int64_t)vu * ld;
 #pragma unroll
-      for (int q = 0; q < RQ; ++q) {
-        const int f = lane + 64 * q;
-        t[u][q] = (ok && f < width) ? r[f] : 0.0f;
-      }
-      const bool upd = MODE == SEG_ENTITY && ok && ((whole >> uu) & 1u);
-      const uint32_t key = (uint32_t)__shfl((int)k, uu & 31, 64);
-      const float* emb = ((key >> g.rb) ? b.emb_j : b.emb_i) + (int64_t)(key & ((1u << g.rb) - 1u)) * g.d;
-#pragma unroll
-      for (int q = 0; q < RQ; ++q) {
-        const int f = lane + 64 * q;
-        th[u][q] = (upd && f < width) ? emb[f] : 0.0f;
+      for (int q = 0; q < RQ; ++q) t[u][q] = th[u][q] = 0.0f;
+      if (uu < np) {
+        const uint32_t vu = (uint32_t)__builtin_amdgcn_readlane((int)vidx, uu);
+        crow_load<RQ>(t[u], rows + (int64_t)vu * ld, lane, width, vec_c);
+        if (MODE == SEG_ENTITY && ((whole >> uu) & 1u)) {
+          const uint32_t key = (uint32_t)__builtin_amdgcn_readlane((int)k, uu);
+          const float* emb = ((key >> g.rb) ? b.emb_j : b.emb_i) + (int64_t)(key & ((1u << g.rb) - 1u)) * g.d;
+          crow_load<RQ>(th[u], emb, lane, width, vec_e);
+        }
       }
     }
 #pragma unroll
@@ -360,16 +411,11 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
     for (int u = 0; u < SB; ++u) {
       const int uu = b0 + u;
       if (uu >= np || !((pend >> uu) & 1u)) continue;
-      const uint32_t key = (uint32_t)__shfl((int)k, uu, 64);
+      const uint32_t key = (uint32_t)__builtin_amdgcn_readlane((int)k, uu);
       if (!((whole >> uu) & 1u)) {
         const bool first = !(pstart & ((2u << uu) - 2u));   // no piece start in (0, uu]
         const int s0 = first ? 0 : last_start;
-        float* out = partial + (int64_t)(p0 + s0) * width;
-#pragma unroll
-        for (int q = 0; q < RQ; ++q) {
-          const int f = lane + 64 * q;
-          if (f < width) out[f] = t[u][q];
-        }
+        crow_store<RQ>(partial + (int64_t)(p0 + s0) * width, t[u], lane, width, vec_c);
       } else if (MODE == SEG_ENTITY) {
         const uint32_t tb = key >> g.rb;
         const uint32_t row = key & ((1u << g.rb) - 1u);
@@ -377,27 +423,27 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
         float gs = 0.0f;
 #pragma unroll
         for (int q = 0; q < RQ; ++q) gs += t[u][q] * t[u][q];
-        const float Gn = __shfl(gold, uu, 64) + wave_sum(gs);
-        const float scale = lr / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
+        const float Gn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gold), uu)) + wave_sum(gs);
+        const float scale = lr * adagrad_rcp(Gn);
+        float nv[RQ];
 #pragma unroll
-        for (int q = 0; q < RQ; ++q) {
-          const int f = lane + 64 * q;
-          if (f < width) emb[f] = th[u][q] - scale * t[u][q];
-        }
+        for (int q = 0; q < RQ; ++q) nv[q] = th[u][q] - scale * t[u][q];
+        crow_store<RQ>(emb, nv, lane, width, vec_e);
         if (lane == 0) (tb ? b.G_j : b.G_i)[row] = Gn;
       } else {
         float* p = b.relp + (int64_t)key * width;
         float* G = b.relG + (int64_t)key * width;
+        float pv[RQ], Gv[RQ];
+        crow_load<RQ>(pv, p, lane, width, vec_c);
+        crow_load<RQ>(Gv, G, lane, width, vec_c);
 #pragma unroll
         for (int q = 0; q < RQ; ++q) {
-          const int f = lane + 64 * q;
-          if (f < width) {
-            const float gf = t[u][q];
-            const float Gn = G[f] + gf * gf;
-            G[f] = Gn;
-            p[f] -= lr * gf / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
-          }
+          const float gf = t[u][q];
+          Gv[q] += gf * gf;
+          pv[q] -= lr * gf * adagrad_rcp(Gv[q]);
         }
+        crow_store<RQ>(G, Gv, lane, width, vec_c);
+        crow_store<RQ>(p, pv, lane, width, vec_c);
       }
     }
   }
@@ -412,7 +458,7 @@ __global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, c
                                                        int width, const float* partial, const uint32_t* segflag,
                                                        float lr) {
   const int lane = threadIdx.x & 63;
-  const int blk = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int blk = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int p0 = blk * SEG_BLOCK;
   const int p1 = p0 + SEG_BLOCK;
   const int nblk = (n + SEG_BLOCK - 1) / SEG_BLOCK;
@@ -530,7 +576,7 @@ __global__ __launch_bounds__(1024) void relation_single_adagrad(float* relp, flo
   for (int q = 0; q < 16; ++q) gt += red[q][lane];
   const float Gn = relG[f] + gt * gt;
   relG[f] = Gn;
-  relp[f] -= lr * gt / (sqrtf(Gn) + PBG_EPS_ADAGRAD);
+  relp[f] -= lr * gt * adagrad_rcp(Gn);
 }
 
 int grid_for(int64_t n, int per_block, int cap) {
