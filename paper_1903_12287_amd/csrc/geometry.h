@@ -22,6 +22,12 @@
 
 enum { OP_IDENTITY = 0, OP_TRANSLATION = 1, OP_DIAGONAL = 2, OP_LINEAR = 3, OP_COMPLEX = 4 };
 enum { CMP_DOT = 0, CMP_COS = 1 };
+
+// With the cos comparator (never with the linear operator) the packed Q and
+// K rows of a chunk equal its first C source and destination candidate rows
+// (g(x_s) and x_d, both normalised), so Q / K row e of side s is read from
+// row e of the candidate tile of side 1 - s and never written separately.
+#define QK_IN_NN(g) ((g).cmp == CMP_COS && (g).op != OP_LINEAR)
 enum { LOSS_RANKING = 0, LOSS_LOGISTIC = 1, LOSS_SOFTMAX = 2 };
 
 #define PBG_EPS_NORM 1e-12f

@@ -143,8 +143,10 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     const float* dq1 = b.dq + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
     float* dn0 = b.dn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
     float* dn1 = b.dn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
-    const float* q = b.qk + ((int64_t)(c * 2 + 0) * g.C + e) * dp;
-    const float* kr = b.qk + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
+    const float* q = QK_IN_NN(g) ? b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp
+                                 : b.qk + ((int64_t)(c * 2 + 0) * g.C + e) * dp;
+    const float* kr = QK_IN_NN(g) ? b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp
+                                  : b.qk + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
     Row Q, Kv, gq0, gq1, gn0, gn1;
     row_load(Q, q, d, cplx, lane);
     row_load(Kv, kr, d, cplx, lane);

@@ -71,9 +71,8 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
       const float nq = row_normalize(gq);
       const float ny = row_normalize(y);
       const float p = row_dot(gq, y);
-      row_store(gq, qrow, d, dp, cplx, lane);
+      // Q and K are these candidate rows (QK_IN_NN)
       row_store(gq, n1row, d, dp, cplx, lane);
-      row_store(y, krow, d, dp, cplx, lane);
       row_store(y, n0row, d, dp, cplx, lane);
       if (lane == 0) {
         b.pos[(int64_t)c * g.C + e] = p;

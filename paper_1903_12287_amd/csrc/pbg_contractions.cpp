@@ -78,11 +78,18 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   const bool bits = g.loss == LOSS_RANKING;
   GemmArgsH fa;
   memset(&fa, 0, sizeof(fa));
-  fa.Af = b.qk;
   fa.Bf = b.nn;
   fa.Cm = b.ds;
-  fa.a_cs = 2ll * C * dp;
-  fa.a_ss = (int64_t)C * dp;
+  if (QK_IN_NN(g)) {
+    // side s reads the candidate rows of side 1 - s
+    fa.Af = b.nn + (int64_t)N * dp;
+    fa.a_cs = 2ll * N * dp;
+    fa.a_ss = -(int64_t)N * dp;
+  } else {
+    fa.Af = b.qk;
+    fa.a_cs = 2ll * C * dp;
+    fa.a_ss = (int64_t)C * dp;
+  }
   fa.b_cs = 2ll * N * dp;
   fa.b_ss = (int64_t)N * dp;
   fa.c_cs = 2ll * C * Np;
@@ -127,7 +134,8 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   // contraction it delays the score kernel by as much as it saves here.
   const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const BufsH& h = ctx->h;
-  launch_split3_t(b.qk, (int64_t)C * dp, C, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, b.nn, (int64_t)N * dp, N,
+  const bool qn = QK_IN_NN(g);
+  launch_split3_t(qn ? b.nn : b.qk, qn ? (int64_t)N * dp : (int64_t)C * dp, qn, C, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, b.nn, (int64_t)N * dp, N,
                   h.nnT3, (int64_t)dpb * Npb, h.n3_ps, Npb, dp, dpb, nch * 2, cs);
   if (bits) {
     // dS is 0 or 1: its products with the pieces are exact (float32 sums)
@@ -182,7 +190,8 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   const int dpb = rup(d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const BufsH& h = ctx->h;
   // bf16 operands: rows [e][f], [t][f] and the transposed copies [f][e], [f][t]
-  launch_to_bf16_t(b.qk, (int64_t)C * dp, C, h.qk, (int64_t)C * dpb, h.qkT, (int64_t)dpb * Cpb, Cpb, b.nn,
+  const bool qn = QK_IN_NN(g);
+  launch_to_bf16_t(qn ? b.nn : b.qk, qn ? (int64_t)N * dp : (int64_t)C * dp, qn, C, h.qk, (int64_t)C * dpb, h.qkT, (int64_t)dpb * Cpb, Cpb, b.nn,
                    (int64_t)N * dp, N, h.nn, (int64_t)N * dpb, h.nnT, (int64_t)dpb * Npb, Npb, dp, dpb, nch * 2, cs);
 
   const bool bits = g.loss == LOSS_RANKING;
