@@ -86,17 +86,16 @@ void launch_gemm_split_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batche
 void launch_gemm_bf16_pair(const GemmArgsH& a0, const GemmArgsH& a1, int batches, hipStream_t s);
 // bf16 path: Q and N rows (fp32, [rows][ld_src]) rounded once to bf16 rows
 // [rows][kp] and transposed copies [kp][ldT], both operands in one launch.
-// q_swap = 1: batch z of Q is read from source batch z ^ 1 (Q and K held as
-// candidate rows of the other side)
-void launch_to_bf16_t(const float* q, int64_t q_bs, int q_swap, int q_rows, uint16_t* qh, int64_t qh_bs, uint16_t* qT,
+// q = nullptr: N only
+void launch_to_bf16_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qh, int64_t qh_bs, uint16_t* qT,
                       int64_t qT_bs, int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nh,
                       int64_t nh_bs, uint16_t* nT, int64_t nT_bs, int n_ldT, int ld_src, int kp, int batches,
                       hipStream_t s);
 // fp32 rows [rows][ld_src] of Q and of N -> the exact bf16 pieces
 // x = h + m + l as three transposed planes [kp][ld_T] each (ps elements
 // apart, rows past `rows` up to ld_T zero), both operands in one launch.
-// ld_src is a multiple of 4, ld_T of 8.  q_swap as for launch_to_bf16_t.
-void launch_split3_t(const float* q, int64_t q_bs, int q_swap, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,
+// ld_src is a multiple of 4, ld_T of 8.  q = nullptr: N only.
+void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,
                      int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nT, int64_t nT_bs,
                      int64_t n_ps, int n_ldT, int ld_src, int kp, int batches, hipStream_t s);
 

@@ -1110,7 +1110,6 @@ __global__ __launch_bounds__(256) void gemm_bits_pair_kernel(GemmArgsH a0, int t
 struct Bf16T {
   const float* src;
   int64_t src_bs;
-  int swap;   // 1: batch z reads source batch z ^ 1 (the other side's rows)
   int rows, ld_src;
   uint16_t* dst;
   int64_t dst_bs;
@@ -1127,7 +1126,7 @@ __global__ __launch_bounds__(256) void to_bf16_t_kernel(Bf16T o0, Bf16T o1, int 
   const int b = first ? blockIdx.z : blockIdx.z - nz0;
   const int r0 = blockIdx.y * 64, k0 = blockIdx.x * 64;
   if (r0 >= o.ld_T) return;
-  const float* s = o.src + (int64_t)(b ^ o.swap) * o.src_bs;
+  const float* s = o.src + (int64_t)b * o.src_bs;
   uint16_t* dr = o.dst + (int64_t)b * o.dst_bs;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -1166,7 +1165,6 @@ __global__ __launch_bounds__(256) void to_bf16_t_kernel(Bf16T o0, Bf16T o1, int 
 struct Split3T {
   const float* src;
   int64_t src_bs;
-  int swap;   // 1: batch z reads source batch z ^ 1 (the other side's rows)
   int rows, ld_src;
   uint16_t* dst;
   int64_t dst_bs, ps;
@@ -1180,7 +1178,7 @@ __global__ __launch_bounds__(256) void split3_t_kernel(Split3T o0, Split3T o1, i
   const int b = first ? blockIdx.z : blockIdx.z - nz0;
   const int r0 = blockIdx.y * 64, k0 = blockIdx.x * 64;
   if (r0 >= o.rows_p) return;
-  const float* s = o.src + (int64_t)(b ^ o.swap) * o.src_bs;
+  const float* s = o.src + (int64_t)b * o.src_bs;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int it = threadIdx.x + 256 * j;
@@ -1350,25 +1348,27 @@ void launch_score_split(const GemmArgsH& a, int epi, int batches, hipStream_t s)
   else score_split_kernel<EPI_STORE, NPROD><<<nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
 }
 
-void launch_to_bf16_t(const float* q, int64_t q_bs, int q_swap, int q_rows, uint16_t* qh, int64_t qh_bs, uint16_t* qT,
+void launch_to_bf16_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qh, int64_t qh_bs, uint16_t* qT,
                       int64_t qT_bs, int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nh,
                       int64_t nh_bs, uint16_t* nT, int64_t nT_bs, int n_ldT, int ld_src, int kp, int batches,
                       hipStream_t s) {
   if (batches <= 0 || kp <= 0) return;
-  const Bf16T o0{q, q_bs, q_swap, q_rows, ld_src, qh, qh_bs, kp, qT, qT_bs, q_ldT};
-  const Bf16T o1{n, n_bs, 0, n_rows, ld_src, nh, nh_bs, kp, nT, nT_bs, n_ldT};
-  dim3 grid((kp + 63) / 64, (std::max(q_ldT, n_ldT) + 63) / 64, 2 * batches);
-  to_bf16_t_kernel<<<grid, 256, 0, s>>>(o0, o1, batches, kp);
+  const Bf16T o0{q, q_bs, q_rows, ld_src, qh, qh_bs, kp, qT, qT_bs, q_ldT};
+  const Bf16T o1{n, n_bs, n_rows, ld_src, nh, nh_bs, kp, nT, nT_bs, n_ldT};
+  const int nq = q ? batches : 0;   // no Q: only N
+  dim3 grid((kp + 63) / 64, (std::max(q ? q_ldT : 0, n_ldT) + 63) / 64, nq + batches);
+  to_bf16_t_kernel<<<grid, 256, 0, s>>>(o0, o1, nq, kp);
 }
 
-void launch_split3_t(const float* q, int64_t q_bs, int q_swap, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,
+void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,
                      int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nT, int64_t nT_bs,
                      int64_t n_ps, int n_ldT, int ld_src, int kp, int batches, hipStream_t s) {
   if (batches <= 0 || kp <= 0) return;
-  const Split3T o0{q, q_bs, q_swap, q_rows, ld_src, qT, qT_bs, q_ps, q_ldT, q_ldT};
-  const Split3T o1{n, n_bs, 0, n_rows, ld_src, nT, nT_bs, n_ps, n_ldT, n_ldT};
-  dim3 grid((kp + 63) / 64, (std::max(q_ldT, n_ldT) + 63) / 64, 2 * batches);
-  split3_t_kernel<<<grid, 256, 0, s>>>(o0, o1, batches, kp);
+  const Split3T o0{q, q_bs, q_rows, ld_src, qT, qT_bs, q_ps, q_ldT, q_ldT};
+  const Split3T o1{n, n_bs, n_rows, ld_src, nT, nT_bs, n_ps, n_ldT, n_ldT};
+  const int nq = q ? batches : 0;   // no Q: only N
+  dim3 grid((kp + 63) / 64, (std::max(q ? q_ldT : 0, n_ldT) + 63) / 64, nq + batches);
+  split3_t_kernel<<<grid, 256, 0, s>>>(o0, o1, nq, kp);
 }
 
 void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s) {

@@ -15,7 +15,8 @@ static int rup(int v, int m) { return (v + m - 1) / m * m; }
 // 3: the exact pieces of the float32 operands, ranking only) n_ps / q_ps
 // elements apart.
 static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t* dsh, const uint16_t* nT,
-                           int64_t n_ps, const uint16_t* qT, int64_t q_ps, int planes, hipStream_t cs) {
+                           int64_t n_ps, const uint16_t* qT, int64_t q_ps, int64_t q_cs, int64_t q_ss, int q_ld,
+                           int planes, hipStream_t cs) {
   const int C = g.C, N = g.N, dp = g.dp, Np = g.Np, nch = g.nchunks;
   const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const bool bits = g.loss == LOSS_RANKING;
@@ -60,11 +61,11 @@ static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t*
   na.B = qT;
   na.b_ps = q_ps;
   na.Cm = b.dn;
-  na.b_cs = 2ll * dpb * Cpb;
-  na.b_ss = (int64_t)dpb * Cpb;
+  na.b_cs = q_cs;
+  na.b_ss = q_ss;
   na.c_cs = 2ll * N * dp;
   na.c_ss = (int64_t)N * dp;
-  na.ldb = Cpb;
+  na.ldb = q_ld;
   na.mdim = DIM_NC;
   na.kdim = DIM_CC;
   launch_gemm_bf16_pair(qa, na, nch * 2, cs);
@@ -134,12 +135,18 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   // contraction it delays the score kernel by as much as it saves here.
   const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const BufsH& h = ctx->h;
+  // with QK_IN_NN, Q^T of side s is the first C columns of N^T of side 1 - s
   const bool qn = QK_IN_NN(g);
-  launch_split3_t(qn ? b.nn : b.qk, qn ? (int64_t)N * dp : (int64_t)C * dp, qn, C, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, b.nn, (int64_t)N * dp, N,
-                  h.nnT3, (int64_t)dpb * Npb, h.n3_ps, Npb, dp, dpb, nch * 2, cs);
+  launch_split3_t(qn ? nullptr : b.qk, (int64_t)C * dp, C, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, b.nn,
+                  (int64_t)N * dp, N, h.nnT3, (int64_t)dpb * Npb, h.n3_ps, Npb, dp, dpb, nch * 2, cs);
   if (bits) {
     // dS is 0 or 1: its products with the pieces are exact (float32 sums)
-    run_backward_h(g, b, nullptr, h.nnT3, h.n3_ps, h.qkT3, h.q3_ps, 3, cs);
+    if (qn)
+      run_backward_h(g, b, nullptr, h.nnT3, h.n3_ps, h.nnT3 + (int64_t)dpb * Npb, h.n3_ps, 2ll * dpb * Npb,
+                     -(int64_t)dpb * Npb, Npb, 3, cs);
+    else
+      run_backward_h(g, b, nullptr, h.nnT3, h.n3_ps, h.qkT3, h.q3_ps, 2ll * dpb * Cpb, (int64_t)dpb * Cpb, Cpb, 3,
+                     cs);
     return;
   }
   // general float32 dS (logistic, softmax): split into pieces as it is staged,
@@ -171,11 +178,19 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   qa.m_step = g.m_step;
   qa.nsides = 2;
   GemmArgsH na = qa;
-  na.B = h.qkT3;
-  na.b_ps = h.q3_ps;
-  na.b_cs = 2ll * dpb * Cpb;
-  na.b_ss = (int64_t)dpb * Cpb;
-  na.ldb = Cpb;
+  if (qn) {
+    na.B = h.nnT3 + (int64_t)dpb * Npb;   // Q^T of side s: N^T of side 1 - s
+    na.b_ps = h.n3_ps;
+    na.b_cs = 2ll * dpb * Npb;
+    na.b_ss = -(int64_t)dpb * Npb;
+    na.ldb = Npb;
+  } else {
+    na.B = h.qkT3;
+    na.b_ps = h.q3_ps;
+    na.b_cs = 2ll * dpb * Cpb;
+    na.b_ss = (int64_t)dpb * Cpb;
+    na.ldb = Cpb;
+  }
   na.Cm = b.dn;
   na.c_cs = 2ll * N * dp;
   na.c_ss = (int64_t)N * dp;
@@ -190,19 +205,27 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   const int dpb = rup(d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const BufsH& h = ctx->h;
   // bf16 operands: rows [e][f], [t][f] and the transposed copies [f][e], [f][t]
+  // with QK_IN_NN, the Q rows of side s are the first C rows of N of side
+  // 1 - s (and Q^T the first C columns of N^T): only N is converted
   const bool qn = QK_IN_NN(g);
-  launch_to_bf16_t(qn ? b.nn : b.qk, qn ? (int64_t)N * dp : (int64_t)C * dp, qn, C, h.qk, (int64_t)C * dpb, h.qkT, (int64_t)dpb * Cpb, Cpb, b.nn,
+  launch_to_bf16_t(qn ? nullptr : b.qk, (int64_t)C * dp, C, h.qk, (int64_t)C * dpb, h.qkT, (int64_t)dpb * Cpb, Cpb, b.nn,
                    (int64_t)N * dp, N, h.nn, (int64_t)N * dpb, h.nnT, (int64_t)dpb * Npb, Npb, dp, dpb, nch * 2, cs);
 
   const bool bits = g.loss == LOSS_RANKING;
   const int nw = (Np + 15) / 16, ldw = rup(C, 8);
   GemmArgsH fa;
   memset(&fa, 0, sizeof(fa));
-  fa.A = h.qk;
   fa.B = h.nn;
   fa.amode = GA_KC;
-  fa.a_cs = 2ll * C * dpb;
-  fa.a_ss = (int64_t)C * dpb;
+  if (qn) {
+    fa.A = h.nn + (int64_t)N * dpb;
+    fa.a_cs = 2ll * N * dpb;
+    fa.a_ss = -(int64_t)N * dpb;
+  } else {
+    fa.A = h.qk;
+    fa.a_cs = 2ll * C * dpb;
+    fa.a_ss = (int64_t)C * dpb;
+  }
   fa.b_cs = 2ll * N * dpb;
   fa.b_ss = (int64_t)N * dpb;
   fa.lda = dpb;
@@ -248,7 +271,11 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   launch_finalize(g, b, ctx->steploss_dev + t, false, cs);
   mark(3);
 
-  run_backward_h(g, b, h.ds, h.nnT, 0, h.qkT, 0, 1, cs);
+  if (qn)
+    run_backward_h(g, b, h.ds, h.nnT, 0, h.nnT + (int64_t)dpb * Npb, 0, 2ll * dpb * Npb, -(int64_t)dpb * Npb, Npb,
+                   1, cs);
+  else
+    run_backward_h(g, b, h.ds, h.nnT, 0, h.qkT, 0, 2ll * dpb * Cpb, (int64_t)dpb * Cpb, Cpb, 1, cs);
 }
 
 // Linear operator with one relation (Sec. 4.3: with a single relation the
