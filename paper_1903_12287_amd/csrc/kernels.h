@@ -69,6 +69,8 @@ struct GemmArgsH {
   float margin;
 };
 
+// bf16-input score contraction with a loss epilogue (EPI_LOSS, EPI_LOSS_BITS or
+// EPI_SOFTMAX_STATS)
 void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s);
 // float32 score contraction with its loss epilogue (EPI_LOSS: float32 dS in
 // Cm; EPI_LOSS_BITS; EPI_SOFTMAX_STATS) on the bf16 instructions, operands

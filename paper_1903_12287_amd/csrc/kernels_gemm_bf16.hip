@@ -1246,22 +1246,6 @@ void launch_t(const GemmArgsH& a, int tiles_n, int tiles_m, int batches, hipStre
   gemm_bf16_kernel<BN, AMODE, EPI, PL><<<(unsigned)nwg, 256, 0, s>>>(a, tiles_n, tiles_m);
 }
 
-template <int BN>
-void launch_store(const GemmArgsH& a, int tiles_n, int tiles_m, int batches, hipStream_t s) {
-  if (a.planes == 3) {
-    // float32 operand as three exact pieces: only the 0/1 ranking dS as A
-    if (a.amode == GA_BITS_ROW) launch_t<BN, GA_BITS_ROW, EPI_STORE, 3>(a, tiles_n, tiles_m, batches, s);
-    else launch_t<BN, GA_BITS_COL, EPI_STORE, 3>(a, tiles_n, tiles_m, batches, s);
-    return;
-  }
-  switch (a.amode) {
-    case GA_KC: launch_t<BN, GA_KC, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
-    case GA_MC: launch_t<BN, GA_MC, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
-    case GA_BITS_ROW: launch_t<BN, GA_BITS_ROW, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
-    default: launch_t<BN, GA_BITS_COL, EPI_STORE>(a, tiles_n, tiles_m, batches, s); break;
-  }
-}
-
 int dim_max(int sel, int fixed, int C, int U) { return sel == DIM_CC ? C : (sel == DIM_NC ? C + U : fixed); }
 
 }  // namespace
@@ -1271,15 +1255,10 @@ void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s) {
   const int maxN = dim_max(a.ndim, a.Nfix, a.C, a.U);
   if (maxM <= 0 || maxN <= 0 || batches <= 0) return;
   const int tiles_m = (maxM + BM - 1) / BM;
-  if (epi != EPI_STORE) {
-    const int tiles_n = (maxN + 127) / 128;   // = nct (PBG_SCORE_BN columns per tile)
-    if (epi == EPI_LOSS) launch_t<128, GA_KC, EPI_LOSS>(a, tiles_n, tiles_m, batches, s);
-    else if (epi == EPI_LOSS_BITS) launch_t<128, GA_KC, EPI_LOSS_BITS>(a, tiles_n, tiles_m, batches, s);
-    else launch_t<128, GA_KC, EPI_SOFTMAX_STATS>(a, tiles_n, tiles_m, batches, s);
-    return;
-  }
-  if (maxN <= 64) launch_store<64>(a, (maxN + 63) / 64, tiles_m, batches, s);
-  else launch_store<128>(a, (maxN + 127) / 128, tiles_m, batches, s);
+  const int tiles_n = (maxN + 127) / 128;   // = nct (PBG_SCORE_BN columns per tile)
+  if (epi == EPI_LOSS) launch_t<128, GA_KC, EPI_LOSS>(a, tiles_n, tiles_m, batches, s);
+  else if (epi == EPI_LOSS_BITS) launch_t<128, GA_KC, EPI_LOSS_BITS>(a, tiles_n, tiles_m, batches, s);
+  else launch_t<128, GA_KC, EPI_SOFTMAX_STATS>(a, tiles_n, tiles_m, batches, s);
 }
 
 namespace {
