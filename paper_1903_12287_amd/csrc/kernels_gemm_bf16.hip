@@ -961,6 +961,7 @@ constexpr int BT = 256;   // rows of a bits-backward tile
 template <int BN, int PL>
 struct SmemD {
   uint16_t Bs[2][PL][BN * BK];
+  uint16_t Ab[2][2 * BT];   // the slice's bit-matrix words (see dma_bits)
   float red[2][BT][2];
   float rowv[2][BT];
 };
@@ -985,41 +986,51 @@ __device__ __forceinline__ void dma_b_tile(uint16_t* dst, rsrc_t rs, int ld, int
   }
 }
 
-// bits of this lane's IM A fragments for the slice at k0 (rows
-// mrow0 + 16 i + l16, k = k0 + 8 g .. + 7): AF = 0 one 16-bit word (eight of
-// its bits), AF = 1 eight words (bit m & 15 of each)
-template <int AF, int IM>
-__device__ __forceinline__ void load_bits_frags(u32x4 (&r)[IM], rsrc_t rs, int ld, int mrow0, int mdim, int k0,
-                                                int kdim, int l16, int g) {
-#pragma unroll
-  for (int i = 0; i < IM; ++i) {
-    const int m = mrow0 + 16 * i + l16;
-    const int k = k0 + 8 * g;
-    uint32_t off = OOB;
-    if (AF == 0) {
-      if (m < mdim && k < ((kdim + 7) & ~7)) off = (uint32_t)(((int64_t)(k >> 4) * ld + m) * 2);
-      r[i] = (u32x4){__builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0), 0u, 0u, 0u};
-    } else {
-      if (m < ((mdim + 7) & ~7) && k < kdim) off = (uint32_t)(((int64_t)(m >> 4) * ld + k) * 2);
-      r[i] = bload16(rs, off);
-    }
-  }
+// The bit-matrix words of one slice (k0 .. k0 + 31) of a 256-row tile, 1 KB,
+// into LDS: each wave moves 256 bytes, four bytes a lane.
+//   AF = 0 (rows of dS): the two word columns k0 / 16, + 1 for rows
+//          m0 .. m0 + 255; wave w: column k0 / 16 + w / 2, rows
+//          m0 + 128 (w % 2) + 2 lane, + 1; LDS word (w / 2) 256 + row
+//   AF = 1 (columns of dS): word columns m0 / 16 .. + 15, rows k0 .. k0 + 31;
+//          wave w: columns 4 w + lane / 16, rows k0 + 2 (lane % 16), + 1;
+//          LDS word 32 column + row
+// The lane's byte offset at k0 = 0 is fixed for the tile (OOB past the
+// matrix); soff moves it to the slice.
+__device__ __forceinline__ void dma_bits(uint16_t* dst, rsrc_t rs, uint32_t off, int soff, int w) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(dst + 128 * w), 4, off,
+                                           soff, 0, 0);
 }
 
 template <int AF>
-__device__ __forceinline__ v8bf expand_bits_frag(u32x4 v, int m, int k, int kdim, int g) {
+__device__ __forceinline__ uint32_t bits_offset(int ld, int m0, int mdim, int kdim, int k0, int w, int lane) {
   if (AF == 0) {
-    const uint32_t bits = v.x >> (8 * (g & 1));
+    const int r = m0 + 128 * (w & 1) + 2 * lane;
+    return r < mdim ? (uint32_t)(((int64_t)(w >> 1) * ld + r) * 2) : OOB;
+  }
+  const int wc = (m0 >> 4) + 4 * w + (lane >> 4);
+  const int k = k0 + 2 * (lane & 15);
+  return (16 * wc < mdim && k < kdim) ? (uint32_t)(((int64_t)wc * ld + 2 * (lane & 15)) * 2) : OOB;
+}
+
+// this lane's fragment i of the slice in LDS -> eight bf16 0 / 1 (AF = 0:
+// row 16 i + l16 of the wave's 128, k = 8 g .. + 7; AF = 1: candidate
+// 16 i + l16 of the wave's 128, rows 8 g .. + 7 of the slice, nv of them
+// inside the chunk)
+template <int AF>
+__device__ __forceinline__ v8bf expand_bits_frag(const uint16_t* ab, int wm, int i, int l16, int g, int nv) {
+  u32x4 v;
+  if (AF == 0) {
+    const uint32_t bits = (uint32_t)ab[(g >> 1) * 256 + 128 * wm + 16 * i + l16] >> (8 * (g & 1));
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = bit_pair(__builtin_amdgcn_ubfe(bits, 2 * i, 2));
+    for (int q = 0; q < 4; ++q) v[q] = bit_pair(__builtin_amdgcn_ubfe(bits, 2 * q, 2));
   } else {
-    const int b = m & 15;
+    v = *(const u32x4*)(ab + (8 * wm + i) * 32 + 8 * g);
+    const int b = l16;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = ((v[i] >> b) & 0x00010001u) * 0x3F80u;
-    const int nv = kdim - k;   // rows from nv on lie outside the chunk
+    for (int q = 0; q < 4; ++q) v[q] = ((v[q] >> b) & 0x00010001u) * 0x3F80u;
     if (nv < 8) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] &= (2 * i + 1 < nv) ? 0xFFFFFFFFu : (2 * i < nv ? 0xFFFFu : 0u);
+      for (int q = 0; q < 4; ++q) v[q] &= (2 * q + 1 < nv) ? 0xFFFFFFFFu : (2 * q < nv ? 0xFFFFu : 0u);
     }
   }
   return __builtin_bit_cast(v8bf, v);
@@ -1037,7 +1048,6 @@ __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, 
   const int w = tid >> 6;
   const int wm = w >> 1, wn = w & 1;
   const int l16 = lane & 15, g = lane >> 4;
-  const int mrow0 = t.m0 + WMR * wm;
   const rsrc_t ra = make_rsrc(a.A + t.c * a.a_cs + t.side * a.a_ss);
   rsrc_t rb[PL];
 #pragma unroll
@@ -1050,8 +1060,11 @@ __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, 
     for (int j = 0; j < JN; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
 
   const int nk = (t.K + BK - 1) / BK;
-  u32x4 pa[IM];
-  load_bits_frags<AF, IM>(pa, ra, a.lda, mrow0, t.M, 0, t.K, l16, g);
+  // bytes per slice of the bit-matrix DMA; the lane's offset is fixed except
+  // in a ragged last slice of the AF = 1 rows
+  const int a_step = AF == 0 ? 4 * a.lda : 2 * BK;
+  uint32_t aoff = bits_offset<AF>(a.lda, t.m0, t.M, t.K, 0, w, lane);
+  dma_bits(sm.Ab[0], ra, aoff, 0, w);
 #pragma unroll
   for (int p = 0; p < PL; ++p) dma_b_tile<BN>(sm.Bs[0][p], rb[p], a.ldb, t.n0, t.N, 0, t.K, w, lane);
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's loads have landed
@@ -1061,10 +1074,12 @@ __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, 
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
     v8bf af[IM];
+    const int nv = t.K - (kt * BK + 8 * g);
 #pragma unroll
-    for (int i = 0; i < IM; ++i) af[i] = expand_bits_frag<AF>(pa[i], mrow0 + 16 * i + l16, kt * BK + 8 * g, t.K, g);
+    for (int i = 0; i < IM; ++i) af[i] = expand_bits_frag<AF>(sm.Ab[buf], wm, i, l16, g, nv);
     if (kt + 1 < nk) {
-      load_bits_frags<AF, IM>(pa, ra, a.lda, mrow0, t.M, (kt + 1) * BK, t.K, l16, g);
+      if (AF == 1 && kt + 2 == nk) aoff = bits_offset<AF>(a.lda, t.m0, t.M, t.K, (kt + 1) * BK, w, lane);
+      dma_bits(sm.Ab[buf ^ 1], ra, aoff, (kt + 1) * a_step, w);
 #pragma unroll
       for (int p = 0; p < PL; ++p)
         dma_b_tile<BN>(sm.Bs[buf ^ 1][p], rb[p], a.ldb, t.n0, t.N, (kt + 1) * BK, t.K, w, lane);
