@@ -233,6 +233,22 @@ pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int32_t* rel, c
                          const int32_t* known_dst, int64_t n_known, int32_t* ranks,
                          double* mrr_host, double* hits10_host);
 
+/* Raw link-prediction ranks against a given candidate set (Sec. 5, Freebase
+ * evaluation: for graphs too large to rank against every entity, each eval
+ * edge is ranked against candidate nodes sampled by their prevalence in the
+ * training data; the caller draws the candidates and passes their ids).
+ * For each triple (s, r, d): destination rank
+ * 1 + #{j : cand[j] != d, f(s, r, cand[j]) >= f(s, r, d)}, then source rank
+ * 1 + #{j : cand[j] != s, f(cand[j], r, d) >= f(s, r, d)}; no filter, and a
+ * candidate listed k times counts k times.  The same n_cand candidates
+ * (device int32, entity ids of partition 0) serve every triple and both
+ * sides.  ranks is int32 [2n] (device): destination ranks first.  mrr_host /
+ * hits10_host (nullable) as for pbg_rank_eval.  Only for P == 1 (else
+ * UNSUPPORTED); an id out of range is INVALID_ARG and nothing is written. */
+pbg_status pbg_rank_sampled(pbg_ctx* ctx, const int32_t* src, const int32_t* rel, const int32_t* dst,
+                            int64_t n, const int32_t* cand, int64_t n_cand, int32_t* ranks,
+                            double* mrr_host, double* hits10_host);
+
 /* The uniform negatives pbg_train_bucket draws (Sec. 4.3; Philox map as
  * described there) for chunks first_chunk .. first_chunk + n_chunks - 1 of
  * bucket (i, j): out (device, int32) is [n_chunks][2][num_uniform], side 0

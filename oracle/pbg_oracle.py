@@ -513,3 +513,44 @@ def rank_eval(model: Model, src, rel, dst, known_src, known_rel, known_dst, tol:
     if tol > 0:
         return ranks, mrr, hits10, lo_r, hi_r
     return ranks, mrr, hits10
+
+
+def rank_sampled(model: Model, src, rel, dst, cand, tol: float = 0.0):
+    """Raw ranks of each triple among a given candidate list (Sec. 5, Freebase
+    evaluation, where each eval edge meets candidate nodes sampled by their
+    prevalence; the caller draws them).
+
+    Destination side: 1 + #{j : cand[j] != d, f(s, r, cand[j]) >= f(s, r, d)};
+    source side: 1 + #{j : cand[j] != s, f(cand[j], r, d) >= f(s, r, d)}.  No
+    filter; a candidate listed k times counts k times.  Same return values as
+    rank_eval (with tol > 0, also the rank bounds for scores within tol)."""
+    assert model.P == 1
+    E = model.emb[0]
+    src = np.asarray(src, np.int64)
+    dst = np.asarray(dst, np.int64)
+    cand = np.asarray(cand, np.int64)
+    rel = np.zeros(len(src), np.int64) if rel is None else np.asarray(rel, np.int64)
+    allx = torch.tensor(E, dtype=_F64)
+    cx = allx[torch.tensor(cand)]
+    ranks = np.zeros(2 * len(src), np.int64)
+    lo_r = np.zeros_like(ranks)
+    hi_r = np.zeros_like(ranks)
+    with torch.no_grad():
+        for e in range(len(src)):
+            s, r, d = int(src[e]), int(rel[e]), int(dst[e])
+            theta = None if model.rel is None else torch.tensor(model.rel[r], dtype=_F64)
+            q = apply_operator(model.op, allx[s:s + 1], theta)
+            pos_score = float(compare_rows(model.cmp, q, allx[d:d + 1])[0])
+            sc_d = compare_all(model.cmp, q, cx)[0].numpy()                  # f(s, r, c)
+            sc_s = compare_all(model.cmp, allx[d:d + 1], apply_operator(model.op, cx, theta))[0].numpy()  # f(c, r, d)
+            for side, sc, true_id in ((0, sc_d, d), (1, sc_s, s)):
+                keep = cand != true_id
+                slot = e if side == 0 else len(src) + e
+                ranks[slot] = 1 + int(np.count_nonzero(keep & (sc >= pos_score)))
+                lo_r[slot] = 1 + int(np.count_nonzero(keep & (sc >= pos_score + tol)))
+                hi_r[slot] = 1 + int(np.count_nonzero(keep & (sc >= pos_score - tol)))
+    mrr = float(np.mean(1.0 / ranks)) if len(ranks) else 0.0
+    hits10 = float(np.mean(ranks <= 10)) if len(ranks) else 0.0
+    if tol > 0:
+        return ranks, mrr, hits10, lo_r, hi_r
+    return ranks, mrr, hits10

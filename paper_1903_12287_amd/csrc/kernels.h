@@ -205,10 +205,13 @@ void launch_rank_tables(const StepGeom& g, const float* emb, const float* relp, 
 void launch_rank_queries(const StepGeom& g, const float* emb, const float* relp, const float* relT,
                          const int32_t* src, const int32_t* rel, const int32_t* dst, int64_t e0, int rows,
                          int side, float* Q, float* pos, float* bias, hipStream_t s);
-void launch_rank_count(const float* S, int64_t ldS, int64_t n_ent, int64_t e0, int rows, int side,
-                       int64_t n_eval, const int32_t* src, const int32_t* rel, const int32_t* dst,
+// cand: entity id of each score column (nullptr: column t is entity t)
+void launch_rank_count(const float* S, int64_t ldS, int64_t n_ent, const int32_t* cand, int64_t e0, int rows,
+                       int side, int64_t n_eval, const int32_t* src, const int32_t* rel, const int32_t* dst,
                        const float* pos, const float* bias, const int32_t* ka, const int32_t* kb,
                        const int32_t* kc, int64_t n_known, int32_t* ranks, hipStream_t s);
+// out[i] = T[idx[i]], rows of ld floats (ids checked by the caller)
+void launch_gather_rows(const float* T, const int32_t* idx, int64_t n, int ld, float* out, hipStream_t s);
 void launch_rank_metrics(const int32_t* ranks, int64_t n, double* out, hipStream_t s);
 void launch_perm_keys(const int32_t* field, const uint32_t* perm, int64_t n, uint32_t* keys,
                       uint32_t* vals_init, hipStream_t s);

@@ -16,6 +16,8 @@
 // candidates at or above the positive score, and takes back the known
 // triples' candidates by reading the same stored scores, so that the count
 // and the filter correction agree element by element.
+#include <algorithm>
+
 #include "kernels.h"
 #include "row_ops.h"
 
@@ -110,8 +112,10 @@ __device__ int64_t lower_bound2(const int32_t* a, const int32_t* b, int64_t lo, 
   return lo;
 }
 
-// one wave per query row of the stored score block
+// one wave per query row of the stored score block; column t is entity t,
+// or entity cand[t] when a candidate list is given (no filter then)
 __global__ __launch_bounds__(256) void rank_count_kernel(const float* S, int64_t ldS, int64_t n_ent,
+                                                         const int32_t* cand,
                                                          int64_t e0, int rows, int side, int64_t n_eval,
                                                          const int32_t* src, const int32_t* rel,
                                                          const int32_t* dst, const float* pos,
@@ -131,7 +135,8 @@ __global__ __launch_bounds__(256) void rank_count_kernel(const float* S, int64_t
   uint32_t cnt = 0;
   for (int64_t t = lane; t < n_ent; t += 64) {
     const float v = row[t] + bq;
-    cnt += (v >= p && t != true_id) ? 1u : 0u;
+    const int64_t id = cand ? (int64_t)cand[t] : t;
+    cnt += (v >= p && id != true_id) ? 1u : 0u;
   }
   // filter: candidates of known triples sharing (s, r) (side 0) or (d, r) (side 1);
   // the known triples are sorted by (s, r, d) for side 0 and (d, r, s) for side 1
@@ -225,13 +230,29 @@ void launch_rank_queries(const StepGeom& g, const float* emb, const float* relp,
                                                      pos, bias);
 }
 
-void launch_rank_count(const float* S, int64_t ldS, int64_t n_ent, int64_t e0, int rows, int side,
-                       int64_t n_eval, const int32_t* src, const int32_t* rel, const int32_t* dst,
+void launch_rank_count(const float* S, int64_t ldS, int64_t n_ent, const int32_t* cand, int64_t e0, int rows,
+                       int side, int64_t n_eval, const int32_t* src, const int32_t* rel, const int32_t* dst,
                        const float* pos, const float* bias, const int32_t* ka, const int32_t* kb,
                        const int32_t* kc, int64_t n_known, int32_t* ranks, hipStream_t s) {
   if (rows <= 0) return;
-  rank_count_kernel<<<(rows + 3) / 4, 256, 0, s>>>(S, ldS, n_ent, e0, rows, side, n_eval, src, rel, dst,
+  rank_count_kernel<<<(rows + 3) / 4, 256, 0, s>>>(S, ldS, n_ent, cand, e0, rows, side, n_eval, src, rel, dst,
                                                    pos, bias, ka, kb, kc, n_known, ranks);
+}
+
+// rows out[i] = T[idx[i]] of ld floats
+__global__ void gather_rows_kernel(const float* T, const int32_t* idx, int64_t n, int ld, float* out) {
+  const int64_t total = n * ld;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < total; k += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = k / ld;
+    out[k] = T[(int64_t)idx[i] * ld + (k - i * ld)];
+  }
+}
+
+void launch_gather_rows(const float* T, const int32_t* idx, int64_t n, int ld, float* out, hipStream_t s) {
+  if (n <= 0) return;
+  const int64_t total = n * ld;
+  const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 4096);
+  gather_rows_kernel<<<blocks, 256, 0, s>>>(T, idx, n, ld, out);
 }
 
 void launch_rank_metrics(const int32_t* ranks, int64_t n, double* out, hipStream_t s) {

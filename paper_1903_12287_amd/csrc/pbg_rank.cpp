@@ -58,18 +58,20 @@ void sort_known(const int32_t* first, int first_bits, const int32_t* second, int
   launch_gather3(vals, first, second, third, n, oa, ob, oc, s);
 }
 
-}  // namespace
-
-extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int32_t* rel, const int32_t* dst,
-                                    int64_t n, const int32_t* known_src, const int32_t* known_rel,
-                                    const int32_t* known_dst, int64_t n_known, int32_t* ranks,
-                                    double* mrr_host, double* hits10_host) {
+// Ranks against all entities with the known triples filtered out (cand ==
+// nullptr), or raw ranks against the n_cand entities cand[] (no filter).
+pbg_status rank_impl(pbg_ctx* ctx, const char* name, const int32_t* src, const int32_t* rel, const int32_t* dst,
+                     int64_t n, const int32_t* known_src, const int32_t* known_rel, const int32_t* known_dst,
+                     int64_t n_known, const int32_t* cand, int64_t n_cand, int32_t* ranks, double* mrr_host,
+                     double* hits10_host) {
   if (!ctx) return PBG_ERR_INVALID_ARG;
   if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
   ctx->err.clear();
-  if (ctx->P != 1) return set_err(ctx, PBG_ERR_UNSUPPORTED, "pbg_rank_eval needs a single partition");
+  if (ctx->P != 1) return set_err(ctx, PBG_ERR_UNSUPPORTED, "%s needs a single partition", name);
   if (n < 0 || n > 0x3FFFFFFFll || n_known < 0 || n_known > 0x7FFFFFFFll)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "n or n_known out of range");
+  if (cand && (n_cand <= 0 || n_cand > 0x7FFFFFFFll))
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "n_cand out of range");
   const Partition& pt = ctx->parts[0];
   if (!pt.emb || pt.where != PBG_MEM_DEVICE)
     return set_err(ctx, PBG_ERR_STATE, "partition 0 must be bound in device memory");
@@ -85,12 +87,13 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
   }
   hipStream_t s = ctx->cs;
   const int64_t n_ent = ctx->n;
+  const int64_t n_col = cand ? n_cand : n_ent;   // score columns
   const int d = ctx->d, dp = (d + 3) / 4 * 4;
   const bool linear = ctx->op == OP_LINEAR;
   const bool sep_src_table = ctx->cmp == CMP_COS && ctx->op != OP_IDENTITY;
 
   // query block: the score block stays near 1 GiB
-  int64_t qb = ((int64_t)1 << 28) / std::max<int64_t>(n_ent, 1);
+  int64_t qb = ((int64_t)1 << 28) / std::max<int64_t>(n_col, 1);
   qb = std::max<int64_t>(128, qb / 128 * 128);
   qb = std::min<int64_t>(qb, (n + 127) / 128 * 128);
 
@@ -102,7 +105,9 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
   float* pos = (float*)buf.get((size_t)n * 4);
   float* bias = (float*)buf.get((size_t)qb * 4);
   float* Q = (float*)buf.get((size_t)qb * dp * 4);
-  float* S = (float*)buf.get((size_t)qb * n_ent * 4);
+  float* S = (float*)buf.get((size_t)qb * n_col * 4);
+  float* C0 = cand ? (float*)buf.get((size_t)n_cand * dp * 4) : nullptr;
+  float* C1 = cand && sep_src_table ? (float*)buf.get((size_t)n_cand * dp * 4) : nullptr;
   double* metrics = (double*)buf.get(16);
   int32_t* kx[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   uint32_t *keys = nullptr, *vals = nullptr;
@@ -128,12 +133,13 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
   launch_check_ids(known_src, n_known, (int32_t)n_ent, flag, 4u, s);
   launch_check_ids(known_dst, n_known, (int32_t)n_ent, flag, 4u, s);
   if (known_rel) launch_check_ids(known_rel, n_known, ctx->R, flag, 8u, s);
+  if (cand) launch_check_ids(cand, n_cand, (int32_t)n_ent, flag, 16u, s);
   uint32_t hflag = 0;
   e = hipMemcpyAsync(&hflag, flag, 4, hipMemcpyDeviceToHost, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) return hip_fail(ctx, e, "id range check");
   if (hflag) return set_err(ctx, PBG_ERR_INVALID_ARG, "an id is out of range (flags %u: 1 eval entity, 2 eval "
-                            "relation, 4 known entity, 8 known relation)", hflag);
+                            "relation, 4 known entity, 8 known relation, 16 candidate)", hflag);
 
   StepGeom g;
   memset(&g, 0, sizeof(g));
@@ -144,6 +150,11 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
   g.cmp = ctx->cmp;
   if (linear) launch_transpose_rel(ctx->relp, relT, ctx->R, d, s);
   launch_rank_tables(g, pt.emb, ctx->relp, n_ent, T0, T1, s);
+  if (cand) {
+    // the candidates' rows of the tables, in candidate order
+    launch_gather_rows(T0, cand, n_cand, dp, C0, s);
+    if (T1) launch_gather_rows(T1, cand, n_cand, dp, C1, s);
+  }
 
   const int ebits = bits_of((uint64_t)n_ent - 1), rbits = bits_of((uint64_t)ctx->R - 1);
   if (n_known > 0) {
@@ -155,7 +166,7 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
   }
 
   for (int side = 0; side < 2; ++side) {
-    const float* T = side == 1 && T1 ? T1 : T0;
+    const float* T = cand ? (side == 1 && C1 ? C1 : C0) : (side == 1 && T1 ? T1 : T0);
     for (int64_t e0 = 0; e0 < n; e0 += qb) {
       const int rows = (int)std::min<int64_t>(qb, n - e0);
       launch_rank_queries(g, pt.emb, ctx->relp, relT, src, rel, dst, e0, rows, side, Q, pos, bias, s);
@@ -167,17 +178,17 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
       a.Cm = S;
       a.lda = dp;
       a.ldb = dp;
-      a.ldc = (int)n_ent;
+      a.ldc = (int)n_col;
       a.mdim = DIM_FIXED;
       a.Mfix = rows;
       a.ndim = DIM_FIXED;
-      a.Nfix = (int)n_ent;
+      a.Nfix = (int)n_col;
       a.kdim = DIM_FIXED;
       a.Kfix = dp;
       a.C = 1;
       a.nsides = 1;
       launch_score_split(a, EPI_STORE, 1, s);
-      launch_rank_count(S, n_ent, n_ent, e0, rows, side, n, src, rel, dst, pos, bias,
+      launch_rank_count(S, n_col, n_col, cand, e0, rows, side, n, src, rel, dst, pos, bias,
                         side == 0 ? kx[0] : kx[3], side == 0 ? kx[1] : kx[4], side == 0 ? kx[2] : kx[5],
                         n_known, ranks, s);
     }
@@ -187,8 +198,26 @@ extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int3
   e = hipGetLastError();
   if (e == hipSuccess) e = hipMemcpyAsync(hm, metrics, 16, hipMemcpyDeviceToHost, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
-  if (e != hipSuccess) return hip_fail(ctx, e, "rank_eval");
+  if (e != hipSuccess) return hip_fail(ctx, e, name);
   if (mrr_host) *mrr_host = hm[0];
   if (hits10_host) *hits10_host = hm[1];
   return PBG_OK;
+}
+
+}  // namespace
+
+extern "C" pbg_status pbg_rank_eval(pbg_ctx* ctx, const int32_t* src, const int32_t* rel, const int32_t* dst,
+                                    int64_t n, const int32_t* known_src, const int32_t* known_rel,
+                                    const int32_t* known_dst, int64_t n_known, int32_t* ranks,
+                                    double* mrr_host, double* hits10_host) {
+  return rank_impl(ctx, "pbg_rank_eval", src, rel, dst, n, known_src, known_rel, known_dst, n_known, nullptr, 0,
+                   ranks, mrr_host, hits10_host);
+}
+
+extern "C" pbg_status pbg_rank_sampled(pbg_ctx* ctx, const int32_t* src, const int32_t* rel, const int32_t* dst,
+                                       int64_t n, const int32_t* cand, int64_t n_cand, int32_t* ranks,
+                                       double* mrr_host, double* hits10_host) {
+  if (ctx && !cand && n > 0) return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL candidate array");
+  return rank_impl(ctx, "pbg_rank_sampled", src, rel, dst, n, nullptr, nullptr, nullptr, 0, cand, n_cand, ranks,
+                   mrr_host, hits10_host);
 }

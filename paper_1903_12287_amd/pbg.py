@@ -35,7 +35,7 @@ EXPORTS = (
     "pbg_bucket_init", "pbg_free", "pbg_last_error", "pbg_partition_rows",
     "pbg_relation_param_floats", "pbg_bucket_edges", "pbg_bind_partition",
     "pbg_bind_relations", "pbg_set_streams", "pbg_train_bucket", "pbg_get_step_losses",
-    "pbg_train_epoch", "pbg_score_edges", "pbg_rank_eval", "pbg_get_stats",
+    "pbg_train_epoch", "pbg_score_edges", "pbg_rank_eval", "pbg_rank_sampled", "pbg_get_stats",
     "pbg_sample_negatives",
 )
 
@@ -96,6 +96,7 @@ def library() -> ctypes.CDLL:
         "pbg_train_epoch": ([vp, vp, vp, vp, vp, ctypes.POINTER(NegConfig), f32, u64, i32, dp], i32),
         "pbg_score_edges": ([vp, i32, i32, vp, vp, vp, i64, vp], i32),
         "pbg_rank_eval": ([vp, vp, vp, vp, i64, vp, vp, vp, i64, vp, dp, dp], i32),
+        "pbg_rank_sampled": ([vp, vp, vp, vp, i64, vp, i64, vp, dp, dp], i32),
         "pbg_get_stats": ([vp, ctypes.POINTER(Stats)], i32),
         "pbg_sample_negatives": ([vp, i32, i32, i64, i64, i32, u64, vp], i32),
     }
@@ -285,6 +286,16 @@ def pbg_rank_eval(ctx, src, rel, dst, known_src, known_rel, known_dst, ranks):
         _ptr(known_rel, torch.int32, "known_rel", allow_none=True),
         _ptr(known_dst, torch.int32, "known_dst", allow_none=nk == 0), nk,
         _ptr(ranks, torch.int32, "ranks", allow_none=n == 0), ctypes.byref(mrr), ctypes.byref(hits)))
+    return mrr.value, hits.value
+
+
+def pbg_rank_sampled(ctx, src, rel, dst, cand, ranks):
+    n, nc = src.numel(), cand.numel()
+    mrr, hits = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _check(ctx, library().pbg_rank_sampled(
+        ctx, _ptr(src, torch.int32, "src", allow_none=n == 0), _ptr(rel, torch.int32, "rel", allow_none=True),
+        _ptr(dst, torch.int32, "dst", allow_none=n == 0), n, _ptr(cand, torch.int32, "cand", allow_none=nc == 0),
+        nc, _ptr(ranks, torch.int32, "ranks", allow_none=n == 0), ctypes.byref(mrr), ctypes.byref(hits)))
     return mrr.value, hits.value
 
 

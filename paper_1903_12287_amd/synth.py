@@ -224,6 +224,15 @@ def follower_graph(n=41_652_230, E=1_468_365_182, P=8, d=100, C=1000, U=1000, S=
                     C, U, S, 0.1, seed, src, None, dst)
 
 
+def prevalence_candidates(src, dst, n: int, k: int, rng) -> np.ndarray:
+    """k entity ids drawn with replacement in proportion to each entity's
+    count among the training edges' endpoints (its prevalence), as the
+    candidates of a sampled-candidate evaluation; int32 [k]."""
+    deg = np.bincount(np.concatenate([np.asarray(src, np.int64), np.asarray(dst, np.int64)]),
+                      minlength=n).astype(np.float64)
+    return rng.choice(n, size=k, replace=True, p=deg / deg.sum()).astype(np.int32)
+
+
 def partition_embeddings(rows, d: int, rng, sigma: float = 1e-3):
     """Initial N(0, sigma) embeddings for partitions of the given row counts."""
     return [init_embeddings(int(r), d, rng, sigma) for r in rows]

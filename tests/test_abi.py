@@ -18,7 +18,7 @@ def _declared():
 
 def test_header_declares_the_boundary():
     names = _declared()
-    for want in ("pbg_bucket_init", "pbg_train_bucket", "pbg_score_edges", "pbg_rank_eval",
+    for want in ("pbg_bucket_init", "pbg_train_bucket", "pbg_score_edges", "pbg_rank_eval", "pbg_rank_sampled",
                  "pbg_bucket_edges", "pbg_train_epoch", "pbg_bind_partition"):
         assert want in names
 

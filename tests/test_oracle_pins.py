@@ -553,6 +553,40 @@ def test_rank_eval_brute_force():
     assert abs(hits - np.mean(ranks <= 10)) < 1e-15
 
 
+def test_rank_sampled_hand_worked():
+    """identity + dot on 1-d embeddings x_v = v + 1: f(s, r, d) = (s + 1)(d + 1).
+    Triple (0, 1): f = 2.  Candidates [3, 2, 1, 1, 0]: destination scores
+    4, 3, 2, 2, 1, the two copies of the true destination 1 left out -> rank 3;
+    source scores f(c, 1) = 2 (c + 1) = 8, 6, 4, 4, 2, the true source 0 left
+    out, both copies of 1 counted -> rank 5."""
+    E = np.arange(1.0, 5.0).reshape(4, 1)
+    model = O.Model.create(4, 1, 1, 1, "identity", "dot", "ranking", 0.1, [E])
+    ranks, mrr, hits = O.rank_sampled(model, [0], None, [1], [3, 2, 1, 1, 0])
+    assert ranks.tolist() == [3, 5]
+    assert abs(mrr - (1 / 3 + 1 / 5) / 2) < 1e-15 and hits == 1.0
+
+
+def test_rank_sampled_invariants():
+    rng = np.random.default_rng(21)
+    n, R, d = 9, 2, 5
+    E = rng.standard_normal((n, d))
+    for op, cmp in (("translation", "cos"), ("complex_diagonal", "dot"), ("diagonal", "dot")):
+        model = O.Model.create(n, 1, R, d if op != "complex_diagonal" else 6, op, cmp, "ranking", 0.1,
+                               [E if op != "complex_diagonal" else rng.standard_normal((n, 6))],
+                               rng.standard_normal((R, d if op != "complex_diagonal" else 6)))
+        src, rel, dst = np.array([0, 4, 8]), np.array([1, 0, 1]), np.array([3, 3, 2])
+        # every entity once, nothing known: the filtered ranks without a filter
+        full, _, _ = O.rank_sampled(model, src, rel, dst, np.arange(n))
+        want, _, _ = O.rank_eval(model, src, rel, dst, [], [], [])
+        assert np.array_equal(full, want)
+        cand = rng.integers(0, n, 15)
+        r1, _, _ = O.rank_sampled(model, src, rel, dst, cand)
+        assert np.all(r1 >= 1) and np.all(r1 <= len(cand) + 1)
+        # every candidate listed twice: every count doubles
+        r2, _, _ = O.rank_sampled(model, src, rel, dst, np.concatenate([cand, cand]))
+        assert np.array_equal(r2 - 1, 2 * (r1 - 1))
+
+
 def test_rank_eval_monotone_construction():
     """identity + dot with x_v = (v + 1) e_1: f(s, r, d) = (s + 1)(d + 1), so the
     destination rank of d among unfiltered candidates is 1 + #{d' > d}."""
