@@ -1,7 +1,10 @@
-// pbg_rank_eval: filtered link-prediction ranks, MRR and Hits@10 (Sec. 5.4).
+// pbg_rank_eval: filtered link-prediction ranks, MRR and Hits@10 (Sec. 5.4);
+// pbg_rank_sampled: raw ranks against a caller-drawn candidate list (Sec. 5,
+// Freebase evaluation: candidates sampled by prevalence).
 //
 // Sequence on the compute stream: range checks of every id (nothing is
-// written on an error); the candidate tables; the known triples sorted twice
+// written on an error); the candidate tables (for a candidate list, its rows
+// gathered in list order); the known triples sorted twice
 // (by (s, r, d) for destination-side filtering, by (d, r, s) for source-side
 // filtering) with three stable radix passes each; then, per side and block of
 // queries, the queries, the score block S = Q . T^T on the matrix cores and
