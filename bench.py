@@ -46,7 +46,7 @@ def parse():
                     help="chunks of the same bucket the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true", help="skip the bf16-input leg")
-    ap.add_argument("--row", choices=["bucketing", "knowledge_graph", "big_bucket", "epoch", "tiny"],
+    ap.add_argument("--row", choices=["bucketing", "knowledge_graph", "big_bucket", "epoch", "tiny", "negatives"],
                     help="measure another row of the hot path instead of the default training step: "
                          "edge bucketing of the follower graph, the knowledge-graph pass and filtered "
                          "rank evaluation, one bucket of the large partitioned graph, the follower-graph "
@@ -635,8 +635,55 @@ def row_tiny():
                              "sample": f"full pass ({w.E} edges), fp64, {ct:.1f} s"}}
 
 
+def row_negatives():
+    """Training speed against the number of negatives per edge, batched and
+    unbatched (the comparison of Sec. 4.3 / Fig. 4), on the social-network
+    graph (translation, cos, ranking, d = 128): batched, a chunk of B/2 edges
+    is corrupted with its own entities and B/2 uniform draws (B negatives per
+    edge, scored by contractions); unbatched, every edge is its own chunk with
+    B uniform draws (chunk_size 1: one score row per edge).  40 chunks a step;
+    each point times whole steps after one warm-up call."""
+    import torch
+    from paper_1903_12287_amd import pbg, synth
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda")
+    src, dst, emb0 = synth.social_network_device(N_NODES, N_EDGES, DIM, SEED)
+    relp0 = torch.zeros(DIM, dtype=torch.float32, device=dev)
+    points = []
+    for B in (10, 50, 100, 200, 500, 1000, 2000):
+        for mode, c, u in (("batched", B // 2, B - B // 2), ("unbatched", 1, B)):
+            steps = 50 if mode == "batched" else 10
+            e_call = steps * 40 * c
+            emb = emb0.clone()
+            G = torch.zeros(N_NODES, dtype=torch.float32, device=dev)
+            relp = relp0.clone()
+            ctx = pbg.pbg_bucket_init(N_NODES, 1, 1, DIM, "translation", "cos", "ranking", MARGIN)
+            try:
+                pbg.pbg_bind_partition(ctx, 0, emb, G)
+                pbg.pbg_bind_relations(ctx, relp, torch.zeros_like(relp))
+                pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
+                run = lambda: pbg.pbg_train_bucket(ctx, 0, 0, src[:e_call], None, dst[:e_call], c, u, 40, LR, SEED)
+                run()
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                run()
+                torch.cuda.synchronize()
+                dt = time.perf_counter() - t0
+            finally:
+                pbg.pbg_free(ctx)
+            points.append({"negatives": B, "mode": mode, "chunk": c, "uniform": u, "edges": e_call,
+                           "edges_per_s": e_call / dt})
+            print(f"# {mode} B={B}: {e_call / dt:.4g} edges/s", file=sys.stderr, flush=True)
+    best = max(p["edges_per_s"] for p in points if p["mode"] == "batched" and p["negatives"] == 1000)
+    return {"metric": "trained edges/sec on 1 MI355X", "value": best, "unit": "edges/s", "dtype": "f32",
+            "config": {"workload": "social_network negatives sweep", "nodes": N_NODES, "dim": DIM,
+                       "operator": "translation", "comparator": "cos", "loss": "ranking", "chunks_per_step": 40},
+            "note": "value: batched, 1000 negatives per edge; points: every (negatives, mode)",
+            "points": points}
+
+
 ROWS = {"bucketing": row_bucketing, "knowledge_graph": row_knowledge_graph, "big_bucket": row_big_bucket,
-        "epoch": row_epoch, "tiny": row_tiny}
+        "epoch": row_epoch, "tiny": row_tiny, "negatives": row_negatives}
 
 
 if __name__ == "__main__":

@@ -72,6 +72,34 @@ def test_one_step_matches_oracle(op, cmp, loss):
         assert ok, ("relG", err)
 
 
+@pytest.mark.parametrize("op,cmp,loss,C,U", [
+    ("translation", "cos", "ranking", 1, 12),
+    ("complex_diagonal", "dot", "softmax", 1, 9),
+    ("diagonal", "dot", "logistic", 1, 1),
+    ("identity", "dot", "ranking", 2, 0),
+])
+def test_unbatched_and_minimal_chunks_match_oracle(op, cmp, loss, C, U):
+    """One-edge chunks (every edge against its own uniform draws: the
+    unbatched negatives of Sec. 4.3) and the smallest chunk_size + num_uniform
+    = 2, over several steps."""
+    pb = make_problem(op, cmp, loss, R=_R_for(op, cmp), m=37, C=C, U=U, S=8, seed=29)
+    gm = GpuModel(pb)
+    try:
+        gl = gm.train()
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol = O.train_bucket(om, pb.i, pb.j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr, pb.seed)
+    assert abs(gl - ol) <= 1e-5 * max(1.0, abs(ol)), (gl, ol)
+    for key, ref in (("G", om.G[0]), ("emb", om.emb[0])):
+        ok, err = _close(st[key][0], ref)
+        assert ok, (key, err)
+    if om.rel is not None:
+        ok, err = _close(st["rel"], om.rel)
+        assert ok, ("rel", err)
+
+
 @pytest.mark.parametrize("op,cmp,loss", COMBOS)
 def test_score_edges_matches_oracle(op, cmp, loss):
     from paper_1903_12287_amd import pbg
