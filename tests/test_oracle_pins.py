@@ -566,6 +566,23 @@ def test_rank_sampled_hand_worked():
     assert abs(mrr - (1 / 3 + 1 / 5) / 2) < 1e-15 and hits == 1.0
 
 
+def test_rank_sampled_brute_force():
+    """Each rank recounted candidate by candidate from single-edge scores."""
+    rng = np.random.default_rng(33)
+    n, R, d = 8, 3, 6
+    model = O.Model.create(n, 1, R, d, "complex_diagonal", "dot", "ranking", 0.1, [rng.standard_normal((n, d))],
+                           rng.standard_normal((R, d)))
+    src, rel, dst = np.array([1, 6, 2]), np.array([2, 0, 1]), np.array([5, 6, 0])
+    cand = np.array([0, 5, 5, 7, 1, 3, 6, 2])
+    ranks, _, _ = O.rank_sampled(model, src, rel, dst, cand)
+    for e in range(len(src)):
+        s, r, t = int(src[e]), int(rel[e]), int(dst[e])
+        pos = O.score_edges(model, 0, 0, [s], [r], [t])[0]
+        rd = 1 + sum(1 for c in cand.tolist() if c != t and O.score_edges(model, 0, 0, [s], [r], [c])[0] >= pos)
+        rs = 1 + sum(1 for c in cand.tolist() if c != s and O.score_edges(model, 0, 0, [c], [r], [t])[0] >= pos)
+        assert (ranks[e], ranks[len(src) + e]) == (rd, rs)
+
+
 def test_rank_sampled_invariants():
     rng = np.random.default_rng(21)
     n, R, d = 9, 2, 5
