@@ -631,6 +631,26 @@ struct TileS {
     }
   }
 
+  // this thread's byte offsets at k = 0 (OOB for rows past xdim): a slice
+  // that lies wholly inside k then loads at base + 4 k0, the k0 part as the
+  // scalar offset, with no per-slice address arithmetic
+  __device__ __forceinline__ static void bases(uint32_t* base, int ld, int x0, int xdim, int tid) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int f = tid + 256 * q;
+      const int gx = x0 + (f >> 2);
+      base[q] = gx < xdim ? (uint32_t)(((int64_t)gx * ld + 8 * (f & 3)) * 4) : OOB;
+    }
+  }
+
+  __device__ __forceinline__ static void load_full(v4f* r, rsrc_t rs, const uint32_t* base, int k0) {
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      r[2 * q] = __builtin_amdgcn_raw_buffer_load_b128(rs, base[q], 4 * k0, 0);
+      r[2 * q + 1] = __builtin_amdgcn_raw_buffer_load_b128(rs, base[q] + 16, 4 * k0, 0);
+    }
+  }
+
   __device__ __forceinline__ static void store(uint16_t (*s)[TX * BK], const v4f* r, int tid) {
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
@@ -696,8 +716,16 @@ __device__ __forceinline__ void score_split_body(const GemmArgsH& a, int tiles_n
   __syncthreads();
 
   const int fa0 = swz(WMR * wm + l16, g), fb0 = swz(WN * wn + l16, g);
+  uint32_t abase[TileS<BM>::LOADS], bbase[TileS<BN>::LOADS];
+  TileS<BM>::bases(abase, a.lda, t.m0, t.M, tid);
+  TileS<BN>::bases(bbase, a.ldb, t.n0, t.N, tid);
+  // slices wholly inside k (rounded up to 4, the zero-padded row length)
+  const int kfull = ((t.K + 3) & ~3) / BK;
   for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) {
+    if (kt + 1 < kfull) {
+      TileS<BM>::load_full(pa, ra, abase, (kt + 1) * BK);
+      TileS<BN>::load_full(pb, rb, bbase, (kt + 1) * BK);
+    } else if (kt + 1 < nk) {
       TileS<BM>::load(pa, ra, a.lda, t.m0, t.M, (kt + 1) * BK, t.K, tid);
       TileS<BN>::load(pb, rb, a.ldb, t.n0, t.N, (kt + 1) * BK, t.K, tid);
     }
