@@ -299,10 +299,21 @@ def chunk_scores(op, cmp, xs, xd, theta_e, rel_e, cand_dst, cand_src, theta_of):
     return p, S0, S1
 
 
-def side_loss(loss, margin, p, S, valid):
-    """Per-edge loss of one corruption side over its valid negatives."""
+def side_loss(loss, margin, p, S, valid, active=None):
+    """Per-edge loss of one corruption side over its valid negatives.
+
+    `active` (ranking only, optional) fixes which hinge terms count: term t of
+    edge e contributes (margin - p_e + n_t) * active[e, t] instead of
+    max(0, margin - p_e + n_t).  With active = [margin - p + n > 0] the two
+    agree; a caller that took the branch of a term lying within rounding
+    error of the kink in lower precision passes its own choice here, so that
+    the rest of the step can be compared exactly (either branch is within
+    that rounding error of the true loss value)."""
     if loss == "ranking":
-        return (torch.relu(margin - p.unsqueeze(1) + S) * valid).sum(1)
+        z = margin - p.unsqueeze(1) + S
+        if active is not None:
+            return (z * active * valid).sum(1)
+        return (torch.relu(z) * valid).sum(1)
     if loss == "logistic":
         k = valid.sum(1)
         neg = (_softplus(S) * valid).sum(1) / torch.clamp(k, min=1.0)
@@ -338,7 +349,8 @@ def step_negatives(model: Model, i: int, j: int, step, seed: int, U: int, first_
 
 
 def train_bucket(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, S: int,
-                 lr: float, seed: int, first_chunk: int = 0, return_steps: bool = False):
+                 lr: float, seed: int, first_chunk: int = 0, return_steps: bool = False,
+                 branches=None):
     """One pass over the edges of bucket (i, j) in the given order.
 
     Chunk c (counted from `first_chunk`) holds edges [cC, min((c+1)C, m)) of the
@@ -346,24 +358,30 @@ def train_bucket(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, S:
     summed loss is taken at the step-start parameters and then applied by
     row-wise Adagrad (entities) and element-wise Adagrad (relations).
     src/dst are local row ids in partitions i / j; rel may be None when R == 1.
+    `branches` (ranking, one step only) gives per chunk of the step the pair
+    (active dst side, active src side) of 0/1 arrays [C_c, C_c + U] that fix
+    the hinge branches (see side_loss).
     Returns the summed loss (and the per-step losses)."""
     src = np.asarray(src, dtype=np.int64)
     dst = np.asarray(dst, dtype=np.int64)
     m = src.shape[0]
     rel = np.zeros(m, dtype=np.int64) if rel is None else np.asarray(rel, dtype=np.int64)
     chunks = chunk_ranges(m, C)
+    if branches is not None and len(chunks) > S:
+        raise ValueError("hinge branches can be given for one step only")
     step_losses = []
     for s0 in range(0, len(chunks), S):
         step = chunks[s0:s0 + S]
         negs = step_negatives(model, i, j, step, seed, U, first_chunk)
-        loss, grads, rel_grad = step_loss_and_grad(model, i, j, src, rel, dst, step, negs)
+        loss, grads, rel_grad = step_loss_and_grad(model, i, j, src, rel, dst, step, negs,
+                                                   branches=branches)
         adagrad_update(model, grads, rel_grad, lr)
         step_losses.append(loss)
     total = float(sum(step_losses))
     return (total, step_losses) if return_steps else total
 
 
-def step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=True):
+def step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=True, branches=None):
     """Summed loss of one step's chunks and its exact gradient (autograd, fp64)
     with respect to every entity row and relation parameter row it touches.
 
@@ -391,7 +409,7 @@ def step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=True):
         return None if rel_leaf is None else rel_leaf[int(np.searchsorted(step_rels, r))]
 
     step_loss = 0.0
-    for (c, lo, hi), (u_dst, u_src) in zip(step, negs):
+    for k, ((c, lo, hi), (u_dst, u_src)) in enumerate(zip(step, negs)):
         Cc = hi - lo
         xs = rows(i, src[lo:hi])
         xd = rows(j, dst[lo:hi])
@@ -404,8 +422,12 @@ def step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=True):
         p, S0, S1 = chunk_scores(model.op, model.cmp, xs, xd, theta_e, r_e,
                                  cand_dst, cand_src, theta_of)
         valid = valid_mask(Cc, len(u_dst))
-        loss = (side_loss(model.loss, model.margin, p, S0, valid).sum()
-                + side_loss(model.loss, model.margin, p, S1, valid).sum())
+        act0 = act1 = None
+        if branches is not None:
+            act0 = torch.as_tensor(np.asarray(branches[k][0], dtype=np.float64))
+            act1 = torch.as_tensor(np.asarray(branches[k][1], dtype=np.float64))
+        loss = (side_loss(model.loss, model.margin, p, S0, valid, act0).sum()
+                + side_loss(model.loss, model.margin, p, S1, valid, act1).sum())
         if with_grad:
             loss.backward()          # gradients of the chunks add up in the leaves
         step_loss += float(loss.detach())
@@ -431,6 +453,51 @@ def adagrad_update(model: Model, grads, rel_grad, lr: float):
         ids, g = rel_grad
         model.relG[ids] += g * g
         model.rel[ids] -= lr * g / (np.sqrt(model.relG[ids]) + EPS_ADAGRAD)
+
+
+def inspect_step(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, seed: int,
+                 first_chunk: int = 0):
+    """The forward half of one step on these edges (all chunks of the call),
+    at the current parameters: for each chunk a dict with
+      p      (C_c,)           positive scores f(s_e, r_e, d_e)
+      S0, S1 (C_c, C_c + U)   destination- and source-side candidate scores
+      loss0, loss1 (C_c,)     each edge's loss per side (side_loss)
+      dS0, dS1 (C_c, C_c + U) dL/dS of each side with p held fixed, 0 on the
+                              excluded induced positive
+      dp     (C_c,)           dL/dp_e (both sides, scores held fixed)
+    all float64 numpy arrays."""
+    src = np.asarray(src, dtype=np.int64)
+    dst = np.asarray(dst, dtype=np.int64)
+    m = src.shape[0]
+    rel = np.zeros(m, dtype=np.int64) if rel is None else np.asarray(rel, dtype=np.int64)
+    step = chunk_ranges(m, C)
+    negs = step_negatives(model, i, j, step, seed, U, first_chunk)
+    theta_all = None if model.rel is None else torch.tensor(model.rel, dtype=_F64)
+    out = []
+    with torch.no_grad():
+        for (c, lo, hi), (u_dst, u_src) in zip(step, negs):
+            xs = torch.tensor(model.emb[i][src[lo:hi]], dtype=_F64)
+            xd = torch.tensor(model.emb[j][dst[lo:hi]], dtype=_F64)
+            cand_dst = torch.cat([xd, torch.tensor(model.emb[j][u_dst], dtype=_F64)], 0)
+            cand_src = torch.cat([xs, torch.tensor(model.emb[i][u_src], dtype=_F64)], 0)
+            r_e = rel[lo:hi]
+            theta_e = None if theta_all is None else theta_all[torch.from_numpy(r_e)]
+            p, S0, S1 = chunk_scores(model.op, model.cmp, xs, xd, theta_e, r_e, cand_dst, cand_src,
+                                     lambda r: None if theta_all is None else theta_all[r])
+            valid = valid_mask(hi - lo, U)
+            rec = {"p": p.numpy()}
+            pg = p.clone().requires_grad_(True)
+            for side, S in ((0, S0), (1, S1)):
+                Sg = S.clone().requires_grad_(True)
+                with torch.enable_grad():
+                    L = side_loss(model.loss, model.margin, pg, Sg, valid)
+                    L.sum().backward()
+                rec[f"S{side}"] = S.numpy()
+                rec[f"loss{side}"] = L.detach().numpy()
+                rec[f"dS{side}"] = Sg.grad.numpy()
+            rec["dp"] = pg.grad.numpy()
+            out.append(rec)
+    return out
 
 
 def train_epoch(model: Model, offsets, src_local, rel, dst_local, C, U, S, lr, seed):

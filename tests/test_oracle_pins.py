@@ -625,3 +625,133 @@ def test_rank_eval_monotone_construction():
     model2 = O.Model.create(n, 1, 1, 2, "identity", "dot", "ranking", 0.1, [E2])
     ranks3, _, _ = O.rank_eval(model2, src[:1], None, dst[:1], src[:1], None, dst[:1])
     assert ranks3[0] == 1 + (n - 1 - 5) + 1
+
+
+# ------------------------------------------- forward half of a step (inspection)
+def _sigmoid(v):
+    return 1.0 / (1.0 + math.exp(-v))
+
+
+@pytest.mark.parametrize("op,cmp,loss", [("identity", "dot", "ranking"), ("translation", "cos", "ranking"),
+                                         ("diagonal", "dot", "logistic"), ("complex_diagonal", "dot", "softmax"),
+                                         ("linear", "dot", "logistic"), ("linear", "cos", "softmax"),
+                                         ("translation", "dot", "softmax")])
+def test_inspect_step_pair_loops(op, cmp, loss):
+    """Scores, per-edge side losses and dL/dS of every chunk against explicit
+    per-pair Python loops and the closed forms of each loss's derivative:
+    ranking [margin - p + n > 0], logistic sigmoid(n) / K_e, softmax
+    exp(n) / (exp(p) + sum of exp over the valid negatives)."""
+    R = 1 if (cmp == "cos" and op != "identity") else 3
+    model = _tiny_model(op, cmp, loss, n=11, P=1, R=R, d=4, seed=2)
+    rng = np.random.default_rng(5)
+    m, C, U, seed = 7, 3, 2, 77
+    src, dst = rng.integers(0, 11, m), rng.integers(0, 11, m)
+    rel = rng.integers(0, R, m)
+    out = O.inspect_step(model, 0, 0, src, rel, dst, C, U, seed)
+    E = model.emb[0]
+    for k, (c, lo, hi) in enumerate(O.chunk_ranges(m, C)):
+        rec = out[k]
+        Cc = hi - lo
+        u_dst = O.uniform_negatives(seed, 0, c, 0, U, 11)
+        u_src = O.uniform_negatives(seed, 0, c, 1, U, 11)
+        cd = list(dst[lo:hi]) + list(u_dst)
+        cs = list(src[lo:hi]) + list(u_src)
+        for e in range(Cc):
+            th = [] if model.rel is None else list(model.rel[rel[lo + e]])
+            ge = _py_operator(op, list(E[src[lo + e]]), th)
+            p = _py_sim(cmp, ge, list(E[dst[lo + e]]))
+            assert abs(rec["p"][e] - p) < 1e-12
+            for side in (0, 1):
+                scores = []
+                for t in range(Cc + U):
+                    if side == 0:
+                        v = _py_sim(cmp, ge, list(E[cd[t]]))
+                    else:
+                        v = _py_sim(cmp, _py_operator(op, list(E[cs[t]]), th), list(E[dst[lo + e]]))
+                    assert abs(rec[f"S{side}"][e, t] - v) < 1e-12
+                    scores.append(v)
+                negs = [scores[t] for t in range(Cc + U) if t != e]
+                K = len(negs)
+                if loss == "ranking":
+                    want_l = sum(max(0.0, model.margin - p + v) for v in negs)
+                    want_d = [0.0 if t == e else float(model.margin - p + scores[t] > 0) for t in range(Cc + U)]
+                elif loss == "logistic":
+                    sp = lambda v: math.log1p(math.exp(v))
+                    want_l = sp(-p) + sum(sp(v) for v in negs) / K
+                    want_d = [0.0 if t == e else _sigmoid(scores[t]) / K for t in range(Cc + U)]
+                else:
+                    z = math.exp(p) + sum(math.exp(v) for v in negs)
+                    want_l = math.log(z) - p
+                    want_d = [0.0 if t == e else math.exp(scores[t]) / z for t in range(Cc + U)]
+                assert abs(rec[f"loss{side}"][e] - want_l) < 1e-12
+                assert np.allclose(rec[f"dS{side}"][e], want_d, atol=1e-14, rtol=0)
+
+
+def test_branch_override_natural_choice_is_identity():
+    """Fixing every hinge branch to the side it falls on reproduces the plain step."""
+    model = _tiny_model("diagonal", "dot", "ranking", n=11, P=1, R=2, d=4, seed=3, scale=0.6)
+    src, rel, dst = _tiny_edges(model, 0, 0, 7, 3)
+    rec = O.inspect_step(model, 0, 0, src, rel, dst, 3, 2, 9)
+    branches = [(r["dS0"] > 0, r["dS1"] > 0) for r in rec]
+    step = O.chunk_ranges(7, 3)
+    negs = O.step_negatives(model, 0, 0, step, 9, 2)
+    l0, g0, r0 = O.step_loss_and_grad(model, 0, 0, src, rel, dst, step, negs)
+    l1, g1, r1 = O.step_loss_and_grad(model, 0, 0, src, rel, dst, step, negs, branches=branches)
+    assert abs(l0 - l1) < 1e-14
+    assert np.array_equal(g0[0][0], g1[0][0]) and np.allclose(g0[0][1], g1[0][1], atol=1e-14, rtol=0)
+    assert np.allclose(r0[1], r1[1], atol=1e-14, rtol=0)
+
+
+def test_branch_override_one_flipped_pair():
+    """identity + dot, one edge (s, d) and one destination-side uniform
+    negative d' whose hinge is inactive: forcing it active adds the pair's
+    closed-form gradient (x_d' - x_d to s, -x_s to d, x_s to d') and its
+    value lambda - <s,d> + <s,d'> to the loss."""
+    n, d = 8, 3
+    for seed in range(1000):
+        u_dst = int(O.uniform_negatives(seed, 0, 0, 0, 1, n)[0])
+        u_src = int(O.uniform_negatives(seed, 0, 0, 1, 1, n)[0])
+        if len({0, 1, u_dst, u_src}) == 4:
+            break
+    E = np.zeros((n, d))
+    E[0] = [1.0, 0.5, 0.0]
+    E[1] = [0.2, 0.1, 0.0]
+    E[u_dst] = [-0.3, 0.2, 0.4]   # 0.1 - 0.25 - 0.2 < 0: inactive
+    E[u_src] = [-5.0, 0.0, 1.0]
+    model = O.Model.create(n, 1, 1, d, "identity", "dot", "ranking", 0.1, [E])
+    step = O.chunk_ranges(1, 1)
+    negs = O.step_negatives(model, 0, 0, step, seed, 1)
+    args = (model, 0, 0, np.array([0]), np.array([0]), np.array([1]), step, negs)
+    l0, g0, _ = O.step_loss_and_grad(*args)
+    flip = [(np.array([[0.0, 1.0]]), np.array([[0.0, 0.0]]))]
+    l1, g1, _ = O.step_loss_and_grad(*args, branches=flip)
+    assert l0 == 0.0 and abs(l1 - (0.1 - 0.25 - 0.2)) < 1e-15
+    ids = [int(r) for r in g0[0][0]]
+    diff = {r: g1[0][1][k] - g0[0][1][k] for k, r in enumerate(ids)}
+    assert np.allclose(diff[0], E[u_dst] - E[1], atol=1e-15)
+    assert np.allclose(diff[1], -E[0], atol=1e-15)
+    assert np.allclose(diff[u_dst], E[0], atol=1e-15)
+    assert np.allclose(diff[u_src], 0.0, atol=0)
+
+
+def test_inspect_step_positive_gradient_closed_form():
+    """dL/dp of each edge: ranking -(number of active hinges on both sides),
+    logistic 2 (sigmoid(p) - 1), softmax sum over sides of (softmax_p - 1)."""
+    for loss in O.LOSSES:
+        model = _tiny_model("diagonal", "dot", loss, n=11, P=1, R=2, d=4, seed=4, scale=0.7)
+        src, rel, dst = _tiny_edges(model, 0, 0, 5, 4)
+        for rec in O.inspect_step(model, 0, 0, src, rel, dst, 5, 3, 21):
+            p = rec["p"]
+            for e in range(p.shape[0]):
+                if loss == "ranking":
+                    want = -float((rec["dS0"][e] > 0).sum() + (rec["dS1"][e] > 0).sum())
+                elif loss == "logistic":
+                    want = 2.0 * (_sigmoid(p[e]) - 1.0)
+                else:
+                    want = 0.0
+                    for side in (0, 1):
+                        S = rec[f"S{side}"][e]
+                        vals = [p[e]] + [S[t] for t in range(S.shape[0]) if t != e]
+                        z = sum(math.exp(v) for v in vals)
+                        want += math.exp(p[e]) / z - 1.0
+                assert abs(rec["dp"][e] - want) < 1e-12
