@@ -74,9 +74,10 @@ enum {
    * stream and report the summed times in pbg_stats (each event adds a few
    * microseconds to a step). */
   PBG_F_PHASE_TIMING = 2u,
-  /* Record HIP events around the score contraction of every eighth step only
+  /* Record HIP events around the score contraction of every second step only
    * (score_ms and score_timed_steps in pbg_stats); PBG_F_PHASE_TIMING times
-   * it on every step. */
+   * it on every step.  With bf16 score inputs the bracket holds the score
+   * contraction alone, not the rounding of its operands. */
   PBG_F_SCORE_TIMING = 4u
 };
 
@@ -131,12 +132,16 @@ typedef struct {
  * Returns INVALID_ARG for unknown enums, dim < 1 or dim > 512, odd dim with
  * COMPLEX_DIAGONAL, P < 1, a partition left empty, num_relations < 1 or a
  * non-finite margin; UNSUPPORTED for COS with a non-identity operator and more
- * than one relation, and for LINEAR with more than one relation or with COS. */
+ * than one relation (the source corruptions of an edge would need the
+ * operator of its own relation applied to every candidate before the
+ * normalisation, which is no longer one product per chunk). */
 pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_partitions,
                            int32_t num_relations, int32_t dim, int32_t op, int32_t cmp,
                            int32_t loss, float margin, uint32_t flags);
 
-/* Releases the context and its workspace (NULL is allowed). */
+/* Releases the context and its workspace (NULL is allowed).  Buffers bound
+ * with pbg_bind_partition / pbg_bind_relations belong to the caller and may
+ * be freed after this call (not before). */
 void pbg_free(pbg_ctx* ctx);
 
 /* Message of the last failed call on ctx ("" if none; a static message when
@@ -165,12 +170,20 @@ pbg_status pbg_bucket_edges(pbg_ctx* ctx, const int64_t* src, const int32_t* rel
  * accumulator adagrad [rows(p)] float32 (one value per row, Sec. 3.1).  where
  * is PBG_MEM_DEVICE (device memory) or PBG_MEM_PINNED_HOST (page-locked host
  * memory, for pbg_train_epoch, which swaps partitions through HBM slots).
- * Initial values are the caller's; the library updates them in place. */
+ * Initial values are the caller's; the library updates them in place.
+ * Lifetime: the library keeps the two pointers, not copies of the data.  Both
+ * buffers must stay allocated until the partition is bound again or the
+ * context is released with pbg_free; freeing one earlier and then calling
+ * any training, scoring or ranking entry point is undefined (the kernels
+ * would read and write freed device memory).  Rebinding is allowed between
+ * calls (every call is synchronous on return). */
 pbg_status pbg_bind_partition(pbg_ctx* ctx, int32_t p, float* emb, float* adagrad, int32_t where);
 
 /* Binds the relation parameters (device, [R x width] float32, width as in
  * pbg_relation_param_floats / R) and their element-wise Adagrad accumulators
- * (same shape).  Not needed (and ignored) for IDENTITY. */
+ * (same shape).  Not needed (and ignored) for IDENTITY.  Lifetime as for
+ * pbg_bind_partition: both buffers must stay allocated until they are bound
+ * again or pbg_free. */
 pbg_status pbg_bind_relations(pbg_ctx* ctx, float* params, float* adagrad);
 
 /* Streams (hipStream_t) for compute and for partition transfers.  NULL means
@@ -256,6 +269,33 @@ pbg_status pbg_rank_sampled(pbg_ctx* ctx, const int32_t* src, const int32_t* rel
  * Produced by the same device code as training; for inspection and tests. */
 pbg_status pbg_sample_negatives(pbg_ctx* ctx, int32_t i, int32_t j, int64_t first_chunk,
                                 int64_t n_chunks, int32_t num_uniform, uint64_t seed, int32_t* out);
+
+/* Inspection of one step (for tests and diagnostics): runs the forward half
+ * of a training step on the n_edges <= chunk_size * chunks_per_step edges of
+ * bucket (i, j) -- gather, relation operator, uniform draws of chunks
+ * neg->first_chunk onwards, the chunk score contraction with its loss
+ * epilogue and the per-edge finalisation (Sec. 3.1 score f and losses,
+ * Sec. 4.3 batched negatives) -- with the same kernels and launch sequence as
+ * pbg_train_bucket, then copies out what they computed.  No parameter or
+ * accumulator is modified; arguments and ids are checked as for
+ * pbg_train_bucket.  With nch = ceil(n_edges / chunk_size), N = chunk_size +
+ * num_uniform, Cc the edges of chunk c and candidates t = the chunk's Cc
+ * in-chunk entities followed by its num_uniform draws, every output is a
+ * nullable device float32 array whose entries outside [Cc] x [Cc + U] are 0:
+ *   scores    [nch][2][chunk_size][N]: side 0 f(s_e, r_e, candidate t of the
+ *             destination side), side 1 f(candidate t of the source side,
+ *             r_e, d_e), from the score contraction's main loop over the same
+ *             operands with a plain store epilogue (so the values the loss
+ *             epilogue saw, up to the bias it adds the same way);
+ *   dscores   [nch][2][chunk_size][N]: dL/dS as the epilogue left it (0 on the
+ *             excluded induced positive);
+ *   row_loss  [nch][2][chunk_size]: each edge's loss on each side;
+ *   pos       [nch][chunk_size]: the positive scores p_e.
+ * loss_host (nullable) receives the summed loss of the step. */
+pbg_status pbg_inspect_step(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
+                            const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
+                            const pbg_neg_config* neg, uint64_t seed, float* scores, float* dscores,
+                            float* row_loss, float* pos, double* loss_host);
 
 /* Timings and algorithmic work of the last training call. */
 pbg_status pbg_get_stats(const pbg_ctx* ctx, pbg_stats* out_host);

@@ -23,11 +23,11 @@
 enum { OP_IDENTITY = 0, OP_TRANSLATION = 1, OP_DIAGONAL = 2, OP_LINEAR = 3, OP_COMPLEX = 4 };
 enum { CMP_DOT = 0, CMP_COS = 1 };
 
-// With the cos comparator (never with the linear operator) the packed Q and
-// K rows of a chunk equal its first C source and destination candidate rows
-// (g(x_s) and x_d, both normalised), so Q / K row e of side s is read from
-// row e of the candidate tile of side 1 - s and never written separately.
-#define QK_IN_NN(g) ((g).cmp == CMP_COS && (g).op != OP_LINEAR)
+// With the cos comparator the packed Q and K rows of a chunk equal its first
+// C source and destination candidate rows (g(x_s) and x_d, both normalised),
+// so Q / K row e of side s is read from row e of the candidate tile of side
+// 1 - s and never written separately.
+#define QK_IN_NN(g) ((g).cmp == CMP_COS)
 enum { LOSS_RANKING = 0, LOSS_LOGISTIC = 1, LOSS_SOFTMAX = 2 };
 
 #define PBG_EPS_NORM 1e-12f
@@ -80,6 +80,7 @@ struct StepBufs {
   float* rowpart;       // [S][2][C][nct][2]  per score tile: (loss, dS sum) or, for
                         // softmax, (tile max, sum exp(s - tile max))
   float* rowscale;      // [S][2][nct][C]  softmax on split pieces: exp(tile max - lse)
+  float* rowloss;       // [S][2][C] each edge's loss per side (inspection only; NULL in training)
   float* dpos;          // [S][C] dL/dp
   float* dsum1;         // [S][C] sum_t dS1[e][t]
   double* chunkloss;    // [S][FIN_BLOCKS(C)]  loss partials of the finalisation
@@ -88,6 +89,8 @@ struct StepBufs {
   float* dq;
   float* dn;
   float* relc;          // [S][N][dr] relation gradient contributions
+  float* lin_x;         // linear + cos: [S][N][dp] raw source candidate rows x_t
+  float* lin_v;         // linear + cos: [S][N][dp] dL/d(A x_t) of the source candidates
   uint32_t* keys;       // [S*2N] sort keys of the contribution rows
   uint32_t* vals;       // [S*2N] contribution row index
   uint32_t* rkeys;      // [S*C]  relation ids of the edges (R > 1)

@@ -70,7 +70,7 @@ struct GemmArgsH {
 };
 
 // bf16-input score contraction with a loss epilogue (EPI_LOSS, EPI_LOSS_BITS or
-// EPI_SOFTMAX_STATS)
+// EPI_SOFTMAX_STATS) or the plain store (EPI_STORE: float32 scores to Cm)
 void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s);
 // float32 score contraction with its loss epilogue (EPI_LOSS: float32 dS in
 // Cm; EPI_LOSS_BITS; EPI_SOFTMAX_STATS) on the bf16 instructions, operands
@@ -114,6 +114,17 @@ void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s
 // scores once Q has been formed by contraction
 void launch_pad_linear(const float* A, int d, int dp, float* Ap, float* ATp, hipStream_t s);
 void launch_positive_scores(const StepGeom& g, const StepBufs& b, hipStream_t s);
+// linear operator with several relations (dot): Q = A_r x, K = A_r^T y and p
+// per edge; the rows' operator backward; the sorted per-relation gradient
+// sums with element-wise Adagrad (keys / vals: sorted relation ids and
+// chunk * N + edge)
+void launch_linear_rows(const StepGeom& g, const StepBufs& b, hipStream_t s);
+void launch_linear_rows_backward(const StepGeom& g, const StepBufs& b, hipStream_t s);
+void launch_linear_relation_update(const StepGeom& g, const StepBufs& b, const uint32_t* keys,
+                                   const uint32_t* vals, int n, float lr, hipStream_t s);
+// linear operator with cos: normalise the source candidates A x_t in place
+// (norms to nrm) and form the positive scores
+void launch_normalize_candidates(const StepGeom& g, const StepBufs& b, hipStream_t s);
 
 // ---- loss finalisation and backward -----------------------------------------
 void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* dsh, int ldh, hipStream_t s);
@@ -228,3 +239,12 @@ void launch_score_edges(const StepGeom& g, const float* emb_i, const float* emb_
                         const int32_t* dst, int64_t n, float* out, hipStream_t s);
 void launch_sample_negatives(uint64_t seed, uint32_t bucket, int64_t chunk0, int64_t n_chunks, int U,
                              uint32_t rows_j, uint32_t rows_i, int32_t* out, hipStream_t s);
+
+// ---- inspection of a step's forward half ----------------------------------------
+enum { DS_BITS = 0, DS_F32 = 1, DS_F32_SCALED = 2, DS_BF16 = 3 };
+// out [c][2][C][N] of the source side (side 1) += the per-edge translation bias
+void launch_add_side_bias(const StepGeom& g, const float* bias, float* out, hipStream_t s);
+// dL/dS as float32 [c][2][C][N] from the layout `mode` (DS_*) the loss left it in
+void launch_expand_ds(const StepGeom& g, int mode, const uint16_t* bits, int nw, int ldw, const float* f32,
+                      const float* scale, const uint16_t* h, int ld, float* out, hipStream_t s);
+void launch_copy_pos(const StepGeom& g, const float* pos, float* out, hipStream_t s);

@@ -39,14 +39,20 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
     }
     double loss;
     float dp, dsum1;
+    float side_loss[2];
     if (g.loss == LOSS_RANKING) {
       loss = (double)l0 + (double)l1;
       dp = -(d0 + d1);
       dsum1 = d1;
+      side_loss[0] = l0;
+      side_loss[1] = l1;
     } else if (g.loss == LOSS_LOGISTIC) {
-      loss = (double)l0 + (double)l1 + 2.0 * (double)softplusf(-p);
+      const float sp = softplusf(-p);
+      loss = (double)l0 + (double)l1 + 2.0 * (double)sp;
       dp = 2.0f * (sigmoidf(p) - 1.0f);
       dsum1 = d1;
+      side_loss[0] = l0 + sp;
+      side_loss[1] = l1 + sp;
     } else {
       // log-sum-exp of each side's row over {p} and its valid candidates, from
       // the per-tile (max M, sum exp(s - M)) partials; each tile's sum is then
@@ -76,6 +82,12 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
       const float s0 = expf(p - lse0), s1 = expf(p - lse1);
       dp = (s0 - 1.0f) + (s1 - 1.0f);
       dsum1 = 1.0f - s1;
+      side_loss[0] = lse0 - p;
+      side_loss[1] = lse1 - p;
+    }
+    if (b.rowloss) {
+      b.rowloss[(int64_t)(c * 2 + 0) * g.C + e] = side_loss[0];
+      b.rowloss[(int64_t)(c * 2 + 1) * g.C + e] = side_loss[1];
     }
     b.dpos[ce] = dp;
     b.dsum1[ce] = dsum1;
@@ -197,8 +209,8 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
       Row dYh = gn0;                                 // x^_d is destination candidate e and K^_e
       row_add(dYh, gq1);
       row_axpy(dYh, dpe, Q);
-      const Row dv = normalize_backward(Q, nq, dQh); // dL/dg(x_s)   (cos: never linear)
-      gs = op_adjoint(g.op, dv, th);
+      const Row dv = normalize_backward(Q, nq, dQh); // dL/dg(x_s)
+      gs = op_adjoint(g.op, dv, th);                 // linear: dv itself (A^T dv follows)
       gd = normalize_backward(Kv, ny, dYh);
       if (g.op == OP_TRANSLATION) {
         grel = dv;
@@ -209,7 +221,10 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
       }
     }
     row_store(gd, dn0, d, dp, cplx, lane);
-    row_store(gs, dn1, d, dp, cplx, lane);
+    // linear + cos: dL/d(A x_s) goes to lin_v, and the source row gradient
+    // A^T dv is formed by a contraction over the step's source candidates
+    float* srow = (cos && g.op == OP_LINEAR) ? b.lin_v + ((int64_t)c * g.N + e) * dp : dn1;
+    row_store(gs, srow, d, dp, cplx, lane);
     if (has_rel && g.op != OP_LINEAR)
       row_store(grel, b.relc + ((int64_t)c * g.N + e) * g.dr, d, g.dr, cplx, lane);
     return;
@@ -244,7 +259,10 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
       }
     }
     Row th;
-    const bool op_side = side == 1 && has_rel;   // the single relation's operator was applied here
+    // the single relation's operator was applied here (linear: A^T dv follows
+    // as a contraction, the gradient of A too)
+    const bool lin_side = side == 1 && g.op == OP_LINEAR;
+    const bool op_side = side == 1 && has_rel && !lin_side;
     if (op_side) row_load(th, b.relp, d, cplx, lane);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -260,7 +278,8 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
         row_store(grel, b.relc + ((int64_t)c * g.N + g.C + k0 + q) * g.dr, d, g.dr, cplx, lane);
         dv = op_adjoint(g.op, dv, th);
       }
-      row_store(dv, b.dn + (rbase + q) * dp, d, dp, cplx, lane);
+      float* drow = lin_side ? b.lin_v + ((int64_t)c * g.N + Cc + k0 + q) * dp : b.dn + (rbase + q) * dp;
+      row_store(dv, drow, d, dp, cplx, lane);
     }
   }
 }

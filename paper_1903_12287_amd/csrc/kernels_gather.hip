@@ -45,8 +45,21 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     float* n0row = b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
     float* n1row = b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
     if (g.op == OP_LINEAR) {
-      // one relation: Q = X A^T and K = Y A are formed afterwards as
-      // contractions over the whole step, from these raw rows
+      if (g.cmp == CMP_COS) {
+        // one relation: the source candidates A x_t are formed afterwards by
+        // a contraction over the step's raw source rows, then normalised;
+        // the destination row is normalised here
+        const float ny = row_normalize(y);
+        row_store(y, n0row, d, dp, cplx, lane);
+        row_store(x, b.lin_x + ((int64_t)c * g.N + e) * dp, d, dp, cplx, lane);
+        if (lane == 0) {
+          b.bias[(int64_t)c * g.C + e] = 0.0f;
+          b.nrm[(int64_t)(c * 2 + 0) * g.N + e] = ny;
+        }
+        return;
+      }
+      // dot: Q = A x and K = A^T y are formed afterwards from these raw rows
+      // (one relation: as contractions over the whole step; several: per edge)
       row_store(y, n0row, d, dp, cplx, lane);
       row_store(x, n1row, d, dp, cplx, lane);
       if (lane == 0) b.bias[(int64_t)c * g.C + e] = 0.0f;
@@ -102,9 +115,12 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     else row_zero(v[q]);
   }
   float nv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  if (g.cmp == CMP_COS) {
+  // linear + cos: the raw source candidates go to lin_x (A x and its norm follow)
+  const bool raw_linear = g.op == OP_LINEAR && g.cmp == CMP_COS && side == 1;
+  const bool unit = g.cmp == CMP_COS && !raw_linear;
+  if (unit) {
     if (side == 1 && g.op != OP_IDENTITY) {
-      // one relation (not linear): its operator is applied to every source candidate
+      // one relation: its operator is applied to every source candidate
       Row th;
       row_load(th, b.relp, d, cplx, lane);
 #pragma unroll
@@ -118,10 +134,12 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     const int k = k0 + q;
     if (k >= g.U) break;
     const int t = Cc + k;
-    row_store(v[q], b.nn + ((int64_t)(c * 2 + side) * g.N + t) * dp, d, dp, cplx, lane);
+    float* dstrow = raw_linear ? b.lin_x + ((int64_t)c * g.N + t) * dp
+                               : b.nn + ((int64_t)(c * 2 + side) * g.N + t) * dp;
+    row_store(v[q], dstrow, d, dp, cplx, lane);
     if (lane == 0) {
       b.neg[(int64_t)(c * 2 + side) * g.U + k] = u[q];
-      if (g.cmp == CMP_COS) b.nrm[(int64_t)(c * 2 + side) * g.N + t] = nv[q];
+      if (unit) b.nrm[(int64_t)(c * 2 + side) * g.N + t] = nv[q];
     }
   }
 }

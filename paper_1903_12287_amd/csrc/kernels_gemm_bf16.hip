@@ -1301,7 +1301,8 @@ void launch_gemm_bf16(const GemmArgsH& a, int epi, int batches, hipStream_t s) {
   const int tiles_n = (maxN + 127) / 128;   // = nct (PBG_SCORE_BN columns per tile)
   if (epi == EPI_LOSS) launch_t<128, GA_KC, EPI_LOSS>(a, tiles_n, tiles_m, batches, s);
   else if (epi == EPI_LOSS_BITS) launch_t<128, GA_KC, EPI_LOSS_BITS>(a, tiles_n, tiles_m, batches, s);
-  else launch_t<128, GA_KC, EPI_SOFTMAX_STATS>(a, tiles_n, tiles_m, batches, s);
+  else if (epi == EPI_SOFTMAX_STATS) launch_t<128, GA_KC, EPI_SOFTMAX_STATS>(a, tiles_n, tiles_m, batches, s);
+  else launch_t<128, GA_KC, EPI_STORE>(a, tiles_n, tiles_m, batches, s);
 }
 
 namespace {

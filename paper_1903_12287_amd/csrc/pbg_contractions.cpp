@@ -71,10 +71,11 @@ static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t*
   launch_gemm_bf16_pair(qa, na, nch * 2, cs);
 }
 
-void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
-                          const std::function<void(int)>& mark) {
-  const int C = g.C, U = g.U, N = g.N, dp = g.dp, Np = g.Np, nch = g.nchunks;
-
+// Arguments of the float32 score contraction of a step with its loss
+// epilogue (operands, dS and row-partial outputs); *epi receives the epilogue
+// the loss takes
+static GemmArgsH score_args_f32(const StepGeom& g, const StepBufs& b, int* epi_out) {
+  const int C = g.C, U = g.U, N = g.N, dp = g.dp, Np = g.Np;
   // ranking: dS is 0 or 1 and travels as bits, 16 columns per word
   const bool bits = g.loss == LOSS_RANKING;
   GemmArgsH fa;
@@ -122,6 +123,16 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
     fa.ldcb = ldw;
     fa.nwcb = nw;
   }
+  *epi_out = epi;
+  return fa;
+}
+
+void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
+                          const std::function<void(int)>& mark, bool forward_only) {
+  const int C = g.C, U = g.U, N = g.N, dp = g.dp, Np = g.Np, nch = g.nchunks;
+  const bool bits = g.loss == LOSS_RANKING;
+  int epi = EPI_LOSS;
+  const GemmArgsH fa = score_args_f32(g, b, &epi);
   launch_score_split(fa, epi, nch * 2, cs);
   mark(2);
   // softmax: the score pass leaves exp(s - tile max), the finalisation each
@@ -129,6 +140,7 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   // stages the exponentials
   launch_finalize(g, b, ctx->steploss_dev + t, g.loss == LOSS_SOFTMAX, cs);
   mark(3);
+  if (forward_only) return;
 
   // Q and N in three exact bf16 pieces each, transposed (the B operands of
   // both backward products).  On the second stream beside the score
@@ -199,20 +211,13 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   launch_gemm_split_pair(qa, na, nch * 2, cs);
 }
 
-void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t,
-                           hipStream_t cs, const std::function<void(int)>& mark) {
-  const int C = g.C, U = g.U, N = g.N, d = g.d, dp = g.dp, Np = g.Np, nch = g.nchunks;
-  const int dpb = rup(d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
+// Operands of the bf16-input score contraction of a step (the rounded copies
+// of Q and N) and its epilogue's per-row inputs
+static GemmArgsH score_args_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b) {
+  const int C = g.C, U = g.U, N = g.N, d = g.d;
+  const int dpb = rup(d, 32);
   const BufsH& h = ctx->h;
-  // bf16 operands: rows [e][f], [t][f] and the transposed copies [f][e], [f][t]
-  // with QK_IN_NN, the Q rows of side s are the first C rows of N of side
-  // 1 - s (and Q^T the first C columns of N^T): only N is converted
   const bool qn = QK_IN_NN(g);
-  launch_to_bf16_t(qn ? nullptr : b.qk, (int64_t)C * dp, C, h.qk, (int64_t)C * dpb, h.qkT, (int64_t)dpb * Cpb, Cpb, b.nn,
-                   (int64_t)N * dp, N, h.nn, (int64_t)N * dpb, h.nnT, (int64_t)dpb * Npb, Npb, dp, dpb, nch * 2, cs);
-
-  const bool bits = g.loss == LOSS_RANKING;
-  const int nw = (Np + 15) / 16, ldw = rup(C, 8);
   GemmArgsH fa;
   memset(&fa, 0, sizeof(fa));
   fa.B = h.nn;
@@ -244,6 +249,25 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   fa.nct = g.nct;
   fa.loss = g.loss;
   fa.margin = g.margin;
+  return fa;
+}
+
+void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t,
+                           hipStream_t cs, const std::function<void(int)>& mark, bool forward_only) {
+  const int C = g.C, U = g.U, N = g.N, d = g.d, dp = g.dp, Np = g.Np, nch = g.nchunks;
+  const int dpb = rup(d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
+  const BufsH& h = ctx->h;
+  // bf16 operands: rows [e][f], [t][f] and the transposed copies [f][e], [f][t]
+  // with QK_IN_NN, the Q rows of side s are the first C rows of N of side
+  // 1 - s (and Q^T the first C columns of N^T): only N is converted
+  const bool qn = QK_IN_NN(g);
+  launch_to_bf16_t(qn ? nullptr : b.qk, (int64_t)C * dp, C, h.qk, (int64_t)C * dpb, h.qkT, (int64_t)dpb * Cpb, Cpb, b.nn,
+                   (int64_t)N * dp, N, h.nn, (int64_t)N * dpb, h.nnT, (int64_t)dpb * Npb, Npb, dp, dpb, nch * 2, cs);
+  mark(1);   // recorded again: the score bracket starts after the operand rounding
+
+  const bool bits = g.loss == LOSS_RANKING;
+  const int nw = (Np + 15) / 16, ldw = rup(C, 8);
+  GemmArgsH fa = score_args_bf16(ctx, g, b);
   if (bits) {
     fa.dsb = b.dsb;
     fa.cb_cs = 2ll * nw * ldw;
@@ -270,6 +294,7 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
   }
   launch_finalize(g, b, ctx->steploss_dev + t, false, cs);
   mark(3);
+  if (forward_only) return;
 
   if (qn)
     run_backward_h(g, b, h.ds, h.nnT, 0, h.nnT + (int64_t)dpb * Npb, 0, 2ll * dpb * Npb, -(int64_t)dpb * Npb, Npb,
@@ -309,6 +334,15 @@ static GemmArgs linear_args(const StepGeom& g, const float* A, int64_t a_cs, con
 
 void run_linear_forward(const StepGeom& g, const StepBufs& b, const float* Ap, const float* ATp, hipStream_t cs) {
   const int64_t n_cs = 2ll * g.N * g.dp, q_cs = 2ll * g.C * g.dp;
+  if (g.cmp == CMP_COS) {
+    // A x_t for every source candidate (raw rows in lin_x) into the candidate
+    // tile of side 1, then normalised, with the positive scores
+    GemmArgs q = linear_args(g, b.lin_x, (int64_t)g.N * g.dp, Ap, b.nn + (int64_t)g.N * g.dp, n_cs);
+    q.mdim = DIM_NC;
+    launch_gemm_f32(q, GEMM_NT, g.nchunks, cs);
+    launch_normalize_candidates(g, b, cs);
+    return;
+  }
   GemmArgs q = linear_args(g, b.nn + (int64_t)g.N * g.dp, n_cs, Ap, b.qk, q_cs);     // Q = X A^T
   launch_gemm_f32(q, GEMM_NT, g.nchunks, cs);
   GemmArgs k = linear_args(g, b.nn, n_cs, ATp, b.qk + (int64_t)g.C * g.dp, q_cs);    // K = Y A
@@ -316,16 +350,94 @@ void run_linear_forward(const StepGeom& g, const StepBufs& b, const float* Ap, c
   launch_positive_scores(g, b, cs);
 }
 
-// the operator's part of the row gradients: source rows += dQ A (i.e. A^T dQ),
-// destination rows += dK A^T (i.e. A dK), added to the contributions that the
-// operator backward left in the candidate-gradient buffer
+// the operator's part of the row gradients.  dot: source rows += dQ A (i.e.
+// A^T dQ), destination rows += dK A^T (i.e. A dK), added to the
+// contributions that the operator backward left in the candidate-gradient
+// buffer.  cos: every source candidate row's gradient is A^T dv, dv the
+// gradient of its A x_t that the operator backward left in lin_v
 void run_linear_backward(const StepGeom& g, const StepBufs& b, const float* Ap, const float* ATp,
                          hipStream_t cs) {
   const int64_t n_cs = 2ll * g.N * g.dp, q_cs = 2ll * g.C * g.dp;
+  if (g.cmp == CMP_COS) {
+    GemmArgs s = linear_args(g, b.lin_v, (int64_t)g.N * g.dp, ATp, b.dn + (int64_t)g.N * g.dp, n_cs);
+    s.mdim = DIM_NC;
+    launch_gemm_f32(s, GEMM_NT, g.nchunks, cs);
+    return;
+  }
   GemmArgs s = linear_args(g, b.dq, q_cs, ATp, b.dn + (int64_t)g.N * g.dp, n_cs);
   s.accumulate = 1;
   launch_gemm_f32(s, GEMM_NT, g.nchunks, cs);
   GemmArgs d = linear_args(g, b.dq + (int64_t)g.C * g.dp, q_cs, Ap, b.dn, n_cs);
   d.accumulate = 1;
   launch_gemm_f32(d, GEMM_NT, g.nchunks, cs);
+}
+
+// Gradient of the single relation matrix, one d x d partial per product and
+// chunk into `partial`; returns the number of partials.  dot: dA = dQ^T X +
+// Y^T dK over the chunk's edges; cos: dA = V^T X over its source candidates.
+int run_linear_relation_grad(const StepGeom& g, const StepBufs& b, float* partial, hipStream_t cs) {
+  const int d = g.d, dp = g.dp, C = g.C, N = g.N;
+  GemmArgs la;
+  memset(&la, 0, sizeof(la));
+  la.lda = dp;
+  la.ldb = dp;
+  la.ldc = d;
+  la.mdim = DIM_FIXED;
+  la.Mfix = d;
+  la.ndim = DIM_FIXED;
+  la.Nfix = d;
+  la.C = C;
+  la.U = g.U;
+  la.m_step = g.m_step;
+  la.nsides = 1;
+  la.Cm = partial;
+  if (g.cmp == CMP_COS) {
+    la.A = b.lin_v;                    // V^T: (m = row of A, k = candidate)
+    la.B = b.lin_x;                    // raw source candidates x_t
+    la.a_cs = (int64_t)N * dp;
+    la.b_cs = (int64_t)N * dp;
+    la.c_cs = (int64_t)d * d;
+    la.kdim = DIM_NC;
+    launch_gemm_f32(la, GEMM_TN, g.nchunks, cs);
+    return g.nchunks;
+  }
+  la.A = b.dq;                         // dQ^T: (m = row of A, k = edge)
+  la.B = b.nn + (int64_t)N * dp;       // source rows x_s (N1[e])
+  la.a_cs = 2ll * C * dp;
+  la.b_cs = 2ll * N * dp;
+  la.c_cs = 2ll * d * d;
+  la.kdim = DIM_CC;
+  launch_gemm_f32(la, GEMM_TN, g.nchunks, cs);
+  GemmArgs lb = la;
+  lb.A = b.nn;                         // destination rows x_d (N0[e])
+  lb.B = b.dq + (int64_t)C * dp;       // dK
+  lb.Cm = partial + (int64_t)d * d;
+  lb.a_cs = 2ll * N * dp;
+  lb.b_cs = 2ll * C * dp;
+  launch_gemm_f32(lb, GEMM_TN, g.nchunks, cs);
+  return 2 * g.nchunks;
+}
+
+// The score contraction of a step again, with the plain store epilogue, into
+// out [nchunks][2][C][C+U] (row pitch C+U): the same operands and main loop as
+// the loss epilogue's launch, so the same float32 values.  The translation
+// bias of the source side (translation with dot) is added afterwards, as the
+// epilogues add it.
+void run_score_store(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, float* out, hipStream_t cs) {
+  GemmArgsH fa;
+  if (ctx->flags & PBG_F_BF16_SCORE) {
+    fa = score_args_bf16(ctx, g, b);
+  } else {
+    int epi = EPI_LOSS;
+    fa = score_args_f32(g, b, &epi);
+  }
+  fa.Cm = out;
+  fa.dsh = nullptr;
+  fa.dsb = nullptr;
+  fa.c_cs = 2ll * g.C * g.N;
+  fa.c_ss = (int64_t)g.C * g.N;
+  fa.ldc = g.N;
+  if (ctx->flags & PBG_F_BF16_SCORE) launch_gemm_bf16(fa, EPI_STORE, g.nchunks * 2, cs);
+  else launch_score_split(fa, EPI_STORE, g.nchunks * 2, cs);
+  if (g.op == OP_TRANSLATION && g.cmp == CMP_DOT) launch_add_side_bias(g, b.bias, out, cs);
 }

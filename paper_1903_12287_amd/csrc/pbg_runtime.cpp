@@ -77,7 +77,7 @@ bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width) {
   return !a.failed;
 }
 
-static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
+pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   if (ctx->ws_ready && ctx->wC == C && ctx->wU == U && ctx->wS == S) return PBG_OK;
   (void)hipStreamSynchronize(ctx->cs);
   ctx->ws.release();
@@ -134,6 +134,10 @@ static pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   if (linear) {
     ctx->relA = (float*)a.get((int64_t)d * dp * 4);
     ctx->relAT = (float*)a.get((int64_t)d * dp * 4);
+    if (ctx->cmp == PBG_CMP_COS) {
+      b.lin_x = (float*)a.get(s * N * dp * 4);
+      b.lin_v = (float*)a.get(s * N * dp * 4);
+    }
   }
   ctx->flag_dev = (uint32_t*)a.get(16);
   ctx->h = BufsH();
@@ -213,7 +217,7 @@ static bool ensure_events(pbg_ctx* ctx, size_t n) {
   return true;
 }
 
-static pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps) {
+pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps) {
   if (ctx->steploss_cap >= nsteps && ctx->steploss_dev) return PBG_OK;
   if (ctx->steploss_dev) (void)hipFree(ctx->steploss_dev);
   ctx->steploss_dev = nullptr;
@@ -263,8 +267,6 @@ pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_part
   if (ps > (1ll << 30)) return fail(PBG_ERR_INVALID_ARG, "partitions above 2^30 rows are not supported");
   if (cmp == PBG_CMP_COS && op != PBG_OP_IDENTITY && num_relations > 1)
     return fail(PBG_ERR_UNSUPPORTED, "cos with a non-identity operator needs a single relation");
-  if (op == PBG_OP_LINEAR && (num_relations > 1 || cmp == PBG_CMP_COS))
-    return fail(PBG_ERR_UNSUPPORTED, "the linear operator is implemented for one relation with dot");
   ctx->n = num_entities;
   ctx->P = num_partitions;
   ctx->R = num_relations;
@@ -390,25 +392,10 @@ pbg_status check_neg_config(pbg_ctx* ctx, const pbg_neg_config* neg) {
   return PBG_OK;
 }
 
-// Runs the step loop on already-validated, device-resident partitions.
-pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i, float* G_i,
-                               float* emb_j, float* G_j, const int32_t* src, const int32_t* rel,
-                               const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg,
-                               float lr, uint64_t seed, double* loss_out,
-                               std::vector<double>* step_losses) {
-  const int C = neg->chunk_size, U = neg->num_uniform, S = neg->chunks_per_step;
-  pbg_status st = ensure_workspace(ctx, C, U, S);
-  if (st != PBG_OK) return st;
-  const int64_t nchunks = (n_edges + C - 1) / C;
-  const int64_t nsteps = (nchunks + S - 1) / S;
-  st = ensure_steploss(ctx, nsteps);
-  if (st != PBG_OK) return st;
-  hipStream_t cs = ctx->cs;
+void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, int C, int U, uint64_t seed, StepGeom& g) {
   const int N = C + U;
   const int d = ctx->d, dp = round_up(d, 4), Np = round_up(N, 4);
   const int64_t rows_i = pbg_partition_rows(ctx, i), rows_j = pbg_partition_rows(ctx, j);
-
-  StepGeom g;
   memset(&g, 0, sizeof(g));
   g.C = C;
   g.U = U;
@@ -429,24 +416,57 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   if (g.rb < 1) g.rb = 1;
   g.bucket = (uint32_t)(i * ctx->P + j);
   g.seed = seed;
-  const int key_bits = g.rb + (g.same_table ? 0 : 1);
-  const int rel_bits = bits_for((uint64_t)ctx->R - 1);
-  const bool has_rel = ctx->op != OP_IDENTITY;
-  const bool linear = ctx->op == OP_LINEAR;
+}
 
+StepBufs bucket_bufs(pbg_ctx* ctx, float* emb_i, float* G_i, float* emb_j, float* G_j) {
   StepBufs b = ctx->bufs;
   b.nuniq = (unsigned long long*)(ctx->steploss_dev + std::max<int64_t>(ctx->steploss_cap, 1));
-  if (hipMemsetAsync(b.nuniq, 0, 8, cs) != hipSuccess) return hip_fail(ctx, hipGetLastError(), "counter reset");
   b.emb_i = emb_i;
   b.emb_j = emb_j;
   b.G_i = G_i;
   b.G_j = G_j;
   b.relp = ctx->relp;
   b.relG = ctx->relG;
-  if (!(has_rel && ctx->R > 1 && !linear)) {
+  if (!(ctx->op != OP_IDENTITY && ctx->R > 1)) {
     b.rkeys = nullptr;
     b.rvals = nullptr;
   }
+  return b;
+}
+
+void run_gather_forward(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, hipStream_t cs) {
+  const bool linear1 = ctx->op == OP_LINEAR && ctx->R == 1;
+  if (linear1) launch_pad_linear(ctx->relp, g.d, g.dp, ctx->relA, ctx->relAT, cs);
+  launch_gather(g, b, cs);
+  if (linear1) run_linear_forward(g, b, ctx->relA, ctx->relAT, cs);
+  else if (ctx->op == OP_LINEAR) launch_linear_rows(g, b, cs);
+}
+
+// Runs the step loop on already-validated, device-resident partitions.
+pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i, float* G_i,
+                               float* emb_j, float* G_j, const int32_t* src, const int32_t* rel,
+                               const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg,
+                               float lr, uint64_t seed, double* loss_out,
+                               std::vector<double>* step_losses) {
+  const int C = neg->chunk_size, U = neg->num_uniform, S = neg->chunks_per_step;
+  pbg_status st = ensure_workspace(ctx, C, U, S);
+  if (st != PBG_OK) return st;
+  const int64_t nchunks = (n_edges + C - 1) / C;
+  const int64_t nsteps = (nchunks + S - 1) / S;
+  st = ensure_steploss(ctx, nsteps);
+  if (st != PBG_OK) return st;
+  hipStream_t cs = ctx->cs;
+  const int N = C + U;
+  const int d = ctx->d, dp = round_up(d, 4);
+  StepGeom g;
+  bucket_geom(ctx, i, j, C, U, seed, g);
+  const int key_bits = g.rb + (g.same_table ? 0 : 1);
+  const int rel_bits = bits_for((uint64_t)ctx->R - 1);
+  const bool has_rel = ctx->op != OP_IDENTITY;
+  const bool linear = ctx->op == OP_LINEAR;
+
+  StepBufs b = bucket_bufs(ctx, emb_i, G_i, emb_j, G_j);
+  if (hipMemsetAsync(b.nuniq, 0, 8, cs) != hipSuccess) return hip_fail(ctx, hipGetLastError(), "counter reset");
 
   if (!ensure_side(ctx)) return set_err(ctx, PBG_ERR_DEVICE, "could not create the side stream");
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
@@ -506,20 +526,19 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
 
     mark(t, 0);
 
-    if (linear) launch_pad_linear(ctx->relp, d, dp, ctx->relA, ctx->relAT, cs);
-    launch_gather(g, b, cs);
-    if (linear) run_linear_forward(g, b, ctx->relA, ctx->relAT, cs);
+    run_gather_forward(ctx, g, b, cs);
     mark(t, 1);
 
     if (ctx->flags & PBG_F_BF16_SCORE) {
-      run_contractions_bf16(ctx, g, b, t, cs, [&](int k) { mark(t, k); });
+      run_contractions_bf16(ctx, g, b, t, cs, [&](int k) { mark(t, k); }, false);
     } else {
-      run_contractions_f32(ctx, g, b, t, cs, [&](int k) { mark(t, k); });
+      run_contractions_f32(ctx, g, b, t, cs, [&](int k) { mark(t, k); }, false);
     }
 
     mark(t, 4);
     launch_op_backward(g, b, cs);
-    if (linear) run_linear_backward(g, b, ctx->relA, ctx->relAT, cs);
+    if (linear && ctx->R == 1) run_linear_backward(g, b, ctx->relA, ctx->relAT, cs);
+    else if (linear) launch_linear_rows_backward(g, b, cs);
     mark(t, 5);
     const bool rel_side = has_rel && !linear && ctx->R == 1;
     if (rel_side) side_fork(ctx);
@@ -529,37 +548,15 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
 
     // relations
     if (has_rel) {
-      if (linear) {
-        // dA = sum over edges of dQ_e x_e^T + x_d,e dK_e^T, per chunk by contraction
-        GemmArgs la;
-        memset(&la, 0, sizeof(la));
-        la.A = b.dq;                       // dQ^T: (m = row of A, k = edge)
-        la.B = b.nn + (int64_t)N * dp;     // source rows x_s (N1[e])
-        la.Cm = ctx->relpartial;
-        la.a_cs = 2ll * C * dp;
-        la.b_cs = 2ll * N * dp;
-        la.c_cs = 2ll * d * d;
-        la.lda = dp;
-        la.ldb = dp;
-        la.ldc = d;
-        la.mdim = DIM_FIXED;
-        la.Mfix = d;
-        la.ndim = DIM_FIXED;
-        la.Nfix = d;
-        la.kdim = DIM_CC;
-        la.C = C;
-        la.U = U;
-        la.m_step = m_step;
-        la.nsides = 1;
-        launch_gemm_f32(la, GEMM_TN, nch, cs);
-        GemmArgs lb = la;
-        lb.A = b.nn;                       // destination rows x_d (N0[e])
-        lb.B = b.dq + (int64_t)C * dp;     // dK
-        lb.Cm = ctx->relpartial + (int64_t)d * d;
-        lb.a_cs = 2ll * N * dp;
-        lb.b_cs = 2ll * C * dp;
-        launch_gemm_f32(lb, GEMM_TN, nch, cs);
-        launch_relation_single_adagrad(ctx->relp, ctx->relG, d * d, ctx->relpartial, 2 * nch, lr, cs);
+      if (linear && ctx->R == 1) {
+        // dA per chunk by contraction, then the fixed-order sum of the
+        // partials and element-wise Adagrad
+        const int nparts = run_linear_relation_grad(g, b, ctx->relpartial, cs);
+        launch_relation_single_adagrad(ctx->relp, ctx->relG, d * d, ctx->relpartial, nparts, lr, cs);
+      } else if (linear) {
+        uint32_t *rk = nullptr, *rv = nullptr;
+        launch_radix_sort_to(b.rkeys, b.rvals, m_step, rel_bits, ctx->sw, &rk, &rv, cs);
+        launch_linear_relation_update(g, b, rk, rv, m_step, lr, cs);
       } else if (ctx->R > 1) {
         uint32_t *rk = nullptr, *rv = nullptr;
         launch_radix_sort_to(b.rkeys, b.rvals, m_step, rel_bits, ctx->sw, &rk, &rv, cs);
@@ -631,31 +628,21 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   return PBG_OK;
 }
 
-extern "C" pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
-                                       const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
-                                       const pbg_neg_config* neg, float lr, uint64_t seed,
-                                       double* loss_host) {
-  if (!ctx) return PBG_ERR_INVALID_ARG;
-  if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
-  ctx->err.clear();
+pbg_status check_bucket_call(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
+                             const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
+                             const pbg_neg_config* neg) {
   if (i < 0 || i >= ctx->P || j < 0 || j >= ctx->P)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "bucket (%d, %d) out of range", i, j);
   pbg_status st = check_neg_config(ctx, neg);
   if (st != PBG_OK) return st;
-  if (!std::isfinite(lr) || lr < 0.f) return set_err(ctx, PBG_ERR_INVALID_ARG, "lr must be finite and >= 0");
   if (n_edges < 0 || n_edges > 0x7FFFFFFFll) return set_err(ctx, PBG_ERR_INVALID_ARG, "n_edges out of range");
   const Partition& pi = ctx->parts[i];
   const Partition& pj = ctx->parts[j];
   if (!pi.emb || !pj.emb) return set_err(ctx, PBG_ERR_STATE, "partition %d or %d is not bound", i, j);
   if (pi.where != PBG_MEM_DEVICE || pj.where != PBG_MEM_DEVICE)
-    return set_err(ctx, PBG_ERR_STATE, "pbg_train_bucket needs device-resident partitions");
+    return set_err(ctx, PBG_ERR_STATE, "training needs device-resident partitions");
   if (ctx->op != OP_IDENTITY && !ctx->relp) return set_err(ctx, PBG_ERR_STATE, "relation parameters are not bound");
-  ctx->stats = pbg_stats();
-  ctx->step_losses.clear();
-  if (n_edges == 0) {
-    if (loss_host) *loss_host = 0.0;
-    return PBG_OK;
-  }
+  if (n_edges == 0) return PBG_OK;
   if (ctx->R > 1 && !rel) return set_err(ctx, PBG_ERR_INVALID_ARG, "rel may be NULL only with one relation");
   if (!src_local || !dst_local) return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL edge arrays");
   st = ensure_workspace(ctx, neg->chunk_size, neg->num_uniform, neg->chunks_per_step);
@@ -674,6 +661,27 @@ extern "C" pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const
   if (flag & 1u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a source id is outside partition %d", i);
   if (flag & 2u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a destination id is outside partition %d", j);
   if (flag & 4u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a relation id is outside [0, %d)", ctx->R);
+  return PBG_OK;
+}
+
+extern "C" pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
+                                       const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
+                                       const pbg_neg_config* neg, float lr, uint64_t seed,
+                                       double* loss_host) {
+  if (!ctx) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
+  ctx->err.clear();
+  if (!std::isfinite(lr) || lr < 0.f) return set_err(ctx, PBG_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  pbg_status st = check_bucket_call(ctx, i, j, src_local, rel, dst_local, n_edges, neg);
+  if (st != PBG_OK) return st;
+  ctx->stats = pbg_stats();
+  ctx->step_losses.clear();
+  if (n_edges == 0) {
+    if (loss_host) *loss_host = 0.0;
+    return PBG_OK;
+  }
+  const Partition& pi = ctx->parts[i];
+  const Partition& pj = ctx->parts[j];
   return train_bucket_device(ctx, i, j, pi.emb, pi.G, pj.emb, pj.G, src_local, rel, dst_local, n_edges,
                              neg, lr, seed, loss_host, &ctx->step_losses);
 }

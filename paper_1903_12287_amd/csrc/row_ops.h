@@ -138,6 +138,30 @@ __device__ __forceinline__ void mat_apply(RowT<RQ>& out, const float* mat, const
   out = o;
 }
 
+// out = M x for a row-major d x d matrix M (out[k] = sum_l M[k*d + l] x[l]):
+// each lane walks its own output rows, so consecutive iterations read
+// consecutive floats of each row (the lines stay in the vector cache).
+template <int RQ>
+__device__ __forceinline__ void mat_rows_apply(RowT<RQ>& out, const float* M, const RowT<RQ>& x, float* stage,
+                                               int d, int lane) {
+#pragma unroll
+  for (int q = 0; q < RQ; ++q)
+    if (lane + 64 * q < d) stage[lane + 64 * q] = x.v[q];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  RowT<RQ> o;
+  row_zero(o);
+  for (int l = 0; l < d; ++l) {
+    const float xl = stage[l];
+#pragma unroll
+    for (int q = 0; q < RQ; ++q)
+      if (lane + 64 * q < d) o.v[q] += M[(size_t)(lane + 64 * q) * d + l] * xl;
+  }
+  __builtin_amdgcn_wave_barrier();
+  out = o;
+}
+
 // g(x, theta) for the non-matrix operators (real or complex layout)
 template <int RQ>
 __device__ __forceinline__ RowT<RQ> op_forward(int op, const RowT<RQ>& x, const RowT<RQ>& th) {

@@ -101,7 +101,7 @@ struct pbg_ctx {
 constexpr int kPhaseEvents = 7;
 // score-only timing brackets every kScoreSample-th step (each event record
 // costs the compute stream a few microseconds)
-constexpr int kScoreSample = 8;
+constexpr int kScoreSample = 2;
 // steps whose entity sort keys are built and sorted together, as one batch
 constexpr int kSortWindow = 32;
 
@@ -114,16 +114,37 @@ void side_fork(pbg_ctx* ctx);
 void side_mark(pbg_ctx* ctx, int k);
 void side_wait(pbg_ctx* ctx, int k);
 
+// the three contractions of step t (forward_only: the score contraction with
+// its loss epilogue and the per-edge finalisation only)
 void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t, hipStream_t cs,
-                          const std::function<void(int)>& mark);
+                          const std::function<void(int)>& mark, bool forward_only);
 void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, int64_t t,
-                           hipStream_t cs, const std::function<void(int)>& mark);
+                           hipStream_t cs, const std::function<void(int)>& mark, bool forward_only);
+void run_score_store(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, float* out, hipStream_t cs);
+// the linear operator with one relation, as contractions over the step (A
+// and A^T row-padded in Ap / ATp)
 void run_linear_forward(const StepGeom& g, const StepBufs& b, const float* Ap, const float* ATp, hipStream_t cs);
 void run_linear_backward(const StepGeom& g, const StepBufs& b, const float* Ap, const float* ATp,
                          hipStream_t cs);
+int run_linear_relation_grad(const StepGeom& g, const StepBufs& b, float* partial, hipStream_t cs);
+// gather + relation operator + uniform draws of a step (with the linear
+// operator's products)
+void run_gather_forward(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, hipStream_t cs);
 pbg_status hip_fail(pbg_ctx* ctx, hipError_t e, const char* what);
 bool alloc_sortwork(Arena& a, SortWork& w, int64_t max_n, int width);
 pbg_status check_neg_config(pbg_ctx* ctx, const pbg_neg_config* neg);
+// the argument and state checks of a training call on bucket (i, j), then the
+// device-side range check of every id (nothing is modified on failure)
+pbg_status check_bucket_call(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
+                             const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
+                             const pbg_neg_config* neg);
+pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S);
+pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps);
+// geometry of the steps of bucket (i, j) (chunk and candidate counts, padded
+// strides, partition rows, key widths) and the step buffers bound to the
+// given partitions and the context's workspace
+void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, int C, int U, uint64_t seed, StepGeom& g);
+StepBufs bucket_bufs(pbg_ctx* ctx, float* emb_i, float* G_i, float* emb_j, float* G_j);
 pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i, float* G_i,
                                float* emb_j, float* G_j, const int32_t* src, const int32_t* rel,
                                const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg,

@@ -36,7 +36,7 @@ EXPORTS = (
     "pbg_relation_param_floats", "pbg_bucket_edges", "pbg_bind_partition",
     "pbg_bind_relations", "pbg_set_streams", "pbg_train_bucket", "pbg_get_step_losses",
     "pbg_train_epoch", "pbg_score_edges", "pbg_rank_eval", "pbg_rank_sampled", "pbg_get_stats",
-    "pbg_sample_negatives",
+    "pbg_sample_negatives", "pbg_inspect_step",
 )
 
 
@@ -99,6 +99,8 @@ def library() -> ctypes.CDLL:
         "pbg_rank_sampled": ([vp, vp, vp, vp, i64, vp, i64, vp, dp, dp], i32),
         "pbg_get_stats": ([vp, ctypes.POINTER(Stats)], i32),
         "pbg_sample_negatives": ([vp, i32, i32, i64, i64, i32, u64, vp], i32),
+        "pbg_inspect_step": ([vp, i32, i32, vp, vp, vp, i64, ctypes.POINTER(NegConfig), u64, vp, vp, vp, vp,
+                              dp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -309,3 +311,27 @@ def pbg_sample_negatives(ctx, i, j, first_chunk, n_chunks, num_uniform, seed, ou
     _check(ctx, library().pbg_sample_negatives(
         ctx, int(i), int(j), int(first_chunk), int(n_chunks), int(num_uniform),
         int(seed) & 0xFFFFFFFFFFFFFFFF, _ptr(out, torch.int32, "out", allow_none=True)))
+
+
+def pbg_inspect_step(ctx, i, j, src_local, rel, dst_local, chunk_size, num_uniform, chunks_per_step, seed,
+                     first_chunk=0, scores=None, dscores=None, row_loss=None, pos=None) -> float:
+    n = src_local.numel()
+    if dst_local.numel() != n or (rel is not None and rel.numel() != n):
+        raise ValueError("edge arrays differ in length")
+    nch = -(-n // int(chunk_size))
+    N = int(chunk_size) + int(num_uniform)
+    for t, want, name in ((scores, nch * 2 * chunk_size * N, "scores"), (dscores, nch * 2 * chunk_size * N, "dscores"),
+                          (row_loss, nch * 2 * chunk_size, "row_loss"), (pos, nch * chunk_size, "pos")):
+        if t is not None and t.numel() != want:
+            raise ValueError(f"{name} must hold {want} floats")
+    neg = _neg(chunk_size, num_uniform, chunks_per_step, first_chunk)
+    loss = ctypes.c_double(0.0)
+    _check(ctx, library().pbg_inspect_step(
+        ctx, int(i), int(j), _ptr(src_local, torch.int32, "src_local", allow_none=n == 0),
+        _ptr(rel, torch.int32, "rel", allow_none=True),
+        _ptr(dst_local, torch.int32, "dst_local", allow_none=n == 0), n, ctypes.byref(neg),
+        int(seed) & 0xFFFFFFFFFFFFFFFF, _ptr(scores, torch.float32, "scores", allow_none=True),
+        _ptr(dscores, torch.float32, "dscores", allow_none=True),
+        _ptr(row_loss, torch.float32, "row_loss", allow_none=True),
+        _ptr(pos, torch.float32, "pos", allow_none=True), ctypes.byref(loss)))
+    return loss.value

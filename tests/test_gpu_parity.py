@@ -15,7 +15,7 @@ import pytest
 import torch
 
 from oracle import pbg_oracle as O
-from tests.pbg_cases import GpuModel, make_problem, oracle_model
+from tests.pbg_cases import GpuModel, make_problem, oracle_model, teacher_forced_step
 
 pytestmark = pytest.mark.gpu
 
@@ -35,11 +35,37 @@ COMBOS = [
     ("complex_diagonal", "cos", "softmax"),
     ("linear", "dot", "logistic"),
     ("linear", "dot", "ranking"),
+    ("linear", "dot", "softmax"),
+    ("linear", "cos", "ranking"),
+    ("linear", "cos", "logistic"),
+    ("linear", "cos", "softmax"),
 ]
 
 
 def _R_for(op, cmp):
-    return 1 if (cmp == "cos" and op != "identity") or op == "linear" else 3
+    # cos with an operator takes one relation (several are UNSUPPORTED)
+    return 1 if (cmp == "cos" and op != "identity") else 3
+
+
+@pytest.mark.parametrize("op,cmp,loss", [("linear", "dot", "ranking"), ("linear", "dot", "logistic")])
+def test_linear_single_relation_one_step(op, cmp, loss):
+    """The linear operator with one relation (contractions over the whole
+    step) next to the several-relation path the combinations above take."""
+    pb = make_problem(op, cmp, loss, R=1, m=95, C=20, U=12, S=8, seed=31)
+    gm = GpuModel(pb)
+    try:
+        gl = gm.train()
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol = O.train_bucket(om, pb.i, pb.j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr, pb.seed)
+    assert abs(gl - ol) <= 1e-5 * max(1.0, abs(ol)), (gl, ol)
+    for key, ref in (("G", om.G[0]), ("emb", om.emb[0])):
+        ok, err = _close(st[key][0], ref)
+        assert ok, (key, err)
+    ok, err = _close(st["rel"], om.rel)
+    assert ok, ("rel", err)
 
 
 def _close(gpu, ref, rel=1e-5, abs_=1e-6):
@@ -124,28 +150,22 @@ BF16_COMBOS = [
     ("complex_diagonal", "dot", "softmax"),
     ("diagonal", "dot", "ranking"),
     ("linear", "dot", "logistic"),
+    ("linear", "cos", "ranking"),
     ("translation", "dot", "softmax"),
 ]
 
 
-def _check_bf16_step(before, st, om, gl, ol):
-    """bf16 bar (2e-2): the loss; the gradient magnitudes, read from the
-    Adagrad accumulators (one step from G = 0 leaves G = |g|^2 per entity row
-    and g^2 per relation element), within 2e-2 of the largest; and the entity
-    update within 2e-2 in Frobenius norm.  Single elements of the update are
-    not compared: Adagrad's first step is lr * g / |g|, so a gradient element
-    near zero may change sign under bf16 rounding (and a ranking hinge within
-    rounding of its kink may switch), which the norms above bound."""
+def _check_bf16_step(gm):
+    """bf16 bar (2e-2), element by element, on one step from the same state
+    (teacher_forced_step with eps = 2e-2): hinge terms within 2e-2 * A of the
+    kink may take the other branch (counted, and followed by the oracle), the
+    step loss within 2e-2 relative, and every embedding, accumulator and
+    relation element within the Adagrad-propagated bound of a gradient error
+    of 2e-2 * A per element."""
+    rep, gl, ol, worst = teacher_forced_step(gm, 0, gm.pb.src.shape[0], 0, 2e-2)
+    print(f"census {rep}, loss gpu {gl:.7g} oracle {ol:.7g}, worst error / bound {worst:.3f}", flush=True)
     assert abs(gl - ol) <= 2e-2 * abs(ol), (gl, ol)
-    g_gpu, g_orc = np.sqrt(st["G"][0]), np.sqrt(om.G[0])
-    assert float(np.max(np.abs(g_gpu - g_orc))) <= 2e-2 * float(np.max(g_orc))
-    d_gpu = st["emb"][0] - before["emb"][0]
-    d_orc = om.emb[0] - before["emb"][0]
-    assert np.all(np.isfinite(d_gpu))
-    assert np.linalg.norm(d_gpu - d_orc) <= 2e-2 * np.linalg.norm(d_orc)
-    if om.rel is not None:
-        r_gpu, r_orc = np.sqrt(st["relG"]), np.sqrt(om.relG)
-        assert float(np.max(np.abs(r_gpu - r_orc))) <= 2e-2 * float(np.max(r_orc))
+    assert worst <= 1.0
 
 
 @pytest.mark.parametrize("op,cmp,loss", BF16_COMBOS)
@@ -155,14 +175,9 @@ def test_bf16_score_path_one_step(op, cmp, loss):
     pb = make_problem(op, cmp, loss, R=_R_for(op, cmp), m=150, C=40, U=24, S=8, seed=13, d=48)
     gm = GpuModel(pb, flags=pbg.F_BF16_SCORE)
     try:
-        before = gm.state()
-        gl = gm.train()
-        st = gm.state()
+        _check_bf16_step(gm)
     finally:
         gm.close()
-    om = oracle_model(pb)
-    ol = O.train_bucket(om, pb.i, pb.j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr, pb.seed)
-    _check_bf16_step(before, st, om, gl, ol)
 
 
 def test_bf16_short_chunks_and_ragged_dims():
@@ -172,11 +187,6 @@ def test_bf16_short_chunks_and_ragged_dims():
     pb = make_problem("diagonal", "dot", "logistic", R=2, m=77, C=19, U=13, S=5, seed=17, d=37)
     gm = GpuModel(pb, flags=pbg.F_BF16_SCORE)
     try:
-        before = gm.state()
-        gl = gm.train()
-        st = gm.state()
+        _check_bf16_step(gm)
     finally:
         gm.close()
-    om = oracle_model(pb)
-    ol = O.train_bucket(om, 0, 0, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr, pb.seed)
-    _check_bf16_step(before, st, om, gl, ol)
