@@ -297,6 +297,24 @@ pbg_status pbg_inspect_step(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* s
                             const pbg_neg_config* neg, uint64_t seed, float* scores, float* dscores,
                             float* row_loss, float* pos, double* loss_host);
 
+/* Largest relation parameter count (R * dim * dim floats, the linear
+ * operator only) that pbg_score_edges_noalloc accepts. */
+#define PBG_NOALLOC_MAX_REL_FLOATS (2 * 1024 * 1024)
+
+/* pbg_score_edges for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, results and errors as pbg_score_edges, computed by the same
+ * kernels; the scratch that pbg_score_edges allocates per call (the id-check
+ * flag and, for LINEAR, a transposed copy of the relation matrices) is a
+ * static device array of the library instead, 8 MiB + 256 bytes, held on
+ * each device the library runs on until the process ends.  INVALID_ARG when
+ * the operator is LINEAR and R * dim * dim exceeds
+ * PBG_NOALLOC_MAX_REL_FLOATS.  The context's device must be current.  All
+ * calls on one device share that device's array: calls that overlap on one
+ * device (several host threads, or several streams in flight) race. */
+pbg_status pbg_score_edges_noalloc(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
+                                   const int32_t* rel, const int32_t* dst_local, int64_t n, float* scores);
+
 /* Timings and algorithmic work of the last training call. */
 pbg_status pbg_get_stats(const pbg_ctx* ctx, pbg_stats* out_host);
 

@@ -232,6 +232,8 @@ void launch_gather3(const uint32_t* perm, const int32_t* a, const int32_t* b, co
 // ---- checks, scoring, ranking --------------------------------------------------
 void launch_check_ids(const int32_t* ids, int64_t n, int32_t limit, uint32_t* flag, uint32_t bit,
                       hipStream_t s);
+// p[0 .. n) = v (a kernel, so that it may sit in a captured graph)
+void launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 void launch_check_ids64(const int64_t* ids, int64_t n, int64_t limit, uint32_t* flag, uint32_t bit,
                         hipStream_t s);
 void launch_score_edges(const StepGeom& g, const float* emb_i, const float* emb_j, const float* relp,

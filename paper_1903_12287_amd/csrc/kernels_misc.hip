@@ -73,6 +73,11 @@ __global__ void sample_negatives_kernel(uint64_t seed, uint32_t bucket, int64_t 
   }
 }
 
+__global__ void fill_u32_kernel(uint32_t* p, int64_t n, uint32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
 int blocks_for(int64_t n) {
   int64_t b = (n + 255) / 256;
   if (b < 1) b = 1;
@@ -109,4 +114,9 @@ void launch_sample_negatives(uint64_t seed, uint32_t bucket, int64_t chunk0, int
   if (total <= 0) return;
   sample_negatives_kernel<<<blocks_for(total), 256, 0, s>>>(seed, bucket, chunk0, n_chunks, U, rows_j,
                                                            rows_i, out);
+}
+
+void launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
+  if (n <= 0) return;
+  fill_u32_kernel<<<blocks_for(n), 256, 0, s>>>(p, n, v);
 }

@@ -283,6 +283,11 @@ pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_part
     (void)hipGetLastError();
     return fail(PBG_ERR_DEVICE, "no HIP device");
   }
+  if (noalloc_scratch_init(ctx) != PBG_OK) {
+    ctx->invalid = true;
+    *out = ctx;
+    return PBG_ERR_DEVICE;
+  }
   *out = ctx;
   return PBG_OK;
 }

@@ -106,6 +106,9 @@ constexpr int kScoreSample = 2;
 constexpr int kSortWindow = 32;
 
 pbg_status set_err(pbg_ctx* ctx, pbg_status st, const char* fmt, ...);
+// device address of the static scratch of pbg_score_edges_noalloc on the
+// context's device (taken once per device; called by pbg_bucket_init)
+pbg_status noalloc_scratch_init(pbg_ctx* ctx);
 // work of a step on the side stream: side_fork makes the side stream wait for
 // what the compute stream has queued so far; side_mark(k) marks what the side
 // stream has queued so far and side_wait(k) makes the compute stream wait for

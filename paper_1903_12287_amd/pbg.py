@@ -27,6 +27,7 @@ F_PHASE_TIMING = 2
 F_SCORE_TIMING = 4
 MEM_DEVICE = 0
 MEM_PINNED_HOST = 1
+NOALLOC_MAX_REL_FLOATS = 2 * 1024 * 1024   # PBG_NOALLOC_MAX_REL_FLOATS
 
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "OUT_OF_MEMORY", 4: "DEVICE", 5: "STATE"}
 
@@ -36,7 +37,7 @@ EXPORTS = (
     "pbg_relation_param_floats", "pbg_bucket_edges", "pbg_bind_partition",
     "pbg_bind_relations", "pbg_set_streams", "pbg_train_bucket", "pbg_get_step_losses",
     "pbg_train_epoch", "pbg_score_edges", "pbg_rank_eval", "pbg_rank_sampled", "pbg_get_stats",
-    "pbg_sample_negatives", "pbg_inspect_step",
+    "pbg_sample_negatives", "pbg_inspect_step", "pbg_score_edges_noalloc",
 )
 
 
@@ -95,6 +96,7 @@ def library() -> ctypes.CDLL:
         "pbg_get_step_losses": ([vp, dp, i64, ctypes.POINTER(ctypes.c_int64)], i32),
         "pbg_train_epoch": ([vp, vp, vp, vp, vp, ctypes.POINTER(NegConfig), f32, u64, i32, dp], i32),
         "pbg_score_edges": ([vp, i32, i32, vp, vp, vp, i64, vp], i32),
+        "pbg_score_edges_noalloc": ([vp, i32, i32, vp, vp, vp, i64, vp], i32),
         "pbg_rank_eval": ([vp, vp, vp, vp, i64, vp, vp, vp, i64, vp, dp, dp], i32),
         "pbg_rank_sampled": ([vp, vp, vp, vp, i64, vp, i64, vp, dp, dp], i32),
         "pbg_get_stats": ([vp, ctypes.POINTER(Stats)], i32),
@@ -272,6 +274,15 @@ def pbg_train_epoch(ctx, offsets, src_local, rel, dst_local, chunk_size, num_uni
 def pbg_score_edges(ctx, i, j, src_local, rel, dst_local, scores):
     n = src_local.numel()
     _check(ctx, library().pbg_score_edges(
+        ctx, int(i), int(j), _ptr(src_local, torch.int32, "src_local", allow_none=n == 0),
+        _ptr(rel, torch.int32, "rel", allow_none=True),
+        _ptr(dst_local, torch.int32, "dst_local", allow_none=n == 0), n,
+        _ptr(scores, torch.float32, "scores", allow_none=n == 0)))
+
+
+def pbg_score_edges_noalloc(ctx, i, j, src_local, rel, dst_local, scores):
+    n = src_local.numel()
+    _check(ctx, library().pbg_score_edges_noalloc(
         ctx, int(i), int(j), _ptr(src_local, torch.int32, "src_local", allow_none=n == 0),
         _ptr(rel, torch.int32, "rel", allow_none=True),
         _ptr(dst_local, torch.int32, "dst_local", allow_none=n == 0), n,
