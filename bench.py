@@ -16,6 +16,11 @@ device synchronisation; the steps walk consecutive chunks of the bucket
 Prints one JSON line with the metric, the roofline figure of the dominant
 kernel (the score contraction with its fused loss epilogue, timed with HIP
 events on the compute stream) and the CPU oracle timed on a bounded sample.
+The line also carries the bf16-input leg of the same workload and, under
+"big_bucket", one whole bucket (3, 7) of the partitioned
+large-knowledge-graph-shaped run (9,375,000 edges, two resident partitions of
+7,576,046 rows, d = 100, diagonal, dot, ranking): the one-GPU share of a
+bucket-parallel run.
 """
 
 from __future__ import annotations
@@ -35,6 +40,7 @@ LR, MARGIN, SEED = 0.1, 0.1, 20190002
 PEAK_FP32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
 PEAK_BF16_MFMA = 2516.6  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8000.0        # GB/s
+SPLIT_PIECES = 6         # bf16 piece products per float32 product in the score contraction
 
 
 def parse():
@@ -46,6 +52,8 @@ def parse():
                     help="chunks of the same bucket the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true", help="skip the bf16-input leg")
+    ap.add_argument("--no-big-bucket", action="store_true",
+                    help="skip the second workload of the default line (one bucket of the partitioned graph)")
     ap.add_argument("--row", choices=["bucketing", "knowledge_graph", "big_bucket", "epoch", "tiny", "negatives"],
                     help="measure another row of the hot path instead of the default training step: "
                          "edge bucketing of the follower graph, the knowledge-graph pass and filtered "
@@ -86,6 +94,23 @@ def train_range(pbg, ctx, src, dst, step0, nsteps, total_steps):
     return loss
 
 
+def host_cpu():
+    """What the oracle's timing ran on: CPU model, cores this process may use
+    (its affinity set) and the threads torch's CPU kernels use."""
+    import torch
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "affinity_cores": len(os.sched_getaffinity(0)),
+            "threads": torch.get_num_threads()}
+
+
 def cpu_baseline(src_h, dst_h, emb_h, chunks):
     """The oracle, as it stands, on the first `chunks` chunks of the bucket."""
     import numpy as np
@@ -98,7 +123,7 @@ def cpu_baseline(src_h, dst_h, emb_h, chunks):
     t0 = time.perf_counter()
     O.train_bucket(model, 0, 0, src_h[:m], None, dst_h[:m], C, U, S, LR, SEED)
     dt = time.perf_counter() - t0
-    return {"value": m / dt, "unit": "edges/s", "cores": torch.get_num_threads(), "kind": "oracle",
+    return {"value": m / dt, "unit": "edges/s", "cores": torch.get_num_threads(), "kind": "oracle", **host_cpu(),
             "sample": f"first {chunks} chunks ({m} edges) of the same bucket from the same initial "
                       f"state, fp64 numpy/torch-CPU oracle, {dt:.1f} s"}
 
@@ -170,24 +195,29 @@ def hbm_rate(st, bytes_key, ms_key, traffic):
     return out
 
 
-def roofline(st, peak, kernel, traffic=None, pieces=None):
+def roofline(st, kernel, traffic=None, pieces=None):
     """Dominant kernel: the score contraction with its fused loss epilogue.
     Algorithmic flops per launch: 2 sides x 2 C N d per chunk (a third of the
-    12 C N d of the three contractions), one launch per step.  `pieces`: the
-    float32 contraction runs as that many exact-piece bf16 products, reported
-    beside it as the executed matrix-instruction rate."""
+    12 C N d of the three contractions), one launch per step.  The kernel
+    issues v_mfma_f32_16x16x32_bf16 in both precisions; a float32 contraction
+    issues `pieces` exact bf16 piece products per product, so its ceiling is
+    the bf16 matrix peak over `pieces` (frac), and its rate against the fp32
+    matrix peak is given beside it (fp32_peak_frac)."""
     launches = max(1, st["steps"])
     timed = max(1, st.get("score_timed_steps") or launches)   # launches the events bracketed
     flops = st["score_flops"] / 3.0 / launches                   # per launch
     avg_ms = st["score_ms"] / timed
     achieved = flops / (avg_ms / 1e3) / 1e12 if avg_ms > 0 else None
+    peak = PEAK_BF16_MFMA / (pieces or 1)
     out = {"kernel": kernel, "bound": "mfma", "achieved": achieved, "peak": peak,
            "unit": "TFLOP/s", "frac": achieved / peak if achieved else None, "traffic": traffic,
            "avg_launch_ms": avg_ms, "flops_per_launch": flops, "timed_launches": timed}
     if pieces and achieved:
-        out["executed"] = {"instruction": "v_mfma_f32_16x16x32_bf16", "piece_products": pieces,
-                           "achieved": pieces * achieved, "peak": PEAK_BF16_MFMA, "unit": "TFLOP/s",
-                           "frac": pieces * achieved / PEAK_BF16_MFMA}
+        out["peak_note"] = (f"bf16 matrix peak {PEAK_BF16_MFMA} / {pieces} exact bf16 piece products "
+                            "per float32 product (the instruction the kernel issues)")
+        out["fp32_peak"] = PEAK_FP32_MFMA
+        out["fp32_peak_frac"] = achieved / PEAK_FP32_MFMA
+        out["executed_tflops"] = pieces * achieved
     return out
 
 
@@ -249,9 +279,8 @@ def main():
                    "operator": "translation", "comparator": "cos", "loss": "ranking",
                    "chunk": C, "uniform_negatives": U, "chunks_per_step": S,
                    "edges_per_step": S * C, "partitions": 1},
-        "roofline": roofline(st, PEAK_FP32_MFMA,
-                             "score_split_kernel3<EPI_LOSS_BITS, 6> (float32 score + ranking epilogue)",
-                             measured_traffic("score"), pieces=6),
+        "roofline": roofline(st, "score_split_kernel3<EPI_LOSS_BITS, 6> (float32 score + ranking epilogue)",
+                             measured_traffic("score"), pieces=SPLIT_PIECES),
         # from the phase-timing run of phase_steps steps
         "phases_ms_per_step": phases(stp),
         "phase_steps": phase_steps,
@@ -269,12 +298,17 @@ def main():
         print(f"# bf16: {st16['edges'] / dt16:.4g} edges/s", file=sys.stderr)
         out["bf16"] = {"value": st16["edges"] / dt16, "unit": "edges/s",
                        "ms_per_step": dt16 * 1e3 / args.steps, "dtype": "bf16 inputs, f32 accumulate",
-                       "roofline": roofline(st16, PEAK_BF16_MFMA,
-                                            "gemm_bf16_kernel<128,GA_KC,EPI_LOSS_BITS,1> (score + ranking epilogue)"),
+                       "roofline": roofline(st16, "gemm_bf16_kernel<128,GA_KC,EPI_LOSS_BITS,1> "
+                                                  "(score + ranking epilogue)"),
                        "phases_ms_per_step": phases(st16p)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(src.cpu().numpy(), dst.cpu().numpy(), emb0.cpu().numpy(),
                                            args.cpu_sample_chunks)
+    if not args.no_big_bucket:
+        # the one-GPU share of the partitioned run: one whole bucket at its real shape
+        del src, dst, emb0
+        torch.cuda.empty_cache()
+        out["big_bucket"] = big_bucket_legs(with_cpu=False)
     print(json.dumps(out))
 
 
@@ -299,6 +333,9 @@ def _median_time(fn, reps=3):
 def _cores():
     import torch
     return torch.get_num_threads()
+
+
+
 
 
 def row_bucketing():
@@ -335,7 +372,7 @@ def row_bucketing():
                          "frac": alg_bytes / dt / 1e9 / PEAK_HBM, "traffic": None,
                          "note": "algorithmic bytes = 24 per edge (two int64 ids in, two int32 local ids out); "
                                  "the call also makes one stable radix pass over 8-byte key/position pairs"},
-            "cpu_baseline": {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+            "cpu_baseline": {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle", **host_cpu(),
                              "sample": f"first {m} edges, numpy stable argsort, {ct:.1f} s"}}
 
 
@@ -378,8 +415,7 @@ def row_knowledge_graph():
         st = pbg.pbg_get_stats(ctx)
         out["value"] = w.E / dt
         out["ms_per_pass"] = dt * 1e3
-        out["roofline"] = roofline(st, PEAK_FP32_MFMA, "score_split_kernel<EPI_SOFTMAX_EXP, 6> (score)",
-                                   pieces=6)
+        out["roofline"] = roofline(st, "score_split_kernel<EPI_SOFTMAX_EXP, 6> (score)", pieces=SPLIT_PIECES)
         out["phases_ms_per_step"] = phases(st)
         # filtered ranks of the held-out triples, known = train + held-out
         hs, hr, hd = t(w.held_src), t(w.held_rel), t(w.held_dst)
@@ -392,8 +428,10 @@ def row_knowledge_graph():
         flops = 2.0 * 2.0 * len(w.held_src) * w.n * w.d
         out["rank_eval"] = {"value": len(w.held_src) / et, "unit": "held-out triples/s (both sides)",
                             "ms": et * 1e3, "mrr": mrr, "hits10": hits,
-                            "roofline": {"bound": "mfma", "achieved": flops / et / 1e12, "peak": PEAK_FP32_MFMA,
-                                         "unit": "TFLOP/s", "frac": flops / et / 1e12 / PEAK_FP32_MFMA,
+                            "roofline": {"bound": "mfma", "achieved": flops / et / 1e12,
+                                         "peak": PEAK_BF16_MFMA / SPLIT_PIECES, "unit": "TFLOP/s",
+                                         "frac": flops / et / 1e12 / (PEAK_BF16_MFMA / SPLIT_PIECES),
+                                         "fp32_peak_frac": flops / et / 1e12 / PEAK_FP32_MFMA,
                                          "traffic": None,
                                          "note": "2 sides x 2 x held-out x entities x dim flops of candidate "
                                                  "scores, whole call time"}}
@@ -408,8 +446,10 @@ def row_knowledge_graph():
         out["rank_sampled"] = {"value": len(w.held_src) / st_, "unit": "held-out triples/s (both sides)",
                                "ms": st_ * 1e3, "candidates": len(cand_h), "mrr": smrr, "hits10": shits,
                                "roofline": {"bound": "mfma", "achieved": sflops / st_ / 1e12,
-                                            "peak": PEAK_FP32_MFMA, "unit": "TFLOP/s",
-                                            "frac": sflops / st_ / 1e12 / PEAK_FP32_MFMA, "traffic": None,
+                                            "peak": PEAK_BF16_MFMA / SPLIT_PIECES, "unit": "TFLOP/s",
+                                            "frac": sflops / st_ / 1e12 / (PEAK_BF16_MFMA / SPLIT_PIECES),
+                                            "fp32_peak_frac": sflops / st_ / 1e12 / PEAK_FP32_MFMA,
+                                            "traffic": None,
                                             "note": "2 sides x 2 x held-out x candidates x dim flops of "
                                                     "candidate scores, whole call time"}}
         emb_h = emb.cpu().numpy()
@@ -422,7 +462,7 @@ def row_knowledge_graph():
     c0 = time.perf_counter()
     O.train_bucket(model, 0, 0, w.src[:m], w.rel[:m], w.dst[:m], w.C, w.U, w.S, w.lr, w.seed)
     ct = time.perf_counter() - c0
-    out["cpu_baseline"] = {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+    out["cpu_baseline"] = {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle", **host_cpu(),
                            "sample": f"first 10 chunks ({m} edges), one step, fp64, {ct:.1f} s"}
     emodel = O.Model.create(w.n, 1, w.R, w.d, w.op, w.cmp, w.loss, w.margin, [emb_h.astype(np.float64)],
                             relp_h.astype(np.float64))
@@ -432,12 +472,12 @@ def row_knowledge_graph():
                 np.concatenate([w.rel, w.held_rel]), np.concatenate([w.dst, w.held_dst]))
     ct = time.perf_counter() - c0
     out["rank_eval"]["cpu_baseline"] = {"value": k / ct, "unit": "held-out triples/s", "cores": _cores(),
-                                        "kind": "oracle", "sample": f"first {k} held-out triples, {ct:.1f} s"}
+                                        "kind": "oracle", **host_cpu(), "sample": f"first {k} held-out triples, {ct:.1f} s"}
     c0 = time.perf_counter()
     O.rank_sampled(emodel, w.held_src[:k], w.held_rel[:k], w.held_dst[:k], cand_h)
     ct = time.perf_counter() - c0
     out["rank_sampled"]["cpu_baseline"] = {"value": k / ct, "unit": "held-out triples/s", "cores": _cores(),
-                                           "kind": "oracle", "sample": f"first {k} held-out triples, {ct:.1f} s"}
+                                           "kind": "oracle", **host_cpu(), "sample": f"first {k} held-out triples, {ct:.1f} s"}
     return out
 
 
@@ -454,11 +494,13 @@ def _big_bucket_tensors(torch, synth):
             emb_i, emb_j)
 
 
-def row_big_bucket():
+def big_bucket_legs(with_cpu=True, phase_steps=20):
     """Bucket (3, 7) of a large partitioned knowledge-graph-shaped run
     (121,216,723 entities in 16 partitions of 7,576,046 rows, 9,375,000 edges,
     5,000 relations Zipf 1.3, d = 100, diagonal, dot, ranking 0.1): one pass
-    in fp32 and one with bf16 score inputs, both partitions resident."""
+    in fp32 and one with bf16 score inputs, both partitions resident in HBM,
+    each after a 10-step warm-up; the phase breakdown from a separate run of
+    `phase_steps` steps with events around every kernel group."""
     import numpy as np
     import torch
     from oracle import pbg_oracle as O
@@ -472,12 +514,13 @@ def row_big_bucket():
                       "rows_per_partition": ps, "edges": E, "relations": R, "dim": d, "operator": "diagonal",
                       "comparator": "dot", "loss": "ranking", "chunk": Cb, "uniform_negatives": Ub,
                       "chunks_per_step": Sb}}
-    for flags, key in ((0, None), (pbg.F_BF16_SCORE, "bf16")):
+
+    def leg(flags, timing, m):
         emb_i, emb_j, relp = emb_i0.clone(), emb_j0.clone(), relp0.clone()
         Gi = torch.zeros(ps, device="cuda")
         Gj = torch.zeros(ps, device="cuda")
         relG = torch.zeros_like(relp)
-        ctx = pbg.pbg_bucket_init(n, P, R, d, "diagonal", "dot", "ranking", 0.1, flags | pbg.F_PHASE_TIMING)
+        ctx = pbg.pbg_bucket_init(n, P, R, d, "diagonal", "dot", "ranking", 0.1, flags | timing)
         try:
             pbg.pbg_bind_partition(ctx, i, emb_i, Gi)
             pbg.pbg_bind_partition(ctx, j, emb_j, Gj)
@@ -487,35 +530,49 @@ def row_big_bucket():
             pbg.pbg_train_bucket(ctx, i, j, src[:w], rel[:w], dst[:w], Cb, Ub, Sb, 0.1, 1)   # warm-up
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            pbg.pbg_train_bucket(ctx, i, j, src, rel, dst, Cb, Ub, Sb, 0.1, 20190004)
+            pbg.pbg_train_bucket(ctx, i, j, src[:m], rel[:m], dst[:m], Cb, Ub, Sb, 0.1, 20190004)
             torch.cuda.synchronize()
             dt = time.perf_counter() - t0
             st = pbg.pbg_get_stats(ctx)
         finally:
             pbg.pbg_free(ctx)
-        peak = PEAK_BF16_MFMA if flags else PEAK_FP32_MFMA
-        leg = {"value": E / dt, "ms_per_pass": dt * 1e3,
-               "roofline": roofline(st, peak, "score contraction with the ranking epilogue",
-                                    pieces=None if flags else 6),
-               "phases_ms_per_step": phases(st)}
+        return dt, st
+
+    for flags, key in ((0, None), (pbg.F_BF16_SCORE, "bf16")):
+        dt, st = leg(flags, pbg.F_SCORE_TIMING, E)
+        _, stp = leg(flags, pbg.F_PHASE_TIMING, phase_steps * Sb * Cb)
+        res = {"value": E / dt, "ms_per_pass": dt * 1e3, "ms_per_step": dt * 1e3 / max(1, st["steps"]),
+               "roofline": roofline(st, "score contraction with the ranking epilogue",
+                                    pieces=None if flags else SPLIT_PIECES),
+               "phases_ms_per_step": phases(stp), "phase_steps": phase_steps,
+               "gather_hbm": hbm_rate(stp, "gather_bytes", "gather_ms", None),
+               "adagrad_hbm": hbm_rate(stp, "update_bytes", "update_ms", None)}
         if key:
-            out[key] = leg
+            res["dtype"] = "bf16 inputs, f32 accumulate"
+            out[key] = res
         else:
-            out.update(leg)
-    # oracle: the first 10 chunks from the same initial state, partitions i and j only
-    m = 10 * Cb
-    model = O.Model(n, P, R, d, "diagonal", "dot", "ranking", 0.1)
-    model.emb = {i: emb_i0.cpu().numpy().astype(np.float64), j: emb_j0.cpu().numpy().astype(np.float64)}
-    model.G = {i: np.zeros(ps), j: np.zeros(ps)}
-    model.rel = np.ones((R, d))
-    model.relG = np.zeros((R, d))
-    hs, hr, hd = src[:m].cpu().numpy(), rel[:m].cpu().numpy(), dst[:m].cpu().numpy()
-    c0 = time.perf_counter()
-    O.train_bucket(model, i, j, hs, hr, hd, Cb, Ub, Sb, 0.1, 20190004)
-    ct = time.perf_counter() - c0
-    out["cpu_baseline"] = {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
-                           "sample": f"first 10 chunks ({m} edges) of the bucket, fp64, {ct:.1f} s"}
+            out.update(res)
+        print(f"# big bucket {key or 'fp32'}: {E / dt:.4g} edges/s", file=sys.stderr, flush=True)
+    if with_cpu:
+        # oracle: the first 10 chunks from the same initial state, partitions i and j only
+        m = 10 * Cb
+        model = O.Model(n, P, R, d, "diagonal", "dot", "ranking", 0.1)
+        model.emb = {i: emb_i0.cpu().numpy().astype(np.float64), j: emb_j0.cpu().numpy().astype(np.float64)}
+        model.G = {i: np.zeros(ps), j: np.zeros(ps)}
+        model.rel = np.ones((R, d))
+        model.relG = np.zeros((R, d))
+        hs, hr, hd = src[:m].cpu().numpy(), rel[:m].cpu().numpy(), dst[:m].cpu().numpy()
+        c0 = time.perf_counter()
+        O.train_bucket(model, i, j, hs, hr, hd, Cb, Ub, Sb, 0.1, 20190004)
+        ct = time.perf_counter() - c0
+        out["cpu_baseline"] = {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+                               **host_cpu(), "sample": f"first 10 chunks ({m} edges) of the bucket, fp64, "
+                                                       f"{ct:.1f} s"}
     return out
+
+
+def row_big_bucket():
+    return big_bucket_legs(with_cpu=True)
 
 
 def row_epoch():
@@ -591,9 +648,9 @@ def row_epoch():
             "partition_loads": st["partition_loads"], "copy_ms": st["copy_ms"],
             "compute_ms": sum(st[k] for k in ("gather_ms", "score_ms", "epilogue_ms", "backward_ms",
                                                "opbwd_ms", "update_ms")),
-            "roofline": roofline(st, PEAK_FP32_MFMA, "score contraction with the logistic epilogue", pieces=6),
+            "roofline": roofline(st, "score contraction with the logistic epilogue", pieces=SPLIT_PIECES),
             "phases_ms_per_step": phases(st),
-            "cpu_baseline": {"value": min(m, b00) / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+            "cpu_baseline": {"value": min(m, b00) / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle", **host_cpu(),
                              "sample": f"first {min(m, b00)} edges of bucket (0, 0), fp64, {ct:.1f} s"}}
 
 
@@ -631,7 +688,7 @@ def row_tiny():
                        "chunks_per_step": w.S},
             "note": "the 1.3 MB table stays in cache and a pass is 25 steps of ~30 small launches: "
                     "launch latency bound, no roofline figure",
-            "cpu_baseline": {"value": w.E / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle",
+            "cpu_baseline": {"value": w.E / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle", **host_cpu(),
                              "sample": f"full pass ({w.E} edges), fp64, {ct:.1f} s"}}
 
 

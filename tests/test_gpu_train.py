@@ -147,3 +147,33 @@ def test_out_of_range_ids_leave_parameters_untouched():
         assert pbg.pbg_train_bucket(gm.ctx, 0, 0, empty, empty, empty, 16, 8, 2, 0.1, 1) == 0.0
     finally:
         gm.close()
+
+
+@pytest.mark.parametrize("op,cmp,loss,d,R", [("diagonal", "dot", "logistic", 200, 4),
+                                             ("translation", "cos", "softmax", 160, 1)])
+def test_long_call_crosses_sort_windows(op, cmp, loss, d, R):
+    """One call of 70 steps: the sort keys of 32 steps are built and sorted
+    together, so the second and third windows (slices 1..31 of each) run;
+    d = 200 / 160 takes the row kernels with four floats a lane (gather,
+    operator backward, segment update).  Per-step losses and the final state
+    against the oracle at 1e-4 (smooth losses, no hinge kinks)."""
+    C, U, S = 24, 16, 2
+    m = 70 * S * C - 5                      # a short last chunk
+    pb = make_problem(op, cmp, loss, n=400, R=R, d=d, m=m, C=C, U=U, S=S, seed=61, sigma=0.2)
+    gm = GpuModel(pb)
+    try:
+        gl = gm.train()
+        from paper_1903_12287_amd import pbg
+        steps = pbg.pbg_get_step_losses(gm.ctx)
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol, osteps = O.train_bucket(om, 0, 0, pb.src, pb.rel_ids, pb.dst, C, U, S, pb.lr, pb.seed, return_steps=True)
+    assert len(steps) == len(osteps) == 70
+    for a, b in zip(steps, osteps):
+        assert abs(a - b) <= 1e-4 * max(1.0, abs(b)), (a, b)
+    err = float(np.max(np.abs(st["emb"][0] - om.emb[0])))
+    assert err <= 1e-4, err
+    gerr = float(np.max(np.abs(st["G"][0] - om.G[0]) / np.maximum(1.0, om.G[0])))
+    assert gerr <= 1e-4, gerr
