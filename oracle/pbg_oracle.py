@@ -30,6 +30,9 @@ with its reason, in the design notes of the repository):
   * complex layout is [re(0..h-1) | im(0..h-1)], h = d/2;
   * linear operator is g(x) = A x with A row-major d x d;
   * chunk c of a bucket holds edges [cC, min((c+1)C, m)); a step holds S chunks;
+    relation-grouped chunks (Sec. 4.3, batches sharing a relation type) cut
+    each relation's run of relation-sorted edges into chunks of C, the run's
+    last chunk holding the rest;
   * separate uniform negative sets per side, U each, also for the short last chunk;
   * only the induced positive (the diagonal t = e) is excluded from the
     in-chunk negatives;
@@ -340,6 +343,36 @@ def chunk_ranges(m: int, C: int):
     return [(c, c * C, min((c + 1) * C, m)) for c in range(-(-m // C))]
 
 
+def chunk_ranges_by_relation(rel, C: int):
+    """Relation-grouped chunks (Sec. 4.3: batches of edges that share their
+    relation type): the edges must be sorted by relation; each maximal run of
+    one relation is cut into chunks of C edges, the run's last chunk holding
+    the rest.  Chunks are numbered in edge order."""
+    rel = np.asarray(rel, dtype=np.int64)
+    if rel.size and np.any(rel[1:] < rel[:-1]):
+        raise ValueError("relation-grouped chunks need the edges sorted by relation")
+    out = []
+    lo = 0
+    while lo < rel.size:
+        hi = lo
+        while hi < rel.size and rel[hi] == rel[lo]:
+            hi += 1
+        for a in range(lo, hi, C):
+            out.append((len(out), a, min(a + C, hi)))
+        lo = hi
+    return out
+
+
+def make_chunks(m: int, C: int, rel, chunking: str):
+    """Chunks of a call: 'consecutive' (C edges each in the given order) or
+    'by_relation' (chunk_ranges_by_relation)."""
+    if chunking == "consecutive" or rel is None:
+        return chunk_ranges(m, C)
+    if chunking == "by_relation":
+        return chunk_ranges_by_relation(rel, C)
+    raise ValueError(chunking)
+
+
 def step_negatives(model: Model, i: int, j: int, step, seed: int, U: int, first_chunk: int = 0):
     """Uniform negatives (destination side, source side) of each chunk of a step."""
     b = i * model.P + j
@@ -350,7 +383,7 @@ def step_negatives(model: Model, i: int, j: int, step, seed: int, U: int, first_
 
 def train_bucket(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, S: int,
                  lr: float, seed: int, first_chunk: int = 0, return_steps: bool = False,
-                 branches=None):
+                 branches=None, chunking: str = "consecutive"):
     """One pass over the edges of bucket (i, j) in the given order.
 
     Chunk c (counted from `first_chunk`) holds edges [cC, min((c+1)C, m)) of the
@@ -360,13 +393,14 @@ def train_bucket(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, S:
     src/dst are local row ids in partitions i / j; rel may be None when R == 1.
     `branches` (ranking, one step only) gives per chunk of the step the pair
     (active dst side, active src side) of 0/1 arrays [C_c, C_c + U] that fix
-    the hinge branches (see side_loss).
+    the hinge branches (see side_loss).  chunking: 'consecutive' or
+    'by_relation' (make_chunks).
     Returns the summed loss (and the per-step losses)."""
     src = np.asarray(src, dtype=np.int64)
     dst = np.asarray(dst, dtype=np.int64)
     m = src.shape[0]
+    chunks = make_chunks(m, C, rel, chunking)
     rel = np.zeros(m, dtype=np.int64) if rel is None else np.asarray(rel, dtype=np.int64)
-    chunks = chunk_ranges(m, C)
     if branches is not None and len(chunks) > S:
         raise ValueError("hinge branches can be given for one step only")
     step_losses = []
@@ -456,7 +490,7 @@ def adagrad_update(model: Model, grads, rel_grad, lr: float):
 
 
 def inspect_step(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, seed: int,
-                 first_chunk: int = 0):
+                 first_chunk: int = 0, chunking: str = "consecutive"):
     """The forward half of one step on these edges (all chunks of the call),
     at the current parameters: for each chunk a dict with
       p      (C_c,)           positive scores f(s_e, r_e, d_e)
@@ -469,8 +503,8 @@ def inspect_step(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, se
     src = np.asarray(src, dtype=np.int64)
     dst = np.asarray(dst, dtype=np.int64)
     m = src.shape[0]
+    step = make_chunks(m, C, rel, chunking)
     rel = np.zeros(m, dtype=np.int64) if rel is None else np.asarray(rel, dtype=np.int64)
-    step = chunk_ranges(m, C)
     negs = step_negatives(model, i, j, step, seed, U, first_chunk)
     theta_all = None if model.rel is None else torch.tensor(model.rel, dtype=_F64)
     out = []
@@ -500,7 +534,7 @@ def inspect_step(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, se
     return out
 
 
-def train_epoch(model: Model, offsets, src_local, rel, dst_local, C, U, S, lr, seed):
+def train_epoch(model: Model, offsets, src_local, rel, dst_local, C, U, S, lr, seed, chunking="consecutive"):
     """One epoch: every bucket with edges, in inside-out order (Sec. 4.1)."""
     P = model.P
     total = 0.0
@@ -511,7 +545,7 @@ def train_epoch(model: Model, offsets, src_local, rel, dst_local, C, U, S, lr, s
             continue
         r = None if rel is None else rel[lo:hi]
         total += train_bucket(model, i, j, src_local[lo:hi], r, dst_local[lo:hi],
-                              C, U, S, lr, seed)
+                              C, U, S, lr, seed, chunking=chunking)
     return total
 
 

@@ -755,3 +755,50 @@ def test_inspect_step_positive_gradient_closed_form():
                         z = sum(math.exp(v) for v in vals)
                         want += math.exp(p[e]) / z - 1.0
                 assert abs(rec["dp"][e] - want) < 1e-12
+
+
+# ----------------------------------------------- relation-grouped chunks (O3)
+def test_relation_grouped_chunks_brute_force():
+    """Every chunk holds one relation and at most C edges, chunks cover the
+    edges in order, and only the last chunk of each relation's run is short;
+    unsorted relations are refused."""
+    rng = np.random.default_rng(3)
+    for C in (1, 3, 7):
+        rel = np.sort(rng.integers(0, 6, 50))
+        ch = O.chunk_ranges_by_relation(rel, C)
+        assert [c for c, _, _ in ch] == list(range(len(ch)))
+        pos = 0
+        for k, (c, lo, hi) in enumerate(ch):
+            assert lo == pos and 0 < hi - lo <= C
+            assert len(set(rel[lo:hi].tolist())) == 1
+            run_continues = hi < len(rel) and rel[hi] == rel[lo]
+            if hi - lo < C:
+                assert not run_continues
+            pos = hi
+        assert pos == len(rel)
+        # the number of chunks is the sum over runs of ceil(run / C)
+        _, counts = np.unique(rel, return_counts=True)
+        assert len(ch) == sum(-(-int(n) // C) for n in counts)
+    with pytest.raises(ValueError):
+        O.chunk_ranges_by_relation(np.array([0, 2, 1]), 4)
+    # one relation: the same chunks as consecutive chunking
+    assert O.chunk_ranges_by_relation(np.zeros(10, int), 4) == O.chunk_ranges(10, 4)
+
+
+def test_relation_grouped_training_matches_explicit_chunks():
+    """train_bucket with grouped chunking equals training the chunks one call
+    per chunk with consecutive chunking and the right chunk numbers (S = 1),
+    so the grouping only moves chunk boundaries."""
+    model = _tiny_model("diagonal", "cos", "softmax", n=11, P=1, R=3, d=4, seed=6, scale=0.6)
+    rng = np.random.default_rng(8)
+    m = 13
+    rel = np.sort(rng.integers(0, 3, m))
+    src, dst = rng.integers(0, 11, m), rng.integers(0, 11, m)
+    a = O.Model.create(11, 1, 3, 4, "diagonal", "cos", "softmax", 0.1, [model.emb[0].copy()], model.rel.copy())
+    b = O.Model.create(11, 1, 3, 4, "diagonal", "cos", "softmax", 0.1, [model.emb[0].copy()], model.rel.copy())
+    la = O.train_bucket(a, 0, 0, src, rel, dst, 3, 2, 1, 0.1, 5, chunking="by_relation")
+    lb = 0.0
+    for c, lo, hi in O.chunk_ranges_by_relation(rel, 3):
+        lb += O.train_bucket(b, 0, 0, src[lo:hi], rel[lo:hi], dst[lo:hi], 3, 2, 1, 0.1, 5, first_chunk=c)
+    assert abs(la - lb) < 1e-12
+    assert np.allclose(a.emb[0], b.emb[0], atol=1e-15, rtol=0) and np.allclose(a.rel, b.rel, atol=1e-15, rtol=0)
