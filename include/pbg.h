@@ -86,20 +86,33 @@ enum { PBG_MEM_DEVICE = 0, PBG_MEM_PINNED_HOST = 1 };
 
 typedef struct pbg_ctx pbg_ctx;
 
-/* Batched negatives (Sec. 4.3, Fig. 3).  Chunk c of a bucket holds edges
- * [c*chunk_size, min((c+1)*chunk_size, n_edges)) in the given order; every edge
- * of a chunk is scored against the chunk's other edges' entities plus
- * num_uniform entities drawn uniformly (separately per side) from the
- * partition of the corrupted side; the induced positive is excluded.  A step
- * of chunks_per_step chunks takes its gradient at the step-start parameters
- * and applies one Adagrad update.  first_chunk numbers the first chunk of the
- * call, so that a bucket may be trained in several calls with the same
- * negatives as one call (the uniform draws are keyed by chunk number). */
+/* Chunking of a call's edges (Sec. 4.3).
+ *  CONSECUTIVE  chunk c holds edges [c*chunk_size, min((c+1)*chunk_size, n_edges))
+ *               in the given order (relations may mix within a chunk);
+ *  BY_RELATION  the edges must be sorted by relation (nondecreasing; e.g. by
+ *               pbg_group_by_relation), and each relation's run of edges is
+ *               cut into chunks of chunk_size, its last chunk holding the rest,
+ *               so that every chunk holds one relation (Sec. 4.3: batches of
+ *               edges that share their relation type).  With one relation the
+ *               two are the same.  The cos comparator with an operator and
+ *               several relations needs it (every source candidate of a chunk
+ *               takes the operator of the chunk's relation). */
+enum { PBG_CHUNK_CONSECUTIVE = 0, PBG_CHUNK_BY_RELATION = 1 };
+
+/* Batched negatives (Sec. 4.3, Fig. 3).  The call's edges are cut into chunks
+ * (see chunking); every edge of a chunk is scored against the chunk's other
+ * edges' entities plus num_uniform entities drawn uniformly (separately per
+ * side) from the partition of the corrupted side; the induced positive is
+ * excluded.  A step of chunks_per_step consecutive chunks takes its gradient
+ * at the step-start parameters and applies one Adagrad update.  first_chunk
+ * numbers the first chunk of the call, so that a bucket may be trained in
+ * several calls with the same negatives as one call (the uniform draws are
+ * keyed by chunk number). */
 typedef struct {
   int32_t chunk_size;       /* >= 1 */
   int32_t num_uniform;      /* >= 0; chunk_size + num_uniform >= 2 */
   int32_t chunks_per_step;  /* >= 1 (40 matches the paper's 40 training threads) */
-  int32_t reserved;         /* must be 0 */
+  int32_t chunking;         /* PBG_CHUNK_CONSECUTIVE or PBG_CHUNK_BY_RELATION */
   int64_t first_chunk;      /* >= 0 */
 } pbg_neg_config;
 
@@ -131,10 +144,13 @@ typedef struct {
  * remainder (Sec. 4.1), num_relations relations, embedding dimension dim.
  * Returns INVALID_ARG for unknown enums, dim < 1 or dim > 512, odd dim with
  * COMPLEX_DIAGONAL, P < 1, a partition left empty, num_relations < 1 or a
- * non-finite margin; UNSUPPORTED for COS with a non-identity operator and more
- * than one relation (the source corruptions of an edge would need the
- * operator of its own relation applied to every candidate before the
- * normalisation, which is no longer one product per chunk). */
+ * non-finite margin; UNSUPPORTED for COS with the LINEAR operator and more
+ * than one relation.  COS with another operator and several relations is
+ * trained with relation-grouped chunks only (PBG_CHUNK_BY_RELATION; with
+ * consecutive chunks the training calls return UNSUPPORTED: the source
+ * corruptions of an edge need its own relation's operator applied to every
+ * candidate before the normalisation), and pbg_rank_eval / pbg_rank_sampled
+ * return UNSUPPORTED for it. */
 pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_partitions,
                            int32_t num_relations, int32_t dim, int32_t op, int32_t cmp,
                            int32_t loss, float margin, uint32_t flags);
@@ -208,6 +224,14 @@ pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* s
                             const pbg_neg_config* neg, float lr, uint64_t seed,
                             double* loss_host);
 
+/* Relation-grouped order of a bucket's edges (Sec. 4.3): writes the n edges
+ * (src, rel, dst: device int32) stably sorted by relation to src_out,
+ * rel_out, dst_out (device int32, not overlapping the inputs), the order that
+ * PBG_CHUNK_BY_RELATION takes.  Relations outside [0, R) give INVALID_ARG with
+ * nothing written. */
+pbg_status pbg_group_by_relation(pbg_ctx* ctx, const int32_t* src, const int32_t* rel, const int32_t* dst,
+                                 int64_t n, int32_t* src_out, int32_t* rel_out, int32_t* dst_out);
+
 /* Per-step losses of the last pbg_train_bucket call: copies
  * min(capacity, steps) values to out_host and the step count to n_steps_host. */
 pbg_status pbg_get_step_losses(const pbg_ctx* ctx, double* out_host, int64_t capacity,
@@ -278,7 +302,8 @@ pbg_status pbg_sample_negatives(pbg_ctx* ctx, int32_t i, int32_t j, int64_t firs
  * Sec. 4.3 batched negatives) -- with the same kernels and launch sequence as
  * pbg_train_bucket, then copies out what they computed.  No parameter or
  * accumulator is modified; arguments and ids are checked as for
- * pbg_train_bucket.  With nch = ceil(n_edges / chunk_size), N = chunk_size +
+ * pbg_train_bucket.  With nch the number of chunks of the call (at most
+ * chunks_per_step; ceil(n_edges / chunk_size) for consecutive chunks), N = chunk_size +
  * num_uniform, Cc the edges of chunk c and candidates t = the chunk's Cc
  * in-chunk entities followed by its num_uniform draws, every output is a
  * nullable device float32 array whose entries outside [Cc] x [Cc + U] are 0:

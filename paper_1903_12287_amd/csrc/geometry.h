@@ -49,11 +49,21 @@ struct StepGeom {
   uint32_t bucket;  // i*P + j
   uint64_t seed;
   int64_t chunk0;   // chunk number (within the bucket) of the step's first chunk
+  const int32_t* cstart;  // relation-grouped chunks: bounds of the step's chunks (device), else NULL
 };
 
+// Chunk c of a step: its edge count and the offset of its first edge in the
+// step's edge arrays.  Consecutive chunks hold C edges each (the step's last
+// one may be short); relation-grouped chunks have their bounds in cstart
+// (offsets in the call's edge arrays, cstart[c + 1] the end of chunk c).
 __host__ __device__ inline int chunk_edges(const StepGeom& g, int c) {
+  if (g.cstart) return g.cstart[c + 1] - g.cstart[c];
   const int r = g.m_step - c * g.C;
   return r < g.C ? r : g.C;
+}
+
+__host__ __device__ inline int chunk_first(const StepGeom& g, int c) {
+  return g.cstart ? g.cstart[c] - g.cstart[0] : c * g.C;
 }
 
 struct StepBufs {

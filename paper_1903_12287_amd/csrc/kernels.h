@@ -24,6 +24,7 @@ struct GemmArgs {
   int mdim, ndim, kdim;  // DIM_* selectors
   int Mfix, Nfix, Kfix;
   int C, U, m_step;      // chunk geometry (m_step = 0: not chunked)
+  const int32_t* cstart; // relation-grouped chunks: chunk c holds cstart[c + 1] - cstart[c] edges
   int nsides;            // batches per chunk
   int accumulate;        // add to C instead of overwriting it
 };
@@ -60,6 +61,7 @@ struct GemmArgsH {
   int mdim, ndim, kdim;
   int Mfix, Nfix, Kfix;
   int C, U, m_step;
+  const int32_t* cstart;
   int nsides;
   const float* pos;
   const float* bias;
@@ -105,10 +107,14 @@ void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s);
 // sort keys and values of the contribution rows of a window of nsteps steps
 // of S chunks ([step][stride], compact per step), and relation keys
-// ([step][S * C]) when rkeys is set
+// ([step][rstride], compact per step) when rkeys is set: the edges' relations,
+// then with uniform_rel the chunk's relation of every uniform source
+// candidate.  Chunks consecutive (cstart NULL) or relation-grouped (bounds
+// cstart[0 .. nchunks] of the window's chunks, offsets in the call's arrays)
 void launch_window_keys(const StepGeom& g, const int32_t* src, const int32_t* dst, const int32_t* rel,
-                        int64_t n_edges, int64_t chunk0, int S, int nsteps, int64_t stride, uint32_t* keys,
-                        uint32_t* vals, uint32_t* rkeys, uint32_t* rvals, hipStream_t s);
+                        int64_t n_edges, const int32_t* cstart, int nchunks, int64_t chunk0, int S, int nsteps,
+                        int64_t stride, uint32_t* keys, uint32_t* vals, uint32_t* rkeys, uint32_t* rvals,
+                        int64_t rstride, int uniform_rel, hipStream_t s);
 void launch_transpose_rel(const float* A, float* AT, int R, int d, hipStream_t s);
 // linear operator (one relation): padded copies of A and A^T, and the positive
 // scores once Q has been formed by contraction
@@ -211,8 +217,10 @@ void launch_bucket_gather(const uint32_t* vals, const int64_t* src, const int32_
                           int32_t* rel_out, int32_t* dst_local, hipStream_t s);
 
 // ---- filtered ranks (Sec. 5.4) -------------------------------------------------
-void launch_rank_tables(const StepGeom& g, const float* emb, const float* relp, int64_t n_ent, float* T0,
-                        float* T1, hipStream_t s);
+// T0: every entity row (unit rows for cos); T1 (cos with an operator, one
+// relation): the unit rows of g(x) (relT: the linear operator's A^T rows)
+void launch_rank_tables(const StepGeom& g, const float* emb, const float* relp, const float* relT, int64_t n_ent,
+                        float* T0, float* T1, hipStream_t s);
 void launch_rank_queries(const StepGeom& g, const float* emb, const float* relp, const float* relT,
                          const int32_t* src, const int32_t* rel, const int32_t* dst, int64_t e0, int rows,
                          int side, float* Q, float* pos, float* bias, hipStream_t s);

@@ -144,9 +144,10 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
   if (item < Cc) {
     const int e = item;
     const int64_t ce = (int64_t)c * g.C + e;
-    const int s = b.src[ce];
-    const int t = b.dst[ce];
-    const int r = b.rel ? b.rel[ce] : 0;
+    const int64_t eg = chunk_first(g, c) + e;   // in the step's edge arrays
+    const int s = b.src[eg];
+    const int t = b.dst[eg];
+    const int r = b.rel ? b.rel[eg] : 0;
     Row th;
     if (has_rel && g.op != OP_LINEAR) row_load(th, b.relp + (int64_t)r * g.dr, d, cplx, lane);
     else row_zero(th);
@@ -263,7 +264,9 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     // as a contraction, the gradient of A too)
     const bool lin_side = side == 1 && g.op == OP_LINEAR;
     const bool op_side = side == 1 && has_rel && !lin_side;
-    if (op_side) row_load(th, b.relp, d, cplx, lane);
+    // the chunk's relation (one relation, or relation-grouped chunks)
+    const int rc = (op_side && b.rel && Cc > 0) ? b.rel[chunk_first(g, c)] : 0;
+    if (op_side) row_load(th, b.relp + (int64_t)rc * g.dr, d, cplx, lane);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (q >= nq) break;

@@ -31,7 +31,7 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   if (item < Cc) {
     // ---- edge item
     const int e = item;
-    const int64_t eg = (int64_t)c * g.C + e;
+    const int64_t eg = chunk_first(g, c) + e;   // in the step's edge arrays
     const int s = b.src[eg];
     const int t = b.dst[eg];
     const int r = b.rel ? b.rel[eg] : 0;
@@ -120,9 +120,11 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   const bool unit = g.cmp == CMP_COS && !raw_linear;
   if (unit) {
     if (side == 1 && g.op != OP_IDENTITY) {
-      // one relation: its operator is applied to every source candidate
+      // the chunk's relation (one relation, or relation-grouped chunks): its
+      // operator is applied to every source candidate
+      const int rc = (b.rel && Cc > 0) ? b.rel[chunk_first(g, c)] : 0;
       Row th;
-      row_load(th, b.relp, d, cplx, lane);
+      row_load(th, b.relp + (int64_t)rc * g.dr, d, cplx, lane);
 #pragma unroll
       for (int q = 0; q < 4; ++q) v[q] = op_forward(g.op, v[q], th);
     }
@@ -146,37 +148,55 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
 
 // Sort keys of a window of steps, from the edges and the negative draws
 // alone (so that the sorts of a whole window run as one batch before its
-// steps): for chunk c of step w the compact key block [side 0: Nc][side 1:
-// Nc] at w * stride + c * 2N holds (table, row) of the row each contribution
+// steps).  The key block of chunk c of step w starts at w * stride +
+// 2 (c U + f_c), f_c the offset of the chunk's first edge in its step, and
+// holds [side 0: Nc][side 1: Nc]: (table, row) of the row each contribution
 // row reaches and, as value, that contribution row's position in the step;
 // edge e: destination t (side 0) and source s (side 1), then the uniform
 // draws of each side.  With several relations the relation of every edge is
-// keyed too ([w][S][C]).  One thread per edge or per four draws; src / dst /
-// rel start at the window's first edge, n_edges edges, chunk0 is the
-// window's first chunk (for the draws).
+// keyed too (at w * rstride + f_c + e, value c N + e), and, with
+// uniform_rel, the chunk's relation for each uniform source candidate (the
+// cos comparator with an operator applies it there; at w * rstride + m_w +
+// c U + k, m_w the step's edge count, value c N + C + k).  One thread per
+// edge or per four draws; src / dst / rel start at the window's first edge.
+// Chunks: consecutive (cstart NULL: n_edges edges) or relation-grouped
+// (bounds cstart[0 .. nchunks], offsets in the call's edge arrays).
 __global__ __launch_bounds__(256) void window_keys_kernel(StepGeom g, const int32_t* src, const int32_t* dst,
-                                                          const int32_t* rel, int64_t n_edges, int64_t chunk0,
+                                                          const int32_t* rel, int64_t n_edges,
+                                                          const int32_t* cstart, int nchunks, int64_t chunk0,
                                                           int S, int64_t stride, uint32_t* keys, uint32_t* vals,
-                                                          uint32_t* rkeys, uint32_t* rvals) {
+                                                          uint32_t* rkeys, uint32_t* rvals, int64_t rstride,
+                                                          int uniform_rel) {
   const int c = blockIdx.y, w = blockIdx.z;
   const int64_t cw = (int64_t)w * S + c;   // chunk within the window
-  const int64_t left = n_edges - cw * g.C;
-  if (left <= 0) return;
-  const int Cc = (int)std::min<int64_t>(g.C, left);
+  int Cc, first;
+  int64_t e0;                              // first edge of the chunk in the window's arrays
+  if (cstart) {
+    if (cw >= nchunks) return;
+    Cc = cstart[cw + 1] - cstart[cw];
+    e0 = cstart[cw] - cstart[0];
+    first = cstart[cw] - cstart[(int64_t)w * S];
+  } else {
+    const int64_t left = n_edges - cw * g.C;
+    if (left <= 0) return;
+    Cc = (int)std::min<int64_t>(g.C, left);
+    e0 = cw * g.C;
+    first = c * g.C;
+  }
   const int Nc = Cc + g.U;
   const int ng = (g.U + 3) >> 2;
   const int item = blockIdx.x * 256 + threadIdx.x;
   const uint32_t tbl_j = g.same_table ? 0u : 1u;
-  const int64_t kbase = w * stride + (int64_t)c * 2 * g.N;
+  const int64_t kbase = w * stride + 2 * ((int64_t)c * g.U + first);
   if (item < Cc) {
     const int e = item;
-    const int64_t eg = cw * g.C + e;
+    const int64_t eg = e0 + e;
     keys[kbase + e] = (tbl_j << g.rb) | (uint32_t)dst[eg];
     vals[kbase + e] = (uint32_t)((c * 2 + 0) * g.N + e);
     keys[kbase + Nc + e] = (uint32_t)src[eg];
     vals[kbase + Nc + e] = (uint32_t)((c * 2 + 1) * g.N + e);
     if (rkeys) {
-      const int64_t rw = (int64_t)w * S * g.C + (int64_t)c * g.C + e;
+      const int64_t rw = (int64_t)w * rstride + first + e;
       rkeys[rw] = (uint32_t)(rel ? rel[eg] : 0);
       rvals[rw] = (uint32_t)((int64_t)c * g.N + e);
     }
@@ -189,6 +209,14 @@ __global__ __launch_bounds__(256) void window_keys_kernel(StepGeom g, const int3
   const uint32_t rows = side == 0 ? (uint32_t)g.rows_j : (uint32_t)g.rows_i;
   int32_t u[4];
   uniform_negatives4(g.seed, g.bucket, (uint64_t)(chunk0 + cw), (uint32_t)side, (uint32_t)k0, rows, u);
+  int64_t m_w = 0;
+  uint32_t r_c = 0;
+  if (uniform_rel && side == 1) {
+    const int64_t w0 = (int64_t)w * S;
+    const int64_t w1 = std::min<int64_t>(w0 + S, nchunks);
+    m_w = cstart[w1] - cstart[w0];
+    r_c = (uint32_t)rel[e0];
+  }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int k = k0 + q;
@@ -196,6 +224,11 @@ __global__ __launch_bounds__(256) void window_keys_kernel(StepGeom g, const int3
     const int t = Cc + k;
     keys[kbase + side * Nc + t] = side == 0 ? ((tbl_j << g.rb) | (uint32_t)u[q]) : (uint32_t)u[q];
     vals[kbase + side * Nc + t] = (uint32_t)((c * 2 + side) * g.N + t);
+    if (uniform_rel && side == 1) {
+      const int64_t rw = (int64_t)w * rstride + m_w + (int64_t)c * g.U + k;
+      rkeys[rw] = r_c;
+      rvals[rw] = (uint32_t)((int64_t)c * g.N + g.C + k);
+    }
   }
 }
 
@@ -238,11 +271,13 @@ __global__ void transpose_rel_kernel(const float* A, float* AT, int R, int d) {
 }  // namespace
 
 void launch_window_keys(const StepGeom& g, const int32_t* src, const int32_t* dst, const int32_t* rel,
-                        int64_t n_edges, int64_t chunk0, int S, int nsteps, int64_t stride, uint32_t* keys,
-                        uint32_t* vals, uint32_t* rkeys, uint32_t* rvals, hipStream_t s) {
+                        int64_t n_edges, const int32_t* cstart, int nchunks, int64_t chunk0, int S, int nsteps,
+                        int64_t stride, uint32_t* keys, uint32_t* vals, uint32_t* rkeys, uint32_t* rvals,
+                        int64_t rstride, int uniform_rel, hipStream_t s) {
   if (nsteps <= 0 || n_edges <= 0) return;
   dim3 grid((g.C + 2 * ((g.U + 3) / 4) + 255) / 256, S, nsteps);
-  window_keys_kernel<<<grid, 256, 0, s>>>(g, src, dst, rel, n_edges, chunk0, S, stride, keys, vals, rkeys, rvals);
+  window_keys_kernel<<<grid, 256, 0, s>>>(g, src, dst, rel, n_edges, cstart, nchunks, chunk0, S, stride, keys, vals,
+                                          rkeys, rvals, rstride, uniform_rel);
 }
 
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s) {

@@ -118,7 +118,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int tiles_n, 
   const int c = z / a.nsides;
   const int side = z - c * a.nsides;
   int Cc = a.C, Nc = a.C + a.U;
-  if (a.m_step > 0) {
+  if (a.cstart) {
+    Cc = a.cstart[c + 1] - a.cstart[c];
+    Nc = Cc + a.U;
+  } else if (a.m_step > 0) {
     Cc = min(a.C, a.m_step - c * a.C);
     Nc = Cc + a.U;
   }

@@ -204,7 +204,10 @@ __device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int ti
   t.side = z - t.c * a.nsides;
   int Cc = a.C;
   t.Nc = a.C + a.U;
-  if (a.m_step > 0) {
+  if (a.cstart) {
+    Cc = a.cstart[t.c + 1] - a.cstart[t.c];
+    t.Nc = Cc + a.U;
+  } else if (a.m_step > 0) {
     Cc = min(a.C, a.m_step - t.c * a.C);
     t.Nc = Cc + a.U;
   }

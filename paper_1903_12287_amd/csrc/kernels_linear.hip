@@ -29,7 +29,7 @@ __global__ __launch_bounds__(256) void linear_rows_kernel(StepGeom g, StepBufs b
   if (e >= chunk_edges(g, c)) return;   // no block-level barriers below
   const int d = g.d, dp = g.dp;
   const int64_t ce = (int64_t)c * g.C + e;
-  const float* A = b.relp + (int64_t)b.rel[ce] * d * d;
+  const float* A = b.relp + (int64_t)b.rel[chunk_first(g, c) + e] * d * d;
   RowQ x, y, q, k;
   row_load(x, b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp, d, false, lane);   // raw x_s
   row_load(y, b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp, d, false, lane);   // raw x_d
@@ -51,7 +51,7 @@ __global__ __launch_bounds__(256) void linear_rows_backward_kernel(StepGeom g, S
   if (e >= chunk_edges(g, c)) return;
   const int d = g.d, dp = g.dp;
   const int64_t ce = (int64_t)c * g.C + e;
-  const float* A = b.relp + (int64_t)b.rel[ce] * d * d;
+  const float* A = b.relp + (int64_t)b.rel[chunk_first(g, c) + e] * d * d;
   // the operator backward left dQ (with the positive score's term) in dq
   // side 0 and dK in dq side 1
   RowQ dQ, dK, ts, td;

@@ -25,7 +25,8 @@ namespace {
 
 // candidate tables: one wave per entity row
 __global__ __launch_bounds__(256) void rank_tables_kernel(StepGeom g, const float* emb, const float* relp,
-                                                          int64_t n_ent, float* T0, float* T1) {
+                                                          const float* relT, int64_t n_ent, float* T0, float* T1) {
+  __shared__ float stage[4][512];
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n_ent) return;
@@ -41,9 +42,14 @@ __global__ __launch_bounds__(256) void rank_tables_kernel(StepGeom g, const floa
   row_store(xh, T0 + row * g.dp, g.d, g.dp, cplx, lane);
   if (T1) {
     // cos with a non-identity operator: one relation, applied to every source candidate
-    Row th;
-    row_load(th, relp, g.d, cplx, lane);
-    Row gx = op_forward(g.op, x, th);
+    Row gx;
+    if (g.op == OP_LINEAR) {
+      mat_apply(gx, relT, x, stage[threadIdx.x >> 6], g.d, lane);   // A x
+    } else {
+      Row th;
+      row_load(th, relp, g.d, cplx, lane);
+      gx = op_forward(g.op, x, th);
+    }
     row_normalize(gx);
     row_store(gx, T1 + row * g.dp, g.d, g.dp, cplx, lane);
   }
@@ -216,10 +222,10 @@ int grid_of(int64_t n) {
 
 }  // namespace
 
-void launch_rank_tables(const StepGeom& g, const float* emb, const float* relp, int64_t n_ent, float* T0,
-                        float* T1, hipStream_t s) {
+void launch_rank_tables(const StepGeom& g, const float* emb, const float* relp, const float* relT, int64_t n_ent,
+                        float* T0, float* T1, hipStream_t s) {
   if (n_ent <= 0) return;
-  rank_tables_kernel<<<(unsigned)((n_ent + 3) / 4), 256, 0, s>>>(g, emb, relp, n_ent, T0, T1);
+  rank_tables_kernel<<<(unsigned)((n_ent + 3) / 4), 256, 0, s>>>(g, emb, relp, relT, n_ent, T0, T1);
 }
 
 void launch_rank_queries(const StepGeom& g, const float* emb, const float* relp, const float* relT,

@@ -54,6 +54,7 @@ static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t*
   qa.C = C;
   qa.U = g.U;
   qa.m_step = g.m_step;
+  qa.cstart = g.cstart;
   qa.nsides = 2;
   // dN = dS^T . Q:  A = dS read by columns, B = Q^T [f][e]
   GemmArgsH na = qa;
@@ -106,6 +107,7 @@ static GemmArgsH score_args_f32(const StepGeom& g, const StepBufs& b, int* epi_o
   fa.C = C;
   fa.U = U;
   fa.m_step = g.m_step;
+  fa.cstart = g.cstart;
   fa.nsides = 2;
   fa.pos = b.pos;
   fa.bias = (g.op == OP_TRANSLATION && g.cmp == CMP_DOT) ? b.bias : nullptr;
@@ -188,6 +190,7 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   qa.C = C;
   qa.U = U;
   qa.m_step = g.m_step;
+  qa.cstart = g.cstart;
   qa.nsides = 2;
   GemmArgsH na = qa;
   if (qn) {
@@ -242,6 +245,7 @@ static GemmArgsH score_args_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs
   fa.C = C;
   fa.U = U;
   fa.m_step = g.m_step;
+  fa.cstart = g.cstart;
   fa.nsides = 2;
   fa.pos = b.pos;
   fa.bias = (g.op == OP_TRANSLATION && g.cmp == CMP_DOT) ? b.bias : nullptr;
@@ -328,6 +332,7 @@ static GemmArgs linear_args(const StepGeom& g, const float* A, int64_t a_cs, con
   la.C = g.C;
   la.U = g.U;
   la.m_step = g.m_step;
+  la.cstart = g.cstart;
   la.nsides = 1;
   return la;
 }
@@ -389,6 +394,7 @@ int run_linear_relation_grad(const StepGeom& g, const StepBufs& b, float* partia
   la.C = C;
   la.U = g.U;
   la.m_step = g.m_step;
+  la.cstart = g.cstart;
   la.nsides = 1;
   la.Cm = partial;
   if (g.cmp == CMP_COS) {

@@ -234,6 +234,17 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
     if (!ctx->parts[p].emb || ctx->parts[p].where != PBG_MEM_PINNED_HOST)
       return set_err(ctx, PBG_ERR_STATE, "partition %d must be bound in page-locked host memory", p);
   if (ctx->op != OP_IDENTITY && !ctx->relp) return set_err(ctx, PBG_ERR_STATE, "relation parameters are not bound");
+  if (chunk_relation_operator(ctx) && !grouped_chunks(ctx, neg))
+    return set_err(ctx, PBG_ERR_UNSUPPORTED,
+                   "cos with an operator and several relations needs relation-grouped chunks (PBG_CHUNK_BY_RELATION)");
+  if (grouped_chunks(ctx, neg) && rel_host) {
+    // every bucket's edges sorted by relation, checked before anything trains
+    for (int b = 0; b < nb; ++b)
+      for (int64_t k = offsets_host[b] + 1; k < offsets_host[b + 1]; ++k)
+        if (rel_host[k] < rel_host[k - 1])
+          return set_err(ctx, PBG_ERR_INVALID_ARG,
+                         "relation-grouped chunks need each bucket's edges sorted by relation (bucket %d)", b);
+  }
 
   ctx->stats = pbg_stats();
   ctx->step_losses.clear();

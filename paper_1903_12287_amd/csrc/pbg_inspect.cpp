@@ -23,11 +23,16 @@ extern "C" pbg_status pbg_inspect_step(pbg_ctx* ctx, int32_t i, int32_t j, const
   pbg_status st = check_bucket_call(ctx, i, j, src_local, rel, dst_local, n_edges, neg);
   if (st != PBG_OK) return st;
   const int C = neg->chunk_size, U = neg->num_uniform, S = neg->chunks_per_step;
-  if (n_edges > (int64_t)C * S)
-    return set_err(ctx, PBG_ERR_INVALID_ARG, "pbg_inspect_step takes at most one step (%lld edges)",
-                   (long long)C * S);
   if (loss_host) *loss_host = 0.0;
   if (n_edges == 0) return PBG_OK;
+  const bool grouped = grouped_chunks(ctx, neg);
+  if (grouped) {
+    st = relation_chunk_bounds(ctx, rel, n_edges, C);
+    if (st != PBG_OK) return st;
+  }
+  const int64_t nchunks = grouped ? (int64_t)ctx->cstart_host.size() - 1 : (n_edges + C - 1) / C;
+  if (nchunks > S)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "pbg_inspect_step takes at most one step (%d chunks)", S);
   st = ensure_steploss(ctx, 1);
   if (st != PBG_OK) return st;
 
@@ -37,10 +42,11 @@ extern "C" pbg_status pbg_inspect_step(pbg_ctx* ctx, int32_t i, int32_t j, const
   StepGeom g;
   bucket_geom(ctx, i, j, C, U, seed, g);
   StepBufs b = bucket_bufs(ctx, pi.emb, pi.G, pj.emb, pj.G);
-  const int nch = (int)((n_edges + C - 1) / C);
+  const int nch = (int)nchunks;
   g.nchunks = nch;
   g.m_step = (int)n_edges;
   g.chunk0 = neg->first_chunk;
+  g.cstart = grouped ? ctx->cstart_dev : nullptr;
   b.src = src_local;
   b.dst = dst_local;
   b.rel = rel;

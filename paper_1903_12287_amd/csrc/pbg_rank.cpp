@@ -71,6 +71,8 @@ pbg_status rank_impl(pbg_ctx* ctx, const char* name, const int32_t* src, const i
   if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
   ctx->err.clear();
   if (ctx->P != 1) return set_err(ctx, PBG_ERR_UNSUPPORTED, "%s needs a single partition", name);
+  if (ctx->cmp == CMP_COS && ctx->op != OP_IDENTITY && ctx->R > 1)
+    return set_err(ctx, PBG_ERR_UNSUPPORTED, "%s: cos with an operator needs a single relation", name);
   if (n < 0 || n > 0x3FFFFFFFll || n_known < 0 || n_known > 0x7FFFFFFFll)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "n or n_known out of range");
   if (cand && (n_cand <= 0 || n_cand > 0x7FFFFFFFll))
@@ -152,7 +154,7 @@ pbg_status rank_impl(pbg_ctx* ctx, const char* name, const int32_t* src, const i
   g.op = ctx->op;
   g.cmp = ctx->cmp;
   if (linear) launch_transpose_rel(ctx->relp, relT, ctx->R, d, s);
-  launch_rank_tables(g, pt.emb, ctx->relp, n_ent, T0, T1, s);
+  launch_rank_tables(g, pt.emb, ctx->relp, relT, n_ent, T0, T1, s);
   if (cand) {
     // the candidates' rows of the tables, in candidate order
     launch_gather_rows(T0, cand, n_cand, dp, C0, s);

@@ -119,8 +119,11 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   ctx->wvals_alt = (uint32_t*)a.get(kSortWindow * nkeys * 4);
   ctx->whist = (uint32_t*)a.get(radix_segments_hist_entries(nkeys, kSortWindow) * 4);
   if (has_rel && ctx->R > 1) {
-    b.rkeys = (uint32_t*)a.get(kSortWindow * s * C * 4);
-    b.rvals = (uint32_t*)a.get(kSortWindow * s * C * 4);
+    // the edges' relations, then (cos with an operator) the chunk relation of
+    // every uniform source candidate
+    const int64_t per = s * (C + (chunk_relation_operator(ctx) ? U : 0));
+    b.rkeys = (uint32_t*)a.get(kSortWindow * per * 4);
+    b.rvals = (uint32_t*)a.get(kSortWindow * per * 4);
   }
   const int width = std::max(d, has_rel && !linear ? ctx->dr : 0);
   if (!alloc_sortwork(a, ctx->sw, std::max<int64_t>(nkeys, s * C), width)) {
@@ -232,6 +235,42 @@ pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps) {
   return PBG_OK;
 }
 
+pbg_status relation_chunk_bounds(pbg_ctx* ctx, const int32_t* rel, int64_t n, int C) {
+  std::vector<int32_t> r((size_t)n);
+  hipError_t e = hipMemcpyAsync(r.data(), rel, (size_t)n * 4, hipMemcpyDeviceToHost, ctx->cs);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->cs);
+  if (e != hipSuccess) return hip_fail(ctx, e, "relation copy");
+  std::vector<int32_t>& cs = ctx->cstart_host;
+  cs.clear();
+  int64_t run0 = 0;
+  for (int64_t k = 0; k <= n; ++k) {
+    if (k < n && k > 0 && r[k] < r[k - 1])
+      return set_err(ctx, PBG_ERR_INVALID_ARG,
+                     "relation-grouped chunks need the edges sorted by relation (edge %lld)", (long long)k);
+    if (k == n || (k > 0 && r[k] != r[k - 1])) {
+      for (int64_t c = run0; c < k; c += C) cs.push_back((int32_t)c);
+      run0 = k;
+    }
+  }
+  cs.push_back((int32_t)n);
+  const int64_t need = (int64_t)cs.size();
+  if (ctx->cstart_cap < need) {
+    if (ctx->cstart_dev) (void)hipFree(ctx->cstart_dev);
+    ctx->cstart_dev = nullptr;
+    ctx->cstart_cap = 0;
+    if (hipMalloc(&ctx->cstart_dev, (size_t)need * 4) != hipSuccess) {
+      (void)hipGetLastError();
+      ctx->cstart_dev = nullptr;
+      return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "chunk bound allocation failed");
+    }
+    ctx->cstart_cap = need;
+  }
+  e = hipMemcpyAsync(ctx->cstart_dev, cs.data(), (size_t)need * 4, hipMemcpyHostToDevice, ctx->cs);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->cs);
+  if (e != hipSuccess) return hip_fail(ctx, e, "chunk bound copy");
+  return PBG_OK;
+}
+
 // --------------------------------------------------------------------------
 // C ABI
 // --------------------------------------------------------------------------
@@ -265,8 +304,8 @@ pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_part
   if ((int64_t)(num_partitions - 1) * ps >= num_entities)
     return fail(PBG_ERR_INVALID_ARG, "a partition would be empty (num_partitions too large for num_entities)");
   if (ps > (1ll << 30)) return fail(PBG_ERR_INVALID_ARG, "partitions above 2^30 rows are not supported");
-  if (cmp == PBG_CMP_COS && op != PBG_OP_IDENTITY && num_relations > 1)
-    return fail(PBG_ERR_UNSUPPORTED, "cos with a non-identity operator needs a single relation");
+  if (cmp == PBG_CMP_COS && op == PBG_OP_LINEAR && num_relations > 1)
+    return fail(PBG_ERR_UNSUPPORTED, "cos with the linear operator needs a single relation");
   ctx->n = num_entities;
   ctx->P = num_partitions;
   ctx->R = num_relations;
@@ -297,6 +336,7 @@ void pbg_free(pbg_ctx* ctx) {
   (void)hipDeviceSynchronize();
   ctx->ws.release();
   if (ctx->steploss_dev) (void)hipFree(ctx->steploss_dev);
+  if (ctx->cstart_dev) (void)hipFree(ctx->cstart_dev);
   for (auto& s : ctx->slots) {
     if (s.emb) (void)hipFree(s.emb);
     if (s.ready) (void)hipEventDestroy(s.ready);
@@ -389,7 +429,8 @@ pbg_status check_neg_config(pbg_ctx* ctx, const pbg_neg_config* neg) {
     return set_err(ctx, PBG_ERR_INVALID_ARG, "chunk_size + num_uniform must be >= 2");
   if (neg->chunks_per_step < 1 || neg->chunks_per_step > 4096)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "chunks_per_step must be in [1, 4096]");
-  if (neg->reserved != 0) return set_err(ctx, PBG_ERR_INVALID_ARG, "reserved field must be 0");
+  if (neg->chunking != PBG_CHUNK_CONSECUTIVE && neg->chunking != PBG_CHUNK_BY_RELATION)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "unknown chunking %d", neg->chunking);
   if (neg->first_chunk < 0 || neg->first_chunk > 0xFFFFFFFFll)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "first_chunk out of range");
   const int64_t keys = (int64_t)neg->chunks_per_step * 2 * (neg->chunk_size + neg->num_uniform);
@@ -456,8 +497,22 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   const int C = neg->chunk_size, U = neg->num_uniform, S = neg->chunks_per_step;
   pbg_status st = ensure_workspace(ctx, C, U, S);
   if (st != PBG_OK) return st;
-  const int64_t nchunks = (n_edges + C - 1) / C;
+  // relation-grouped chunks: bounds in the call's edge arrays (checked before
+  // anything is updated)
+  const bool grouped = grouped_chunks(ctx, neg);
+  if (grouped) {
+    st = relation_chunk_bounds(ctx, rel, n_edges, C);
+    if (st != PBG_OK) return st;
+  }
+  const std::vector<int32_t>& cbound = ctx->cstart_host;
+  const int64_t nchunks = grouped ? (int64_t)cbound.size() - 1 : (n_edges + C - 1) / C;
+  // first edge of chunk c (c <= nchunks)
+  auto chunk_at = [&](int64_t c) -> int64_t {
+    return grouped ? (int64_t)cbound[(size_t)c] : std::min<int64_t>(n_edges, c * C);
+  };
   const int64_t nsteps = (nchunks + S - 1) / S;
+  const bool uniform_rel = chunk_relation_operator(ctx);
+  const int64_t rstride = (int64_t)S * (C + (uniform_rel ? U : 0));   // relation keys per step
   st = ensure_steploss(ctx, nsteps);
   if (st != PBG_OK) return st;
   hipStream_t cs = ctx->cs;
@@ -498,13 +553,15 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   for (int64_t t = 0; t < nsteps; ++t) {
     const int64_t c0 = t * S;
     const int nch = (int)std::min<int64_t>(S, nchunks - c0);
-    const int m_step = (int)std::min<int64_t>((int64_t)S * C, n_edges - c0 * C);
+    const int64_t e_lo = chunk_at(c0);
+    const int m_step = (int)(chunk_at(c0 + nch) - e_lo);
     g.nchunks = nch;
     g.m_step = m_step;
     g.chunk0 = neg->first_chunk + c0;
-    b.src = src + c0 * C;
-    b.dst = dst + c0 * C;
-    b.rel = rel ? rel + c0 * C : nullptr;
+    g.cstart = grouped ? ctx->cstart_dev + c0 : nullptr;
+    b.src = src + e_lo;
+    b.dst = dst + e_lo;
+    b.rel = rel ? rel + e_lo : nullptr;
 
     // the sort keys (table, row) of every contribution row follow from the
     // edges and the negative draws alone: at the start of each window of
@@ -512,22 +569,34 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     const int64_t wi = t % kSortWindow;
     if (wi == 0) {
       const int wn = (int)std::min<int64_t>(kSortWindow, nsteps - t);
-      const int64_t e1 = std::min<int64_t>(n_edges, (t + wn) * (int64_t)S * C);
-      launch_window_keys(g, src + c0 * C, dst + c0 * C, rel ? rel + c0 * C : nullptr, e1 - c0 * C,
-                         neg->first_chunk + c0, S, wn, kstride, win_keys, win_vals, win_rkeys, win_rvals, cs);
+      const int64_t cw1 = std::min<int64_t>(nchunks, (t + wn) * (int64_t)S);   // chunks of the window end here
+      if (grouped) {
+        // steps of relation-grouped chunks hold fewer keys than a full step:
+        // the rest of each step's key block sorts last, past every real key
+        launch_fill_u32(win_keys, wn * kstride, 1u << key_bits, cs);
+      }
+      launch_window_keys(g, src + e_lo, dst + e_lo, rel ? rel + e_lo : nullptr, chunk_at(cw1) - e_lo,
+                         grouped ? ctx->cstart_dev + c0 : nullptr, (int)(cw1 - c0), neg->first_chunk + c0, S, wn,
+                         kstride, win_keys, win_vals, win_rkeys, win_rvals, rstride, uniform_rel ? 1 : 0, cs);
       const int64_t tl = t + wn - 1;   // the window's last step
       const int nch_l = (int)std::min<int64_t>(S, nchunks - tl * S);
-      const int m_l = (int)std::min<int64_t>((int64_t)S * C, n_edges - tl * S * C);
-      launch_radix_sort_segments(win_keys, win_vals, ctx->wkeys_alt, ctx->wvals_alt, kstride, (int)kstride,
-                                 2 * (nch_l * U + m_l), wn, key_bits, ctx->whist, &wsk, &wsv, cs);
+      const int m_l = (int)(chunk_at(tl * S + nch_l) - chunk_at(tl * S));
+      if (grouped)
+        launch_radix_sort_segments(win_keys, win_vals, ctx->wkeys_alt, ctx->wvals_alt, kstride, (int)kstride,
+                                   (int)kstride, wn, key_bits + 1, ctx->whist, &wsk, &wsv, cs);
+      else
+        launch_radix_sort_segments(win_keys, win_vals, ctx->wkeys_alt, ctx->wvals_alt, kstride, (int)kstride,
+                                   2 * (nch_l * U + m_l), wn, key_bits, ctx->whist, &wsk, &wsv, cs);
     }
     const int nkeys = 2 * (nch * U + m_step);
     uint32_t* skeys = wsk + wi * kstride;
     uint32_t* svals = wsv + wi * kstride;
     if (win_rkeys) {
-      b.rkeys = win_rkeys + wi * (int64_t)S * C;
-      b.rvals = win_rvals + wi * (int64_t)S * C;
+      b.rkeys = win_rkeys + wi * rstride;
+      b.rvals = win_rvals + wi * rstride;
     }
+    // relation keys of the step: the edges', then the uniform source candidates'
+    const int n_relkeys = m_step + (uniform_rel ? nch * U : 0);
 
     mark(t, 0);
 
@@ -564,8 +633,8 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
         launch_linear_relation_update(g, b, rk, rv, m_step, lr, cs);
       } else if (ctx->R > 1) {
         uint32_t *rk = nullptr, *rv = nullptr;
-        launch_radix_sort_to(b.rkeys, b.rvals, m_step, rel_bits, ctx->sw, &rk, &rv, cs);
-        launch_relation_update_sorted(g, b, rk, rv, m_step, ctx->sw, lr, cs);
+        launch_radix_sort_to(b.rkeys, b.rvals, n_relkeys, rel_bits, ctx->sw, &rk, &rv, cs);
+        launch_relation_update_sorted(g, b, rk, rv, n_relkeys, ctx->sw, lr, cs);
       } else {
         // the single relation's gradient sums and update read only what the
         // operator backward wrote: on the side stream, beside the entity sort
@@ -621,7 +690,7 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   // algorithmic work (full chunks approximated by the actual chunk sizes)
   const double U_d = U;
   for (int64_t c = 0; c < nchunks; ++c) {
-    const double Cc = (double)std::min<int64_t>(C, n_edges - c * C);
+    const double Cc = (double)(chunk_at(c + 1) - chunk_at(c));
     const double Nc = Cc + U_d;
     ctx->stats.gather_bytes += (2 * Cc + 2 * U_d) * d * 4.0;
     ctx->stats.score_flops += 12.0 * Cc * Nc * d;
@@ -650,6 +719,9 @@ pbg_status check_bucket_call(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* 
   if (n_edges == 0) return PBG_OK;
   if (ctx->R > 1 && !rel) return set_err(ctx, PBG_ERR_INVALID_ARG, "rel may be NULL only with one relation");
   if (!src_local || !dst_local) return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL edge arrays");
+  if (chunk_relation_operator(ctx) && !grouped_chunks(ctx, neg))
+    return set_err(ctx, PBG_ERR_UNSUPPORTED,
+                   "cos with an operator and several relations needs relation-grouped chunks (PBG_CHUNK_BY_RELATION)");
   st = ensure_workspace(ctx, neg->chunk_size, neg->num_uniform, neg->chunks_per_step);
   if (st != PBG_OK) return st;
   // device-side range check before any update
@@ -767,5 +839,49 @@ extern "C" pbg_status pbg_sample_negatives(pbg_ctx* ctx, int32_t i, int32_t j, i
   hipError_t e = hipGetLastError();
   if (e == hipSuccess) e = hipStreamSynchronize(ctx->cs);
   if (e != hipSuccess) return hip_fail(ctx, e, "sample_negatives");
+  return PBG_OK;
+}
+
+extern "C" pbg_status pbg_group_by_relation(pbg_ctx* ctx, const int32_t* src, const int32_t* rel,
+                                            const int32_t* dst, int64_t n, int32_t* src_out, int32_t* rel_out,
+                                            int32_t* dst_out) {
+  if (!ctx) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
+  ctx->err.clear();
+  if (n < 0 || n > 0x7FFFFFFFll) return set_err(ctx, PBG_ERR_INVALID_ARG, "n out of range");
+  if (n == 0) return PBG_OK;
+  if (!src || !rel || !dst || !src_out || !rel_out || !dst_out)
+    return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL array");
+  hipStream_t cs = ctx->cs;
+  // a stable radix sort of (relation, position) pairs, then one gather
+  Arena a;
+  uint32_t* flag = (uint32_t*)a.get(16);
+  uint32_t* keys = (uint32_t*)a.get((size_t)n * 4);
+  uint32_t* vals = (uint32_t*)a.get((size_t)n * 4);
+  SortWork w{};
+  if (a.failed || !alloc_sortwork(a, w, n, 0)) {
+    a.release();
+    return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "work buffer allocation failed");
+  }
+  hipError_t e = hipMemsetAsync(flag, 0, 4, cs);
+  if (e == hipSuccess) {
+    launch_check_ids(rel, n, ctx->R, flag, 4u, cs);
+    uint32_t hflag = 0;
+    e = hipMemcpyAsync(&hflag, flag, 4, hipMemcpyDeviceToHost, cs);
+    if (e == hipSuccess) e = hipStreamSynchronize(cs);
+    if (e == hipSuccess && hflag) {
+      a.release();
+      return set_err(ctx, PBG_ERR_INVALID_ARG, "a relation id is outside [0, %d)", ctx->R);
+    }
+  }
+  if (e == hipSuccess) {
+    launch_perm_keys(rel, nullptr, n, keys, vals, cs);
+    launch_radix_sort(keys, vals, (int)n, std::max(1, bits_for((uint64_t)ctx->R - 1)), w, cs);
+    launch_gather3(vals, src, rel, dst, n, src_out, rel_out, dst_out, cs);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(cs);
+  }
+  a.release();
+  if (e != hipSuccess) return hip_fail(ctx, e, "group_by_relation");
   return PBG_OK;
 }

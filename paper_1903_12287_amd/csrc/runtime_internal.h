@@ -84,6 +84,11 @@ struct pbg_ctx {
   uint32_t* flag_dev = nullptr;
   double* steploss_dev = nullptr;
   int64_t steploss_cap = 0;
+  // relation-grouped chunks of the current call: bounds in the call's edge
+  // arrays (host copy and device copy)
+  std::vector<int32_t> cstart_host;
+  int32_t* cstart_dev = nullptr;
+  int64_t cstart_cap = 0;
 
   std::vector<double> step_losses;
   pbg_stats stats{};
@@ -142,6 +147,20 @@ pbg_status check_bucket_call(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* 
                              const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
                              const pbg_neg_config* neg);
 pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S);
+// chunk bounds of a call's edges for PBG_CHUNK_BY_RELATION (rel: device, n
+// edges sorted by relation): ctx->cstart_host / cstart_dev; INVALID_ARG when
+// the relations are not in nondecreasing order
+pbg_status relation_chunk_bounds(pbg_ctx* ctx, const int32_t* rel, int64_t n, int C);
+// the call's chunks are relation-grouped (PBG_CHUNK_BY_RELATION with several
+// relations; with one relation both chunkings are the same)
+inline bool grouped_chunks(const pbg_ctx* ctx, const pbg_neg_config* neg) {
+  return neg->chunking == PBG_CHUNK_BY_RELATION && ctx->R > 1;
+}
+// the cos comparator with an operator and several relations applies each
+// chunk's relation to its source candidates: relation-grouped chunks only
+inline bool chunk_relation_operator(const pbg_ctx* ctx) {
+  return ctx->cmp == PBG_CMP_COS && ctx->op != PBG_OP_IDENTITY && ctx->R > 1;
+}
 pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps);
 // geometry of the steps of bucket (i, j) (chunk and candidate counts, padded
 // strides, partition rows, key widths) and the step buffers bound to the

@@ -25,6 +25,7 @@ LOSSES = {"ranking": 0, "logistic": 1, "softmax": 2}
 F_BF16_SCORE = 1
 F_PHASE_TIMING = 2
 F_SCORE_TIMING = 4
+CHUNKINGS = {"consecutive": 0, "by_relation": 1}
 MEM_DEVICE = 0
 MEM_PINNED_HOST = 1
 NOALLOC_MAX_REL_FLOATS = 2 * 1024 * 1024   # PBG_NOALLOC_MAX_REL_FLOATS
@@ -37,7 +38,7 @@ EXPORTS = (
     "pbg_relation_param_floats", "pbg_bucket_edges", "pbg_bind_partition",
     "pbg_bind_relations", "pbg_set_streams", "pbg_train_bucket", "pbg_get_step_losses",
     "pbg_train_epoch", "pbg_score_edges", "pbg_rank_eval", "pbg_rank_sampled", "pbg_get_stats",
-    "pbg_sample_negatives", "pbg_inspect_step", "pbg_score_edges_noalloc",
+    "pbg_sample_negatives", "pbg_inspect_step", "pbg_score_edges_noalloc", "pbg_group_by_relation",
 )
 
 
@@ -50,7 +51,7 @@ class PbgError(RuntimeError):
 
 class NegConfig(ctypes.Structure):
     _fields_ = [("chunk_size", ctypes.c_int32), ("num_uniform", ctypes.c_int32),
-                ("chunks_per_step", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("chunks_per_step", ctypes.c_int32), ("chunking", ctypes.c_int32),
                 ("first_chunk", ctypes.c_int64)]
 
 
@@ -97,6 +98,7 @@ def library() -> ctypes.CDLL:
         "pbg_train_epoch": ([vp, vp, vp, vp, vp, ctypes.POINTER(NegConfig), f32, u64, i32, dp], i32),
         "pbg_score_edges": ([vp, i32, i32, vp, vp, vp, i64, vp], i32),
         "pbg_score_edges_noalloc": ([vp, i32, i32, vp, vp, vp, i64, vp], i32),
+        "pbg_group_by_relation": ([vp, vp, vp, vp, i64, vp, vp, vp], i32),
         "pbg_rank_eval": ([vp, vp, vp, vp, i64, vp, vp, vp, i64, vp, dp, dp], i32),
         "pbg_rank_sampled": ([vp, vp, vp, vp, i64, vp, i64, vp, dp, dp], i32),
         "pbg_get_stats": ([vp, ctypes.POINTER(Stats)], i32),
@@ -225,16 +227,17 @@ def pbg_bucket_edges(ctx, src, rel, dst, offsets, src_local, rel_out, dst_local)
         _ptr(dst_local, torch.int32, "dst_local", allow_none=n == 0)))
 
 
-def _neg(chunk_size, num_uniform, chunks_per_step, first_chunk):
-    return NegConfig(int(chunk_size), int(num_uniform), int(chunks_per_step), 0, int(first_chunk))
+def _neg(chunk_size, num_uniform, chunks_per_step, first_chunk, chunking="consecutive"):
+    return NegConfig(int(chunk_size), int(num_uniform), int(chunks_per_step), _enum(CHUNKINGS, chunking, "chunking"),
+                     int(first_chunk))
 
 
 def pbg_train_bucket(ctx, i, j, src_local, rel, dst_local, chunk_size, num_uniform,
-                     chunks_per_step, lr, seed, first_chunk=0) -> float:
+                     chunks_per_step, lr, seed, first_chunk=0, chunking="consecutive") -> float:
     n = src_local.numel()
     if dst_local.numel() != n or (rel is not None and rel.numel() != n):
         raise ValueError("edge arrays differ in length")
-    neg = _neg(chunk_size, num_uniform, chunks_per_step, first_chunk)
+    neg = _neg(chunk_size, num_uniform, chunks_per_step, first_chunk, chunking)
     loss = ctypes.c_double(0.0)
     _check(ctx, library().pbg_train_bucket(
         ctx, int(i), int(j), _ptr(src_local, torch.int32, "src_local", allow_none=n == 0),
@@ -253,13 +256,13 @@ def pbg_get_step_losses(ctx):
 
 
 def pbg_train_epoch(ctx, offsets, src_local, rel, dst_local, chunk_size, num_uniform,
-                    chunks_per_step, lr, seed, max_resident) -> float:
+                    chunks_per_step, lr, seed, max_resident, chunking="consecutive") -> float:
     for t, name in ((src_local, "src_local"), (dst_local, "dst_local")):
         if t.numel() and not t.is_pinned():
             raise ValueError(f"{name} must be in page-locked host memory")
     if offsets.device.type != "cpu":
         raise ValueError("offsets must be a host tensor")
-    neg = _neg(chunk_size, num_uniform, chunks_per_step, 0)
+    neg = _neg(chunk_size, num_uniform, chunks_per_step, 0, chunking)
     loss = ctypes.c_double(0.0)
     _check(ctx, library().pbg_train_epoch(
         ctx, _ptr(offsets, torch.int64, "offsets", device=False),
@@ -278,6 +281,17 @@ def pbg_score_edges(ctx, i, j, src_local, rel, dst_local, scores):
         _ptr(rel, torch.int32, "rel", allow_none=True),
         _ptr(dst_local, torch.int32, "dst_local", allow_none=n == 0), n,
         _ptr(scores, torch.float32, "scores", allow_none=n == 0)))
+
+
+def pbg_group_by_relation(ctx, src, rel, dst, src_out, rel_out, dst_out):
+    n = src.numel()
+    if rel.numel() != n or dst.numel() != n:
+        raise ValueError("edge arrays differ in length")
+    _check(ctx, library().pbg_group_by_relation(
+        ctx, _ptr(src, torch.int32, "src", allow_none=n == 0), _ptr(rel, torch.int32, "rel", allow_none=n == 0),
+        _ptr(dst, torch.int32, "dst", allow_none=n == 0), n,
+        _ptr(src_out, torch.int32, "src_out", allow_none=n == 0), _ptr(rel_out, torch.int32, "rel_out", allow_none=n == 0),
+        _ptr(dst_out, torch.int32, "dst_out", allow_none=n == 0)))
 
 
 def pbg_score_edges_noalloc(ctx, i, j, src_local, rel, dst_local, scores):
@@ -325,17 +339,19 @@ def pbg_sample_negatives(ctx, i, j, first_chunk, n_chunks, num_uniform, seed, ou
 
 
 def pbg_inspect_step(ctx, i, j, src_local, rel, dst_local, chunk_size, num_uniform, chunks_per_step, seed,
-                     first_chunk=0, scores=None, dscores=None, row_loss=None, pos=None) -> float:
+                     first_chunk=0, scores=None, dscores=None, row_loss=None, pos=None, chunking="consecutive",
+                     n_chunks=None) -> float:
+    """n_chunks: chunks of the call (consecutive chunking: ceil(n / chunk_size))."""
     n = src_local.numel()
     if dst_local.numel() != n or (rel is not None and rel.numel() != n):
         raise ValueError("edge arrays differ in length")
-    nch = -(-n // int(chunk_size))
+    nch = -(-n // int(chunk_size)) if n_chunks is None else int(n_chunks)
     N = int(chunk_size) + int(num_uniform)
     for t, want, name in ((scores, nch * 2 * chunk_size * N, "scores"), (dscores, nch * 2 * chunk_size * N, "dscores"),
                           (row_loss, nch * 2 * chunk_size, "row_loss"), (pos, nch * chunk_size, "pos")):
         if t is not None and t.numel() != want:
             raise ValueError(f"{name} must hold {want} floats")
-    neg = _neg(chunk_size, num_uniform, chunks_per_step, first_chunk)
+    neg = _neg(chunk_size, num_uniform, chunks_per_step, first_chunk, chunking)
     loss = ctypes.c_double(0.0)
     _check(ctx, library().pbg_inspect_step(
         ctx, int(i), int(j), _ptr(src_local, torch.int32, "src_local", allow_none=n == 0),

@@ -34,12 +34,14 @@ class Problem:
     S: int
     lr: float
     seed: int
+    chunking: str = "consecutive"
 
 
 def make_problem(op, cmp, loss, n=60, P=1, R=1, d=16, m=300, C=20, U=12, S=4, i=0, j=0,
-                 seed=1, sigma=0.3, rel_scale=0.3, lr=0.1, margin=0.1, zipf=1.1):
+                 seed=1, sigma=0.3, rel_scale=0.3, lr=0.1, margin=0.1, zipf=1.1, chunking="consecutive"):
     """A small seeded problem with Zipf endpoints (duplicates in chunks) and
-    perturbed relation parameters."""
+    perturbed relation parameters; with chunking='by_relation' the edges are
+    sorted by relation (stably)."""
     rng = synth.rng_for(seed)
     rows = [O.partition_rows(n, P, p) for p in range(P)]
     parts = synth.partition_embeddings(rows, d, rng, sigma)
@@ -47,8 +49,11 @@ def make_problem(op, cmp, loss, n=60, P=1, R=1, d=16, m=300, C=20, U=12, S=4, i=
     dst = synth.BoundedZipf(rows[j], zipf, rng).sample(rng, m)
     rel_ids = None if R == 1 else rng.integers(0, R, m).astype(np.int32)
     relp = synth.perturbed_relation_params(op, R, d, rng, rel_scale)
+    if chunking == "by_relation" and rel_ids is not None:
+        order = np.argsort(rel_ids, kind="stable")
+        src, rel_ids, dst = src[order], rel_ids[order], dst[order]
     return Problem(n, P, R, d, op, cmp, loss, margin, parts, relp, i, j, src, rel_ids, dst,
-                   C, U, S, lr, seed + 1000)
+                   C, U, S, lr, seed + 1000, chunking)
 
 
 def oracle_model(pb: Problem) -> O.Model:
@@ -85,7 +90,7 @@ class GpuModel:
         hi = pb.src.shape[0] if hi is None else hi
         r = None if self.rel_ids is None else self.rel_ids[lo:hi]
         return self.pbg.pbg_train_bucket(self.ctx, pb.i, pb.j, self.src[lo:hi], r, self.dst[lo:hi],
-                                         pb.C, pb.U, pb.S, pb.lr, pb.seed, first_chunk)
+                                         pb.C, pb.U, pb.S, pb.lr, pb.seed, first_chunk, pb.chunking)
 
     def state(self):
         torch.cuda.synchronize()
@@ -142,13 +147,13 @@ def _norm(v):
     return np.maximum(np.linalg.norm(v, axis=-1), O.EPS_NORM)
 
 
-def score_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk=0):
+def score_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk=0, chunking="consecutive"):
     """Per chunk of a step: (Ap (C_c,), A0 (C_c, N_c), A1 (C_c, N_c))."""
     src = np.asarray(src, np.int64)
     dst = np.asarray(dst, np.int64)
     m = src.shape[0]
+    step = O.make_chunks(m, C, rel, chunking)
     rel = np.zeros(m, np.int64) if rel is None else np.asarray(rel, np.int64)
-    step = O.chunk_ranges(m, C)
     negs = O.step_negatives(model, i, j, step, seed, U, first_chunk)
     Ei, Ej = model.emb[i], model.emb[j]
     out = []
@@ -163,7 +168,7 @@ def score_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk=0):
             gq = O.apply_operator(model.op, torch.tensor(xs), None if th is None else torch.tensor(th)).numpy()
             aq = aq / _norm(gq)[:, None]
             acd = np.abs(cd) / _norm(cd)[:, None]
-            th0 = None if model.rel is None else model.rel[0]
+            th0 = None if model.rel is None else model.rel[rel[lo]]   # the chunk's relation
             gcs = O.apply_operator(model.op, torch.tensor(cs), None if th0 is None else torch.tensor(th0)).numpy()
             acs = _abs_forward(model.op, np.abs(cs), None if th0 is None else np.abs(th0)) / _norm(gcs)[:, None]
             ay = np.abs(xd) / _norm(xd)[:, None]
@@ -189,7 +194,8 @@ def gpu_inspect(gm, lo, hi, first_chunk):
     pbg, p = pb
     n = hi - lo
     C, U = p.C, p.U
-    nch = -(-n // C)
+    rel_h = None if p.rel_ids is None else p.rel_ids[lo:hi]
+    nch = len(O.make_chunks(n, C, rel_h, p.chunking))
     N = C + U
     dev = torch.device("cuda")
     scores = torch.empty(nch * 2 * C * N, dtype=torch.float32, device=dev)
@@ -198,14 +204,14 @@ def gpu_inspect(gm, lo, hi, first_chunk):
     pos = torch.empty(nch * C, dtype=torch.float32, device=dev)
     r = None if gm.rel_ids is None else gm.rel_ids[lo:hi]
     loss = pbg.pbg_inspect_step(gm.ctx, p.i, p.j, gm.src[lo:hi], r, gm.dst[lo:hi], C, U, p.S, p.seed,
-                                first_chunk, scores, dscores, row_loss, pos)
+                                first_chunk, scores, dscores, row_loss, pos, p.chunking, nch)
     S = scores.view(nch, 2, C, N).cpu().numpy().astype(np.float64)
     dS = dscores.view(nch, 2, C, N).cpu().numpy().astype(np.float64)
     L = row_loss.view(nch, 2, C).cpu().numpy().astype(np.float64)
     P_ = pos.view(nch, C).cpu().numpy().astype(np.float64)
     out = []
-    for c in range(nch):
-        Cc = min(C, n - c * C)
+    for c, clo, chi in O.make_chunks(n, C, rel_h, p.chunking):
+        Cc = chi - clo
         Nc = Cc + U
         # outside the chunk's block every output is zero
         assert not S[c, :, Cc:].any() and not S[c, :, :, Nc:].any()
@@ -296,15 +302,15 @@ def _abs_adj_t(op, y, th):
     return torch.cat([tr * yr + ti * yi, tr * yi + ti * yr], -1)
 
 
-def gradient_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk, insp):
+def gradient_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk, insp, chunking="consecutive"):
     """A of every gradient element of one step (insp: O.inspect_step of the
     same edges at the same state).  Returns ({partition: (row ids, A rows)},
     (relation ids, A rows) or None), ids as in O.step_loss_and_grad."""
     src = np.asarray(src, np.int64)
     dst = np.asarray(dst, np.int64)
     m = src.shape[0]
+    step = O.make_chunks(m, C, rel, chunking)
     rel = np.zeros(m, np.int64) if rel is None else np.asarray(rel, np.int64)
-    step = O.chunk_ranges(m, C)
     negs = O.step_negatives(model, i, j, step, seed, U, first_chunk)
     touched = {i: [], j: []}
     for (c, lo, hi), (u_dst, u_src) in zip(step, negs):
@@ -342,8 +348,9 @@ def gradient_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk, insp):
             raw_cd = torch.cat([raw_xd, rows(j, u_dst, False)], 0)
             raw_cs = torch.cat([raw_xs, rows(i, u_src, False)], 0)
             nq = O._clamped_norm(O.apply_operator(model.op, raw_xs, thr)).unsqueeze(-1)
-            th0 = None if rleaf is None else rleaf[0].expand(raw_cs.shape[0], -1)
-            thr0 = None if rleaf is None else torch.tensor(model.rel[0], dtype=torch.float64)
+            k0 = 0 if rleaf is None else int(np.searchsorted(step_rels, r_e[0]))   # the chunk's relation
+            th0 = None if rleaf is None else rleaf[k0].expand(raw_cs.shape[0], -1)
+            thr0 = None if rleaf is None else torch.tensor(model.rel[r_e[0]], dtype=torch.float64)
             ncs = O._clamped_norm(O.apply_operator(model.op, raw_cs, thr0)).unsqueeze(-1)
             q = _abs_fwd_t(model.op, xs, th) / nq
             yh = xd / O._clamped_norm(raw_xd).unsqueeze(-1)
@@ -416,16 +423,17 @@ def oracle_step_with_scales(pb, om, src, rel, dst, first_chunk, branches=None):
     the step takes those hinge branches and the scales weigh every term that
     either branch makes active."""
     m = len(src)
-    insp = O.inspect_step(om, pb.i, pb.j, src, rel, dst, pb.C, pb.U, pb.seed, first_chunk)
+    insp = O.inspect_step(om, pb.i, pb.j, src, rel, dst, pb.C, pb.U, pb.seed, first_chunk, pb.chunking)
     if branches is not None:
         for rec, (a0, a1) in zip(insp, branches):
             rec["dS0"] = np.maximum(np.abs(rec["dS0"]), a0)
             rec["dS1"] = np.maximum(np.abs(rec["dS1"]), a1)
-    step = O.chunk_ranges(m, pb.C)
+    step = O.make_chunks(m, pb.C, rel, pb.chunking)
     negs = O.step_negatives(om, pb.i, pb.j, step, pb.seed, pb.U, first_chunk)
     rel_a = np.zeros(m, np.int64) if rel is None else rel
     loss, grads, rel_grad = O.step_loss_and_grad(om, pb.i, pb.j, src, rel_a, dst, step, negs, branches=branches)
-    ent_sc, rel_sc = gradient_scales(om, pb.i, pb.j, src, rel, dst, pb.C, pb.U, pb.seed, first_chunk, insp)
+    ent_sc, rel_sc = gradient_scales(om, pb.i, pb.j, src, rel, dst, pb.C, pb.U, pb.seed, first_chunk, insp,
+                                     pb.chunking)
     return loss, grads, rel_grad, ent_sc, rel_sc
 
 
@@ -446,8 +454,8 @@ def teacher_forced_step(gm, lo, hi, first_chunk, eps):
     rep = branches = None
     if pb.loss == "ranking":
         gpu, _ = gpu_inspect(gm, lo, hi, first_chunk)
-        orc = O.inspect_step(om, pb.i, pb.j, src, rel, dst, pb.C, pb.U, pb.seed, first_chunk)
-        scales = score_scales(om, pb.i, pb.j, src, rel, dst, pb.C, pb.U, pb.seed, first_chunk)
+        orc = O.inspect_step(om, pb.i, pb.j, src, rel, dst, pb.C, pb.U, pb.seed, first_chunk, pb.chunking)
+        scales = score_scales(om, pb.i, pb.j, src, rel, dst, pb.C, pb.U, pb.seed, first_chunk, pb.chunking)
         rep = check_inspection(om, gpu, orc, scales, eps)
         branches = [(g["dS0"] > 0, g["dS1"] > 0) for g in gpu]
         del gpu, orc, scales

@@ -53,5 +53,5 @@ def test_init_rejects_bad_arguments_without_a_device():
                                 kw["dim"], kw["op"], kw["cmp"], kw["loss"])
         assert ei.value.status_name == "INVALID_ARG", kw
     with pytest.raises(pbg.PbgError) as ei:
-        pbg.pbg_bucket_init(100, 1, 3, 8, "translation", "cos", "ranking")
+        pbg.pbg_bucket_init(100, 1, 3, 8, "linear", "cos", "ranking")
     assert ei.value.status_name == "UNSUPPORTED"

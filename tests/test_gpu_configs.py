@@ -49,7 +49,7 @@ CONFIGS = {
 S = 40
 
 
-def make_config(name, m, seed=20190010):
+def make_config(name, m, seed=20190010, chunking="consecutive"):
     op, cmp, loss, d, R, n, P, (i, j), C, U, zs, zd, zr = CONFIGS[name]
     rng = synth.rng_for(seed)
     rows = [O.partition_rows(n, P, p) for p in range(P)]
@@ -58,7 +58,11 @@ def make_config(name, m, seed=20190010):
     dst = synth.BoundedZipf(rows[j], zd, rng).sample(rng, m)
     rel = None if R == 1 else synth.BoundedZipf(R, zr, rng).sample(rng, m).astype(np.int32)
     relp = synth.identity_relation_params(op, R, d)
-    return Problem(n, P, R, d, op, cmp, loss, 0.1, parts, relp, i, j, src, rel, dst, C, U, S, 0.1, seed + 1)
+    if chunking == "by_relation":
+        order = np.argsort(rel, kind="stable")
+        src, rel, dst = src[order], rel[order], dst[order]
+    return Problem(n, P, R, d, op, cmp, loss, 0.1, parts, relp, i, j, src, rel, dst, C, U, S, 0.1, seed + 1,
+                   chunking)
 
 
 def _model_from(pb, st):
@@ -67,8 +71,9 @@ def _model_from(pb, st):
 
 
 def _step_edges(pb, t):
-    per = S * pb.C
-    lo, hi = t * per, (t + 1) * per
+    """Edges [lo, hi) of step t (S chunks of the call's chunking)."""
+    ch = O.make_chunks(len(pb.src), pb.C, pb.rel_ids, pb.chunking)
+    lo, hi = ch[t * S][1], ch[min(len(ch), (t + 1) * S) - 1][2]
     rel = None if pb.rel_ids is None else pb.rel_ids[lo:hi]
     return lo, hi, pb.src[lo:hi], rel, pb.dst[lo:hi]
 
@@ -78,21 +83,25 @@ def _oracle_step(pb, om, t):
     return oracle_step_with_scales(pb, om, src, rel, dst, t * S)
 
 
-@pytest.mark.parametrize("name,warm,forced", [("tiny_social", 3, 2), ("social_network", 2, 2),
-                                              ("knowledge_graph", 1, 1), ("big_bucket", 2, 2),
-                                              ("follower", 2, 2)])
-def test_teacher_forced_steps(name, warm, forced):
+@pytest.mark.parametrize("name,warm,forced,chunking", [("tiny_social", 3, 2, "consecutive"),
+                                                       ("social_network", 2, 2, "consecutive"),
+                                                       ("knowledge_graph", 1, 1, "consecutive"),
+                                                       ("knowledge_graph", 1, 1, "by_relation"),
+                                                       ("big_bucket", 2, 2, "consecutive"),
+                                                       ("follower", 2, 2, "consecutive")])
+def test_teacher_forced_steps(name, warm, forced, chunking):
     C = CONFIGS[name][8]
     per = S * C
     m = (warm + forced) * per
-    pb = make_config(name, m)
+    pb = make_config(name, m, chunking=chunking)
     print(f"\n[{name}] C={pb.C} U={pb.U} S={S} d={pb.d} R={pb.R} P={pb.P} bucket=({pb.i},{pb.j}) "
-          f"warm={warm} forced={forced}", flush=True)
+          f"warm={warm} forced={forced} chunking={chunking}", flush=True)
     gm = GpuModel(pb)
     try:
-        gm.train(0, warm * per, 0)
+        gm.train(0, _step_edges(pb, warm)[0], 0)
         for t in range(warm, warm + forced):
-            rep, gl, ol, worst = teacher_forced_step(gm, t * per, (t + 1) * per, t * S, 1e-5)
+            lo, hi = _step_edges(pb, t)[:2]
+            rep, gl, ol, worst = teacher_forced_step(gm, lo, hi, t * S, 1e-5)
             if rep is not None:
                 print(f"  step {t} census: {rep['near_kink']} hinge terms within the float32 error band "
                       f"of the kink, {rep['flips']} flipped", flush=True)

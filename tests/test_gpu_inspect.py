@@ -44,7 +44,11 @@ SHAPES = {
     # d > 128 row kernels (four floats a lane), ragged tiles
     "wide_rows": ("diagonal", "dot", "logistic", 200, 7, 5_000, 1, (0, 0), 300, 260, 1.1, 1.1, 1.0),
     "translation_dot": ("translation", "dot", "softmax", 64, 9, 3_000, 2, (1, 0), 256, 300, 1.1, 1.1, 1.0),
+    # relation-grouped chunks: cos with an operator and 40 relations (each
+    # chunk's relation applied to its source candidates)
+    "grouped_cos": ("translation", "cos", "ranking", 64, 40, 20_000, 1, (0, 0), 1000, 1000, 1.0, 1.0, 0.8),
 }
+GROUPED = {"grouped_cos"}
 
 
 def make_shape(name, m, sigma=0.1, seed=5):
@@ -58,7 +62,12 @@ def make_shape(name, m, sigma=0.1, seed=5):
     relp = synth.perturbed_relation_params(op, R, d, rng, 0.3)
     if op == "linear":
         relp = (synth.identity_relation_params(op, R, d) + 0.05 * rng.standard_normal((R, d * d))).astype(np.float32)
-    return Problem(n, P, R, d, op, cmp, loss, 0.1, parts, relp, i, j, src, rel, dst, C, U, 40, 0.1, seed + 99)
+    chunking = "by_relation" if name in GROUPED else "consecutive"
+    if chunking == "by_relation":
+        order = np.argsort(rel, kind="stable")
+        src, rel, dst = src[order], rel[order], dst[order]
+    return Problem(n, P, R, d, op, cmp, loss, 0.1, parts, relp, i, j, src, rel, dst, C, U, 40, 0.1, seed + 99,
+                   chunking)
 
 
 CASES = [(name, bf16) for name in SHAPES for bf16 in (False, True)]
@@ -85,8 +94,8 @@ def test_step_forward_elementwise(name, bf16):
     if "rel" in before:
         assert np.array_equal(before["rel"], after["rel"])
     om = oracle_model(pb)
-    orc = O.inspect_step(om, pb.i, pb.j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.seed, 7)
-    scales = score_scales(om, pb.i, pb.j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.seed, 7)
+    orc = O.inspect_step(om, pb.i, pb.j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.seed, 7, pb.chunking)
+    scales = score_scales(om, pb.i, pb.j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.seed, 7, pb.chunking)
     rep = check_inspection(om, gpu, orc, scales, 2e-2 if bf16 else 1e-5)
     print(f"[{name} bf16={bf16}] {rep}", flush=True)
     assert rep["p_ratio"] <= 1.0 and rep["s_ratio"] <= 1.0

@@ -177,3 +177,84 @@ def test_long_call_crosses_sort_windows(op, cmp, loss, d, R):
     assert err <= 1e-4, err
     gerr = float(np.max(np.abs(st["G"][0] - om.G[0]) / np.maximum(1.0, om.G[0])))
     assert gerr <= 1e-4, gerr
+
+
+@pytest.mark.parametrize("op,cmp,loss,R", [("translation", "cos", "ranking", 4),
+                                           ("complex_diagonal", "cos", "softmax", 3),
+                                           ("diagonal", "cos", "logistic", 6),
+                                           ("diagonal", "dot", "logistic", 5),
+                                           ("linear", "dot", "ranking", 4)])
+def test_relation_grouped_chunks_match_oracle(op, cmp, loss, R):
+    """Relation-grouped chunks (Sec. 4.3: batches sharing a relation type),
+    edges sorted by relation: several steps of short and full chunks, cos with
+    an operator and several relations included (each chunk's relation is
+    applied to its source candidates)."""
+    pb = make_problem(op, cmp, loss, n=150, R=R, d=24, m=437, C=16, U=10, S=3, seed=71, sigma=0.2,
+                      chunking="by_relation")
+    gm = GpuModel(pb)
+    try:
+        gl = gm.train()
+        from paper_1903_12287_amd import pbg
+        steps = pbg.pbg_get_step_losses(gm.ctx)
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol, osteps = O.train_bucket(om, 0, 0, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr, pb.seed,
+                                return_steps=True, chunking="by_relation")
+    assert len(steps) == len(osteps)
+    for a, b in zip(steps, osteps):
+        assert abs(a - b) <= 1e-4 * max(1.0, abs(b)), (a, b)
+    assert float(np.max(np.abs(st["emb"][0] - om.emb[0]))) <= 1e-4
+    assert float(np.max(np.abs(st["rel"] - om.rel))) <= 1e-4
+
+
+def test_relation_grouping_helper_and_errors():
+    from paper_1903_12287_amd import pbg
+    # pbg_group_by_relation is a stable sort by relation
+    rng = np.random.default_rng(5)
+    n, R = 100_003, 37
+    src = torch.from_numpy(rng.integers(0, 1000, n).astype(np.int32)).cuda()
+    dst = torch.from_numpy(rng.integers(0, 1000, n).astype(np.int32)).cuda()
+    relh = rng.integers(0, R, n).astype(np.int32)
+    rel = torch.from_numpy(relh).cuda()
+    ctx = pbg.pbg_bucket_init(1000, 1, R, 8, "diagonal", "dot", "ranking")
+    try:
+        outs = [torch.empty(n, dtype=torch.int32, device="cuda") for _ in range(3)]
+        pbg.pbg_group_by_relation(ctx, src, rel, dst, *outs)
+        order = np.argsort(relh, kind="stable")
+        assert np.array_equal(outs[0].cpu().numpy(), src.cpu().numpy()[order])
+        assert np.array_equal(outs[1].cpu().numpy(), relh[order])
+        assert np.array_equal(outs[2].cpu().numpy(), dst.cpu().numpy()[order])
+        bad = rel.clone()
+        bad[17] = R
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_group_by_relation(ctx, src, bad, dst, *outs)
+        assert ei.value.status_name == "INVALID_ARG"
+    finally:
+        pbg.pbg_free(ctx)
+    # cos + operator + several relations: consecutive chunks are refused, and
+    # unsorted relations with relation-grouped chunks leave everything untouched
+    pb = make_problem("translation", "cos", "ranking", n=60, R=3, m=80, seed=4)
+    gm = GpuModel(pb)
+    try:
+        before = gm.state()
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_train_bucket(gm.ctx, 0, 0, gm.src, gm.rel_ids, gm.dst, 16, 8, 2, 0.1, 1)
+        assert ei.value.status_name == "UNSUPPORTED"
+        unsorted = gm.rel_ids.clone()
+        unsorted[0], unsorted[1] = 2, 0
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_train_bucket(gm.ctx, 0, 0, gm.src, unsorted, gm.dst, 16, 8, 2, 0.1, 1, chunking="by_relation")
+        assert ei.value.status_name == "INVALID_ARG"
+        after = gm.state()
+        assert np.array_equal(before["emb"][0], after["emb"][0]) and np.array_equal(before["rel"], after["rel"])
+        ranks = torch.empty(2 * 4, dtype=torch.int32, device="cuda")
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_rank_eval(gm.ctx, gm.src[:4], gm.rel_ids[:4], gm.dst[:4], gm.src, gm.rel_ids, gm.dst, ranks)
+        assert ei.value.status_name == "UNSUPPORTED"
+    finally:
+        gm.close()
+    with pytest.raises(pbg.PbgError) as ei:
+        pbg.pbg_bucket_init(100, 1, 3, 8, "linear", "cos", "ranking")
+    assert ei.value.status_name == "UNSUPPORTED"
