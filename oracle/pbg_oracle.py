@@ -43,7 +43,12 @@ with its reason, in the design notes of the repository):
     starts from G = 0; relations use element-wise Adagrad with the same lr;
   * the gradient of a step is taken at the step-start parameters (batch-
     synchronous update of S chunks; S = 40 by default);
-  * rank ties count against the model; filtered = known triples removed.
+  * rank ties count against the model; filtered = known triples removed;
+  * reciprocal predicates (Sec. 5.4, separate relation parameters for the
+    source and destination negatives): relation r keeps a second parameter
+    row r + R; the source-corruption side scores sim(g(x_d, theta_{r+R}), x_t)
+    with its own positive sim(g(x_d, theta_{r+R}), x_s), while the destination
+    side and the edge score f keep theta_r.
 """
 
 from __future__ import annotations
@@ -245,17 +250,18 @@ class Model:
     margin: float = 0.1
     emb: dict = field(default_factory=dict)      # p -> (rows, d) float64
     G: dict = field(default_factory=dict)        # p -> (rows,) float64, row-summed Adagrad
-    rel: np.ndarray | None = None                # (R, width) float64
-    relG: np.ndarray | None = None               # (R, width) float64, element-wise Adagrad
+    rel: np.ndarray | None = None                # (R or 2R, width) float64
+    relG: np.ndarray | None = None               # (R or 2R, width) float64, element-wise Adagrad
+    reciprocal: bool = False                     # rows R..2R-1 of rel: the source-side parameters
 
     @staticmethod
     def create(n, P, R, d, op, cmp, loss, margin, emb_parts, rel_params=None,
-               G_parts=None, relG=None):
+               G_parts=None, relG=None, reciprocal=False):
         if op not in OPERATORS or cmp not in COMPARATORS or loss not in LOSSES:
             raise ValueError("unknown operator, comparator or loss")
         if op == "complex_diagonal" and d % 2:
             raise ValueError("complex_diagonal needs an even dimension")
-        m = Model(n, P, R, d, op, cmp, loss, float(margin))
+        m = Model(n, P, R, d, op, cmp, loss, float(margin), reciprocal=bool(reciprocal))
         for p in range(P):
             e = np.array(emb_parts[p], dtype=np.float64)
             assert e.shape == (partition_rows(n, P, p), d)
@@ -263,10 +269,15 @@ class Model:
             m.G[p] = (np.zeros(e.shape[0]) if G_parts is None
                       else np.array(G_parts[p], dtype=np.float64))
         width = relation_param_width(op, d)
+        rows = 2 * R if reciprocal else R
         if width:
-            m.rel = np.array(rel_params, dtype=np.float64).reshape(R, width)
-            m.relG = np.zeros_like(m.rel) if relG is None else np.array(relG, np.float64).reshape(R, width)
+            m.rel = np.array(rel_params, dtype=np.float64).reshape(rows, width)
+            m.relG = np.zeros_like(m.rel) if relG is None else np.array(relG, np.float64).reshape(rows, width)
         return m
+
+    def reverse_rel(self, r):
+        """Parameter row of the source side of relation r (reciprocal: r + R)."""
+        return np.asarray(r, dtype=np.int64) + (self.R if self.reciprocal else 0)
 
 
 # --------------------------------------------------------------------------
@@ -300,6 +311,22 @@ def chunk_scores(op, cmp, xs, xd, theta_e, rel_e, cand_dst, cand_src, theta_of):
         order.append(idx)
     S1 = torch.cat(rows, 0)[np.argsort(np.concatenate(order), kind="stable")]
     return p, S0, S1
+
+
+def chunk_scores_reciprocal(op, cmp, xs, xd, theta_fwd, theta_rev, cand_dst, cand_src):
+    """Scores of one chunk with reciprocal predicates (Sec. 5.4): each side
+    compares the operator applied to the entity it keeps with the raw
+    candidates of the side it corrupts.
+
+    theta_fwd (C, w) theta_r of each edge, theta_rev (C, w) theta_{r+R} (None
+    for identity).  Returns p0 (C,) = sim(g(x_s, theta_r), x_d), p1 (C,) =
+    sim(g(x_d, theta_{r+R}), x_s), S0 (C, N) with S0[e, t] = sim(g(x_s,
+    theta_r), cand_dst[t]) and S1 (C, N) with S1[e, t] = sim(g(x_d,
+    theta_{r+R}), cand_src[t])."""
+    q = apply_operator(op, xs, theta_fwd)
+    k = apply_operator(op, xd, theta_rev)
+    return (compare_rows(cmp, q, xd), compare_rows(cmp, k, xs),
+            compare_all(cmp, q, cand_dst), compare_all(cmp, k, cand_src))
 
 
 def side_loss(loss, margin, p, S, valid, active=None):
@@ -432,6 +459,8 @@ def step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=True, b
         leaf[p] = torch.tensor(model.emb[p][ids], dtype=_F64, requires_grad=with_grad)
         ids_of[p] = ids
     step_rels = np.unique(np.concatenate([rel[lo:hi] for (_, lo, hi) in step]))
+    if model.reciprocal:
+        step_rels = np.unique(np.concatenate([step_rels, model.reverse_rel(step_rels)]))
     rel_leaf = None
     if model.rel is not None:
         rel_leaf = torch.tensor(model.rel[step_rels], dtype=_F64, requires_grad=with_grad)
@@ -450,18 +479,25 @@ def step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=True, b
         cand_dst = torch.cat([xd, rows(j, u_dst)], 0)
         cand_src = torch.cat([xs, rows(i, u_src)], 0)
         r_e = rel[lo:hi]
-        theta_e = None
+        theta_e = theta_rev = None
         if rel_leaf is not None:
             theta_e = rel_leaf[torch.from_numpy(np.searchsorted(step_rels, r_e))]
-        p, S0, S1 = chunk_scores(model.op, model.cmp, xs, xd, theta_e, r_e,
-                                 cand_dst, cand_src, theta_of)
+            if model.reciprocal:
+                theta_rev = rel_leaf[torch.from_numpy(np.searchsorted(step_rels, model.reverse_rel(r_e)))]
+        if model.reciprocal:
+            p, p1, S0, S1 = chunk_scores_reciprocal(model.op, model.cmp, xs, xd, theta_e, theta_rev,
+                                                    cand_dst, cand_src)
+        else:
+            p, S0, S1 = chunk_scores(model.op, model.cmp, xs, xd, theta_e, r_e,
+                                     cand_dst, cand_src, theta_of)
+            p1 = p
         valid = valid_mask(Cc, len(u_dst))
         act0 = act1 = None
         if branches is not None:
             act0 = torch.as_tensor(np.asarray(branches[k][0], dtype=np.float64))
             act1 = torch.as_tensor(np.asarray(branches[k][1], dtype=np.float64))
         loss = (side_loss(model.loss, model.margin, p, S0, valid, act0).sum()
-                + side_loss(model.loss, model.margin, p, S1, valid, act1).sum())
+                + side_loss(model.loss, model.margin, p1, S1, valid, act1).sum())
         if with_grad:
             loss.backward()          # gradients of the chunks add up in the leaves
         step_loss += float(loss.detach())
@@ -499,7 +535,9 @@ def inspect_step(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, se
       dS0, dS1 (C_c, C_c + U) dL/dS of each side with p held fixed, 0 on the
                               excluded induced positive
       dp     (C_c,)           dL/dp_e (both sides, scores held fixed)
-    all float64 numpy arrays."""
+    all float64 numpy arrays.  With reciprocal predicates each side has its own
+    positive: p and dp belong to the destination side, p1 and dp1 to the
+    source side."""
     src = np.asarray(src, dtype=np.int64)
     dst = np.asarray(dst, dtype=np.int64)
     m = src.shape[0]
@@ -516,20 +554,29 @@ def inspect_step(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, se
             cand_src = torch.cat([xs, torch.tensor(model.emb[i][u_src], dtype=_F64)], 0)
             r_e = rel[lo:hi]
             theta_e = None if theta_all is None else theta_all[torch.from_numpy(r_e)]
-            p, S0, S1 = chunk_scores(model.op, model.cmp, xs, xd, theta_e, r_e, cand_dst, cand_src,
-                                     lambda r: None if theta_all is None else theta_all[r])
+            if model.reciprocal:
+                theta_rev = None if theta_all is None else theta_all[torch.from_numpy(model.reverse_rel(r_e))]
+                p, p1, S0, S1 = chunk_scores_reciprocal(model.op, model.cmp, xs, xd, theta_e, theta_rev,
+                                                        cand_dst, cand_src)
+            else:
+                p, S0, S1 = chunk_scores(model.op, model.cmp, xs, xd, theta_e, r_e, cand_dst, cand_src,
+                                         lambda r: None if theta_all is None else theta_all[r])
             valid = valid_mask(hi - lo, U)
             rec = {"p": p.numpy()}
             pg = p.clone().requires_grad_(True)
-            for side, S in ((0, S0), (1, S1)):
+            pg1 = p1.clone().requires_grad_(True) if model.reciprocal else pg
+            for side, S, pp in ((0, S0, pg), (1, S1, pg1)):
                 Sg = S.clone().requires_grad_(True)
                 with torch.enable_grad():
-                    L = side_loss(model.loss, model.margin, pg, Sg, valid)
+                    L = side_loss(model.loss, model.margin, pp, Sg, valid)
                     L.sum().backward()
                 rec[f"S{side}"] = S.numpy()
                 rec[f"loss{side}"] = L.detach().numpy()
                 rec[f"dS{side}"] = Sg.grad.numpy()
             rec["dp"] = pg.grad.numpy()
+            if model.reciprocal:
+                rec["p1"] = p1.numpy()
+                rec["dp1"] = pg1.grad.numpy()
             out.append(rec)
     return out
 
@@ -568,7 +615,8 @@ def rank_eval(model: Model, src, rel, dst, known_src, known_rel, known_dst, tol:
     """Filtered ranks of each triple among all entities (single partition).
 
     Destination side: 1 + #{d' != d : (s, r, d') not known, f(s, r, d') >= f(s, r, d)};
-    source side symmetric.  Returns (ranks[2n] -- destination side first, then
+    source side symmetric (with reciprocal predicates its scores, the true
+    source's included, are sim(g(x_d, theta_{r+R}), x_s')).  Returns (ranks[2n] -- destination side first, then
     source side --, MRR, Hits@10).  With tol > 0 it also returns the ranks that
     count only candidates with f >= f_pos + tol and those counting f >= f_pos - tol:
     bounds for a computation whose scores carry an error up to tol."""
@@ -596,9 +644,16 @@ def rank_eval(model: Model, src, rel, dst, known_src, known_rel, known_dst, tol:
             # destination corruptions f(s, r, d') for every d'
             q = apply_operator(model.op, allx[s:s + 1], theta)
             sc_d = compare_all(model.cmp, q, allx)[0].numpy()
-            # source corruptions f(s', r, d) for every s'
-            g_all = apply_operator(model.op, allx, theta)
-            sc_s = compare_all(model.cmp, allx[d:d + 1], g_all)[0].numpy()
+            if model.reciprocal:
+                # source corruptions scored by the reciprocal relation:
+                # sim(g(x_d, theta_{r+R}), x_s') for every s'
+                th_rev = None if model.rel is None else torch.tensor(model.rel[r + model.R], dtype=_F64)
+                k = apply_operator(model.op, allx[d:d + 1], th_rev)
+                sc_s = compare_all(model.cmp, k, allx)[0].numpy()
+            else:
+                # source corruptions f(s', r, d) for every s'
+                g_all = apply_operator(model.op, allx, theta)
+                sc_s = compare_all(model.cmp, allx[d:d + 1], g_all)[0].numpy()
             for side, sc, true_id in ((0, sc_d, d), (1, sc_s, s)):
                 keep = np.ones(n, bool)
                 keep[true_id] = False
@@ -622,8 +677,9 @@ def rank_sampled(model: Model, src, rel, dst, cand, tol: float = 0.0):
     prevalence; the caller draws them).
 
     Destination side: 1 + #{j : cand[j] != d, f(s, r, cand[j]) >= f(s, r, d)};
-    source side: 1 + #{j : cand[j] != s, f(cand[j], r, d) >= f(s, r, d)}.  No
-    filter; a candidate listed k times counts k times.  Same return values as
+    source side: 1 + #{j : cand[j] != s, f(cand[j], r, d) >= f(s, r, d)} (with
+    reciprocal predicates sim(g(x_d, theta_{r+R}), .) on both sides of the
+    comparison).  No filter; a candidate listed k times counts k times.  Same return values as
     rank_eval (with tol > 0, also the rank bounds for scores within tol)."""
     assert model.P == 1
     E = model.emb[0]
@@ -641,10 +697,17 @@ def rank_sampled(model: Model, src, rel, dst, cand, tol: float = 0.0):
             s, r, d = int(src[e]), int(rel[e]), int(dst[e])
             theta = None if model.rel is None else torch.tensor(model.rel[r], dtype=_F64)
             q = apply_operator(model.op, allx[s:s + 1], theta)
-            pos_score = float(compare_rows(model.cmp, q, allx[d:d + 1])[0])
+            pos_dst = float(compare_rows(model.cmp, q, allx[d:d + 1])[0])
             sc_d = compare_all(model.cmp, q, cx)[0].numpy()                  # f(s, r, c)
-            sc_s = compare_all(model.cmp, allx[d:d + 1], apply_operator(model.op, cx, theta))[0].numpy()  # f(c, r, d)
-            for side, sc, true_id in ((0, sc_d, d), (1, sc_s, s)):
+            if model.reciprocal:
+                th_rev = None if model.rel is None else torch.tensor(model.rel[r + model.R], dtype=_F64)
+                k = apply_operator(model.op, allx[d:d + 1], th_rev)
+                pos_src = float(compare_rows(model.cmp, k, allx[s:s + 1])[0])
+                sc_s = compare_all(model.cmp, k, cx)[0].numpy()
+            else:
+                pos_src = pos_dst
+                sc_s = compare_all(model.cmp, allx[d:d + 1], apply_operator(model.op, cx, theta))[0].numpy()  # f(c, r, d)
+            for side, sc, true_id, pos_score in ((0, sc_d, d, pos_dst), (1, sc_s, s, pos_src)):
                 keep = cand != true_id
                 slot = e if side == 0 else len(src) + e
                 ranks[slot] = 1 + int(np.count_nonzero(keep & (sc >= pos_score)))

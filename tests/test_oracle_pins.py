@@ -802,3 +802,225 @@ def test_relation_grouped_training_matches_explicit_chunks():
         lb += O.train_bucket(b, 0, 0, src[lo:hi], rel[lo:hi], dst[lo:hi], 3, 2, 1, 0.1, 5, first_chunk=c)
     assert abs(la - lb) < 1e-12
     assert np.allclose(a.emb[0], b.emb[0], atol=1e-15, rtol=0) and np.allclose(a.rel, b.rel, atol=1e-15, rtol=0)
+
+
+# ------------------------------------------------ reciprocal predicates (Sec. 5.4)
+def _adjoint_params(op, th):
+    """Parameters of the operator that is the adjoint of g(., th) under the dot
+    product: theta itself for diagonal (and identity), conj(theta) for complex."""
+    th = np.asarray(th, dtype=np.float64)
+    if op == "complex_diagonal":
+        h = th.shape[-1] // 2
+        return np.concatenate([th[..., :h], -th[..., h:]], -1)
+    return th.copy()
+
+
+def _reciprocal_twin(base, rev_rows):
+    return O.Model.create(base.n, base.P, base.R, base.d, base.op, base.cmp, base.loss, base.margin,
+                          [base.emb[p] for p in range(base.P)], np.concatenate([base.rel, rev_rows]),
+                          reciprocal=True)
+
+
+@pytest.mark.parametrize("op", ["diagonal", "complex_diagonal"])
+@pytest.mark.parametrize("loss", O.LOSSES)
+def test_reciprocal_with_adjoint_rows_reproduces_the_shared_operator(op, loss):
+    """With dot, <g(x_t, th), x_d> = <x_t, g*(x_d, th)>.  A reciprocal model whose
+    source-side rows r + R hold the adjoint's parameters scores every source
+    corruption as the ordinary model does: same scores, losses and entity
+    gradients, and the ordinary model's relation gradient is row r's plus row
+    r + R's mapped back through the adjoint (a self-inverse linear map).
+    Complex parameters make rows r and r + R differ, so reading row r on the
+    source side fails here."""
+    base = _tiny_model(op, "dot", loss, R=3, seed=3)
+    recip = _reciprocal_twin(base, _adjoint_params(op, base.rel))
+    i, j = 0, 1
+    src, rel, dst = _tiny_edges(base, i, j, 7, 3)
+    step = O.chunk_ranges(7, 3)
+    negs = O.step_negatives(base, i, j, step, 9, 2)
+    la, ga, ra = O.step_loss_and_grad(base, i, j, src, rel, dst, step, negs)
+    lb, gb, rb = O.step_loss_and_grad(recip, i, j, src, rel, dst, step, negs)
+    assert abs(la - lb) < 1e-12 * max(1.0, abs(la))
+    for p in ga:
+        assert np.array_equal(ga[p][0], gb[p][0])
+        assert np.allclose(ga[p][1], gb[p][1], atol=1e-12, rtol=0)
+    ids_b = list(rb[0])
+    for a, r in enumerate(ra[0]):
+        fwd = rb[1][ids_b.index(r)]
+        rev = rb[1][ids_b.index(r + base.R)]
+        assert np.allclose(ra[1][a], fwd + _adjoint_params(op, rev), atol=1e-12, rtol=0)
+    ins_a = O.inspect_step(base, i, j, src, rel, dst, 3, 2, 9)
+    ins_b = O.inspect_step(recip, i, j, src, rel, dst, 3, 2, 9)
+    for ca, cb in zip(ins_a, ins_b):
+        for key in ("S0", "S1", "loss0", "loss1", "dS0", "dS1"):
+            assert np.allclose(ca[key], cb[key], atol=1e-12, rtol=0), key
+        assert np.allclose(cb["p1"], ca["p"], atol=1e-12, rtol=0)
+        assert np.allclose(cb["dp"] + cb["dp1"], ca["dp"], atol=1e-12, rtol=0)
+
+
+@pytest.mark.parametrize("op,cmp", [(o, c) for o in O.OPERATORS for c in O.COMPARATORS])
+def test_reciprocal_sides_swap_roles(op, cmp):
+    """The source side of edge (s, r, d) is the destination side of (d, r + R, s)
+    with the row roles exchanged; and each entry is the explicit-loop
+    operator and comparator (the independent statement pinned above)."""
+    rng = np.random.default_rng(21)
+    d, C, U = 4, 3, 2
+    w = max(O.relation_param_width(op, d), 1)
+    src_rows = rng.standard_normal((C + U, d))
+    dst_rows = rng.standard_normal((C + U, d))
+    thf = rng.standard_normal((C, w))
+    thr = rng.standard_normal((C, w))
+    xs, xd = torch.tensor(src_rows[:C]), torch.tensor(dst_rows[:C])
+    cs, cd = torch.tensor(src_rows), torch.tensor(dst_rows)
+    tf = None if op == "identity" else torch.tensor(thf)
+    tr = None if op == "identity" else torch.tensor(thr)
+    p0, p1, S0, S1 = O.chunk_scores_reciprocal(op, cmp, xs, xd, tf, tr, cd, cs)
+    q0, q1, T0, T1 = O.chunk_scores_reciprocal(op, cmp, xd, xs, tr, tf, cs, cd)
+    assert torch.equal(p0, q1) and torch.equal(p1, q0)
+    assert torch.equal(S0, T1) and torch.equal(S1, T0)
+    for e in range(C):
+        gq = _py_operator(op, list(src_rows[e]), list(thf[e]))
+        gk = _py_operator(op, list(dst_rows[e]), list(thr[e]))
+        assert abs(p0[e].item() - _py_sim(cmp, gq, list(dst_rows[e]))) < 1e-12
+        assert abs(p1[e].item() - _py_sim(cmp, gk, list(src_rows[e]))) < 1e-12
+        for t in range(C + U):
+            assert abs(S0[e, t].item() - _py_sim(cmp, gq, list(dst_rows[t]))) < 1e-12
+            assert abs(S1[e, t].item() - _py_sim(cmp, gk, list(src_rows[t]))) < 1e-12
+
+
+def test_reciprocal_translation_logistic_gradient_closed_form():
+    """translation + dot + logistic, reciprocal: with k_e = x_d + theta_{r+R},
+    p1 = <k_e, x_s> and S1[e, t] = <k_e, c_t>, the source side contributes
+    dL/dtheta_{r+R} = sum over the edges of r of (sigmoid(p1) - 1) x_s +
+    (1 / K_e) sum over valid t of sigmoid(S1[e, t]) c_t, and nothing to theta_r;
+    the destination side likewise gives theta_r's gradient with x_s + theta_r."""
+    base = _tiny_model("translation", "dot", "logistic", R=2, seed=8)
+    rng = np.random.default_rng(8)
+    recip = _reciprocal_twin(base, rng.standard_normal(base.rel.shape) * 0.5)
+    i, j = 1, 0
+    src, rel, dst = _tiny_edges(base, i, j, 5, 8)
+    step = O.chunk_ranges(5, 5)
+    negs = O.step_negatives(base, i, j, step, 4, 3)
+    _, _, (ids, g) = O.step_loss_and_grad(recip, i, j, src, rel, dst, step, negs)
+    R = base.R
+    expect = {r: np.zeros(base.d) for r in range(2 * R)}
+    u_dst, u_src = negs[0]
+    Xs, Xd = recip.emb[i][src], recip.emb[j][dst]
+    cand_src = np.concatenate([Xs, recip.emb[i][u_src]])
+    cand_dst = np.concatenate([Xd, recip.emb[j][u_dst]])
+    sig = lambda v: 1.0 / (1.0 + math.exp(-v))
+    for e in range(len(src)):
+        r = int(rel[e])
+        for row, anchor, other, cands in ((r, Xs[e], Xd[e], cand_dst), (r + R, Xd[e], Xs[e], cand_src)):
+            k = anchor + recip.rel[row]
+            K = len(cands) - 1
+            acc = (sig(float(k @ other)) - 1.0) * other
+            for t in range(len(cands)):
+                if t != e:
+                    acc = acc + sig(float(k @ cands[t])) * cands[t] / K
+            expect[row] += acc
+    for a, row in enumerate(ids):
+        assert np.allclose(g[a], expect[int(row)], atol=1e-12, rtol=0), row
+
+
+RECIP_COMBOS = [("translation", "cos", "ranking"), ("complex_diagonal", "dot", "softmax"),
+                ("linear", "cos", "logistic"), ("diagonal", "cos", "softmax"), ("linear", "dot", "ranking"),
+                ("identity", "dot", "logistic")]
+
+
+@pytest.mark.parametrize("op,cmp,loss", RECIP_COMBOS)
+def test_reciprocal_step_gradient_matches_finite_differences(op, cmp, loss):
+    """The reciprocal step gradient (several relations, relations mixed inside
+    the chunks, cos with an operator included) against central differences of
+    the step loss."""
+    i, j = 0, 1
+    for seed in range(20):
+        base = _tiny_model(op, cmp, loss, R=2, seed=seed)
+        rev = None if base.rel is None else base.rel[::-1].copy() * 0.9
+        model = base if base.rel is None else _reciprocal_twin(base, rev)
+        model.reciprocal = True
+        src, rel, dst = _tiny_edges(model, i, j, 7, seed)
+        step = O.chunk_ranges(7, 3)
+        negs = O.step_negatives(model, i, j, step, seed + 5, 2)
+        if loss != "ranking":
+            break
+        ins = O.inspect_step(model, i, j, src, rel, dst, 3, 2, seed + 5)
+        z = [np.abs(model.margin - c[pk][:, None] + c[sk])[O.valid_mask(len(c[pk]), 2).numpy() > 0]
+             for c in ins for pk, sk in (("p", "S0"), ("p1", "S1"))]
+        if min(float(v.min()) for v in z) > 1e-3:
+            break
+    _, grads, rel_grad = O.step_loss_and_grad(model, i, j, src, rel, dst, step, negs)
+    h = 1e-6
+
+    def f():
+        return O.step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=False)[0]
+
+    def check(arr, idx, gval):
+        keep = arr[idx]
+        arr[idx] = keep + h
+        up = f()
+        arr[idx] = keep - h
+        dn = f()
+        arr[idx] = keep
+        fd = (up - dn) / (2 * h)
+        assert abs(fd - gval) <= 1e-6 * max(1.0, abs(gval)), (idx, fd, gval)
+
+    for p, (ids, g) in grads.items():
+        for a, row in enumerate(ids):
+            for k in range(model.d):
+                check(model.emb[p], (row, k), g[a, k])
+    if rel_grad is not None:
+        ids, g = rel_grad
+        assert set(ids.tolist()) - set(range(model.R)), "no source-side row was touched"
+        for a, r in enumerate(ids):
+            for k in range(0, model.rel.shape[1], max(1, model.rel.shape[1] // 8)):
+                check(model.rel, (r, k), g[a, k])
+
+
+@pytest.mark.parametrize("op", ["diagonal", "complex_diagonal"])
+def test_reciprocal_ranks_with_adjoint_rows_equal_the_shared_operator(op):
+    rng = np.random.default_rng(31)
+    n, R, d = 9, 2, 4
+    E = rng.standard_normal((n, d))
+    th = rng.standard_normal((R, d))
+    base = O.Model.create(n, 1, R, d, op, "dot", "ranking", 0.1, [E], th)
+    recip = _reciprocal_twin(base, _adjoint_params(op, th))
+    src = np.array([0, 3, 5, 5, 8])
+    rel = np.array([1, 0, 1, 1, 0])
+    dst = np.array([2, 4, 6, 0, 1])
+    ka = O.rank_eval(base, src, rel, dst, src, rel, dst)[0]
+    kb = O.rank_eval(recip, src, rel, dst, src, rel, dst)[0]
+    assert np.array_equal(ka, kb)
+    cand = rng.integers(0, n, 12)
+    assert np.array_equal(O.rank_sampled(base, src, rel, dst, cand)[0], O.rank_sampled(recip, src, rel, dst, cand)[0])
+
+
+def test_reciprocal_rank_eval_brute_force():
+    """Source side of a reciprocal model: 1 + #{c != s, (c, r, d) not known,
+    sim(g(x_d, theta_{r+R}), x_c) >= sim(g(x_d, theta_{r+R}), x_s)}; translation
+    with cos, explicit loops."""
+    rng = np.random.default_rng(33)
+    n, R, d = 8, 2, 3
+    E = rng.standard_normal((n, d))
+    rows = rng.standard_normal((2 * R, d))
+    model = O.Model.create(n, 1, R, d, "translation", "cos", "ranking", 0.1, [E], rows, reciprocal=True)
+    src = np.array([0, 3, 5, 7])
+    rel = np.array([1, 0, 1, 0])
+    dst = np.array([2, 4, 6, 1])
+    ks = np.concatenate([src, [0, 2, 1]])
+    kr = np.concatenate([rel, [1, 0, 1]])
+    kd = np.concatenate([dst, [5, 4, 6]])
+    known = set(zip(ks.tolist(), kr.tolist(), kd.tolist()))
+    ranks = O.rank_eval(model, src, rel, dst, ks, kr, kd)[0]
+    cand = np.array([1, 1, 4, 0, 6, 3])
+    sranks = O.rank_sampled(model, src, rel, dst, cand)[0]
+    for e in range(len(src)):
+        s, r, t = int(src[e]), int(rel[e]), int(dst[e])
+        q = _py_operator("translation", list(E[s]), list(rows[r]))
+        k = _py_operator("translation", list(E[t]), list(rows[r + R]))
+        p0, p1 = _py_sim("cos", q, list(E[t])), _py_sim("cos", k, list(E[s]))
+        rd = 1 + sum(1 for c in range(n) if c != t and (s, r, c) not in known and _py_sim("cos", q, list(E[c])) >= p0)
+        rs = 1 + sum(1 for c in range(n) if c != s and (c, r, t) not in known and _py_sim("cos", k, list(E[c])) >= p1)
+        assert ranks[e] == rd and ranks[len(src) + e] == rs
+        sd = 1 + sum(1 for c in cand if c != t and _py_sim("cos", q, list(E[c])) >= p0)
+        ss = 1 + sum(1 for c in cand if c != s and _py_sim("cos", k, list(E[c])) >= p1)
+        assert sranks[e] == sd and sranks[len(src) + e] == ss
