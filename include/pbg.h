@@ -78,7 +78,16 @@ enum {
    * (score_ms and score_timed_steps in pbg_stats); PBG_F_PHASE_TIMING times
    * it on every step.  With bf16 score inputs the bracket holds the score
    * contraction alone, not the rounding of its operands. */
-  PBG_F_SCORE_TIMING = 4u
+  PBG_F_SCORE_TIMING = 4u,
+  /* Reciprocal predicates (Sec. 5.4: separate relation parameters for source
+   * and destination negatives).  Relation r keeps a second parameter row
+   * r + R.  The destination side scores sim(g(x_s, theta_r), x_t) as without
+   * the flag; the source side scores sim(g(x_d, theta_{r+R}), x_t), with its
+   * own positive sim(g(x_d, theta_{r+R}), x_s), so the operator never touches
+   * a candidate.  The edge score f (pbg_score_edges) uses theta_r; the source
+   * side of pbg_rank_eval / pbg_rank_sampled uses theta_{r+R}.  Every operator
+   * and comparator works with any number of relations and either chunking. */
+  PBG_F_RECIPROCAL = 8u
 };
 
 /* Where a bound partition lives. */
@@ -144,13 +153,14 @@ typedef struct {
  * remainder (Sec. 4.1), num_relations relations, embedding dimension dim.
  * Returns INVALID_ARG for unknown enums, dim < 1 or dim > 512, odd dim with
  * COMPLEX_DIAGONAL, P < 1, a partition left empty, num_relations < 1 or a
- * non-finite margin; UNSUPPORTED for COS with the LINEAR operator and more
- * than one relation.  COS with another operator and several relations is
- * trained with relation-grouped chunks only (PBG_CHUNK_BY_RELATION; with
- * consecutive chunks the training calls return UNSUPPORTED: the source
- * corruptions of an edge need its own relation's operator applied to every
- * candidate before the normalisation), and pbg_rank_eval / pbg_rank_sampled
- * return UNSUPPORTED for it. */
+ * non-finite margin.  Without PBG_F_RECIPROCAL: UNSUPPORTED for COS with the
+ * LINEAR operator and more than one relation; COS with another operator and
+ * several relations is trained with relation-grouped chunks only
+ * (PBG_CHUNK_BY_RELATION; with consecutive chunks the training calls return
+ * UNSUPPORTED: the source corruptions of an edge need its own relation's
+ * operator applied to every candidate before the normalisation), and
+ * pbg_rank_eval / pbg_rank_sampled return UNSUPPORTED for it.  With
+ * PBG_F_RECIPROCAL none of these limits applies. */
 pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_partitions,
                            int32_t num_relations, int32_t dim, int32_t op, int32_t cmp,
                            int32_t loss, float margin, uint32_t flags);
@@ -168,7 +178,8 @@ const char* pbg_last_error(const pbg_ctx* ctx);
 int64_t pbg_partition_rows(const pbg_ctx* ctx, int32_t p);
 
 /* Floats of all relation parameters: R*dim (translation, diagonal, complex),
- * R*dim*dim (linear) or 0 (identity). */
+ * R*dim*dim (linear) or 0 (identity); twice that with PBG_F_RECIPROCAL (rows
+ * 0..R-1 for theta_r, rows R..2R-1 for the source side's theta_{r+R}). */
 int64_t pbg_relation_param_floats(const pbg_ctx* ctx);
 
 /* Edge bucketing (Sec. 4.1): edge (s, r, d) with global ids goes to bucket
@@ -195,8 +206,8 @@ pbg_status pbg_bucket_edges(pbg_ctx* ctx, const int64_t* src, const int32_t* rel
  * calls (every call is synchronous on return). */
 pbg_status pbg_bind_partition(pbg_ctx* ctx, int32_t p, float* emb, float* adagrad, int32_t where);
 
-/* Binds the relation parameters (device, [R x width] float32, width as in
- * pbg_relation_param_floats / R) and their element-wise Adagrad accumulators
+/* Binds the relation parameters (device, [R x width] float32, or [2R x width]
+ * with PBG_F_RECIPROCAL; width = dim, dim*dim for LINEAR) and their element-wise Adagrad accumulators
  * (same shape).  Not needed (and ignored) for IDENTITY.  Lifetime as for
  * pbg_bind_partition: both buffers must stay allocated until they are bound
  * again or pbg_free. */
@@ -315,7 +326,8 @@ pbg_status pbg_sample_negatives(pbg_ctx* ctx, int32_t i, int32_t j, int64_t firs
  *   dscores   [nch][2][chunk_size][N]: dL/dS as the epilogue left it (0 on the
  *             excluded induced positive);
  *   row_loss  [nch][2][chunk_size]: each edge's loss on each side;
- *   pos       [nch][chunk_size]: the positive scores p_e.
+ *   pos       [nch][chunk_size]: the positive scores p_e; with
+ *             PBG_F_RECIPROCAL [nch][2][chunk_size], each side's own positive.
  * loss_host (nullable) receives the summed loss of the step. */
 pbg_status pbg_inspect_step(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
                             const int32_t* rel, const int32_t* dst_local, int64_t n_edges,

@@ -6,7 +6,9 @@
 //
 // Packed float32 buffers (row stride dp = dim rounded up to 4, pad columns 0):
 //   qk  [S][2][C][dp]   side 0: Q = g(x_s) (dot) or its unit vector (cos)
-//                       side 1: K = g*(x_d) (dot) or the unit x_d (cos)
+//                       side 1: K = g*(x_d) (dot) or the unit x_d (cos);
+//                       reciprocal predicates: K = g(x_d, theta_{r+R}) (or its
+//                       unit vector), and nn holds the raw (or unit) entities
 //   nn  [S][2][N][dp]   side 0: destination candidates, side 1: source candidates
 //   ds  [S][2][C][Np]   score gradient dL/dS (raw scores between softmax passes);
 //                       for the ranking loss dL/dS is 0 or 1 and is kept as bits,
@@ -26,8 +28,9 @@ enum { CMP_DOT = 0, CMP_COS = 1 };
 // With the cos comparator the packed Q and K rows of a chunk equal its first
 // C source and destination candidate rows (g(x_s) and x_d, both normalised),
 // so Q / K row e of side s is read from row e of the candidate tile of side
-// 1 - s and never written separately.
-#define QK_IN_NN(g) ((g).cmp == CMP_COS)
+// 1 - s and never written separately.  Not with reciprocal predicates: there
+// the candidates never carry the operator and both queries do.
+#define QK_IN_NN(g) ((g).cmp == CMP_COS && !(g).recip)
 enum { LOSS_RANKING = 0, LOSS_LOGISTIC = 1, LOSS_SOFTMAX = 2 };
 
 #define PBG_EPS_NORM 1e-12f
@@ -50,7 +53,16 @@ struct StepGeom {
   uint64_t seed;
   int64_t chunk0;   // chunk number (within the bucket) of the step's first chunk
   const int32_t* cstart;  // relation-grouped chunks: bounds of the step's chunks (device), else NULL
+  int recip;        // reciprocal predicates: the source side uses relation row r + R
+  int R;            // relations (the offset of the source side's rows)
+  int relN;         // rows of relc per chunk (N; 2C with reciprocal predicates)
 };
+
+// index of edge e's positive score of side s in pos / dpos: one shared
+// score per edge, or one per side with reciprocal predicates
+__host__ __device__ inline int64_t pos_index(const StepGeom& g, int c, int side, int e) {
+  return g.recip ? ((int64_t)(c * 2 + side) * g.C + e) : ((int64_t)c * g.C + e);
+}
 
 // Chunk c of a step: its edge count and the offset of its first edge in the
 // step's edge arrays.  Consecutive chunks hold C edges each (the step's last
@@ -82,7 +94,7 @@ struct StepBufs {
   float* qk;
   float* nn;
   float* nrm;           // [S][2][N] norms of the raw vectors behind nn (cos)
-  float* pos;           // [S][C] positive scores
+  float* pos;           // [S][C] positive scores ([S][2][C] with reciprocal predicates)
   float* bias;          // [S][C] <theta_r, x_d> (translation + dot)
   int32_t* neg;         // [S][2][U] uniform draws (side 0 from partition j, side 1 from i)
   float* ds;            // [S][2][C][Np] dL/dS (logistic, softmax)
@@ -91,18 +103,22 @@ struct StepBufs {
                         // softmax, (tile max, sum exp(s - tile max))
   float* rowscale;      // [S][2][nct][C]  softmax on split pieces: exp(tile max - lse)
   float* rowloss;       // [S][2][C] each edge's loss per side (inspection only; NULL in training)
-  float* dpos;          // [S][C] dL/dp
+  float* dpos;          // [S][C] dL/dp ([S][2][C] with reciprocal predicates)
   float* dsum1;         // [S][C] sum_t dS1[e][t]
   double* chunkloss;    // [S][FIN_BLOCKS(C)]  loss partials of the finalisation
   unsigned long long* nuniq;   // rows touched by the entity updates of the call (segment count)
   unsigned int* fin_ticket;    // finished workgroups of the finalisation (zero between steps)
   float* dq;
   float* dn;
-  float* relc;          // [S][N][dr] relation gradient contributions
-  float* lin_x;         // linear + cos: [S][N][dp] raw source candidate rows x_t
-  float* lin_v;         // linear + cos: [S][N][dp] dL/d(A x_t) of the source candidates
+  float* relc;          // [S][relN][dr] relation gradient contributions: edge rows, then the
+                        // uniform source candidates' (cos with an operator) or, with
+                        // reciprocal predicates, the edges' source-side rows r + R
+  float* qnrm;          // reciprocal + cos: [S][2][C] norms of the raw queries
+  float* lin_x;         // linear + cos: [S][N][dp] raw source candidate rows x_t (reciprocal
+                        // predicates: [S][2][C][dp], the edges' raw x_s, then x_d)
+  float* lin_v;         // linear + cos, one relation: [S][N][dp] dL/d(A x_t) of the source candidates
   uint32_t* keys;       // [S*2N] sort keys of the contribution rows
   uint32_t* vals;       // [S*2N] contribution row index
-  uint32_t* rkeys;      // [S*C]  relation ids of the edges (R > 1)
-  uint32_t* rvals;      // [S*C]  relc row index
+  uint32_t* rkeys;      // relation ids of the contribution rows (R > 1 or reciprocal predicates)
+  uint32_t* rvals;      // their relc row index
 };

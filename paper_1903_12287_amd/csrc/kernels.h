@@ -63,7 +63,8 @@ struct GemmArgsH {
   int C, U, m_step;
   const int32_t* cstart;
   int nsides;
-  const float* pos;
+  const float* pos;      // positive scores [c][C], or [c][2][C] with pos_sides = 2
+  int pos_sides;         // 2: one positive score per side (reciprocal predicates)
   const float* bias;
   float* rowpart;
   int nct;

@@ -5,7 +5,8 @@
 //   dq[c][s][e] = sum_t dS_s[e][t] N_s[t]      (gradient of side s's query row)
 //   dn[c][s][t] = sum_e dS_s[e][t] Q_s[e]      (gradient of candidate row t)
 // The positive score p_e = sim(g(x_s), x_d) is computed once and shared by
-// both sides; dL/dp_e collects both sides.  op_backward folds everything that
+// both sides; dL/dp_e collects both sides.  With reciprocal predicates each
+// side has its own positive score and its own dL/dp.  op_backward folds everything that
 // reaches one embedding row of the chunk into that row's contribution,
 // in place in dn: side 0 rows are destinations (in-chunk, then uniform
 // draws from partition j), side 1 rows are sources (partition i).
@@ -23,7 +24,8 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
   const int e = blockIdx.x * FIN_THREADS + threadIdx.x;
   if (e < Cc) {
     const int64_t ce = (int64_t)c * g.C + e;
-    const float p = b.pos[ce];
+    const float p = b.pos[pos_index(g, c, 0, e)];
+    const float p1 = b.pos[pos_index(g, c, 1, e)];   // p itself without reciprocal predicates
     float l0 = 0.f, l1 = 0.f, d0 = 0.f, d1 = 0.f;
     if (g.loss != LOSS_SOFTMAX) {
       const float* r0 = b.rowpart + ((int64_t)(c * 2 + 0) * g.C + e) * g.nct * 2;
@@ -38,9 +40,49 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
       }
     }
     double loss;
-    float dp, dsum1;
+    float dp, dp1 = 0.f, dsum1;
     float side_loss[2];
-    if (g.loss == LOSS_RANKING) {
+    if (g.recip) {
+      // each side with its own positive score
+      const float ps[2] = {p, p1};
+      const float ls[2] = {l0, l1}, dsn[2] = {d0, d1};
+      float dps[2];
+      loss = 0.0;
+#pragma unroll
+      for (int side = 0; side < 2; ++side) {
+        const float pp = ps[side];
+        if (g.loss == LOSS_RANKING) {
+          side_loss[side] = ls[side];
+          dps[side] = -dsn[side];
+        } else if (g.loss == LOSS_LOGISTIC) {
+          side_loss[side] = ls[side] + softplusf(-pp);
+          dps[side] = sigmoidf(pp) - 1.0f;
+        } else {
+          const float* rp = b.rowpart + ((int64_t)(c * 2 + side) * g.C + e) * g.nct * 2;
+          float M = pp;
+          for (int ct = 0; ct < g.nct; ++ct) M = fmaxf(M, rp[2 * ct]);
+          float Z = expf(pp - M);
+          for (int ct = 0; ct < g.nct; ++ct) {
+            const float mx = rp[2 * ct];
+            if (mx > -INFINITY) Z += rp[2 * ct + 1] * expf(mx - M);
+          }
+          const float lse = M + logf(Z);
+          if (softmax_scales) {
+            float* rs = b.rowscale + (int64_t)(c * 2 + side) * g.nct * g.C + e;
+            for (int ct = 0; ct < g.nct; ++ct) {
+              const float mx = rp[2 * ct];
+              rs[(int64_t)ct * g.C] = mx > -INFINITY ? expf(mx - lse) : 0.0f;
+            }
+          }
+          side_loss[side] = lse - pp;
+          dps[side] = expf(pp - lse) - 1.0f;
+        }
+        loss += (double)side_loss[side];
+      }
+      dp = dps[0];
+      dp1 = dps[1];
+      dsum1 = 0.0f;   // no translation bias: both queries carry the operator
+    } else if (g.loss == LOSS_RANKING) {
       loss = (double)l0 + (double)l1;
       dp = -(d0 + d1);
       dsum1 = d1;
@@ -89,7 +131,8 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
       b.rowloss[(int64_t)(c * 2 + 0) * g.C + e] = side_loss[0];
       b.rowloss[(int64_t)(c * 2 + 1) * g.C + e] = side_loss[1];
     }
-    b.dpos[ce] = dp;
+    b.dpos[pos_index(g, c, 0, e)] = dp;
+    if (g.recip) b.dpos[pos_index(g, c, 1, e)] = dp1;
     b.dsum1[ce] = dsum1;
     acc += loss;
   }
@@ -127,6 +170,70 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
 }
 
 // ---- operator / comparator backward: contributions and sort keys -----------
+// Reciprocal predicates, edge e of chunk c: Q = g(x_s, theta_r) and
+// K = g(x_d, theta_{r+R}) against the entity rows (unit vectors for cos), the
+// positive scores p0 = sim(Q, x_d) and p1 = sim(K, x_s).  The source row
+// collects its candidate gradient, p1's term and J_g(theta_r)^T dQ, the
+// destination row likewise with p0 and theta_{r+R}; the two parameter rows'
+// contributions go to relc rows c relN + e and c relN + C + e.  The linear
+// operator leaves dL/dQ and dL/dK in dq for its per-edge products.
+template <int RQ>
+__device__ __forceinline__ void op_backward_reciprocal(const StepGeom& g, const StepBufs& b, int c, int e, int s,
+                                                       int t, int r, const RowT<RQ>& th, int lane) {
+  using RowR = RowT<RQ>;
+  const bool cplx = g.op == OP_COMPLEX;
+  const bool cos = g.cmp == CMP_COS;
+  const int d = g.d, dp = g.dp;
+  const float dp0 = b.dpos[pos_index(g, c, 0, e)];
+  const float dp1 = b.dpos[pos_index(g, c, 1, e)];
+  RowR tr;
+  if (g.op != OP_IDENTITY && g.op != OP_LINEAR) row_load(tr, b.relp + (int64_t)(r + g.R) * g.dr, d, cplx, lane);
+  else row_zero(tr);
+  float* dq0 = b.dq + ((int64_t)(c * 2 + 0) * g.C + e) * dp;
+  float* dq1 = b.dq + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
+  float* dn0 = b.dn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
+  float* dn1 = b.dn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
+  RowR Q, K, xh, yh, dQ, dK, dX, dY;
+  row_load(Q, b.qk + ((int64_t)(c * 2 + 0) * g.C + e) * dp, d, cplx, lane);
+  row_load(K, b.qk + ((int64_t)(c * 2 + 1) * g.C + e) * dp, d, cplx, lane);
+  row_load(yh, b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp, d, cplx, lane);
+  row_load(xh, b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp, d, cplx, lane);
+  row_load(dQ, dq0, d, cplx, lane);
+  row_load(dK, dq1, d, cplx, lane);
+  row_load(dY, dn0, d, cplx, lane);
+  row_load(dX, dn1, d, cplx, lane);
+  row_axpy(dQ, dp0, yh);   // p0 = <Q, y>
+  row_axpy(dK, dp1, xh);   // p1 = <K, x>
+  row_axpy(dY, dp0, Q);
+  row_axpy(dX, dp1, K);
+  RowR x = xh, y = yh;     // the operators' inputs
+  if (cos) {
+    dQ = normalize_backward(Q, b.qnrm[(int64_t)(c * 2 + 0) * g.C + e], dQ);
+    dK = normalize_backward(K, b.qnrm[(int64_t)(c * 2 + 1) * g.C + e], dK);
+    dY = normalize_backward(yh, b.nrm[(int64_t)(c * 2 + 0) * g.N + e], dY);
+    dX = normalize_backward(xh, b.nrm[(int64_t)(c * 2 + 1) * g.N + e], dX);
+    if (g.op == OP_DIAGONAL || g.op == OP_COMPLEX) {
+      row_load(x, b.emb_i + (int64_t)s * d, d, cplx, lane);
+      row_load(y, b.emb_j + (int64_t)t * d, d, cplx, lane);
+    }
+  }
+  if (g.op == OP_LINEAR) {
+    row_store(dQ, dq0, d, dp, cplx, lane);
+    row_store(dK, dq1, d, dp, cplx, lane);
+  } else {
+    row_add(dX, op_adjoint(g.op, dQ, th));   // identity: dQ itself
+    row_add(dY, op_adjoint(g.op, dK, tr));
+  }
+  if (g.op != OP_LINEAR && g.op != OP_IDENTITY) {
+    const RowR gf = op_param_grad(g.op, x, dQ);
+    const RowR gr = op_param_grad(g.op, y, dK);
+    row_store(gf, b.relc + ((int64_t)c * g.relN + e) * g.dr, d, g.dr, cplx, lane);
+    row_store(gr, b.relc + ((int64_t)c * g.relN + g.C + e) * g.dr, d, g.dr, cplx, lane);
+  }
+  row_store(dY, dn0, d, dp, cplx, lane);
+  row_store(dX, dn1, d, dp, cplx, lane);
+}
+
 template <int RQ>
 __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b) {
   using Row = RowT<RQ>;
@@ -151,6 +258,10 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     Row th;
     if (has_rel && g.op != OP_LINEAR) row_load(th, b.relp + (int64_t)r * g.dr, d, cplx, lane);
     else row_zero(th);
+    if (g.recip) {
+      op_backward_reciprocal(g, b, c, e, s, t, r, th, lane);
+      return;
+    }
     const float dpe = b.dpos[ce];
     float* dq0 = b.dq + ((int64_t)(c * 2 + 0) * g.C + e) * dp;
     const float* dq1 = b.dq + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
@@ -227,7 +338,7 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     float* srow = (cos && g.op == OP_LINEAR) ? b.lin_v + ((int64_t)c * g.N + e) * dp : dn1;
     row_store(gs, srow, d, dp, cplx, lane);
     if (has_rel && g.op != OP_LINEAR)
-      row_store(grel, b.relc + ((int64_t)c * g.N + e) * g.dr, d, g.dr, cplx, lane);
+      row_store(grel, b.relc + ((int64_t)c * g.relN + e) * g.dr, d, g.dr, cplx, lane);
     return;
   }
 
@@ -262,8 +373,8 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     Row th;
     // the single relation's operator was applied here (linear: A^T dv follows
     // as a contraction, the gradient of A too)
-    const bool lin_side = side == 1 && g.op == OP_LINEAR;
-    const bool op_side = side == 1 && has_rel && !lin_side;
+    const bool lin_side = side == 1 && g.op == OP_LINEAR && !g.recip;
+    const bool op_side = side == 1 && has_rel && !lin_side && !g.recip;
     // the chunk's relation (one relation, or relation-grouped chunks)
     const int rc = (op_side && b.rel && Cc > 0) ? b.rel[chunk_first(g, c)] : 0;
     if (op_side) row_load(th, b.relp + (int64_t)rc * g.dr, d, cplx, lane);
@@ -278,7 +389,7 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
           row_load(x, b.emb_i + (int64_t)u[q] * d, d, cplx, lane);
           grel = op_param_grad(g.op, x, dv);
         }
-        row_store(grel, b.relc + ((int64_t)c * g.N + g.C + k0 + q) * g.dr, d, g.dr, cplx, lane);
+        row_store(grel, b.relc + ((int64_t)c * g.relN + g.C + k0 + q) * g.dr, d, g.dr, cplx, lane);
         dv = op_adjoint(g.op, dv, th);
       }
       float* drow = lin_side ? b.lin_v + ((int64_t)c * g.N + Cc + k0 + q) * dp : b.dn + (rbase + q) * dp;

@@ -10,6 +10,9 @@
 // (<g(x), y> = <x, g*(y)>, plus <theta, y> for translation), so every
 // candidate row is copied raw.  For cos every packed row is a unit vector and
 // the source candidates carry g (one relation, or the identity operator).
+// With reciprocal predicates both queries carry an operator, Q = g(x_s,
+// theta_r) and K = g(x_d, theta_{r+R}), each side has its own positive score,
+// and every candidate row is the entity itself (a unit vector for cos).
 #include <algorithm>
 #include "kernels.h"
 #include "row_ops.h"
@@ -44,6 +47,54 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     float* krow = b.qk + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
     float* n0row = b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
     float* n1row = b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
+    if (g.recip) {
+      if (g.op == OP_LINEAR) {
+        // Q = A_r x and K = A_{r+R} y follow per edge from the raw rows (cos:
+        // kept in lin_x, the candidate rows here are unit vectors)
+        if (g.cmp == CMP_COS) {
+          row_store(x, b.lin_x + ((int64_t)(c * 2 + 0) * g.C + e) * dp, d, dp, cplx, lane);
+          row_store(y, b.lin_x + ((int64_t)(c * 2 + 1) * g.C + e) * dp, d, dp, cplx, lane);
+          const float nx = row_normalize(x);
+          const float ny = row_normalize(y);
+          if (lane == 0) {
+            b.nrm[(int64_t)(c * 2 + 0) * g.N + e] = ny;
+            b.nrm[(int64_t)(c * 2 + 1) * g.N + e] = nx;
+          }
+        }
+        row_store(y, n0row, d, dp, cplx, lane);
+        row_store(x, n1row, d, dp, cplx, lane);
+        return;
+      }
+      Row tr;
+      if (g.op != OP_IDENTITY) row_load(tr, b.relp + (int64_t)(r + g.R) * g.dr, d, cplx, lane);
+      else row_zero(tr);
+      Row gq = op_forward(g.op, x, th);
+      Row gk = op_forward(g.op, y, tr);
+      float nq = 0.f, nk = 0.f, nx = 0.f, ny = 0.f;
+      if (g.cmp == CMP_COS) {
+        nq = row_normalize(gq);
+        nk = row_normalize(gk);
+        nx = row_normalize(x);
+        ny = row_normalize(y);
+      }
+      const float p0 = row_dot(gq, y);
+      const float p1 = row_dot(gk, x);
+      row_store(gq, qrow, d, dp, cplx, lane);
+      row_store(gk, krow, d, dp, cplx, lane);
+      row_store(y, n0row, d, dp, cplx, lane);
+      row_store(x, n1row, d, dp, cplx, lane);
+      if (lane == 0) {
+        b.pos[(int64_t)(c * 2 + 0) * g.C + e] = p0;
+        b.pos[(int64_t)(c * 2 + 1) * g.C + e] = p1;
+        if (g.cmp == CMP_COS) {
+          b.nrm[(int64_t)(c * 2 + 0) * g.N + e] = ny;
+          b.nrm[(int64_t)(c * 2 + 1) * g.N + e] = nx;
+          b.qnrm[(int64_t)(c * 2 + 0) * g.C + e] = nq;
+          b.qnrm[(int64_t)(c * 2 + 1) * g.C + e] = nk;
+        }
+      }
+      return;
+    }
     if (g.op == OP_LINEAR) {
       if (g.cmp == CMP_COS) {
         // one relation: the source candidates A x_t are formed afterwards by
@@ -116,10 +167,10 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   }
   float nv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   // linear + cos: the raw source candidates go to lin_x (A x and its norm follow)
-  const bool raw_linear = g.op == OP_LINEAR && g.cmp == CMP_COS && side == 1;
+  const bool raw_linear = g.op == OP_LINEAR && g.cmp == CMP_COS && side == 1 && !g.recip;
   const bool unit = g.cmp == CMP_COS && !raw_linear;
   if (unit) {
-    if (side == 1 && g.op != OP_IDENTITY) {
+    if (side == 1 && g.op != OP_IDENTITY && !g.recip) {
       // the chunk's relation (one relation, or relation-grouped chunks): its
       // operator is applied to every source candidate
       const int rc = (b.rel && Cc > 0) ? b.rel[chunk_first(g, c)] : 0;
@@ -153,12 +204,15 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
 // holds [side 0: Nc][side 1: Nc]: (table, row) of the row each contribution
 // row reaches and, as value, that contribution row's position in the step;
 // edge e: destination t (side 0) and source s (side 1), then the uniform
-// draws of each side.  With several relations the relation of every edge is
-// keyed too (at w * rstride + f_c + e, value c N + e), and, with
-// uniform_rel, the chunk's relation for each uniform source candidate (the
-// cos comparator with an operator applies it there; at w * rstride + m_w +
-// c U + k, m_w the step's edge count, value c N + C + k).  One thread per
-// edge or per four draws; src / dst / rel start at the window's first edge.
+// draws of each side.  With several relation rows the relation of every edge
+// is keyed too (at w * rstride + f_c + e, value c relN + e, its row of the
+// relation contributions), and either, with uniform_rel, the chunk's relation
+// for each uniform source candidate (the cos comparator with an operator
+// applies it there; at w * rstride + m_w + c U + k, m_w the step's edge count,
+// value c relN + C + k) or, with reciprocal predicates, every edge's source-
+// side row r + R (at w * rstride + m_w + f_c + e, value c relN + C + e).  One
+// thread per edge or per four draws; src / dst / rel start at the window's
+// first edge.
 // Chunks: consecutive (cstart NULL: n_edges edges) or relation-grouped
 // (bounds cstart[0 .. nchunks], offsets in the call's edge arrays).
 __global__ __launch_bounds__(256) void window_keys_kernel(StepGeom g, const int32_t* src, const int32_t* dst,
@@ -188,6 +242,12 @@ __global__ __launch_bounds__(256) void window_keys_kernel(StepGeom g, const int3
   const int item = blockIdx.x * 256 + threadIdx.x;
   const uint32_t tbl_j = g.same_table ? 0u : 1u;
   const int64_t kbase = w * stride + 2 * ((int64_t)c * g.U + first);
+  int64_t m_w = 0;   // edges of the step
+  if (rkeys && (uniform_rel || g.recip)) {
+    const int64_t w0 = (int64_t)w * S;
+    if (cstart) m_w = cstart[std::min<int64_t>(w0 + S, nchunks)] - cstart[w0];
+    else m_w = std::min<int64_t>((int64_t)S * g.C, n_edges - w0 * g.C);
+  }
   if (item < Cc) {
     const int e = item;
     const int64_t eg = e0 + e;
@@ -196,9 +256,14 @@ __global__ __launch_bounds__(256) void window_keys_kernel(StepGeom g, const int3
     keys[kbase + Nc + e] = (uint32_t)src[eg];
     vals[kbase + Nc + e] = (uint32_t)((c * 2 + 1) * g.N + e);
     if (rkeys) {
+      const uint32_t r = (uint32_t)(rel ? rel[eg] : 0);
       const int64_t rw = (int64_t)w * rstride + first + e;
-      rkeys[rw] = (uint32_t)(rel ? rel[eg] : 0);
-      rvals[rw] = (uint32_t)((int64_t)c * g.N + e);
+      rkeys[rw] = r;
+      rvals[rw] = (uint32_t)((int64_t)c * g.relN + e);
+      if (g.recip) {
+        rkeys[rw + m_w] = r + (uint32_t)g.R;
+        rvals[rw + m_w] = (uint32_t)((int64_t)c * g.relN + g.C + e);
+      }
     }
     return;
   }
@@ -209,14 +274,7 @@ __global__ __launch_bounds__(256) void window_keys_kernel(StepGeom g, const int3
   const uint32_t rows = side == 0 ? (uint32_t)g.rows_j : (uint32_t)g.rows_i;
   int32_t u[4];
   uniform_negatives4(g.seed, g.bucket, (uint64_t)(chunk0 + cw), (uint32_t)side, (uint32_t)k0, rows, u);
-  int64_t m_w = 0;
-  uint32_t r_c = 0;
-  if (uniform_rel && side == 1) {
-    const int64_t w0 = (int64_t)w * S;
-    const int64_t w1 = std::min<int64_t>(w0 + S, nchunks);
-    m_w = cstart[w1] - cstart[w0];
-    r_c = (uint32_t)rel[e0];
-  }
+  const uint32_t r_c = (uniform_rel && side == 1) ? (uint32_t)rel[e0] : 0u;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int k = k0 + q;
@@ -227,7 +285,7 @@ __global__ __launch_bounds__(256) void window_keys_kernel(StepGeom g, const int3
     if (uniform_rel && side == 1) {
       const int64_t rw = (int64_t)w * rstride + m_w + (int64_t)c * g.U + k;
       rkeys[rw] = r_c;
-      rvals[rw] = (uint32_t)((int64_t)c * g.N + g.C + k);
+      rvals[rw] = (uint32_t)((int64_t)c * g.relN + g.C + k);
     }
   }
 }

@@ -240,7 +240,8 @@ __device__ __forceinline__ void load_rowv(const GemmArgsH& a, const TileGeo& t, 
     const int m = t.m0 + tid;
     const bool mrow = m < t.M;
     const int64_t o = (int64_t)t.c * a.C + m;
-    const float p = mrow ? a.pos[o] : 0.0f;
+    const int64_t op = a.pos_sides == 2 ? (int64_t)(t.c * 2 + t.side) * a.C + m : o;
+    const float p = mrow ? a.pos[op] : 0.0f;
     const float bm = (mrow && a.bias && t.side == 1) ? a.bias[o] : 0.0f;
     if (EPI == EPI_LOSS_BITS) {
       rowv[0][tid] = mrow ? a.margin - p + bm : -INFINITY;
@@ -1265,7 +1266,7 @@ __global__ __launch_bounds__(256) void softmax_rows_bf16_kernel(StepGeom g, cons
   const int Cc = chunk_edges(g, c);
   if (row >= Cc) return;
   const int Nc = Cc + g.U;
-  const float p = pos[(int64_t)c * g.C + row];
+  const float p = pos[pos_index(g, c, z & 1, row)];
   const float* rp = rowpart + ((int64_t)z * g.C + row) * g.nct * 2;
   float Mx = p;
   for (int ct = 0; ct < g.nct; ++ct) Mx = fmaxf(Mx, rp[2 * ct]);

@@ -50,12 +50,14 @@ __global__ __launch_bounds__(256) void expand_ds_kernel(StepGeom g, int mode, co
   }
 }
 
-// positive scores [c][C] (0 past a short chunk's edges)
+// positive scores [c][C], or [c][2][C] with reciprocal predicates (0 past a
+// short chunk's edges)
 __global__ __launch_bounds__(256) void copy_pos_kernel(StepGeom g, const float* pos, float* out) {
-  const int c = blockIdx.y;
+  const int z = blockIdx.y;   // chunk, or chunk * 2 + side
+  const int c = g.recip ? z >> 1 : z;
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= g.C) return;
-  out[(int64_t)c * g.C + e] = e < chunk_edges(g, c) ? pos[(int64_t)c * g.C + e] : 0.0f;
+  out[(int64_t)z * g.C + e] = e < chunk_edges(g, c) ? pos[(int64_t)z * g.C + e] : 0.0f;
 }
 
 }  // namespace
@@ -75,6 +77,6 @@ void launch_expand_ds(const StepGeom& g, int mode, const uint16_t* bits, int nw,
 
 void launch_copy_pos(const StepGeom& g, const float* pos, float* out, hipStream_t s) {
   if (g.nchunks <= 0) return;
-  dim3 grid((g.C + 255) / 256, g.nchunks);
+  dim3 grid((g.C + 255) / 256, g.nchunks * (g.recip ? 2 : 1));
   copy_pos_kernel<<<grid, 256, 0, s>>>(g, pos, out);
 }

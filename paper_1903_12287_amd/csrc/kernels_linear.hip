@@ -12,6 +12,11 @@
 //             relation segment of the sorted relation keys
 // One relation with cos: the source candidate rows A x_t (a contraction over
 // the step) are normalised here, and the positive scores follow.
+// Reciprocal predicates (any relation count, dot or cos): Q_e = A_r x_e and
+// K_e = A_{r+R} y_e per edge (normalised for cos), each side's positive score;
+// backward source row += A_r^T dQ_e, destination row += A_{r+R}^T dK_e;
+// dA_r = sum of dQ_e x_e^T and dA_{r+R} = sum of dK_e y_e^T over the sorted
+// relation keys.
 #include "kernels.h"
 #include "row_ops.h"
 
@@ -29,8 +34,39 @@ __global__ __launch_bounds__(256) void linear_rows_kernel(StepGeom g, StepBufs b
   if (e >= chunk_edges(g, c)) return;   // no block-level barriers below
   const int d = g.d, dp = g.dp;
   const int64_t ce = (int64_t)c * g.C + e;
-  const float* A = b.relp + (int64_t)b.rel[chunk_first(g, c) + e] * d * d;
+  const int r = b.rel ? b.rel[chunk_first(g, c) + e] : 0;
+  const float* A = b.relp + (int64_t)r * d * d;
   RowQ x, y, q, k;
+  if (g.recip) {
+    const bool cos = g.cmp == CMP_COS;
+    const float* Bm = b.relp + (int64_t)(r + g.R) * d * d;
+    const float* xs = cos ? b.lin_x + ((int64_t)(c * 2 + 0) * g.C + e) * dp : b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
+    const float* yd = cos ? b.lin_x + ((int64_t)(c * 2 + 1) * g.C + e) * dp : b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
+    row_load(x, xs, d, false, lane);   // raw x_s
+    row_load(y, yd, d, false, lane);   // raw x_d
+    mat_rows_apply(q, A, x, stage[w], d, lane);    // A_r x
+    mat_rows_apply(k, Bm, y, stage[w], d, lane);   // A_{r+R} y
+    if (cos) {
+      const float nq = row_normalize(q);
+      const float nk = row_normalize(k);
+      // the unit entity rows the gather stored
+      row_load(y, b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp, d, false, lane);
+      row_load(x, b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp, d, false, lane);
+      if (lane == 0) {
+        b.qnrm[(int64_t)(c * 2 + 0) * g.C + e] = nq;
+        b.qnrm[(int64_t)(c * 2 + 1) * g.C + e] = nk;
+      }
+    }
+    row_store(q, b.qk + ((int64_t)(c * 2 + 0) * g.C + e) * dp, d, dp, false, lane);
+    row_store(k, b.qk + ((int64_t)(c * 2 + 1) * g.C + e) * dp, d, dp, false, lane);
+    const float p0 = row_dot(q, y);
+    const float p1 = row_dot(k, x);
+    if (lane == 0) {
+      b.pos[(int64_t)(c * 2 + 0) * g.C + e] = p0;
+      b.pos[(int64_t)(c * 2 + 1) * g.C + e] = p1;
+    }
+    return;
+  }
   row_load(x, b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp, d, false, lane);   // raw x_s
   row_load(y, b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp, d, false, lane);   // raw x_d
   mat_rows_apply(q, A, x, stage[w], d, lane);   // A x
@@ -50,15 +86,17 @@ __global__ __launch_bounds__(256) void linear_rows_backward_kernel(StepGeom g, S
   const int e = blockIdx.x * kWaves + w;
   if (e >= chunk_edges(g, c)) return;
   const int d = g.d, dp = g.dp;
-  const int64_t ce = (int64_t)c * g.C + e;
-  const float* A = b.relp + (int64_t)b.rel[chunk_first(g, c) + e] * d * d;
+  const int r = b.rel ? b.rel[chunk_first(g, c) + e] : 0;
+  const float* A = b.relp + (int64_t)r * d * d;
   // the operator backward left dQ (with the positive score's term) in dq
-  // side 0 and dK in dq side 1
+  // side 0 and dK in dq side 1 (reciprocal predicates: the gradients of
+  // A_r x_s and A_{r+R} x_d)
   RowQ dQ, dK, ts, td;
   row_load(dQ, b.dq + ((int64_t)(c * 2 + 0) * g.C + e) * dp, d, false, lane);
   row_load(dK, b.dq + ((int64_t)(c * 2 + 1) * g.C + e) * dp, d, false, lane);
   mat_apply(ts, A, dQ, stage[w], d, lane);         // A^T dQ
-  mat_rows_apply(td, A, dK, stage[w], d, lane);    // A dK
+  if (g.recip) mat_apply(td, b.relp + (int64_t)(r + g.R) * d * d, dK, stage[w], d, lane);   // A_{r+R}^T dK
+  else mat_rows_apply(td, A, dK, stage[w], d, lane);                                        // A dK
   float* srow = b.dn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
   float* drow = b.dn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
   RowQ s0, d0;
@@ -71,8 +109,9 @@ __global__ __launch_bounds__(256) void linear_rows_backward_kernel(StepGeom g, S
 }
 
 // Sorted relation keys (stable: edges of one relation in step order); vals
-// hold chunk * N + edge.  The workgroup at the first position of a relation's
-// run sums that relation's matrix gradient over the run and applies
+// hold chunk * relN + edge (reciprocal predicates: + C for the source-side
+// row r + R, whose gradient is dK y^T).  The workgroup at the first position
+// of a relation's run sums that relation's matrix gradient over the run and applies
 // element-wise Adagrad; the others leave at once.  Every element belongs to
 // one thread, and the edges are added in order: the result is reproducible.
 constexpr int kLinBatch = 4;     // edges staged in LDS at a time
@@ -119,13 +158,29 @@ __global__ __launch_bounds__(256) void linear_relation_update_kernel(StepGeom g,
         const int eb = idx / (4 * d), rem = idx - eb * 4 * d;
         const int which = rem / d, f = rem - which * d;
         const uint32_t v = vals[q0 + eb];
-        const int c = (int)(v / (uint32_t)g.N), e = (int)(v - (uint32_t)c * g.N);
-        const float* src;
-        if (which == 0) src = b.dq + ((int64_t)(c * 2 + 0) * g.C + e) * dp;        // dQ_e
-        else if (which == 1) src = b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;   // x_e
-        else if (which == 2) src = b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;   // y_e
-        else src = b.dq + ((int64_t)(c * 2 + 1) * g.C + e) * dp;                   // dK_e
-        rows[eb][which][f] = src[f];
+        const int c = (int)(v / (uint32_t)g.relN);
+        int e = (int)(v - (uint32_t)c * g.relN);
+        float val;
+        if (g.recip) {
+          // dQ x^T (row r) or dK y^T (row r + R); the raw rows: the candidate
+          // tiles (dot) or lin_x (cos)
+          const int rev = e >= g.C ? 1 : 0;
+          e -= rev * g.C;
+          const bool cos = g.cmp == CMP_COS;
+          const float* raw = cos ? b.lin_x + ((int64_t)(c * 2 + rev) * g.C + e) * dp
+                                 : b.nn + ((int64_t)(c * 2 + 1 - rev) * g.N + e) * dp;
+          if (which == 0) val = b.dq[((int64_t)(c * 2 + rev) * g.C + e) * dp + f];
+          else if (which == 1) val = raw[f];
+          else val = 0.0f;
+        } else {
+          const float* src;
+          if (which == 0) src = b.dq + ((int64_t)(c * 2 + 0) * g.C + e) * dp;        // dQ_e
+          else if (which == 1) src = b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;   // x_e
+          else if (which == 2) src = b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;   // y_e
+          else src = b.dq + ((int64_t)(c * 2 + 1) * g.C + e) * dp;                   // dK_e
+          val = src[f];
+        }
+        rows[eb][which][f] = val;
       }
       __syncthreads();
       for (int eb = 0; eb < nb; ++eb) {

@@ -12,6 +12,10 @@
 //                     translation adds the per-query constant <theta_r, x_d>)
 //                     or the unit x_d (cos); T = the entity table (dot) or the
 //                     unit rows of g(x) under the single relation (cos).
+//   reciprocal predicates: the source side's Q = g(x_d, theta_{r+R}) (a unit
+//                     vector for cos) against the entity table, and its own
+//                     positive score sim(Q, x_s), which replaces the
+//                     destination side's in pos once that side is counted.
 // The count kernel then reads each query's row of S once, counts the
 // candidates at or above the positive score, and takes back the known
 // triples' candidates by reading the same stored scores, so that the count
@@ -56,7 +60,8 @@ __global__ __launch_bounds__(256) void rank_tables_kernel(StepGeom g, const floa
 }
 
 // queries of rows [e0, e0 + rows) for one side; side 0 also writes the
-// positive score p_e = f(s, r, d), computed as pbg_score_edges does
+// positive score p_e = f(s, r, d), computed as pbg_score_edges does, and the
+// source side with reciprocal predicates its own
 __global__ __launch_bounds__(256) void rank_queries_kernel(StepGeom g, const float* emb, const float* relp,
                                                            const float* relT, const int32_t* src,
                                                            const int32_t* rel, const int32_t* dst,
@@ -87,6 +92,26 @@ __global__ __launch_bounds__(256) void rank_queries_kernel(StepGeom g, const flo
     const float p = row_dot(gq, y);
     row_store(gq, qrow, d, g.dp, cplx, lane);
     if (lane == 0) pos[e] = p;
+  } else if (g.recip) {
+    Row k;
+    if (g.op == OP_LINEAR) {
+      mat_apply(k, relT + (int64_t)(r + g.R) * d * d, y, stage[w], d, lane);   // A_{r+R} y
+    } else {
+      Row tr;
+      if (g.op != OP_IDENTITY) row_load(tr, relp + (int64_t)(r + g.R) * g.dr, d, cplx, lane);
+      else row_zero(tr);
+      k = op_forward(g.op, y, tr);
+    }
+    if (g.cmp == CMP_COS) {
+      row_normalize(k);
+      row_normalize(x);
+    }
+    const float p1 = row_dot(k, x);
+    row_store(k, qrow, d, g.dp, cplx, lane);
+    if (lane == 0) {
+      pos[e] = p1;
+      bias[q] = 0.0f;
+    }
   } else {
     Row k;
     float bs = 0.0f;

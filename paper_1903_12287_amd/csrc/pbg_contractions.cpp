@@ -110,7 +110,8 @@ static GemmArgsH score_args_f32(const StepGeom& g, const StepBufs& b, int* epi_o
   fa.cstart = g.cstart;
   fa.nsides = 2;
   fa.pos = b.pos;
-  fa.bias = (g.op == OP_TRANSLATION && g.cmp == CMP_DOT) ? b.bias : nullptr;
+  fa.pos_sides = g.recip ? 2 : 1;
+  fa.bias = (g.op == OP_TRANSLATION && g.cmp == CMP_DOT && !g.recip) ? b.bias : nullptr;
   fa.rowpart = b.rowpart;
   fa.nct = g.nct;
   fa.loss = g.loss;
@@ -248,7 +249,8 @@ static GemmArgsH score_args_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs
   fa.cstart = g.cstart;
   fa.nsides = 2;
   fa.pos = b.pos;
-  fa.bias = (g.op == OP_TRANSLATION && g.cmp == CMP_DOT) ? b.bias : nullptr;
+  fa.pos_sides = g.recip ? 2 : 1;
+  fa.bias = (g.op == OP_TRANSLATION && g.cmp == CMP_DOT && !g.recip) ? b.bias : nullptr;
   fa.rowpart = b.rowpart;
   fa.nct = g.nct;
   fa.loss = g.loss;
@@ -445,5 +447,5 @@ void run_score_store(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, float* 
   fa.ldc = g.N;
   if (ctx->flags & PBG_F_BF16_SCORE) launch_gemm_bf16(fa, EPI_STORE, g.nchunks * 2, cs);
   else launch_score_split(fa, EPI_STORE, g.nchunks * 2, cs);
-  if (g.op == OP_TRANSLATION && g.cmp == CMP_DOT) launch_add_side_bias(g, b.bias, out, cs);
+  if (g.op == OP_TRANSLATION && g.cmp == CMP_DOT && !g.recip) launch_add_side_bias(g, b.bias, out, cs);
 }

@@ -71,8 +71,10 @@ pbg_status rank_impl(pbg_ctx* ctx, const char* name, const int32_t* src, const i
   if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
   ctx->err.clear();
   if (ctx->P != 1) return set_err(ctx, PBG_ERR_UNSUPPORTED, "%s needs a single partition", name);
-  if (ctx->cmp == CMP_COS && ctx->op != OP_IDENTITY && ctx->R > 1)
-    return set_err(ctx, PBG_ERR_UNSUPPORTED, "%s: cos with an operator needs a single relation", name);
+  const bool recip = reciprocal(ctx);
+  if (ctx->cmp == CMP_COS && ctx->op != OP_IDENTITY && ctx->R > 1 && !recip)
+    return set_err(ctx, PBG_ERR_UNSUPPORTED,
+                   "%s: cos with an operator needs a single relation (or reciprocal predicates)", name);
   if (n < 0 || n > 0x3FFFFFFFll || n_known < 0 || n_known > 0x7FFFFFFFll)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "n or n_known out of range");
   if (cand && (n_cand <= 0 || n_cand > 0x7FFFFFFFll))
@@ -95,7 +97,9 @@ pbg_status rank_impl(pbg_ctx* ctx, const char* name, const int32_t* src, const i
   const int64_t n_col = cand ? n_cand : n_ent;   // score columns
   const int d = ctx->d, dp = (d + 3) / 4 * 4;
   const bool linear = ctx->op == OP_LINEAR;
-  const bool sep_src_table = ctx->cmp == CMP_COS && ctx->op != OP_IDENTITY;
+  // cos with an operator applies it to every source candidate, except with
+  // reciprocal predicates (the source side's query carries theta_{r+R})
+  const bool sep_src_table = ctx->cmp == CMP_COS && ctx->op != OP_IDENTITY && !recip;
 
   // query block: the score block stays near 1 GiB
   int64_t qb = ((int64_t)1 << 28) / std::max<int64_t>(n_col, 1);
@@ -106,7 +110,7 @@ pbg_status rank_impl(pbg_ctx* ctx, const char* name, const int32_t* src, const i
   uint32_t* flag = (uint32_t*)buf.get(16);
   float* T0 = (float*)buf.get((size_t)n_ent * dp * 4);
   float* T1 = sep_src_table ? (float*)buf.get((size_t)n_ent * dp * 4) : nullptr;
-  float* relT = linear ? (float*)buf.get((size_t)ctx->R * d * d * 4) : nullptr;
+  float* relT = linear ? (float*)buf.get((size_t)relation_rows(ctx) * d * d * 4) : nullptr;
   float* pos = (float*)buf.get((size_t)n * 4);
   float* bias = (float*)buf.get((size_t)qb * 4);
   float* Q = (float*)buf.get((size_t)qb * dp * 4);
@@ -153,7 +157,9 @@ pbg_status rank_impl(pbg_ctx* ctx, const char* name, const int32_t* src, const i
   g.dr = ctx->dr;
   g.op = ctx->op;
   g.cmp = ctx->cmp;
-  if (linear) launch_transpose_rel(ctx->relp, relT, ctx->R, d, s);
+  g.recip = recip ? 1 : 0;
+  g.R = ctx->R;
+  if (linear) launch_transpose_rel(ctx->relp, relT, relation_rows(ctx), d, s);
   launch_rank_tables(g, pt.emb, ctx->relp, relT, n_ent, T0, T1, s);
   if (cand) {
     // the candidates' rows of the tables, in candidate order

@@ -92,7 +92,8 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   b.qk = (float*)a.get(s * 2 * C * dp * 4);
   b.nn = (float*)a.get(s * 2 * N * dp * 4);
   b.nrm = (float*)a.get(s * 2 * N * 4);
-  b.pos = (float*)a.get(s * C * 4);
+  const int64_t psides = reciprocal(ctx) ? 2 : 1;   // positive scores per edge
+  b.pos = (float*)a.get(s * psides * C * 4);
   b.bias = (float*)a.get(s * C * 4);
   b.neg = (int32_t*)a.get(s * 2 * std::max(U, 1) * 4);
   // the ranking loss keeps dS as bits (word-column major, row pitch C rounded
@@ -102,7 +103,7 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   b.dsb = ranking ? (uint16_t*)a.get(s * 2 * (int64_t)round_up(C, 8) * ((Np + 15) / 16) * 2) : nullptr;
   b.rowpart = (float*)a.get(s * 2 * C * nct * 2 * 4);
   if (ctx->loss == PBG_LOSS_SOFTMAX) b.rowscale = (float*)a.get(s * 2 * nct * (int64_t)C * 4);
-  b.dpos = (float*)a.get(s * C * 4);
+  b.dpos = (float*)a.get(s * psides * C * 4);
   b.dsum1 = (float*)a.get(s * C * 4);
   b.chunkloss = (double*)a.get(s * fin_blocks(C) * 8);
   b.fin_ticket = (unsigned int*)a.get(4);
@@ -110,7 +111,9 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   b.dn = (float*)a.get(s * 2 * N * dp * 4);
   const bool has_rel = ctx->op != OP_IDENTITY;
   const bool linear = ctx->op == OP_LINEAR;
-  if (has_rel && !linear) b.relc = (float*)a.get(s * N * ctx->dr * 4);
+  const int relN = reciprocal(ctx) ? 2 * C : N;
+  if (has_rel && !linear) b.relc = (float*)a.get(s * relN * ctx->dr * 4);
+  if (reciprocal(ctx) && ctx->cmp == PBG_CMP_COS) b.qnrm = (float*)a.get(s * 2 * C * 4);
   const int64_t nkeys = s * 2 * N;
   // a window of steps: keys, values, the sort's alternate buffers and counts
   b.keys = (uint32_t*)a.get(kSortWindow * nkeys * 4);
@@ -118,10 +121,11 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   ctx->wkeys_alt = (uint32_t*)a.get(kSortWindow * nkeys * 4);
   ctx->wvals_alt = (uint32_t*)a.get(kSortWindow * nkeys * 4);
   ctx->whist = (uint32_t*)a.get(radix_segments_hist_entries(nkeys, kSortWindow) * 4);
-  if (has_rel && ctx->R > 1) {
+  if (sorted_relation_keys(ctx)) {
     // the edges' relations, then (cos with an operator) the chunk relation of
-    // every uniform source candidate
-    const int64_t per = s * (C + (chunk_relation_operator(ctx) ? U : 0));
+    // every uniform source candidate or (reciprocal predicates) every edge's
+    // source-side row
+    const int64_t per = s * (reciprocal(ctx) ? 2 * C : C + (chunk_relation_operator(ctx) ? U : 0));
     b.rkeys = (uint32_t*)a.get(kSortWindow * per * 4);
     b.rvals = (uint32_t*)a.get(kSortWindow * per * 4);
   }
@@ -138,7 +142,7 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
     ctx->relA = (float*)a.get((int64_t)d * dp * 4);
     ctx->relAT = (float*)a.get((int64_t)d * dp * 4);
     if (ctx->cmp == PBG_CMP_COS) {
-      b.lin_x = (float*)a.get(s * N * dp * 4);
+      b.lin_x = (float*)a.get(s * std::max(N, 2 * C) * dp * 4);
       b.lin_v = (float*)a.get(s * N * dp * 4);
     }
   }
@@ -298,14 +302,15 @@ pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_part
   if (loss < PBG_LOSS_RANKING || loss > PBG_LOSS_SOFTMAX) return fail(PBG_ERR_INVALID_ARG, "unknown loss");
   if (op == PBG_OP_COMPLEX_DIAGONAL && (dim % 2)) return fail(PBG_ERR_INVALID_ARG, "complex_diagonal needs an even dim");
   if (!std::isfinite(margin)) return fail(PBG_ERR_INVALID_ARG, "margin must be finite");
-  if (flags & ~(uint32_t)(PBG_F_BF16_SCORE | PBG_F_PHASE_TIMING | PBG_F_SCORE_TIMING))
+  if (flags & ~(uint32_t)(PBG_F_BF16_SCORE | PBG_F_PHASE_TIMING | PBG_F_SCORE_TIMING | PBG_F_RECIPROCAL))
     return fail(PBG_ERR_INVALID_ARG, "unknown flags");
   const int64_t ps = (num_entities + num_partitions - 1) / num_partitions;
   if ((int64_t)(num_partitions - 1) * ps >= num_entities)
     return fail(PBG_ERR_INVALID_ARG, "a partition would be empty (num_partitions too large for num_entities)");
   if (ps > (1ll << 30)) return fail(PBG_ERR_INVALID_ARG, "partitions above 2^30 rows are not supported");
-  if (cmp == PBG_CMP_COS && op == PBG_OP_LINEAR && num_relations > 1)
-    return fail(PBG_ERR_UNSUPPORTED, "cos with the linear operator needs a single relation");
+  if (cmp == PBG_CMP_COS && op == PBG_OP_LINEAR && num_relations > 1 && !(flags & PBG_F_RECIPROCAL))
+    return fail(PBG_ERR_UNSUPPORTED,
+                "cos with the linear operator needs a single relation (or reciprocal predicates)");
   ctx->n = num_entities;
   ctx->P = num_partitions;
   ctx->R = num_relations;
@@ -363,7 +368,7 @@ int64_t pbg_partition_rows(const pbg_ctx* ctx, int32_t p) {
 
 int64_t pbg_relation_param_floats(const pbg_ctx* ctx) {
   if (!ctx || ctx->invalid) return -1;
-  return (int64_t)ctx->R * ctx->dr;
+  return (int64_t)relation_rows(ctx) * ctx->dr;
 }
 
 pbg_status pbg_bind_partition(pbg_ctx* ctx, int32_t p, float* emb, float* adagrad, int32_t where) {
@@ -462,6 +467,9 @@ void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, int C, int U, uint64_
   if (g.rb < 1) g.rb = 1;
   g.bucket = (uint32_t)(i * ctx->P + j);
   g.seed = seed;
+  g.recip = reciprocal(ctx) ? 1 : 0;
+  g.R = ctx->R;
+  g.relN = g.recip ? 2 * C : N;
 }
 
 StepBufs bucket_bufs(pbg_ctx* ctx, float* emb_i, float* G_i, float* emb_j, float* G_j) {
@@ -473,7 +481,7 @@ StepBufs bucket_bufs(pbg_ctx* ctx, float* emb_i, float* G_i, float* emb_j, float
   b.G_j = G_j;
   b.relp = ctx->relp;
   b.relG = ctx->relG;
-  if (!(ctx->op != OP_IDENTITY && ctx->R > 1)) {
+  if (!sorted_relation_keys(ctx)) {
     b.rkeys = nullptr;
     b.rvals = nullptr;
   }
@@ -481,7 +489,7 @@ StepBufs bucket_bufs(pbg_ctx* ctx, float* emb_i, float* G_i, float* emb_j, float
 }
 
 void run_gather_forward(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, hipStream_t cs) {
-  const bool linear1 = ctx->op == OP_LINEAR && ctx->R == 1;
+  const bool linear1 = linear_step_contractions(ctx);
   if (linear1) launch_pad_linear(ctx->relp, g.d, g.dp, ctx->relA, ctx->relAT, cs);
   launch_gather(g, b, cs);
   if (linear1) run_linear_forward(g, b, ctx->relA, ctx->relAT, cs);
@@ -512,7 +520,9 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   };
   const int64_t nsteps = (nchunks + S - 1) / S;
   const bool uniform_rel = chunk_relation_operator(ctx);
-  const int64_t rstride = (int64_t)S * (C + (uniform_rel ? U : 0));   // relation keys per step
+  const bool recip = reciprocal(ctx);
+  // relation keys per step
+  const int64_t rstride = (int64_t)S * (recip ? 2 * C : C + (uniform_rel ? U : 0));
   st = ensure_steploss(ctx, nsteps);
   if (st != PBG_OK) return st;
   hipStream_t cs = ctx->cs;
@@ -521,7 +531,7 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   StepGeom g;
   bucket_geom(ctx, i, j, C, U, seed, g);
   const int key_bits = g.rb + (g.same_table ? 0 : 1);
-  const int rel_bits = bits_for((uint64_t)ctx->R - 1);
+  const int rel_bits = bits_for((uint64_t)relation_rows(ctx) - 1);
   const bool has_rel = ctx->op != OP_IDENTITY;
   const bool linear = ctx->op == OP_LINEAR;
 
@@ -595,8 +605,9 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
       b.rkeys = win_rkeys + wi * rstride;
       b.rvals = win_rvals + wi * rstride;
     }
-    // relation keys of the step: the edges', then the uniform source candidates'
-    const int n_relkeys = m_step + (uniform_rel ? nch * U : 0);
+    // relation keys of the step: the edges', then the uniform source
+    // candidates' or the edges' source-side rows
+    const int n_relkeys = recip ? 2 * m_step : m_step + (uniform_rel ? nch * U : 0);
 
     mark(t, 0);
 
@@ -611,10 +622,10 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
 
     mark(t, 4);
     launch_op_backward(g, b, cs);
-    if (linear && ctx->R == 1) run_linear_backward(g, b, ctx->relA, ctx->relAT, cs);
+    if (linear_step_contractions(ctx)) run_linear_backward(g, b, ctx->relA, ctx->relAT, cs);
     else if (linear) launch_linear_rows_backward(g, b, cs);
     mark(t, 5);
-    const bool rel_side = has_rel && !linear && ctx->R == 1;
+    const bool rel_side = has_rel && !linear && !sorted_relation_keys(ctx);
     if (rel_side) side_fork(ctx);
 
     // entities: contribution rows in (table, row) order, segment sums, Adagrad
@@ -622,16 +633,16 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
 
     // relations
     if (has_rel) {
-      if (linear && ctx->R == 1) {
+      if (linear_step_contractions(ctx)) {
         // dA per chunk by contraction, then the fixed-order sum of the
         // partials and element-wise Adagrad
         const int nparts = run_linear_relation_grad(g, b, ctx->relpartial, cs);
         launch_relation_single_adagrad(ctx->relp, ctx->relG, d * d, ctx->relpartial, nparts, lr, cs);
       } else if (linear) {
         uint32_t *rk = nullptr, *rv = nullptr;
-        launch_radix_sort_to(b.rkeys, b.rvals, m_step, rel_bits, ctx->sw, &rk, &rv, cs);
-        launch_linear_relation_update(g, b, rk, rv, m_step, lr, cs);
-      } else if (ctx->R > 1) {
+        launch_radix_sort_to(b.rkeys, b.rvals, n_relkeys, rel_bits, ctx->sw, &rk, &rv, cs);
+        launch_linear_relation_update(g, b, rk, rv, n_relkeys, lr, cs);
+      } else if (sorted_relation_keys(ctx)) {
         uint32_t *rk = nullptr, *rv = nullptr;
         launch_radix_sort_to(b.rkeys, b.rvals, n_relkeys, rel_bits, ctx->sw, &rk, &rv, cs);
         launch_relation_update_sorted(g, b, rk, rv, n_relkeys, ctx->sw, lr, cs);

@@ -156,10 +156,24 @@ pbg_status relation_chunk_bounds(pbg_ctx* ctx, const int32_t* rel, int64_t n, in
 inline bool grouped_chunks(const pbg_ctx* ctx, const pbg_neg_config* neg) {
   return neg->chunking == PBG_CHUNK_BY_RELATION && ctx->R > 1;
 }
+inline bool reciprocal(const pbg_ctx* ctx) { return (ctx->flags & PBG_F_RECIPROCAL) != 0; }
+// relation parameter rows (R, or 2R with reciprocal predicates)
+inline int relation_rows(const pbg_ctx* ctx) { return reciprocal(ctx) ? 2 * ctx->R : ctx->R; }
 // the cos comparator with an operator and several relations applies each
 // chunk's relation to its source candidates: relation-grouped chunks only
+// (not with reciprocal predicates, where no candidate carries the operator)
 inline bool chunk_relation_operator(const pbg_ctx* ctx) {
-  return ctx->cmp == PBG_CMP_COS && ctx->op != PBG_OP_IDENTITY && ctx->R > 1;
+  return ctx->cmp == PBG_CMP_COS && ctx->op != PBG_OP_IDENTITY && ctx->R > 1 && !reciprocal(ctx);
+}
+// relation gradients summed through sorted relation keys (more than one
+// parameter row), not by the single-relation sums
+inline bool sorted_relation_keys(const pbg_ctx* ctx) {
+  return ctx->op != PBG_OP_IDENTITY && relation_rows(ctx) > 1;
+}
+// the linear operator as contractions over the whole step (one relation
+// matrix); otherwise one matrix-vector product per edge
+inline bool linear_step_contractions(const pbg_ctx* ctx) {
+  return ctx->op == PBG_OP_LINEAR && relation_rows(ctx) == 1;
 }
 pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps);
 // geometry of the steps of bucket (i, j) (chunk and candidate counts, padded

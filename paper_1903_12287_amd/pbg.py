@@ -25,6 +25,7 @@ LOSSES = {"ranking": 0, "logistic": 1, "softmax": 2}
 F_BF16_SCORE = 1
 F_PHASE_TIMING = 2
 F_SCORE_TIMING = 4
+F_RECIPROCAL = 8
 CHUNKINGS = {"consecutive": 0, "by_relation": 1}
 MEM_DEVICE = 0
 MEM_PINNED_HOST = 1
@@ -166,6 +167,7 @@ def pbg_bucket_init(num_entities, num_partitions, num_relations, dim, op, cmp, l
         if ctx.value:
             L.pbg_free(ctx)
         raise PbgError(st, msg)
+    ctx._flags = int(flags)   # the layouts some outputs take depend on them
     return ctx
 
 
@@ -341,14 +343,16 @@ def pbg_sample_negatives(ctx, i, j, first_chunk, n_chunks, num_uniform, seed, ou
 def pbg_inspect_step(ctx, i, j, src_local, rel, dst_local, chunk_size, num_uniform, chunks_per_step, seed,
                      first_chunk=0, scores=None, dscores=None, row_loss=None, pos=None, chunking="consecutive",
                      n_chunks=None) -> float:
-    """n_chunks: chunks of the call (consecutive chunking: ceil(n / chunk_size))."""
+    """n_chunks: chunks of the call (consecutive chunking: ceil(n / chunk_size)).
+    pos holds nch * chunk_size floats, twice that with F_RECIPROCAL."""
     n = src_local.numel()
     if dst_local.numel() != n or (rel is not None and rel.numel() != n):
         raise ValueError("edge arrays differ in length")
     nch = -(-n // int(chunk_size)) if n_chunks is None else int(n_chunks)
     N = int(chunk_size) + int(num_uniform)
+    psides = 2 if getattr(ctx, "_flags", 0) & F_RECIPROCAL else 1   # positive scores per edge
     for t, want, name in ((scores, nch * 2 * chunk_size * N, "scores"), (dscores, nch * 2 * chunk_size * N, "dscores"),
-                          (row_loss, nch * 2 * chunk_size, "row_loss"), (pos, nch * chunk_size, "pos")):
+                          (row_loss, nch * 2 * chunk_size, "row_loss"), (pos, nch * psides * chunk_size, "pos")):
         if t is not None and t.numel() != want:
             raise ValueError(f"{name} must hold {want} floats")
     neg = _neg(chunk_size, num_uniform, chunks_per_step, first_chunk, chunking)

@@ -35,31 +35,33 @@ class Problem:
     lr: float
     seed: int
     chunking: str = "consecutive"
+    reciprocal: bool = False   # rel holds 2R rows: theta_r, then the source side's theta_{r+R}
 
 
 def make_problem(op, cmp, loss, n=60, P=1, R=1, d=16, m=300, C=20, U=12, S=4, i=0, j=0,
-                 seed=1, sigma=0.3, rel_scale=0.3, lr=0.1, margin=0.1, zipf=1.1, chunking="consecutive"):
+                 seed=1, sigma=0.3, rel_scale=0.3, lr=0.1, margin=0.1, zipf=1.1, chunking="consecutive",
+                 reciprocal=False):
     """A small seeded problem with Zipf endpoints (duplicates in chunks) and
-    perturbed relation parameters; with chunking='by_relation' the edges are
-    sorted by relation (stably)."""
+    perturbed relation parameters (2R rows with reciprocal predicates); with
+    chunking='by_relation' the edges are sorted by relation (stably)."""
     rng = synth.rng_for(seed)
     rows = [O.partition_rows(n, P, p) for p in range(P)]
     parts = synth.partition_embeddings(rows, d, rng, sigma)
     src = synth.BoundedZipf(rows[i], zipf, rng).sample(rng, m)
     dst = synth.BoundedZipf(rows[j], zipf, rng).sample(rng, m)
     rel_ids = None if R == 1 else rng.integers(0, R, m).astype(np.int32)
-    relp = synth.perturbed_relation_params(op, R, d, rng, rel_scale)
+    relp = synth.perturbed_relation_params(op, 2 * R if reciprocal else R, d, rng, rel_scale)
     if chunking == "by_relation" and rel_ids is not None:
         order = np.argsort(rel_ids, kind="stable")
         src, rel_ids, dst = src[order], rel_ids[order], dst[order]
     return Problem(n, P, R, d, op, cmp, loss, margin, parts, relp, i, j, src, rel_ids, dst,
-                   C, U, S, lr, seed + 1000, chunking)
+                   C, U, S, lr, seed + 1000, chunking, reciprocal)
 
 
 def oracle_model(pb: Problem) -> O.Model:
     return O.Model.create(pb.n, pb.P, pb.R, pb.d, pb.op, pb.cmp, pb.loss, pb.margin,
                           [p.astype(np.float64) for p in pb.parts],
-                          None if pb.rel is None else pb.rel.astype(np.float64))
+                          None if pb.rel is None else pb.rel.astype(np.float64), reciprocal=pb.reciprocal)
 
 
 class GpuModel:
@@ -70,6 +72,8 @@ class GpuModel:
         self.pbg = pbg
         self.pb = pb
         dev = torch.device("cuda")
+        if pb.reciprocal:
+            flags |= pbg.F_RECIPROCAL
         self.ctx = pbg.pbg_bucket_init(pb.n, pb.P, pb.R, pb.d, pb.op, pb.cmp, pb.loss, pb.margin, flags)
         self.emb = [torch.from_numpy(p.copy()).to(dev) for p in pb.parts]
         self.G = [torch.zeros(p.shape[0], dtype=torch.float32, device=dev) for p in pb.parts]
@@ -148,7 +152,8 @@ def _norm(v):
 
 
 def score_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk=0, chunking="consecutive"):
-    """Per chunk of a step: (Ap (C_c,), A0 (C_c, N_c), A1 (C_c, N_c))."""
+    """Per chunk of a step: (Ap (C_c,), A0 (C_c, N_c), A1 (C_c, N_c), Ap1 (C_c,)),
+    Ap1 the source side's positive score scale (reciprocal predicates; else Ap)."""
     src = np.asarray(src, np.int64)
     dst = np.asarray(dst, np.int64)
     m = src.shape[0]
@@ -164,6 +169,20 @@ def score_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk=0, chunking
         th = None if model.rel is None else model.rel[rel[lo:hi]]
         ath = None if th is None else np.abs(th)
         aq = _abs_forward(model.op, np.abs(xs), ath)
+        if model.reciprocal:
+            # both queries carry an operator: Q = g(x_s, theta_r), K = g(x_d, theta_{r+R})
+            thr = None if model.rel is None else model.rel[model.reverse_rel(rel[lo:hi])]
+            ak = _abs_forward(model.op, np.abs(xd), None if thr is None else np.abs(thr))
+            acd, acs, ay, ax = np.abs(cd), np.abs(cs), np.abs(xd), np.abs(xs)
+            if model.cmp == "cos":
+                tq = None if th is None else torch.tensor(th)
+                tk = None if thr is None else torch.tensor(thr)
+                aq = aq / _norm(O.apply_operator(model.op, torch.tensor(xs), tq).numpy())[:, None]
+                ak = ak / _norm(O.apply_operator(model.op, torch.tensor(xd), tk).numpy())[:, None]
+                acd, acs = acd / _norm(cd)[:, None], acs / _norm(cs)[:, None]
+                ay, ax = ay / _norm(xd)[:, None], ax / _norm(xs)[:, None]
+            out.append((np.sum(aq * ay, 1), aq @ acd.T, ak @ acs.T, np.sum(ak * ax, 1)))
+            continue
         if model.cmp == "cos":
             gq = O.apply_operator(model.op, torch.tensor(xs), None if th is None else torch.tensor(th)).numpy()
             aq = aq / _norm(gq)[:, None]
@@ -182,7 +201,7 @@ def score_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk=0, chunking
             A1 = np.einsum("ek,tk->et", ak, np.abs(cs))
             if model.op == "translation":
                 A1 = A1 + np.sum(ath * np.abs(xd), 1)[:, None]
-        out.append((Ap, A0, A1))
+        out.append((Ap, A0, A1, Ap))
     return out
 
 
@@ -201,14 +220,15 @@ def gpu_inspect(gm, lo, hi, first_chunk):
     scores = torch.empty(nch * 2 * C * N, dtype=torch.float32, device=dev)
     dscores = torch.empty_like(scores)
     row_loss = torch.empty(nch * 2 * C, dtype=torch.float32, device=dev)
-    pos = torch.empty(nch * C, dtype=torch.float32, device=dev)
+    psides = 2 if p.reciprocal else 1
+    pos = torch.empty(nch * psides * C, dtype=torch.float32, device=dev)
     r = None if gm.rel_ids is None else gm.rel_ids[lo:hi]
     loss = pbg.pbg_inspect_step(gm.ctx, p.i, p.j, gm.src[lo:hi], r, gm.dst[lo:hi], C, U, p.S, p.seed,
                                 first_chunk, scores, dscores, row_loss, pos, p.chunking, nch)
     S = scores.view(nch, 2, C, N).cpu().numpy().astype(np.float64)
     dS = dscores.view(nch, 2, C, N).cpu().numpy().astype(np.float64)
     L = row_loss.view(nch, 2, C).cpu().numpy().astype(np.float64)
-    P_ = pos.view(nch, C).cpu().numpy().astype(np.float64)
+    P_ = pos.view(nch, psides, C).cpu().numpy().astype(np.float64)
     out = []
     for c, clo, chi in O.make_chunks(n, C, rel_h, p.chunking):
         Cc = chi - clo
@@ -216,9 +236,13 @@ def gpu_inspect(gm, lo, hi, first_chunk):
         # outside the chunk's block every output is zero
         assert not S[c, :, Cc:].any() and not S[c, :, :, Nc:].any()
         assert not dS[c, :, Cc:].any() and not dS[c, :, :, Nc:].any()
-        out.append({"p": P_[c, :Cc], "S0": S[c, 0, :Cc, :Nc], "S1": S[c, 1, :Cc, :Nc],
-                    "loss0": L[c, 0, :Cc], "loss1": L[c, 1, :Cc],
-                    "dS0": dS[c, 0, :Cc, :Nc], "dS1": dS[c, 1, :Cc, :Nc]})
+        rec = {"p": P_[c, 0, :Cc], "S0": S[c, 0, :Cc, :Nc], "S1": S[c, 1, :Cc, :Nc],
+               "loss0": L[c, 0, :Cc], "loss1": L[c, 1, :Cc],
+               "dS0": dS[c, 0, :Cc, :Nc], "dS1": dS[c, 1, :Cc, :Nc]}
+        if p.reciprocal:
+            rec["p1"] = P_[c, 1, :Cc]
+            assert not P_[c, :, Cc:].any()
+        out.append(rec)
     return out, loss
 
 
@@ -228,19 +252,20 @@ def check_inspection(model, gpu, orc, scales, tol_s, tol_p=1e-5, margin=0.1):
     ranking loss, the number of hinge terms whose branch differs (each of them
     must lie within the score error bound of the kink)."""
     rep = {"s_ratio": 0.0, "p_ratio": 0.0, "loss_ratio": 0.0, "ds_ratio": 0.0, "flips": 0, "near_kink": 0}
-    for g, o, (Ap, A0, A1) in zip(gpu, orc, scales):
+    for g, o, (Ap0, A0, A1, Ap1) in zip(gpu, orc, scales):
         Cc = o["p"].shape[0]
-        eP = tol_p * Ap + 1e-30
-        rep["p_ratio"] = max(rep["p_ratio"], float(np.max(np.abs(g["p"] - o["p"]) / eP)))
         valid = np.ones_like(A0, dtype=bool)
         valid[np.arange(Cc), np.arange(Cc)] = False
-        for side, A in ((0, A0), (1, A1)):
+        for side, A, Ap in ((0, A0, Ap0), (1, A1, Ap1)):
+            pk = "p1" if (side == 1 and "p1" in o) else "p"   # each side's positive score
+            eP = tol_p * Ap + 1e-30
+            rep["p_ratio"] = max(rep["p_ratio"], float(np.max(np.abs(g[pk] - o[pk]) / eP)))
             eS = tol_s * A + 1e-30
             dS_o, dS_g = o[f"dS{side}"], g[f"dS{side}"]
             rep["s_ratio"] = max(rep["s_ratio"], float(np.max((np.abs(g[f"S{side}"] - o[f"S{side}"]) / eS)[valid])))
             K = valid.sum(1)
             if model.loss == "ranking":
-                z = margin - o["p"][:, None] + o[f"S{side}"]
+                z = margin - o[pk][:, None] + o[f"S{side}"]
                 band = eS + eP[:, None]
                 near = valid & (np.abs(z) <= band)
                 flip = valid & ((dS_g > 0) != (z > 0))
@@ -323,6 +348,8 @@ def gradient_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk, insp, c
         leaf[p] = raw[p].abs().requires_grad_(True)
         ids_of[p] = ids
     step_rels = np.unique(np.concatenate([rel[lo:hi] for (_, lo, hi) in step]))
+    if model.reciprocal:
+        step_rels = np.unique(np.concatenate([step_rels, model.reverse_rel(step_rels)]))
     rleaf = None
     if model.rel is not None:
         rraw = torch.tensor(model.rel[step_rels], dtype=torch.float64)
@@ -342,6 +369,31 @@ def gradient_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk, insp, c
         W0 = torch.from_numpy(np.abs(rec["dS0"]))
         W1 = torch.from_numpy(np.abs(rec["dS1"]))
         wp = torch.from_numpy(np.abs(rec["dp"]))
+        if model.reciprocal:
+            # Q = g(x_s, theta_r) against the destination candidates, K =
+            # g(x_d, theta_{r+R}) against the source candidates, a positive
+            # score per side
+            rk = model.reverse_rel(r_e)
+            thk = None if rleaf is None else rleaf[torch.from_numpy(np.searchsorted(step_rels, rk))]
+            wp1 = torch.from_numpy(np.abs(rec["dp1"]))
+            q, k = _abs_fwd_t(model.op, xs, th), _abs_fwd_t(model.op, xd, thk)
+            cdh, csh, yh, xh = cd, cs, xd, xs
+            if cos:
+                tq = None if rleaf is None else torch.tensor(model.rel[r_e], dtype=torch.float64)
+                tk = None if rleaf is None else torch.tensor(model.rel[rk], dtype=torch.float64)
+                raw_xs, raw_xd = rows(i, src[lo:hi], False), rows(j, dst[lo:hi], False)
+                raw_cd = torch.cat([raw_xd, rows(j, u_dst, False)], 0)
+                raw_cs = torch.cat([raw_xs, rows(i, u_src, False)], 0)
+                q = q / O._clamped_norm(O.apply_operator(model.op, raw_xs, tq)).unsqueeze(-1)
+                k = k / O._clamped_norm(O.apply_operator(model.op, raw_xd, tk)).unsqueeze(-1)
+                cdh = cd / O._clamped_norm(raw_cd).unsqueeze(-1)
+                csh = cs / O._clamped_norm(raw_cs).unsqueeze(-1)
+                yh = xd / O._clamped_norm(raw_xd).unsqueeze(-1)
+                xh = xs / O._clamped_norm(raw_xs).unsqueeze(-1)
+            L = ((W0 * (q @ cdh.T)).sum() + (W1 * (k @ csh.T)).sum() + (wp * (q * yh).sum(1)).sum()
+                 + (wp1 * (k * xh).sum(1)).sum())
+            L.backward()
+            continue
         if cos:
             thr = None if rleaf is None else torch.tensor(model.rel[r_e], dtype=torch.float64)
             raw_xs, raw_xd = rows(i, src[lo:hi], False), rows(j, dst[lo:hi], False)
@@ -448,7 +500,8 @@ def teacher_forced_step(gm, lo, hi, first_chunk, eps):
     pb = gm.pb
     before = gm.state()
     om = O.Model.create(pb.n, pb.P, pb.R, pb.d, pb.op, pb.cmp, pb.loss, pb.margin, before["emb"],
-                        before.get("rel"), G_parts=before["G"], relG=before.get("relG"))
+                        before.get("rel"), G_parts=before["G"], relG=before.get("relG"),
+                        reciprocal=pb.reciprocal)
     src, dst = pb.src[lo:hi], pb.dst[lo:hi]
     rel = None if pb.rel_ids is None else pb.rel_ids[lo:hi]
     rep = branches = None

@@ -1,0 +1,213 @@
+"""Reciprocal predicates (Sec. 5.4: separate relation parameters for the source
+and the destination negatives) on the GPU, against the oracle.
+
+With PBG_F_RECIPROCAL the destination side scores g(x_s, theta_r) against the
+destination candidates and the source side g(x_d, theta_{r+R}) against the
+source candidates, each with its own positive score; no candidate carries an
+operator, so cos with any operator and any number of relations trains with
+consecutive chunks.  Tolerances as in test_gpu_train (free-running passes at
+1e-4), test_gpu_inspect (element-wise forward half) and test_gpu_rank (rank
+bounds for scores within float32 error of the positive's).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import pbg_oracle as O
+from paper_1903_12287_amd import synth
+from tests.pbg_cases import (GpuModel, Problem, check_inspection, gpu_inspect, make_problem, oracle_model,
+                             score_scales, teacher_forced_step)
+from tests.test_gpu_rank import _tol
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("op,cmp,loss,R,P,ij,chunking", [
+    ("complex_diagonal", "dot", "softmax", 5, 1, (0, 0), "consecutive"),
+    ("translation", "cos", "ranking", 4, 2, (1, 0), "consecutive"),
+    ("translation", "dot", "logistic", 3, 1, (0, 0), "consecutive"),
+    ("diagonal", "cos", "softmax", 6, 1, (0, 0), "by_relation"),
+    ("diagonal", "dot", "logistic", 4, 3, (2, 1), "consecutive"),
+    ("linear", "dot", "ranking", 1, 1, (0, 0), "consecutive"),
+    ("linear", "cos", "logistic", 3, 2, (0, 1), "consecutive"),
+    ("identity", "cos", "softmax", 1, 1, (0, 0), "consecutive"),
+])
+def test_reciprocal_multi_step_pass_matches_oracle(op, cmp, loss, R, P, ij, chunking):
+    """Several steps with a short last chunk: per-step losses and the final
+    state, both parameter rows of every relation included."""
+    from paper_1903_12287_amd import pbg
+    i, j = ij
+    pb = make_problem(op, cmp, loss, n=150, P=P, R=R, d=24, m=437, C=16, U=10, S=3, i=i, j=j,
+                      seed=17, sigma=0.2, chunking=chunking, reciprocal=True)
+    print(f"\n[{op} {cmp} {loss} R={R} {chunking}]", flush=True)
+    gm = GpuModel(pb)
+    try:
+        assert pbg.pbg_relation_param_floats(gm.ctx) == (0 if pb.rel is None else pb.rel.size)
+        gm.train()
+        steps = pbg.pbg_get_step_losses(gm.ctx)
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol, osteps = O.train_bucket(om, i, j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr,
+                                pb.seed, return_steps=True, chunking=chunking)
+    assert len(steps) == len(osteps)
+    for a, b in zip(steps, osteps):
+        assert abs(a - b) <= 1e-4 * max(1.0, abs(b)), (a, b)
+    for p in sorted({i, j}):
+        err = float(np.max(np.abs(st["emb"][p] - om.emb[p])))
+        assert err <= 1e-4, (p, err)
+        gerr = float(np.max(np.abs(st["G"][p] - om.G[p]) / np.maximum(1.0, om.G[p])))
+        assert gerr <= 1e-4, (p, gerr)
+    if om.rel is not None:
+        assert float(np.max(np.abs(st["rel"] - om.rel))) <= 1e-4
+        # the source-side rows moved: they take part in the training
+        assert np.any(st["rel"][pb.R:] != pb.rel[pb.R:])
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_reciprocal_knowledge_graph_forward_elementwise(bf16):
+    """The knowledge-graph chunk shape (complex, d = 400, softmax, 1,345
+    relations with Zipf frequencies, C = U = 1000) with reciprocal predicates:
+    every score, both positives, the side losses and dL/dS element by element."""
+    from paper_1903_12287_amd import pbg
+    n, d, R, C, U = 15_000, 400, 1345, 1000, 1000
+    m = 5 * C + C // 2 + 3
+    rng = synth.rng_for(41)
+    parts = synth.partition_embeddings([n], d, rng, 0.1)
+    src = synth.BoundedZipf(n, 1.0, rng).sample(rng, m)
+    dst = synth.BoundedZipf(n, 1.0, rng).sample(rng, m)
+    rel = synth.BoundedZipf(R, 1.2, rng).sample(rng, m).astype(np.int32)
+    relp = synth.perturbed_relation_params("complex_diagonal", 2 * R, d, rng, 0.3)
+    pb = Problem(n, 1, R, d, "complex_diagonal", "dot", "softmax", 0.1, parts, relp, 0, 0, src, rel, dst, C, U,
+                 40, 0.1, 140, "consecutive", True)
+    gm = GpuModel(pb, flags=pbg.F_BF16_SCORE if bf16 else 0)
+    try:
+        gpu, gloss = gpu_inspect(gm, 0, m, 3)
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    orc = O.inspect_step(om, 0, 0, src, rel, dst, C, U, pb.seed, 3)
+    scales = score_scales(om, 0, 0, src, rel, dst, C, U, pb.seed, 3)
+    rep = check_inspection(om, gpu, orc, scales, 2e-2 if bf16 else 1e-5)
+    print(f"\n[knowledge graph, reciprocal, bf16={bf16}] {rep}", flush=True)
+    assert rep["p_ratio"] <= 1.0 and rep["s_ratio"] <= 1.0
+    assert rep["loss_ratio"] <= 1.0 and rep["ds_ratio"] <= 1.0
+    ol = sum(float(o["loss0"].sum() + o["loss1"].sum()) for o in orc)
+    assert abs(gloss - ol) <= (2e-2 if bf16 else 1e-5) * abs(ol)
+
+
+@pytest.mark.parametrize("op,cmp,loss,d,R,chunking", [
+    ("complex_diagonal", "dot", "softmax", 400, 1345, "consecutive"),
+    ("translation", "cos", "ranking", 128, 40, "consecutive"),
+    ("linear", "cos", "logistic", 32, 5, "by_relation"),
+])
+def test_reciprocal_teacher_forced_steps(op, cmp, loss, d, R, chunking):
+    """Steps at the real chunk shape (C = U = 1000, S = 40), each checked against
+    the oracle loaded with the GPU's step-start state: every entity row, both
+    parameter rows of every relation and their accumulators within the
+    Adagrad-propagated bound of a gradient error 1e-5 * A (ranking: the hinge
+    census, terms within rounding of the kink follow the GPU's branch)."""
+    n, C, U, S = 15_000, 1000, 1000, 40
+    m = 2 * S * C
+    rng = synth.rng_for(43)
+    parts = synth.partition_embeddings([n], d, rng, 0.1)
+    src = synth.BoundedZipf(n, 1.0, rng).sample(rng, m)
+    dst = synth.BoundedZipf(n, 1.0, rng).sample(rng, m)
+    rel = synth.BoundedZipf(R, 1.2, rng).sample(rng, m).astype(np.int32)
+    relp = synth.perturbed_relation_params(op, 2 * R, d, rng, 0.3)
+    if op == "linear":
+        relp = (synth.identity_relation_params(op, 2 * R, d) + 0.05 * rng.standard_normal((2 * R, d * d))).astype(np.float32)
+    if chunking == "by_relation":
+        order = np.argsort(rel, kind="stable")
+        src, rel, dst = src[order], rel[order], dst[order]
+    pb = Problem(n, 1, R, d, op, cmp, loss, 0.1, parts, relp, 0, 0, src, rel, dst, C, U, S, 0.1, 150, chunking, True)
+    chunks = O.make_chunks(m, C, rel, chunking)
+    b1 = chunks[S][1]
+    b2 = chunks[min(len(chunks), 2 * S) - 1][2]
+    print(f"\n[{op} {cmp} {loss} d={d} R={R} {chunking}] step edges {b1}..{b2}", flush=True)
+    gm = GpuModel(pb)
+    try:
+        gm.train(0, b1, 0)
+        rep, gl, ol, worst = teacher_forced_step(gm, b1, b2, S, 1e-5)
+    finally:
+        gm.close()
+    print(f"  census {rep}  loss gpu {gl:.6f} oracle {ol:.6f}  worst {worst:.3f}", flush=True)
+    assert abs(gl - ol) <= 1e-5 * abs(ol)
+    assert worst <= 1.0
+    if rep is not None:
+        assert rep["p_ratio"] <= 1.0 and rep["s_ratio"] <= 1.0 and rep["loss_ratio"] <= 1.0
+
+
+def _rank_ctx(n, R, d, op, cmp, emb, relp):
+    from paper_1903_12287_amd import pbg
+    dev = torch.device("cuda")
+    ctx = pbg.pbg_bucket_init(n, 1, R, d, op, cmp, "softmax", 0.1, pbg.F_RECIPROCAL)
+    keep = [torch.from_numpy(emb).to(dev), torch.zeros(n, dtype=torch.float32, device=dev)]
+    pbg.pbg_bind_partition(ctx, 0, keep[0], keep[1])
+    if relp is not None:
+        keep += [torch.from_numpy(relp).to(dev), torch.zeros(relp.shape, dtype=torch.float32, device=dev)]
+        pbg.pbg_bind_relations(ctx, keep[2], keep[3])
+    pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
+    return ctx, keep
+
+
+@pytest.mark.parametrize("op,cmp,R", [("complex_diagonal", "dot", 7), ("translation", "cos", 5),
+                                      ("linear", "cos", 3), ("diagonal", "dot", 1), ("identity", "cos", 1)])
+def test_reciprocal_ranks_match_oracle(op, cmp, R):
+    """Filtered ranks (all entities) and sampled-candidate ranks, the source side
+    scored by g(x_d, theta_{r+R}) with its own positive score."""
+    from paper_1903_12287_amd import pbg
+    n, d, m_train, m_eval = 300, 24, 3000, 200
+    rng = synth.rng_for(61 + R)
+    emb = (rng.standard_normal((n, d)) * 0.3).astype(np.float32)
+    relp = synth.perturbed_relation_params(op, 2 * R, d, rng, 0.3)
+    src, dst = synth.zipf_edges(n, m_train + m_eval, 1.0, 1.0, rng)
+    rel = rng.integers(0, R, m_train + m_eval).astype(np.int32) if R > 1 else None
+    es, ed = src[m_train:], dst[m_train:]
+    er = None if rel is None else rel[m_train:]
+    cand = rng.integers(0, n, 500)
+    dev = torch.device("cuda")
+    t = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
+    ctx, keep = _rank_ctx(n, R, d, op, cmp, emb, relp)
+    try:
+        ranks = torch.zeros(2 * m_eval, dtype=torch.int32, device=dev)
+        mrr, hits = pbg.pbg_rank_eval(ctx, t(es), t(er), t(ed), t(src), t(rel), t(dst), ranks)
+        got = ranks.cpu().numpy().astype(np.int64)
+        ranks2 = torch.zeros(2 * m_eval, dtype=torch.int32, device=dev)
+        pbg.pbg_rank_sampled(ctx, t(es), t(er), t(ed), t(cand), ranks2)
+        got2 = ranks2.cpu().numpy().astype(np.int64)
+    finally:
+        pbg.pbg_free(ctx)
+    assert abs(mrr - float(np.mean(1.0 / got))) <= 1e-12
+    assert abs(hits - float(np.mean(got <= 10))) <= 1e-12
+    model = O.Model.create(n, 1, R, d, op, cmp, "softmax", 0.1, [emb.astype(np.float64)],
+                           None if relp is None else relp.astype(np.float64), reciprocal=True)
+    tol = _tol(op, cmp, emb, relp)
+    for g, res in ((got, O.rank_eval(model, es, er, ed, src, rel, dst, tol=tol)),
+                   (got2, O.rank_sampled(model, es, er, ed, cand, tol=tol))):
+        want, _, _, lo, hi = res
+        assert np.all(g >= lo) and np.all(g <= hi), (np.nonzero((g < lo) | (g > hi))[0][:10], tol)
+        assert np.mean(g == want) >= 0.97
+
+
+def test_reciprocal_lifts_the_operator_limits():
+    """Without the flag, cos with the linear operator and several relations is
+    refused at init, and cos with another operator and several relations with
+    consecutive chunks at training and ranking; with it, all are accepted
+    (their results are checked above)."""
+    from paper_1903_12287_amd import pbg
+    with pytest.raises(pbg.PbgError) as ei:
+        pbg.pbg_bucket_init(100, 1, 3, 8, "linear", "cos", "ranking")
+    assert ei.value.status_name == "UNSUPPORTED"
+    ctx = pbg.pbg_bucket_init(100, 1, 3, 8, "linear", "cos", "ranking", 0.1, pbg.F_RECIPROCAL)
+    try:
+        assert pbg.pbg_relation_param_floats(ctx) == 2 * 3 * 8 * 8
+    finally:
+        pbg.pbg_free(ctx)
+    ctx = pbg.pbg_bucket_init(100, 1, 3, 8, "diagonal", "cos", "ranking", 0.1, pbg.F_RECIPROCAL)
+    try:
+        assert pbg.pbg_relation_param_floats(ctx) == 2 * 3 * 8
+    finally:
+        pbg.pbg_free(ctx)
