@@ -54,7 +54,8 @@ def parse():
     ap.add_argument("--no-bf16", action="store_true", help="skip the bf16-input leg")
     ap.add_argument("--no-big-bucket", action="store_true",
                     help="skip the second workload of the default line (one bucket of the partitioned graph)")
-    ap.add_argument("--row", choices=["bucketing", "knowledge_graph", "big_bucket", "epoch", "tiny", "negatives"],
+    ap.add_argument("--row", choices=["bucketing", "knowledge_graph", "knowledge_graph_reciprocal", "big_bucket",
+                                      "epoch", "tiny", "negatives"],
                     help="measure another row of the hot path instead of the default training step: "
                          "edge bucketing of the follower graph, the knowledge-graph pass and filtered "
                          "rank evaluation, one bucket of the large partitioned graph, the follower-graph "
@@ -376,11 +377,13 @@ def row_bucketing():
                              "sample": f"first {m} edges, numpy stable argsort, {ct:.1f} s"}}
 
 
-def row_knowledge_graph():
+def row_knowledge_graph(reciprocal=False):
     """Knowledge-graph-shaped graph (15,000 entities, 1,345 relations, 483,000
     training + 50,000 held-out triples, d = 400, complex_diagonal, dot,
     softmax): one training pass and the filtered rank evaluation of the
-    held-out triples against all entities on both sides."""
+    held-out triples against all entities on both sides.  reciprocal: with
+    reciprocal predicates (a second parameter row per relation for the source
+    side, Sec. 5.4's recipe for this model)."""
     import numpy as np
     import torch
     from oracle import pbg_oracle as O
@@ -389,19 +392,21 @@ def row_knowledge_graph():
     w = synth.knowledge_graph()
     rng = synth.rng_for(w.seed + 1)
     emb0 = synth.init_embeddings(w.n, w.d, rng)
-    rel0 = synth.identity_relation_params(w.op, w.R, w.d)
+    rel0 = synth.identity_relation_params(w.op, 2 * w.R if reciprocal else w.R, w.d)
     dev = torch.device("cuda")
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
     src, rel, dst = t(w.src), t(w.rel), t(w.dst)
     out = {"metric": "trained edges/sec on 1 MI355X", "unit": "edges/s", "dtype": "f32",
            "config": {"workload": "knowledge_graph", "entities": w.n, "relations": w.R, "train": w.E,
                       "held_out": len(w.held_src), "dim": w.d, "operator": w.op, "comparator": w.cmp,
-                      "loss": w.loss, "chunk": w.C, "uniform_negatives": w.U, "chunks_per_step": w.S}}
+                      "loss": w.loss, "chunk": w.C, "uniform_negatives": w.U, "chunks_per_step": w.S,
+                      "reciprocal_predicates": reciprocal}}
     emb = torch.from_numpy(emb0.copy()).to(dev)
     G = torch.zeros(w.n, dtype=torch.float32, device=dev)
     relp = torch.from_numpy(rel0.copy()).to(dev)
     relG = torch.zeros_like(relp)
-    ctx = pbg.pbg_bucket_init(w.n, 1, w.R, w.d, w.op, w.cmp, w.loss, w.margin, pbg.F_PHASE_TIMING)
+    ctx = pbg.pbg_bucket_init(w.n, 1, w.R, w.d, w.op, w.cmp, w.loss, w.margin,
+                              pbg.F_PHASE_TIMING | (pbg.F_RECIPROCAL if reciprocal else 0))
     try:
         pbg.pbg_bind_partition(ctx, 0, emb, G)
         pbg.pbg_bind_relations(ctx, relp, relG)
@@ -457,7 +462,7 @@ def row_knowledge_graph():
     finally:
         pbg.pbg_free(ctx)
     model = O.Model.create(w.n, 1, w.R, w.d, w.op, w.cmp, w.loss, w.margin, [emb0.astype(np.float64)],
-                           rel0.astype(np.float64))
+                           rel0.astype(np.float64), reciprocal=reciprocal)
     m = 10 * w.C
     c0 = time.perf_counter()
     O.train_bucket(model, 0, 0, w.src[:m], w.rel[:m], w.dst[:m], w.C, w.U, w.S, w.lr, w.seed)
@@ -465,7 +470,7 @@ def row_knowledge_graph():
     out["cpu_baseline"] = {"value": m / ct, "unit": "edges/s", "cores": _cores(), "kind": "oracle", **host_cpu(),
                            "sample": f"first 10 chunks ({m} edges), one step, fp64, {ct:.1f} s"}
     emodel = O.Model.create(w.n, 1, w.R, w.d, w.op, w.cmp, w.loss, w.margin, [emb_h.astype(np.float64)],
-                            relp_h.astype(np.float64))
+                            relp_h.astype(np.float64), reciprocal=reciprocal)
     k = 100
     c0 = time.perf_counter()
     O.rank_eval(emodel, w.held_src[:k], w.held_rel[:k], w.held_dst[:k], np.concatenate([w.src, w.held_src]),
@@ -739,7 +744,8 @@ def row_negatives():
             "points": points}
 
 
-ROWS = {"bucketing": row_bucketing, "knowledge_graph": row_knowledge_graph, "big_bucket": row_big_bucket,
+ROWS = {"bucketing": row_bucketing, "knowledge_graph": row_knowledge_graph,
+        "knowledge_graph_reciprocal": lambda: row_knowledge_graph(reciprocal=True), "big_bucket": row_big_bucket,
         "epoch": row_epoch, "tiny": row_tiny, "negatives": row_negatives}
 
 
