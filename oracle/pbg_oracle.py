@@ -48,7 +48,17 @@ with its reason, in the design notes of the repository):
     source and destination negatives): relation r keeps a second parameter
     row r + R; the source-corruption side scores sim(g(x_d, theta_{r+R}), x_t)
     with its own positive sim(g(x_d, theta_{r+R}), x_s), while the destination
-    side and the edge score f keep theta_r.
+    side and the edge score f keep theta_r;
+  * entity types (Sec. 3.1 negatives of the relation's types, Sec. 4.1
+    unpartitioned types): each relation fixes a source and a destination type,
+    a type is split into P parts or kept whole (its partition index is 0), and
+    an edge's bucket is (partition of s in its type, partition of d in its
+    type).  A bucket's edges, sorted by relation, train in runs of consecutive
+    chunks whose relations share the (source type, destination type) pair;
+    the negatives of a run's chunks come from the tables of that pair, and a
+    step never spans two runs;
+  * per-relation edge weights (Sec. 1 and 6, per-relation configuration):
+    the weight of an edge's relation multiplies that edge's loss on both sides.
 """
 
 from __future__ import annotations
@@ -253,6 +263,9 @@ class Model:
     rel: np.ndarray | None = None                # (R or 2R, width) float64
     relG: np.ndarray | None = None               # (R or 2R, width) float64, element-wise Adagrad
     reciprocal: bool = False                     # rows R..2R-1 of rel: the source-side parameters
+    weights: np.ndarray | None = None            # (R,) per-relation edge weights (None: all 1)
+    types: "EntityTypes | None" = None           # entity types (None: one partitioned type; emb keyed
+                                                 # by partition p, else by (type, partition))
 
     @staticmethod
     def create(n, P, R, d, op, cmp, loss, margin, emb_parts, rel_params=None,
@@ -275,9 +288,92 @@ class Model:
             m.relG = np.zeros_like(m.rel) if relG is None else np.array(relG, np.float64).reshape(rows, width)
         return m
 
+    @staticmethod
+    def create_typed(types: "EntityTypes", P, R, d, op, cmp, loss, margin, tables, rel_params=None,
+                     weights=None, reciprocal=False):
+        """A model over several entity types: tables maps (type, partition) to
+        its (rows, d) embedding array, for every partition of every type."""
+        if len(types.rel_src) != R or len(types.rel_dst) != R:
+            raise ValueError("every relation needs a source and a destination type")
+        m = Model.create(P, P, R, d, op, cmp, loss, margin, [np.zeros((1, d)) for _ in range(P)],
+                         rel_params, reciprocal=reciprocal)
+        m.n = None
+        m.emb, m.G = {}, {}
+        for t in range(types.count):
+            for p in range(types.parts(t, P)):
+                e = np.array(tables[(t, p)], dtype=np.float64)
+                assert e.shape == (types.rows(t, P, p), d), (t, p, e.shape)
+                m.emb[(t, p)] = e
+                m.G[(t, p)] = np.zeros(e.shape[0])
+        m.types = types
+        if weights is not None:
+            m.weights = np.array(weights, dtype=np.float64).reshape(R)
+        return m
+
+    def edge_weights(self, r):
+        """Weight of each edge from its relation (1 without weights)."""
+        r = np.asarray(r, dtype=np.int64)
+        return np.ones(r.shape) if self.weights is None else self.weights[r]
+
     def reverse_rel(self, r):
         """Parameter row of the source side of relation r (reciprocal: r + R)."""
         return np.asarray(r, dtype=np.int64) + (self.R if self.reciprocal else 0)
+
+
+@dataclass
+class EntityTypes:
+    """Entity types of a graph: counts[t] entities of type t, each type split
+    into P contiguous parts or kept whole, and the (source, destination) type of
+    every relation."""
+    counts: list
+    partitioned: list
+    rel_src: np.ndarray
+    rel_dst: np.ndarray
+
+    @property
+    def count(self):
+        return len(self.counts)
+
+    def parts(self, t, P):
+        return P if self.partitioned[t] else 1
+
+    def rows(self, t, P, p):
+        return partition_rows(self.counts[t], self.parts(t, P), p)
+
+    def tables(self, r, i, j):
+        """(source table, destination table) of relation r's edges in bucket
+        (i, j), or None when its types cannot have edges there (a whole type
+        lives in partition 0)."""
+        st, dt = int(self.rel_src[r]), int(self.rel_dst[r])
+        if (not self.partitioned[st] and i != 0) or (not self.partitioned[dt] and j != 0):
+            return None
+        return (st, i), (dt, j)
+
+
+def bucket_edges_typed(src, rel, dst, types: EntityTypes, P: int):
+    """Bucketing with entity types (Sec. 4.1): ids are per type; an edge goes
+    to bucket part(s) * P + part(d), part(v) its partition within its type (0
+    for a type kept whole), keeping the input order inside each bucket.
+    Returns (offsets[P*P+1], src_local, rel, dst_local) as bucket_edges."""
+    src = np.asarray(src, dtype=np.int64)
+    dst = np.asarray(dst, dtype=np.int64)
+    rel = np.asarray(rel, dtype=np.int64)
+    st, dt = np.asarray(types.rel_src)[rel], np.asarray(types.rel_dst)[rel]
+    ns = np.asarray(types.counts, np.int64)[st]
+    nd = np.asarray(types.counts, np.int64)[dt]
+    if src.size and (src.min() < 0 or dst.min() < 0 or np.any(src >= ns) or np.any(dst >= nd)):
+        raise ValueError("entity id out of range for its type")
+    parts = np.array([types.parts(t, P) for t in range(types.count)], np.int64)
+    ps_s = -(-ns // parts[st])
+    ps_d = -(-nd // parts[dt])
+    ps_part, pd_part = src // ps_s, dst // ps_d
+    b = ps_part * P + pd_part
+    order = np.argsort(b, kind="stable")
+    counts = np.bincount(b, minlength=P * P)
+    offsets = np.zeros(P * P + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    return (offsets, (src - ps_part * ps_s)[order].astype(np.int32), rel[order].astype(np.int32),
+            (dst - pd_part * ps_d)[order].astype(np.int32))
 
 
 # --------------------------------------------------------------------------
@@ -400,10 +496,13 @@ def make_chunks(m: int, C: int, rel, chunking: str):
     raise ValueError(chunking)
 
 
-def step_negatives(model: Model, i: int, j: int, step, seed: int, U: int, first_chunk: int = 0):
-    """Uniform negatives (destination side, source side) of each chunk of a step."""
+def step_negatives(model: Model, i: int, j: int, step, seed: int, U: int, first_chunk: int = 0, tables=None):
+    """Uniform negatives (destination side, source side) of each chunk of a step
+    of bucket (i, j), drawn over the rows of the source and destination tables
+    (tables: their keys, by default partitions i and j)."""
     b = i * model.P + j
-    rows_i, rows_j = model.emb[i].shape[0], model.emb[j].shape[0]
+    ti, tj = (i, j) if tables is None else tables
+    rows_i, rows_j = model.emb[ti].shape[0], model.emb[tj].shape[0]
     return [(uniform_negatives(seed, b, first_chunk + c, 0, U, rows_j),
              uniform_negatives(seed, b, first_chunk + c, 1, U, rows_i)) for (c, _, _) in step]
 
@@ -428,18 +527,43 @@ def train_bucket(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, S:
     m = src.shape[0]
     chunks = make_chunks(m, C, rel, chunking)
     rel = np.zeros(m, dtype=np.int64) if rel is None else np.asarray(rel, dtype=np.int64)
-    if branches is not None and len(chunks) > S:
+    runs = type_runs(model, i, j, chunks, rel)
+    if branches is not None and (len(runs) > 1 or len(chunks) > S):
         raise ValueError("hinge branches can be given for one step only")
     step_losses = []
-    for s0 in range(0, len(chunks), S):
-        step = chunks[s0:s0 + S]
-        negs = step_negatives(model, i, j, step, seed, U, first_chunk)
-        loss, grads, rel_grad = step_loss_and_grad(model, i, j, src, rel, dst, step, negs,
-                                                   branches=branches)
-        adagrad_update(model, grads, rel_grad, lr)
-        step_losses.append(loss)
+    for run, tables in runs:
+        for s0 in range(0, len(run), S):
+            step = run[s0:s0 + S]
+            negs = step_negatives(model, i, j, step, seed, U, first_chunk, tables)
+            loss, grads, rel_grad = step_loss_and_grad(model, tables[0], tables[1], src, rel, dst, step, negs,
+                                                       branches=branches)
+            adagrad_update(model, grads, rel_grad, lr)
+            step_losses.append(loss)
     total = float(sum(step_losses))
     return (total, step_losses) if return_steps else total
+
+
+def type_runs(model: Model, i: int, j: int, chunks, rel):
+    """The call's chunks as runs of consecutive chunks that share their
+    tables, with those tables' keys: one run over partitions i and j without
+    entity types; with types, a new run wherever the (source type,
+    destination type) of the chunks' relation changes (the chunks must each
+    hold one relation, as relation-grouped chunks do)."""
+    if model.types is None:
+        return [(list(chunks), (i, j))] if chunks else []
+    runs = []
+    for ch in chunks:
+        r = np.unique(rel[ch[1]:ch[2]])
+        if len(r) != 1:
+            raise ValueError("with entity types every chunk must hold one relation (relation-grouped chunks)")
+        tables = model.types.tables(int(r[0]), i, j)
+        if tables is None:
+            raise ValueError(f"relation {int(r[0])} has no edges in bucket ({i}, {j})")
+        if runs and runs[-1][1] == tables:
+            runs[-1][0].append(ch)
+        else:
+            runs.append(([ch], tables))
+    return runs
 
 
 def step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=True, branches=None):
@@ -496,8 +620,9 @@ def step_loss_and_grad(model, i, j, src, rel, dst, step, negs, with_grad=True, b
         if branches is not None:
             act0 = torch.as_tensor(np.asarray(branches[k][0], dtype=np.float64))
             act1 = torch.as_tensor(np.asarray(branches[k][1], dtype=np.float64))
-        loss = (side_loss(model.loss, model.margin, p, S0, valid, act0).sum()
-                + side_loss(model.loss, model.margin, p1, S1, valid, act1).sum())
+        w_e = torch.as_tensor(model.edge_weights(r_e))
+        loss = ((w_e * side_loss(model.loss, model.margin, p, S0, valid, act0)).sum()
+                + (w_e * side_loss(model.loss, model.margin, p1, S1, valid, act1)).sum())
         if with_grad:
             loss.backward()          # gradients of the chunks add up in the leaves
         step_loss += float(loss.detach())
@@ -537,21 +662,27 @@ def inspect_step(model: Model, i: int, j: int, src, rel, dst, C: int, U: int, se
       dp     (C_c,)           dL/dp_e (both sides, scores held fixed)
     all float64 numpy arrays.  With reciprocal predicates each side has its own
     positive: p and dp belong to the destination side, p1 and dp1 to the
-    source side."""
+    source side.  Losses and gradients are those of the unweighted loss (a
+    relation weight multiplies all of them).  With entity types the chunks
+    must share one (source type, destination type) pair."""
     src = np.asarray(src, dtype=np.int64)
     dst = np.asarray(dst, dtype=np.int64)
     m = src.shape[0]
     step = make_chunks(m, C, rel, chunking)
     rel = np.zeros(m, dtype=np.int64) if rel is None else np.asarray(rel, dtype=np.int64)
-    negs = step_negatives(model, i, j, step, seed, U, first_chunk)
+    runs = type_runs(model, i, j, step, rel)
+    if len(runs) > 1:
+        raise ValueError("the chunks span several (source type, destination type) pairs")
+    ti, tj = runs[0][1] if runs else (i, j)
+    negs = step_negatives(model, i, j, step, seed, U, first_chunk, (ti, tj))
     theta_all = None if model.rel is None else torch.tensor(model.rel, dtype=_F64)
     out = []
     with torch.no_grad():
         for (c, lo, hi), (u_dst, u_src) in zip(step, negs):
-            xs = torch.tensor(model.emb[i][src[lo:hi]], dtype=_F64)
-            xd = torch.tensor(model.emb[j][dst[lo:hi]], dtype=_F64)
-            cand_dst = torch.cat([xd, torch.tensor(model.emb[j][u_dst], dtype=_F64)], 0)
-            cand_src = torch.cat([xs, torch.tensor(model.emb[i][u_src], dtype=_F64)], 0)
+            xs = torch.tensor(model.emb[ti][src[lo:hi]], dtype=_F64)
+            xd = torch.tensor(model.emb[tj][dst[lo:hi]], dtype=_F64)
+            cand_dst = torch.cat([xd, torch.tensor(model.emb[tj][u_dst], dtype=_F64)], 0)
+            cand_src = torch.cat([xs, torch.tensor(model.emb[ti][u_src], dtype=_F64)], 0)
             r_e = rel[lo:hi]
             theta_e = None if theta_all is None else theta_all[torch.from_numpy(r_e)]
             if model.reciprocal:

@@ -1024,3 +1024,240 @@ def test_reciprocal_rank_eval_brute_force():
         sd = 1 + sum(1 for c in cand if c != t and _py_sim("cos", q, list(E[c])) >= p0)
         ss = 1 + sum(1 for c in cand if c != s and _py_sim("cos", k, list(E[c])) >= p1)
         assert sranks[e] == sd and sranks[len(src) + e] == ss
+
+
+# --------------------------------- entity types and relation weights (NEXT-4)
+def _typed(counts, partitioned, rel_src, rel_dst, P, d, op, cmp, loss, seed, R=None, weights=None, scale=0.5):
+    types = O.EntityTypes(list(counts), list(partitioned), np.asarray(rel_src), np.asarray(rel_dst))
+    R = len(rel_src) if R is None else R
+    rng = np.random.default_rng(seed)
+    tables = {(t, p): rng.standard_normal((types.rows(t, P, p), d)) * scale
+              for t in range(types.count) for p in range(types.parts(t, P))}
+    w = O.relation_param_width(op, d)
+    relp = None if w == 0 else rng.standard_normal((R, w)) * 0.5 + (np.eye(d).reshape(-1) if op == "linear" else 0)
+    return O.Model.create_typed(types, P, R, d, op, cmp, loss, 0.1, tables, relp, weights=weights)
+
+
+def test_typed_bucketing_brute_force():
+    """Three types, type 2 kept whole: bucket = (partition of s in its type,
+    partition of d in its type), local ids, stable order, by explicit loops."""
+    counts, part = [10, 7, 4], [True, True, False]
+    rel_src, rel_dst = np.array([0, 1, 2, 0]), np.array([1, 2, 0, 0])
+    types = O.EntityTypes(counts, part, rel_src, rel_dst)
+    P = 3
+    rng = np.random.default_rng(3)
+    m = 60
+    rel = rng.integers(0, 4, m)
+    src = np.array([rng.integers(0, counts[rel_src[r]]) for r in rel])
+    dst = np.array([rng.integers(0, counts[rel_dst[r]]) for r in rel])
+    off, sl, rl, dl = O.bucket_edges_typed(src, rel, dst, types, P)
+    want = {}
+    for e in range(m):
+        r = int(rel[e])
+        loc = []
+        for t, v in ((rel_src[r], src[e]), (rel_dst[r], dst[e])):
+            size = -(-counts[t] // P) if part[t] else counts[t]
+            loc.append((int(v) // size, int(v) % size))
+        want.setdefault(loc[0][0] * P + loc[1][0], []).append((loc[0][1], r, loc[1][1]))
+    for b in range(P * P):
+        got = list(zip(sl[off[b]:off[b + 1]].tolist(), rl[off[b]:off[b + 1]].tolist(), dl[off[b]:off[b + 1]].tolist()))
+        assert got == want.get(b, []), b
+
+
+def test_typed_bucketing_unpartitioned_destinations_give_p_buckets():
+    """If every destination type is kept whole, edges fall into the P buckets
+    (i, 0) only (Sec. 4.1)."""
+    types = O.EntityTypes([1000, 30], [True, False], np.array([0, 0]), np.array([1, 1]))
+    P = 4
+    rng = np.random.default_rng(5)
+    rel = rng.integers(0, 2, 500)
+    src, dst = rng.integers(0, 1000, 500), rng.integers(0, 30, 500)
+    off = O.bucket_edges_typed(src, rel, dst, types, P)[0]
+    counts = np.diff(off).reshape(P, P)
+    assert counts[:, 1:].sum() == 0 and np.all(counts[:, 0] > 0)
+
+
+def test_one_type_typed_model_is_the_untyped_model():
+    P, d = 2, 4
+    typed = _typed([9], [True], [0, 0], [0, 0], P, d, "diagonal", "dot", "logistic", 11)
+    untyped = O.Model.create(9, P, 2, d, "diagonal", "dot", "logistic", 0.1,
+                             [typed.emb[(0, p)] for p in range(P)], typed.rel)
+    src, rel, dst = _tiny_edges(untyped, 0, 1, 11, 11)
+    order = np.argsort(rel, kind="stable")
+    src, rel, dst = src[order], rel[order], dst[order]
+    la = O.train_bucket(typed, 0, 1, src, rel, dst, 3, 2, 2, 0.1, 8, chunking="by_relation")
+    lb = O.train_bucket(untyped, 0, 1, src, rel, dst, 3, 2, 2, 0.1, 8, chunking="by_relation")
+    assert la == lb
+    for p in range(P):
+        assert np.array_equal(typed.emb[(0, p)], untyped.emb[p])
+    assert np.array_equal(typed.rel, untyped.rel)
+
+
+def test_runs_of_disjoint_type_pairs_train_independently():
+    """Relations 0: type 0 -> 1 and 1: type 2 -> 3 touch disjoint tables.  A pass
+    over both equals a pass over relation 0's edges followed by one over
+    relation 1's with the chunk numbering continued: runs never share a step,
+    and each run draws its negatives from its own tables."""
+    mk = lambda: _typed([6, 9, 5, 8], [False] * 4, [0, 2], [1, 3], 1, 4, "translation", "cos", "softmax", 17)
+    rng = np.random.default_rng(17)
+    m0, m1 = 7, 5
+    src = np.concatenate([rng.integers(0, 6, m0), rng.integers(0, 5, m1)])
+    dst = np.concatenate([rng.integers(0, 9, m0), rng.integers(0, 8, m1)])
+    rel = np.array([0] * m0 + [1] * m1)
+    a, b = mk(), mk()
+    la = O.train_bucket(a, 0, 0, src, rel, dst, 3, 2, 4, 0.1, 21, chunking="by_relation")
+    n0 = len(O.chunk_ranges(m0, 3))
+    lb = (O.train_bucket(b, 0, 0, src[:m0], rel[:m0], dst[:m0], 3, 2, 4, 0.1, 21, chunking="by_relation")
+          + O.train_bucket(b, 0, 0, src[m0:], rel[m0:], dst[m0:], 3, 2, 4, 0.1, 21, first_chunk=n0,
+                           chunking="by_relation"))
+    assert abs(la - lb) < 1e-12
+    for k in a.emb:
+        assert np.array_equal(a.emb[k], b.emb[k]), k
+    assert np.array_equal(a.rel, b.rel)
+
+
+def test_negatives_come_from_the_relation_types():
+    """Relation 0 goes from a type of 7 entities to one of 3,000: the destination
+    side's draws cover the large type and the source side's stay below 7, and
+    only rows of those two tables move."""
+    model = _typed([7, 3000, 50], [False] * 3, [0], [1], 1, 4, "identity", "dot", "ranking", 23)
+    rng = np.random.default_rng(23)
+    src, dst, rel = rng.integers(0, 7, 40), rng.integers(0, 3000, 40), np.zeros(40, int)
+    chunks = O.chunk_ranges(40, 10)
+    ((run, tables),) = O.type_runs(model, 0, 0, chunks, rel)
+    assert tables == ((0, 0), (1, 0))
+    negs = O.step_negatives(model, 0, 0, run, 29, 100, 0, tables)
+    dst_draws = np.concatenate([u for u, _ in negs])
+    src_draws = np.concatenate([v for _, v in negs])
+    assert src_draws.max() < 7 and dst_draws.max() > 2000
+    before = {k: v.copy() for k, v in model.emb.items()}
+    O.train_bucket(model, 0, 0, src, rel, dst, 10, 100, 2, 0.1, 29, chunking="by_relation")
+    assert np.array_equal(before[(2, 0)], model.emb[(2, 0)])
+    assert not np.array_equal(before[(0, 0)], model.emb[(0, 0)])
+
+
+def test_uniform_relation_weight_scales_loss_and_gradient():
+    model = _tiny_model("complex_diagonal", "dot", "softmax", R=2, seed=4)
+    src, rel, dst = _tiny_edges(model, 0, 1, 7, 4)
+    step = O.chunk_ranges(7, 3)
+    negs = O.step_negatives(model, 0, 1, step, 6, 2)
+    l1, g1, r1 = O.step_loss_and_grad(model, 0, 1, src, rel, dst, step, negs)
+    model.weights = np.array([2.5, 2.5])
+    l2, g2, r2 = O.step_loss_and_grad(model, 0, 1, src, rel, dst, step, negs)
+    assert abs(l2 - 2.5 * l1) < 1e-12 * abs(l2)
+    for p in g1:
+        assert np.allclose(g2[p][1], 2.5 * g1[p][1], atol=1e-13, rtol=1e-13)
+    assert np.allclose(r2[1], 2.5 * r1[1], atol=1e-13, rtol=1e-13)
+
+
+def test_relation_weights_weigh_each_chunk():
+    """Relation-grouped chunks, weights (0.5, 0, 3): the step's gradient is the
+    sum over chunks of the chunk's relation weight times its unit-weight
+    gradient, and a relation of weight 0 has no effect."""
+    model = _tiny_model("translation", "cos", "logistic", R=3, seed=9)
+    src, rel, dst = _tiny_edges(model, 1, 0, 12, 9)
+    order = np.argsort(rel, kind="stable")
+    src, rel, dst = src[order], rel[order], dst[order]
+    step = O.chunk_ranges_by_relation(rel, 3)
+    negs = O.step_negatives(model, 1, 0, step, 2, 2)
+    w = np.array([0.5, 0.0, 3.0])
+    total_l, total = 0.0, {}
+    for ch, ng in zip(step, negs):
+        l, g, rg = O.step_loss_and_grad(model, 1, 0, src, rel, dst, [ch], [ng])
+        wc = w[rel[ch[1]]]
+        total_l += wc * l
+        for p, (ids, gr) in g.items():
+            for a, row in enumerate(ids):
+                total[(p, row)] = total.get((p, row), 0) + wc * gr[a]
+        for a, r in enumerate(rg[0]):
+            total[("rel", r)] = total.get(("rel", r), 0) + wc * rg[1][a]
+    model.weights = w
+    l, g, rg = O.step_loss_and_grad(model, 1, 0, src, rel, dst, step, negs)
+    assert abs(l - total_l) < 1e-12 * max(1.0, abs(l))
+    for p, (ids, gr) in g.items():
+        for a, row in enumerate(ids):
+            assert np.allclose(gr[a], total[(p, row)], atol=1e-12, rtol=0)
+    for a, r in enumerate(rg[0]):
+        assert np.allclose(rg[1][a], total[("rel", r)], atol=1e-12, rtol=0)
+        if r == 1:
+            assert not rg[1][a].any()
+
+
+def test_typed_weighted_step_matches_finite_differences():
+    """Unbalanced types (5 vs 40 entities), two type pairs, weights; the first
+    run holds the chunks of two relations of one type pair: central
+    differences of its step."""
+    model = _typed([5, 40], [False, False], [0, 0, 1], [1, 1, 1], 1, 3, "diagonal", "dot", "logistic", 31,
+                   weights=[0.7, 1.9, 1.3])
+    rng = np.random.default_rng(31)
+    rel = np.array([0, 0, 0, 0, 1, 1, 2, 2, 2])
+    src = np.array([rng.integers(0, 5 if r < 2 else 40) for r in rel])
+    dst = rng.integers(0, 40, len(rel))
+    chunks = O.chunk_ranges_by_relation(rel, 3)
+    runs = O.type_runs(model, 0, 0, chunks, rel)
+    assert [t for _, t in runs] == [((0, 0), (1, 0)), ((1, 0), (1, 0))]
+    run, tables = runs[0]
+    negs = O.step_negatives(model, 0, 0, run, 3, 2, 0, tables)
+    _, grads, rel_grad = O.step_loss_and_grad(model, tables[0], tables[1], src, rel, dst, run, negs)
+    f = lambda: O.step_loss_and_grad(model, tables[0], tables[1], src, rel, dst, run, negs, with_grad=False)[0]
+    h = 1e-6
+    for key, (ids, g) in grads.items():
+        for a, row in enumerate(ids):
+            for k in range(model.d):
+                keep = model.emb[key][row, k]
+                model.emb[key][row, k] = keep + h
+                up = f()
+                model.emb[key][row, k] = keep - h
+                dn = f()
+                model.emb[key][row, k] = keep
+                assert abs((up - dn) / (2 * h) - g[a, k]) <= 1e-6 * max(1.0, abs(g[a, k]))
+    ids, g = rel_grad
+    for a, r in enumerate(ids):
+        for k in range(model.d):
+            keep = model.rel[r, k]
+            model.rel[r, k] = keep + h
+            up = f()
+            model.rel[r, k] = keep - h
+            dn = f()
+            model.rel[r, k] = keep
+            assert abs((up - dn) / (2 * h) - g[a, k]) <= 1e-6 * max(1.0, abs(g[a, k]))
+
+
+def test_whole_type_lives_in_partition_zero():
+    """P = 2, users split in two, items kept whole; relations user -> item,
+    item -> user, user -> user.  Bucketing puts item endpoints in partition 0,
+    every bucket with edges trains against its relation's tables (an epoch in
+    inside-out order), and asking for item-source edges in bucket (1, 0) is
+    an error."""
+    types = O.EntityTypes([20, 6], [True, False], np.array([0, 1, 0]), np.array([1, 0, 0]))
+    P, d = 2, 3
+    rng = np.random.default_rng(37)
+    tables = {(t, p): rng.standard_normal((types.rows(t, P, p), d)) * 0.5
+              for t in range(2) for p in range(types.parts(t, P))}
+    model = O.Model.create_typed(types, P, 3, d, "translation", "dot", "ranking", 0.1, tables,
+                                 rng.standard_normal((3, d)) * 0.3)
+    m = 90
+    rel = rng.integers(0, 3, m)
+    src = np.array([rng.integers(0, types.counts[types.rel_src[r]]) for r in rel])
+    dst = np.array([rng.integers(0, types.counts[types.rel_dst[r]]) for r in rel])
+    off, sl, rl, dl = O.bucket_edges_typed(src, rel, dst, types, P)
+    per = np.diff(off).reshape(P, P)
+    assert per[1, 1] == 0 or np.all(rl[off[3]:off[4]] == 2)
+    # item endpoints: the item-source relation only in buckets (0, *), the item-destination one only in (*, 0)
+    for b in range(P * P):
+        r_b = rl[off[b]:off[b + 1]]
+        if b // P == 1:
+            assert not np.any(r_b == 1)
+        if b % P == 1:
+            assert not np.any(r_b == 0)
+    # sort each bucket by relation for the relation-grouped chunks
+    for b in range(P * P):
+        lo, hi = off[b], off[b + 1]
+        o = np.argsort(rl[lo:hi], kind="stable")
+        sl[lo:hi], rl[lo:hi], dl[lo:hi] = sl[lo:hi][o], rl[lo:hi][o], dl[lo:hi][o]
+    before = {k: v.copy() for k, v in model.emb.items()}
+    O.train_epoch(model, off, sl, rl, dl, 4, 3, 2, 0.1, 41, chunking="by_relation")
+    assert all(not np.array_equal(before[k], model.emb[k]) for k in model.emb)
+    with pytest.raises(ValueError):
+        O.train_bucket(model, 1, 0, np.array([0, 1]), np.array([1, 1]), np.array([0, 1]), 4, 3, 2, 0.1, 41,
+                       chunking="by_relation")
