@@ -235,6 +235,58 @@ pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* s
                             const pbg_neg_config* neg, float lr, uint64_t seed,
                             double* loss_host);
 
+/* Entity types (Sec. 3.1: negatives only from the entity type of the edge's
+ * relation; Sec. 4.1 and Fig. 1 centre: a small type may stay unpartitioned).
+ * Replaces the single type of pbg_bucket_init with num_types types: type t
+ * has type_entities[t] entities (host int64) and is split into the context's
+ * P contiguous partitions when type_partitioned[t] != 0, else kept whole in
+ * one table at partition 0.  Relation r goes from type rel_src_type[r] to
+ * type rel_dst_type[r] (host int32, R entries).  Ids of entities are per type.
+ * Every table is unbound afterwards (bind them with pbg_bind_type_partition);
+ * call it before any training.  INVALID_ARG for num_types outside [1, 4096],
+ * a type without entities or with an empty partition, or a relation naming a
+ * type outside [0, num_types).
+ * With several types:
+ *  - pbg_bucket_edges takes per-type ids; edge (s, r, d) goes to bucket
+ *    (partition of s in its type, partition of d in its type), 0 for a whole
+ *    type (so with every destination type whole only the P buckets (i, 0)
+ *    have edges);
+ *  - pbg_train_bucket on bucket (i, j) takes the bucket's edges sorted by
+ *    relation (PBG_CHUNK_BY_RELATION when R > 1) and trains them in runs of
+ *    consecutive relations that share a (source type, destination type):
+ *    each run's chunks score against, and draw their uniform negatives from,
+ *    table (source type, i) and table (destination type, j); steps never span
+ *    two runs; chunk numbers continue across runs.  Each run's ids are
+ *    checked against its tables before anything trains;
+ *  - pbg_train_epoch needs every table bound in device memory (no swapping);
+ *    all ids are checked on the host first;
+ *  - pbg_inspect_step takes edges of one run;
+ *  - pbg_score_edges, pbg_score_edges_noalloc, pbg_rank_eval and
+ *    pbg_rank_sampled return UNSUPPORTED;
+ *  - pbg_bind_partition, pbg_partition_rows and pbg_sample_negatives refer to
+ *    type 0. */
+pbg_status pbg_set_entity_types(pbg_ctx* ctx, int32_t num_types, const int64_t* type_entities,
+                                const int32_t* type_partitioned, const int32_t* rel_src_type,
+                                const int32_t* rel_dst_type);
+
+/* Binds table (type t, partition p) as pbg_bind_partition binds a partition
+ * (rows: pbg_type_partition_rows).  INVALID_ARG for a table that does not
+ * exist (p > 0 of a whole type). */
+pbg_status pbg_bind_type_partition(pbg_ctx* ctx, int32_t t, int32_t p, float* emb, float* adagrad, int32_t where);
+
+/* Rows of table (type t, partition p), or -1 when it does not exist. */
+int64_t pbg_type_partition_rows(const pbg_ctx* ctx, int32_t t, int32_t p);
+
+/* Per-relation edge weights (Sec. 1 and 6: per-relation configuration):
+ * weights_host[r] (host float32, R entries, finite and >= 0) multiplies the
+ * loss of every edge of relation r on both sides, and so its gradients.
+ * NULL restores weight 1 for every relation.  The weight is applied per
+ * chunk, so a training call whose chunks may mix relations of different
+ * weights (consecutive chunks with R > 1) returns UNSUPPORTED unless all
+ * weights are equal.  loss_host and the step losses include the weights;
+ * pbg_inspect_step's row_loss and dscores are those of the unweighted loss. */
+pbg_status pbg_set_relation_weights(pbg_ctx* ctx, const float* weights_host);
+
 /* Relation-grouped order of a bucket's edges (Sec. 4.3): writes the n edges
  * (src, rel, dst: device int32) stably sorted by relation to src_out,
  * rel_out, dst_out (device int32, not overlapping the inputs), the order that

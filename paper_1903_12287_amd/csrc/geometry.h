@@ -56,6 +56,7 @@ struct StepGeom {
   int recip;        // reciprocal predicates: the source side uses relation row r + R
   int R;            // relations (the offset of the source side's rows)
   int relN;         // rows of relc per chunk (N; 2C with reciprocal predicates)
+  const float* cweight;   // relation weight of each chunk of the step (device), NULL: all 1
 };
 
 // index of edge e's positive score of side s in pos / dpos: one shared

@@ -70,6 +70,7 @@ struct GemmArgsH {
   int nct;
   int loss;
   float margin;
+  const float* cscale;   // EPI_STORE: output of chunk c times cscale[c] (NULL: as is)
 };
 
 // bf16-input score contraction with a loss epilogue (EPI_LOSS, EPI_LOSS_BITS or
@@ -213,6 +214,16 @@ void launch_bucket_scatter(const int64_t* src, const int64_t* dst, const int32_t
 void launch_bucket_keys(const int64_t* src, const int64_t* dst, int64_t n, int64_t ps, int P,
                         uint32_t* keys, uint32_t* vals, hipStream_t s);
 void launch_bucket_offsets(const uint32_t* keys, int64_t n, int nb, int64_t* offsets, hipStream_t s);
+// entity types: bucket keys from each relation's type geometry geo [R][4] =
+// (source partition size, source entities, destination partition size,
+// destination entities), range checks into flag (1 source, 2 destination,
+// 4 relation); then local ids through the sorted positions
+void launch_typed_bucket_keys(const int64_t* src, const int32_t* rel, const int64_t* dst, int64_t n,
+                              const int64_t* geo, int R, int P, uint32_t* keys, uint32_t* vals, uint32_t* flag,
+                              hipStream_t s);
+void launch_typed_bucket_gather(const uint32_t* vals, const int64_t* src, const int32_t* rel, const int64_t* dst,
+                                int64_t n, const int64_t* geo, int32_t* src_local, int32_t* rel_out,
+                                int32_t* dst_local, hipStream_t s);
 void launch_bucket_gather(const uint32_t* vals, const int64_t* src, const int32_t* rel,
                           const int64_t* dst, int64_t n, int64_t ps, int32_t* src_local,
                           int32_t* rel_out, int32_t* dst_local, hipStream_t s);

@@ -131,6 +131,15 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
       b.rowloss[(int64_t)(c * 2 + 0) * g.C + e] = side_loss[0];
       b.rowloss[(int64_t)(c * 2 + 1) * g.C + e] = side_loss[1];
     }
+    if (g.cweight) {
+      // the chunk's relation weight multiplies the edge's loss and every
+      // gradient (the contractions' share is scaled as they store it)
+      const float w = g.cweight[c];
+      loss *= (double)w;
+      dp *= w;
+      dp1 *= w;
+      dsum1 *= w;
+    }
     b.dpos[pos_index(g, c, 0, e)] = dp;
     if (g.recip) b.dpos[pos_index(g, c, 1, e)] = dp1;
     b.dsum1[ce] = dsum1;

@@ -45,6 +45,48 @@ __global__ void bucket_gather_kernel(const uint32_t* vals, const int64_t* src, c
   }
 }
 
+// ---- entity types: each relation's (partition size, entity count) of its
+// source and destination type in geo[r * 4 .. r * 4 + 3].  Bit 4 of flag: a
+// relation id out of range (its edge keyed with relation 0, never used), bits
+// 1 / 2: a source / destination id out of its type's range.
+__global__ void typed_bucket_keys_kernel(const int64_t* src, const int32_t* rel, const int64_t* dst, int64_t n,
+                                         const int64_t* geo, int R, int P, uint32_t* keys, uint32_t* vals,
+                                         uint32_t* flag) {
+  uint32_t bad = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    int r = rel ? rel[i] : 0;
+    if (r < 0 || r >= R) {
+      bad |= 4u;
+      r = 0;
+    }
+    const int64_t* gr = geo + (int64_t)r * 4;
+    const int64_t s = src[i], d = dst[i];
+    if (s < 0 || s >= gr[1]) bad |= 1u;
+    if (d < 0 || d >= gr[3]) bad |= 2u;
+    const int64_t ps = s < 0 || s >= gr[1] ? 0 : s / gr[0];
+    const int64_t pd = d < 0 || d >= gr[3] ? 0 : d / gr[2];
+    keys[i] = (uint32_t)(ps * P + pd);
+    vals[i] = (uint32_t)i;
+  }
+  if (bad) atomicOr(flag, bad);
+}
+
+__global__ void typed_bucket_gather_kernel(const uint32_t* vals, const int64_t* src, const int32_t* rel,
+                                           const int64_t* dst, int64_t n, const int64_t* geo, int32_t* src_local,
+                                           int32_t* rel_out, int32_t* dst_local) {
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
+       k += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = vals[k];
+    const int r = rel ? rel[i] : 0;
+    const int64_t* gr = geo + (int64_t)r * 4;
+    const int64_t s = src[i], d = dst[i];
+    src_local[k] = (int32_t)(s - (s / gr[0]) * gr[0]);
+    dst_local[k] = (int32_t)(d - (d / gr[2]) * gr[2]);
+    if (rel_out) rel_out[k] = r;
+  }
+}
+
 // ---- direct counting sort (at most BUCKET_DIRECT_MAX buckets) -------------
 // The edges are cut into tiles of BUCKET_TILE consecutive edges.  Pass 1 counts
 // each tile's edges per bucket (and checks the ids); an exclusive scan over
@@ -284,4 +326,19 @@ void launch_bucket_gather(const uint32_t* vals, const int64_t* src, const int32_
   if (n <= 0) return;
   bucket_gather_kernel<<<grid_cap(n), 256, 0, s>>>(vals, src, rel, dst, n, ps, src_local, rel_out,
                                                    dst_local);
+}
+
+void launch_typed_bucket_keys(const int64_t* src, const int32_t* rel, const int64_t* dst, int64_t n,
+                              const int64_t* geo, int R, int P, uint32_t* keys, uint32_t* vals, uint32_t* flag,
+                              hipStream_t s) {
+  if (n <= 0) return;
+  typed_bucket_keys_kernel<<<grid_cap(n), 256, 0, s>>>(src, rel, dst, n, geo, R, P, keys, vals, flag);
+}
+
+void launch_typed_bucket_gather(const uint32_t* vals, const int64_t* src, const int32_t* rel, const int64_t* dst,
+                                int64_t n, const int64_t* geo, int32_t* src_local, int32_t* rel_out,
+                                int32_t* dst_local, hipStream_t s) {
+  if (n <= 0) return;
+  typed_bucket_gather_kernel<<<grid_cap(n), 256, 0, s>>>(vals, src, rel, dst, n, geo, src_local, rel_out,
+                                                          dst_local);
 }

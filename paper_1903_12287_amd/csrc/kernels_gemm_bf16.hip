@@ -461,6 +461,8 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
   const int colb = n0 + WN * wn + l16;
   if (EPI == EPI_STORE) {
     float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
+    const bool scaled = a.cscale != nullptr;
+    const float sc = scaled ? a.cscale[c] : 1.0f;
 #pragma unroll
     for (int i = 0; i < IM; ++i)
 #pragma unroll
@@ -470,7 +472,8 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
 #pragma unroll
           for (int j = 0; j < JN; ++j) {
             const int n = colb + 16 * j;
-            if (n < N) Cm[(int64_t)m * a.ldc + n] = acc[i][j][r];
+            const float v = acc[i][j][r];
+            if (n < N) Cm[(int64_t)m * a.ldc + n] = scaled ? v * sc : v;
           }
         }
       }

@@ -58,6 +58,7 @@ extern "C" pbg_status pbg_bucket_edges(pbg_ctx* ctx, const int64_t* src, const i
   const int P = ctx->P;
   const int nb = P * P;
   if (nb > (1 << 24)) return set_err(ctx, PBG_ERR_UNSUPPORTED, "too many buckets");
+  if (ctx->T > 1) return bucket_edges_typed(ctx, src, rel, dst, n, offsets, src_local, rel_out, dst_local);
   hipStream_t s = ctx->cs;
   DevBuf buf;
   if (nb <= BUCKET_DIRECT_MAX) {

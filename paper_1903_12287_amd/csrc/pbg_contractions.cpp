@@ -69,6 +69,8 @@ static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t*
   na.ldb = q_ld;
   na.mdim = DIM_NC;
   na.kdim = DIM_CC;
+  // the relation weight of each chunk scales its gradients (NULL: weight 1)
+  qa.cscale = na.cscale = g.cweight;
   launch_gemm_bf16_pair(qa, na, nch * 2, cs);
 }
 
@@ -212,6 +214,7 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   na.c_ss = (int64_t)N * dp;
   na.mdim = DIM_NC;
   na.kdim = DIM_CC;
+  qa.cscale = na.cscale = g.cweight;   // the chunks' relation weights
   launch_gemm_split_pair(qa, na, nch * 2, cs);
 }
 

@@ -230,6 +230,9 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
     return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL edge arrays");
   if (ctx->R > 1 && total > 0 && !rel_host)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "rel may be NULL only with one relation");
+  if (ctx->T > 1)
+    return train_epoch_typed(ctx, offsets_host, src_local_host, ctx->R > 1 ? rel_host : nullptr, dst_local_host, neg,
+                             lr, seed, loss_host);
   for (int p = 0; p < P; ++p)
     if (!ctx->parts[p].emb || ctx->parts[p].where != PBG_MEM_PINNED_HOST)
       return set_err(ctx, PBG_ERR_STATE, "partition %d must be bound in page-locked host memory", p);
@@ -351,8 +354,16 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
     (void)hipStreamWaitEvent(run.cs, run.eb[k].ready, 0);
     const int64_t n = offsets_host[b + 1] - offsets_host[b];
     double loss = 0.0;
-    st = train_bucket_device(ctx, i, j, si.emb, si.G, sj.emb, sj.G, run.eb[k].src, run.hrel ? run.eb[k].rel : nullptr,
-                             run.eb[k].dst, n, neg, lr, seed, &loss, &ctx->step_losses);
+    BucketTables tb;
+    tb.emb_i = si.emb;
+    tb.G_i = si.G;
+    tb.emb_j = sj.emb;
+    tb.G_j = sj.G;
+    tb.rows_i = run.rows(i);
+    tb.rows_j = run.rows(j);
+    tb.same = i == j;
+    st = train_bucket_device(ctx, i, j, tb, run.eb[k].src, run.hrel ? run.eb[k].rel : nullptr, run.eb[k].dst, n, neg,
+                             lr, seed, &loss, &ctx->step_losses);
     if (st != PBG_OK) return st;
     total_loss += loss;
     (void)hipEventRecord(si.released, run.cs);

@@ -20,7 +20,15 @@ extern "C" pbg_status pbg_inspect_step(pbg_ctx* ctx, int32_t i, int32_t j, const
   if (!ctx) return PBG_ERR_INVALID_ARG;
   if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
   ctx->err.clear();
-  pbg_status st = check_bucket_call(ctx, i, j, src_local, rel, dst_local, n_edges, neg);
+  BucketTables tb;
+  pbg_status st = PBG_OK;
+  if (ctx->T > 1) {
+    // entity types: the edges must form one run (one pair of tables)
+    st = typed_single_run(ctx, i, j, src_local, rel, dst_local, n_edges, neg, &tb);
+  } else {
+    st = check_bucket_call(ctx, i, j, src_local, rel, dst_local, n_edges, neg);
+    tb = partition_tables(ctx, i, j);
+  }
   if (st != PBG_OK) return st;
   const int C = neg->chunk_size, U = neg->num_uniform, S = neg->chunks_per_step;
   if (loss_host) *loss_host = 0.0;
@@ -37,11 +45,9 @@ extern "C" pbg_status pbg_inspect_step(pbg_ctx* ctx, int32_t i, int32_t j, const
   if (st != PBG_OK) return st;
 
   hipStream_t cs = ctx->cs;
-  const Partition& pi = ctx->parts[i];
-  const Partition& pj = ctx->parts[j];
   StepGeom g;
-  bucket_geom(ctx, i, j, C, U, seed, g);
-  StepBufs b = bucket_bufs(ctx, pi.emb, pi.G, pj.emb, pj.G);
+  bucket_geom(ctx, i, j, tb, C, U, seed, g);
+  StepBufs b = bucket_bufs(ctx, tb);
   const int nch = (int)nchunks;
   g.nchunks = nch;
   g.m_step = (int)n_edges;

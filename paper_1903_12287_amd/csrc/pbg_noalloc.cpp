@@ -52,6 +52,7 @@ extern "C" pbg_status pbg_score_edges_noalloc(pbg_ctx* ctx, int32_t i, int32_t j
   if (!ctx) return PBG_ERR_INVALID_ARG;
   if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
   ctx->err.clear();
+  if (ctx->T > 1) return set_err(ctx, PBG_ERR_UNSUPPORTED, "pbg_score_edges_noalloc takes one entity type");
   if (i < 0 || i >= ctx->P || j < 0 || j >= ctx->P)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "bucket (%d, %d) out of range", i, j);
   if (n < 0 || n > 0x7FFFFFFFll) return set_err(ctx, PBG_ERR_INVALID_ARG, "n out of range");

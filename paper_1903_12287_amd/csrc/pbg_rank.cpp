@@ -70,6 +70,7 @@ pbg_status rank_impl(pbg_ctx* ctx, const char* name, const int32_t* src, const i
   if (!ctx) return PBG_ERR_INVALID_ARG;
   if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
   ctx->err.clear();
+  if (ctx->T > 1) return set_err(ctx, PBG_ERR_UNSUPPORTED, "%s takes one entity type", name);
   if (ctx->P != 1) return set_err(ctx, PBG_ERR_UNSUPPORTED, "%s needs a single partition", name);
   const bool recip = reciprocal(ctx);
   if (ctx->cmp == CMP_COS && ctx->op != OP_IDENTITY && ctx->R > 1 && !recip)

@@ -246,13 +246,17 @@ pbg_status relation_chunk_bounds(pbg_ctx* ctx, const int32_t* rel, int64_t n, in
   if (e != hipSuccess) return hip_fail(ctx, e, "relation copy");
   std::vector<int32_t>& cs = ctx->cstart_host;
   cs.clear();
+  ctx->crel_host.clear();
   int64_t run0 = 0;
   for (int64_t k = 0; k <= n; ++k) {
     if (k < n && k > 0 && r[k] < r[k - 1])
       return set_err(ctx, PBG_ERR_INVALID_ARG,
                      "relation-grouped chunks need the edges sorted by relation (edge %lld)", (long long)k);
     if (k == n || (k > 0 && r[k] != r[k - 1])) {
-      for (int64_t c = run0; c < k; c += C) cs.push_back((int32_t)c);
+      for (int64_t c = run0; c < k; c += C) {
+        cs.push_back((int32_t)c);
+        ctx->crel_host.push_back(r[run0]);
+      }
       run0 = k;
     }
   }
@@ -323,6 +327,11 @@ pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_part
   ctx->ps = ps;
   ctx->dr = op == PBG_OP_IDENTITY ? 0 : (op == PBG_OP_LINEAR ? dim * dim : dim);
   ctx->parts.assign(num_partitions, Partition());
+  ctx->T = 1;
+  ctx->type_n.assign(1, num_entities);
+  ctx->type_part.assign(1, 1);
+  ctx->rel_st.assign(num_relations, 0);
+  ctx->rel_dt.assign(num_relations, 0);
   if (hipGetDevice(&ctx->device) != hipSuccess) {
     (void)hipGetLastError();
     return fail(PBG_ERR_DEVICE, "no HIP device");
@@ -342,6 +351,7 @@ void pbg_free(pbg_ctx* ctx) {
   ctx->ws.release();
   if (ctx->steploss_dev) (void)hipFree(ctx->steploss_dev);
   if (ctx->cstart_dev) (void)hipFree(ctx->cstart_dev);
+  if (ctx->cweight_dev) (void)hipFree(ctx->cweight_dev);
   for (auto& s : ctx->slots) {
     if (s.emb) (void)hipFree(s.emb);
     if (s.ready) (void)hipEventDestroy(s.ready);
@@ -361,10 +371,7 @@ const char* pbg_last_error(const pbg_ctx* ctx) {
   return ctx->err.c_str();
 }
 
-int64_t pbg_partition_rows(const pbg_ctx* ctx, int32_t p) {
-  if (!ctx || ctx->invalid || p < 0 || p >= ctx->P) return -1;
-  return std::min<int64_t>(ctx->ps, ctx->n - (int64_t)p * ctx->ps);
-}
+int64_t pbg_partition_rows(const pbg_ctx* ctx, int32_t p) { return table_rows(ctx, 0, p); }
 
 int64_t pbg_relation_param_floats(const pbg_ctx* ctx) {
   if (!ctx || ctx->invalid) return -1;
@@ -443,10 +450,32 @@ pbg_status check_neg_config(pbg_ctx* ctx, const pbg_neg_config* neg) {
   return PBG_OK;
 }
 
-void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, int C, int U, uint64_t seed, StepGeom& g) {
+int64_t table_rows(const pbg_ctx* ctx, int t, int p) {
+  if (!ctx || ctx->invalid || t < 0 || t >= ctx->T) return -1;
+  const int parts = ctx->type_part[(size_t)t] ? ctx->P : 1;
+  if (p < 0 || p >= parts) return -1;
+  const int64_t n = ctx->type_n[(size_t)t];
+  const int64_t ps = (n + parts - 1) / parts;
+  return std::min<int64_t>(ps, n - (int64_t)p * ps);
+}
+
+BucketTables partition_tables(pbg_ctx* ctx, int32_t i, int32_t j) {
+  BucketTables tb;
+  tb.emb_i = ctx->parts[i].emb;
+  tb.G_i = ctx->parts[i].G;
+  tb.emb_j = ctx->parts[j].emb;
+  tb.G_j = ctx->parts[j].G;
+  tb.rows_i = pbg_partition_rows(ctx, i);
+  tb.rows_j = pbg_partition_rows(ctx, j);
+  tb.same = i == j;
+  return tb;
+}
+
+void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, const BucketTables& tb, int C, int U, uint64_t seed,
+                 StepGeom& g) {
   const int N = C + U;
   const int d = ctx->d, dp = round_up(d, 4), Np = round_up(N, 4);
-  const int64_t rows_i = pbg_partition_rows(ctx, i), rows_j = pbg_partition_rows(ctx, j);
+  const int64_t rows_i = tb.rows_i, rows_j = tb.rows_j;
   memset(&g, 0, sizeof(g));
   g.C = C;
   g.U = U;
@@ -460,7 +489,7 @@ void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, int C, int U, uint64_
   g.cmp = ctx->cmp;
   g.loss = ctx->loss;
   g.margin = ctx->margin;
-  g.same_table = (i == j) ? 1 : 0;
+  g.same_table = tb.same ? 1 : 0;
   g.rows_i = (int)rows_i;
   g.rows_j = (int)rows_j;
   g.rb = bits_for((uint64_t)std::max(rows_i, rows_j) - 1);
@@ -472,13 +501,13 @@ void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, int C, int U, uint64_
   g.relN = g.recip ? 2 * C : N;
 }
 
-StepBufs bucket_bufs(pbg_ctx* ctx, float* emb_i, float* G_i, float* emb_j, float* G_j) {
+StepBufs bucket_bufs(pbg_ctx* ctx, const BucketTables& tb) {
   StepBufs b = ctx->bufs;
   b.nuniq = (unsigned long long*)(ctx->steploss_dev + std::max<int64_t>(ctx->steploss_cap, 1));
-  b.emb_i = emb_i;
-  b.emb_j = emb_j;
-  b.G_i = G_i;
-  b.G_j = G_j;
+  b.emb_i = tb.emb_i;
+  b.emb_j = tb.emb_j;
+  b.G_i = tb.G_i;
+  b.G_j = tb.G_j;
   b.relp = ctx->relp;
   b.relG = ctx->relG;
   if (!sorted_relation_keys(ctx)) {
@@ -497,11 +526,41 @@ void run_gather_forward(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, hipS
 }
 
 // Runs the step loop on already-validated, device-resident partitions.
-pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i, float* G_i,
-                               float* emb_j, float* G_j, const int32_t* src, const int32_t* rel,
-                               const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg,
-                               float lr, uint64_t seed, double* loss_out,
-                               std::vector<double>* step_losses) {
+pbg_status chunk_weights(pbg_ctx* ctx, bool grouped, int64_t nchunks, const float** out) {
+  *out = nullptr;
+  if (ctx->relw.empty() || nchunks <= 0) return PBG_OK;
+  std::vector<float> w((size_t)nchunks);
+  if (grouped) {
+    for (int64_t c = 0; c < nchunks; ++c) w[(size_t)c] = ctx->relw[(size_t)ctx->crel_host[(size_t)c]];
+  } else {
+    // consecutive chunks may mix relations: one weight for all of them
+    for (float v : ctx->relw)
+      if (v != ctx->relw[0])
+        return set_err(ctx, PBG_ERR_UNSUPPORTED,
+                       "relation weights that differ need relation-grouped chunks (PBG_CHUNK_BY_RELATION)");
+    std::fill(w.begin(), w.end(), ctx->relw[0]);
+  }
+  if (ctx->cweight_cap < nchunks) {
+    if (ctx->cweight_dev) (void)hipFree(ctx->cweight_dev);
+    ctx->cweight_dev = nullptr;
+    ctx->cweight_cap = 0;
+    if (hipMalloc(&ctx->cweight_dev, (size_t)nchunks * 4) != hipSuccess) {
+      (void)hipGetLastError();
+      ctx->cweight_dev = nullptr;
+      return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "chunk weight allocation failed");
+    }
+    ctx->cweight_cap = nchunks;
+  }
+  hipError_t e = hipMemcpyAsync(ctx->cweight_dev, w.data(), (size_t)nchunks * 4, hipMemcpyHostToDevice, ctx->cs);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->cs);
+  if (e != hipSuccess) return hip_fail(ctx, e, "chunk weight copy");
+  *out = ctx->cweight_dev;
+  return PBG_OK;
+}
+
+pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketTables& tb, const int32_t* src,
+                               const int32_t* rel, const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg,
+                               float lr, uint64_t seed, double* loss_out, std::vector<double>* step_losses) {
   const int C = neg->chunk_size, U = neg->num_uniform, S = neg->chunks_per_step;
   pbg_status st = ensure_workspace(ctx, C, U, S);
   if (st != PBG_OK) return st;
@@ -514,6 +573,9 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   }
   const std::vector<int32_t>& cbound = ctx->cstart_host;
   const int64_t nchunks = grouped ? (int64_t)cbound.size() - 1 : (n_edges + C - 1) / C;
+  const float* cweight = nullptr;
+  st = chunk_weights(ctx, grouped, nchunks, &cweight);
+  if (st != PBG_OK) return st;
   // first edge of chunk c (c <= nchunks)
   auto chunk_at = [&](int64_t c) -> int64_t {
     return grouped ? (int64_t)cbound[(size_t)c] : std::min<int64_t>(n_edges, c * C);
@@ -529,13 +591,13 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
   const int N = C + U;
   const int d = ctx->d, dp = round_up(d, 4);
   StepGeom g;
-  bucket_geom(ctx, i, j, C, U, seed, g);
+  bucket_geom(ctx, i, j, tb, C, U, seed, g);
   const int key_bits = g.rb + (g.same_table ? 0 : 1);
   const int rel_bits = bits_for((uint64_t)relation_rows(ctx) - 1);
   const bool has_rel = ctx->op != OP_IDENTITY;
   const bool linear = ctx->op == OP_LINEAR;
 
-  StepBufs b = bucket_bufs(ctx, emb_i, G_i, emb_j, G_j);
+  StepBufs b = bucket_bufs(ctx, tb);
   if (hipMemsetAsync(b.nuniq, 0, 8, cs) != hipSuccess) return hip_fail(ctx, hipGetLastError(), "counter reset");
 
   if (!ensure_side(ctx)) return set_err(ctx, PBG_ERR_DEVICE, "could not create the side stream");
@@ -569,6 +631,7 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i,
     g.m_step = m_step;
     g.chunk0 = neg->first_chunk + c0;
     g.cstart = grouped ? ctx->cstart_dev + c0 : nullptr;
+    g.cweight = cweight ? cweight + c0 : nullptr;
     b.src = src + e_lo;
     b.dst = dst + e_lo;
     b.rel = rel ? rel + e_lo : nullptr;
@@ -760,6 +823,13 @@ extern "C" pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const
   if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
   ctx->err.clear();
   if (!std::isfinite(lr) || lr < 0.f) return set_err(ctx, PBG_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (ctx->T > 1) {
+    // entity types: the call's runs are checked and trained one by one
+    ctx->stats = pbg_stats();
+    ctx->step_losses.clear();
+    return train_bucket_typed(ctx, i, j, src_local, rel, dst_local, n_edges, neg, lr, seed, loss_host,
+                              &ctx->step_losses);
+  }
   pbg_status st = check_bucket_call(ctx, i, j, src_local, rel, dst_local, n_edges, neg);
   if (st != PBG_OK) return st;
   ctx->stats = pbg_stats();
@@ -768,10 +838,8 @@ extern "C" pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const
     if (loss_host) *loss_host = 0.0;
     return PBG_OK;
   }
-  const Partition& pi = ctx->parts[i];
-  const Partition& pj = ctx->parts[j];
-  return train_bucket_device(ctx, i, j, pi.emb, pi.G, pj.emb, pj.G, src_local, rel, dst_local, n_edges,
-                             neg, lr, seed, loss_host, &ctx->step_losses);
+  return train_bucket_device(ctx, i, j, partition_tables(ctx, i, j), src_local, rel, dst_local, n_edges, neg, lr,
+                             seed, loss_host, &ctx->step_losses);
 }
 
 extern "C" pbg_status pbg_score_edges(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
@@ -780,6 +848,7 @@ extern "C" pbg_status pbg_score_edges(pbg_ctx* ctx, int32_t i, int32_t j, const 
   if (!ctx) return PBG_ERR_INVALID_ARG;
   if (ctx->invalid) return set_err(ctx, PBG_ERR_STATE, "context failed to initialise");
   ctx->err.clear();
+  if (ctx->T > 1) return set_err(ctx, PBG_ERR_UNSUPPORTED, "pbg_score_edges takes one entity type");
   if (i < 0 || i >= ctx->P || j < 0 || j >= ctx->P)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "bucket (%d, %d) out of range", i, j);
   if (n < 0 || n > 0x7FFFFFFFll) return set_err(ctx, PBG_ERR_INVALID_ARG, "n out of range");

@@ -51,7 +51,7 @@ struct BufsH {
 };
 
 struct pbg_ctx {
-  int64_t n = 0;
+  int64_t n = 0;                   // entities of type 0 (the only type without pbg_set_entity_types)
   int P = 1, R = 1, d = 1, op = 0, cmp = 0, loss = 0;
   float margin = 0.f;
   uint32_t flags = 0;
@@ -61,7 +61,19 @@ struct pbg_ctx {
   bool invalid = false;
   hipStream_t cs = nullptr;  // compute stream
   hipStream_t xs = nullptr;  // copy stream
-  std::vector<Partition> parts;
+  std::vector<Partition> parts;    // table (type t, partition p) at t * P + p
+  // entity types (Sec. 3.1, Sec. 4.1): entities per type, whether a type is
+  // split into P partitions (else one table at partition 0), and the source
+  // and destination type of every relation
+  int T = 1;
+  std::vector<int64_t> type_n;
+  std::vector<int> type_part;
+  std::vector<int> rel_st, rel_dt;
+  // per-relation edge weights (empty: every weight 1), and the weights of the
+  // current call's chunks on the device
+  std::vector<float> relw;
+  float* cweight_dev = nullptr;
+  int64_t cweight_cap = 0;
   float* relp = nullptr;
   float* relG = nullptr;
   std::string err;
@@ -87,6 +99,7 @@ struct pbg_ctx {
   // relation-grouped chunks of the current call: bounds in the call's edge
   // arrays (host copy and device copy)
   std::vector<int32_t> cstart_host;
+  std::vector<int32_t> crel_host;  // the relation of each of those chunks
   int32_t* cstart_dev = nullptr;
   int64_t cstart_cap = 0;
 
@@ -176,13 +189,44 @@ inline bool linear_step_contractions(const pbg_ctx* ctx) {
   return ctx->op == PBG_OP_LINEAR && relation_rows(ctx) == 1;
 }
 pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps);
+
+// rows of table (type t, partition p), or -1
+int64_t table_rows(const pbg_ctx* ctx, int t, int p);
+inline Partition& table_of(pbg_ctx* ctx, int t, int p) { return ctx->parts[(size_t)t * ctx->P + p]; }
+// the source and destination tables of a bucket's edges (one run of the
+// call: a single (source type, destination type) pair)
+struct BucketTables {
+  float* emb_i = nullptr;
+  float* G_i = nullptr;
+  float* emb_j = nullptr;
+  float* G_j = nullptr;
+  int64_t rows_i = 0, rows_j = 0;
+  bool same = false;   // one table serves both sides
+};
+// partitions i and j of type 0
+BucketTables partition_tables(pbg_ctx* ctx, int32_t i, int32_t j);
 // geometry of the steps of bucket (i, j) (chunk and candidate counts, padded
-// strides, partition rows, key widths) and the step buffers bound to the
-// given partitions and the context's workspace
-void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, int C, int U, uint64_t seed, StepGeom& g);
-StepBufs bucket_bufs(pbg_ctx* ctx, float* emb_i, float* G_i, float* emb_j, float* G_j);
-pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, float* emb_i, float* G_i,
-                               float* emb_j, float* G_j, const int32_t* src, const int32_t* rel,
-                               const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg,
-                               float lr, uint64_t seed, double* loss_out,
-                               std::vector<double>* step_losses);
+// strides, table rows, key widths) and the step buffers bound to the given
+// tables and the context's workspace
+void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, const BucketTables& tb, int C, int U, uint64_t seed,
+                 StepGeom& g);
+StepBufs bucket_bufs(pbg_ctx* ctx, const BucketTables& tb);
+pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketTables& tb, const int32_t* src,
+                               const int32_t* rel, const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg,
+                               float lr, uint64_t seed, double* loss_out, std::vector<double>* step_losses);
+// relation weights of the call's chunks into ctx->cweight_dev (NULL when no
+// weights are set); UNSUPPORTED when consecutive chunks would mix relations of
+// different weights.  Needs ctx->crel_host for relation-grouped chunks.
+pbg_status chunk_weights(pbg_ctx* ctx, bool grouped, int64_t nchunks, const float** out);
+// typed contexts: the runs of a call and their training (pbg_types.cpp)
+pbg_status train_bucket_typed(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src, const int32_t* rel,
+                              const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg, float lr, uint64_t seed,
+                              double* loss_out, std::vector<double>* step_losses);
+// the tables of a typed call whose edges form one run (pbg_inspect_step)
+pbg_status typed_single_run(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src, const int32_t* rel,
+                            const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg, BucketTables* tb);
+pbg_status train_epoch_typed(pbg_ctx* ctx, const int64_t* offsets_host, const int32_t* src_host,
+                             const int32_t* rel_host, const int32_t* dst_host, const pbg_neg_config* neg, float lr,
+                             uint64_t seed, double* loss_host);
+pbg_status bucket_edges_typed(pbg_ctx* ctx, const int64_t* src, const int32_t* rel, const int64_t* dst, int64_t n,
+                              int64_t* offsets, int32_t* src_local, int32_t* rel_out, int32_t* dst_local);

@@ -40,6 +40,7 @@ EXPORTS = (
     "pbg_bind_relations", "pbg_set_streams", "pbg_train_bucket", "pbg_get_step_losses",
     "pbg_train_epoch", "pbg_score_edges", "pbg_rank_eval", "pbg_rank_sampled", "pbg_get_stats",
     "pbg_sample_negatives", "pbg_inspect_step", "pbg_score_edges_noalloc", "pbg_group_by_relation",
+    "pbg_set_entity_types", "pbg_bind_type_partition", "pbg_type_partition_rows", "pbg_set_relation_weights",
 )
 
 
@@ -106,6 +107,10 @@ def library() -> ctypes.CDLL:
         "pbg_sample_negatives": ([vp, i32, i32, i64, i64, i32, u64, vp], i32),
         "pbg_inspect_step": ([vp, i32, i32, vp, vp, vp, i64, ctypes.POINTER(NegConfig), u64, vp, vp, vp, vp,
                               dp], i32),
+        "pbg_set_entity_types": ([vp, i32, vp, vp, vp, vp], i32),
+        "pbg_bind_type_partition": ([vp, i32, i32, vp, vp, i32], i32),
+        "pbg_type_partition_rows": ([vp, i32, i32], i64),
+        "pbg_set_relation_weights": ([vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -168,6 +173,7 @@ def pbg_bucket_init(num_entities, num_partitions, num_relations, dim, op, cmp, l
             L.pbg_free(ctx)
         raise PbgError(st, msg)
     ctx._flags = int(flags)   # the layouts some outputs take depend on them
+    ctx._R = int(num_relations)
     return ctx
 
 
@@ -207,6 +213,49 @@ def pbg_bind_partition(ctx, p, emb, adagrad, where=MEM_DEVICE):
     _check(ctx, library().pbg_bind_partition(ctx, int(p), _ptr(emb, torch.float32, "emb", on_dev),
                                              _ptr(adagrad, torch.float32, "adagrad", on_dev), int(where)))
     _keep(ctx, ("partition", int(p)), emb, adagrad)
+
+
+def pbg_set_entity_types(ctx, type_entities, type_partitioned, rel_src_type, rel_dst_type):
+    """Host sequences: entities per type, partitioned flags per type, and the
+    source and destination type of every relation."""
+    import numpy as np
+    n = np.ascontiguousarray(type_entities, dtype=np.int64)
+    part = np.ascontiguousarray(type_partitioned, dtype=np.int32)
+    rs = np.ascontiguousarray(rel_src_type, dtype=np.int32)
+    rd = np.ascontiguousarray(rel_dst_type, dtype=np.int32)
+    if part.size != n.size or rs.size != getattr(ctx, "_R", rs.size) or rd.size != rs.size:
+        raise ValueError("one partitioned flag per type and one source and destination type per relation")
+    _check(ctx, library().pbg_set_entity_types(ctx, int(n.size), n.ctypes.data, part.ctypes.data, rs.ctypes.data,
+                                               rd.ctypes.data))
+    bound = getattr(ctx, "_bound", None)
+    if bound is not None:   # the tables are unbound
+        for k in [k for k in bound if isinstance(k, tuple) and k[0] in ("partition", "table")]:
+            del bound[k]
+
+
+def pbg_bind_type_partition(ctx, t, p, emb, adagrad, where=MEM_DEVICE):
+    on_dev = where == MEM_DEVICE
+    if not on_dev and not (emb.is_pinned() and adagrad.is_pinned()):
+        raise ValueError("host partitions must be in page-locked (pinned) memory")
+    _check(ctx, library().pbg_bind_type_partition(ctx, int(t), int(p), _ptr(emb, torch.float32, "emb", on_dev),
+                                                  _ptr(adagrad, torch.float32, "adagrad", on_dev), int(where)))
+    _keep(ctx, ("table", int(t), int(p)), emb, adagrad)
+
+
+def pbg_type_partition_rows(ctx, t, p) -> int:
+    return int(library().pbg_type_partition_rows(ctx, int(t), int(p)))
+
+
+def pbg_set_relation_weights(ctx, weights):
+    """weights: host sequence of R floats, or None for weight 1 everywhere."""
+    import numpy as np
+    if weights is None:
+        _check(ctx, library().pbg_set_relation_weights(ctx, None))
+        return
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    if w.size != getattr(ctx, "_R", w.size):
+        raise ValueError("one weight per relation")
+    _check(ctx, library().pbg_set_relation_weights(ctx, w.ctypes.data))
 
 
 def pbg_bind_relations(ctx, params, adagrad):

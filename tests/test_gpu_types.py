@@ -1,0 +1,272 @@
+"""Entity types (type-restricted negatives, unpartitioned types) and
+per-relation edge weights on the GPU, against the oracle.
+
+A typed context keeps one table per (type, partition); a bucket's relation-
+sorted edges train in runs that share a (source type, destination type), each
+run's negatives drawn from its two tables.  Relation weights scale each
+relation's loss and gradients.  Free-running passes are compared at 1e-4 as
+in test_gpu_train; bucketing is integer work and must match bit for bit.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import pbg_oracle as O
+from paper_1903_12287_amd import synth
+from tests.pbg_cases import GpuModel, make_problem, oracle_model
+
+pytestmark = pytest.mark.gpu
+
+
+class TypedGpu:
+    """Device tables of a typed graph bound to a library context."""
+
+    def __init__(self, types, P, R, d, op, cmp, loss, tables, relp, weights=None, flags=0):
+        from paper_1903_12287_amd import pbg
+        self.pbg = pbg
+        dev = torch.device("cuda")
+        self.ctx = pbg.pbg_bucket_init(types.counts[0], P, R, d, op, cmp, loss, 0.1, flags)
+        pbg.pbg_set_entity_types(self.ctx, types.counts, [int(v) for v in types.partitioned], types.rel_src,
+                                 types.rel_dst)
+        self.emb, self.G = {}, {}
+        for (t, p), e in tables.items():
+            assert pbg.pbg_type_partition_rows(self.ctx, t, p) == e.shape[0]
+            self.emb[(t, p)] = torch.from_numpy(e.astype(np.float32)).to(dev)
+            self.G[(t, p)] = torch.zeros(e.shape[0], dtype=torch.float32, device=dev)
+            pbg.pbg_bind_type_partition(self.ctx, t, p, self.emb[(t, p)], self.G[(t, p)])
+        self.relp = self.relG = None
+        if relp is not None:
+            self.relp = torch.from_numpy(relp.astype(np.float32)).to(dev)
+            self.relG = torch.zeros_like(self.relp)
+            pbg.pbg_bind_relations(self.ctx, self.relp, self.relG)
+        if weights is not None:
+            pbg.pbg_set_relation_weights(self.ctx, weights)
+        pbg.pbg_set_streams(self.ctx, torch.cuda.current_stream(), None)
+
+    def train(self, i, j, src, rel, dst, C, U, S, lr, seed, first_chunk=0, chunking="by_relation"):
+        dev = torch.device("cuda")
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
+        loss = self.pbg.pbg_train_bucket(self.ctx, i, j, t(src), t(rel), t(dst), C, U, S, lr, seed, first_chunk,
+                                         chunking)
+        return loss, self.pbg.pbg_get_step_losses(self.ctx)
+
+    def state(self):
+        torch.cuda.synchronize()
+        out = {"emb": {k: v.cpu().numpy().astype(np.float64) for k, v in self.emb.items()},
+               "G": {k: v.cpu().numpy().astype(np.float64) for k, v in self.G.items()}}
+        if self.relp is not None:
+            out["rel"] = self.relp.cpu().numpy().astype(np.float64)
+        return out
+
+    def close(self):
+        self.pbg.pbg_free(self.ctx)
+
+
+def _graph(seed, d, op, reciprocal=False):
+    """Users (600, partitioned), items (40, kept whole), tags (150, partitioned);
+    relations 0 user->item, 1 user->user, 2 item->user, 3 tag->user, 4 user->item."""
+    types = O.EntityTypes([600, 40, 150], [True, False, True], np.array([0, 0, 1, 2, 0]),
+                          np.array([1, 0, 0, 0, 1]))
+    P, R = 2, 5
+    rng = synth.rng_for(seed)
+    tables = {(t, p): (rng.standard_normal((types.rows(t, P, p), d)) * 0.2).astype(np.float32)
+              for t in range(types.count) for p in range(types.parts(t, P))}
+    relp = synth.perturbed_relation_params(op, 2 * R if reciprocal else R, d, rng, 0.3)
+    m = 1500
+    rel = synth.BoundedZipf(R, 0.8, rng).sample(rng, m).astype(np.int64)
+    src = np.array([rng.integers(0, types.counts[types.rel_src[r]]) for r in rel])
+    dst = np.array([rng.integers(0, types.counts[types.rel_dst[r]]) for r in rel])
+    return types, P, R, tables, relp, src, rel, dst
+
+
+def _sorted_buckets(off, sl, rl, dl, P):
+    sl, rl, dl = sl.copy(), rl.copy(), dl.copy()
+    for b in range(P * P):
+        lo, hi = off[b], off[b + 1]
+        o = np.argsort(rl[lo:hi], kind="stable")
+        sl[lo:hi], rl[lo:hi], dl[lo:hi] = sl[lo:hi][o], rl[lo:hi][o], dl[lo:hi][o]
+    return sl, rl, dl
+
+
+def test_typed_bucketing_matches_oracle():
+    from paper_1903_12287_amd import pbg
+    types, P, R, tables, relp, src, rel, dst = _graph(3, 8, "diagonal")
+    dev = torch.device("cuda")
+    g = TypedGpu(types, P, R, 8, "diagonal", "dot", "logistic", tables, relp)
+    try:
+        n = len(src)
+        off = torch.empty(P * P + 1, dtype=torch.int64, device=dev)
+        sl, rl, dl = (torch.empty(n, dtype=torch.int32, device=dev) for _ in range(3))
+        t64 = lambda a: torch.from_numpy(np.asarray(a, np.int64)).to(dev)
+        t32 = lambda a: torch.from_numpy(np.asarray(a, np.int32)).to(dev)
+        pbg.pbg_bucket_edges(g.ctx, t64(src), t32(rel), t64(dst), off, sl, rl, dl)
+        want = O.bucket_edges_typed(src, rel, dst, types, P)
+        for a, b in zip((off, sl, rl, dl), want):
+            assert np.array_equal(a.cpu().numpy(), b)
+        # with every destination type whole only buckets (i, 0) would have
+        # edges; here the item -> user relation fills buckets (0, 1)
+        per = np.diff(want[0]).reshape(P, P)
+        assert per[1, 1] > 0 and per[0, 1] > 0
+        bad = np.array(dst)
+        bad[7] = types.counts[types.rel_dst[rel[7]]]   # one past its type's range
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_bucket_edges(g.ctx, t64(src), t32(rel), t64(bad), off, sl, rl, dl)
+        assert ei.value.status_name == "INVALID_ARG"
+    finally:
+        g.close()
+
+
+@pytest.mark.parametrize("op,cmp,loss,weights,reciprocal", [
+    ("diagonal", "dot", "logistic", None, False),
+    ("translation", "cos", "ranking", [0.5, 2.0, 1.0, 0.0, 1.5], False),
+    ("complex_diagonal", "dot", "softmax", [1.0, 0.7, 2.5, 1.2, 0.3], True),
+    ("linear", "dot", "logistic", [1.3, 1.0, 0.6, 1.0, 2.0], False),
+])
+def test_typed_buckets_match_oracle(op, cmp, loss, weights, reciprocal):
+    """Buckets (1, 0), (0, 1) and (0, 0) of the typed graph trained in turn:
+    runs of several type pairs per bucket, a whole type, relation weights."""
+    from paper_1903_12287_amd import pbg
+    d = 16
+    types, P, R, tables, relp, src, rel, dst = _graph(7, d, op, reciprocal)
+    off, sl, rl, dl = O.bucket_edges_typed(src, rel, dst, types, P)
+    sl, rl, dl = _sorted_buckets(off, sl, rl, dl, P)
+    C, U, S, lr, seed = 16, 10, 3, 0.1, 77
+    g = TypedGpu(types, P, R, d, op, cmp, loss, tables, relp, weights, pbg.F_RECIPROCAL if reciprocal else 0)
+    om = O.Model.create_typed(types, P, R, d, op, cmp, loss, 0.1, {k: v.astype(np.float64) for k, v in tables.items()},
+                              None if relp is None else relp.astype(np.float64), weights=weights,
+                              reciprocal=reciprocal)
+    try:
+        for (i, j) in [(1, 0), (0, 1), (0, 0)]:
+            b = i * P + j
+            lo, hi = off[b], off[b + 1]
+            gl, gsteps = g.train(i, j, sl[lo:hi], rl[lo:hi], dl[lo:hi], C, U, S, lr, seed)
+            ol, osteps = O.train_bucket(om, i, j, sl[lo:hi], rl[lo:hi], dl[lo:hi], C, U, S, lr, seed,
+                                        return_steps=True, chunking="by_relation")
+            runs = O.type_runs(om, i, j, O.chunk_ranges_by_relation(rl[lo:hi], C), rl[lo:hi])
+            print(f"\n[{op} bucket ({i},{j})] {hi - lo} edges, {len(runs)} runs, {len(osteps)} steps", flush=True)
+            assert len(gsteps) == len(osteps)
+            for a, o in zip(gsteps, osteps):
+                assert abs(a - o) <= 1e-4 * max(1.0, abs(o)), (i, j, a, o)
+        st = g.state()
+    finally:
+        g.close()
+    for k in om.emb:
+        err = float(np.max(np.abs(st["emb"][k] - om.emb[k])))
+        assert err <= 1e-4, (k, err)
+        gerr = float(np.max(np.abs(st["G"][k] - om.G[k]) / np.maximum(1.0, om.G[k])))
+        assert gerr <= 1e-4, (k, gerr)
+    if om.rel is not None:
+        assert float(np.max(np.abs(st["rel"] - om.rel))) <= 1e-4
+
+
+def test_typed_epoch_matches_oracle():
+    """One epoch over every bucket of the typed graph (tables in device memory),
+    inside-out order, against the oracle's epoch."""
+    from paper_1903_12287_amd import pbg
+    d = 12
+    types, P, R, tables, relp, src, rel, dst = _graph(11, d, "translation")
+    off, sl, rl, dl = O.bucket_edges_typed(src, rel, dst, types, P)
+    sl, rl, dl = _sorted_buckets(off, sl, rl, dl, P)
+    C, U, S, lr, seed = 16, 8, 2, 0.1, 91
+    weights = [1.0, 0.5, 2.0, 1.0, 0.8]
+    g = TypedGpu(types, P, R, d, "translation", "dot", "softmax", tables, relp, weights)
+    try:
+        pin = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a, dt)).pin_memory()
+        gl = pbg.pbg_train_epoch(g.ctx, torch.from_numpy(np.asarray(off, np.int64)), pin(sl, np.int32),
+                                 pin(rl, np.int32), pin(dl, np.int32), C, U, S, lr, seed, 2, "by_relation")
+        st = g.state()
+    finally:
+        g.close()
+    om = O.Model.create_typed(types, P, R, d, "translation", "dot", "softmax", 0.1,
+                              {k: v.astype(np.float64) for k, v in tables.items()}, relp.astype(np.float64),
+                              weights=weights)
+    ol = O.train_epoch(om, off, sl, rl, dl, C, U, S, lr, seed, chunking="by_relation")
+    assert abs(gl - ol) <= 1e-4 * abs(ol), (gl, ol)
+    for k in om.emb:
+        assert float(np.max(np.abs(st["emb"][k] - om.emb[k]))) <= 1e-4, k
+
+
+def test_typed_errors():
+    from paper_1903_12287_amd import pbg
+    types, P, R, tables, relp, src, rel, dst = _graph(5, 8, "diagonal")
+    dev = torch.device("cuda")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
+    g = TypedGpu(types, P, R, 8, "diagonal", "dot", "logistic", tables, relp)
+    try:
+        # item-source edges (relation 2) cannot be in bucket (1, 0): items are whole
+        z = np.array([0, 1])
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_train_bucket(g.ctx, 1, 0, t(z), t([2, 2]), t(z), 4, 2, 2, 0.1, 1, 0, "by_relation")
+        assert ei.value.status_name == "INVALID_ARG"
+        # unsorted relations, consecutive chunks with several relations
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_train_bucket(g.ctx, 0, 0, t(z), t([1, 0]), t(z), 4, 2, 2, 0.1, 1, 0, "by_relation")
+        assert ei.value.status_name == "INVALID_ARG"
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_train_bucket(g.ctx, 0, 0, t(z), t([0, 0]), t(z), 4, 2, 2, 0.1, 1, 0, "consecutive")
+        assert ei.value.status_name == "UNSUPPORTED"
+        # an id past its type's table (items have 40 rows)
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_train_bucket(g.ctx, 0, 0, t([0, 1]), t([0, 0]), t([3, 40]), 4, 2, 2, 0.1, 1, 0, "by_relation")
+        assert ei.value.status_name == "INVALID_ARG"
+        before = g.state()
+        assert all(not v.any() for v in before["G"].values())   # nothing trained
+        # entry points that take one entity type
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_score_edges(g.ctx, 0, 0, t(z), t([0, 0]), t(z), torch.empty(2, device=dev))
+        assert ei.value.status_name == "UNSUPPORTED"
+        assert pbg.pbg_type_partition_rows(g.ctx, 1, 1) == -1 and pbg.pbg_type_partition_rows(g.ctx, 0, 1) == 300
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_set_relation_weights(g.ctx, [1.0, -1.0, 1.0, 1.0, 1.0])
+        assert ei.value.status_name == "INVALID_ARG"
+    finally:
+        g.close()
+
+
+@pytest.mark.parametrize("op,cmp,loss,R,chunking,weights", [
+    ("complex_diagonal", "dot", "softmax", 4, "by_relation", [0.5, 0.0, 2.0, 1.3]),
+    ("translation", "cos", "ranking", 4, "by_relation", [1.5, 0.25, 1.0, 3.0]),
+    ("linear", "dot", "logistic", 1, "consecutive", [2.5]),
+    ("diagonal", "dot", "ranking", 3, "consecutive", [0.6, 0.6, 0.6]),
+])
+def test_relation_weights_match_oracle(op, cmp, loss, R, chunking, weights):
+    """One entity type, relation weights (a zero weight included): several steps
+    with a short last chunk against the oracle."""
+    from paper_1903_12287_amd import pbg
+    pb = make_problem(op, cmp, loss, n=150, P=2, R=R, d=20, m=437, C=16, U=10, S=3, i=1, j=0, seed=23, sigma=0.2,
+                      chunking=chunking)
+    gm = GpuModel(pb)
+    try:
+        pbg.pbg_set_relation_weights(gm.ctx, weights)
+        gm.train()
+        steps = pbg.pbg_get_step_losses(gm.ctx)
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    om.weights = np.asarray(weights, np.float64)
+    ol, osteps = O.train_bucket(om, 1, 0, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr, pb.seed,
+                                return_steps=True, chunking=chunking)
+    assert len(steps) == len(osteps)
+    for a, b in zip(steps, osteps):
+        assert abs(a - b) <= 1e-4 * max(1.0, abs(b)), (a, b)
+    for p in (0, 1):
+        assert float(np.max(np.abs(st["emb"][p] - om.emb[p]))) <= 1e-4, p
+    if om.rel is not None:
+        assert float(np.max(np.abs(st["rel"] - om.rel))) <= 1e-4
+
+
+def test_unequal_weights_need_grouped_chunks():
+    from paper_1903_12287_amd import pbg
+    pb = make_problem("diagonal", "dot", "logistic", n=100, R=3, d=8, m=100, C=16, U=4, S=2, seed=2)
+    gm = GpuModel(pb)
+    try:
+        pbg.pbg_set_relation_weights(gm.ctx, [1.0, 2.0, 1.0])
+        with pytest.raises(pbg.PbgError) as ei:
+            gm.train()
+        assert ei.value.status_name == "UNSUPPORTED"
+        pbg.pbg_set_relation_weights(gm.ctx, None)
+        gm.train()
+    finally:
+        gm.close()
