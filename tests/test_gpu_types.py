@@ -270,3 +270,49 @@ def test_unequal_weights_need_grouped_chunks():
         gm.train()
     finally:
         gm.close()
+
+
+def test_typed_bucket_at_chunk_scale():
+    """A typed bucket at the workloads' chunk shape (C = U = 1000, S = 40,
+    d = 100): users split in 4 partitions of 100,000, items (20,000) kept
+    whole; bucket (2, 0) holds user -> item (weight 1.5) and user -> user
+    (weight 0.7) edges, two steps of each.  Logistic loss (no hinge kinks):
+    per-step losses and every table against the oracle."""
+    from paper_1903_12287_amd import pbg
+    types = O.EntityTypes([400_000, 20_000], [True, False], np.array([0, 0]), np.array([1, 0]))
+    P, R, d, C, U, S = 4, 2, 100, 1000, 1000, 40
+    weights = [1.5, 0.7]
+    rng = synth.rng_for(97)
+    users = (rng.standard_normal((types.rows(0, P, 2), d)) * 0.1).astype(np.float32)
+    users0 = (rng.standard_normal((types.rows(0, P, 0), d)) * 0.1).astype(np.float32)
+    items = (rng.standard_normal((types.rows(1, P, 0), d)) * 0.1).astype(np.float32)
+    tables = {(0, 2): users, (0, 0): users0, (1, 0): items}
+    for p in (1, 3):
+        tables[(0, p)] = np.zeros((types.rows(0, P, p), d), np.float32)
+    relp = synth.perturbed_relation_params("diagonal", R, d, rng, 0.3)
+    m = 2 * S * C
+    src = np.concatenate([synth.BoundedZipf(100_000, 1.0, rng).sample(rng, m) for _ in range(2)])
+    dst = np.concatenate([synth.BoundedZipf(20_000, 1.0, rng).sample(rng, m),
+                          synth.BoundedZipf(100_000, 1.0, rng).sample(rng, m)])
+    rel = np.repeat(np.arange(2), m)
+    g = TypedGpu(types, P, R, d, "diagonal", "dot", "logistic", tables, relp, weights)
+    try:
+        gl, gsteps = g.train(2, 0, src, rel, dst, C, U, S, 0.1, 101)
+        st = g.state()
+    finally:
+        g.close()
+    om = O.Model.create_typed(types, P, R, d, "diagonal", "dot", "logistic", 0.1,
+                              {k: v.astype(np.float64) for k, v in tables.items()}, relp.astype(np.float64),
+                              weights=weights)
+    ol, osteps = O.train_bucket(om, 2, 0, src, rel, dst, C, U, S, 0.1, 101, return_steps=True, chunking="by_relation")
+    print(f"\n[typed chunk scale] steps {len(gsteps)} loss gpu {gl:.6f} oracle {ol:.6f}", flush=True)
+    assert len(gsteps) == len(osteps) == 4
+    for a, o in zip(gsteps, osteps):
+        assert abs(a - o) <= 1e-5 * abs(o), (a, o)
+    for k in om.emb:
+        err = float(np.max(np.abs(st["emb"][k] - om.emb[k])))
+        assert err <= 1e-4, (k, err)
+    assert float(np.max(np.abs(st["rel"] - om.rel))) <= 1e-4
+    # only the tables of the two runs moved
+    for p in (1, 3):
+        assert not st["G"][(0, p)].any()
