@@ -46,8 +46,16 @@ constexpr uint32_t OOB = 0x80000000u;
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// A buffer descriptor must be wave-uniform.  Tile base addresses are, but
+// their 64-bit products are formed on the vector unit, and a descriptor left
+// in vector registers would make the compiler wrap every load that uses it in
+// a loop over lanes; reading the address back from the first lane keeps it
+// scalar.
 __device__ __forceinline__ rsrc_t make_rsrc(const void* p) {
-  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, 0x7FFFFFF0, 0x00020000);
+  const uint64_t v = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, 0x7FFFFFF0, 0x00020000);
 }
 __device__ __forceinline__ u32x4 bload16(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
