@@ -283,8 +283,8 @@ int64_t pbg_type_partition_rows(const pbg_ctx* ctx, int32_t t, int32_t p);
  * NULL restores weight 1 for every relation.  The weight is applied per
  * chunk, so a training call whose chunks may mix relations of different
  * weights (consecutive chunks with R > 1) returns UNSUPPORTED unless all
- * weights are equal.  loss_host and the step losses include the weights;
- * pbg_inspect_step's row_loss and dscores are those of the unweighted loss. */
+ * weights are equal.  The training calls' losses include the weights;
+ * pbg_inspect_step reports the unweighted loss (loss_host, row_loss, dscores). */
 pbg_status pbg_set_relation_weights(pbg_ctx* ctx, const float* weights_host);
 
 /* Relation-grouped order of a bucket's edges (Sec. 4.3): writes the n edges

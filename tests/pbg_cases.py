@@ -151,16 +151,19 @@ def _norm(v):
     return np.maximum(np.linalg.norm(v, axis=-1), O.EPS_NORM)
 
 
-def score_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk=0, chunking="consecutive"):
+def score_scales(model, i, j, src, rel, dst, C, U, seed, first_chunk=0, chunking="consecutive", tables=None):
     """Per chunk of a step: (Ap (C_c,), A0 (C_c, N_c), A1 (C_c, N_c), Ap1 (C_c,)),
-    Ap1 the source side's positive score scale (reciprocal predicates; else Ap)."""
+    Ap1 the source side's positive score scale (reciprocal predicates; else Ap).
+    tables: the keys of the source and destination tables (entity types;
+    by default partitions i and j)."""
     src = np.asarray(src, np.int64)
     dst = np.asarray(dst, np.int64)
     m = src.shape[0]
     step = O.make_chunks(m, C, rel, chunking)
     rel = np.zeros(m, np.int64) if rel is None else np.asarray(rel, np.int64)
-    negs = O.step_negatives(model, i, j, step, seed, U, first_chunk)
-    Ei, Ej = model.emb[i], model.emb[j]
+    negs = O.step_negatives(model, i, j, step, seed, U, first_chunk, tables)
+    ti, tj = (i, j) if tables is None else tables
+    Ei, Ej = model.emb[ti], model.emb[tj]
     out = []
     for (c, lo, hi), (u_dst, u_src) in zip(step, negs):
         xs, xd = Ei[src[lo:hi]], Ej[dst[lo:hi]]

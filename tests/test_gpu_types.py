@@ -316,3 +316,61 @@ def test_typed_bucket_at_chunk_scale():
     # only the tables of the two runs moved
     for p in (1, 3):
         assert not st["G"][(0, p)].any()
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_typed_run_forward_elementwise(bf16):
+    """pbg_inspect_step on one run of a typed bucket at the chunk shape (C = U =
+    1000): users (partition 1 of 2, 60,000 rows) -> items (8,000, kept whole),
+    d = 96, translation + cos + ranking.  Every score, positive, side loss and
+    dL/dS element by element against the oracle (bounds as in
+    test_gpu_inspect), with the destination draws over the item table."""
+    from paper_1903_12287_amd import pbg
+    from tests.pbg_cases import check_inspection, score_scales
+    types = O.EntityTypes([120_000, 8_000], [True, False], np.array([0]), np.array([1]))
+    P, R, d, C, U = 2, 1, 96, 1000, 1000
+    rng = synth.rng_for(113)
+    tables = {(0, p): (rng.standard_normal((types.rows(0, P, p), d)) * 0.1).astype(np.float32) for p in range(P)}
+    tables[(1, 0)] = (rng.standard_normal((8_000, d)) * 0.1).astype(np.float32)
+    relp = synth.perturbed_relation_params("translation", R, d, rng, 0.3)
+    m = 5 * C + 517
+    src = synth.BoundedZipf(60_000, 1.0, rng).sample(rng, m)
+    dst = synth.BoundedZipf(8_000, 1.0, rng).sample(rng, m)
+    rel = np.zeros(m, np.int64)
+    dev = torch.device("cuda")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(dev)
+    nch = -(-m // C)
+    N = C + U
+    g = TypedGpu(types, P, R, d, "translation", "cos", "ranking", tables, relp,
+                 flags=pbg.F_BF16_SCORE if bf16 else 0)
+    try:
+        scores = torch.empty(nch * 2 * C * N, dtype=torch.float32, device=dev)
+        dscores = torch.empty_like(scores)
+        row_loss = torch.empty(nch * 2 * C, dtype=torch.float32, device=dev)
+        pos = torch.empty(nch * C, dtype=torch.float32, device=dev)
+        gloss = pbg.pbg_inspect_step(g.ctx, 1, 0, t(src), None, t(dst), C, U, 40, 131, 5, scores, dscores,
+                                     row_loss, pos)
+    finally:
+        g.close()
+    S = scores.view(nch, 2, C, N).cpu().numpy().astype(np.float64)
+    dS = dscores.view(nch, 2, C, N).cpu().numpy().astype(np.float64)
+    L = row_loss.view(nch, 2, C).cpu().numpy().astype(np.float64)
+    Pp = pos.view(nch, C).cpu().numpy().astype(np.float64)
+    gpu = []
+    for c, lo, hi in O.chunk_ranges(m, C):
+        Cc = hi - lo
+        gpu.append({"p": Pp[c, :Cc], "S0": S[c, 0, :Cc, :Cc + U], "S1": S[c, 1, :Cc, :Cc + U],
+                    "loss0": L[c, 0, :Cc], "loss1": L[c, 1, :Cc], "dS0": dS[c, 0, :Cc, :Cc + U],
+                    "dS1": dS[c, 1, :Cc, :Cc + U]})
+    om = O.Model.create_typed(types, P, R, d, "translation", "cos", "ranking", 0.1,
+                              {k: v.astype(np.float64) for k, v in tables.items()}, relp.astype(np.float64))
+    orc = O.inspect_step(om, 1, 0, src, rel, dst, C, U, 131, 5)
+    sc = score_scales(om, 1, 0, src, rel, dst, C, U, 131, 5, tables=((0, 1), (1, 0)))
+    rep = check_inspection(om, gpu, orc, sc, 2e-2 if bf16 else 1e-5)
+    print(f"\n[typed run, bf16={bf16}] {rep}", flush=True)
+    assert rep["p_ratio"] <= 1.0 and rep["s_ratio"] <= 1.0 and rep["loss_ratio"] <= 1.0
+    ol = sum(float(o["loss0"].sum() + o["loss1"].sum()) for o in orc)
+    assert abs(gloss - ol) <= (2e-2 if bf16 else 1e-5) * abs(ol)
+    # the destination side's uniform draws cover the item table, not the users'
+    negs = O.step_negatives(om, 1, 0, O.chunk_ranges(m, C), 131, U, 5, ((0, 1), (1, 0)))
+    assert max(int(u.max()) for u, _ in negs) < 8_000 and max(int(v.max()) for _, v in negs) > 8_000
