@@ -258,8 +258,11 @@ pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* s
  *    table (source type, i) and table (destination type, j); steps never span
  *    two runs; chunk numbers continue across runs.  Each run's ids are
  *    checked against its tables before anything trains;
- *  - pbg_train_epoch needs every table bound in device memory (no swapping);
- *    all ids are checked on the host first;
+ *  - pbg_train_epoch takes each table where it is bound: tables in device
+ *    memory are used in place, tables in page-locked host memory are swapped
+ *    through at most max_resident HBM slots (at least as many as the swapped
+ *    tables one bucket needs at once, else INVALID_ARG); all ids are checked
+ *    on the host first;
  *  - pbg_inspect_step takes edges of one run;
  *  - pbg_score_edges, pbg_score_edges_noalloc, pbg_rank_eval and
  *    pbg_rank_sampled return UNSUPPORTED;

@@ -60,6 +60,10 @@ struct EpochRun {
   const int64_t* off;
   const int32_t *hsrc, *hrel, *hdst;
   std::vector<std::pair<int, int>> order;   // non-empty buckets
+  // tables each of those buckets needs in a slot: table t * P + p, type 0's
+  // partitions i and j without entity types, the swapped tables of the
+  // bucket's relations with them
+  std::vector<std::vector<int>> need;
   std::vector<void*> allocs;
   std::vector<hipEvent_t> evs;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> copy_spans;
@@ -79,11 +83,11 @@ struct EpochRun {
     evs.push_back(e);
     return e;
   }
-  int64_t rows(int p) const { return pbg_partition_rows(ctx, p); }
+  int64_t rows(int tid) const { return table_rows(ctx, tid / ctx->P, tid % ctx->P); }
 
-  int64_t next_use(int p, size_t from) const {
+  int64_t next_use(int tid, size_t from) const {
     for (size_t t = from; t < order.size(); ++t)
-      if (order[t].first == p || order[t].second == p) return (int64_t)t;
+      if (std::find(need[t].begin(), need[t].end(), tid) != need[t].end()) return (int64_t)t;
     return INT64_MAX;
   }
   int slot_of(int p) const {
@@ -161,8 +165,7 @@ struct EpochRun {
   }
 };
 
-pbg_status ensure_slots(pbg_ctx* ctx, int count) {
-  const int64_t cap = ctx->ps;
+pbg_status ensure_slots(pbg_ctx* ctx, int count, int64_t cap) {
   bool ok = (int)ctx->slots.size() == count;
   for (auto& s : ctx->slots) ok = ok && s.rows_cap >= cap;
   if (ok) {
@@ -214,6 +217,7 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
   if (neg->first_chunk != 0) return set_err(ctx, PBG_ERR_INVALID_ARG, "first_chunk must be 0 for an epoch");
   if (!std::isfinite(lr) || lr < 0.f) return set_err(ctx, PBG_ERR_INVALID_ARG, "lr must be finite and >= 0");
   if (max_resident < 2) return set_err(ctx, PBG_ERR_INVALID_ARG, "max_resident must be >= 2");
+  const int32_t asked_slots = max_resident;
   max_resident = std::min(max_resident, P);
   if (max_resident < 2) max_resident = 2;
   const int nb = P * P;
@@ -230,12 +234,25 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
     return set_err(ctx, PBG_ERR_INVALID_ARG, "NULL edge arrays");
   if (ctx->R > 1 && total > 0 && !rel_host)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "rel may be NULL only with one relation");
-  if (ctx->T > 1)
-    return train_epoch_typed(ctx, offsets_host, src_local_host, ctx->R > 1 ? rel_host : nullptr, dst_local_host, neg,
-                             lr, seed, loss_host);
-  for (int p = 0; p < P; ++p)
-    if (!ctx->parts[p].emb || ctx->parts[p].where != PBG_MEM_PINNED_HOST)
-      return set_err(ctx, PBG_ERR_STATE, "partition %d must be bound in page-locked host memory", p);
+  const bool typed = ctx->T > 1;
+  const int32_t* rel_used = ctx->R > 1 ? rel_host : nullptr;
+  bool any_pinned = false;
+  if (typed) {
+    // entity types: every id, relation and bucket membership checked on the
+    // host; tables bound in page-locked host memory are swapped through HBM
+    // slots, tables in device memory are used in place
+    st = validate_typed_epoch(ctx, offsets_host, src_local_host, rel_used, dst_local_host);
+    if (st != PBG_OK) return st;
+    for (int t = 0; t < ctx->T; ++t)
+      for (int p = 0; p < (ctx->type_part[(size_t)t] ? P : 1); ++p)
+        any_pinned = any_pinned || table_of(ctx, t, p).where == PBG_MEM_PINNED_HOST;
+    if (!any_pinned) return train_epoch_typed(ctx, offsets_host, src_local_host, rel_used, dst_local_host, neg, lr,
+                                              seed, loss_host);
+  } else {
+    for (int p = 0; p < P; ++p)
+      if (!ctx->parts[p].emb || ctx->parts[p].where != PBG_MEM_PINNED_HOST)
+        return set_err(ctx, PBG_ERR_STATE, "partition %d must be bound in page-locked host memory", p);
+  }
   if (ctx->op != OP_IDENTITY && !ctx->relp) return set_err(ctx, PBG_ERR_STATE, "relation parameters are not bound");
   if (chunk_relation_operator(ctx) && !grouped_chunks(ctx, neg))
     return set_err(ctx, PBG_ERR_UNSUPPORTED,
@@ -266,11 +283,49 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
   run.hsrc = src_local_host;
   run.hrel = ctx->R > 1 ? rel_host : nullptr;
   run.hdst = dst_local_host;
-  for (auto& bk : inside_out(P))
-    if (offsets_host[bk.first * P + bk.second + 1] > offsets_host[bk.first * P + bk.second]) run.order.push_back(bk);
+  int64_t slot_rows = ctx->ps;   // rows a slot holds
+  for (auto& bk : inside_out(P)) {
+    const int b = bk.first * P + bk.second;
+    if (offsets_host[b + 1] <= offsets_host[b]) continue;
+    run.order.push_back(bk);
+    std::vector<int> nd;
+    if (!typed) {
+      nd.push_back(bk.first);
+      if (bk.second != bk.first) nd.push_back(bk.second);
+    } else {
+      // the swapped tables of the bucket's relations
+      std::vector<char> seen((size_t)ctx->R, 0);
+      for (int64_t k = offsets_host[b]; k < offsets_host[b + 1]; ++k) seen[(size_t)(rel_used ? rel_used[k] : 0)] = 1;
+      for (int r = 0; r < ctx->R; ++r) {
+        if (!seen[(size_t)r]) continue;
+        for (int tid : {ctx->rel_st[(size_t)r] * P + bk.first, ctx->rel_dt[(size_t)r] * P + bk.second})
+          if (ctx->parts[(size_t)tid].where == PBG_MEM_PINNED_HOST &&
+              std::find(nd.begin(), nd.end(), tid) == nd.end())
+            nd.push_back(tid);
+      }
+    }
+    run.need.push_back(nd);
+  }
   if (run.order.empty()) {
     if (loss_host) *loss_host = 0.0;
     return PBG_OK;
+  }
+  if (typed) {
+    // slots: as many as asked for, at most one per swapped table, at least
+    // the most tables one bucket needs; each as large as the largest one
+    int swapped = 0;
+    size_t most = 0;
+    slot_rows = 0;
+    for (int tid = 0; tid < ctx->T * P; ++tid)
+      if (ctx->parts[(size_t)tid].where == PBG_MEM_PINNED_HOST) {
+        ++swapped;
+        slot_rows = std::max(slot_rows, run.rows(tid));
+      }
+    for (const auto& nd : run.need) most = std::max(most, nd.size());
+    if ((size_t)asked_slots < most)
+      return set_err(ctx, PBG_ERR_INVALID_ARG, "a bucket needs %d swapped tables at once; max_resident is %d",
+                     (int)most, asked_slots);
+    max_resident = std::max(1, std::min(asked_slots, swapped));
   }
 
   // staging buffers for two buckets' edges, and the id-check flag
@@ -297,9 +352,10 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
   run.allocs.push_back(flag_p);
   uint32_t* flag = (uint32_t*)flag_p;
 
-  // every id is checked before any parameter changes
+  // every id is checked before any parameter changes (with entity types on
+  // the host, above)
   hipError_t e = hipMemsetAsync(flag, 0, 4, run.xs);
-  for (size_t t = 0; t < run.order.size() && e == hipSuccess; ++t) {
+  for (size_t t = 0; t < run.order.size() && e == hipSuccess && !typed; ++t) {
     const int i = run.order[t].first, j = run.order[t].second;
     const int b = i * P + j;
     const int k = (int)(t & 1);
@@ -325,7 +381,9 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
     eb.bucket = -1;
   }
 
-  st = ensure_slots(ctx, max_resident);
+  st = ensure_slots(ctx, max_resident, slot_rows);
+  if (st != PBG_OK) return st;
+  if (typed) ctx->table_override.assign((size_t)ctx->T * P, Partition());
   if (st != PBG_OK) return st;
 
   double total_loss = 0.0;
@@ -334,7 +392,7 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
     const int i = run.order[t].first, j = run.order[t].second;
     const int b = i * P + j;
     const int k = (int)(t & 1);
-    std::vector<int> need = {i, j};
+    const std::vector<int>& need = run.need[t];
     for (int p : need)
       if (run.slot_of(p) < 0 && !run.load(p, t, need))
         return set_err(ctx, PBG_ERR_STATE, "no free partition slot (max_resident %d)", max_resident);
@@ -343,34 +401,50 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
     if (t + 1 < T) {
       const int i2 = run.order[t + 1].first, j2 = run.order[t + 1].second;
       run.stage_edges((int)((t + 1) & 1), i2 * P + j2);
-      std::vector<int> keep = {i, j, i2, j2};
-      for (int p : {i2, j2})
+      std::vector<int> keep = need;
+      keep.insert(keep.end(), run.need[t + 1].begin(), run.need[t + 1].end());
+      for (int p : run.need[t + 1])
         if (run.slot_of(p) < 0) run.load(p, t + 1, keep);
     }
-    Slot& si = ctx->slots[run.slot_of(i)];
-    Slot& sj = ctx->slots[run.slot_of(j)];
-    (void)hipStreamWaitEvent(run.cs, si.ready, 0);
-    if (&sj != &si) (void)hipStreamWaitEvent(run.cs, sj.ready, 0);
+    for (int p : need) (void)hipStreamWaitEvent(run.cs, ctx->slots[run.slot_of(p)].ready, 0);
     (void)hipStreamWaitEvent(run.cs, run.eb[k].ready, 0);
     const int64_t n = offsets_host[b + 1] - offsets_host[b];
     double loss = 0.0;
-    BucketTables tb;
-    tb.emb_i = si.emb;
-    tb.G_i = si.G;
-    tb.emb_j = sj.emb;
-    tb.G_j = sj.G;
-    tb.rows_i = run.rows(i);
-    tb.rows_j = run.rows(j);
-    tb.same = i == j;
-    st = train_bucket_device(ctx, i, j, tb, run.eb[k].src, run.hrel ? run.eb[k].rel : nullptr, run.eb[k].dst, n, neg,
-                             lr, seed, &loss, &ctx->step_losses);
-    if (st != PBG_OK) return st;
+    if (typed) {
+      // the bucket's swapped tables are read from their slots
+      for (int p : need) {
+        const Slot& sl = ctx->slots[run.slot_of(p)];
+        Partition& ov = ctx->table_override[(size_t)p];
+        ov.emb = sl.emb;
+        ov.G = sl.G;
+        ov.where = PBG_MEM_DEVICE;
+      }
+      st = train_bucket_typed(ctx, i, j, run.eb[k].src, run.hrel ? run.eb[k].rel : nullptr, run.eb[k].dst, n, neg, lr,
+                              seed, &loss, &ctx->step_losses);
+      for (int p : need) ctx->table_override[(size_t)p] = Partition();
+    } else {
+      const Slot& si = ctx->slots[run.slot_of(i)];
+      const Slot& sj = ctx->slots[run.slot_of(j)];
+      BucketTables tb;
+      tb.emb_i = si.emb;
+      tb.G_i = si.G;
+      tb.emb_j = sj.emb;
+      tb.G_j = sj.G;
+      tb.rows_i = run.rows(i);
+      tb.rows_j = run.rows(j);
+      tb.same = i == j;
+      st = train_bucket_device(ctx, i, j, tb, run.eb[k].src, run.hrel ? run.eb[k].rel : nullptr, run.eb[k].dst, n,
+                               neg, lr, seed, &loss, &ctx->step_losses);
+    }
+    if (st != PBG_OK) {
+      ctx->table_override.clear();
+      return st;
+    }
     total_loss += loss;
-    (void)hipEventRecord(si.released, run.cs);
-    si.used = true;
-    if (&sj != &si) {
-      (void)hipEventRecord(sj.released, run.cs);
-      sj.used = true;
+    for (int p : need) {
+      Slot& sl = ctx->slots[run.slot_of(p)];
+      (void)hipEventRecord(sl.released, run.cs);
+      sl.used = true;
     }
     (void)hipEventRecord(run.eb[k].consumed, run.cs);
     run.eb[k].used = true;
@@ -380,6 +454,7 @@ extern "C" pbg_status pbg_train_epoch(pbg_ctx* ctx, const int64_t* offsets_host,
     ctx->slots[v].part = -1;
     ctx->slots[v].used = false;
   }
+  ctx->table_override.clear();
   e = hipGetLastError();
   if (e == hipSuccess) e = hipStreamSynchronize(run.xs);
   if (e == hipSuccess) e = hipStreamSynchronize(run.cs);

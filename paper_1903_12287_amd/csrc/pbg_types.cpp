@@ -113,8 +113,8 @@ pbg_status typed_runs(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src, co
       return set_err(ctx, PBG_ERR_INVALID_ARG,
                      "bucket (%d, %d) holds edges of relation %d, whose %s type is kept whole (partition 0 only)", i,
                      j, r[(size_t)tr.lo], !ctx->type_part[(size_t)tr.st] && i != 0 ? "source" : "destination");
-    Partition& ps = table_of(ctx, tr.st, i);
-    Partition& pd = table_of(ctx, tr.dt, j);
+    const Partition ps = resolve_table(ctx, tr.st, i);
+    const Partition pd = resolve_table(ctx, tr.dt, j);
     if (!ps.emb || !pd.emb)
       return set_err(ctx, PBG_ERR_STATE, "table (type %d, partition %d) or (type %d, partition %d) is not bound",
                      tr.st, i, tr.dt, j);
@@ -183,27 +183,20 @@ pbg_status typed_single_run(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* s
   return PBG_OK;
 }
 
-// One epoch over a typed graph whose tables are all device-resident: the
-// buckets with edges in inside-out order (Sec. 4.1, Fig. 1 right), each
-// trained as pbg_train_bucket trains it.  Every id, relation and bucket
-// membership is checked on the host before anything trains.
-pbg_status train_epoch_typed(pbg_ctx* ctx, const int64_t* off, const int32_t* hs, const int32_t* hr,
-                             const int32_t* hd, const pbg_neg_config* neg, float lr, uint64_t seed,
-                             double* loss_host) {
+// Host checks of a typed epoch, before anything trains: every table bound,
+// every relation id in range and sorted within its bucket, every relation's
+// types able to have edges in the bucket, every id inside its table.
+pbg_status validate_typed_epoch(pbg_ctx* ctx, const int64_t* off, const int32_t* hs, const int32_t* hr,
+                                const int32_t* hd) {
   const int P = ctx->P;
   const int nb = P * P;
   for (int t = 0; t < ctx->T; ++t)
-    for (int p = 0; p < (ctx->type_part[(size_t)t] ? P : 1); ++p) {
-      const Partition& tp = table_of(ctx, t, p);
-      if (!tp.emb || tp.where != PBG_MEM_DEVICE)
-        return set_err(ctx, PBG_ERR_STATE, "with entity types every table must be bound in device memory "
-                                           "(type %d, partition %d)", t, p);
-    }
-  int64_t max_bucket = 0;
+    for (int p = 0; p < (ctx->type_part[(size_t)t] ? P : 1); ++p)
+      if (!table_of(ctx, t, p).emb)
+        return set_err(ctx, PBG_ERR_STATE, "table (type %d, partition %d) is not bound", t, p);
   for (int b = 0; b < nb; ++b) {
     const int i = b / P, j = b % P;
     const int64_t lo = off[b], hi = off[b + 1];
-    max_bucket = std::max(max_bucket, hi - lo);
     for (int64_t k = lo; k < hi; ++k) {
       const int32_t r = hr ? hr[k] : 0;
       if (r < 0 || r >= ctx->R) return set_err(ctx, PBG_ERR_INVALID_ARG, "a relation id is outside [0, %d)", ctx->R);
@@ -219,6 +212,18 @@ pbg_status train_epoch_typed(pbg_ctx* ctx, const int64_t* off, const int32_t* hs
         return set_err(ctx, PBG_ERR_INVALID_ARG, "an id of bucket %d is outside its type's table", b);
     }
   }
+  return PBG_OK;
+}
+
+// One epoch over a typed graph whose tables are all device-resident (checked
+// by validate_typed_epoch): the buckets with edges in inside-out order
+// (Sec. 4.1, Fig. 1 right), each trained as pbg_train_bucket trains it.
+pbg_status train_epoch_typed(pbg_ctx* ctx, const int64_t* off, const int32_t* hs, const int32_t* hr,
+                             const int32_t* hd, const pbg_neg_config* neg, float lr, uint64_t seed,
+                             double* loss_host) {
+  const int P = ctx->P;
+  int64_t max_bucket = 0;
+  for (int b = 0; b < P * P; ++b) max_bucket = std::max(max_bucket, off[b + 1] - off[b]);
   ctx->stats = pbg_stats();
   ctx->step_losses.clear();
   DevPtrs buf;

@@ -62,6 +62,9 @@ struct pbg_ctx {
   hipStream_t cs = nullptr;  // compute stream
   hipStream_t xs = nullptr;  // copy stream
   std::vector<Partition> parts;    // table (type t, partition p) at t * P + p
+  // during a typed epoch: the HBM slot standing in for a swapped table (emb
+  // NULL: none), same indexing
+  std::vector<Partition> table_override;
   // entity types (Sec. 3.1, Sec. 4.1): entities per type, whether a type is
   // split into P partitions (else one table at partition 0), and the source
   // and destination type of every relation
@@ -193,6 +196,12 @@ pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps);
 // rows of table (type t, partition p), or -1
 int64_t table_rows(const pbg_ctx* ctx, int t, int p);
 inline Partition& table_of(pbg_ctx* ctx, int t, int p) { return ctx->parts[(size_t)t * ctx->P + p]; }
+// the table training reads: its HBM slot during a typed epoch, else as bound
+inline Partition resolve_table(const pbg_ctx* ctx, int t, int p) {
+  const size_t k = (size_t)t * ctx->P + p;
+  if (k < ctx->table_override.size() && ctx->table_override[k].emb) return ctx->table_override[k];
+  return ctx->parts[k];
+}
 // the source and destination tables of a bucket's edges (one run of the
 // call: a single (source type, destination type) pair)
 struct BucketTables {
@@ -225,6 +234,10 @@ pbg_status train_bucket_typed(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t*
 // the tables of a typed call whose edges form one run (pbg_inspect_step)
 pbg_status typed_single_run(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src, const int32_t* rel,
                             const int32_t* dst, int64_t n_edges, const pbg_neg_config* neg, BucketTables* tb);
+// host checks of a typed epoch's edges (ids, relations, order, bucket
+// membership); then the epoch with every table in device memory
+pbg_status validate_typed_epoch(pbg_ctx* ctx, const int64_t* offsets_host, const int32_t* src_host,
+                                const int32_t* rel_host, const int32_t* dst_host);
 pbg_status train_epoch_typed(pbg_ctx* ctx, const int64_t* offsets_host, const int32_t* src_host,
                              const int32_t* rel_host, const int32_t* dst_host, const pbg_neg_config* neg, float lr,
                              uint64_t seed, double* loss_host);

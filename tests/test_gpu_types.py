@@ -22,7 +22,7 @@ pytestmark = pytest.mark.gpu
 class TypedGpu:
     """Device tables of a typed graph bound to a library context."""
 
-    def __init__(self, types, P, R, d, op, cmp, loss, tables, relp, weights=None, flags=0):
+    def __init__(self, types, P, R, d, op, cmp, loss, tables, relp, weights=None, flags=0, pinned=()):
         from paper_1903_12287_amd import pbg
         self.pbg = pbg
         dev = torch.device("cuda")
@@ -32,9 +32,15 @@ class TypedGpu:
         self.emb, self.G = {}, {}
         for (t, p), e in tables.items():
             assert pbg.pbg_type_partition_rows(self.ctx, t, p) == e.shape[0]
-            self.emb[(t, p)] = torch.from_numpy(e.astype(np.float32)).to(dev)
-            self.G[(t, p)] = torch.zeros(e.shape[0], dtype=torch.float32, device=dev)
-            pbg.pbg_bind_type_partition(self.ctx, t, p, self.emb[(t, p)], self.G[(t, p)])
+            if (t, p) in pinned:
+                # page-locked host memory: swapped through HBM slots in an epoch
+                self.emb[(t, p)] = torch.from_numpy(e.astype(np.float32)).pin_memory()
+                self.G[(t, p)] = torch.zeros(e.shape[0], dtype=torch.float32).pin_memory()
+                pbg.pbg_bind_type_partition(self.ctx, t, p, self.emb[(t, p)], self.G[(t, p)], pbg.MEM_PINNED_HOST)
+            else:
+                self.emb[(t, p)] = torch.from_numpy(e.astype(np.float32)).to(dev)
+                self.G[(t, p)] = torch.zeros(e.shape[0], dtype=torch.float32, device=dev)
+                pbg.pbg_bind_type_partition(self.ctx, t, p, self.emb[(t, p)], self.G[(t, p)])
         self.relp = self.relG = None
         if relp is not None:
             self.relp = torch.from_numpy(relp.astype(np.float32)).to(dev)
@@ -374,3 +380,48 @@ def test_typed_run_forward_elementwise(bf16):
     # the destination side's uniform draws cover the item table, not the users'
     negs = O.step_negatives(om, 1, 0, O.chunk_ranges(m, C), 131, U, 5, ((0, 1), (1, 0)))
     assert max(int(u.max()) for u, _ in negs) < 8_000 and max(int(v.max()) for _, v in negs) > 8_000
+
+
+def test_typed_epoch_swaps_pinned_tables():
+    """The typed epoch with the partitioned tables (users and tags, 2 x 2) in
+    page-locked host memory, swapped through HBM slots, and the whole item
+    table in device memory: bitwise the epoch with every table in device
+    memory, and within 1e-4 of the oracle's epoch.  Bucket (1, 0) needs three
+    swapped tables at once (users 1 and 0, tags 1), so two slots are refused."""
+    from paper_1903_12287_amd import pbg
+    d = 12
+    types, P, R, tables, relp, src, rel, dst = _graph(13, d, "diagonal")
+    off, sl, rl, dl = O.bucket_edges_typed(src, rel, dst, types, P)
+    sl, rl, dl = _sorted_buckets(off, sl, rl, dl, P)
+    C, U, S, lr, seed = 16, 8, 2, 0.1, 93
+    pin = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a, dt)).pin_memory()
+    args = (torch.from_numpy(np.asarray(off, np.int64)), pin(sl, np.int32), pin(rl, np.int32), pin(dl, np.int32))
+    swapped = {(0, 0), (0, 1), (2, 0), (2, 1)}
+    states, losses = [], []
+    for pinned, slots in (((), 2), (swapped, 3)):
+        g = TypedGpu(types, P, R, d, "diagonal", "dot", "logistic", tables, relp, [1.0, 0.5, 2.0, 1.0, 0.8],
+                     pinned=pinned)
+        try:
+            if pinned:
+                with pytest.raises(pbg.PbgError) as ei:
+                    pbg.pbg_train_epoch(g.ctx, *args, C, U, S, lr, seed, 2, "by_relation")
+                assert ei.value.status_name == "INVALID_ARG"
+            losses.append(pbg.pbg_train_epoch(g.ctx, *args, C, U, S, lr, seed, slots, "by_relation"))
+            if pinned:
+                st = pbg.pbg_get_stats(g.ctx)
+                assert st["partition_loads"] >= 4
+            states.append(g.state())
+        finally:
+            g.close()
+    assert losses[0] == losses[1]
+    for k in states[0]["emb"]:
+        assert np.array_equal(states[0]["emb"][k], states[1]["emb"][k]), k
+        assert np.array_equal(states[0]["G"][k], states[1]["G"][k]), k
+    assert np.array_equal(states[0]["rel"], states[1]["rel"])
+    om = O.Model.create_typed(types, P, R, d, "diagonal", "dot", "logistic", 0.1,
+                              {k: v.astype(np.float64) for k, v in tables.items()}, relp.astype(np.float64),
+                              weights=[1.0, 0.5, 2.0, 1.0, 0.8])
+    ol = O.train_epoch(om, off, sl, rl, dl, C, U, S, lr, seed, chunking="by_relation")
+    assert abs(losses[1] - ol) <= 1e-4 * abs(ol)
+    for k in om.emb:
+        assert float(np.max(np.abs(states[1]["emb"][k] - om.emb[k]))) <= 1e-4, k
