@@ -19,18 +19,18 @@ from paper_1903_12287_amd import synth
 pytestmark = pytest.mark.gpu
 
 
-def _problem(n, P, R, op, loss, m, seed, d=16):
+def _problem(n, P, R, op, loss, m, seed, d=16, reciprocal=False):
     rng = synth.rng_for(seed)
     src, dst = synth.zipf_edges(n, m, 1.2, 0.9, rng)
     rel = rng.integers(0, R, m).astype(np.int32) if R > 1 else np.zeros(m, np.int32)
     off, sl, rl, dl = O.bucket_edges(src, rel, dst, n, P)
     rows = [O.partition_rows(n, P, p) for p in range(P)]
     parts = synth.partition_embeddings(rows, d, rng, 0.2)
-    relp = synth.perturbed_relation_params(op, R, d, rng, 0.2)
+    relp = synth.perturbed_relation_params(op, 2 * R if reciprocal else R, d, rng, 0.2)
     if op == "linear":
         relp = (synth.identity_relation_params(op, R, d) + 0.05 * rng.standard_normal((R, d * d))).astype(np.float32)
     return dict(n=n, P=P, R=R, d=d, op=op, loss=loss, off=off, src=sl, rel=rl if R > 1 else None, dst=dl,
-                parts=parts, relp=relp)
+                parts=parts, relp=relp, reciprocal=reciprocal)
 
 
 def _pinned(a):
@@ -39,7 +39,8 @@ def _pinned(a):
 
 def _epoch_gpu(pb, C, U, S, lr, seed, max_resident):
     from paper_1903_12287_amd import pbg
-    ctx = pbg.pbg_bucket_init(pb["n"], pb["P"], pb["R"], pb["d"], pb["op"], "dot", pb["loss"], 0.1)
+    ctx = pbg.pbg_bucket_init(pb["n"], pb["P"], pb["R"], pb["d"], pb["op"], "dot", pb["loss"], 0.1,
+                              pbg.F_RECIPROCAL if pb.get("reciprocal") else 0)
     try:
         emb = [_pinned(p.copy()) for p in pb["parts"]]
         G = [_pinned(np.zeros(p.shape[0], np.float32)) for p in pb["parts"]]
@@ -68,7 +69,8 @@ def _resident_gpu(pb, C, U, S, lr, seed):
     """The same buckets, in the same order, trained by pbg_train_bucket with
     every partition in device memory."""
     from paper_1903_12287_amd import pbg
-    ctx = pbg.pbg_bucket_init(pb["n"], pb["P"], pb["R"], pb["d"], pb["op"], "dot", pb["loss"], 0.1)
+    ctx = pbg.pbg_bucket_init(pb["n"], pb["P"], pb["R"], pb["d"], pb["op"], "dot", pb["loss"], 0.1,
+                              pbg.F_RECIPROCAL if pb.get("reciprocal") else 0)
     try:
         emb = [torch.from_numpy(p.copy()).cuda() for p in pb["parts"]]
         G = [torch.zeros(p.shape[0], dtype=torch.float32, device="cuda") for p in pb["parts"]]
@@ -97,9 +99,11 @@ def _resident_gpu(pb, C, U, S, lr, seed):
         pbg.pbg_free(ctx)
 
 
-@pytest.mark.parametrize("op,loss,R,P", [("linear", "logistic", 1, 4), ("diagonal", "logistic", 3, 3)])
-def test_swapped_epoch_equals_resident_and_oracle(op, loss, R, P):
-    pb = _problem(n=400, P=P, R=R, op=op, loss=loss, m=3000, seed=20 + P)
+@pytest.mark.parametrize("op,loss,R,P,reciprocal", [("linear", "logistic", 1, 4, False),
+                                                   ("diagonal", "logistic", 3, 3, False),
+                                                   ("complex_diagonal", "softmax", 3, 3, True)])
+def test_swapped_epoch_equals_resident_and_oracle(op, loss, R, P, reciprocal):
+    pb = _problem(n=400, P=P, R=R, op=op, loss=loss, m=3000, seed=20 + P, reciprocal=reciprocal)
     C, U, S, lr, seed = 24, 16, 3, 0.1, 77
     res_loss, res = _resident_gpu(pb, C, U, S, lr, seed)
     for max_resident in (2, 3, P):
@@ -114,7 +118,8 @@ def test_swapped_epoch_equals_resident_and_oracle(op, loss, R, P):
         if max_resident == P:
             assert stats["partition_loads"] == P
     model = O.Model.create(pb["n"], P, R, pb["d"], op, "dot", loss, 0.1,
-                           [p.astype(np.float64) for p in pb["parts"]], pb["relp"].astype(np.float64))
+                           [p.astype(np.float64) for p in pb["parts"]], pb["relp"].astype(np.float64),
+                           reciprocal=reciprocal)
     o_loss = O.train_epoch(model, pb["off"], pb["src"], pb["rel"], pb["dst"], C, U, S, lr, seed)
     assert abs(res_loss - o_loss) <= 1e-4 * abs(o_loss)
     for p in range(P):

@@ -211,3 +211,21 @@ def test_reciprocal_lifts_the_operator_limits():
         assert pbg.pbg_relation_param_floats(ctx) == 2 * 3 * 8
     finally:
         pbg.pbg_free(ctx)
+
+
+@pytest.mark.parametrize("op,cmp,loss,R", [("translation", "cos", "ranking", 3), ("complex_diagonal", "dot", "softmax", 4),
+                                           ("linear", "cos", "logistic", 2)])
+def test_reciprocal_bf16_step(op, cmp, loss, R):
+    """bf16 inputs to the three contractions with reciprocal predicates: one
+    step checked element by element at the bf16 bar (2e-2 * A, the hinge census
+    for ranking), as test_gpu_parity checks the shared-operator bf16 path."""
+    from paper_1903_12287_amd import pbg
+    pb = make_problem(op, cmp, loss, R=R, m=150, C=40, U=24, S=8, seed=19, d=48, reciprocal=True)
+    gm = GpuModel(pb, flags=pbg.F_BF16_SCORE)
+    try:
+        rep, gl, ol, worst = teacher_forced_step(gm, 0, pb.src.shape[0], 0, 2e-2)
+    finally:
+        gm.close()
+    print(f"\n[{op} {cmp} {loss}] census {rep}, loss gpu {gl:.7g} oracle {ol:.7g}, worst {worst:.3f}", flush=True)
+    assert abs(gl - ol) <= 2e-2 * abs(ol)
+    assert worst <= 1.0
