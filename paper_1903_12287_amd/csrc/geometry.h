@@ -65,18 +65,29 @@ __host__ __device__ inline int64_t pos_index(const StepGeom& g, int c, int side,
   return g.recip ? ((int64_t)(c * 2 + side) * g.C + e) : ((int64_t)c * g.C + e);
 }
 
+// A value that every lane of the wave reads from the same address, kept in a
+// scalar register.  The loads that bring it are vector loads, so without this
+// everything derived from it (tile bounds, row limits, scales) would live in
+// vector registers, and a conditional use would wait for all of the wave's
+// outstanding memory operations, stores included.
+__device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ float wave_uniform(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, v)));
+}
+
 // Chunk c of a step: its edge count and the offset of its first edge in the
 // step's edge arrays.  Consecutive chunks hold C edges each (the step's last
 // one may be short); relation-grouped chunks have their bounds in cstart
 // (offsets in the call's edge arrays, cstart[c + 1] the end of chunk c).
-__host__ __device__ inline int chunk_edges(const StepGeom& g, int c) {
-  if (g.cstart) return g.cstart[c + 1] - g.cstart[c];
+// c must be the same in every lane of the wave.
+__device__ inline int chunk_edges(const StepGeom& g, int c) {
+  if (g.cstart) return wave_uniform(g.cstart[c + 1] - g.cstart[c]);
   const int r = g.m_step - c * g.C;
   return r < g.C ? r : g.C;
 }
 
-__host__ __device__ inline int chunk_first(const StepGeom& g, int c) {
-  return g.cstart ? g.cstart[c] - g.cstart[0] : c * g.C;
+__device__ inline int chunk_first(const StepGeom& g, int c) {
+  return g.cstart ? wave_uniform(g.cstart[c] - g.cstart[0]) : c * g.C;
 }
 
 struct StepBufs {

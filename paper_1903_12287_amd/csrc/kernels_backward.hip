@@ -134,7 +134,7 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
     if (g.cweight) {
       // the chunk's relation weight multiplies the edge's loss and every
       // gradient (the contractions' share is scaled as they store it)
-      const float w = g.cweight[c];
+      const float w = wave_uniform(g.cweight[c]);
       loss *= (double)w;
       dp *= w;
       dp1 *= w;
@@ -385,7 +385,7 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     const bool lin_side = side == 1 && g.op == OP_LINEAR && !g.recip;
     const bool op_side = side == 1 && has_rel && !lin_side && !g.recip;
     // the chunk's relation (one relation, or relation-grouped chunks)
-    const int rc = (op_side && b.rel && Cc > 0) ? b.rel[chunk_first(g, c)] : 0;
+    const int rc = (op_side && b.rel && Cc > 0) ? wave_uniform(b.rel[chunk_first(g, c)]) : 0;
     if (op_side) row_load(th, b.relp + (int64_t)rc * g.dr, d, cplx, lane);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {

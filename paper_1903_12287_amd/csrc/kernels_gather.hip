@@ -173,7 +173,7 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     if (side == 1 && g.op != OP_IDENTITY && !g.recip) {
       // the chunk's relation (one relation, or relation-grouped chunks): its
       // operator is applied to every source candidate
-      const int rc = (b.rel && Cc > 0) ? b.rel[chunk_first(g, c)] : 0;
+      const int rc = (b.rel && Cc > 0) ? wave_uniform(b.rel[chunk_first(g, c)]) : 0;
       Row th;
       row_load(th, b.relp + (int64_t)rc * g.dr, d, cplx, lane);
 #pragma unroll

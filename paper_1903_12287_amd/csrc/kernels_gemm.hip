@@ -127,7 +127,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a, int tiles_n, 
   const int side = z - c * a.nsides;
   int Cc = a.C, Nc = a.C + a.U;
   if (a.cstart) {
-    Cc = a.cstart[c + 1] - a.cstart[c];
+    Cc = wave_uniform(a.cstart[c + 1] - a.cstart[c]);
     Nc = Cc + a.U;
   } else if (a.m_step > 0) {
     Cc = min(a.C, a.m_step - c * a.C);

@@ -33,6 +33,7 @@
 // 8 lanes over 32 banks per cycle, and so do the tile stores (four groups of
 // consecutive rows).
 #include <algorithm>
+#include <type_traits>
 
 #include "kernels.h"
 #include "device_common.h"
@@ -213,7 +214,7 @@ __device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int ti
   int Cc = a.C;
   t.Nc = a.C + a.U;
   if (a.cstart) {
-    Cc = a.cstart[t.c + 1] - a.cstart[t.c];
+    Cc = wave_uniform(a.cstart[t.c + 1] - a.cstart[t.c]);
     t.Nc = Cc + a.U;
   } else if (a.m_step > 0) {
     Cc = min(a.C, a.m_step - t.c * a.C);
@@ -248,7 +249,9 @@ __device__ __forceinline__ void load_rowv(const GemmArgsH& a, const TileGeo& t, 
     const int m = t.m0 + tid;
     const bool mrow = m < t.M;
     const int64_t o = (int64_t)t.c * a.C + m;
-    const int64_t op = a.pos_sides == 2 ? (int64_t)(t.c * 2 + t.side) * a.C + m : o;
+    // row of pos: chunk c (pos_sides = 1), or chunk c and side (pos_sides = 2);
+    // arithmetic rather than a select keeps the tile loop free of spills
+    const int64_t op = (int64_t)(t.c * a.pos_sides + (a.pos_sides - 1) * t.side) * a.C + m;
     const float p = mrow ? a.pos[op] : 0.0f;
     const float bm = (mrow && a.bias && t.side == 1) ? a.bias[o] : 0.0f;
     if (EPI == EPI_LOSS_BITS) {
@@ -469,22 +472,24 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
   const int colb = n0 + WN * wn + l16;
   if (EPI == EPI_STORE) {
     float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
-    const bool scaled = a.cscale != nullptr;
-    const float sc = scaled ? a.cscale[c] : 1.0f;
+    auto store = [&](auto scaled, float sc) {
 #pragma unroll
-    for (int i = 0; i < IM; ++i)
+      for (int i = 0; i < IM; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + WMR * wm + 16 * i + 4 * g + r;
-        if (m < M) {
+        for (int r = 0; r < 4; ++r) {
+          const int m = m0 + WMR * wm + 16 * i + 4 * g + r;
+          if (m < M) {
 #pragma unroll
-          for (int j = 0; j < JN; ++j) {
-            const int n = colb + 16 * j;
-            const float v = acc[i][j][r];
-            if (n < N) Cm[(int64_t)m * a.ldc + n] = scaled ? v * sc : v;
+            for (int j = 0; j < JN; ++j) {
+              const int n = colb + 16 * j;
+              const float v = acc[i][j][r];
+              if (n < N) Cm[(int64_t)m * a.ldc + n] = decltype(scaled)::value ? v * sc : v;
+            }
           }
         }
-      }
+    };
+    if (a.cscale) store(std::true_type{}, wave_uniform(a.cscale[c]));
+    else store(std::false_type{}, 1.0f);
     return;
   }
 
