@@ -90,6 +90,13 @@ __device__ inline int chunk_first(const StepGeom& g, int c) {
   return g.cstart ? wave_uniform(g.cstart[c] - g.cstart[0]) : c * g.C;
 }
 
+// Relation of edge eg of the step.  With one relation every (validated) id is
+// 0, so the id array is not read and the relation row's load does not wait
+// for it.
+__device__ inline int edge_relation(const StepGeom& g, const int32_t* rel, int64_t eg) {
+  return (rel && g.R > 1) ? rel[eg] : 0;
+}
+
 struct StepBufs {
   // edges of the step (device, int32)
   const int32_t* src;

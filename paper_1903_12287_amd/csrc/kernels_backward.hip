@@ -263,7 +263,7 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     const int64_t eg = chunk_first(g, c) + e;   // in the step's edge arrays
     const int s = b.src[eg];
     const int t = b.dst[eg];
-    const int r = b.rel ? b.rel[eg] : 0;
+    const int r = edge_relation(g, b.rel, eg);
     Row th;
     if (has_rel && g.op != OP_LINEAR) row_load(th, b.relp + (int64_t)r * g.dr, d, cplx, lane);
     else row_zero(th);
@@ -385,7 +385,7 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     const bool lin_side = side == 1 && g.op == OP_LINEAR && !g.recip;
     const bool op_side = side == 1 && has_rel && !lin_side && !g.recip;
     // the chunk's relation (one relation, or relation-grouped chunks)
-    const int rc = (op_side && b.rel && Cc > 0) ? wave_uniform(b.rel[chunk_first(g, c)]) : 0;
+    const int rc = (op_side && Cc > 0) ? wave_uniform(edge_relation(g, b.rel, chunk_first(g, c))) : 0;
     if (op_side) row_load(th, b.relp + (int64_t)rc * g.dr, d, cplx, lane);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {

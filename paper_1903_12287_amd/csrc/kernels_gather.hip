@@ -19,7 +19,7 @@
 
 namespace {
 
-template <int RQ>
+template <int RQ, bool RECIP>
 __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) {
   using Row = RowT<RQ>;
   const int lane = threadIdx.x & 63;
@@ -37,7 +37,7 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     const int64_t eg = chunk_first(g, c) + e;   // in the step's edge arrays
     const int s = b.src[eg];
     const int t = b.dst[eg];
-    const int r = b.rel ? b.rel[eg] : 0;
+    const int r = edge_relation(g, b.rel, eg);
     Row x, y, th;
     row_load(x, b.emb_i + (int64_t)s * d, d, cplx, lane);
     row_load(y, b.emb_j + (int64_t)t * d, d, cplx, lane);
@@ -47,7 +47,7 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
     float* krow = b.qk + ((int64_t)(c * 2 + 1) * g.C + e) * dp;
     float* n0row = b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp;
     float* n1row = b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp;
-    if (g.recip) {
+    if (RECIP) {
       if (g.op == OP_LINEAR) {
         // Q = A_r x and K = A_{r+R} y follow per edge from the raw rows (cos:
         // kept in lin_x, the candidate rows here are unit vectors)
@@ -167,13 +167,13 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   }
   float nv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   // linear + cos: the raw source candidates go to lin_x (A x and its norm follow)
-  const bool raw_linear = g.op == OP_LINEAR && g.cmp == CMP_COS && side == 1 && !g.recip;
+  const bool raw_linear = g.op == OP_LINEAR && g.cmp == CMP_COS && side == 1 && !RECIP;
   const bool unit = g.cmp == CMP_COS && !raw_linear;
   if (unit) {
-    if (side == 1 && g.op != OP_IDENTITY && !g.recip) {
+    if (side == 1 && g.op != OP_IDENTITY && !RECIP) {
       // the chunk's relation (one relation, or relation-grouped chunks): its
       // operator is applied to every source candidate
-      const int rc = (b.rel && Cc > 0) ? wave_uniform(b.rel[chunk_first(g, c)]) : 0;
+      const int rc = Cc > 0 ? wave_uniform(edge_relation(g, b.rel, chunk_first(g, c))) : 0;
       Row th;
       row_load(th, b.relp + (int64_t)rc * g.dr, d, cplx, lane);
 #pragma unroll
@@ -340,10 +340,17 @@ void launch_window_keys(const StepGeom& g, const int32_t* src, const int32_t* ds
 
 void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s) {
   dim3 grid((g.C + 2 * ((g.U + 3) / 4) + 3) / 4, g.nchunks);
-  switch (row_width_for(g.d)) {
-    case 2: gather_op_kernel<2><<<grid, 256, 0, s>>>(g, b); break;
-    case 4: gather_op_kernel<4><<<grid, 256, 0, s>>>(g, b); break;
-    default: gather_op_kernel<8><<<grid, 256, 0, s>>>(g, b); break;
+  // reciprocal predicates take their own instantiation, which keeps the
+  // common kernel as small as it is without them
+  const int rq = row_width_for(g.d);
+  if (g.recip) {
+    if (rq == 2) gather_op_kernel<2, true><<<grid, 256, 0, s>>>(g, b);
+    else if (rq == 4) gather_op_kernel<4, true><<<grid, 256, 0, s>>>(g, b);
+    else gather_op_kernel<8, true><<<grid, 256, 0, s>>>(g, b);
+  } else {
+    if (rq == 2) gather_op_kernel<2, false><<<grid, 256, 0, s>>>(g, b);
+    else if (rq == 4) gather_op_kernel<4, false><<<grid, 256, 0, s>>>(g, b);
+    else gather_op_kernel<8, false><<<grid, 256, 0, s>>>(g, b);
   }
 }
 

@@ -33,7 +33,6 @@
 // 8 lanes over 32 banks per cycle, and so do the tile stores (four groups of
 // consecutive rows).
 #include <algorithm>
-#include <type_traits>
 
 #include "kernels.h"
 #include "device_common.h"
@@ -78,10 +77,15 @@ __device__ __forceinline__ uint32_t f2_to_bf16x2(float a, float b) {
 // at most 16 significant bits, m = bf16 of that remainder leaves at most 8,
 // which l holds exactly (for |x| >= 2^-110, where every piece is a normal
 // number).  Two floats at a time: pc[0..2] = packed h, m, l.
+// The empty asm statements hide h and m from the optimiser, which would
+// otherwise form h << 16 from a second conversion of a alone (one extra
+// instruction per level and pair).
 __device__ __forceinline__ void split3_pair(float a, float b, uint32_t* pc) {
-  const uint32_t h = f2_to_bf16x2(a, b);
+  uint32_t h = f2_to_bf16x2(a, b);
+  __asm__("" : "+v"(h));
   const float ra = a - __uint_as_float(h << 16), rb = b - __uint_as_float(h & 0xFFFF0000u);
-  const uint32_t m = f2_to_bf16x2(ra, rb);
+  uint32_t m = f2_to_bf16x2(ra, rb);
+  __asm__("" : "+v"(m));
   pc[0] = h;
   pc[1] = m;
   pc[2] = f2_to_bf16x2(ra - __uint_as_float(m << 16), rb - __uint_as_float(m & 0xFFFF0000u));
@@ -472,24 +476,22 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
   const int colb = n0 + WN * wn + l16;
   if (EPI == EPI_STORE) {
     float* Cm = a.Cm + c * a.c_cs + side * a.c_ss;
-    auto store = [&](auto scaled, float sc) {
+    // the chunk's weight (1 without weights: the product is exact), read once
+    // into a scalar register
+    const float sc = a.cscale ? wave_uniform(a.cscale[c]) : 1.0f;
 #pragma unroll
-      for (int i = 0; i < IM; ++i)
+    for (int i = 0; i < IM; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = m0 + WMR * wm + 16 * i + 4 * g + r;
-          if (m < M) {
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + WMR * wm + 16 * i + 4 * g + r;
+        if (m < M) {
 #pragma unroll
-            for (int j = 0; j < JN; ++j) {
-              const int n = colb + 16 * j;
-              const float v = acc[i][j][r];
-              if (n < N) Cm[(int64_t)m * a.ldc + n] = decltype(scaled)::value ? v * sc : v;
-            }
+          for (int j = 0; j < JN; ++j) {
+            const int n = colb + 16 * j;
+            if (n < N) Cm[(int64_t)m * a.ldc + n] = acc[i][j][r] * sc;
           }
         }
-    };
-    if (a.cscale) store(std::true_type{}, wave_uniform(a.cscale[c]));
-    else store(std::false_type{}, 1.0f);
+      }
     return;
   }
 
@@ -1064,13 +1066,15 @@ __device__ __forceinline__ uint32_t bits_offset(int ld, int m0, int mdim, int kd
 // row 16 i + l16 of the wave's 128, k = 8 g .. + 7; AF = 1: candidate
 // 16 i + l16 of the wave's 128, rows 8 g .. + 7 of the slice, nv of them
 // inside the chunk)
+// AF = 0 looks the fragment's byte up in lut (entry b: the eight bf16 0 / 1
+// of the bits of b, bit 0 first; see fill_bits_lut).
 template <int AF>
-__device__ __forceinline__ v8bf expand_bits_frag(const uint16_t* ab, int wm, int i, int l16, int g, int nv) {
+__device__ __forceinline__ v8bf expand_bits_frag(const uint16_t* ab, const u32x4* lut, int wm, int i, int l16, int g,
+                                                 int nv) {
   u32x4 v;
   if (AF == 0) {
-    const uint32_t bits = (uint32_t)ab[(g >> 1) * 256 + 128 * wm + 16 * i + l16] >> (8 * (g & 1));
-#pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = bit_pair(__builtin_amdgcn_ubfe(bits, 2 * q, 2));
+    const uint32_t word = ab[(g >> 1) * 256 + 128 * wm + 16 * i + l16];
+    v = lut[__builtin_amdgcn_ubfe(word, 8 * (g & 1), 8)];
   } else {
     v = *(const u32x4*)(ab + (8 * wm + i) * 32 + 8 * g);
     const int b = l16;
@@ -1084,9 +1088,15 @@ __device__ __forceinline__ v8bf expand_bits_frag(const uint16_t* ab, int wm, int
   return __builtin_bit_cast(v8bf, v);
 }
 
+// the 256 expansions of a byte of dS bits, one per thread of the workgroup
+__device__ __forceinline__ void fill_bits_lut(u32x4* lut) {
+  const uint32_t b = threadIdx.x;
+  lut[b] = (u32x4){bit_pair(b & 3), bit_pair((b >> 2) & 3), bit_pair((b >> 4) & 3), bit_pair(b >> 6)};
+}
+
 template <int BN, int AF, int PL>
 __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, int tiles_m, int nwg, int id,
-                                               SmemD<BN, PL>& sm) {
+                                               SmemD<BN, PL>& sm, u32x4* lut) {
   constexpr int WN = BN / 2, WMR = BT / 2;
   constexpr int JN = WN / 16, IM = WMR / 16;
   TileGeo t;
@@ -1112,6 +1122,7 @@ __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, 
   // in a ragged last slice of the AF = 1 rows
   const int a_step = AF == 0 ? 4 * a.lda : 2 * BK;
   uint32_t aoff = bits_offset<AF>(a.lda, t.m0, t.M, t.K, 0, w, lane);
+  if (AF == 0) fill_bits_lut(lut);   // visible after the barrier below
   dma_bits(sm.Ab[0], ra, aoff, 0, w);
 #pragma unroll
   for (int p = 0; p < PL; ++p) dma_b_tile<BN>(sm.Bs[0][p], rb[p], a.ldb, t.n0, t.N, 0, t.K, w, lane);
@@ -1124,7 +1135,7 @@ __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, 
     v8bf af[IM];
     const int nv = t.K - (kt * BK + 8 * g);
 #pragma unroll
-    for (int i = 0; i < IM; ++i) af[i] = expand_bits_frag<AF>(sm.Ab[buf], wm, i, l16, g, nv);
+    for (int i = 0; i < IM; ++i) af[i] = expand_bits_frag<AF>(sm.Ab[buf], lut, wm, i, l16, g, nv);
     if (kt + 1 < nk) {
       if (AF == 1 && kt + 2 == nk) aoff = bits_offset<AF>(a.lda, t.m0, t.M, t.K, (kt + 1) * BK, w, lane);
       dma_bits(sm.Ab[buf ^ 1], ra, aoff, (kt + 1) * a_step, w);
@@ -1158,9 +1169,11 @@ template <int BN, int PL>
 __global__ __launch_bounds__(256) void gemm_bits_pair_kernel(GemmArgsH a0, int tn0, int tm0, int nwg0,
                                                              GemmArgsH a1, int tn1, int tm1) {
   __shared__ __align__(16) SmemD<BN, PL> sm;
+  __shared__ __align__(16) u32x4 lut[256];
+  static_assert(sizeof(lut) / sizeof(lut[0]) == 256, "one entry per thread");
   const int id = blockIdx.x;
-  if (id < nwg0) gemm_bits_tile<BN, 0, PL>(a0, tn0, tm0, nwg0, id, sm);
-  else gemm_bits_tile<BN, 1, PL>(a1, tn1, tm1, (int)gridDim.x - nwg0, id - nwg0, sm);
+  if (id < nwg0) gemm_bits_tile<BN, 0, PL>(a0, tn0, tm0, nwg0, id, sm, lut);
+  else gemm_bits_tile<BN, 1, PL>(a1, tn1, tm1, (int)gridDim.x - nwg0, id - nwg0, sm, lut);
 }
 
 // fp32 rows [rows][ld_src] (columns [d, ld_src) zero) of Q and of N -> bf16

@@ -34,7 +34,7 @@ __global__ __launch_bounds__(256) void linear_rows_kernel(StepGeom g, StepBufs b
   if (e >= chunk_edges(g, c)) return;   // no block-level barriers below
   const int d = g.d, dp = g.dp;
   const int64_t ce = (int64_t)c * g.C + e;
-  const int r = b.rel ? b.rel[chunk_first(g, c) + e] : 0;
+  const int r = edge_relation(g, b.rel, chunk_first(g, c) + e);
   const float* A = b.relp + (int64_t)r * d * d;
   RowQ x, y, q, k;
   if (g.recip) {
@@ -86,7 +86,7 @@ __global__ __launch_bounds__(256) void linear_rows_backward_kernel(StepGeom g, S
   const int e = blockIdx.x * kWaves + w;
   if (e >= chunk_edges(g, c)) return;
   const int d = g.d, dp = g.dp;
-  const int r = b.rel ? b.rel[chunk_first(g, c) + e] : 0;
+  const int r = edge_relation(g, b.rel, chunk_first(g, c) + e);
   const float* A = b.relp + (int64_t)r * d * d;
   // the operator backward left dQ (with the positive score's term) in dq
   // side 0 and dK in dq side 1 (reciprocal predicates: the gradients of
