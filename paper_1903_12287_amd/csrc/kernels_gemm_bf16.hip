@@ -1068,7 +1068,7 @@ __device__ __forceinline__ uint32_t bits_offset(int ld, int m0, int mdim, int kd
 // inside the chunk)
 // AF = 0 looks the fragment's byte up in lut (entry b: the eight bf16 0 / 1
 // of the bits of b, bit 0 first; see fill_bits_lut).
-template <int AF>
+template <int AF, bool TAIL>
 __device__ __forceinline__ v8bf expand_bits_frag(const uint16_t* ab, const u32x4* lut, int wm, int i, int l16, int g,
                                                  int nv) {
   u32x4 v;
@@ -1080,7 +1080,7 @@ __device__ __forceinline__ v8bf expand_bits_frag(const uint16_t* ab, const u32x4
     const int b = l16;
 #pragma unroll
     for (int q = 0; q < 4; ++q) v[q] = ((v[q] >> b) & 0x00010001u) * 0x3F80u;
-    if (nv < 8) {
+    if (TAIL && nv < 8) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) v[q] &= (2 * q + 1 < nv) ? 0xFFFFFFFFu : (2 * q < nv ? 0xFFFFu : 0u);
     }
@@ -1134,8 +1134,15 @@ __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, 
     const int buf = kt & 1;
     v8bf af[IM];
     const int nv = t.K - (kt * BK + 8 * g);
+    // rows of dS past the chunk's edges (AF = 1) are masked in a slice that
+    // reaches them only: the check is uniform, the masks are per lane
+    if (AF == 1 && (kt + 1) * BK > t.K) {
 #pragma unroll
-    for (int i = 0; i < IM; ++i) af[i] = expand_bits_frag<AF>(sm.Ab[buf], lut, wm, i, l16, g, nv);
+      for (int i = 0; i < IM; ++i) af[i] = expand_bits_frag<AF, true>(sm.Ab[buf], lut, wm, i, l16, g, nv);
+    } else {
+#pragma unroll
+      for (int i = 0; i < IM; ++i) af[i] = expand_bits_frag<AF, false>(sm.Ab[buf], lut, wm, i, l16, g, nv);
+    }
     if (kt + 1 < nk) {
       if (AF == 1 && kt + 2 == nk) aoff = bits_offset<AF>(a.lda, t.m0, t.M, t.K, (kt + 1) * BK, w, lane);
       dma_bits(sm.Ab[buf ^ 1], ra, aoff, (kt + 1) * a_step, w);
