@@ -55,11 +55,12 @@ def parse():
     ap.add_argument("--no-big-bucket", action="store_true",
                     help="skip the second workload of the default line (one bucket of the partitioned graph)")
     ap.add_argument("--row", choices=["bucketing", "knowledge_graph", "knowledge_graph_reciprocal", "big_bucket",
-                                      "epoch", "tiny", "negatives"],
+                                      "epoch", "tiny", "negatives", "library_gemm"],
                     help="measure another row of the hot path instead of the default training step: "
                          "edge bucketing of the follower graph, the knowledge-graph pass and filtered "
                          "rank evaluation, one bucket of the large partitioned graph, the follower-graph "
-                         "epoch with partition swapping, or the tiny social graph")
+                         "epoch with partition swapping, or the tiny social graph; library_gemm times the "
+                         "vendor GEMMs at the score shape and large square shapes for context")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy five times (reference kernel of known "
                          "size for scaling hardware byte counters) and exit")
@@ -744,9 +745,56 @@ def row_negatives():
             "points": points}
 
 
+def row_library_gemm():
+    """Context for the matrix-peak fractions: what the vendor GEMM libraries
+    (torch.bmm / torch.matmul on ROCm) reach on this GPU, at the score
+    contraction's shape (80 chunk-sides of 1000 x 128 times 128 x 2000, the
+    library writing S, no loss) and as large square products.  Not part of
+    the hot path."""
+    import torch
+    torch.backends.cuda.matmul.allow_tf32 = False
+    dev = torch.device("cuda")
+
+    def timed(f, it):
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(it):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / it
+
+    out = []
+    B, M, K, Nn = 2 * S, C, DIM, C + U
+    for name, dt in (("f32", torch.float32), ("bf16", torch.bfloat16)):
+        q = torch.randn(B, M, K, device=dev, dtype=dt)
+        nt = torch.randn(B, Nn, K, device=dev, dtype=dt).transpose(1, 2).contiguous()
+        ms = timed(lambda: torch.bmm(q, nt), 20)
+        fl = 2.0 * B * M * Nn * K
+        peak = PEAK_FP32_MFMA if dt == torch.float32 else PEAK_BF16_MFMA
+        out.append({"op": "bmm", "dtype": name, "shape": [B, M, K, Nn], "us": ms * 1e3,
+                    "tflops": fl / ms / 1e9, "peak": peak, "frac": fl / ms / 1e9 / peak})
+        del q, nt
+    for sz in (4096, 8192):
+        for name, dt in (("bf16", torch.bfloat16), ("f32", torch.float32)):
+            a = torch.randn(sz, sz, device=dev, dtype=dt)
+            b = torch.randn(sz, sz, device=dev, dtype=dt)
+            ms = timed(lambda: a @ b, 10)
+            fl = 2.0 * sz ** 3
+            peak = PEAK_FP32_MFMA if dt == torch.float32 else PEAK_BF16_MFMA
+            out.append({"op": "matmul", "dtype": name, "shape": [sz, sz, sz], "us": ms * 1e3,
+                        "tflops": fl / ms / 1e9, "peak": peak, "frac": fl / ms / 1e9 / peak})
+            del a, b
+    return {"row": "library_gemm", "unit": "TFLOP/s", "results": out}
+
+
 ROWS = {"bucketing": row_bucketing, "knowledge_graph": row_knowledge_graph,
         "knowledge_graph_reciprocal": lambda: row_knowledge_graph(reciprocal=True), "big_bucket": row_big_bucket,
-        "epoch": row_epoch, "tiny": row_tiny, "negatives": row_negatives}
+        "epoch": row_epoch, "tiny": row_tiny, "negatives": row_negatives, "library_gemm": row_library_gemm}
 
 
 if __name__ == "__main__":

@@ -160,7 +160,11 @@ typedef struct {
  * UNSUPPORTED: the source corruptions of an edge need its own relation's
  * operator applied to every candidate before the normalisation), and
  * pbg_rank_eval / pbg_rank_sampled return UNSUPPORTED for it.  With
- * PBG_F_RECIPROCAL none of these limits applies. */
+ * PBG_F_RECIPROCAL none of these limits applies.  out NULL: INVALID_ARG and
+ * nothing else.  On any other failure *out may still hold a context that only
+ * carries the message: read it with pbg_last_error and release it with
+ * pbg_free; every other call on it returns PBG_ERR_STATE (the row and size
+ * queries return -1). */
 pbg_status pbg_bucket_init(pbg_ctx** out, int64_t num_entities, int32_t num_partitions,
                            int32_t num_relations, int32_t dim, int32_t op, int32_t cmp,
                            int32_t loss, float margin, uint32_t flags);

@@ -71,6 +71,42 @@ def build(verbose: bool = True) -> str:
     return LIB
 
 
+def build_asan(verbose: bool = False) -> str:
+    """A copy of the library whose host code (the *.cpp runtime) is built with
+    AddressSanitizer, for host-side tests of the ABI's error paths; the
+    kernels are the regular objects (device code is never instrumented).  The
+    AddressSanitizer runtime comes from the executable that loads it.
+    Returns the path of _build/asan/libpbg_asan.so."""
+    if not all(os.path.exists(os.path.join(OBJ_DIR, os.path.basename(f) + ".o"))
+               for f in sources() if f.endswith(".hip")):
+        build(verbose=False)
+    out_dir = os.path.join(OBJ_DIR, "asan")
+    os.makedirs(out_dir, exist_ok=True)
+    host = [f for f in sources() if f.endswith(".cpp")]
+    # host code only: each sanitizer flag applies to the host pass
+    asan = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+
+    def compile_host(src):
+        obj = os.path.join(out_dir, os.path.basename(src) + ".o")
+        r = subprocess.run([HIPCC, *COMMON, *asan, "-x", "hip", "-c", src, "-o", obj], capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr[-6000:]}")
+        return obj
+
+    jobs = min(len(host), int(os.environ.get("MAX_JOBS", "8")))
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(compile_host, host))
+    kern = [os.path.join(OBJ_DIR, os.path.basename(f) + ".o") for f in sources() if f.endswith(".hip")]
+    lib = os.path.join(out_dir, "libpbg_asan.so")
+    r = subprocess.run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", lib, *objs, *kern],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stderr[-6000:]}")
+    if verbose:
+        print(f"built {lib}")
+    return lib
+
+
 if __name__ == "__main__":
     build()
     sys.exit(0)

@@ -413,6 +413,7 @@ pbg_status pbg_set_streams(pbg_ctx* ctx, void* compute_stream, void* copy_stream
 
 pbg_status pbg_get_stats(const pbg_ctx* ctx, pbg_stats* out_host) {
   if (!ctx || !out_host) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return PBG_ERR_STATE;
   *out_host = ctx->stats;
   return PBG_OK;
 }
@@ -420,6 +421,7 @@ pbg_status pbg_get_stats(const pbg_ctx* ctx, pbg_stats* out_host) {
 pbg_status pbg_get_step_losses(const pbg_ctx* ctx, double* out_host, int64_t capacity,
                                int64_t* n_steps_host) {
   if (!ctx || (capacity > 0 && !out_host)) return PBG_ERR_INVALID_ARG;
+  if (ctx->invalid) return PBG_ERR_STATE;
   const int64_t n = (int64_t)ctx->step_losses.size();
   for (int64_t k = 0; k < std::min(capacity, n); ++k) out_host[k] = ctx->step_losses[k];
   if (n_steps_host) *n_steps_host = n;
