@@ -257,12 +257,15 @@ def main():
     print(f"# workload drawn on device in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr)
     total_steps = -(-N_EDGES // (S * C))
 
-    dt, st = run_leg(pbg, torch, 0, emb0, relp0, src, dst, args, total_steps)
-    # the phase breakdown from a separate, shorter run with events around every
+    # the phase breakdown comes from a separate run with events around every
     # kernel group (they add to each step, so the timed run records only the
-    # two around the score contraction)
-    phase_steps = min(args.steps, 100)
+    # two around the score contraction).  It runs first: after the host-side
+    # preparation the GPU takes some 40 ms of this work to reach its loaded
+    # clock (the score contraction runs ~15 % slower at first), more than a
+    # few warm-up steps cover, and the phase run spans that time.
+    phase_steps = 100
     _, stp = run_leg(pbg, torch, 0, emb0, relp0, src, dst, args, total_steps, pbg.F_PHASE_TIMING, phase_steps)
+    dt, st = run_leg(pbg, torch, 0, emb0, relp0, src, dst, args, total_steps)
     print(f"# fp32: {st['edges'] / dt:.4g} edges/s", file=sys.stderr)
     out = {
         "metric": "trained edges/sec on 1 MI355X",
@@ -294,9 +297,9 @@ def main():
         "adagrad_hbm": hbm_rate(stp, "update_bytes", "update_ms", measured_traffic("adagrad")),
     }
     if not args.no_bf16:
-        dt16, st16 = run_leg(pbg, torch, pbg.F_BF16_SCORE, emb0, relp0, src, dst, args, total_steps)
         _, st16p = run_leg(pbg, torch, pbg.F_BF16_SCORE, emb0, relp0, src, dst, args, total_steps,
                            pbg.F_PHASE_TIMING, phase_steps)
+        dt16, st16 = run_leg(pbg, torch, pbg.F_BF16_SCORE, emb0, relp0, src, dst, args, total_steps)
         print(f"# bf16: {st16['edges'] / dt16:.4g} edges/s", file=sys.stderr)
         out["bf16"] = {"value": st16["edges"] / dt16, "unit": "edges/s",
                        "ms_per_step": dt16 * 1e3 / args.steps, "dtype": "bf16 inputs, f32 accumulate",
@@ -545,8 +548,9 @@ def big_bucket_legs(with_cpu=True, phase_steps=20):
         return dt, st
 
     for flags, key in ((0, None), (pbg.F_BF16_SCORE, "bf16")):
-        dt, st = leg(flags, pbg.F_SCORE_TIMING, E)
+        # the phase run first, as in the default line (it brings the GPU to its loaded clock)
         _, stp = leg(flags, pbg.F_PHASE_TIMING, phase_steps * Sb * Cb)
+        dt, st = leg(flags, pbg.F_SCORE_TIMING, E)
         res = {"value": E / dt, "ms_per_pass": dt * 1e3, "ms_per_step": dt * 1e3 / max(1, st["steps"]),
                "roofline": roofline(st, "score contraction with the ranking epilogue",
                                     pieces=None if flags else SPLIT_PIECES),
