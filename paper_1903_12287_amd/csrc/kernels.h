@@ -71,6 +71,9 @@ struct GemmArgsH {
   int loss;
   float margin;
   const float* cscale;   // EPI_STORE: output of chunk c times cscale[c] (NULL: as is)
+  int share_cc;          // launch_score_split with Q of each side the first C candidate rows of the
+                         // other: the in-chunk block of side 1 is the transpose of side 0's, and side 0's
+                         // full tiles inside it produce side 1's too
 };
 
 // bf16-input score contraction with a loss epilogue (EPI_LOSS, EPI_LOSS_BITS or

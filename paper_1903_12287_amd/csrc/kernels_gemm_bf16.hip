@@ -229,6 +229,9 @@ __device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int ti
   t.K = pick_dim(a.kdim, a.Kfix, Cc, t.Nc);
   t.m0 = tm * TM;
   t.n0 = t.tn * BN;
+  // shared in-chunk blocks: side 1's full tiles of [0, Cc) x [0, Cc) come
+  // from side 0's tiles (tn, tm), transposed
+  if (a.share_cc && t.side == 1 && tm < Cc / TM && t.tn < Cc / BN) return false;
   if (t.m0 >= t.M) return false;
   if (t.n0 >= t.N) {
     const int tid = threadIdx.x;
@@ -696,15 +699,51 @@ struct TileS {
 };
 
 // one LDS buffer of three A and three B planes (single-buffered, so that
-// three workgroups fit a CU), and the row partials
+// three workgroups fit a CU), and the row partials; rowv1: the per-row values
+// of side 1's rows of a shared tile
 template <int TM>
 struct SmemST {
   uint16_t As[3][TM * BK];
   uint16_t Bs[3][128 * BK];
   float red[2][TM][2];
   float rowv[2][TM];
+  float rowv1[2][TM];
 };
 using SmemS = SmemST<BM>;
+
+// The 128 x 128 tile held as four 64 x 64 wave blocks in the matrix-instruction
+// layout (acc[i][j][r] is row 16 i + 4 g + r, column 16 j + l16 of the block of
+// wave (wm, wn)) becomes its transpose: wave (wm, wn) ends with block (wn, wm)
+// transposed.  The two off-diagonal waves swap through LDS first, then the two
+// diagonal ones transpose in place; a block passes through a [64][68] float32
+// slot (rows padded so that the 4-byte writes and 16-byte reads meet distinct
+// banks).  L: 2 * 64 * 68 floats.  Every wave of the workgroup calls it.
+__device__ __forceinline__ void transpose_tile(v4f (&acc)[4][4], float* L, int wm, int wn, int l16, int g) {
+  constexpr int LD = 68;
+  const bool off = wm != wn;
+#pragma unroll
+  for (int phase = 0; phase < 2; ++phase) {
+    const bool mine = (phase == 0) == off;
+    if (mine) {
+      float* s = L + wm * 64 * LD;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) s[(16 * i + 4 * g + r) * LD + 16 * j + l16] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (mine) {
+      const float* s = L + wn * 64 * LD;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = *(const v4f*)(s + (16 * j + l16) * LD + 16 * i + 4 * g);
+    }
+    __syncthreads();
+  }
+}
 
 // Score tile body: four waves of 64 x 64.  One A plane and one B plane in
 // registers at a time (B planes are read again for each A plane).
@@ -712,6 +751,7 @@ template <int EPI, int NPROD>
 __device__ __forceinline__ void score_split_body(const GemmArgsH& a, int tiles_n, int tiles_m) {
   constexpr int BN = 128, WN = 64, JN = 4, WMR = BM / 2, IM = BM / 32;
   __shared__ __align__(16) SmemS sm;
+  static_assert(sizeof(sm.As) + sizeof(sm.Bs) >= 2 * 64 * 68 * sizeof(float), "transpose slots");
   TileGeo t;
   if (!tile_geo<BN, EPI>(a, tiles_n, tiles_m, gridDim.x, blockIdx.x, t)) return;
   if (EPI != EPI_STORE) load_rowv<EPI>(a, t, sm.rowv);
@@ -776,7 +816,23 @@ __device__ __forceinline__ void score_split_body(const GemmArgsH& a, int tiles_n
       __syncthreads();
     }
   }
-  tile_epilogue<BN, EPI>(a, t, acc, sm.red, sm.rowv);
+  // a full side-0 tile inside the in-chunk block also gives side 1's tile
+  // (tm, tn) -> (tn, tm), its transpose (M = the chunk's edges here): a second
+  // pass of the same epilogue on the transposed accumulators
+  const bool shared = a.share_cc && t.side == 0 && t.m0 / BM < t.M / BM && t.tn < t.M / BN;
+  for (int pass = 0; pass < (shared ? 2 : 1); ++pass) {
+    if (pass == 1) {
+      t.side = 1;
+      const int m0 = t.m0;
+      t.m0 = t.n0;
+      t.n0 = m0;
+      t.tn = m0 / BN;
+      if (EPI != EPI_STORE) load_rowv<EPI>(a, t, sm.rowv1);   // visible after the transpose's barriers
+      // every wave is past the first pass's barrier, so past its last reads of the planes
+      transpose_tile(acc, reinterpret_cast<float*>(&sm.As[0][0]), wm, wn, l16, g);
+    }
+    tile_epilogue<BN, EPI>(a, t, acc, sm.red, pass ? sm.rowv1 : sm.rowv);
+  }
 }
 
 // The ranking-bits epilogue keeps register use low enough for three waves per

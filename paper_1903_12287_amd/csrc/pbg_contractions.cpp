@@ -86,10 +86,12 @@ static GemmArgsH score_args_f32(const StepGeom& g, const StepBufs& b, int* epi_o
   fa.Bf = b.nn;
   fa.Cm = b.ds;
   if (QK_IN_NN(g)) {
-    // side s reads the candidate rows of side 1 - s
+    // side s reads the candidate rows of side 1 - s, so the scores of side 1
+    // against the chunk's own candidates are the transposed ones of side 0
     fa.Af = b.nn + (int64_t)N * dp;
     fa.a_cs = 2ll * N * dp;
     fa.a_ss = -(int64_t)N * dp;
+    fa.share_cc = 1;
   } else {
     fa.Af = b.qk;
     fa.a_cs = 2ll * C * dp;
