@@ -197,14 +197,16 @@ def hbm_rate(st, bytes_key, ms_key, traffic):
     return out
 
 
-def roofline(st, kernel, traffic=None, pieces=None):
+def roofline(st, kernel, traffic=None, pieces=None, issued=1.0):
     """Dominant kernel: the score contraction with its fused loss epilogue.
     Algorithmic flops per launch: 2 sides x 2 C N d per chunk (a third of the
     12 C N d of the three contractions), one launch per step.  The kernel
     issues v_mfma_f32_16x16x32_bf16 in both precisions; a float32 contraction
     issues `pieces` exact bf16 piece products per product, so its ceiling is
     the bf16 matrix peak over `pieces` (frac), and its rate against the fp32
-    matrix peak is given beside it (fp32_peak_frac)."""
+    matrix peak is given beside it (fp32_peak_frac).  `issued`: the share of
+    the algorithmic products the kernel computes (with cos, side 1's in-chunk
+    block comes transposed from side 0's tiles)."""
     launches = max(1, st["steps"])
     timed = max(1, st.get("score_timed_steps") or launches)   # launches the events bracketed
     flops = st["score_flops"] / 3.0 / launches                   # per launch
@@ -219,7 +221,9 @@ def roofline(st, kernel, traffic=None, pieces=None):
                             "per float32 product (the instruction the kernel issues)")
         out["fp32_peak"] = PEAK_FP32_MFMA
         out["fp32_peak_frac"] = achieved / PEAK_FP32_MFMA
-        out["executed_tflops"] = pieces * achieved
+        out["executed_tflops"] = pieces * issued * achieved
+    if issued != 1.0:
+        out["issued_share"] = issued
     return out
 
 
@@ -285,7 +289,8 @@ def main():
                    "chunk": C, "uniform_negatives": U, "chunks_per_step": S,
                    "edges_per_step": S * C, "partitions": 1},
         "roofline": roofline(st, "score_split_kernel3<EPI_LOSS_BITS, 6> (float32 score + ranking epilogue)",
-                             measured_traffic("score"), pieces=SPLIT_PIECES),
+                             measured_traffic("score"), pieces=SPLIT_PIECES,
+                             issued=1.0 - (128 * (C // 128)) ** 2 / (2.0 * C * (C + U))),
         # from the phase-timing run of phase_steps steps
         "phases_ms_per_step": phases(stp),
         "phase_steps": phase_steps,
