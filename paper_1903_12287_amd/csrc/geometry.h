@@ -57,6 +57,8 @@ struct StepGeom {
   int R;            // relations (the offset of the source side's rows)
   int relN;         // rows of relc per chunk (N; 2C with reciprocal predicates)
   const float* cweight;   // relation weight of each chunk of the step (device), NULL: all 1
+  int dq_has_dn;    // with QK_IN_NN: dq of side s, row e < Cc, already holds dn of side 1 - s, row e (the
+                    // ranking backward merged them), and those dn rows are not written
 };
 
 // index of edge e's positive score of side s in pos / dpos: one shared

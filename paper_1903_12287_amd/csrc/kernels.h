@@ -74,6 +74,10 @@ struct GemmArgsH {
   int share_cc;          // launch_score_split with Q of each side the first C candidate rows of the
                          // other: the in-chunk block of side 1 is the transpose of side 0's, and side 0's
                          // full tiles inside it produce side 1's too
+  int merge_cc;          // ranking backward with the same Q / candidate rows (launch_gemm_bf16_pair, three
+                         // planes): a0's dQ rows e < Cc of side s also take dN of candidate e of side 1 - s
+                         // (the same vector; a0.A's other side read by columns over k < Cc), and a1's dN rows
+                         // start at Cc rounded down to 16 (the rows below are left unwritten)
 };
 
 // bf16-input score contraction with a loss epilogue (EPI_LOSS, EPI_LOSS_BITS or

@@ -285,8 +285,14 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     row_load(Kv, kr, d, cplx, lane);
     row_load(gq0, dq0, d, cplx, lane);
     row_load(gq1, dq1, d, cplx, lane);
-    row_load(gn0, dn0, d, cplx, lane);
-    row_load(gn1, dn1, d, cplx, lane);
+    if (g.dq_has_dn) {
+      // the ranking backward added dn of side 1 - s into dq of side s
+      row_zero(gn0);
+      row_zero(gn1);
+    } else {
+      row_load(gn0, dn0, d, cplx, lane);
+      row_load(gn1, dn1, d, cplx, lane);
+    }
     Row gs, gd, grel;
     row_zero(grel);
     if (!cos) {

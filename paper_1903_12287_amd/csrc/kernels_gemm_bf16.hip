@@ -232,6 +232,9 @@ __device__ __forceinline__ bool tile_geo(const GemmArgsH& a, int tiles_n, int ti
   // shared in-chunk blocks: side 1's full tiles of [0, Cc) x [0, Cc) come
   // from side 0's tiles (tn, tm), transposed
   if (a.share_cc && t.side == 1 && tm < Cc / TM && t.tn < Cc / BN) return false;
+  // merged ranking backward: the dN rows below Cc (rounded down to a 16-row
+  // bit word) are taken by the other side's dQ
+  if (a.merge_cc && a.mdim == DIM_NC) t.m0 += Cc & ~15;
   if (t.m0 >= t.M) return false;
   if (t.n0 >= t.N) {
     const int tid = threadIdx.x;
@@ -1068,6 +1071,7 @@ template <int BN, int PL>
 struct SmemD {
   uint16_t Bs[2][PL][BN * BK];
   uint16_t Ab[2][2 * BT];   // the slice's bit-matrix words (see dma_bits)
+  uint16_t Ab1[2][2 * BT];  // merged dQ rows: the other side's words read by columns
   float red[2][BT][2];
   float rowv[2][BT];
 };
@@ -1150,9 +1154,44 @@ __device__ __forceinline__ void fill_bits_lut(u32x4* lut) {
   lut[b] = (u32x4){bit_pair(b & 3), bit_pair((b >> 2) & 3), bit_pair((b >> 4) & 3), bit_pair(b >> 6)};
 }
 
-template <int BN, int AF, int PL>
+// Merged dQ rows: each element of A is a count c in {0, 1, 2} (the bit of this
+// side's dS row plus the bit of the other side's dS column), whose bf16 value
+// 0, 1.0 (0x3F80) or 2.0 (0x4000) comes out of one byte permute: the selector
+// of an element pair is 0x03000300 + c0 * 0x0101 + c1 * 0x01010000 (low byte
+// c, high byte 3 + c) over the table bytes {00 80 00 | 00 3F 40}.
+constexpr uint32_t kCountLo = 0x00008000u, kCountHi = 0x0000403Fu;
+__device__ __forceinline__ void fill_count_lut(u32x4* lut) {
+  const uint32_t b = threadIdx.x;
+  u32x4 v;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) v[q] = 0x03000300u + (((((b >> (2 * q)) & 3u) * 0x8001u) & 0x10001u) * 0x0101u);
+  lut[b] = v;
+}
+
+// fragment i of a merged slice: this side's row bits (by byte, from lutc) plus
+// the other side's column bits (AF = 1 layout in ab1, TAIL: only nv of the
+// eight k inside the chunk)
+template <bool TAIL>
+__device__ __forceinline__ v8bf expand_count_frag(const uint16_t* ab, const uint16_t* ab1, const u32x4* lutc, int wm,
+                                                  int i, int l16, int g, int nv) {
+  const uint32_t word = ab[(g >> 1) * 256 + 128 * wm + 16 * i + l16];
+  u32x4 sel = lutc[__builtin_amdgcn_ubfe(word, 8 * (g & 1), 8)];
+  const u32x4 v = *(const u32x4*)(ab1 + (8 * wm + i) * 32 + 8 * g);
+  u32x4 out;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint32_t e = ((v[q] >> l16) & 0x00010001u) * 0x0101u;
+    if (TAIL) e &= (2 * q + 1 < nv) ? 0xFFFFFFFFu : (2 * q < nv ? 0xFFFFu : 0u);
+    out[q] = __builtin_amdgcn_perm(kCountHi, kCountLo, sel[q] + e);
+  }
+  return __builtin_bit_cast(v8bf, out);
+}
+
+// MERGE (AF = 0, a.merge_cc): the merged dQ rows described at GemmArgsH; the
+// slices k < Cc take the other side's column bits too (counts, lutc).
+template <int BN, int AF, int PL, bool MERGE>
 __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, int tiles_m, int nwg, int id,
-                                               SmemD<BN, PL>& sm, u32x4* lut) {
+                                               SmemD<BN, PL>& sm, u32x4* lut, u32x4* lutc) {
   constexpr int WN = BN / 2, WMR = BT / 2;
   constexpr int JN = WN / 16, IM = WMR / 16;
   TileGeo t;
@@ -1179,7 +1218,15 @@ __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, 
   const int a_step = AF == 0 ? 4 * a.lda : 2 * BK;
   uint32_t aoff = bits_offset<AF>(a.lda, t.m0, t.M, t.K, 0, w, lane);
   if (AF == 0) fill_bits_lut(lut);   // visible after the barrier below
+  if (MERGE) fill_count_lut(lutc);
   dma_bits(sm.Ab[0], ra, aoff, 0, w);
+  // merged rows: the other side's matrix by columns, rows k < kc = Cc (the dQ
+  // tile's M)
+  const rsrc_t ra1 = MERGE ? make_rsrc(a.A + t.c * a.a_cs + (1 - t.side) * a.a_ss) : ra;
+  const int kc = MERGE ? t.M : 0;
+  const int nk1 = (kc + BK - 1) / BK;
+  uint32_t aoff1 = MERGE ? bits_offset<1>(a.lda, t.m0, t.M, kc, 0, w, lane) : 0;
+  if (MERGE && nk1 > 0) dma_bits(sm.Ab1[0], ra1, aoff1, 0, w);
 #pragma unroll
   for (int p = 0; p < PL; ++p) dma_b_tile<BN>(sm.Bs[0][p], rb[p], a.ldb, t.n0, t.N, 0, t.K, w, lane);
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's loads have landed
@@ -1192,7 +1239,16 @@ __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, 
     const int nv = t.K - (kt * BK + 8 * g);
     // rows of dS past the chunk's edges (AF = 1) are masked in a slice that
     // reaches them only: the check is uniform, the masks are per lane
-    if (AF == 1 && (kt + 1) * BK > t.K) {
+    if (MERGE && kt < nk1) {
+      const int nv1 = kc - (kt * BK + 8 * g);
+      if ((kt + 1) * BK > kc) {
+#pragma unroll
+        for (int i = 0; i < IM; ++i) af[i] = expand_count_frag<true>(sm.Ab[buf], sm.Ab1[buf], lutc, wm, i, l16, g, nv1);
+      } else {
+#pragma unroll
+        for (int i = 0; i < IM; ++i) af[i] = expand_count_frag<false>(sm.Ab[buf], sm.Ab1[buf], lutc, wm, i, l16, g, nv1);
+      }
+    } else if (AF == 1 && (kt + 1) * BK > t.K) {
 #pragma unroll
       for (int i = 0; i < IM; ++i) af[i] = expand_bits_frag<AF, true>(sm.Ab[buf], lut, wm, i, l16, g, nv);
     } else {
@@ -1202,6 +1258,10 @@ __device__ __forceinline__ void gemm_bits_tile(const GemmArgsH& a, int tiles_n, 
     if (kt + 1 < nk) {
       if (AF == 1 && kt + 2 == nk) aoff = bits_offset<AF>(a.lda, t.m0, t.M, t.K, (kt + 1) * BK, w, lane);
       dma_bits(sm.Ab[buf ^ 1], ra, aoff, (kt + 1) * a_step, w);
+      if (MERGE && kt + 1 < nk1) {
+        if (kt + 2 == nk1) aoff1 = bits_offset<1>(a.lda, t.m0, t.M, kc, (kt + 1) * BK, w, lane);
+        dma_bits(sm.Ab1[buf ^ 1], ra1, aoff1, (kt + 1) * 2 * BK, w);
+      }
 #pragma unroll
       for (int p = 0; p < PL; ++p)
         dma_b_tile<BN>(sm.Bs[buf ^ 1][p], rb[p], a.ldb, t.n0, t.N, (kt + 1) * BK, t.K, w, lane);
@@ -1233,10 +1293,15 @@ __global__ __launch_bounds__(256) void gemm_bits_pair_kernel(GemmArgsH a0, int t
                                                              GemmArgsH a1, int tn1, int tm1) {
   __shared__ __align__(16) SmemD<BN, PL> sm;
   __shared__ __align__(16) u32x4 lut[256];
+  __shared__ __align__(16) u32x4 lutc[256];
   static_assert(sizeof(lut) / sizeof(lut[0]) == 256, "one entry per thread");
   const int id = blockIdx.x;
-  if (id < nwg0) gemm_bits_tile<BN, 0, PL>(a0, tn0, tm0, nwg0, id, sm, lut);
-  else gemm_bits_tile<BN, 1, PL>(a1, tn1, tm1, (int)gridDim.x - nwg0, id - nwg0, sm, lut);
+  if (id < nwg0) {
+    if (a0.merge_cc) gemm_bits_tile<BN, 0, PL, true>(a0, tn0, tm0, nwg0, id, sm, lut, lutc);
+    else gemm_bits_tile<BN, 0, PL, false>(a0, tn0, tm0, nwg0, id, sm, lut, lutc);
+  } else {
+    gemm_bits_tile<BN, 1, PL, false>(a1, tn1, tm1, (int)gridDim.x - nwg0, id - nwg0, sm, lut, lutc);
+  }
 }
 
 // fp32 rows [rows][ld_src] (columns [d, ld_src) zero) of Q and of N -> bf16
@@ -1418,7 +1483,9 @@ void launch_bits_pair_t(const GemmArgsH& a0, const GemmArgsH& a1, int batches, h
   const int tn0 = (dim_max(a0.ndim, a0.Nfix, a0.C, a0.U) + BN - 1) / BN;
   const int tm0 = (dim_max(a0.mdim, a0.Mfix, a0.C, a0.U) + BT - 1) / BT;
   const int tn1 = (dim_max(a1.ndim, a1.Nfix, a1.C, a1.U) + BN - 1) / BN;
-  const int tm1 = (dim_max(a1.mdim, a1.Mfix, a1.C, a1.U) + BT - 1) / BT;
+  // merged: dN rows from Cc rounded down to 16, at most U + 15 of them
+  const int rows1 = a1.merge_cc ? a1.U + 15 : dim_max(a1.mdim, a1.Mfix, a1.C, a1.U);
+  const int tm1 = (rows1 + BT - 1) / BT;
   const int64_t nwg0 = (int64_t)tn0 * tm0 * batches, nwg1 = (int64_t)tn1 * tm1 * batches;
   gemm_bits_pair_kernel<BN, PL><<<(unsigned)(nwg0 + nwg1), 256, 0, s>>>(a0, tn0, tm0, (int)nwg0, a1, tn1, tm1);
 }

@@ -16,7 +16,7 @@ static int rup(int v, int m) { return (v + m - 1) / m * m; }
 // elements apart.
 static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t* dsh, const uint16_t* nT,
                            int64_t n_ps, const uint16_t* qT, int64_t q_ps, int64_t q_cs, int64_t q_ss, int q_ld,
-                           int planes, hipStream_t cs) {
+                           int planes, hipStream_t cs, bool merge = false) {
   const int C = g.C, N = g.N, dp = g.dp, Np = g.Np, nch = g.nchunks;
   const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const bool bits = g.loss == LOSS_RANKING;
@@ -71,6 +71,8 @@ static void run_backward_h(const StepGeom& g, const StepBufs& b, const uint16_t*
   na.kdim = DIM_CC;
   // the relation weight of each chunk scales its gradients (NULL: weight 1)
   qa.cscale = na.cscale = g.cweight;
+  // dN rows e < Cc of side 1 - s into dQ of side s (the same vectors)
+  qa.merge_cc = na.merge_cc = merge ? 1 : 0;
   launch_gemm_bf16_pair(qa, na, nch * 2, cs);
 }
 
@@ -162,7 +164,7 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
     // dS is 0 or 1: its products with the pieces are exact (float32 sums)
     if (qn)
       run_backward_h(g, b, nullptr, h.nnT3, h.n3_ps, h.nnT3 + (int64_t)dpb * Npb, h.n3_ps, 2ll * dpb * Npb,
-                     -(int64_t)dpb * Npb, Npb, 3, cs);
+                     -(int64_t)dpb * Npb, Npb, 3, cs, g.dq_has_dn != 0);
     else
       run_backward_h(g, b, nullptr, h.nnT3, h.n3_ps, h.qkT3, h.q3_ps, 2ll * dpb * Cpb, (int64_t)dpb * Cpb, Cpb, 3,
                      cs);

@@ -501,6 +501,7 @@ void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, const BucketTables& t
   g.recip = reciprocal(ctx) ? 1 : 0;
   g.R = ctx->R;
   g.relN = g.recip ? 2 * C : N;
+  g.dq_has_dn = merged_ranking_backward(ctx, g) ? 1 : 0;
 }
 
 StepBufs bucket_bufs(pbg_ctx* ctx, const BucketTables& tb) {

@@ -188,6 +188,12 @@ inline bool sorted_relation_keys(const pbg_ctx* ctx) {
 }
 // the linear operator as contractions over the whole step (one relation
 // matrix); otherwise one matrix-vector product per edge
+// The float32 ranking backward with the queries as candidate rows (QK_IN_NN)
+// merges dN rows e < Cc of one side into dQ of the other (kernels.h, merge_cc).
+inline bool merged_ranking_backward(const pbg_ctx* ctx, const StepGeom& g) {
+  return QK_IN_NN(g) && g.loss == LOSS_RANKING && !(ctx->flags & PBG_F_BF16_SCORE);
+}
+
 inline bool linear_step_contractions(const pbg_ctx* ctx) {
   return ctx->op == PBG_OP_LINEAR && relation_rows(ctx) == 1;
 }
