@@ -713,8 +713,10 @@ def row_negatives():
     graph (translation, cos, ranking, d = 128): batched, a chunk of B/2 edges
     is corrupted with its own entities and B/2 uniform draws (B negatives per
     edge, scored by contractions); unbatched, every edge is its own chunk with
-    B uniform draws (chunk_size 1: one score row per edge).  40 chunks a step;
-    each point times whole steps after one warm-up call."""
+    B uniform draws (chunk_size 1: one score row per edge).  Batched: 40 chunks
+    a step, 50 steps; unbatched: 1,000 one-edge chunks a step (so that a step
+    carries 1,000 edges, not 40), 10 steps.  Each point times whole steps after
+    one warm-up call."""
     import torch
     from paper_1903_12287_amd import pbg, synth
     torch.cuda.set_device(0)
@@ -724,8 +726,8 @@ def row_negatives():
     points = []
     for B in (10, 50, 100, 200, 500, 1000, 2000):
         for mode, c, u in (("batched", B // 2, B - B // 2), ("unbatched", 1, B)):
-            steps = 50 if mode == "batched" else 10
-            e_call = steps * 40 * c
+            steps, S_ = (50, 40) if mode == "batched" else (10, 1000)
+            e_call = steps * S_ * c
             emb = emb0.clone()
             G = torch.zeros(N_NODES, dtype=torch.float32, device=dev)
             relp = relp0.clone()
@@ -734,7 +736,7 @@ def row_negatives():
                 pbg.pbg_bind_partition(ctx, 0, emb, G)
                 pbg.pbg_bind_relations(ctx, relp, torch.zeros_like(relp))
                 pbg.pbg_set_streams(ctx, torch.cuda.current_stream(), None)
-                run = lambda: pbg.pbg_train_bucket(ctx, 0, 0, src[:e_call], None, dst[:e_call], c, u, 40, LR, SEED)
+                run = lambda: pbg.pbg_train_bucket(ctx, 0, 0, src[:e_call], None, dst[:e_call], c, u, S_, LR, SEED)
                 run()
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
@@ -743,13 +745,13 @@ def row_negatives():
                 dt = time.perf_counter() - t0
             finally:
                 pbg.pbg_free(ctx)
-            points.append({"negatives": B, "mode": mode, "chunk": c, "uniform": u, "edges": e_call,
-                           "edges_per_s": e_call / dt})
+            points.append({"negatives": B, "mode": mode, "chunk": c, "uniform": u, "chunks_per_step": S_,
+                           "edges": e_call, "edges_per_s": e_call / dt})
             print(f"# {mode} B={B}: {e_call / dt:.4g} edges/s", file=sys.stderr, flush=True)
     best = max(p["edges_per_s"] for p in points if p["mode"] == "batched" and p["negatives"] == 1000)
     return {"metric": "trained edges/sec on 1 MI355X", "value": best, "unit": "edges/s", "dtype": "f32",
             "config": {"workload": "social_network negatives sweep", "nodes": N_NODES, "dim": DIM,
-                       "operator": "translation", "comparator": "cos", "loss": "ranking", "chunks_per_step": 40},
+                       "operator": "translation", "comparator": "cos", "loss": "ranking"},
             "note": "value: batched, 1000 negatives per edge; points: every (negatives, mode)",
             "points": points}
 
