@@ -47,6 +47,10 @@ SHAPES = {
     # relation-grouped chunks: cos with an operator and 40 relations (each
     # chunk's relation applied to its source candidates)
     "grouped_cos": ("translation", "cos", "ranking", 64, 40, 20_000, 1, (0, 0), 1000, 1000, 1.0, 1.0, 0.8),
+    # cos with the value losses at chunks holding full 128-row score tiles: side
+    # 1's in-chunk tiles come transposed from side 0's (shared block)
+    "cos_logistic": ("diagonal", "cos", "logistic", 64, 1, 20_000, 1, (0, 0), 300, 260, 1.1, 1.1, None),
+    "cos_softmax": ("translation", "cos", "softmax", 96, 1, 20_000, 1, (0, 0), 400, 300, 1.1, 1.1, None),
 }
 GROUPED = {"grouped_cos"}
 

@@ -258,3 +258,35 @@ def test_relation_grouping_helper_and_errors():
     with pytest.raises(pbg.PbgError) as ei:
         pbg.pbg_bucket_init(100, 1, 3, 8, "linear", "cos", "ranking")
     assert ei.value.status_name == "UNSUPPORTED"
+
+
+@pytest.mark.parametrize("op,cmp,loss,C,U", [("diagonal", "cos", "logistic", 300, 200),
+                                             ("translation", "cos", "softmax", 260, 140),
+                                             ("identity", "cos", "softmax", 520, 100)])
+def test_shared_score_block_steps_match_oracle(op, cmp, loss, C, U):
+    """Chunks of 260 to 520 edges with cos: the scores of side 1 against the
+    chunk's own candidates come from side 0's full 128 x 128 tiles, transposed
+    (Sec. 4.3: both sides' in-chunk negatives are the same products).  Several
+    steps with a short last chunk, per-step losses and the final state against
+    the oracle at 1e-4 (smooth losses)."""
+    S = 2
+    m = 3 * S * C - 37
+    pb = make_problem(op, cmp, loss, n=3000, R=1, d=48, m=m, C=C, U=U, S=S, seed=83, sigma=0.2)
+    gm = GpuModel(pb)
+    try:
+        gm.train()
+        from paper_1903_12287_amd import pbg
+        steps = pbg.pbg_get_step_losses(gm.ctx)
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol, osteps = O.train_bucket(om, 0, 0, pb.src, pb.rel_ids, pb.dst, C, U, S, pb.lr, pb.seed, return_steps=True)
+    assert len(steps) == len(osteps) == 3
+    for a, b in zip(steps, osteps):
+        assert abs(a - b) <= 1e-4 * max(1.0, abs(b)), (a, b)
+    err = float(np.max(np.abs(st["emb"][0] - om.emb[0])))
+    assert err <= 1e-4, err
+    if "rel" in st:
+        rerr = float(np.max(np.abs(st["rel"] - om.rel)))
+        assert rerr <= 1e-4, rerr
