@@ -539,6 +539,42 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgsH& a, const TileGeo&
 }
 
 
+// The 128 x 128 tile held as four 64 x 64 wave blocks in the matrix-instruction
+// layout (acc[i][j][r] is row 16 i + 4 g + r, column 16 j + l16 of the block of
+// wave (wm, wn)) becomes its transpose: wave (wm, wn) ends with block (wn, wm)
+// transposed.  The two off-diagonal waves swap through LDS first, then the two
+// diagonal ones transpose in place; a block passes through a [64][68] float32
+// slot (rows padded so that the 4-byte writes and 16-byte reads meet distinct
+// banks).  L: kTransposeFloats floats.  Every wave of the workgroup calls it.
+constexpr int kTransposeLd = 68;
+constexpr int kTransposeFloats = 2 * 64 * kTransposeLd;
+__device__ __forceinline__ void transpose_tile(v4f (&acc)[4][4], float* L, int wm, int wn, int l16, int g) {
+  constexpr int LD = kTransposeLd;
+  const bool off = wm != wn;
+#pragma unroll
+  for (int phase = 0; phase < 2; ++phase) {
+    const bool mine = (phase == 0) == off;
+    if (mine) {
+      float* s = L + wm * 64 * LD;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) s[(16 * i + 4 * g + r) * LD + 16 * j + l16] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (mine) {
+      const float* s = L + wn * 64 * LD;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = *(const v4f*)(s + (16 * j + l16) * LD + 16 * i + 4 * g);
+    }
+    __syncthreads();
+  }
+}
+
 // One 128 x BN output tile of A . B with bf16 operands (B in PL planes).
 template <int BN, int AMODE, int EPI, int PL>
 __device__ __forceinline__ void gemm_bf16_tile(const GemmArgsH& a, int tiles_n, int tiles_m, int nwg, int id,
@@ -714,39 +750,6 @@ struct SmemST {
 };
 using SmemS = SmemST<BM>;
 
-// The 128 x 128 tile held as four 64 x 64 wave blocks in the matrix-instruction
-// layout (acc[i][j][r] is row 16 i + 4 g + r, column 16 j + l16 of the block of
-// wave (wm, wn)) becomes its transpose: wave (wm, wn) ends with block (wn, wm)
-// transposed.  The two off-diagonal waves swap through LDS first, then the two
-// diagonal ones transpose in place; a block passes through a [64][68] float32
-// slot (rows padded so that the 4-byte writes and 16-byte reads meet distinct
-// banks).  L: 2 * 64 * 68 floats.  Every wave of the workgroup calls it.
-__device__ __forceinline__ void transpose_tile(v4f (&acc)[4][4], float* L, int wm, int wn, int l16, int g) {
-  constexpr int LD = 68;
-  const bool off = wm != wn;
-#pragma unroll
-  for (int phase = 0; phase < 2; ++phase) {
-    const bool mine = (phase == 0) == off;
-    if (mine) {
-      float* s = L + wm * 64 * LD;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) s[(16 * i + 4 * g + r) * LD + 16 * j + l16] = acc[i][j][r];
-    }
-    __syncthreads();
-    if (mine) {
-      const float* s = L + wn * 64 * LD;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = *(const v4f*)(s + (16 * j + l16) * LD + 16 * i + 4 * g);
-    }
-    __syncthreads();
-  }
-}
 
 // Score tile body: four waves of 64 x 64.  One A plane and one B plane in
 // registers at a time (B planes are read again for each A plane).
@@ -754,7 +757,7 @@ template <int EPI, int NPROD>
 __device__ __forceinline__ void score_split_body(const GemmArgsH& a, int tiles_n, int tiles_m) {
   constexpr int BN = 128, WN = 64, JN = 4, WMR = BM / 2, IM = BM / 32;
   __shared__ __align__(16) SmemS sm;
-  static_assert(sizeof(sm.As) + sizeof(sm.Bs) >= 2 * 64 * 68 * sizeof(float), "transpose slots");
+  static_assert(sizeof(sm.As) + sizeof(sm.Bs) >= kTransposeFloats * sizeof(float), "transpose slots");
   TileGeo t;
   if (!tile_geo<BN, EPI>(a, tiles_n, tiles_m, gridDim.x, blockIdx.x, t)) return;
   if (EPI != EPI_STORE) load_rowv<EPI>(a, t, sm.rowv);
