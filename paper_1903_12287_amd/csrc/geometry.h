@@ -56,6 +56,8 @@ struct StepGeom {
   int recip;        // reciprocal predicates: the source side uses relation row r + R
   int R;            // relations (the offset of the source side's rows)
   int relN;         // rows of relc per chunk (N; 2C with reciprocal predicates)
+  int relsum;       // one relation operator for every edge (not linear): the operator backward adds the
+                    // parameter-gradient rows of each block and relc holds one row per block
   const float* cweight;   // relation weight of each chunk of the step (device), NULL: all 1
   int dq_has_dn;    // with QK_IN_NN: dq of side s, row e < Cc, already holds dn of side 1 - s, row e (the
                     // ranking backward merged them), and those dn rows are not written
@@ -133,7 +135,8 @@ struct StepBufs {
   float* dn;
   float* relc;          // [S][relN][dr] relation gradient contributions: edge rows, then the
                         // uniform source candidates' (cos with an operator) or, with
-                        // reciprocal predicates, the edges' source-side rows r + R
+                        // reciprocal predicates, the edges' source-side rows; with relsum
+                        // [S][blocks of the operator backward][dr], one summed row per block r + R
   float* qnrm;          // reciprocal + cos: [S][2][C] norms of the raw queries
   float* lin_x;         // linear + cos: [S][N][dp] raw source candidate rows x_t (reciprocal
                         // predicates: [S][2][C][dp], the edges' raw x_s, then x_d)

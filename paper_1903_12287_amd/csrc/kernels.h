@@ -151,6 +151,13 @@ inline int fin_blocks(int C) { return (C + FIN_THREADS - 1) / FIN_THREADS; }
 void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, bool softmax_scales,
                      hipStream_t s);
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s);
+// blocks per chunk of the operator backward's grid (relc rows per chunk with
+// relsum): one wave per edge, and with cos one per four uniform candidates of
+// a side
+inline int op_backward_blocks(int C, int U, int cmp) {
+  const int items = C + (cmp == CMP_COS ? 2 * ((U + 3) / 4) : 0);
+  return (items + 3) / 4;
+}
 
 // ---- sort, segments, updates ----------------------------------------------------
 // sorted positions per wave of the segment update (a power of two <= 32)
@@ -195,9 +202,10 @@ void launch_entity_update(const StepGeom& g, const StepBufs& b, const uint32_t* 
 void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, const uint32_t* keys,
                                    const uint32_t* vals, int n, SortWork& w, float lr, hipStream_t s);
 // pieces per chunk of the single-relation gradient sum (partial rows per chunk)
-#define RELSUM_PIECES 32
-void launch_relation_chunk_sums(const StepGeom& g, const float* rows, int64_t ld, int include_uniform,
-                                float* partial, hipStream_t s);
+#define RELSUM_PIECES 8
+// sums of the nblk rows per chunk that the operator backward leaves with
+// StepGeom::relsum, RELSUM_PIECES partial rows per chunk
+void launch_relation_block_sums(const StepGeom& g, const float* rows, int nblk, float* partial, hipStream_t s);
 void launch_relation_single_adagrad(float* relp, float* relG, int width, const float* partial,
                                     int nparts, float lr, hipStream_t s);
 void launch_exclusive_scan(const uint32_t* in, int64_t n, uint32_t* out, uint32_t* tmp,

@@ -243,15 +243,14 @@ __device__ __forceinline__ void op_backward_reciprocal(const StepGeom& g, const 
   row_store(dX, dn1, d, dp, cplx, lane);
 }
 
-template <int RQ>
-__global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b) {
+// One item of the operator / normalisation backward: edge `item` of chunk c,
+// or four uniform candidates of one side.  Relation-parameter gradient rows
+// go to relc, or with RELSUM (one relation shared by every edge) are added to
+// rsum.
+template <int RQ, bool RELSUM>
+__device__ __forceinline__ void op_backward_item(const StepGeom& g, const StepBufs& b, int c, int Cc, int item,
+                                                 int lane, RowT<RQ>& rsum) {
   using Row = RowT<RQ>;
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
-  const int c = blockIdx.y;
-  const int Cc = chunk_edges(g, c);
-  const int item = blockIdx.x * 4 + w;
-  if (item >= Cc + 2 * ((g.U + 3) >> 2)) return;   // no block-level barriers below
   const bool cplx = g.op == OP_COMPLEX;
   const int d = g.d, dp = g.dp;
   const bool cos = g.cmp == CMP_COS;
@@ -267,7 +266,7 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     Row th;
     if (has_rel && g.op != OP_LINEAR) row_load(th, b.relp + (int64_t)r * g.dr, d, cplx, lane);
     else row_zero(th);
-    if (g.recip) {
+    if (!RELSUM && g.recip) {   // reciprocal predicates make 2R relation operators: never RELSUM
       op_backward_reciprocal(g, b, c, e, s, t, r, th, lane);
       return;
     }
@@ -352,7 +351,8 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
     // A^T dv is formed by a contraction over the step's source candidates
     float* srow = (cos && g.op == OP_LINEAR) ? b.lin_v + ((int64_t)c * g.N + e) * dp : dn1;
     row_store(gs, srow, d, dp, cplx, lane);
-    if (has_rel && g.op != OP_LINEAR)
+    if (RELSUM) row_add(rsum, grel);
+    else if (has_rel && g.op != OP_LINEAR)
       row_store(grel, b.relc + ((int64_t)c * g.relN + e) * g.dr, d, g.dr, cplx, lane);
     return;
   }
@@ -404,13 +404,42 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
           row_load(x, b.emb_i + (int64_t)u[q] * d, d, cplx, lane);
           grel = op_param_grad(g.op, x, dv);
         }
-        row_store(grel, b.relc + ((int64_t)c * g.relN + g.C + k0 + q) * g.dr, d, g.dr, cplx, lane);
+        if (RELSUM) row_add(rsum, grel);
+        else row_store(grel, b.relc + ((int64_t)c * g.relN + g.C + k0 + q) * g.dr, d, g.dr, cplx, lane);
         dv = op_adjoint(g.op, dv, th);
       }
       float* drow = lin_side ? b.lin_v + ((int64_t)c * g.N + Cc + k0 + q) * dp : b.dn + (rbase + q) * dp;
       row_store(dv, drow, d, dp, cplx, lane);
     }
   }
+}
+
+template <int RQ, bool RELSUM>
+__global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b) {
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int c = blockIdx.y;
+  const int Cc = chunk_edges(g, c);
+  const int item = blockIdx.x * 4 + w;
+  RowT<RQ> rsum;
+  row_zero(rsum);
+  if (item < Cc + 2 * ((g.U + 3) >> 2)) op_backward_item<RQ, RELSUM>(g, b, c, Cc, item, lane, rsum);
+  if (!RELSUM) return;
+  // one relation: the four waves' sums are added in wave order and the block
+  // writes one row, relc row blockIdx.x of chunk c (every block writes its
+  // row, zero where no wave had an item)
+  __shared__ float red[4][RQ * 64];
+#pragma unroll
+  for (int q = 0; q < RQ; ++q) red[w][q * 64 + lane] = rsum.v[q];
+  __syncthreads();
+  if (w != 0) return;
+  RowT<RQ> tot;
+#pragma unroll
+  for (int q = 0; q < RQ; ++q) {
+    const int f = q * 64 + lane;
+    tot.v[q] = (red[0][f] + red[1][f]) + (red[2][f] + red[3][f]);
+  }
+  row_store(tot, b.relc + ((int64_t)c * gridDim.x + blockIdx.x) * g.dr, g.d, g.dr, g.op == OP_COMPLEX, lane);
 }
 
 }  // namespace
@@ -425,11 +454,15 @@ void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slo
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s) {
   // waves for the uniform candidates only where the cos normalisation has a
   // backward to run
-  const int items = g.C + (g.cmp == CMP_COS ? 2 * ((g.U + 3) / 4) : 0);
-  dim3 grid((items + 3) / 4, g.nchunks);
-  switch (row_width_for(g.d)) {
-    case 2: op_backward_kernel<2><<<grid, 256, 0, s>>>(g, b); break;
-    case 4: op_backward_kernel<4><<<grid, 256, 0, s>>>(g, b); break;
-    default: op_backward_kernel<8><<<grid, 256, 0, s>>>(g, b); break;
+  dim3 grid(op_backward_blocks(g.C, g.U, g.cmp), g.nchunks);
+  const int rq = row_width_for(g.d);
+  if (g.relsum) {
+    if (rq == 2) op_backward_kernel<2, true><<<grid, 256, 0, s>>>(g, b);
+    else if (rq == 4) op_backward_kernel<4, true><<<grid, 256, 0, s>>>(g, b);
+    else op_backward_kernel<8, true><<<grid, 256, 0, s>>>(g, b);
+  } else {
+    if (rq == 2) op_backward_kernel<2, false><<<grid, 256, 0, s>>>(g, b);
+    else if (rq == 4) op_backward_kernel<4, false><<<grid, 256, 0, s>>>(g, b);
+    else op_backward_kernel<8, false><<<grid, 256, 0, s>>>(g, b);
   }
 }

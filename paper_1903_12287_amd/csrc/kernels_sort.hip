@@ -512,44 +512,46 @@ __global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, c
   seg_apply<MODE, RQ>(g, b, key, acc, width, lr, lane);
 }
 
-// First level of the single-relation gradient sum: block (c, piece) adds, in
-// a fixed order, the contribution rows of chunk c that fall in its piece of
-// the chunk's row list (the Cc edge rows, then the U uniform rows when they
-// carry relation gradient).  Spreading a chunk over RELSUM_PIECES blocks keeps
-// enough waves in flight to stream the rows at HBM speed.
-__global__ __launch_bounds__(256) void relation_chunk_sums(StepGeom g, const float* rows, int64_t ld,
-                                                           int include_uniform, float* partial) {
-  __shared__ float red[4][512];
+// Second level of the single-relation gradient sum: the operator backward
+// left nblk rows per chunk (one per block of its grid); block (c, piece) adds,
+// in row order, the rows of chunk c that fall in its piece (wave w the rows
+// k0 + w, k0 + w + 4, ..., 32 / RQ of them loaded at a time).
+template <int RQ>
+__global__ __launch_bounds__(256) void relation_block_sums(const float* rows, int nblk, int dr, float* partial) {
+  __shared__ float red[4][RQ * 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int c = blockIdx.x;
   const int piece = blockIdx.y;
-  const int Cc = chunk_edges(g, c);
-  const int nrows = Cc + (include_uniform ? g.U : 0);
-  const int per = (nrows + RELSUM_PIECES - 1) / RELSUM_PIECES;
+  const int per = (nblk + RELSUM_PIECES - 1) / RELSUM_PIECES;
   const int k0 = piece * per;
-  const int k1 = min(nrows, k0 + per);
-  const float* base = rows + (int64_t)c * g.N * ld;
-  float acc[ROWQ];
+  const int k1 = min(nblk, k0 + per);
+  const float* base = rows + (int64_t)c * nblk * dr;
+  float acc[RQ];
 #pragma unroll
-  for (int q = 0; q < ROWQ; ++q) acc[q] = 0.0f;
-#pragma unroll 16
-  for (int k = k0 + w; k < k1; k += 4) {
-    const int row = k < Cc ? k : g.C + (k - Cc);
-    const float* r = base + (int64_t)row * ld;
+  for (int q = 0; q < RQ; ++q) acc[q] = 0.0f;
+  constexpr int B = 32 / RQ;
+  for (int k = k0 + w; k < k1; k += 4 * B) {
+    float v[B][RQ];
 #pragma unroll
-    for (int q = 0; q < ROWQ; ++q) {
-      const int f = lane + 64 * q;
-      if (f < g.dr) acc[q] += r[f];
+    for (int u = 0; u < B; ++u) {
+      const int kk = k + 4 * u;
+      const float* r = base + (int64_t)kk * dr;
+#pragma unroll
+      for (int q = 0; q < RQ; ++q) {
+        const int f = lane + 64 * q;
+        v[u][q] = (kk < k1 && f < dr) ? r[f] : 0.0f;
+      }
     }
+#pragma unroll
+    for (int u = 0; u < B; ++u)
+#pragma unroll
+      for (int q = 0; q < RQ; ++q) acc[q] += v[u][q];
   }
 #pragma unroll
-  for (int q = 0; q < ROWQ; ++q) {
-    const int f = lane + 64 * q;
-    if (f < g.dr) red[w][f] = acc[q];
-  }
+  for (int q = 0; q < RQ; ++q) red[w][lane + 64 * q] = acc[q];
   __syncthreads();
-  float* out = partial + ((int64_t)c * RELSUM_PIECES + piece) * g.dr;
-  for (int f = threadIdx.x; f < g.dr; f += 256) out[f] = (red[0][f] + red[1][f]) + (red[2][f] + red[3][f]);
+  float* out = partial + ((int64_t)c * RELSUM_PIECES + piece) * dr;
+  for (int f = threadIdx.x; f < dr; f += 256) out[f] = (red[0][f] + red[1][f]) + (red[2][f] + red[3][f]);
 }
 
 // Second level and element-wise Adagrad: 64 elements per block; wave w of 16
@@ -718,9 +720,13 @@ void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, const u
   seg_update<SEG_RELATION>(g, b, keys, vals, n, b.relc, g.dr, g.dr, w, lr, s);
 }
 
-void launch_relation_chunk_sums(const StepGeom& g, const float* rows, int64_t ld, int include_uniform,
-                                float* partial, hipStream_t s) {
-  relation_chunk_sums<<<dim3(g.nchunks, RELSUM_PIECES), 256, 0, s>>>(g, rows, ld, include_uniform, partial);
+void launch_relation_block_sums(const StepGeom& g, const float* rows, int nblk, float* partial, hipStream_t s) {
+  const dim3 grid(g.nchunks, RELSUM_PIECES);
+  switch (row_width_for(g.dr)) {
+    case 2: relation_block_sums<2><<<grid, 256, 0, s>>>(rows, nblk, g.dr, partial); break;
+    case 4: relation_block_sums<4><<<grid, 256, 0, s>>>(rows, nblk, g.dr, partial); break;
+    default: relation_block_sums<8><<<grid, 256, 0, s>>>(rows, nblk, g.dr, partial); break;
+  }
 }
 
 void launch_relation_single_adagrad(float* relp, float* relG, int width, const float* partial,

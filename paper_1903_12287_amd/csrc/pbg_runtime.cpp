@@ -111,7 +111,9 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   b.dn = (float*)a.get(s * 2 * N * dp * 4);
   const bool has_rel = ctx->op != OP_IDENTITY;
   const bool linear = ctx->op == OP_LINEAR;
-  const int relN = reciprocal(ctx) ? 2 * C : N;
+  // rows per chunk: contributions, or with one relation the operator
+  // backward's per-block sums
+  const int relN = reciprocal(ctx) ? 2 * C : (single_relation_sums(ctx) ? op_backward_blocks(C, U, ctx->cmp) : N);
   if (has_rel && !linear) b.relc = (float*)a.get(s * relN * ctx->dr * 4);
   if (reciprocal(ctx) && ctx->cmp == PBG_CMP_COS) b.qnrm = (float*)a.get(s * 2 * C * 4);
   const int64_t nkeys = s * 2 * N;
@@ -183,34 +185,6 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   ctx->ws_ready = true;
   return PBG_OK;
 }
-
-// the side stream and its events, created once per context
-static bool ensure_side(pbg_ctx* ctx) {
-  if (ctx->side) return true;
-  hipStream_t st = nullptr;
-  if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) {
-    (void)hipGetLastError();
-    return false;
-  }
-  if ((!ctx->fork_ev && hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming) != hipSuccess) ||
-      (!ctx->join_ev[0] && hipEventCreateWithFlags(&ctx->join_ev[0], hipEventDisableTiming) != hipSuccess) ||
-      (!ctx->join_ev[1] && hipEventCreateWithFlags(&ctx->join_ev[1], hipEventDisableTiming) != hipSuccess)) {
-    (void)hipGetLastError();
-    (void)hipStreamDestroy(st);
-    return false;
-  }
-  ctx->side = st;
-  return true;
-}
-
-void side_fork(pbg_ctx* ctx) {
-  (void)hipEventRecord(ctx->fork_ev, ctx->cs);
-  (void)hipStreamWaitEvent(ctx->side, ctx->fork_ev, 0);
-}
-
-void side_mark(pbg_ctx* ctx, int k) { (void)hipEventRecord(ctx->join_ev[k], ctx->side); }
-
-void side_wait(pbg_ctx* ctx, int k) { (void)hipStreamWaitEvent(ctx->cs, ctx->join_ev[k], 0); }
 
 static bool ensure_events(pbg_ctx* ctx, size_t n) {
   while (ctx->events.size() < n) {
@@ -358,10 +332,6 @@ void pbg_free(pbg_ctx* ctx) {
     if (s.released) (void)hipEventDestroy(s.released);
   }
   if (ctx->own_xs) (void)hipStreamDestroy(ctx->own_xs);
-  if (ctx->side) (void)hipStreamDestroy(ctx->side);
-  if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
-  for (hipEvent_t e : ctx->join_ev)
-    if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
   delete ctx;
 }
@@ -501,6 +471,7 @@ void bucket_geom(const pbg_ctx* ctx, int32_t i, int32_t j, const BucketTables& t
   g.recip = reciprocal(ctx) ? 1 : 0;
   g.R = ctx->R;
   g.relN = g.recip ? 2 * C : N;
+  g.relsum = single_relation_sums(ctx) ? 1 : 0;
   g.dq_has_dn = merged_ranking_backward(ctx, g) ? 1 : 0;
 }
 
@@ -603,7 +574,6 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
   StepBufs b = bucket_bufs(ctx, tb);
   if (hipMemsetAsync(b.nuniq, 0, 8, cs) != hipSuccess) return hip_fail(ctx, hipGetLastError(), "counter reset");
 
-  if (!ensure_side(ctx)) return set_err(ctx, PBG_ERR_DEVICE, "could not create the side stream");
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   (void)hipEventCreate(&ev0);
   (void)hipEventCreate(&ev1);
@@ -691,8 +661,6 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
     if (linear_step_contractions(ctx)) run_linear_backward(g, b, ctx->relA, ctx->relAT, cs);
     else if (linear) launch_linear_rows_backward(g, b, cs);
     mark(t, 5);
-    const bool rel_side = has_rel && !linear && !sorted_relation_keys(ctx);
-    if (rel_side) side_fork(ctx);
 
     // entities: contribution rows in (table, row) order, segment sums, Adagrad
     launch_entity_update(g, b, skeys, svals, nkeys, ctx->sw, lr, cs);
@@ -713,14 +681,11 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
         launch_radix_sort_to(b.rkeys, b.rvals, n_relkeys, rel_bits, ctx->sw, &rk, &rv, cs);
         launch_relation_update_sorted(g, b, rk, rv, n_relkeys, ctx->sw, lr, cs);
       } else {
-        // the single relation's gradient sums and update read only what the
-        // operator backward wrote: on the side stream, beside the entity sort
-        // and update, joined before the step ends
-        launch_relation_chunk_sums(g, b.relc, ctx->dr, ctx->cmp == CMP_COS ? 1 : 0, ctx->relpartial, ctx->side);
+        // one relation: the operator backward left one gradient row per
+        // block of its grid; their fixed-order sums, then element-wise Adagrad
+        launch_relation_block_sums(g, b.relc, op_backward_blocks(g.C, g.U, g.cmp), ctx->relpartial, cs);
         launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch * RELSUM_PIECES,
-                                       lr, ctx->side);
-        side_mark(ctx, 1);
-        side_wait(ctx, 1);
+                                       lr, cs);
       }
     }
     mark(t, 6);

@@ -110,12 +110,6 @@ struct pbg_ctx {
   pbg_stats stats{};
   std::vector<Slot> slots;
   hipStream_t own_xs = nullptr;    // copy stream created for pbg_train_epoch when none was given
-  // second compute stream for work of a step that does not depend on its
-  // neighbours on the compute stream (default priority), with the events that
-  // fork work onto it and join it back
-  hipStream_t side = nullptr;
-  hipEvent_t fork_ev = nullptr;
-  hipEvent_t join_ev[2] = {nullptr, nullptr};
   std::vector<hipEvent_t> events;  // phase-timing events, kPhaseEvents per step
 };
 
@@ -130,13 +124,6 @@ pbg_status set_err(pbg_ctx* ctx, pbg_status st, const char* fmt, ...);
 // device address of the static scratch of pbg_score_edges_noalloc on the
 // context's device (taken once per device; called by pbg_bucket_init)
 pbg_status noalloc_scratch_init(pbg_ctx* ctx);
-// work of a step on the side stream: side_fork makes the side stream wait for
-// what the compute stream has queued so far; side_mark(k) marks what the side
-// stream has queued so far and side_wait(k) makes the compute stream wait for
-// that mark (two marks, k = 0, 1)
-void side_fork(pbg_ctx* ctx);
-void side_mark(pbg_ctx* ctx, int k);
-void side_wait(pbg_ctx* ctx, int k);
 
 // the three contractions of step t (forward_only: the score contraction with
 // its loss epilogue and the per-edge finalisation only)
@@ -186,14 +173,20 @@ inline bool chunk_relation_operator(const pbg_ctx* ctx) {
 inline bool sorted_relation_keys(const pbg_ctx* ctx) {
   return ctx->op != PBG_OP_IDENTITY && relation_rows(ctx) > 1;
 }
-// the linear operator as contractions over the whole step (one relation
-// matrix); otherwise one matrix-vector product per edge
+// one relation operator with a parameter row (translation, diagonal, complex
+// diagonal; no reciprocal predicates): the operator backward adds each
+// block's parameter-gradient rows, and the fixed-order sum of those rows and
+// the element-wise Adagrad step follow it
+inline bool single_relation_sums(const pbg_ctx* ctx) {
+  return ctx->op != PBG_OP_IDENTITY && ctx->op != PBG_OP_LINEAR && !sorted_relation_keys(ctx);
+}
 // The float32 ranking backward with the queries as candidate rows (QK_IN_NN)
 // merges dN rows e < Cc of one side into dQ of the other (kernels.h, merge_cc).
 inline bool merged_ranking_backward(const pbg_ctx* ctx, const StepGeom& g) {
   return QK_IN_NN(g) && g.loss == LOSS_RANKING && !(ctx->flags & PBG_F_BF16_SCORE);
 }
-
+// the linear operator as contractions over the whole step (one relation
+// matrix); otherwise one matrix-vector product per edge
 inline bool linear_step_contractions(const pbg_ctx* ctx) {
   return ctx->op == PBG_OP_LINEAR && relation_rows(ctx) == 1;
 }

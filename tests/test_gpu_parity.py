@@ -68,6 +68,35 @@ def test_linear_single_relation_one_step(op, cmp, loss):
     assert ok, ("rel", err)
 
 
+@pytest.mark.parametrize("op,cmp,loss,d,C,U", [("translation", "dot", "logistic", 24, 20, 12),
+                                               ("complex_diagonal", "dot", "ranking", 20, 20, 12),
+                                               ("diagonal", "dot", "softmax", 19, 13, 9),
+                                               ("complex_diagonal", "cos", "ranking", 36, 20, 12),
+                                               ("diagonal", "cos", "softmax", 130, 37, 29)])
+def test_single_relation_sums_match_oracle(op, cmp, loss, d, C, U):
+    """One relation: each block of the operator backward adds its rows of the
+    parameter gradient (edges, and with cos the uniform source candidates),
+    then fixed pieces per chunk are added; ragged chunks and blocks with idle
+    waves included.  Relation parameters, embeddings and Adagrad state."""
+    pb = make_problem(op, cmp, loss, R=1, d=d, m=95, C=C, U=U, S=3, seed=37)
+    gm = GpuModel(pb)
+    try:
+        gl = gm.train()
+        st = gm.state()
+    finally:
+        gm.close()
+    om = oracle_model(pb)
+    ol = O.train_bucket(om, pb.i, pb.j, pb.src, pb.rel_ids, pb.dst, pb.C, pb.U, pb.S, pb.lr, pb.seed)
+    assert abs(gl - ol) <= 1e-5 * max(1.0, abs(ol)), (gl, ol)
+    for key, ref in (("G", om.G[0]), ("emb", om.emb[0])):
+        ok, err = _close(st[key][0], ref)
+        assert ok, (key, err)
+    ok, err = _close(st["rel"], om.rel)
+    assert ok, ("rel", err)
+    ok, err = _close(st["relG"], om.relG)
+    assert ok, ("relG", err)
+
+
 def _close(gpu, ref, rel=1e-5, abs_=1e-6):
     scale = max(1.0, float(np.max(np.abs(ref)))) if ref.size else 1.0
     err = float(np.max(np.abs(gpu - ref))) if ref.size else 0.0
