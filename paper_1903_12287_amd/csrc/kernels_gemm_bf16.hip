@@ -294,20 +294,24 @@ __device__ __forceinline__ void bits_rows(const GemmArgsH& a, const TileGeo& t, 
   for (int i = 0; i < IM; ++i) {
     const int mb = WMR * wm + 16 * i + 4 * g;   // first of this lane group's four rows
     const v4f thr = *(const v4f*)&rowv[0][mb];
-    float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float ls[4] = {-0.0f, -0.0f, -0.0f, -0.0f};   // -0 + x is x: the first add folds away
     uint32_t cnt[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int j = 0; j < JN; ++j) {
       uint32_t wd[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        float z = acc[i][j][r] + thr[r];
+        // s + thr > 0 exactly when s > -thr (an IEEE sum is positive exactly
+        // when the exact sum is), so the compare needs no add; the hinge sum
+        // of the row is the sum of its selected scores plus thr per bit
+        const float s = acc[i][j][r];
+        bool hit = s > -thr[r];
         if (MASKED) {
           const int n = colb + 16 * j;
-          if (n >= t.N || n == t.m0 + mb + r) z = -INFINITY;
+          if (n >= t.N || n == t.m0 + mb + r) hit = false;
         }
-        const uint64_t mk = __ballot(z > 0.0f);
-        ls[r] += z > 0.0f ? z : 0.0f;   // one select on the compare already made
+        const uint64_t mk = __ballot(hit);
+        ls[r] += hit ? s : 0.0f;   // one select on the compare already made
         wd[r] = (uint32_t)(mk >> (16 * g)) & 0xFFFFu;
         cnt[r] += __builtin_popcount(wd[r]);
       }
@@ -318,7 +322,7 @@ __device__ __forceinline__ void bits_rows(const GemmArgsH& a, const TileGeo& t, 
     for (int r = 0; r < 4; ++r) {
       const float v0 = group16_sum(ls[r]);
       if (l16 == 0) {
-        red[wn][mb + r][0] = v0;
+        red[wn][mb + r][0] = fmaf(thr[r], (float)cnt[r], v0);   // rows past the batch: unused
         red[wn][mb + r][1] = (float)cnt[r];
       }
     }
