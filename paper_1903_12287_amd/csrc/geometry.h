@@ -135,8 +135,9 @@ struct StepBufs {
   float* dn;
   float* relc;          // [S][relN][dr] relation gradient contributions: edge rows, then the
                         // uniform source candidates' (cos with an operator) or, with
-                        // reciprocal predicates, the edges' source-side rows; with relsum
-                        // [S][blocks of the operator backward][dr], one summed row per block r + R
+                        // reciprocal predicates, the edges' source-side rows r + R; with
+                        // relsum [S][blocks of the operator backward][dr], one summed row
+                        // per block
   float* qnrm;          // reciprocal + cos: [S][2][C] norms of the raw queries
   float* lin_x;         // linear + cos: [S][N][dp] raw source candidate rows x_t (reciprocal
                         // predicates: [S][2][C][dp], the edges' raw x_s, then x_d)
