@@ -128,9 +128,7 @@ struct StepBufs {
   float* rowloss;       // [S][2][C] each edge's loss per side (inspection only; NULL in training)
   float* dpos;          // [S][C] dL/dp ([S][2][C] with reciprocal predicates)
   float* dsum1;         // [S][C] sum_t dS1[e][t]
-  double* chunkloss;    // [S][FIN_BLOCKS(C)]  loss partials of the finalisation
   unsigned long long* nuniq;   // rows touched by the entity updates of the call (segment count)
-  unsigned int* fin_ticket;    // finished workgroups of the finalisation (zero between steps)
   float* dq;
   float* dn;
   float* relc;          // [S][relN][dr] relation gradient contributions: edge rows, then the

@@ -148,8 +148,12 @@ void launch_softmax_rows_bf16(const StepGeom& g, const StepBufs& b, uint16_t* ds
 // backward on split pieces (score epilogue EPI_SOFTMAX_EXP)
 #define FIN_THREADS 256
 inline int fin_blocks(int C) { return (C + FIN_THREADS - 1) / FIN_THREADS; }
-void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, bool softmax_scales,
-                     hipStream_t s);
+// parts: the step's fin_blocks(C) loss partials per chunk, [chunk][block]
+void launch_finalize(const StepGeom& g, const StepBufs& b, double* parts, bool softmax_scales, hipStream_t s);
+// out[t] = the fixed-order sum of the n partials of step t (stride apart;
+// n_full per step, n_last in the last)
+void launch_step_losses(const double* parts, int64_t stride, int n_full, int n_last, int64_t nsteps, double* out,
+                        hipStream_t s);
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s);
 // blocks per chunk of the operator backward's grid (relc rows per chunk with
 // relsum): one wave per edge, and with cos one per four uniform candidates of

@@ -17,7 +17,7 @@ namespace {
 
 // ---- per-edge dL/dp, translation bias gradient, losses ------------------------
 __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepBufs b, int softmax_scales,
-                                                                double* step_loss) {
+                                                                double* parts) {
   const int c = blockIdx.y;
   const int Cc = chunk_edges(g, c);
   double acc = 0.0;
@@ -153,29 +153,23 @@ __global__ __launch_bounds__(FIN_THREADS) void finalize_kernel(StepGeom g, StepB
     if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
     __syncthreads();
   }
-  // the last workgroup to finish adds all partials into the step loss, in a
-  // fixed order (lane l sums partials l, l + 64, ..., then a fixed butterfly
-  // over the wave), and re-arms the ticket for the next step
-  __shared__ bool last;
-  if (threadIdx.x == 0) {
-    b.chunkloss[(int64_t)c * gridDim.x + blockIdx.x] = red[0];
-    __threadfence();
-    const unsigned total = gridDim.x * gridDim.y;
-    last = atomicAdd(b.fin_ticket, 1u) == total - 1;
-  }
-  __syncthreads();
-  if (last && threadIdx.x < 64) {
-    __threadfence();
-    const int n = (int)(gridDim.x * gridDim.y);
-    const volatile double* part = b.chunkloss;
-    double sum = 0.0;
-    for (int i = threadIdx.x; i < n; i += 64) sum += part[i];
-    sum = wave_sum_d(sum);
-    if (threadIdx.x == 0) {
-      *step_loss = sum;
-      *b.fin_ticket = 0u;
-    }
-  }
+  if (threadIdx.x == 0) parts[(int64_t)c * gridDim.x + blockIdx.x] = red[0];
+}
+
+// Step losses from the finalisation's partials: wave t adds the n partials of
+// step t in a fixed order (lane l sums partials l, l + 64, ..., then a fixed
+// butterfly over the wave).
+__global__ __launch_bounds__(64) void step_loss_kernel(const double* parts, int64_t stride, int n_full, int n_last,
+                                                       int64_t nsteps, double* out) {
+  const int64_t t = blockIdx.x;
+  if (t >= nsteps) return;
+  const int n = t == nsteps - 1 ? n_last : n_full;
+  const double* p = parts + t * stride;
+  double sum = 0.0;
+#pragma unroll 8
+  for (int i = threadIdx.x; i < n; i += 64) sum += p[i];
+  sum = wave_sum_d(sum);
+  if (threadIdx.x == 0) out[t] = sum;
 }
 
 // ---- operator / comparator backward: contributions and sort keys -----------
@@ -445,10 +439,15 @@ __global__ __launch_bounds__(256) void op_backward_kernel(StepGeom g, StepBufs b
 }  // namespace
 
 
-void launch_finalize(const StepGeom& g, const StepBufs& b, double* step_loss_slot, bool softmax_scales,
-                     hipStream_t s) {
+void launch_finalize(const StepGeom& g, const StepBufs& b, double* parts, bool softmax_scales, hipStream_t s) {
   const int fb = fin_blocks(g.C);
-  finalize_kernel<<<dim3(fb, g.nchunks), FIN_THREADS, 0, s>>>(g, b, softmax_scales ? 1 : 0, step_loss_slot);
+  finalize_kernel<<<dim3(fb, g.nchunks), FIN_THREADS, 0, s>>>(g, b, softmax_scales ? 1 : 0, parts);
+}
+
+void launch_step_losses(const double* parts, int64_t stride, int n_full, int n_last, int64_t nsteps, double* out,
+                        hipStream_t s) {
+  if (nsteps <= 0) return;
+  step_loss_kernel<<<(unsigned)nsteps, 64, 0, s>>>(parts, stride, n_full, n_last, nsteps, out);
 }
 
 void launch_op_backward(const StepGeom& g, const StepBufs& b, hipStream_t s) {

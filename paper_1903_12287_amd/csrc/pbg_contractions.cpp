@@ -147,7 +147,7 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   // softmax: the score pass leaves exp(s - tile max), the finalisation each
   // row's log-sum-exp and per-tile scales, and the backward forms dS as it
   // stages the exponentials
-  launch_finalize(g, b, ctx->steploss_dev + t, g.loss == LOSS_SOFTMAX, cs);
+  launch_finalize(g, b, ctx->lossparts + t * ctx->lossparts_pps, g.loss == LOSS_SOFTMAX, cs);
   mark(3);
   if (forward_only) return;
 
@@ -305,7 +305,7 @@ void run_contractions_bf16(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, i
     launch_gemm_bf16(fa, EPI_LOSS, nch * 2, cs);
     mark(2);
   }
-  launch_finalize(g, b, ctx->steploss_dev + t, false, cs);
+  launch_finalize(g, b, ctx->lossparts + t * ctx->lossparts_pps, false, cs);
   mark(3);
   if (forward_only) return;
 

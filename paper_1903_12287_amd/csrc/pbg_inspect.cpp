@@ -43,6 +43,8 @@ extern "C" pbg_status pbg_inspect_step(pbg_ctx* ctx, int32_t i, int32_t j, const
     return set_err(ctx, PBG_ERR_INVALID_ARG, "pbg_inspect_step takes at most one step (%d chunks)", S);
   st = ensure_steploss(ctx, 1);
   if (st != PBG_OK) return st;
+  st = ensure_lossparts(ctx, 1, nchunks * fin_blocks(C));
+  if (st != PBG_OK) return st;
 
   hipStream_t cs = ctx->cs;
   StepGeom g;
@@ -86,6 +88,8 @@ extern "C" pbg_status pbg_inspect_step(pbg_ctx* ctx, int32_t i, int32_t j, const
       launch_expand_ds(g, DS_F32, nullptr, 0, 0, b.ds, nullptr, nullptr, Np, dscores, cs);
   }
   if (pos) launch_copy_pos(g, b.pos, pos, cs);
+  launch_step_losses(ctx->lossparts, ctx->lossparts_pps, nch * fin_blocks(C), nch * fin_blocks(C), 1,
+                     ctx->steploss_dev, cs);
   double loss = 0.0;
   e = hipGetLastError();
   if (e == hipSuccess) e = hipMemcpyAsync(&loss, ctx->steploss_dev, 8, hipMemcpyDeviceToHost, cs);

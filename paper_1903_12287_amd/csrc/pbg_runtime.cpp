@@ -105,8 +105,6 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   if (ctx->loss == PBG_LOSS_SOFTMAX) b.rowscale = (float*)a.get(s * 2 * nct * (int64_t)C * 4);
   b.dpos = (float*)a.get(s * psides * C * 4);
   b.dsum1 = (float*)a.get(s * C * 4);
-  b.chunkloss = (double*)a.get(s * fin_blocks(C) * 8);
-  b.fin_ticket = (unsigned int*)a.get(4);
   b.dq = (float*)a.get(s * 2 * C * dp * 4);
   b.dn = (float*)a.get(s * 2 * N * dp * 4);
   const bool has_rel = ctx->op != OP_IDENTITY;
@@ -173,7 +171,6 @@ pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S) {
   // bf16 transposes copy them: start from zeros so they always hold finite values
   hipError_t ez = hipMemsetAsync(b.qk, 0, (size_t)s * 2 * C * dp * 4, ctx->cs);
   if (ez == hipSuccess) ez = hipMemsetAsync(b.nn, 0, (size_t)s * 2 * N * dp * 4, ctx->cs);
-  if (ez == hipSuccess) ez = hipMemsetAsync(b.fin_ticket, 0, 4, ctx->cs);
   if (ez == hipSuccess) ez = hipStreamSynchronize(ctx->cs);
   if (ez != hipSuccess) {
     ctx->ws.release();
@@ -196,6 +193,22 @@ static bool ensure_events(pbg_ctx* ctx, size_t n) {
     ctx->events.push_back(e);
   }
   return true;
+}
+
+pbg_status ensure_lossparts(pbg_ctx* ctx, int64_t nsteps, int64_t pps) {
+  const int64_t n = std::max<int64_t>(nsteps, 1) * std::max<int64_t>(pps, 1);
+  ctx->lossparts_pps = pps;
+  if (ctx->lossparts_cap >= n && ctx->lossparts) return PBG_OK;
+  if (ctx->lossparts) (void)hipFree(ctx->lossparts);
+  ctx->lossparts = nullptr;
+  ctx->lossparts_cap = 0;
+  if (hipMalloc(&ctx->lossparts, (size_t)n * 8) != hipSuccess) {
+    (void)hipGetLastError();
+    ctx->lossparts = nullptr;
+    return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "loss-partial buffer allocation failed");
+  }
+  ctx->lossparts_cap = n;
+  return PBG_OK;
 }
 
 pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps) {
@@ -324,6 +337,7 @@ void pbg_free(pbg_ctx* ctx) {
   (void)hipDeviceSynchronize();
   ctx->ws.release();
   if (ctx->steploss_dev) (void)hipFree(ctx->steploss_dev);
+  if (ctx->lossparts) (void)hipFree(ctx->lossparts);
   if (ctx->cstart_dev) (void)hipFree(ctx->cstart_dev);
   if (ctx->cweight_dev) (void)hipFree(ctx->cweight_dev);
   for (auto& s : ctx->slots) {
@@ -561,6 +575,9 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
   const int64_t rstride = (int64_t)S * (recip ? 2 * C : C + (uniform_rel ? U : 0));
   st = ensure_steploss(ctx, nsteps);
   if (st != PBG_OK) return st;
+  const int64_t fb = fin_blocks(C);
+  st = ensure_lossparts(ctx, nsteps, (int64_t)S * fb);
+  if (st != PBG_OK) return st;
   hipStream_t cs = ctx->cs;
   const int N = C + U;
   const int d = ctx->d, dp = round_up(d, 4);
@@ -689,6 +706,11 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
       }
     }
     mark(t, 6);
+  }
+  {
+    const int nch_last = (int)(nchunks - (nsteps - 1) * S);
+    launch_step_losses(ctx->lossparts, ctx->lossparts_pps, (int)(S * fb), (int)(nch_last * fb), nsteps,
+                       ctx->steploss_dev, cs);
   }
   (void)hipEventRecord(ev1, cs);
   hipError_t e = hipGetLastError();

@@ -99,6 +99,10 @@ struct pbg_ctx {
   uint32_t* flag_dev = nullptr;
   double* steploss_dev = nullptr;
   int64_t steploss_cap = 0;
+  // the finalisation's loss partials of every step of a call, lossparts_pps
+  // apart (added up per step after the call's last step)
+  double* lossparts = nullptr;
+  int64_t lossparts_cap = 0, lossparts_pps = 0;
   // relation-grouped chunks of the current call: bounds in the call's edge
   // arrays (host copy and device copy)
   std::vector<int32_t> cstart_host;
@@ -191,6 +195,8 @@ inline bool linear_step_contractions(const pbg_ctx* ctx) {
   return ctx->op == PBG_OP_LINEAR && relation_rows(ctx) == 1;
 }
 pbg_status ensure_steploss(pbg_ctx* ctx, int64_t nsteps);
+// room for nsteps steps of pps loss partials each (sets lossparts_pps)
+pbg_status ensure_lossparts(pbg_ctx* ctx, int64_t nsteps, int64_t pps);
 
 // rows of table (type t, partition p), or -1
 int64_t table_rows(const pbg_ctx* ctx, int t, int p);
