@@ -210,6 +210,13 @@ void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, const u
 // sums of the nblk rows per chunk that the operator backward leaves with
 // StepGeom::relsum, RELSUM_PIECES partial rows per chunk
 void launch_relation_block_sums(const StepGeom& g, const float* rows, int nblk, float* partial, hipStream_t s);
+// the entity update with the single relation's block sums (b.relc, nblk rows
+// per chunk, into partial) and its Adagrad step riding along as extra
+// workgroups of its two launches; false (nothing launched) when the
+// relation rows need another row width than the entity rows
+bool launch_entity_update_with_relation(const StepGeom& g, const StepBufs& b, const uint32_t* keys,
+                                        const uint32_t* vals, int n, SortWork& w, float lr, int nblk, float* partial,
+                                        float* relp, float* relG, hipStream_t s);
 void launch_relation_single_adagrad(float* relp, float* relG, int width, const float* partial,
                                     int nparts, float lr, hipStream_t s);
 void launch_exclusive_scan(const uint32_t* in, int64_t n, uint32_t* out, uint32_t* tmp,

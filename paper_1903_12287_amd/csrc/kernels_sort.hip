@@ -310,6 +310,83 @@ __device__ __forceinline__ void crow_store(float* r, const float (&v)[RQ], int l
   }
 }
 
+// Second level of the single-relation gradient sum: the operator backward
+// left nblk rows per chunk (one per block of its grid); block (c, piece) adds,
+// in row order, the rows of chunk c that fall in its piece (wave w the rows
+// k0 + w, k0 + w + 4, ..., 32 / RQ of them loaded at a time).
+template <int RQ>
+__device__ __forceinline__ void relation_block_sums_body(const float* rows, int nblk, int dr, float* partial, int c,
+                                                         int piece) {
+  __shared__ float red[4][RQ * 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int per = (nblk + RELSUM_PIECES - 1) / RELSUM_PIECES;
+  const int k0 = piece * per;
+  const int k1 = min(nblk, k0 + per);
+  const float* base = rows + (int64_t)c * nblk * dr;
+  float acc[RQ];
+#pragma unroll
+  for (int q = 0; q < RQ; ++q) acc[q] = 0.0f;
+  constexpr int B = 32 / RQ;
+  for (int k = k0 + w; k < k1; k += 4 * B) {
+    float v[B][RQ];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int kk = k + 4 * u;
+      const float* r = base + (int64_t)kk * dr;
+#pragma unroll
+      for (int q = 0; q < RQ; ++q) {
+        const int f = lane + 64 * q;
+        v[u][q] = (kk < k1 && f < dr) ? r[f] : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < B; ++u)
+#pragma unroll
+      for (int q = 0; q < RQ; ++q) acc[q] += v[u][q];
+  }
+#pragma unroll
+  for (int q = 0; q < RQ; ++q) red[w][lane + 64 * q] = acc[q];
+  __syncthreads();
+  float* out = partial + ((int64_t)c * RELSUM_PIECES + piece) * dr;
+  for (int f = threadIdx.x; f < dr; f += 256) out[f] = (red[0][f] + red[1][f]) + (red[2][f] + red[3][f]);
+}
+
+// The same element-wise Adagrad in 256-thread workgroups (64 elements each,
+// wave w of 4 adding a contiguous quarter of the partial rows in order), for
+// the workgroups that ride along with the entity update's second launch.
+__device__ __forceinline__ void relation_adagrad4_body(float* relp, float* relG, int width, const float* partial,
+                                                       int nparts, float lr, int blk) {
+  __shared__ float red4[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int f = blk * 64 + lane;
+  const int per = (nparts + 3) / 4;
+  const int p0 = w * per, p1 = min(nparts, p0 + per);
+  float gsum = 0.0f;
+  if (f < width) {
+#pragma unroll 16
+    for (int c = p0; c < p1; ++c) gsum += partial[(int64_t)c * width + f];
+  }
+  red4[w][lane] = gsum;
+  __syncthreads();
+  if (w != 0 || f >= width) return;
+  const float gt = (red4[0][lane] + red4[1][lane]) + (red4[2][lane] + red4[3][lane]);
+  const float Gn = relG[f] + gt * gt;
+  relG[f] = Gn;
+  relp[f] -= lr * gt * adagrad_rcp(Gn);
+}
+
+// The single relation's gradient sums and Adagrad step ride along with the
+// entity update: workgroups past the update's own run them, the block sums
+// with its first launch and the Adagrad step over their partial rows with
+// the second (rows NULL: no riders).
+struct RelRider {
+  const float* rows;   // the operator backward's block rows, nblk per chunk
+  int nblk, nchunks, dr, nparts;
+  float* partial;      // RELSUM_PIECES rows per chunk
+  float* relp;
+  float* relG;
+};
+
 // Block of SEG_BLOCK sorted positions, one wave.  RQ floats of a row per lane
 // (lane L holds elements RQ L .. RQ L + RQ - 1; width <= 64 RQ).  The rows are
 // loaded SB positions at a time, together with the embedding rows of the
@@ -322,7 +399,12 @@ template <int MODE, int RQ>
 __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, const uint32_t* keys,
                                                         const uint32_t* vals, int n, const float* rows,
                                                         int64_t ld, int width, float* partial, uint32_t* segflag,
-                                                        float lr) {
+                                                        float lr, RelRider rr, int own_blocks) {
+  if ((int)blockIdx.x >= own_blocks) {
+    const int k = blockIdx.x - own_blocks;
+    relation_block_sums_body<RQ>(rr.rows, rr.nblk, rr.dr, rr.partial, k / RELSUM_PIECES, k % RELSUM_PIECES);
+    return;
+  }
   constexpr int SB = 32 / RQ;                      // positions per batch of loads
   const int lane = threadIdx.x & 63;
   const int blk = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
@@ -456,7 +538,11 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
 template <int MODE, int RQ>
 __global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, const uint32_t* keys, int n,
                                                        int width, const float* partial, const uint32_t* segflag,
-                                                       float lr) {
+                                                       float lr, RelRider rr, int own_blocks) {
+  if ((int)blockIdx.x >= own_blocks) {
+    relation_adagrad4_body(rr.relp, rr.relG, rr.dr, rr.partial, rr.nparts, lr, blockIdx.x - own_blocks);
+    return;
+  }
   const int lane = threadIdx.x & 63;
   const int blk = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int p0 = blk * SEG_BLOCK;
@@ -512,46 +598,9 @@ __global__ __launch_bounds__(256) void seg_update_span(StepGeom g, StepBufs b, c
   seg_apply<MODE, RQ>(g, b, key, acc, width, lr, lane);
 }
 
-// Second level of the single-relation gradient sum: the operator backward
-// left nblk rows per chunk (one per block of its grid); block (c, piece) adds,
-// in row order, the rows of chunk c that fall in its piece (wave w the rows
-// k0 + w, k0 + w + 4, ..., 32 / RQ of them loaded at a time).
 template <int RQ>
 __global__ __launch_bounds__(256) void relation_block_sums(const float* rows, int nblk, int dr, float* partial) {
-  __shared__ float red[4][RQ * 64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int c = blockIdx.x;
-  const int piece = blockIdx.y;
-  const int per = (nblk + RELSUM_PIECES - 1) / RELSUM_PIECES;
-  const int k0 = piece * per;
-  const int k1 = min(nblk, k0 + per);
-  const float* base = rows + (int64_t)c * nblk * dr;
-  float acc[RQ];
-#pragma unroll
-  for (int q = 0; q < RQ; ++q) acc[q] = 0.0f;
-  constexpr int B = 32 / RQ;
-  for (int k = k0 + w; k < k1; k += 4 * B) {
-    float v[B][RQ];
-#pragma unroll
-    for (int u = 0; u < B; ++u) {
-      const int kk = k + 4 * u;
-      const float* r = base + (int64_t)kk * dr;
-#pragma unroll
-      for (int q = 0; q < RQ; ++q) {
-        const int f = lane + 64 * q;
-        v[u][q] = (kk < k1 && f < dr) ? r[f] : 0.0f;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < B; ++u)
-#pragma unroll
-      for (int q = 0; q < RQ; ++q) acc[q] += v[u][q];
-  }
-#pragma unroll
-  for (int q = 0; q < RQ; ++q) red[w][lane + 64 * q] = acc[q];
-  __syncthreads();
-  float* out = partial + ((int64_t)c * RELSUM_PIECES + piece) * dr;
-  for (int f = threadIdx.x; f < dr; f += 256) out[f] = (red[0][f] + red[1][f]) + (red[2][f] + red[3][f]);
+  relation_block_sums_body<RQ>(rows, nblk, dr, partial, blockIdx.x, blockIdx.y);
 }
 
 // Second level and element-wise Adagrad: 64 elements per block; wave w of 16
@@ -692,27 +741,49 @@ void launch_radix_sort(uint32_t* keys, uint32_t* vals, int n, int bits, SortWork
 
 template <int MODE>
 static void seg_update(const StepGeom& g, const StepBufs& b, const uint32_t* keys, const uint32_t* vals, int n,
-                       const float* rows, int64_t ld, int width, SortWork& w, float lr, hipStream_t s) {
-  if (n <= 0) return;
+                       const float* rows, int64_t ld, int width, SortWork& w, float lr, hipStream_t s,
+                       const RelRider* rider = nullptr) {
+  if (n < 0) n = 0;
+  if (n == 0 && !rider) return;
   const int blocks = (n + 4 * SEG_BLOCK - 1) / (4 * SEG_BLOCK);
+  RelRider rr{};
+  int extra1 = 0, extra2 = 0;
+  if (rider) {
+    rr = *rider;
+    extra1 = rr.nchunks * RELSUM_PIECES;
+    extra2 = (rr.dr + 63) / 64;
+  }
   if (width <= 128) {
-    seg_update_local<MODE, 2><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial,
-                                                      w.segflag, lr);
-    seg_update_span<MODE, 2><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, w.segflag, lr);
+    seg_update_local<MODE, 2><<<blocks + extra1, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial,
+                                                               w.segflag, lr, rr, blocks);
+    seg_update_span<MODE, 2><<<blocks + extra2, 256, 0, s>>>(g, b, keys, n, width, w.partial, w.segflag, lr, rr,
+                                                              blocks);
   } else if (width <= 256) {
-    seg_update_local<MODE, 4><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial,
-                                                      w.segflag, lr);
-    seg_update_span<MODE, 4><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, w.segflag, lr);
+    seg_update_local<MODE, 4><<<blocks + extra1, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial,
+                                                               w.segflag, lr, rr, blocks);
+    seg_update_span<MODE, 4><<<blocks + extra2, 256, 0, s>>>(g, b, keys, n, width, w.partial, w.segflag, lr, rr,
+                                                              blocks);
   } else {
-    seg_update_local<MODE, 8><<<blocks, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial,
-                                                      w.segflag, lr);
-    seg_update_span<MODE, 8><<<blocks, 256, 0, s>>>(g, b, keys, n, width, w.partial, w.segflag, lr);
+    seg_update_local<MODE, 8><<<blocks + extra1, 256, 0, s>>>(g, b, keys, vals, n, rows, ld, width, w.partial,
+                                                               w.segflag, lr, rr, blocks);
+    seg_update_span<MODE, 8><<<blocks + extra2, 256, 0, s>>>(g, b, keys, n, width, w.partial, w.segflag, lr, rr,
+                                                              blocks);
   }
 }
 
 void launch_entity_update(const StepGeom& g, const StepBufs& b, const uint32_t* keys, const uint32_t* vals,
                           int n, SortWork& w, float lr, hipStream_t s) {
   seg_update<SEG_ENTITY>(g, b, keys, vals, n, b.dn, g.dp, g.d, w, lr, s);
+}
+
+bool launch_entity_update_with_relation(const StepGeom& g, const StepBufs& b, const uint32_t* keys,
+                                        const uint32_t* vals, int n, SortWork& w, float lr, int nblk, float* partial,
+                                        float* relp, float* relG, hipStream_t s) {
+  // the riders use the entity kernels' row width
+  if (row_width_for(g.dr) != row_width_for(g.d)) return false;
+  const RelRider rr{b.relc, nblk, g.nchunks, g.dr, g.nchunks * RELSUM_PIECES, partial, relp, relG};
+  seg_update<SEG_ENTITY>(g, b, keys, vals, n, b.dn, g.dp, g.d, w, lr, s, &rr);
+  return true;
 }
 
 void launch_relation_update_sorted(const StepGeom& g, const StepBufs& b, const uint32_t* keys,

@@ -679,8 +679,14 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
     else if (linear) launch_linear_rows_backward(g, b, cs);
     mark(t, 5);
 
-    // entities: contribution rows in (table, row) order, segment sums, Adagrad
-    launch_entity_update(g, b, skeys, svals, nkeys, ctx->sw, lr, cs);
+    // entities: contribution rows in (table, row) order, segment sums, Adagrad;
+    // one relation: its gradient sums and update ride along as extra
+    // workgroups of the same two launches
+    const bool rel_riders = single_relation_sums(ctx) &&
+                            launch_entity_update_with_relation(g, b, skeys, svals, nkeys, ctx->sw, lr,
+                                                               op_backward_blocks(g.C, g.U, g.cmp), ctx->relpartial,
+                                                               ctx->relp, ctx->relG, cs);
+    if (!rel_riders) launch_entity_update(g, b, skeys, svals, nkeys, ctx->sw, lr, cs);
 
     // relations
     if (has_rel) {
@@ -699,10 +705,13 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
         launch_relation_update_sorted(g, b, rk, rv, n_relkeys, ctx->sw, lr, cs);
       } else {
         // one relation: the operator backward left one gradient row per
-        // block of its grid; their fixed-order sums, then element-wise Adagrad
-        launch_relation_block_sums(g, b.relc, op_backward_blocks(g.C, g.U, g.cmp), ctx->relpartial, cs);
-        launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch * RELSUM_PIECES,
-                                       lr, cs);
+        // block of its grid; their fixed-order sums, then element-wise
+        // Adagrad (unless they rode along with the entity update)
+        if (!rel_riders) {
+          launch_relation_block_sums(g, b.relc, op_backward_blocks(g.C, g.U, g.cmp), ctx->relpartial, cs);
+          launch_relation_single_adagrad(ctx->relp, ctx->relG, ctx->dr, ctx->relpartial, nch * RELSUM_PIECES,
+                                         lr, cs);
+        }
       }
     }
     mark(t, 6);
