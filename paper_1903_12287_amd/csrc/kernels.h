@@ -108,6 +108,11 @@ void launch_to_bf16_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qh, in
 // x = h + m + l as three transposed planes [kp][ld_T] each (ps elements
 // apart, rows past `rows` up to ld_T zero), both operands in one launch.
 // ld_src is a multiple of 4, ld_T of 8.  q = nullptr: N only.
+// launch_finalize and launch_split3_t (same arguments) as one launch
+void launch_finalize_split3_t(const StepGeom& g, const StepBufs& b, double* parts, bool softmax_scales,
+                              const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,
+                              int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nT, int64_t nT_bs,
+                              int64_t n_ps, int n_ldT, int ld_src, int kp, int batches, hipStream_t s);
 void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,
                      int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nT, int64_t nT_bs,
                      int64_t n_ps, int n_ldT, int ld_src, int kp, int batches, hipStream_t s);

@@ -36,6 +36,7 @@
 
 #include "kernels.h"
 #include "device_common.h"
+#include "finalize_body.h"
 
 namespace {
 
@@ -1382,12 +1383,14 @@ struct Split3T {
   int ld_T, rows_p;
 };
 
-__global__ __launch_bounds__(256) void split3_t_kernel(Split3T o0, Split3T o1, int nz0, int kp) {
+// workgroup (bx, by, bz) of the split's grid
+__device__ __forceinline__ void split3_t_block(const Split3T& o0, const Split3T& o1, int nz0, int kp, int bx, int by,
+                                               int bz) {
   __shared__ float tile[64][65];
-  const bool first = (int)blockIdx.z < nz0;
+  const bool first = bz < nz0;
   const Split3T& o = first ? o0 : o1;
-  const int b = first ? blockIdx.z : blockIdx.z - nz0;
-  const int r0 = blockIdx.y * 64, k0 = blockIdx.x * 64;
+  const int b = first ? bz : bz - nz0;
+  const int r0 = by * 64, k0 = bx * 64;
   if (r0 >= o.rows_p) return;
   const float* s = o.src + (int64_t)b * o.src_bs;
 #pragma unroll
@@ -1417,6 +1420,26 @@ __global__ __launch_bounds__(256) void split3_t_kernel(Split3T o0, Split3T o1, i
     for (int p = 0; p < 3; ++p)
       *(u32x4*)(dst + p * o.ps + (int64_t)k * o.ld_T + r) = (u32x4){pc[0][p], pc[1][p], pc[2][p], pc[3][p]};
   }
+}
+
+__global__ __launch_bounds__(256) void split3_t_kernel(Split3T o0, Split3T o1, int nz0, int kp) {
+  split3_t_block(o0, o1, nz0, kp, blockIdx.x, blockIdx.y, blockIdx.z);
+}
+
+// The finalisation (nfin = fb x nchunks workgroups first) and the transposed
+// piece split (gx x gy x gz workgroups after them) in one launch: the split
+// reads only the candidate rows, so it need not wait for the finalisation,
+// whose short, latency-bound workgroups run beside its streaming ones.
+__global__ __launch_bounds__(256) void finalize_split3_t_kernel(StepGeom g, StepBufs b, int softmax_scales,
+                                                                double* parts, int fb, int nfin, Split3T o0,
+                                                                Split3T o1, int nz0, int kp, int gx, int gy) {
+  const int id = blockIdx.x;
+  if (id < nfin) {
+    finalize_block(g, b, softmax_scales, parts, id / fb, id % fb, fb);
+    return;
+  }
+  const int k = id - nfin;
+  split3_t_block(o0, o1, nz0, kp, k % gx, (k / gx) % gy, k / (gx * gy));
 }
 
 // softmax row pass in bf16 mode: raw fp32 scores -> dS = softmax (masked),
@@ -1551,6 +1574,22 @@ void launch_to_bf16_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qh, in
   const int nq = q ? batches : 0;   // no Q: only N
   dim3 grid((kp + 63) / 64, (std::max(q ? q_ldT : 0, n_ldT) + 63) / 64, nq + batches);
   to_bf16_t_kernel<<<grid, 256, 0, s>>>(o0, o1, nq, kp);
+}
+
+void launch_finalize_split3_t(const StepGeom& g, const StepBufs& b, double* parts, bool softmax_scales,
+                              const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,
+                              int q_ldT, const float* n, int64_t n_bs, int n_rows, uint16_t* nT, int64_t nT_bs,
+                              int64_t n_ps, int n_ldT, int ld_src, int kp, int batches, hipStream_t s) {
+  const int fb = fin_blocks(g.C);
+  const int nfin = fb * g.nchunks;
+  const Split3T o0{q, q_bs, q_rows, ld_src, qT, qT_bs, q_ps, q_ldT, q_ldT};
+  const Split3T o1{n, n_bs, n_rows, ld_src, nT, nT_bs, n_ps, n_ldT, n_ldT};
+  const int nq = q ? batches : 0;
+  const int gx = (kp + 63) / 64, gy = (std::max(q ? q_ldT : 0, n_ldT) + 63) / 64;
+  const int nsplit = (batches > 0 && kp > 0) ? gx * gy * (nq + batches) : 0;
+  if (nfin + nsplit <= 0) return;
+  finalize_split3_t_kernel<<<nfin + nsplit, 256, 0, s>>>(g, b, softmax_scales ? 1 : 0, parts, fb, nfin, o0, o1, nq,
+                                                         kp, gx, gy);
 }
 
 void launch_split3_t(const float* q, int64_t q_bs, int q_rows, uint16_t* qT, int64_t qT_bs, int64_t q_ps,

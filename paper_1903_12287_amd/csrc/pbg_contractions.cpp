@@ -147,19 +147,24 @@ void run_contractions_f32(pbg_ctx* ctx, const StepGeom& g, const StepBufs& b, in
   // softmax: the score pass leaves exp(s - tile max), the finalisation each
   // row's log-sum-exp and per-tile scales, and the backward forms dS as it
   // stages the exponentials
-  launch_finalize(g, b, ctx->lossparts + t * ctx->lossparts_pps, g.loss == LOSS_SOFTMAX, cs);
-  mark(3);
-  if (forward_only) return;
-
+  double* const parts = ctx->lossparts + t * ctx->lossparts_pps;
+  if (forward_only) {
+    launch_finalize(g, b, parts, g.loss == LOSS_SOFTMAX, cs);
+    mark(3);
+    return;
+  }
   // Q and N in three exact bf16 pieces each, transposed (the B operands of
-  // both backward products).  On the second stream beside the score
-  // contraction it delays the score kernel by as much as it saves here.
+  // both backward products), in the same launch as the finalisation.  On the
+  // second stream beside the score contraction it delays the score kernel by
+  // as much as it saves here.
   const int dpb = rup(g.d, 32), Cpb = rup(C, 32), Npb = rup(N, 32);
   const BufsH& h = ctx->h;
   // with QK_IN_NN, Q^T of side s is the first C columns of N^T of side 1 - s
   const bool qn = QK_IN_NN(g);
-  launch_split3_t(qn ? nullptr : b.qk, (int64_t)C * dp, C, h.qkT3, (int64_t)dpb * Cpb, h.q3_ps, Cpb, b.nn,
-                  (int64_t)N * dp, N, h.nnT3, (int64_t)dpb * Npb, h.n3_ps, Npb, dp, dpb, nch * 2, cs);
+  launch_finalize_split3_t(g, b, parts, g.loss == LOSS_SOFTMAX, qn ? nullptr : b.qk, (int64_t)C * dp, C, h.qkT3,
+                           (int64_t)dpb * Cpb, h.q3_ps, Cpb, b.nn, (int64_t)N * dp, N, h.nnT3, (int64_t)dpb * Npb,
+                           h.n3_ps, Npb, dp, dpb, nch * 2, cs);
+  mark(3);
   if (bits) {
     // dS is 0 or 1: its products with the pieces are exact (float32 sums)
     if (qn)
