@@ -19,7 +19,10 @@
 
 namespace {
 
-template <int RQ, bool RECIP>
+// EP edges per edge item: 2 for the cos comparator without reciprocal
+// predicates or the linear operator (both edges' four rows load together),
+// else 1.
+template <int RQ, bool RECIP, int EP>
 __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) {
   using Row = RowT<RQ>;
   const int lane = threadIdx.x & 63;
@@ -27,11 +30,53 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   const int Cc = chunk_edges(g, c);
   const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
   const bool cplx = g.op == OP_COMPLEX;
-  const bool active = item < Cc + 2 * ((g.U + 3) >> 2);
+  const int ne = (Cc + EP - 1) / EP;   // edge items
+  const bool active = item < ne + 2 * ((g.U + 3) >> 2);
   const int d = g.d, dp = g.dp;
 
   if (!active) return;   // no block-level barriers below: idle waves may leave
-  if (item < Cc) {
+  if (EP == 2 && item < ne) {
+    // ---- edges 2 item and 2 item + 1 (the second may not exist)
+    const int e0 = 2 * item;
+    const bool two = e0 + 1 < Cc;
+    const int64_t eg0 = chunk_first(g, c) + e0;
+    const int64_t eg1 = two ? eg0 + 1 : eg0;
+    const int s0 = b.src[eg0], t0 = b.dst[eg0], s1 = b.src[eg1], t1 = b.dst[eg1];
+    const int r0 = edge_relation(g, b.rel, eg0), r1 = edge_relation(g, b.rel, eg1);
+    Row x0, y0, x1, y1, th0, th1;
+    row_load(x0, b.emb_i + (int64_t)s0 * d, d, cplx, lane);
+    row_load(y0, b.emb_j + (int64_t)t0 * d, d, cplx, lane);
+    row_load(x1, b.emb_i + (int64_t)s1 * d, d, cplx, lane);
+    row_load(y1, b.emb_j + (int64_t)t1 * d, d, cplx, lane);
+    if (g.op != OP_IDENTITY) {
+      row_load(th0, b.relp + (int64_t)r0 * g.dr, d, cplx, lane);
+      row_load(th1, b.relp + (int64_t)r1 * g.dr, d, cplx, lane);
+    } else {
+      row_zero(th0);
+      row_zero(th1);
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      if (k == 1 && !two) break;
+      const int e = e0 + k;
+      Row gq = op_forward(g.op, k ? x1 : x0, k ? th1 : th0);
+      Row y = k ? y1 : y0;
+      const float nq = row_normalize(gq);
+      const float ny = row_normalize(y);
+      const float p = row_dot(gq, y);
+      // Q and K are these candidate rows (QK_IN_NN)
+      row_store(gq, b.nn + ((int64_t)(c * 2 + 1) * g.N + e) * dp, d, dp, cplx, lane);
+      row_store(y, b.nn + ((int64_t)(c * 2 + 0) * g.N + e) * dp, d, dp, cplx, lane);
+      if (lane == 0) {
+        b.pos[(int64_t)c * g.C + e] = p;
+        b.bias[(int64_t)c * g.C + e] = 0.0f;
+        b.nrm[(int64_t)(c * 2 + 0) * g.N + e] = ny;
+        b.nrm[(int64_t)(c * 2 + 1) * g.N + e] = nq;
+      }
+    }
+    return;
+  }
+  if (EP == 1 && item < Cc) {
     // ---- edge item
     const int e = item;
     const int64_t eg = chunk_first(g, c) + e;   // in the step's edge arrays
@@ -152,7 +197,7 @@ __global__ __launch_bounds__(256) void gather_op_kernel(StepGeom g, StepBufs b) 
   // per wave (one Philox block gives all four words, the four rows load
   // together)
   const int ng = (g.U + 3) >> 2;
-  const int grp = item - Cc;
+  const int grp = item - ne;
   const int side = grp < ng ? 0 : 1;
   const int k0 = 4 * (grp - side * ng);
   const uint32_t rows = side == 0 ? (uint32_t)g.rows_j : (uint32_t)g.rows_i;
@@ -344,13 +389,22 @@ void launch_gather(const StepGeom& g, const StepBufs& b, hipStream_t s) {
   // common kernel as small as it is without them
   const int rq = row_width_for(g.d);
   if (g.recip) {
-    if (rq == 2) gather_op_kernel<2, true><<<grid, 256, 0, s>>>(g, b);
-    else if (rq == 4) gather_op_kernel<4, true><<<grid, 256, 0, s>>>(g, b);
-    else gather_op_kernel<8, true><<<grid, 256, 0, s>>>(g, b);
+    if (rq == 2) gather_op_kernel<2, true, 1><<<grid, 256, 0, s>>>(g, b);
+    else if (rq == 4) gather_op_kernel<4, true, 1><<<grid, 256, 0, s>>>(g, b);
+    else gather_op_kernel<8, true, 1><<<grid, 256, 0, s>>>(g, b);
   } else {
-    if (rq == 2) gather_op_kernel<2, false><<<grid, 256, 0, s>>>(g, b);
-    else if (rq == 4) gather_op_kernel<4, false><<<grid, 256, 0, s>>>(g, b);
-    else gather_op_kernel<8, false><<<grid, 256, 0, s>>>(g, b);
+    if (QK_IN_NN(g) && g.op != OP_LINEAR) {
+      const dim3 grid2(((g.C + 1) / 2 + 2 * ((g.U + 3) / 4) + 3) / 4, g.nchunks);
+      if (rq == 2) gather_op_kernel<2, false, 2><<<grid2, 256, 0, s>>>(g, b);
+      else if (rq == 4) gather_op_kernel<4, false, 2><<<grid2, 256, 0, s>>>(g, b);
+      else gather_op_kernel<8, false, 2><<<grid2, 256, 0, s>>>(g, b);
+    } else if (rq == 2) {
+      gather_op_kernel<2, false, 1><<<grid, 256, 0, s>>>(g, b);
+    } else if (rq == 4) {
+      gather_op_kernel<4, false, 1><<<grid, 256, 0, s>>>(g, b);
+    } else {
+      gather_op_kernel<8, false, 1><<<grid, 256, 0, s>>>(g, b);
+    }
   }
 }
 
