@@ -74,7 +74,7 @@ enum {
    * stream and report the summed times in pbg_stats (each event adds a few
    * microseconds to a step). */
   PBG_F_PHASE_TIMING = 2u,
-  /* Record HIP events around the score contraction of every second step only
+  /* Record HIP events around the score contraction of every fourth step only
    * (score_ms and score_timed_steps in pbg_stats); PBG_F_PHASE_TIMING times
    * it on every step.  With bf16 score inputs the bracket holds the score
    * contraction alone, not the rounding of its operands. */

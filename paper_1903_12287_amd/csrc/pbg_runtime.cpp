@@ -346,6 +346,8 @@ void pbg_free(pbg_ctx* ctx) {
     if (s.released) (void)hipEventDestroy(s.released);
   }
   if (ctx->own_xs) (void)hipStreamDestroy(ctx->own_xs);
+  if (ctx->hflag) (void)hipHostFree(ctx->hflag);
+  if (ctx->check_ev) (void)hipEventDestroy(ctx->check_ev);
   for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
   delete ctx;
 }
@@ -555,6 +557,11 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
   // relation-grouped chunks: bounds in the call's edge arrays (checked before
   // anything is updated)
   const bool grouped = grouped_chunks(ctx, neg);
+  if (ctx->check_pending && (grouped || !ctx->relw.empty())) {
+    // the host reads relation ids below: their range is checked first
+    st = finish_id_check(ctx, i, j);
+    if (st != PBG_OK) return st;
+  }
   if (grouped) {
     st = relation_chunk_bounds(ctx, rel, n_edges, C);
     if (st != PBG_OK) return st;
@@ -650,6 +657,15 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
       else
         launch_radix_sort_segments(win_keys, win_vals, ctx->wkeys_alt, ctx->wvals_alt, kstride, (int)kstride,
                                    2 * (nch_l * U + m_l), wn, key_bits, ctx->whist, &wsk, &wsv, cs);
+    }
+    if (ctx->check_pending) {
+      const pbg_status cst = finish_id_check(ctx, i, j);
+      if (cst != PBG_OK) {
+        (void)hipStreamSynchronize(cs);   // the queued sort touches scratch only
+        (void)hipEventDestroy(ev0);
+        (void)hipEventDestroy(ev1);
+        return cst;
+      }
     }
     const int nkeys = 2 * (nch * U + m_step);
     uint32_t* skeys = wsk + wi * kstride;
@@ -777,7 +793,8 @@ pbg_status train_bucket_device(pbg_ctx* ctx, int32_t i, int32_t j, const BucketT
 
 pbg_status check_bucket_call(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
                              const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
-                             const pbg_neg_config* neg) {
+                             const pbg_neg_config* neg, bool defer) {
+  ctx->check_pending = false;
   if (i < 0 || i >= ctx->P || j < 0 || j >= ctx->P)
     return set_err(ctx, PBG_ERR_INVALID_ARG, "bucket (%d, %d) out of range", i, j);
   pbg_status st = check_neg_config(ctx, neg);
@@ -804,10 +821,31 @@ pbg_status check_bucket_call(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* 
   launch_check_ids(src_local, n_edges, (int32_t)pbg_partition_rows(ctx, i), ctx->flag_dev, 1u, cs);
   launch_check_ids(dst_local, n_edges, (int32_t)pbg_partition_rows(ctx, j), ctx->flag_dev, 2u, cs);
   if (rel) launch_check_ids(rel, n_edges, ctx->R, ctx->flag_dev, 4u, cs);
-  uint32_t flag = 0;
-  e = hipMemcpyAsync(&flag, ctx->flag_dev, 4, hipMemcpyDeviceToHost, cs);
-  if (e == hipSuccess) e = hipStreamSynchronize(cs);
+  if (!ctx->hflag && hipHostMalloc((void**)&ctx->hflag, 16) != hipSuccess) {
+    (void)hipGetLastError();
+    ctx->hflag = nullptr;
+    return set_err(ctx, PBG_ERR_OUT_OF_MEMORY, "page-locked flag allocation failed");
+  }
+  if (!ctx->check_ev && hipEventCreateWithFlags(&ctx->check_ev, hipEventDisableTiming) != hipSuccess) {
+    (void)hipGetLastError();
+    ctx->check_ev = nullptr;
+    return set_err(ctx, PBG_ERR_DEVICE, "hipEventCreate failed");
+  }
+  e = hipMemcpyAsync(ctx->hflag, ctx->flag_dev, 4, hipMemcpyDeviceToHost, cs);
+  if (e == hipSuccess) e = hipEventRecord(ctx->check_ev, cs);
   if (e != hipSuccess) return hip_fail(ctx, e, "id range check");
+  if (defer) {
+    ctx->check_pending = true;
+    return PBG_OK;
+  }
+  return finish_id_check(ctx, i, j);
+}
+
+pbg_status finish_id_check(pbg_ctx* ctx, int32_t i, int32_t j) {
+  ctx->check_pending = false;
+  const hipError_t e = hipEventSynchronize(ctx->check_ev);
+  if (e != hipSuccess) return hip_fail(ctx, e, "id range check");
+  const uint32_t flag = *(volatile uint32_t*)ctx->hflag;
   if (flag & 1u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a source id is outside partition %d", i);
   if (flag & 2u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a destination id is outside partition %d", j);
   if (flag & 4u) return set_err(ctx, PBG_ERR_INVALID_ARG, "a relation id is outside [0, %d)", ctx->R);
@@ -829,7 +867,9 @@ extern "C" pbg_status pbg_train_bucket(pbg_ctx* ctx, int32_t i, int32_t j, const
     return train_bucket_typed(ctx, i, j, src_local, rel, dst_local, n_edges, neg, lr, seed, loss_host,
                               &ctx->step_losses);
   }
-  pbg_status st = check_bucket_call(ctx, i, j, src_local, rel, dst_local, n_edges, neg);
+  // the id check's verdict is awaited after the first window's sort keys are
+  // queued (they need no valid ids), so the device does not idle meanwhile
+  pbg_status st = check_bucket_call(ctx, i, j, src_local, rel, dst_local, n_edges, neg, true);
   if (st != PBG_OK) return st;
   ctx->stats = pbg_stats();
   ctx->step_losses.clear();

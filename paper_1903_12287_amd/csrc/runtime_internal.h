@@ -97,6 +97,9 @@ struct pbg_ctx {
   float* relA = nullptr;    // linear operator: A and A^T, rows padded to dp
   float* relAT = nullptr;
   uint32_t* flag_dev = nullptr;
+  uint32_t* hflag = nullptr;          // page-locked copy of the id check's flags
+  hipEvent_t check_ev = nullptr;      // the copy has landed
+  bool check_pending = false;
   double* steploss_dev = nullptr;
   int64_t steploss_cap = 0;
   // the finalisation's loss partials of every step of a call, lossparts_pps
@@ -120,7 +123,7 @@ struct pbg_ctx {
 constexpr int kPhaseEvents = 7;
 // score-only timing brackets every kScoreSample-th step (each event record
 // costs the compute stream a few microseconds)
-constexpr int kScoreSample = 2;
+constexpr int kScoreSample = 4;
 // steps whose entity sort keys are built and sorted together, as one batch
 constexpr int kSortWindow = 32;
 
@@ -152,7 +155,12 @@ pbg_status check_neg_config(pbg_ctx* ctx, const pbg_neg_config* neg);
 // device-side range check of every id (nothing is modified on failure)
 pbg_status check_bucket_call(pbg_ctx* ctx, int32_t i, int32_t j, const int32_t* src_local,
                              const int32_t* rel, const int32_t* dst_local, int64_t n_edges,
-                             const pbg_neg_config* neg);
+                             const pbg_neg_config* neg,
+                             bool defer = false);
+// the id range check's verdict (waits for it); with defer the check above only
+// launches it, and the caller finishes it once it has queued work that needs
+// no valid ids (check_pending)
+pbg_status finish_id_check(pbg_ctx* ctx, int32_t i, int32_t j);
 pbg_status ensure_workspace(pbg_ctx* ctx, int C, int U, int S);
 // chunk bounds of a call's edges for PBG_CHUNK_BY_RELATION (rel: device, n
 // edges sorted by relation): ctx->cstart_host / cstart_dev; INVALID_ARG when
