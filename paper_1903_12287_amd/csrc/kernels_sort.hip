@@ -405,7 +405,7 @@ __global__ __launch_bounds__(256) void seg_update_local(StepGeom g, StepBufs b, 
     relation_block_sums_body<RQ>(rr.rows, rr.nblk, rr.dr, rr.partial, k / RELSUM_PIECES, k % RELSUM_PIECES);
     return;
   }
-  constexpr int SB = 32 / RQ;                      // positions per batch of loads
+  constexpr int SB = 16 / RQ;                      // positions per batch of loads
   const int lane = threadIdx.x & 63;
   const int blk = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int p0 = blk * SEG_BLOCK;
