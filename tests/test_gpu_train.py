@@ -132,6 +132,13 @@ def test_out_of_range_ids_leave_parameters_untouched():
         with pytest.raises(pbg.PbgError) as ei:
             pbg.pbg_train_bucket(gm.ctx, 0, 0, gm.src, gm.rel_ids, bad_dst, 16, 8, 2, 0.1, 1)
         assert ei.value.status_name == "INVALID_ARG"
+        # an id far past the table: the range check's verdict comes after the
+        # sort keys are queued, whose key bits it overflows
+        bad_src = gm.src.clone()
+        bad_src[40] = 1 << 30
+        with pytest.raises(pbg.PbgError) as ei:
+            pbg.pbg_train_bucket(gm.ctx, 0, 0, bad_src, gm.rel_ids, gm.dst, 16, 8, 2, 0.1, 1)
+        assert ei.value.status_name == "INVALID_ARG"
         bad_rel = gm.rel_ids.clone()
         bad_rel[3] = -1
         with pytest.raises(pbg.PbgError):
